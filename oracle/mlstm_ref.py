@@ -1,0 +1,196 @@
+"""NumPy fp64 forms of the mLSTM cell.
+
+TEST INFRASTRUCTURE ONLY: the oracle side of the parity tests.  Only
+``tests/``, the smoke check and the benchmark's CPU-baseline leg may import
+this module; it shares no code with the HIP library and imports nothing from
+it.
+
+All functions take fp64 arrays with a leading sequence axis S (= B * NH,
+every (batch, head) pair is an independent cell):
+
+    q, k   [S, T, DQK]      v [S, T, DV]      ipre, fpre [S, T]
+    C0     [S, DQK, DV]     n0 [S, DQK]       m0 [S]     (all None: zero state, m0 = 0)
+
+and return ``h [S, T, DV]`` (the h~ of Eq. 5) and the final state
+``(C [S, DQK, DV], n [S, DQK], m [S])``.
+
+Forms, each written from the paper's statement of the cell (Sec. 2):
+
+* ``recurrent``              Eqs. 2-5, 7-8, step by step (the definition).
+* ``recurrent_unstabilized`` the same recurrence without the max state:
+                             C~_t = e^{logsig f~_t} C~_{t-1} + e^{i~_t} k v^T, and the
+                             floor exp(-m_t) becomes 1 in these unscaled units.
+* ``parallel_quadratic``     the fully parallel form H = mLSTMCell(X) (Eq. 10):
+                             a causal, gate-weighted T x T matrix.
+* ``chunkwise``              the chunkwise-parallel form, following the sub-steps
+                             of the FLOP count in App. D.1 (chunkwise gates, gates and
+                             max state, inter-chunk numerator and denominator, gate
+                             matrix, gated logits, intra-chunk numerator and
+                             denominator, output combination), for any chunk size;
+                             the last chunk may be shorter.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def logsigmoid(x):
+    """log(sigmoid(x)) = min(x, 0) - log1p(exp(-|x|)), exact in value, no overflow."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.minimum(x, 0.0) - np.log1p(np.exp(-np.abs(x)))
+
+
+def _init_state(S, DQK, DV, C0, n0, m0):
+    if C0 is None:
+        assert n0 is None and m0 is None
+        return np.zeros((S, DQK, DV)), np.zeros((S, DQK)), np.zeros((S,))
+    return (np.array(C0, dtype=np.float64, copy=True), np.array(n0, dtype=np.float64, copy=True),
+            np.array(m0, dtype=np.float64, copy=True))
+
+
+def recurrent(q, k, v, ipre, fpre, C0=None, n0=None, m0=None):
+    """Recurrent form, Eqs. 2-5 with Eqs. 7-8 (Sec. 2, generation mode)."""
+    S, T, DQK = q.shape
+    DV = v.shape[2]
+    C, n, m = _init_state(S, DQK, DV, C0, n0, m0)
+    h = np.empty((S, T, DV))
+    scale = 1.0 / np.sqrt(DQK)
+    for t in range(T):
+        a = logsigmoid(fpre[:, t])
+        it = ipre[:, t]
+        m_new = np.maximum(a + m, it)                      # Eq. 2
+        f = np.exp(a + m - m_new)                          # Eq. 7
+        i = np.exp(it - m_new)                             # Eq. 8
+        kt, vt = k[:, t, :], v[:, t, :]
+        C = f[:, None, None] * C + i[:, None, None] * kt[:, :, None] * vt[:, None, :]   # Eq. 3
+        n = f[:, None] * n + i[:, None] * kt               # Eq. 4
+        m = m_new
+        qh = q[:, t, :] * scale
+        num = np.einsum("sdv,sd->sv", C, qh)               # C_t^T q^_t
+        den = np.maximum(np.abs(np.einsum("sd,sd->s", n, qh)), np.exp(-m))
+        h[:, t, :] = num / den[:, None]                    # Eq. 5
+    return h, C, n, m
+
+
+def recurrent_unstabilized(q, k, v, ipre, fpre, C0=None, n0=None, m0=None):
+    """The recurrence in unscaled units (no max state).
+
+    With C~ = e^{m} C and n~ = e^{m} n, Eqs. 3-5 become
+    C~_t = e^{logsig f~_t} C~_{t-1} + e^{i~_t} k_t v_t^T (same for n~), and the
+    floor max(|n^T q^|, e^{-m}) turns into max(|n~^T q^|, 1).  Returns h and the
+    unscaled final (C~, n~).  Only for small inputs: e^{i~} is not bounded.
+    """
+    S, T, DQK = q.shape
+    DV = v.shape[2]
+    C, n, m = _init_state(S, DQK, DV, C0, n0, m0)
+    Cb = np.exp(m)[:, None, None] * C
+    nb = np.exp(m)[:, None] * n
+    h = np.empty((S, T, DV))
+    scale = 1.0 / np.sqrt(DQK)
+    for t in range(T):
+        fa = np.exp(logsigmoid(fpre[:, t]))
+        ia = np.exp(ipre[:, t])
+        kt, vt = k[:, t, :], v[:, t, :]
+        Cb = fa[:, None, None] * Cb + ia[:, None, None] * kt[:, :, None] * vt[:, None, :]
+        nb = fa[:, None] * nb + ia[:, None] * kt
+        qh = q[:, t, :] * scale
+        num = np.einsum("sdv,sd->sv", Cb, qh)
+        den = np.maximum(np.abs(np.einsum("sd,sd->s", nb, qh)), 1.0)
+        h[:, t, :] = num / den[:, None]
+    return h, Cb, nb
+
+
+def parallel_quadratic(q, k, v, ipre, fpre, C0=None, n0=None, m0=None):
+    """Fully parallel form (Eq. 10): every output row is a gate-weighted sum over all
+    earlier tokens plus the decayed initial state.
+
+    Token j reaches step t >= j with log weight i~_j + sum_{j<s<=t} logsig(f~_s) and the
+    initial state with log weight m_0 + sum_{s<=t} logsig(f~_s).  The row maximum
+    of these log weights is the max state m_t, which stabilises the row and sets the
+    floor exp(-m_t).
+    """
+    S, T, DQK = q.shape
+    DV = v.shape[2]
+    C, n, m = _init_state(S, DQK, DV, C0, n0, m0)
+    h = np.empty((S, T, DV))
+    CT = np.empty((S, DQK, DV))
+    nT = np.empty((S, DQK))
+    mT = np.empty((S,))
+    scale = 1.0 / np.sqrt(DQK)
+    for s in range(S):
+        a = logsigmoid(fpre[s])
+        # seg[t, j] = sum_{j < s' <= t} logsig(f~_s'), summed directly (not as a difference of
+        # prefix sums) so that a forget gate of exactly zero (logsig = -inf) stays exact.
+        seg = np.full((T, T), -np.inf)
+        for j in range(T):
+            seg[j, j] = 0.0
+            if j + 1 < T:
+                seg[j + 1:, j] = np.cumsum(a[j + 1:])
+        logD = ipre[s][None, :] + seg
+        log0 = m[s] + np.cumsum(a)                         # initial-state weight per row
+        mrow = np.maximum(log0, logD.max(axis=1)) if T else log0
+        D = np.exp(logD - mrow[:, None])
+        w0 = np.exp(log0 - mrow)
+        Qh = q[s] * scale
+        Sm = (Qh @ k[s].T) * D
+        num = Sm @ v[s] + w0[:, None] * (Qh @ C[s])
+        den = Sm.sum(axis=1) + w0 * (Qh @ n[s])
+        h[s] = num / np.maximum(np.abs(den), np.exp(-mrow))[:, None]
+        if T:
+            mT[s] = mrow[-1]
+            wl = D[-1]                                     # last row: weights of every token at T
+            CT[s] = w0[-1] * C[s] + (k[s] * wl[:, None]).T @ v[s]
+            nT[s] = w0[-1] * n[s] + k[s].T @ wl
+        else:
+            mT[s], CT[s], nT[s] = m[s], C[s], n[s]
+    return h, CT, nT, mT
+
+
+def chunkwise(q, k, v, ipre, fpre, C0=None, n0=None, m0=None, L=64):
+    """Chunkwise-parallel form with chunk size L, in the sub-steps of App. D.1.
+
+    Within chunk k (positions tau = 1..Lc) with previous state (C, n, m_prev):
+      chunkwise gates   b_tau = sum_{s<=tau} logsig(f~_s),  g = b_Lc
+      max state         m_tau = max(b_tau + m_prev, max_{sig<=tau}(i~_sig + b_tau - b_sig))
+                        m_k   = max(g + m_prev, max_tau(i~_tau + g - b_tau))
+      gate matrix       D[tau, sig] = exp(i~_sig + b_tau - b_sig - m_tau),  sig <= tau
+      gated logits      S = (Q^ K^T) * D
+      numerator         e^{b_tau + m_prev - m_tau} Q^ C  +  S V
+      denominator       e^{b_tau + m_prev - m_tau} Q^ n  +  rowsum(S)
+      output            h_tau = numerator / max(|denominator|, e^{-m_tau})
+      state update      C <- e^{g + m_prev - m_k} C + (w * K)^T V,  w_tau = e^{i~_tau + g - b_tau - m_k}
+                        n <- e^{g + m_prev - m_k} n + K^T w,        m_prev <- m_k
+    """
+    S, T, DQK = q.shape
+    DV = v.shape[2]
+    C, n, m = _init_state(S, DQK, DV, C0, n0, m0)
+    h = np.empty((S, T, DV))
+    scale = 1.0 / np.sqrt(DQK)
+    for s in range(S):
+        Cs, ns, mp = C[s].copy(), n[s].copy(), m[s]
+        for t0 in range(0, T, L):
+            t1 = min(T, t0 + L)
+            a = logsigmoid(fpre[s, t0:t1])
+            it = ipre[s, t0:t1]
+            b = np.cumsum(a)
+            g = b[-1]
+            Lc = t1 - t0
+            tri = np.tril(np.ones((Lc, Lc), dtype=bool))
+            logD = np.where(tri, it[None, :] + b[:, None] - b[None, :], -np.inf)
+            m_tau = np.maximum(b + mp, logD.max(axis=1))
+            D = np.exp(logD - m_tau[:, None])
+            Qh = q[s, t0:t1] * scale
+            K, V = k[s, t0:t1], v[s, t0:t1]
+            Sm = (Qh @ K.T) * D
+            inter = np.exp(b + mp - m_tau)
+            num = inter[:, None] * (Qh @ Cs) + Sm @ V
+            den = inter * (Qh @ ns) + Sm.sum(axis=1)
+            h[s, t0:t1] = num / np.maximum(np.abs(den), np.exp(-m_tau))[:, None]
+            m_k = max(g + mp, np.max(it + g - b))
+            w = np.exp(it + g - b - m_k)
+            decay = np.exp(g + mp - m_k)
+            Cs = decay * Cs + (K * w[:, None]).T @ V
+            ns = decay * ns + K.T @ w
+            mp = m_k
+        C[s], n[s], m[s] = Cs, ns, mp
+    return h, C, n, m

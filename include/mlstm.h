@@ -1,0 +1,140 @@
+/*
+ * libmlstm: the mLSTM matrix-memory cell of xLSTM 7B (arXiv 2503.13427) on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The cell (Sec. 2 of the paper, Eqs. 2-5 with the gate activations of
+ * Eqs. 7-8), per independent (batch, head) sequence with q^ = q / sqrt(DQK):
+ *
+ *   m_t  = max(logsig(f~_t) + m_{t-1}, i~_t)
+ *   f_t  = exp(logsig(f~_t) + m_{t-1} - m_t),   i_t = exp(i~_t - m_t)
+ *   C_t  = f_t C_{t-1} + i_t k_t v_t^T          (DQK x DV, fp32)
+ *   n_t  = f_t n_{t-1} + i_t k_t                (DQK, fp32)
+ *   h_t  = C_t^T q^_t / max(|n_t^T q^_t|, exp(-m_t))
+ *
+ * h is the h~ of Eq. 5: the output gate and Norm of Eq. 6 are not applied.
+ * h_{t-1} is not an input (Eq. 1 lists it, Eqs. 2-9 never use it).
+ *
+ * Conventions shared by every entry point:
+ *  - All tensor pointers are DEVICE pointers, contiguous and row-major, with
+ *    16-byte aligned base addresses.  The caller owns every buffer; the
+ *    library allocates nothing.
+ *  - q, k, v and h share one element type, mlstm_dtype; gates and the state
+ *    (C, n, m) are always fp32.
+ *  - Arguments are validated on the host before anything is launched; a
+ *    rejected call touches no memory and launches nothing.
+ *  - Work is enqueued on `hip_stream` (a hipStream_t; NULL = the null stream)
+ *    and the call returns after enqueue.  Launch failures are reported as
+ *    MLSTM_ERR_HIP; faults during execution surface at the caller's next
+ *    synchronisation.
+ *  - Inputs are assumed finite, except that i~ = -inf (nothing written) and
+ *    f~ = +inf (nothing forgotten) are allowed.  f~ = -inf (a forget gate of
+ *    exactly zero) is supported by mlstm_step only; the chunkwise form takes
+ *    differences of in-chunk prefix sums of logsig(f~).  NaN/Inf are not
+ *    checked on the hot path and propagate.
+ *  - The library is stateless and re-entrant.
+ */
+#ifndef LIBMLSTM_MLSTM_H
+#define LIBMLSTM_MLSTM_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MLSTM_OK = 0,
+    MLSTM_ERR_NULL_PTR = 1,     /* a required pointer is NULL                         */
+    MLSTM_ERR_BAD_SHAPE = 2,    /* negative/zero size, or T % L != 0                  */
+    MLSTM_ERR_UNSUPPORTED = 3,  /* (dtype, DQK, DV, L) combination not built          */
+    MLSTM_ERR_MISALIGNED = 4,   /* a tensor base pointer is not 16-byte aligned       */
+    MLSTM_ERR_ALIAS = 5,        /* outputs overlap inputs in a way that is not allowed */
+    MLSTM_ERR_WORKSPACE = 6,    /* workspace given but smaller than required          */
+    MLSTM_ERR_HIP = 7           /* the HIP runtime reported an error at launch         */
+} mlstm_status;
+
+typedef enum {
+    MLSTM_F32 = 0,   /* q, k, v, h in IEEE fp32                     */
+    MLSTM_BF16 = 1   /* q, k, v, h in bfloat16 (bit pattern uint16) */
+} mlstm_dtype;
+
+/*
+ * Chunkwise-parallel prefill (Sec. 2, "Training Mode": the hidden states are
+ * computed chunk by chunk without materialising the per-step states; the
+ * sub-steps are those of the FLOP count in App. D.1).
+ *
+ * Shapes (S = B * NH independent sequences):
+ *   q, k  [B, NH, T, DQK]   (dt)        v  [B, NH, T, DV]   (dt)
+ *   ipre, fpre [B, NH, T]   fp32 gate pre-activations i~, f~
+ *   C0 [B, NH, DQK, DV], n0 [B, NH, DQK], m0 [B, NH]   fp32 initial state;
+ *       all three NULL = zero state with m0 = 0; giving only some of them is
+ *       MLSTM_ERR_NULL_PTR.
+ *   h  [B, NH, T, DV]       (dt)       output h~ for every step
+ *   CT [B, NH, DQK, DV], nT [B, NH, DQK], mT [B, NH]   fp32 final state
+ *
+ * L is the chunk size; T % L == 0 is required (else MLSTM_ERR_BAD_SHAPE).
+ * T == 0 copies the initial state to the final state; q, k, v, ipre, fpre
+ * and h are then not accessed and may be NULL.  The result does not
+ * depend on L except through rounding; mT equals the recurrent m_T of Eq. 2.
+ *
+ * Built combinations (else MLSTM_ERR_UNSUPPORTED):
+ *   - MLSTM_BF16, DQK = 256, DV = 512, L in {64, 128}, T < 2^21: the bf16
+ *     MFMA kernel (the xLSTM 7B head shape);
+ *   - otherwise any dtype and sizes whose fp32 working set (a DQK x DVt state
+ *     tile, the chunk's Q, K and V, the L x L gate matrix) fits in 64 KB of
+ *     LDS for some power-of-two tile DVt dividing DV, e.g. DQK = DV = 16 with
+ *     L = 16: the fp32 VALU kernel.
+ *
+ * workspace: optional device scratch.  workspace_bytes == 0 runs the fused
+ * single-pass kernel.  Otherwise it must be at least
+ * mlstm_chunkwise_workspace_bytes(...) (else MLSTM_ERR_WORKSPACE), and the
+ * sequence is split into segments processed in parallel, with the segment
+ * boundary states passed through the workspace.  Contents on entry are
+ * ignored; on return they are undefined.
+ *
+ * Aliasing: no output may overlap any input or another output
+ * (MLSTM_ERR_ALIAS).
+ */
+mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                                 const float* ipre, const float* fpre,
+                                 const float* C0, const float* n0, const float* m0,
+                                 int B, int NH, int T, int DQK, int DV, int L,
+                                 void* h, float* CT, float* nT, float* mT,
+                                 void* workspace, size_t workspace_bytes, void* hip_stream);
+
+/*
+ * Workspace size (bytes) for the segment-parallel schedule of
+ * mlstm_chunkwise_fwd with these arguments; 0 when that schedule would not be
+ * used (the call then runs the fused kernel whatever workspace is given).
+ */
+size_t mlstm_chunkwise_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L, mlstm_dtype dt);
+
+/*
+ * One recurrent step (Sec. 2, "Generation Mode", Eqs. 2-5, 7-8), fused into
+ * one kernel that streams C once (Sec. 3.1, "Fused Generation Kernels").
+ *
+ *   q, k [B, NH, DQK] (dt)   v [B, NH, DV] (dt)   ipre, fpre [B, NH] fp32
+ *   C [B, NH, DQK, DV], n [B, NH, DQK], m [B, NH]   fp32 state in
+ *   h [B, NH, DV] (dt)   C_out, n_out, m_out: the state after the step
+ *
+ * DQK >= 1 and DV a multiple of 4, DQK * DV <= 2^20.  In-place is allowed:
+ * C_out == C, n_out == n and m_out == m may each be equal (exactly, not
+ * partially overlapping); any other overlap is MLSTM_ERR_ALIAS.
+ */
+mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                        const float* ipre, const float* fpre,
+                        const float* C, const float* n, const float* m,
+                        int B, int NH, int DQK, int DV,
+                        void* h, float* C_out, float* n_out, float* m_out, void* hip_stream);
+
+/* Static, human-readable name of a status code. */
+const char* mlstm_status_string(mlstm_status s);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int mlstm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBMLSTM_MLSTM_H */

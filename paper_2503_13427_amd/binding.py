@@ -1,0 +1,116 @@
+"""ctypes binding of libmlstm (``include/mlstm.h``): argument marshalling only.
+
+Every step of the cell runs in the HIP library; this module turns torch
+tensors into device pointers and sizes, picks the current HIP stream, and
+raises ``MlstmError`` on a non-OK status.  torch supplies device memory and
+streams only.  If ``libmlstm.so`` is not built, importing this module fails
+loudly: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmlstm.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"libmlstm.so is not built at {LIB_PATH}; run __graft_entry__.build() "
+                      "or python -m paper_2503_13427_amd.build")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+MLSTM_OK = 0
+MLSTM_F32 = 0
+MLSTM_BF16 = 1
+STATUS_NAMES = {0: "MLSTM_OK", 1: "MLSTM_ERR_NULL_PTR", 2: "MLSTM_ERR_BAD_SHAPE", 3: "MLSTM_ERR_UNSUPPORTED",
+                4: "MLSTM_ERR_MISALIGNED", 5: "MLSTM_ERR_ALIAS", 6: "MLSTM_ERR_WORKSPACE", 7: "MLSTM_ERR_HIP"}
+
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+lib.mlstm_chunkwise_fwd.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                                    _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+lib.mlstm_chunkwise_fwd.restype = _i
+lib.mlstm_chunkwise_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i]
+lib.mlstm_chunkwise_workspace_bytes.restype = ctypes.c_size_t
+lib.mlstm_step.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp]
+lib.mlstm_step.restype = _i
+lib.mlstm_status_string.argtypes = [_i]
+lib.mlstm_status_string.restype = ctypes.c_char_p
+lib.mlstm_version.argtypes = []
+lib.mlstm_version.restype = _i
+
+
+class MlstmError(RuntimeError):
+    def __init__(self, status: int):
+        self.status = status
+        super().__init__(mlstm_status_string(status))
+
+
+def mlstm_status_string(status: int) -> str:
+    return lib.mlstm_status_string(int(status)).decode()
+
+
+def mlstm_version() -> int:
+    return lib.mlstm_version()
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return MLSTM_BF16
+    if t.dtype == torch.float32:
+        return MLSTM_F32
+    raise TypeError(f"q/k/v must be bfloat16 or float32, got {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("libmlstm needs contiguous tensors")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _check(status: int) -> None:
+    if status != MLSTM_OK:
+        raise MlstmError(status)
+
+
+def mlstm_chunkwise_workspace_bytes(B: int, NH: int, T: int, DQK: int, DV: int, L: int,
+                                    dtype: torch.dtype = torch.bfloat16) -> int:
+    code = MLSTM_BF16 if dtype == torch.bfloat16 else MLSTM_F32
+    return int(lib.mlstm_chunkwise_workspace_bytes(B, NH, T, DQK, DV, L, code))
+
+
+def mlstm_chunkwise_fwd(q, k, v, ipre, fpre, C0, n0, m0, L, h, CT, nT, mT,
+                        workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Chunkwise prefill.  Tensors as in ``include/mlstm.h``; shapes are read from q and v.
+    ``C0, n0, m0`` all None means the zero state.  ``workspace`` is an optional uint8 device
+    tensor of at least ``mlstm_chunkwise_workspace_bytes`` bytes."""
+    B, NH, T, DQK = q.shape
+    DV = v.shape[3]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.mlstm_chunkwise_fwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre),
+                                   _ptr(C0), _ptr(n0), _ptr(m0), B, NH, T, DQK, DV, int(L),
+                                   _ptr(h), _ptr(CT), _ptr(nT), _ptr(mT), _ptr(workspace), ws_bytes,
+                                   _stream(stream)))
+
+
+def mlstm_step(q, k, v, ipre, fpre, C, n, m, h, C_out, n_out, m_out, stream=None) -> None:
+    """One decode step.  q, k [B, NH, DQK]; v, h [B, NH, DV]; state outputs may be the inputs."""
+    B, NH, DQK = q.shape
+    DV = v.shape[2]
+    _check(lib.mlstm_step(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre), _ptr(C),
+                          _ptr(n), _ptr(m), B, NH, DQK, DV, _ptr(h), _ptr(C_out), _ptr(n_out), _ptr(m_out),
+                          _stream(stream)))

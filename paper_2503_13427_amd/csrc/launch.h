@@ -1,0 +1,46 @@
+// Internal launch interface between the C-ABI layer and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+#include "mlstm.h"
+
+namespace mlstm {
+
+// --- decode step -----------------------------------------------------------
+hipError_t launch_step(mlstm_dtype dt, const void* q, const void* k, const void* v, const float* ipre,
+                       const float* fpre, const float* C, const float* n, const float* m, int B, int NH,
+                       int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
+                       hipStream_t stream);
+size_t step_lds_bytes(int DQK, int DV);
+
+// --- chunkwise prefill, fp32 VALU kernel (small heads) -----------------------
+struct ChunkArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* ipre;
+    const float* fpre;
+    const float* C0;  // may be NULL (zero state)
+    const float* n0;
+    const float* m0;
+    int B, NH, T, DQK, DV, L;
+    void* h;
+    float* CT;
+    float* nT;
+    float* mT;
+};
+
+// Returns the dv tile the fp32 kernel would use, or 0 if no tile fits its LDS budget.
+int chunk_f32_tile(int DQK, int DV, int L);
+hipError_t launch_chunk_f32(mlstm_dtype dt, const ChunkArgs& a, hipStream_t stream);
+
+// --- chunkwise prefill, bf16 MFMA kernels (DQK = 256, DV = 512) --------------
+bool chunk_mfma_supported(mlstm_dtype dt, int DQK, int DV, int L);
+// Number of sequence segments the segment-parallel schedule uses (1 = fused single pass).
+int chunk_mfma_segments(int B, int NH, int T, int L);
+size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L);
+hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+}  // namespace mlstm

@@ -1,0 +1,165 @@
+// C-ABI layer of libmlstm: argument validation (pure host code, no HIP call
+// before a call is accepted), kernel selection and launch.
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+#include "launch.h"
+#include "mlstm.h"
+
+namespace {
+
+struct Range {
+    uintptr_t lo, hi;  // [lo, hi)
+};
+
+inline Range range_of(const void* p, size_t bytes) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    return Range{a, a + bytes};
+}
+
+inline bool overlap(Range a, Range b) {
+    if (a.lo == a.hi || b.lo == b.hi) return false;
+    return a.lo < b.hi && b.lo < a.hi;
+}
+
+inline bool misaligned(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u); }
+
+inline bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+    if (a < 0 || b < 0) return false;
+    if (a != 0 && b > INT64_MAX / a) return false;
+    *out = a * b;
+    return true;
+}
+
+inline size_t elem_bytes(mlstm_dtype dt) { return dt == MLSTM_BF16 ? 2 : 4; }
+
+}  // namespace
+
+extern "C" {
+
+const char* mlstm_status_string(mlstm_status s) {
+    switch (s) {
+        case MLSTM_OK: return "MLSTM_OK";
+        case MLSTM_ERR_NULL_PTR: return "MLSTM_ERR_NULL_PTR: a required pointer is NULL, or the initial state is partially given";
+        case MLSTM_ERR_BAD_SHAPE: return "MLSTM_ERR_BAD_SHAPE: invalid size, or T is not a multiple of L";
+        case MLSTM_ERR_UNSUPPORTED: return "MLSTM_ERR_UNSUPPORTED: this (dtype, DQK, DV, L) combination is not built";
+        case MLSTM_ERR_MISALIGNED: return "MLSTM_ERR_MISALIGNED: a tensor pointer is not 16-byte aligned";
+        case MLSTM_ERR_ALIAS: return "MLSTM_ERR_ALIAS: an output overlaps an input or another output";
+        case MLSTM_ERR_WORKSPACE: return "MLSTM_ERR_WORKSPACE: workspace smaller than mlstm_chunkwise_workspace_bytes";
+        case MLSTM_ERR_HIP: return "MLSTM_ERR_HIP: the HIP runtime reported an error at launch";
+    }
+    return "MLSTM_UNKNOWN_STATUS";
+}
+
+int mlstm_version(void) { return 100; }
+
+size_t mlstm_chunkwise_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L, mlstm_dtype dt) {
+    if (B <= 0 || NH <= 0 || T < 0 || L <= 0 || (T % L)) return 0;
+    if (!mlstm::chunk_mfma_supported(dt, DQK, DV, L)) return 0;
+    return mlstm::chunk_mfma_workspace_bytes(B, NH, T, DQK, DV, L);
+}
+
+mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                                 const float* ipre, const float* fpre, const float* C0, const float* n0,
+                                 const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
+                                 float* CT, float* nT, float* mT, void* workspace, size_t workspace_bytes,
+                                 void* hip_stream) {
+    // per-token buffers are empty (and may be NULL) when T == 0
+    if (T != 0 && (!q || !k || !v || !ipre || !fpre || !h)) return MLSTM_ERR_NULL_PTR;
+    if (!CT || !nT || !mT) return MLSTM_ERR_NULL_PTR;
+    const int n_init = (C0 != nullptr) + (n0 != nullptr) + (m0 != nullptr);
+    if (n_init != 0 && n_init != 3) return MLSTM_ERR_NULL_PTR;
+    if (workspace_bytes > 0 && !workspace) return MLSTM_ERR_NULL_PTR;
+    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (B <= 0 || NH <= 0 || T < 0 || DQK <= 0 || DV <= 0 || L <= 0) return MLSTM_ERR_BAD_SHAPE;
+    if (T % L) return MLSTM_ERR_BAD_SHAPE;
+
+    int64_t S, ST, nq, nv, nC, nn;
+    if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &ST) || !mul_ok(ST, DQK, &nq) || !mul_ok(ST, DV, &nv) ||
+        !mul_ok(S, static_cast<int64_t>(DQK) * DV, &nC) || !mul_ok(S, DQK, &nn) || S > INT32_MAX)
+        return MLSTM_ERR_BAD_SHAPE;
+
+    const void* ptrs[] = {q, k, v, ipre, fpre, C0, n0, m0, h, CT, nT, mT, workspace};
+    for (const void* p : ptrs)
+        if (misaligned(p)) return MLSTM_ERR_MISALIGNED;
+
+    const size_t eb = elem_bytes(dt);
+    const Range in[] = {range_of(q, nq * eb), range_of(k, nq * eb), range_of(v, nv * eb),
+                        range_of(ipre, ST * 4), range_of(fpre, ST * 4), range_of(C0, C0 ? nC * 4 : 0),
+                        range_of(n0, n0 ? nn * 4 : 0), range_of(m0, m0 ? S * 4 : 0)};
+    const Range out[] = {range_of(h, nv * eb), range_of(CT, nC * 4), range_of(nT, nn * 4), range_of(mT, S * 4),
+                         range_of(workspace, workspace_bytes)};
+    for (const Range& o : out) {
+        for (const Range& i : in)
+            if (overlap(o, i)) return MLSTM_ERR_ALIAS;
+    }
+    for (size_t a = 0; a < sizeof(out) / sizeof(out[0]); ++a)
+        for (size_t b = a + 1; b < sizeof(out) / sizeof(out[0]); ++b)
+            if (overlap(out[a], out[b])) return MLSTM_ERR_ALIAS;
+
+    const bool mfma = mlstm::chunk_mfma_supported(dt, DQK, DV, L);
+    if (!mfma && mlstm::chunk_f32_tile(DQK, DV, L) == 0) return MLSTM_ERR_UNSUPPORTED;
+    // the MFMA kernel addresses one sequence's v through a 32-bit buffer range
+    if (mfma && static_cast<int64_t>(T) * DV * 2 >= (int64_t(1) << 31)) return MLSTM_ERR_UNSUPPORTED;
+
+    size_t ws_need = 0;
+    if (mfma) ws_need = mlstm::chunk_mfma_workspace_bytes(B, NH, T, DQK, DV, L);
+    if (workspace_bytes > 0 && workspace_bytes < ws_need) return MLSTM_ERR_WORKSPACE;
+
+    mlstm::ChunkArgs a{q, k, v, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT};
+    hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+    hipError_t e = mfma ? mlstm::launch_chunk_mfma(a, workspace_bytes ? workspace : nullptr,
+                                                   workspace_bytes, stream)
+                        : mlstm::launch_chunk_f32(dt, a, stream);
+    return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
+mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,
+                        const float* fpre, const float* C, const float* n, const float* m, int B, int NH,
+                        int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
+                        void* hip_stream) {
+    if (!q || !k || !v || !ipre || !fpre || !C || !n || !m || !h || !C_out || !n_out || !m_out)
+        return MLSTM_ERR_NULL_PTR;
+    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (B <= 0 || NH <= 0 || DQK <= 0 || DV <= 0 || (DV % 4)) return MLSTM_ERR_BAD_SHAPE;
+    if (static_cast<int64_t>(DQK) * DV > (int64_t(1) << 20) || DQK > 4096) return MLSTM_ERR_UNSUPPORTED;
+    int64_t S;
+    if (!mul_ok(B, NH, &S) || S > INT32_MAX) return MLSTM_ERR_BAD_SHAPE;
+
+    const void* ptrs[] = {q, k, v, ipre, fpre, C, n, m, h, C_out, n_out, m_out};
+    for (const void* p : ptrs)
+        if (misaligned(p)) return MLSTM_ERR_MISALIGNED;
+
+    const size_t eb = elem_bytes(dt);
+    const int64_t nC = S * DQK * DV, nn = S * DQK;
+    const Range rq = range_of(q, S * DQK * eb), rk = range_of(k, S * DQK * eb), rv = range_of(v, S * DV * eb);
+    const Range ri = range_of(ipre, S * 4), rf = range_of(fpre, S * 4);
+    const Range rC = range_of(C, nC * 4), rn = range_of(n, nn * 4), rm = range_of(m, S * 4);
+    const Range rh = range_of(h, S * DV * eb), rCo = range_of(C_out, nC * 4), rno = range_of(n_out, nn * 4),
+                rmo = range_of(m_out, S * 4);
+    // h overlaps nothing
+    for (const Range& r : {rq, rk, rv, ri, rf, rC, rn, rm, rCo, rno, rmo})
+        if (overlap(rh, r)) return MLSTM_ERR_ALIAS;
+    // each state output may equal its own input exactly, and overlaps nothing else
+    struct Pair {
+        Range out;
+        Range same;
+        bool exact;
+    };
+    const Pair pairs[] = {{rCo, rC, C_out == C}, {rno, rn, n_out == n}, {rmo, rm, m_out == m}};
+    for (const Pair& p : pairs) {
+        if (overlap(p.out, p.same) && !p.exact) return MLSTM_ERR_ALIAS;
+        for (const Range& r : {rq, rk, rv, ri, rf})
+            if (overlap(p.out, r)) return MLSTM_ERR_ALIAS;
+    }
+    if (overlap(rCo, rn) || overlap(rCo, rm) || overlap(rno, rC) || overlap(rno, rm) || overlap(rmo, rC) ||
+        overlap(rmo, rn) || overlap(rCo, rno) || overlap(rCo, rmo) || overlap(rno, rmo))
+        return MLSTM_ERR_ALIAS;
+
+    hipError_t e = mlstm::launch_step(dt, q, k, v, ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
+                                      static_cast<hipStream_t>(hip_stream));
+    return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
+}  // extern "C"

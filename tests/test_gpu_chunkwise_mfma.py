@@ -1,0 +1,198 @@
+"""mlstm_chunkwise_fwd on the bf16 MFMA kernel (DQK=256, DV=512, L in {64, 128}) against the
+fp64 recurrent oracle.
+
+Parity bar: max relative error <= 2e-2 per (batch, head) slice for h and the final state
+(bf16 q/k/v/h, fp32 state).  Covers several chunks and segments, an initial state, the
+floor branch, short and long memory, the soft-capped gates, T = 0, the segment-parallel
+schedule (workspace), chunk-size independence, state carry, decode steps == prefill,
+run-to-run determinism, and the three prefill workloads at full size (sampled heads).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import coracle
+from paper_2503_13427_amd import configs
+from paper_2503_13427_amd.inputs import GateDist, StateDist, make_prefill
+from tests.helpers import (TOL_BF16, alloc_prefill_outputs, host_f64, rel_err, state_errs, upload_prefill)
+
+pytestmark = pytest.mark.gpu
+
+
+def _mb():
+    from paper_2503_13427_amd import binding
+    return binding
+
+
+def run(inp, L, workspace=True, dev_inputs=None):
+    d = dev_inputs or upload_prefill(inp)
+    o = alloc_prefill_outputs(inp)
+    ws = None
+    if workspace:
+        nb = _mb().mlstm_chunkwise_workspace_bytes(inp.B, inp.NH, inp.T, inp.DQK, inp.DV, L)
+        if nb:
+            ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    _mb().mlstm_chunkwise_fwd(d["q"], d["k"], d["v"], d["ipre"], d["fpre"], d["C0"], d["n0"], d["m0"], L,
+                              o["h"], o["CT"], o["nT"], o["mT"], workspace=ws)
+    torch.cuda.synchronize()
+    return o
+
+
+def check(inp, o, heads=None, label=""):
+    """Compare device outputs with the oracle; ``heads`` selects global head indices (then
+    ``inp`` must be the matching subset drawn with the same heads)."""
+    S_all = o["h"].shape[0] * o["h"].shape[1]
+    hr, Cr, nr, mr = coracle.recurrent_inputs(inp)
+    sel = np.arange(S_all) if heads is None else np.asarray(heads)
+    idx = torch.from_numpy(sel).cuda()
+    T = o["h"].shape[2]
+    h = host_f64(o["h"].reshape(S_all, T, -1).index_select(0, idx))
+    C = host_f64(o["CT"].reshape(S_all, 256, 512).index_select(0, idx))
+    n = host_f64(o["nT"].reshape(S_all, 256).index_select(0, idx))
+    m = host_f64(o["mT"].reshape(S_all).index_select(0, idx))
+    S = len(sel)
+    eh = rel_err(h.reshape(S, -1), hr.reshape(S, -1), 1)
+    eC, en, em = state_errs(C, n, m, Cr, nr, mr)
+    print(f"{label} h {eh:.3e} C {eC:.3e} n {en:.3e} m {em:.3e}")
+    assert np.isfinite(h).all()
+    assert eh <= TOL_BF16 and eC <= TOL_BF16 and en <= TOL_BF16 and em <= TOL_BF16, (eh, eC, en, em)
+    return eh, eC, en, em
+
+
+CASES = [
+    # (B, NH, T, L, gates, state)
+    (1, 2, 256, 64, GateDist(), None),
+    (1, 2, 256, 128, GateDist(), None),
+    (2, 1, 384, 64, GateDist(f_mu=5, f_sd=2, cap=15.0), StateDist()),
+    (1, 2, 512, 128, GateDist(f_mu=5, f_sd=2, cap=15.0), StateDist()),
+    (1, 2, 192, 64, GateDist(i_mu=-10.0), None),                 # floor branch active
+    (1, 2, 256, 64, GateDist(f_mu=-1.0, f_sd=2.0), StateDist()),  # short memory
+    (1, 1, 64, 64, GateDist(), StateDist()),                     # a single chunk
+    (1, 1, 128, 128, GateDist(i_mu=2.0, i_sd=3.0), None),        # large input gates
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"B{c[0]}NH{c[1]}T{c[2]}L{c[3]}-{c[4]}-{c[5] is not None}")
+@pytest.mark.parametrize("workspace", [False, True], ids=["fused", "segments"])
+def test_mfma_matches_oracle(case, workspace):
+    B, NH, T, L, g, st = case
+    inp = make_prefill(workload=95, B=B, NH=NH, T=T, DQK=256, DV=512, dtype="bf16", gates=g, state=st)
+    o = run(inp, L, workspace=workspace)
+    check(inp, o, label=str(case))
+
+
+def test_segment_schedule_is_used_and_agrees():
+    """The workload shape of the T=2048 prefill asks for a workspace; both schedules agree."""
+    w = configs.PREFILL_T2048
+    assert _mb().mlstm_chunkwise_workspace_bytes(w.B, w.NH, w.T, 256, 512, w.L) > 0
+    inp = w.prefill_inputs(T=1024)
+    a = run(inp, 64, workspace=False)
+    b = run(inp, 64, workspace=True)
+    S = inp.B * inp.NH
+    assert rel_err(host_f64(a["h"]).reshape(S, -1), host_f64(b["h"]).reshape(S, -1), 1) < 1e-2
+    np.testing.assert_allclose(host_f64(a["mT"]), host_f64(b["mT"]), rtol=1e-5, atol=1e-5)
+
+
+def test_workspace_too_small_is_rejected():
+    w = configs.PREFILL_T2048
+    inp = w.prefill_inputs(T=512)
+    nb = _mb().mlstm_chunkwise_workspace_bytes(1, 8, 512, 256, 512, 64)
+    assert nb > 0
+    d = upload_prefill(inp)
+    o = alloc_prefill_outputs(inp)
+    ws = torch.empty(nb - 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(_mb().MlstmError) as e:
+        _mb().mlstm_chunkwise_fwd(d["q"], d["k"], d["v"], d["ipre"], d["fpre"], None, None, None, 64,
+                                  o["h"], o["CT"], o["nT"], o["mT"], workspace=ws)
+    assert e.value.status == 6
+
+
+def test_empty_sequence_mfma():
+    inp = make_prefill(workload=96, B=1, NH=2, T=0, DQK=256, DV=512, dtype="bf16", gates=GateDist(),
+                       state=StateDist())
+    o = run(inp, 64)
+    np.testing.assert_array_equal(host_f64(o["CT"]), inp.C0.astype(np.float64))
+    np.testing.assert_array_equal(host_f64(o["nT"]), inp.n0.astype(np.float64))
+    np.testing.assert_array_equal(host_f64(o["mT"]), inp.m0.astype(np.float64))
+
+
+def test_chunk_size_independence_and_determinism():
+    inp = make_prefill(workload=97, B=1, NH=2, T=512, DQK=256, DV=512, dtype="bf16", gates=GateDist(),
+                       state=StateDist())
+    a = run(inp, 64)
+    b = run(inp, 128)
+    c = run(inp, 64)
+    assert rel_err(host_f64(a["h"]).reshape(2, -1), host_f64(b["h"]).reshape(2, -1), 1) < 1e-2
+    np.testing.assert_allclose(host_f64(a["mT"]), host_f64(b["mT"]), rtol=1e-5, atol=1e-5)
+    for k in a:
+        assert torch.equal(a[k], c[k]), k
+
+
+def test_state_carry():
+    """prefill(T1) -> (C, n, m) -> prefill(T2) == prefill(T1 + T2), within the bf16 bar."""
+    inp = make_prefill(workload=98, B=1, NH=2, T=512, DQK=256, DV=512, dtype="bf16", gates=GateDist(),
+                       state=StateDist())
+    d = upload_prefill(inp)
+    full = run(inp, 64, dev_inputs=d)
+    first = {k: (v[:, :, :256].contiguous() if k in ("q", "k", "v", "ipre", "fpre") else v) for k, v in d.items()}
+    second = {k: (v[:, :, 256:].contiguous() if k in ("q", "k", "v", "ipre", "fpre") else v) for k, v in d.items()}
+    o1 = alloc_prefill_outputs(make_prefill(workload=98, B=1, NH=2, T=256, DQK=256, DV=512, dtype="bf16",
+                                            gates=GateDist()))
+    mb = _mb()
+    mb.mlstm_chunkwise_fwd(first["q"], first["k"], first["v"], first["ipre"], first["fpre"], d["C0"], d["n0"],
+                           d["m0"], 64, o1["h"], o1["CT"], o1["nT"], o1["mT"])
+    o2 = alloc_prefill_outputs(make_prefill(workload=98, B=1, NH=2, T=256, DQK=256, DV=512, dtype="bf16",
+                                            gates=GateDist()))
+    mb.mlstm_chunkwise_fwd(second["q"], second["k"], second["v"], second["ipre"], second["fpre"], o1["CT"],
+                           o1["nT"], o1["mT"], 64, o2["h"], o2["CT"], o2["nT"], o2["mT"])
+    torch.cuda.synchronize()
+    h12 = torch.cat([o1["h"], o2["h"]], dim=2)
+    assert rel_err(host_f64(h12).reshape(2, -1), host_f64(full["h"]).reshape(2, -1), 1) < 1e-2
+    eC, en, em = state_errs(host_f64(o2["CT"]).reshape(2, 256, 512), host_f64(o2["nT"]).reshape(2, 256),
+                            host_f64(o2["mT"]).reshape(2), host_f64(full["CT"]).reshape(2, 256, 512),
+                            host_f64(full["nT"]).reshape(2, 256), host_f64(full["mT"]).reshape(2))
+    assert max(eC, en) < 1e-2 and em < 1e-5
+
+
+def test_decode_steps_equal_prefill_bf16():
+    """T steps of mlstm_step == mlstm_chunkwise_fwd over the same T tokens (both on the GPU)."""
+    inp = make_prefill(workload=99, B=1, NH=2, T=128, DQK=256, DV=512, dtype="bf16", gates=GateDist(),
+                       state=StateDist())
+    d = upload_prefill(inp)
+    pre = run(inp, 64, dev_inputs=d)
+    C, n, m = d["C0"].clone(), d["n0"].clone(), d["m0"].clone()
+    hs = []
+    for t in range(inp.T):
+        h = torch.empty(1, 2, 512, dtype=torch.bfloat16, device="cuda")
+        _mb().mlstm_step(d["q"][:, :, t].contiguous(), d["k"][:, :, t].contiguous(), d["v"][:, :, t].contiguous(),
+                         d["ipre"][:, :, t].contiguous(), d["fpre"][:, :, t].contiguous(), C, n, m, h, C, n, m)
+        hs.append(h)
+    torch.cuda.synchronize()
+    hstep = host_f64(torch.stack(hs, dim=2))
+    assert rel_err(hstep.reshape(2, -1), host_f64(pre["h"]).reshape(2, -1), 1) < 1e-2
+    eC, en, em = state_errs(host_f64(C).reshape(2, 256, 512), host_f64(n).reshape(2, 256), host_f64(m).reshape(2),
+                            host_f64(pre["CT"]).reshape(2, 256, 512), host_f64(pre["nT"]).reshape(2, 256),
+                            host_f64(pre["mT"]).reshape(2))
+    assert max(eC, en) < 1e-2 and em < 1e-5
+
+
+# ---- the prefill workloads at full size -----------------------------------------------------------
+
+def test_prefill_T2048_full():
+    """B=1, NH=8, T=2048, L=64, zero state: every head against the oracle."""
+    w = configs.PREFILL_T2048
+    inp = w.prefill_inputs()
+    o = run(inp, w.L)
+    check(inp, o, label=w.name)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("wl", [configs.PREFILL_T8192, configs.CONT_PREFILL_T32768], ids=lambda w: w.name)
+def test_prefill_full_size_sampled_heads(wl):
+    """Full-size launch (every head on the GPU, the benchmark's launch configuration) with a
+    sample of heads checked against the oracle."""
+    inp = wl.prefill_inputs()
+    o = run(inp, wl.L)
+    heads = [0, wl.heads - 1]
+    sub = wl.prefill_inputs(heads=heads)
+    check(sub, o, heads=heads, label=wl.name)

@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Benchmark of libmlstm on one MI355X: prefill tokens/s (%MFMA) and decode step us (%HBM).
+
+One JSON line on stdout.  The headline ``value`` is the chunkwise prefill of
+the xLSTM-7B-shaped workload B=1, NH=8, T=2048, DQK=256, DV=512, L=64 (bf16
+q/k/v, fp32 gates and state, zero initial state): one "step" is one
+mlstm_chunkwise_fwd call over that batch, all of its kernels included.
+Inputs are seeded synthetic data already resident in HBM; NINPUT copies are
+rotated so consecutive steps do not hit a warm Infinity Cache.
+
+Extra objects on the same line:
+  roofline      achieved bf16 TFLOP/s (App. D.1 FLOP count per call / call
+                duration from HIP events on the launch stream) vs 2.5 PFLOP/s;
+  cpu_baseline  the fp64 CPU oracle on the same workload (host cores);
+  decode        1024 consecutive mlstm_step calls at B=256, NH=8: us per step,
+                us per sequence-token, achieved GB/s vs 8 TB/s;
+  prefill       the two larger prefill workloads (B=8 x T=8192 soft-capped,
+                and B=4 x T=32768 from a nonzero state, L=128).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+from paper_2503_13427_amd import accounting as acc  # noqa: E402
+from paper_2503_13427_amd import configs  # noqa: E402
+
+METRIC = "mLSTM prefill tokens/s (%MFMA peak); decode step µs/token (%HBM BW)"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def dev(x, device="cuda"):
+    if x is None:
+        return None
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    if x.dtype == np.uint16:
+        t = t.view(torch.bfloat16)
+    return t.to(device)
+
+
+class Prefill:
+    """Device buffers for one prefill workload, NINPUT rotated input copies."""
+
+    def __init__(self, w, ninput=1, device="cuda"):
+        from paper_2503_13427_amd import binding
+        self.mb = binding
+        self.w = w
+        inp = w.prefill_inputs()
+        self.sets = []
+        for i in range(ninput):
+            self.sets.append(dict(q=dev(inp.q), k=dev(inp.k), v=dev(inp.v), ipre=dev(inp.ipre), fpre=dev(inp.fpre),
+                                  C0=dev(inp.C0), n0=dev(inp.n0), m0=dev(inp.m0)))
+        B, NH, T = w.B, w.NH, w.T
+        self.h = torch.empty(B, NH, T, w.DV, dtype=torch.bfloat16, device=device)
+        self.CT = torch.empty(B, NH, w.DQK, w.DV, device=device)
+        self.nT = torch.empty(B, NH, w.DQK, device=device)
+        self.mT = torch.empty(B, NH, device=device)
+        nb = binding.mlstm_chunkwise_workspace_bytes(B, NH, T, w.DQK, w.DV, w.L)
+        self.ws = torch.empty(nb, dtype=torch.uint8, device=device) if nb else None
+        self.i = 0
+
+    def step(self, stream=None):
+        d = self.sets[self.i % len(self.sets)]
+        self.i += 1
+        self.mb.mlstm_chunkwise_fwd(d["q"], d["k"], d["v"], d["ipre"], d["fpre"], d["C0"], d["n0"], d["m0"], self.w.L,
+                                    self.h, self.CT, self.nT, self.mT, workspace=self.ws, stream=stream)
+
+    def flops(self):
+        w = self.w
+        return acc.flops_chunkwise(w.B * w.NH, w.T, w.L, w.DQK, w.DV).total
+
+    def bytes(self):
+        w = self.w
+        return acc.prefill_bytes(w.B, w.NH, w.T, w.DQK, w.DV, with_initial_state=w.state is not None)
+
+
+def time_steps(fn, steps, warmup, stream):
+    """Wall time and HIP-event time (on the launch stream) of ``steps`` calls of fn."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall, e0.elapsed_time(e1) / 1e3
+
+
+def bench_prefill(w, steps, warmup, ninput, stream):
+    p = Prefill(w, ninput)
+    wall, ev = time_steps(lambda: p.step(stream), steps, warmup, stream)
+    t = ev / steps
+    fl = p.flops()
+    tok = w.B * w.T
+    out = dict(workload=w.name, tokens_per_s=tok / t, us_per_call=t * 1e6, tflops=fl / t / 1e12,
+               mfma_frac=fl / t / 1e12 / acc.PEAK_BF16_MFMA_TFLOPS, gbs=p.bytes() / t / 1e9,
+               hbm_frac=p.bytes() / t / 1e9 / acc.PEAK_HBM_GBS, wall_s=wall, steps=steps,
+               flops_per_call=fl, bytes_per_call=p.bytes(),
+               workspace_bytes=0 if p.ws is None else p.ws.numel())
+    return out, p
+
+
+def bench_decode(w, steps, stream, warm=16):
+    """``steps`` consecutive decode steps on device-resident per-step inputs; the initial state
+    comes from the library's own prefill of the workload's 128-token prompt."""
+    from paper_2503_13427_amd import binding as mb
+    log(f"decode: drawing {steps} steps of inputs for {w.heads} heads")
+    dec = w.decode_inputs(steps=steps)
+    q, k, v = dev(dec.q), dev(dec.k), dev(dec.v)
+    ip, fp = dev(dec.ipre), dev(dec.fpre)
+    del dec
+    # per-step contiguous slices, resident before timing
+    qs = [q[:, :, t].contiguous() for t in range(steps)]
+    ks = [k[:, :, t].contiguous() for t in range(steps)]
+    vs = [v[:, :, t].contiguous() for t in range(steps)]
+    ips = [ip[:, :, t].contiguous() for t in range(steps)]
+    fps = [fp[:, :, t].contiguous() for t in range(steps)]
+    del q, k, v, ip, fp
+    pre = w.prefill_inputs()
+    C = torch.empty(w.B, w.NH, w.DQK, w.DV, device="cuda")
+    n = torch.empty(w.B, w.NH, w.DQK, device="cuda")
+    m = torch.empty(w.B, w.NH, device="cuda")
+    hpre = torch.empty(w.B, w.NH, w.T, w.DV, dtype=torch.bfloat16, device="cuda")
+    mb.mlstm_chunkwise_fwd(dev(pre.q), dev(pre.k), dev(pre.v), dev(pre.ipre), dev(pre.fpre), None, None, None, w.L,
+                           hpre, C, n, m, stream=stream)
+    h = torch.empty(w.B, w.NH, w.DV, dtype=torch.bfloat16, device="cuda")
+    C0, n0, m0 = C.clone(), n.clone(), m.clone()
+    for t in range(warm):   # warm-up on a copy of the state
+        mb.mlstm_step(qs[t], ks[t], vs[t], ips[t], fps[t], C0, n0, m0, h, C0, n0, m0, stream=stream)
+    del C0, n0, m0
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for t in range(steps):
+        mb.mlstm_step(qs[t], ks[t], vs[t], ips[t], fps[t], C, n, m, h, C, n, m, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    t_step = e0.elapsed_time(e1) / 1e3 / steps
+    by = acc.step_bytes(w.B, w.NH, w.DQK, w.DV)
+    finite = bool(torch.isfinite(C).all().item())
+    return dict(workload=w.name, steps=steps, us_per_step=t_step * 1e6, us_per_token=t_step * 1e6 / w.B,
+                gbs=by / t_step / 1e9, hbm_frac=by / t_step / 1e9 / acc.PEAK_HBM_GBS, bytes_per_step=by,
+                wall_s=wall, state_finite=finite)
+
+
+def cpu_baseline(w, max_seconds=30.0):
+    """The fp64 oracle on the headline workload, timed on the host.  Heads are independent, so
+    the sample is a subset of heads over the full sequence (all heads if they fit the budget)."""
+    from oracle import coracle
+    aff = len(os.sched_getaffinity(0))
+    heads = list(range(w.heads))
+    threads = max(1, min(aff, len(heads), 16))
+    inp = w.prefill_inputs()
+    t0 = time.perf_counter()
+    coracle.recurrent_inputs(inp, nthreads=threads)
+    dt = time.perf_counter() - t0
+    return dict(value=w.B * w.T / dt, unit="tokens/s", cores=threads, kind="oracle",
+                sample=f"full workload {w.name} (all {w.heads} heads x {w.T} tokens), fp64 recurrent form, "
+                       f"{dt:.2f} s wall on {threads} threads", seconds=dt)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--ninput", type=int, default=8, help="rotated input copies (defeats a warm MALL)")
+    ap.add_argument("--decode-steps", type=int, default=1024)
+    ap.add_argument("--skip-decode", action="store_true")
+    ap.add_argument("--skip-large", action="store_true")
+    ap.add_argument("--skip-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["prefill", "decode", "large"], default=None,
+                    help="run one part only (profiling runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported (every (batch, head) "
+              "sequence is independent, so more GPUs would shard B*NH with no exchange)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    w = configs.PREFILL_T2048
+
+    res = {}
+    if args.only in (None, "prefill"):
+        log(f"prefill {w.name}: {args.warmup} warm-up + {args.steps} timed steps, {args.ninput} rotated inputs")
+        head, p = bench_prefill(w, args.steps, args.warmup, args.ninput, stream)
+        # warm-cache figure for reference: one input set
+        warm, _ = bench_prefill(w, args.steps, args.warmup, 1, stream)
+        head["warm_mall_us_per_call"] = warm["us_per_call"]
+        res["prefill"] = head
+        del p
+    if args.only in (None, "large") and not args.skip_large:
+        res["prefill_large"] = []
+        for wl, steps in ((configs.PREFILL_T8192, max(3, args.steps // 20)),
+                          (configs.CONT_PREFILL_T32768, max(2, args.steps // 40))):
+            log(f"prefill {wl.name}: {steps} timed steps")
+            r, p = bench_prefill(wl, steps, 1, 1, stream)
+            res["prefill_large"].append(r)
+            del p
+            torch.cuda.empty_cache()
+    if args.only in (None, "decode") and not args.skip_decode:
+        log(f"decode {configs.DECODE_B256.name}: {args.decode_steps} steps")
+        res["decode"] = bench_decode(configs.DECODE_B256, args.decode_steps, stream)
+        torch.cuda.empty_cache()
+
+    line = {"metric": METRIC, "value": None, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": None, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": w.name, "B": w.B, "NH": w.NH, "T": w.T, "dqk": w.DQK, "dv": w.DV, "L": w.L,
+                       "qkv": "bf16", "gates_state": "fp32", "initial_state": "zero"}}
+    if "prefill" in res:
+        hp = res["prefill"]
+        line["value"] = hp["tokens_per_s"]
+        line["ms_per_step"] = hp["us_per_call"] / 1e3
+        line["roofline"] = {"bound": "mfma", "achieved": hp["tflops"], "peak": acc.PEAK_BF16_MFMA_TFLOPS,
+                            "unit": "TFLOP/s", "frac": hp["mfma_frac"], "traffic": None,
+                            "kernel": "chunk_mfma_kernel<64, FULL> (+ local-state and combine kernels of the "
+                                      "segment schedule; achieved uses the whole call's duration)",
+                            "flops_per_call": hp["flops_per_call"], "hbm_frac": hp["hbm_frac"]}
+        line["prefill"] = hp
+    if "prefill_large" in res:
+        line["prefill_large"] = res["prefill_large"]
+    if "decode" in res:
+        line["decode"] = res["decode"]
+    if not args.skip_cpu_baseline and args.only in (None, "prefill"):
+        log("cpu baseline: fp64 oracle")
+        line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -7,16 +7,19 @@
 // place: every element of C and n is read and written by the same thread, and
 // m is written only after a barrier that follows every read of it.
 //
-// The kernel is HBM-bound: C is streamed as float4 (128-bit) loads and stores
-// along DV, each thread walks a column group down the DQK rows with the loads
-// of several rows in flight, and the read-out C'^T q^ is reduced across the
-// row groups in LDS.
+// The kernel is HBM-bound: C is streamed as float4 (128-bit) non-temporal loads
+// and stores along DV; each thread walks a column group down the DQK rows with
+// kBatch rows in flight, and the read-out C'^T q^ is reduced across the row
+// groups in LDS.
 #include "device_common.h"
 #include "launch.h"
 
 namespace mlstm {
 
-constexpr int kStepThreads = 256;
+constexpr int kStepThreads = 512;
+constexpr int kBatch = 16;   // rows per pipeline stage
+
+typedef float f4_t __attribute__((ext_vector_type(4)));
 
 template <typename TIn>
 __global__ void __launch_bounds__(kStepThreads)
@@ -34,6 +37,23 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
     const int tid = threadIdx.x;
     const int NC4 = DV >> 2;
     const int RG = NC4 >= kStepThreads ? 1 : kStepThreads / NC4;
+    const int rg = RG == 1 ? 0 : tid / NC4;    // row group: rows rg, rg + RG, ...
+    const int c4_first = tid % NC4;            // first float4 column
+    const int c4_stride = RG == 1 ? kStepThreads : NC4;
+    const bool active = rg < RG;
+    const int nrows = active ? (DQK - rg + RG - 1) / RG : 0;
+
+    // C' = f C + (i k) v^T is streamed once (Eq. 3) with kBatch rows in flight per thread.
+    // C_out may be C itself, so the compiler cannot hoist loads over stores; the next batch
+    // is loaded explicitly before the current one is stored (disjoint rows, so the order is
+    // exact).  The first batch is issued before the gate prologue, which it does not need.
+    const f4_t* Ch = reinterpret_cast<const f4_t*>(C + head * static_cast<int64_t>(DQK) * DV);
+    f4_t* Ch_out = reinterpret_cast<f4_t*>(C_out + head * static_cast<int64_t>(DQK) * DV);
+    auto row = [&](int r) { return static_cast<int64_t>(rg + r * RG) * NC4; };
+    f4_t cur[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+        if (u < nrows) cur[u] = __builtin_nontemporal_load(&Ch[row(u) + c4_first]);
 
     // s1: scalar gates (Eqs. 2, 7, 8), computed redundantly by every thread
     const float mprev = m[head];
@@ -66,48 +86,61 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
     float qn = 0.0f;
 #pragma unroll
     for (int w = 0; w < kStepThreads / 64; ++w) qn += wsum[w];
+    const float inv = 1.0f / fmaxf(fabsf(qn), expf(-mnew));
 
-    // s2 + s4: C' = f C + (i k) v^T streamed once; num = C'^T q^ (Eqs. 3, 5)
-    const float4* Ch = reinterpret_cast<const float4*>(C + head * static_cast<int64_t>(DQK) * DV);
-    float4* Ch_out = reinterpret_cast<float4*>(C_out + head * static_cast<int64_t>(DQK) * DV);
+    // s2 + s4: the C stream and num = C'^T q^ (Eqs. 3, 5)
     const TIn* vh = v + head * DV;
-    for (int c4 = tid % NC4; c4 < NC4; c4 += (RG == 1 ? kStepThreads : NC4)) {
-        const int rg = RG == 1 ? 0 : tid / NC4;
-        if (rg >= RG) break;
+    for (int c4 = c4_first; active && c4 < NC4; c4 += c4_stride) {
+        if (c4 != c4_first) {
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u)
+                if (u < nrows) cur[u] = __builtin_nontemporal_load(&Ch[row(u) + c4]);
+        }
         const float v0 = io<TIn>::load(vh, 4 * c4 + 0), v1 = io<TIn>::load(vh, 4 * c4 + 1);
         const float v2 = io<TIn>::load(vh, 4 * c4 + 2), v3 = io<TIn>::load(vh, 4 * c4 + 3);
         float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-#pragma unroll 8
-        for (int d = rg; d < DQK; d += RG) {
-            float4 c = Ch[static_cast<int64_t>(d) * NC4 + c4];
-            const float ikd = iks[d];
-            c.x = fg * c.x + ikd * v0;
-            c.y = fg * c.y + ikd * v1;
-            c.z = fg * c.z + ikd * v2;
-            c.w = fg * c.w + ikd * v3;
-            Ch_out[static_cast<int64_t>(d) * NC4 + c4] = c;
-            const float qd = qs[d];
-            a0 += qd * c.x;
-            a1 += qd * c.y;
-            a2 += qd * c.z;
-            a3 += qd * c.w;
+        for (int r0 = 0; r0 < nrows; r0 += kBatch) {
+            f4_t nxt[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int r = r0 + kBatch + u;
+                if (r < nrows) nxt[u] = __builtin_nontemporal_load(&Ch[row(r) + c4]);
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int r = r0 + u;
+                if (r < nrows) {
+                    const int d = rg + r * RG;
+                    f4_t c = cur[u];
+                    const float ikd = iks[d];
+                    c.x = fg * c.x + ikd * v0;
+                    c.y = fg * c.y + ikd * v1;
+                    c.z = fg * c.z + ikd * v2;
+                    c.w = fg * c.w + ikd * v3;
+                    __builtin_nontemporal_store(c, &Ch_out[row(r) + c4]);
+                    const float qd = qs[d];
+                    a0 += qd * c.x;
+                    a1 += qd * c.y;
+                    a2 += qd * c.z;
+                    a3 += qd * c.w;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) cur[u] = nxt[u];
         }
         if (RG == 1) {
             // s5: h = num / max(|n'.q^|, exp(-m'))
-            const float inv = 1.0f / fmaxf(fabsf(qn), expf(-mnew));
             TIn* hh = h + head * DV;
             io<TIn>::store(hh, 4 * c4 + 0, a0 * inv);
             io<TIn>::store(hh, 4 * c4 + 1, a1 * inv);
             io<TIn>::store(hh, 4 * c4 + 2, a2 * inv);
             io<TIn>::store(hh, 4 * c4 + 3, a3 * inv);
         } else {
-            float4* r = reinterpret_cast<float4*>(red) + rg * NC4 + c4;
-            *r = make_float4(a0, a1, a2, a3);
+            reinterpret_cast<float4*>(red)[rg * NC4 + c4] = make_float4(a0, a1, a2, a3);
         }
     }
     if (RG > 1) {
         __syncthreads();
-        const float inv = 1.0f / fmaxf(fabsf(qn), expf(-mnew));
         TIn* hh = h + head * DV;
         for (int j = tid; j < DV; j += kStepThreads) {
             float s = 0.0f;

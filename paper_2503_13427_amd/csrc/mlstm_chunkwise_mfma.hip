@@ -15,30 +15,43 @@
 //   w_tau = exp(x_tau - M_L),  m_next = b_L + M_L.
 // Every exponent is a difference against M and is <= 0 by construction.
 //
+// Lazily scaled matrix memory.  The accumulators hold C_acc with C = C_acc e^{s}.
+// A chunk's decay is folded into s (s += m_prev - M_L) and into the key weights
+// of the update (w e^{-s} <= e^{-kRenorm}), so the 128 accumulator registers of a
+// wave are not rescaled by VALU work in most chunks; when s would fall below
+// kRenorm the chunk applies the decay eagerly instead (C_acc *= e^{s + m_prev - M_L},
+// between the read-out (iii) and the update (iv)) and s returns to 0.  The
+// inter-chunk term uses exp(m_prev - M_tau + s); the exit state is C_acc e^{s}.
+//
 // Products and their MFMA mapping (gfx950 bf16 MFMA, fp32 accumulate):
 //   (i)   S^T = K Q^T             16x16x32: A = K rows, B = Q rows (both d-contiguous)
-//   (ii)  N^T += V^T S~^T         32x32x16: A = V^T (sigma-contiguous), B = S~ rows
-//   (iii) N^T += C^T Q^T          32x32x16: A = C straight from the accumulators of
-//                                 (iv), converted to bf16 in registers, B = Q rows
-//   (iv)  C += (wK)^T V           32x32x16: A = (wK)^T, B = V^T (both tau-contiguous)
+//   (ii)  N^T += V^T S~^T         32x32x16: A = V read transposed, B = S~ rows
+//   (iii) N^T += C^T Q^T          32x32x16: A = the C accumulators of (iv), converted to
+//                                 bf16 in registers, B = Q rows
+//   (iv)  C += K^T (w e^{-s} V)   32x32x16: A = K read transposed, B = V read transposed
+//                                 and scaled by the key weights in registers
+//   Q n and K^T w                 16x16x32 with the fp32 normaliser and weights split into
+//                                 bf16 hi + lo rows (relative error ~2^-17)
+// "Read transposed" is the LDS transpose read of gfx950 (ds_read_b64_tr_b16): in each
+// 16-lane group, lane 4s+q supplies 4 consecutive elements of row s of a 4 x 16 tile and
+// lane c receives column c, so a row-major [k][m] tile arrives k-contiguous, as an MFMA
+// operand wants it.  Q, K and V therefore live in LDS only in their natural layout.
 // (iii) consumes C in the accumulator layout of (iv): the contraction index d is
-// permuted consistently in both operands, so no LDS round trip is needed.  The
-// outputs come out transposed (rows v, columns tau), so each lane holds runs of
-// four consecutive v of one h row and stores 8 bytes at a time.
+// permuted consistently in both operands.  Outputs come out transposed (rows v,
+// columns tau), so each lane stores runs of four consecutive v of one h row.
 //
 // Work decomposition.  One workgroup of 4 waves owns one (sequence, 128-column
 // dv tile, segment) and walks the segment's chunks in order.  Wave w owns the
-// 256 x 32 fp32 slice C[:, 32w:32w+32] of the matrix memory in its MFMA
-// accumulators for the whole segment (128 registers per lane); n lives in LDS.
-// Within a chunk, Q and K are staged in four 64-wide d blocks; the next block
-// (and the next chunk's V and gates) is prefetched into registers while the
-// current block is multiplied.  K^T and V^T are transposed in registers on the
-// way into LDS.  The four dv tiles of a (sequence, segment) are dispatched
-// consecutively onto the same XCD so their shared Q/K reads hit one L2.
+// 256 x 32 slice C[:, 32w:32w+32] in its accumulators for the whole segment.
+// Q and K are staged in two 128-wide d halves; the next half (and the next
+// chunk's V and gates) is prefetched into registers while the current half is
+// multiplied.  The four dv
+// tiles of a (sequence, segment) are dispatched consecutively onto one XCD so
+// their shared Q/K reads hit one L2.
 //
 // Segment-parallel schedule (optional workspace).  With G segments per
 // sequence: (1) the LOCAL variant computes each of the first G-1 segments' state
-// from an empty state (C = 0, n = 0, m = -inf) -- gates, (wK)^T V and n only;
+// from an empty state (C = 0, n = 0, m = -inf) -- gates, the C and n updates only;
 // (2) a combine kernel scans those local states into each segment's entry state,
 // m_in' = max(gsum + m_in, m_loc), C_in' = e^{gsum + m_in - m_in'} C_in + e^{m_loc - m_in'} C_loc;
 // (3) the FULL variant runs every segment from its entry state.
@@ -52,18 +65,20 @@ constexpr int kDQK = 256;
 constexpr int kDV = 512;
 constexpr int kDVT = 128;             // dv columns per workgroup
 constexpr int kNTile = kDV / kDVT;    // 4 dv tiles per sequence
-constexpr int kDB = 64;               // d block staged per step
-constexpr int kNDB = kDQK / kDB;      // 4 d blocks
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kQScale = 0.0625f;    // 1 / sqrt(256), exact
+constexpr float kRenorm = -20.0f;     // rescale C eagerly when its lazy log-scale would drop below this
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x4_t mfma16(u32x4_t a, u32x4_t b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
@@ -74,60 +89,89 @@ __device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
                                                    c, 0, 0, 0);
 }
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-
 // Two fp32 -> packed bf16 pair, round to nearest even (one v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 __device__ __forceinline__ float lo_f32(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_f32(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-__device__ __forceinline__ uint32_t lo16(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
-__device__ __forceinline__ uint32_t hi16(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
-
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Accumulator access through single instructions: keeps the register allocator from
+// parking copies of whole accumulator tiles in VGPRs across the chunk loop.
+__device__ __forceinline__ float acc_read(float x) {
+    float t;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(t) : "a"(x));
+    return t;
+}
+__device__ __forceinline__ void scale_acc(f32x16_t& acc, float s) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        float x = acc[j];
+        float t;
+        asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
+                     : "+a"(x), "=&v"(t)
+                     : "v"(s));
+        acc[j] = x;
+    }
+}
+
+// LDS transpose read: 4 bf16 per lane (see the header comment for the lane mapping).
+__device__ __forceinline__ u32x2_t tr_read(const uint16_t* p) {
+    typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+    return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p)));
+}
+__device__ __forceinline__ u32x4_t cat(u32x2_t a, u32x2_t b) { return u32x4_t{a[0], a[1], b[0], b[1]}; }
+
+template <int L>
+struct Cfg {
+    static constexpr int NDB = 2;                   // d blocks staged per chunk
+    static constexpr int DB = kDQK / NDB;           // 256 or 128
+    static constexpr int DT = DB / 32;              // 32-row C tiles per d block
+    static constexpr int QP = DB + 8;               // row pitch (elements) of Q and K blocks
+    static constexpr int VP = kDVT + 8;             // row pitch of V
+    static constexpr int SP = L + 8;                // row pitch of S~
+    static constexpr int NB = L / 16;               // 16-wide blocks along the chunk
+};
 
 template <int L>
 struct Smem {
-    static constexpr int QP = kDB + 8;   // row pitch (elements) of the d-contiguous Q/K block tiles
-    static constexpr int TP = L + 8;     // row pitch of the tau-contiguous tiles
-    static constexpr int NB = L / 16;    // 16-wide blocks along the chunk
-    uint16_t Qb[L * QP];                 // Q[tau][d]  (current d block)
-    uint16_t Kb[L * QP];                 // K[tau][d]
-    uint16_t Ktb[kDB * TP];              // (w K)^T[d][tau]
-    uint16_t Vt[kDVT * TP];              // V^T[v][tau]  (this workgroup's 128 columns)
-    uint16_t St[L * TP];                 // S~[tau][sig]
-    float n[2][kDQK];                    // normaliser, double-buffered across chunks
-    float x2[L];                         // (i~ - b) * log2 e
-    float M2[L];                         // M * log2 e
-    float inter[L];                      // exp(m_prev - M) / sqrt(DQK)
-    float floorv[L];                     // exp(-(b + M))
-    float w[L];                          // key weights exp(x - M_L)
-    float dq[L];                         // Q n_{k-1} (unscaled q)
-    float hinv[L];                       // 1 / max(|den|, floor)
-    float rs[NB][L];                     // row sums of S~ per 16-wide sigma block
-    float scal[4];                       // [0] decay, [1] m_next, [2] gsum (log forget total)
+    using C = Cfg<L>;
+    uint16_t Qs[L * C::QP];        // Q[tau][d]  (current d block)
+    uint16_t Ks[L * C::QP];        // K[tau][d]
+    uint16_t Vs[L * C::VP];        // V[tau][v]  (this workgroup's 128 columns)
+    uint16_t St[L * C::SP];        // S~[tau][sig]
+    uint16_t nb[2][2][kDQK];       // normaliser as bf16 hi / lo rows, double-buffered
+    uint16_t wb[2][L];             // n-update weights as bf16 hi / lo rows
+    float n[2][kDQK];              // fp32 normaliser, double-buffered across chunks
+    float x2[L];                   // (i~ - b) * log2 e
+    float M2[L];                   // M * log2 e
+    float interC[L];               // exp(m_prev - M + s) / sqrt(DQK): scale of C_acc^T Q^T
+    float interN[L];               // exp(m_prev - M) / sqrt(DQK):     scale of Q n
+    float floorv[L];               // exp(-(b + M))
+    float wC[L];                   // C-update weights exp(x - M_L - s_new)
+    float dq[L];                   // Q n_{k-1} (unscaled q)
+    float hinv[L];                 // 1 / max(|den|, floor)
+    float rs[L / 16][L];           // row sums of S~ per 16-wide sigma block
+    float scal[8];                 // [0] n decay, [1] m_next, [2] gsum, [3] s_new, [4] eager C scale
 };
 
 // Per-thread staging registers.
 template <int L>
 struct QKRegs {
-    static constexpr int NQ = (L * kDB / 8) / kThreads;   // 16-byte Q chunks per thread
-    static constexpr int NK = (L / 4) * (kDB / 4) / kThreads;   // 4x4 K blocks per thread
-    u32x4_t q[NQ];
-    u32x2_t k[NK][4];
+    static constexpr int N = (L * Cfg<L>::DB / 8) / kThreads;   // 16-byte pieces per thread per matrix
+    u32x4_t q[N];
+    u32x4_t k[N];
 };
 template <int L>
 struct VRegs {
-    static constexpr int NV = (L / 8) * (kDVT / 4) / kThreads;   // 8x4 V blocks per thread
-    u32x2_t v[NV][8];
+    static constexpr int N = (L * kDVT / 8) / kThreads;
+    u32x4_t v[N];
     float ig, fg, ig2, fg2;   // gates (wave 0; two per lane when L == 128)
 };
 
-// Buffer resources (SGPRs) for one sequence's inputs: loads then need one 32-bit
-// VGPR offset per staging item plus immediate offsets, instead of a 64-bit
-// address per load.  Out-of-range buffer reads return zero.
+// Buffer resources (SGPRs) for one sequence's inputs: loads need one 32-bit VGPR
+// offset per staging item plus immediate offsets.  Out-of-range reads return zero.
 constexpr int kRsrcWord3 = 0x00020000;
 
 struct SeqRsrc {
@@ -141,45 +185,41 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint3
 __device__ __forceinline__ u32x4_t bload128(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
-__device__ __forceinline__ u32x2_t bload64(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-    return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
-}
 __device__ __forceinline__ float bloadf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
 
-// q/k rows are 512 bytes, v rows 1024 bytes; offsets below are in bytes.
+// Q and K rows are 512 bytes, V rows 1024 bytes; offsets are in bytes.
 template <int L, bool FULL>
 __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, int p, int tid) {
-    const uint32_t soff = static_cast<uint32_t>(t0) * (kDQK * 2) + p * (kDB * 2);
-    if constexpr (FULL) {
+    constexpr int DB = Cfg<L>::DB, PR = DB / 8;   // 16-byte pieces per row
+    const uint32_t soff = static_cast<uint32_t>(t0) * (kDQK * 2) + p * (DB * 2);
 #pragma unroll
-        for (int i = 0; i < QKRegs<L>::NQ; ++i) {
-            const int item = tid + i * kThreads;
-            const int tau = item >> 3, c = item & 7;
-            r.q[i] = bload128(R.q, tau * (kDQK * 2) + 16 * c, soff);
-        }
-    }
-#pragma unroll
-    for (int i = 0; i < QKRegs<L>::NK; ++i) {
+    for (int i = 0; i < QKRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
-        const int dg = item & 15, tg = item >> 4;
-        const uint32_t voff = (4 * tg) * (kDQK * 2) + 8 * dg;
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) r.k[i][r4] = bload64(R.k, voff + r4 * (kDQK * 2), soff);
+        const uint32_t voff = (item / PR) * (kDQK * 2) + 16 * (item % PR);
+        if constexpr (FULL) r.q[i] = bload128(R.q, voff, soff);
+        r.k[i] = bload128(R.k, voff, soff);
     }
 }
-
+template <int L, bool FULL>
+__device__ __forceinline__ void store_qk(Smem<L>& S, const QKRegs<L>& r, int tid) {
+    constexpr int PR = Cfg<L>::DB / 8, QP = Cfg<L>::QP;
+#pragma unroll
+    for (int i = 0; i < QKRegs<L>::N; ++i) {
+        const int item = tid + i * kThreads;
+        const int off = (item / PR) * QP + 8 * (item % PR);
+        if constexpr (FULL) *reinterpret_cast<u32x4_t*>(&S.Qs[off]) = r.q[i];
+        *reinterpret_cast<u32x4_t*>(&S.Ks[off]) = r.k[i];
+    }
+}
 template <int L>
 __device__ __forceinline__ void load_v(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int tid) {
     const uint32_t soff = static_cast<uint32_t>(t0) * (kDV * 2) + v0 * 2;
 #pragma unroll
-    for (int i = 0; i < VRegs<L>::NV; ++i) {
+    for (int i = 0; i < VRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
-        const int vg = item & 31, tg = item >> 5;
-        const uint32_t voff = (8 * tg) * (kDV * 2) + 8 * vg;
-#pragma unroll
-        for (int r8 = 0; r8 < 8; ++r8) r.v[i][r8] = bload64(R.v, voff + r8 * (kDV * 2), soff);
+        r.v[i] = bload128(R.v, (item / 16) * (kDV * 2) + 16 * (item % 16), soff);
     }
     if (tid < 64) {
         const uint32_t goff = static_cast<uint32_t>(t0) * 4;
@@ -191,63 +231,12 @@ __device__ __forceinline__ void load_v(VRegs<L>& r, const SeqRsrc& R, int t0, in
         }
     }
 }
-
-template <int L, bool FULL>
-__device__ __forceinline__ void store_qk(Smem<L>& S, const QKRegs<L>& r, int tid) {
-    constexpr int QP = Smem<L>::QP, TP = Smem<L>::TP;
-    if constexpr (FULL) {
-#pragma unroll
-        for (int i = 0; i < QKRegs<L>::NQ; ++i) {
-            const int item = tid + i * kThreads;
-            const int tau = item >> 3, c = item & 7;
-            *reinterpret_cast<u32x4_t*>(&S.Qb[tau * QP + 8 * c]) = r.q[i];
-        }
-    }
-#pragma unroll
-    for (int i = 0; i < QKRegs<L>::NK; ++i) {
-        const int item = tid + i * kThreads;
-        const int dg = item & 15, tg = item >> 4;
-        float wv[4];
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-            *reinterpret_cast<u32x2_t*>(&S.Kb[(4 * tg + r4) * QP + 4 * dg]) = r.k[i][r4];
-            wv[r4] = S.w[4 * tg + r4];
-        }
-        // (w K)^T for d = 4dg..4dg+3, tau = 4tg..4tg+3
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            float kv[4];
-#pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) {
-                const uint32_t word = r.k[i][r4][c >> 1];
-                kv[r4] = ((c & 1) ? hi_f32(word) : lo_f32(word)) * wv[r4];
-            }
-            u32x2_t o;
-            o[0] = pack_bf16x2(kv[0], kv[1]);
-            o[1] = pack_bf16x2(kv[2], kv[3]);
-            *reinterpret_cast<u32x2_t*>(&S.Ktb[(4 * dg + c) * TP + 4 * tg]) = o;
-        }
-    }
-}
-
 template <int L>
 __device__ __forceinline__ void store_v(Smem<L>& S, const VRegs<L>& r, int tid) {
-    constexpr int TP = Smem<L>::TP;
 #pragma unroll
-    for (int i = 0; i < VRegs<L>::NV; ++i) {
+    for (int i = 0; i < VRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
-        const int vg = item & 31, tg = item >> 5;
-        // 8 rows (tau) x 4 columns (v) -> 4 rows of V^T with 8 consecutive tau
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            u32x4_t o;
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const uint32_t a = r.v[i][2 * m][c >> 1], b = r.v[i][2 * m + 1][c >> 1];
-                o[m] = (c & 1) ? hi16(a, b) : lo16(a, b);
-            }
-            *reinterpret_cast<u32x4_t*>(&S.Vt[(4 * vg + c) * TP + 8 * tg]) = o;
-        }
+        *reinterpret_cast<u32x4_t*>(&S.Vs[(item / 16) * Cfg<L>::VP + 8 * (item % 16)]) = r.v[i];
     }
 }
 
@@ -269,9 +258,10 @@ __device__ __forceinline__ float wave_incl_max(float x, int lane) {
     return x;
 }
 
-// Gate phase (wave 0): chunkwise gates, max state and all per-row scales.
+// Gate phase (wave 0): chunkwise gates, max state, the lazy scale, and every per-row
+// scale of the chunk.
 template <int L>
-__device__ __forceinline__ void gate_phase(Smem<L>& S, const VRegs<L>& r, float m_prev, int lane) {
+__device__ __forceinline__ void gate_phase(Smem<L>& S, const VRegs<L>& r, float m_prev, float s_old, int lane) {
     float a = logsigmoid(r.fg);
     float b = wave_incl_sum(a, lane);
     float x = r.ig - b;
@@ -287,27 +277,39 @@ __device__ __forceinline__ void gate_phase(Smem<L>& S, const VRegs<L>& r, float 
     const float pL = (L == 128) ? __shfl(p2, 63, 64) : __shfl(p, 63, 64);
     const float bL = (L == 128) ? __shfl(b2, 63, 64) : __shfl(b, 63, 64);
     const float ML = fmaxf(m_prev, pL);
-    // An empty state (m = -inf, only in the local-state pass) contributes nothing; the guards
-    // keep -inf - -inf out of the exponentials when a chunk also writes nothing (all i~ = -inf).
+    // an empty state (m = -inf, local-state pass only) has nothing to decay
+    const bool empty = (m_prev == -INFINITY);
+    const float dlog = empty ? 0.0f : m_prev - ML;
+    const float s_try = s_old + dlog;
+    const bool eager = s_try < kRenorm;
+    const float s_new = eager ? 0.0f : s_try;
     auto emit = [&](int tau, float bb, float xx, float pp) {
         const float M = fmaxf(m_prev, pp);
         S.x2[tau] = xx * kLog2e;
         S.M2[tau] = M * kLog2e;
-        S.inter[tau] = (M == -INFINITY) ? 0.0f : expf(m_prev - M) * kQScale;
+        S.interC[tau] = (M == -INFINITY) ? 0.0f : expf(m_prev - M + s_old) * kQScale;
+        S.interN[tau] = (M == -INFINITY) ? 0.0f : expf(m_prev - M) * kQScale;
         S.floorv[tau] = expf(-(bb + M));
-        S.w[tau] = (xx == -INFINITY) ? 0.0f : expf(xx - ML);
+        const bool none = (xx == -INFINITY);
+        S.wC[tau] = none ? 0.0f : expf(xx - ML - s_new);
+        const float wn = none ? 0.0f : expf(xx - ML);
+        const uint16_t whi = f32_to_bf16(wn);
+        S.wb[0][tau] = whi;
+        S.wb[1][tau] = f32_to_bf16(wn - bf16_to_f32(whi));
     };
     emit(lane, b, x, p);
     if constexpr (L == 128) emit(64 + lane, b2, x2, p2);
     if (lane == 0) {
-        S.scal[0] = (ML == -INFINITY) ? 0.0f : expf(m_prev - ML);
+        S.scal[0] = (empty || ML == -INFINITY) ? 0.0f : expf(m_prev - ML);
         S.scal[1] = bL + ML;
         S.scal[2] += bL;
+        S.scal[3] = s_new;
+        S.scal[4] = eager ? expf(s_try) : 1.0f;
     }
 }
 
-// XCD-aware block order: the hardware deals consecutive workgroups round-robin
-// to the 8 XCDs; renumber so that consecutive work items (the four dv tiles of a
+// XCD-aware block order: the hardware deals consecutive workgroups round-robin to
+// the 8 XCDs; renumber so that consecutive work items (the four dv tiles of a
 // sequence/segment) run on the same XCD.
 __device__ __forceinline__ int work_index() {
     const int nb = gridDim.x, b = blockIdx.x;
@@ -341,18 +343,27 @@ template <int L, bool FULL>
 __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     Smem<L>& S = *reinterpret_cast<Smem<L>*>(smem_raw);
-    constexpr int QP = Smem<L>::QP, TP = Smem<L>::TP, NB = Smem<L>::NB;
+    using CF = Cfg<L>;
+    constexpr int QP = CF::QP, VP = CF::VP, SP = CF::SP, NB = CF::NB, DB = CF::DB, DT = CF::DT;
     constexpr int NT_S = NB * (NB + 1) / 2;          // causal 16x16 tiles of S^T
     constexpr int MAXT = (NT_S + kWaves - 1) / kWaves;
     constexpr int NTT = L / 32;                       // 32-wide tau tiles
+    constexpr int NKS = L / 16;                       // k steps of 16 along the chunk
+    constexpr int DQT = (L / 16 + kWaves - 1) / kWaves;    // 16-row Q n tiles per wave
+    constexpr int NUT = (DB / 16) / kWaves;                // 16-col n-update tiles per wave per block
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int kg = lane >> 5;   // 32x32 k group
     const int l32 = lane & 31;
-    const int g16 = lane >> 4;  // 16x16 k group
+    const int g16 = lane >> 4;  // 16x16 k group, also the 16-lane group of the transpose read
     const int l16 = lane & 15;
+    // transpose-read lane roles inside a 16-lane group
+    const int tr_row = (l16 >> 2) + 8 * (g16 >> 1);   // + 4r + k base
+    const int tr_col = 4 * (l16 & 3) + 16 * (g16 & 1);  // + m/n base (32x32 operands)
+    const int tr_row16 = (l16 >> 2) + 8 * g16;          // 16x16x32 B operand: k rows
+    const int tr_col16 = 4 * (l16 & 3);                  // 16x16x32 B operand: n columns
 
     const int wi = work_index();
     const int tile = wi % kNTile;
@@ -389,16 +400,26 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         nin = slot + kDQK * kDV;
         m_prev = slot[kDQK * kDV + kDQK + 2];
     }
+    // one 32x32 tile at a time, so at most 16 loaded values wait in VGPRs
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const int d = 32 * dt + 8 * (j >> 2) + 4 * kg + (j & 3);
-            Cacc[dt][j] = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + 32 * wave + l32] : 0.0f;
+            const float x = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + 32 * wave + l32] : 0.0f;
+            asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(Cacc[dt][j]) : "v"(x));
         }
+        __builtin_amdgcn_sched_barrier(0);
     }
-    S.n[0][tid] = nin ? nin[tid] : 0.0f;
+    {
+        const float nv = nin ? nin[tid] : 0.0f;
+        S.n[0][tid] = nv;
+        const uint16_t hi = f32_to_bf16(nv);
+        S.nb[0][0][tid] = hi;
+        S.nb[0][1][tid] = f32_to_bf16(nv - bf16_to_f32(hi));
+    }
     if (tid == 0) S.scal[2] = 0.0f;
+    float s_off = 0.0f;   // C = C_acc * e^{s_off}
 
     VRegs<L> rv;
     QKRegs<L> rqk;
@@ -409,39 +430,54 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 
     f32x16_t Nacc[NTT];
     f32x4_t Sacc[MAXT];
-    float dq_part = 0.0f;
+    f32x4_t dqacc[DQT];
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * L;
-        const int nb_cur = (c - c_begin) & 1;
-        float* n_old = S.n[nb_cur];
-        float* n_new = S.n[nb_cur ^ 1];
-        __syncthreads();   // previous chunk fully consumed (Vt, St, gate vectors)
-        if (wave == 0) gate_phase<L>(S, rv, m_prev, lane);
+        const int cur = (c - c_begin) & 1;
+        __syncthreads();   // the previous chunk's LDS reads are done
+        if (wave == 0) gate_phase<L>(S, rv, m_prev, s_off, lane);
         store_v<L>(S, rv, tid);
-        if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid);
+        store_qk<L, FULL>(S, rqk, tid);
         __syncthreads();
-        const float decay = S.scal[0];
+        if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid);
+        load_qk<L, FULL>(rqk, P, t0, 1, tid);
+        const float decay_n = S.scal[0];
         const float m_next = S.scal[1];
+        const float s_new = S.scal[3];
+        const float c_scale = S.scal[4];   // != 1: apply this chunk's decay to C_acc eagerly
 
         if constexpr (FULL) {
 #pragma unroll
             for (int T = 0; T < NTT; ++T) Nacc[T] = f32x16_t{};
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) Sacc[i] = f32x4_t{};
-            dq_part = 0.0f;
+#pragma unroll
+            for (int i = 0; i < DQT; ++i) dqacc[i] = f32x4_t{};
+        }
+        const float* n_old = S.n[cur];
+        float* n_new = S.n[cur ^ 1];
+
+        // V operands of (iv), read transposed once per chunk and scaled by the C-update key weights
+        u32x4_t Vw[NKS];
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            const uint16_t* vb = &S.Vs[(16 * ks + tr_row) * VP + 32 * wave + tr_col];
+            const u32x4_t raw = cat(tr_read(vb), tr_read(vb + 4 * VP));
+            const float* wv = &S.wC[16 * ks + 8 * kg];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                Vw[ks][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
         }
 
 #pragma unroll
-        for (int p = 0; p < kNDB; ++p) {
-            store_qk<L, FULL>(S, rqk, tid);
-            __syncthreads();
-            if (p + 1 < kNDB) {
-                load_qk<L, FULL>(rqk, P, t0, p + 1, tid);
-            } else if (c + 1 < c_end) {
-                load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
+        for (int p = 0; p < CF::NDB; ++p) {
+            if (p > 0) {
+                __syncthreads();   // block p-1 fully read
+                store_qk<L, FULL>(S, rqk, tid);
+                __syncthreads();
+                if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
             }
-
             if constexpr (FULL) {
                 // (i) S^T += K_p Q_p^T on this wave's causal tiles
 #pragma unroll
@@ -451,97 +487,99 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                         int tb = 0, rem = t;
                         while (rem > tb) { rem -= tb + 1; ++tb; }
                         const int sb = rem;
+                        const uint16_t* ka = &S.Ks[(16 * sb + l16) * QP + 8 * g16];
+                        const uint16_t* qb = &S.Qs[(16 * tb + l16) * QP + 8 * g16];
 #pragma unroll
-                        for (int ks = 0; ks < kDB / 32; ++ks) {
-                            const u32x4_t a = *reinterpret_cast<const u32x4_t*>(&S.Kb[(16 * sb + l16) * QP + 32 * ks + 8 * g16]);
-                            const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&S.Qb[(16 * tb + l16) * QP + 32 * ks + 8 * g16]);
-                            Sacc[i] = mfma16(a, b, Sacc[i]);
+                        for (int ks = 0; ks < DB / 32; ++ks)
+                            Sacc[i] = mfma16(*reinterpret_cast<const u32x4_t*>(ka + 32 * ks),
+                                             *reinterpret_cast<const u32x4_t*>(qb + 32 * ks), Sacc[i]);
+                    }
+                }
+                // Q n_{k-1} over this d block: A = Q rows, B = n as bf16 hi / lo columns
+#pragma unroll
+                for (int i = 0; i < DQT; ++i) {
+                    const int tt = wave + kWaves * i;
+                    if (tt < L / 16) {
+                        const uint16_t* qa = &S.Qs[(16 * tt + l16) * QP + 8 * g16];
+                        const uint16_t* nbp = &S.nb[cur][l16 & 1][p * DB + 8 * g16];
+#pragma unroll
+                        for (int ks = 0; ks < DB / 32; ++ks) {
+                            const u32x4_t nbv = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(nbp + 32 * ks)
+                                                          : u32x4_t{0u, 0u, 0u, 0u};
+                            dqacc[i] = mfma16(*reinterpret_cast<const u32x4_t*>(qa + 32 * ks), nbv, dqacc[i]);
                         }
                     }
                 }
                 // (iii) N^T += C_p^T Q_p^T, A operand straight from the C accumulators
 #pragma unroll
-                for (int st = 0; st < 4; ++st) {
-                    const f32x16_t& cc = Cacc[2 * p + (st >> 1)];
-                    const int hh = st & 1;
-                    u32x4_t a;
-                    a[0] = pack_bf16x2(cc[8 * hh + 0], cc[8 * hh + 1]);
-                    a[1] = pack_bf16x2(cc[8 * hh + 2], cc[8 * hh + 3]);
-                    a[2] = pack_bf16x2(cc[8 * hh + 4], cc[8 * hh + 5]);
-                    a[3] = pack_bf16x2(cc[8 * hh + 6], cc[8 * hh + 7]);
-                    const int dl = 32 * (st >> 1) + 16 * hh + 4 * kg;
+                for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
-                    for (int T = 0; T < NTT; ++T) {
-                        const uint16_t* qrow = &S.Qb[(32 * T + l32) * QP + dl];
-                        u32x4_t b;
-                        const u32x2_t b0 = *reinterpret_cast<const u32x2_t*>(qrow);
-                        const u32x2_t b1 = *reinterpret_cast<const u32x2_t*>(qrow + 8);
-                        b[0] = b0[0]; b[1] = b0[1]; b[2] = b1[0]; b[3] = b1[1];
-                        Nacc[T] = mfma32(a, b, Nacc[T]);
-                    }
-                }
-                // Q n_{k-1} partial over this d block (fp32 VALU)
-                {
-                    constexpr int TPR = kThreads / L;           // threads per row: 4 (L=64) or 2 (L=128)
-                    constexpr int DPT = kDB / TPR;               // d per thread: 16 or 32
-                    const int tau = tid / TPR, part = tid % TPR;
-                    const uint16_t* qrow = &S.Qb[tau * QP + part * DPT];
-                    const float* nrow = &n_old[p * kDB + part * DPT];
+                    for (int hh = 0; hh < 2; ++hh) {
+                        const f32x16_t& cc = Cacc[p * DT + dt];
+                        u32x4_t a;
+                        a[0] = pack_bf16x2(acc_read(cc[8 * hh + 0]), acc_read(cc[8 * hh + 1]));
+                        a[1] = pack_bf16x2(acc_read(cc[8 * hh + 2]), acc_read(cc[8 * hh + 3]));
+                        a[2] = pack_bf16x2(acc_read(cc[8 * hh + 4]), acc_read(cc[8 * hh + 5]));
+                        a[3] = pack_bf16x2(acc_read(cc[8 * hh + 6]), acc_read(cc[8 * hh + 7]));
+                        const int dl = 32 * dt + 16 * hh + 4 * kg;
 #pragma unroll
-                    for (int e = 0; e < DPT; e += 8) {
-                        const u32x4_t qq = *reinterpret_cast<const u32x4_t*>(qrow + e);
-#pragma unroll
-                        for (int u = 0; u < 4; ++u)
-                            dq_part += lo_f32(qq[u]) * nrow[e + 2 * u] + hi_f32(qq[u]) * nrow[e + 2 * u + 1];
+                        for (int T = 0; T < NTT; ++T) {
+                            const uint16_t* qrow = &S.Qs[(32 * T + l32) * QP + dl];
+                            const u32x2_t b0 = *reinterpret_cast<const u32x2_t*>(qrow);
+                            const u32x2_t b1 = *reinterpret_cast<const u32x2_t*>(qrow + 8);
+                            Nacc[T] = mfma32(a, cat(b0, b1), Nacc[T]);
+                        }
                     }
                 }
             }
 
-            // (iv) C_p = decay C_p + (w K)_p^T V
+            // (iv) C_p += K_p^T (w e^{-s} V): A = K read transposed, B = the scaled V operands
+            if (c_scale != 1.0f) {
 #pragma unroll
-            for (int dt = 0; dt < 2; ++dt) Cacc[2 * p + dt] *= decay;
+                for (int dt = 0; dt < DT; ++dt) scale_acc(Cacc[p * DT + dt], c_scale);
+            }
 #pragma unroll
-            for (int ks = 0; ks < L / 16; ++ks) {
-                const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&S.Vt[(32 * wave + l32) * TP + 16 * ks + 8 * kg]);
+            for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
-                for (int dt = 0; dt < 2; ++dt) {
-                    const u32x4_t a = *reinterpret_cast<const u32x4_t*>(&S.Ktb[(32 * dt + l32) * TP + 16 * ks + 8 * kg]);
-                    Cacc[2 * p + dt] = mfma32(a, b, Cacc[2 * p + dt]);
+                for (int dt = 0; dt < DT; ++dt) {
+                    const uint16_t* kb = &S.Ks[(16 * ks + tr_row) * QP + 32 * dt + tr_col];
+                    Cacc[p * DT + dt] = mfma32(cat(tr_read(kb), tr_read(kb + 4 * QP)), Vw[ks], Cacc[p * DT + dt]);
                 }
             }
-            // n_p = decay n_p + K_p^T w  (fp32: exact bf16 K times fp32 w)
-            {
-                const int tp = tid & 7, dp = tid >> 3;   // 8 tau parts x 32 d pairs
-                float s0 = 0.f, s1 = 0.f;
+            // n_p = decay n_p + K_p^T w: A = w as bf16 hi / lo rows, B = K read transposed
 #pragma unroll
-                for (int e = 0; e < L / 8; ++e) {
-                    const int tau = tp * (L / 8) + e;
-                    const uint32_t kk = *reinterpret_cast<const uint32_t*>(&S.Kb[tau * QP + 2 * dp]);
-                    const float wt = S.w[tau];
-                    s0 += wt * lo_f32(kk);
-                    s1 += wt * hi_f32(kk);
-                }
+            for (int j = 0; j < NUT; ++j) {
+                const int ut = wave * NUT + j;   // 16-column tile of this d block
+                f32x4_t nacc = f32x4_t{};
 #pragma unroll
-                for (int o = 1; o < 8; o <<= 1) {
-                    s0 += __shfl_xor(s0, o, 64);
-                    s1 += __shfl_xor(s1, o, 64);
+                for (int ks = 0; ks < L / 32; ++ks) {
+                    const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&S.wb[l16 & 1][32 * ks + 8 * g16])
+                                                 : u32x4_t{0u, 0u, 0u, 0u};
+                    const uint16_t* kb = &S.Ks[(32 * ks + tr_row16) * QP + 16 * ut + tr_col16];
+                    nacc = mfma16(wa, cat(tr_read(kb), tr_read(kb + 4 * QP)), nacc);
                 }
-                if (tp == 0) {
-                    const int d = p * kDB + 2 * dp;
-                    n_new[d] = decay * n_old[d] + s0;
-                    n_new[d + 1] = decay * n_old[d + 1] + s1;
+                // rows 0 and 1 (hi and lo weights) of column l16 sit in lanes 0..15
+                if (g16 == 0) {
+                    const int d = p * DB + 16 * ut + l16;
+                    const float nv = decay_n * n_old[d] + nacc[0] + nacc[1];
+                    n_new[d] = nv;
+                    const uint16_t hi = f32_to_bf16(nv);
+                    S.nb[cur ^ 1][0][d] = hi;
+                    S.nb[cur ^ 1][1][d] = f32_to_bf16(nv - bf16_to_f32(hi));
                 }
             }
-            __syncthreads();
         }
 
         if constexpr (FULL) {
-            // finish Q n
-            {
-                constexpr int TPR = kThreads / L;
+            // finish Q n: columns 0 and 1 of the 16x16 tile are lanes l16 = 0 and 1
 #pragma unroll
-                for (int o = 1; o < TPR; o <<= 1) dq_part += __shfl_xor(dq_part, o, 64);
-                if ((tid % TPR) == 0) S.dq[tid / TPR] = dq_part;
+            for (int i = 0; i < DQT; ++i) {
+                const int tt = wave + kWaves * i;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float other = __shfl_down(dqacc[i][j], 1, 64);
+                    if (tt < L / 16 && l16 == 0) S.dq[16 * tt + 4 * g16 + j] = dqacc[i][j] + other;
+                }
             }
             // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums
 #pragma unroll
@@ -566,7 +604,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     u32x2_t o;
                     o[0] = pack_bf16x2(vals[0], vals[1]);
                     o[1] = pack_bf16x2(vals[2], vals[3]);
-                    *reinterpret_cast<u32x2_t*>(&S.St[tau * TP + 16 * sb + 4 * g16]) = o;
+                    *reinterpret_cast<u32x2_t*>(&S.St[tau * SP + 16 * sb + 4 * g16]) = o;
                     rsum += __shfl_xor(rsum, 16, 64);
                     rsum += __shfl_xor(rsum, 32, 64);
                     if (g16 == 0) S.rs[sb][tau] = rsum;
@@ -575,27 +613,27 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             // zero the masked 16x16 tiles inside each diagonal 32x32 block
             for (int T = wave; T < NTT; T += kWaves) {
                 const int tau = 32 * T + l16;
-                *reinterpret_cast<u32x2_t*>(&S.St[tau * TP + 32 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
+                *reinterpret_cast<u32x2_t*>(&S.St[tau * SP + 32 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
             }
             __syncthreads();
             // denominators
             if (tid < L) {
                 const int tau = tid;
-                float den = S.inter[tau] * S.dq[tau];
+                float den = S.interN[tau] * S.dq[tau];
                 for (int sb = 0; sb <= tau / 16; ++sb) den += S.rs[sb][tau];
                 S.hinv[tau] = 1.0f / fmaxf(fabsf(den), S.floorv[tau]);
             }
             __syncthreads();
-            // (ii) N^T = inter * N^T + V^T S~^T, then h
+            // (ii) N^T = interC * N^T + V^T S~^T, then h
 #pragma unroll
             for (int T = 0; T < NTT; ++T) {
                 const int tau = 32 * T + l32;
-                Nacc[T] *= S.inter[tau];
+                scale_acc(Nacc[T], S.interC[tau]);
 #pragma unroll
                 for (int ks = 0; ks < 2 * T + 2; ++ks) {
-                    const u32x4_t a = *reinterpret_cast<const u32x4_t*>(&S.Vt[(32 * wave + l32) * TP + 16 * ks + 8 * kg]);
-                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&S.St[tau * TP + 16 * ks + 8 * kg]);
-                    Nacc[T] = mfma32(a, b, Nacc[T]);
+                    const uint16_t* vb = &S.Vs[(16 * ks + tr_row) * VP + 32 * wave + tr_col];
+                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&S.St[tau * SP + 16 * ks + 8 * kg]);
+                    Nacc[T] = mfma32(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, Nacc[T]);
                 }
                 const float hv = S.hinv[tau];
                 uint16_t* hrow = A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + 32 * wave + 4 * kg;
@@ -608,6 +646,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 }
             }
         }
+        s_off = s_new;
         m_prev = m_next;
     }
     __syncthreads();
@@ -617,7 +656,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     float* Cout;
     float* nout;
     float* mout;
-    bool write_nm = (tile == 0);
+    const bool write_nm = (tile == 0);
     if (FULL) {
         if (g != A.G - 1) return;
         Cout = A.CT + static_cast<int64_t>(s) * kDQK * kDV;
@@ -630,12 +669,13 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         mout = nout + kDQK;   // m_loc, then gsum
         if (write_nm && tid == 0) mout[1] = S.scal[2];
     }
+    const float esc = expf(s_off);
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const int d = 32 * dt + 8 * (j >> 2) + 4 * kg + (j & 3);
-            Cout[static_cast<int64_t>(d) * kDV + v0 + 32 * wave + l32] = Cacc[dt][j];
+            Cout[static_cast<int64_t>(d) * kDV + v0 + 32 * wave + l32] = acc_read(Cacc[dt][j]) * esc;
         }
     }
     if (write_nm) {
@@ -682,14 +722,9 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
     }
 }
 
-template <int L>
-size_t smem_bytes() {
-    return sizeof(Smem<L>);
-}
-
 template <int L, bool FULL>
 hipError_t launch_variant(const ChunkKernelArgs& a, int S, hipStream_t stream) {
-    const size_t lds = smem_bytes<L>();
+    const size_t lds = sizeof(Smem<L>);
     auto kern = chunk_mfma_kernel<L, FULL>;
     static bool attr_set = false;
     if (!attr_set) {

@@ -23,15 +23,15 @@
 // between the read-out (iii) and the update (iv)) and s returns to 0.  The
 // inter-chunk term uses exp(m_prev - M_tau + s); the exit state is C_acc e^{s}.
 //
-// Products and their MFMA mapping (gfx950 bf16 MFMA, fp32 accumulate):
-//   (i)   S^T = K Q^T             16x16x32: A = K rows, B = Q rows (both d-contiguous)
-//   (ii)  N^T += V^T S~^T         32x32x16: A = V read transposed, B = S~ rows
-//   (iii) N^T += C^T Q^T          32x32x16: A = the C accumulators of (iv), converted to
-//                                 bf16 in registers, B = Q rows
-//   (iv)  C += K^T (w e^{-s} V)   32x32x16: A = K read transposed, B = V read transposed
-//                                 and scaled by the key weights in registers
-//   Q n and K^T w                 16x16x32 with the fp32 normaliser and weights split into
-//                                 bf16 hi + lo rows (relative error ~2^-17)
+// Products and their MFMA mapping (gfx950 bf16 16x16x32 MFMA, fp32 accumulate):
+//   (i)   S^T = K Q^T             A = K rows, B = Q rows (both d-contiguous)
+//   (ii)  N^T += V^T S~^T         A = V read transposed, B = S~ rows
+//   (iii) N^T += C^T Q^T          A = the C accumulators of (iv), converted to bf16 in
+//                                 registers, B = Q rows
+//   (iv)  C += K^T (w e^{-s} V)   A = K read transposed, B = V read transposed and scaled
+//                                 by the key weights in registers
+//   Q n and K^T w                 the fp32 normaliser and weights split into bf16 hi + lo
+//                                 rows (relative error ~2^-17)
 // "Read transposed" is the LDS transpose read of gfx950 (ds_read_b64_tr_b16): in each
 // 16-lane group, lane 4s+q supplies 4 consecutive elements of row s of a 4 x 16 tile and
 // lane c receives column c, so a row-major [k][m] tile arrives k-contiguous, as an MFMA
@@ -40,14 +40,16 @@
 // permuted consistently in both operands.  Outputs come out transposed (rows v,
 // columns tau), so each lane stores runs of four consecutive v of one h row.
 //
-// Work decomposition.  One workgroup of 4 waves owns one (sequence, 128-column
-// dv tile, segment) and walks the segment's chunks in order.  Wave w owns the
-// 256 x 32 slice C[:, 32w:32w+32] in its accumulators for the whole segment.
-// Q and K are staged in two 128-wide d halves; the next half (and the next
-// chunk's V and gates) is prefetched into registers while the current half is
-// multiplied.  The four dv
-// tiles of a (sequence, segment) are dispatched consecutively onto one XCD so
-// their shared Q/K reads hit one L2.
+// Work decomposition.  One workgroup of 8 waves (two per SIMD, so one wave's
+// LDS and memory waits are covered by the other's MFMAs) owns one (sequence,
+// 128-column dv tile, segment) and walks the segment's chunks in order.  Wave w
+// owns the 256 x 16 slice C[:, 16w:16w+16] in its accumulators (64 registers) for
+// the whole segment; S~, Q n and the gates are computed once per workgroup.
+// Q and K are staged in d blocks (two of 128 for L = 64, four of 64 for L = 128);
+// the next block (and the next chunk's V and gates) is prefetched into registers
+// while the current block is multiplied.  The four dv tiles of a (sequence,
+// segment) are dispatched consecutively onto one XCD so their shared Q/K reads
+// hit one L2.
 //
 // Segment-parallel schedule (optional workspace).  With G segments per
 // sequence: (1) the LOCAL variant computes each of the first G-1 segments' state
@@ -65,8 +67,10 @@ constexpr int kDQK = 256;
 constexpr int kDV = 512;
 constexpr int kDVT = 128;             // dv columns per workgroup
 constexpr int kNTile = kDV / kDVT;    // 4 dv tiles per sequence
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
+constexpr int kThreads = 512;
+constexpr int kWaves = 8;
+constexpr int kVW = kDVT / kWaves;    // 16 dv columns of C per wave
+constexpr int kGateWave = kWaves - 1; // the wave with the least MFMA work runs the gate scans
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kQScale = 0.0625f;    // 1 / sqrt(256), exact
 constexpr float kRenorm = -20.0f;     // rescale C eagerly when its lazy log-scale would drop below this
@@ -116,6 +120,18 @@ __device__ __forceinline__ void scale_acc(f32x16_t& acc, float s) {
     }
 }
 
+__device__ __forceinline__ void scale_acc4(f32x4_t& acc, float s) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        float x = acc[j];
+        float t;
+        asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
+                     : "+a"(x), "=&v"(t)
+                     : "v"(s));
+        acc[j] = x;
+    }
+}
+
 // LDS transpose read: 4 bf16 per lane (see the header comment for the lane mapping).
 __device__ __forceinline__ u32x2_t tr_read(const uint16_t* p) {
     typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
@@ -125,9 +141,9 @@ __device__ __forceinline__ u32x4_t cat(u32x2_t a, u32x2_t b) { return u32x4_t{a[
 
 template <int L>
 struct Cfg {
-    static constexpr int NDB = 2;                   // d blocks staged per chunk
-    static constexpr int DB = kDQK / NDB;           // 256 or 128
-    static constexpr int DT = DB / 32;              // 32-row C tiles per d block
+    static constexpr int NDB = (L == 128) ? 4 : 2;  // d blocks staged per chunk
+    static constexpr int DB = kDQK / NDB;           // 128 or 64
+    static constexpr int DT = DB / 16;              // 16-row C tiles per d block
     static constexpr int QP = DB + 8;               // row pitch (elements) of Q and K blocks
     static constexpr int VP = kDVT + 8;             // row pitch of V
     static constexpr int SP = L + 8;                // row pitch of S~
@@ -221,13 +237,14 @@ __device__ __forceinline__ void load_v(VRegs<L>& r, const SeqRsrc& R, int t0, in
         const int item = tid + i * kThreads;
         r.v[i] = bload128(R.v, (item / 16) * (kDV * 2) + 16 * (item % 16), soff);
     }
-    if (tid < 64) {
+    if ((tid >> 6) == kGateWave) {
         const uint32_t goff = static_cast<uint32_t>(t0) * 4;
-        r.ig = bloadf(R.ig, 4 * tid, goff);
-        r.fg = bloadf(R.fg, 4 * tid, goff);
+        const int lane = tid & 63;
+        r.ig = bloadf(R.ig, 4 * lane, goff);
+        r.fg = bloadf(R.fg, 4 * lane, goff);
         if constexpr (L == 128) {
-            r.ig2 = bloadf(R.ig, 4 * tid + 256, goff);
-            r.fg2 = bloadf(R.fg, 4 * tid + 256, goff);
+            r.ig2 = bloadf(R.ig, 4 * lane + 256, goff);
+            r.fg2 = bloadf(R.fg, 4 * lane + 256, goff);
         }
     }
 }
@@ -258,11 +275,17 @@ __device__ __forceinline__ float wave_incl_max(float x, int lane) {
     return x;
 }
 
-// Gate phase (wave 0): chunkwise gates, max state, the lazy scale, and every per-row
+// exp and log sigmoid through the hardware exp2 / log2 (v_exp_f32, v_log_f32).
+__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
+__device__ __forceinline__ float flogsig(float x) {
+    return fminf(x, 0.0f) - 0.6931471805599453f * __builtin_amdgcn_logf(1.0f + fexp(-fabsf(x)));
+}
+
+// Gate phase (one wave): chunkwise gates, max state, the lazy scale, and every per-row
 // scale of the chunk.
 template <int L>
 __device__ __forceinline__ void gate_phase(Smem<L>& S, const VRegs<L>& r, float m_prev, float s_old, int lane) {
-    float a = logsigmoid(r.fg);
+    float a = flogsig(r.fg);
     float b = wave_incl_sum(a, lane);
     float x = r.ig - b;
     float p = wave_incl_max(x, lane);
@@ -270,7 +293,7 @@ __device__ __forceinline__ void gate_phase(Smem<L>& S, const VRegs<L>& r, float 
     if constexpr (L == 128) {
         const float btot = __shfl(b, 63, 64);
         const float ptot = __shfl(p, 63, 64);
-        b2 = btot + wave_incl_sum(logsigmoid(r.fg2), lane);
+        b2 = btot + wave_incl_sum(flogsig(r.fg2), lane);
         x2 = r.ig2 - b2;
         p2 = fmaxf(ptot, wave_incl_max(x2, lane));
     }
@@ -287,12 +310,12 @@ __device__ __forceinline__ void gate_phase(Smem<L>& S, const VRegs<L>& r, float 
         const float M = fmaxf(m_prev, pp);
         S.x2[tau] = xx * kLog2e;
         S.M2[tau] = M * kLog2e;
-        S.interC[tau] = (M == -INFINITY) ? 0.0f : expf(m_prev - M + s_old) * kQScale;
-        S.interN[tau] = (M == -INFINITY) ? 0.0f : expf(m_prev - M) * kQScale;
-        S.floorv[tau] = expf(-(bb + M));
+        S.interC[tau] = (M == -INFINITY) ? 0.0f : fexp(m_prev - M + s_old) * kQScale;
+        S.interN[tau] = (M == -INFINITY) ? 0.0f : fexp(m_prev - M) * kQScale;
+        S.floorv[tau] = fexp(-(bb + M));
         const bool none = (xx == -INFINITY);
-        S.wC[tau] = none ? 0.0f : expf(xx - ML - s_new);
-        const float wn = none ? 0.0f : expf(xx - ML);
+        S.wC[tau] = none ? 0.0f : fexp(xx - ML - s_new);
+        const float wn = none ? 0.0f : fexp(xx - ML);
         const uint16_t whi = f32_to_bf16(wn);
         S.wb[0][tau] = whi;
         S.wb[1][tau] = f32_to_bf16(wn - bf16_to_f32(whi));
@@ -300,11 +323,11 @@ __device__ __forceinline__ void gate_phase(Smem<L>& S, const VRegs<L>& r, float 
     emit(lane, b, x, p);
     if constexpr (L == 128) emit(64 + lane, b2, x2, p2);
     if (lane == 0) {
-        S.scal[0] = (empty || ML == -INFINITY) ? 0.0f : expf(m_prev - ML);
+        S.scal[0] = (empty || ML == -INFINITY) ? 0.0f : fexp(m_prev - ML);
         S.scal[1] = bL + ML;
         S.scal[2] += bL;
         S.scal[3] = s_new;
-        S.scal[4] = eager ? expf(s_try) : 1.0f;
+        S.scal[4] = eager ? fexp(s_try) : 1.0f;
     }
 }
 
@@ -347,23 +370,20 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     constexpr int QP = CF::QP, VP = CF::VP, SP = CF::SP, NB = CF::NB, DB = CF::DB, DT = CF::DT;
     constexpr int NT_S = NB * (NB + 1) / 2;          // causal 16x16 tiles of S^T
     constexpr int MAXT = (NT_S + kWaves - 1) / kWaves;
-    constexpr int NTT = L / 32;                       // 32-wide tau tiles
-    constexpr int NKS = L / 16;                       // k steps of 16 along the chunk
-    constexpr int DQT = (L / 16 + kWaves - 1) / kWaves;    // 16-row Q n tiles per wave
-    constexpr int NUT = (DB / 16) / kWaves;                // 16-col n-update tiles per wave per block
+    constexpr int NTT = L / 16;                       // 16-wide tau tiles
+    constexpr int NKS = L / 32;                       // k steps of 32 along the chunk
+    constexpr int NCT = kDQK / 16;                    // 16-row tiles of this wave's C slice
+    constexpr int NUT = (DB / 16 + kWaves - 1) / kWaves;           // 16-col n-update tiles per wave per block
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int kg = lane >> 5;   // 32x32 k group
-    const int l32 = lane & 31;
-    const int g16 = lane >> 4;  // 16x16 k group, also the 16-lane group of the transpose read
+    const int g16 = lane >> 4;  // k group of the 16x16x32 operands, also the transpose-read group
     const int l16 = lane & 15;
-    // transpose-read lane roles inside a 16-lane group
-    const int tr_row = (l16 >> 2) + 8 * (g16 >> 1);   // + 4r + k base
-    const int tr_col = 4 * (l16 & 3) + 16 * (g16 & 1);  // + m/n base (32x32 operands)
-    const int tr_row16 = (l16 >> 2) + 8 * g16;          // 16x16x32 B operand: k rows
-    const int tr_col16 = 4 * (l16 & 3);                  // 16x16x32 B operand: n columns
+    // transpose-read lane roles inside a 16-lane group (16x16x32 operands)
+    const int tr_row = (l16 >> 2) + 8 * g16;   // + 4r + k base
+    const int tr_col = 4 * (l16 & 3);           // + m/n base
+    const int vc = kVW * wave;                  // this wave's first column of the dv tile
 
     const int wi = work_index();
     const int tile = wi % kNTile;
@@ -384,7 +404,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
 
     // ---- entry state ------------------------------------------------------------------------
-    f32x16_t Cacc[8];
+    // Cacc[t] lane holds C[16 t + 4 g16 + j][vc + l16], j = 0..3
+    f32x4_t Cacc[NCT];
     const float* Cin = nullptr;
     const float* nin = nullptr;
     float m_prev;
@@ -400,18 +421,17 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         nin = slot + kDQK * kDV;
         m_prev = slot[kDQK * kDV + kDQK + 2];
     }
-    // one 32x32 tile at a time, so at most 16 loaded values wait in VGPRs
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
+    for (int t = 0; t < NCT; ++t) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const int d = 32 * dt + 8 * (j >> 2) + 4 * kg + (j & 3);
-            const float x = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + 32 * wave + l32] : 0.0f;
-            asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(Cacc[dt][j]) : "v"(x));
+        for (int j = 0; j < 4; ++j) {
+            const int d = 16 * t + 4 * g16 + j;
+            const float x = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + vc + l16] : 0.0f;
+            asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(Cacc[t][j]) : "v"(x));
         }
-        __builtin_amdgcn_sched_barrier(0);
+        if ((t & 3) == 3) __builtin_amdgcn_sched_barrier(0);
     }
-    {
+    if (tid < kDQK) {
         const float nv = nin ? nin[tid] : 0.0f;
         S.n[0][tid] = nv;
         const uint16_t hi = f32_to_bf16(nv);
@@ -428,15 +448,15 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         load_qk<L, FULL>(rqk, P, c_begin * L, 0, tid);
     }
 
-    f32x16_t Nacc[NTT];
+    f32x4_t Nacc[NTT];
     f32x4_t Sacc[MAXT];
-    f32x4_t dqacc[DQT];
+    f32x4_t dqacc;
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * L;
         const int cur = (c - c_begin) & 1;
         __syncthreads();   // the previous chunk's LDS reads are done
-        if (wave == 0) gate_phase<L>(S, rv, m_prev, s_off, lane);
+        if (wave == kGateWave) gate_phase<L>(S, rv, m_prev, s_off, lane);
         store_v<L>(S, rv, tid);
         store_qk<L, FULL>(S, rqk, tid);
         __syncthreads();
@@ -446,28 +466,28 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         const float m_next = S.scal[1];
         const float s_new = S.scal[3];
         const float c_scale = S.scal[4];   // != 1: apply this chunk's decay to C_acc eagerly
-
-        if constexpr (FULL) {
-#pragma unroll
-            for (int T = 0; T < NTT; ++T) Nacc[T] = f32x16_t{};
-#pragma unroll
-            for (int i = 0; i < MAXT; ++i) Sacc[i] = f32x4_t{};
-#pragma unroll
-            for (int i = 0; i < DQT; ++i) dqacc[i] = f32x4_t{};
-        }
         const float* n_old = S.n[cur];
         float* n_new = S.n[cur ^ 1];
 
-        // V operands of (iv), read transposed once per chunk and scaled by the C-update key weights
+        // B operands of (iv): V read transposed once per chunk and scaled by the C-update key
+        // weights; lane (n = column vc + l16, k group g16) holds tau = 32 ks + 8 g16 + 0..7
         u32x4_t Vw[NKS];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
-            const uint16_t* vb = &S.Vs[(16 * ks + tr_row) * VP + 32 * wave + tr_col];
+            const uint16_t* vb = &S.Vs[(32 * ks + tr_row) * VP + vc + tr_col];
             const u32x4_t raw = cat(tr_read(vb), tr_read(vb + 4 * VP));
-            const float* wv = &S.wC[16 * ks + 8 * kg];
+            const float* wv = &S.wC[32 * ks + 8 * g16];
 #pragma unroll
             for (int u = 0; u < 4; ++u)
                 Vw[ks][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
+        }
+
+        if constexpr (FULL) {
+#pragma unroll
+            for (int T = 0; T < NTT; ++T) Nacc[T] = f32x4_t{};
+#pragma unroll
+            for (int i = 0; i < MAXT; ++i) Sacc[i] = f32x4_t{};
+            dqacc = f32x4_t{};
         }
 
 #pragma unroll
@@ -476,14 +496,15 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 __syncthreads();   // block p-1 fully read
                 store_qk<L, FULL>(S, rqk, tid);
                 __syncthreads();
-                if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
+                if (p + 1 < CF::NDB) load_qk<L, FULL>(rqk, P, t0, p + 1, tid);
+                else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
             }
             if constexpr (FULL) {
                 // (i) S^T += K_p Q_p^T on this wave's causal tiles
 #pragma unroll
                 for (int i = 0; i < MAXT; ++i) {
-                    const int t = wave + kWaves * i;
-                    if (t < NT_S) {
+                    const int t = (L == 128) ? min(wave + kWaves * i, NT_S - 1) : wave + kWaves * i;
+                    if (L == 128 || t < NT_S) {
                         int tb = 0, rem = t;
                         while (rem > tb) { rem -= tb + 1; ++tb; }
                         const int sb = rem;
@@ -496,39 +517,34 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     }
                 }
                 // Q n_{k-1} over this d block: A = Q rows, B = n as bf16 hi / lo columns
+                if (wave < NTT) {
+                    const uint16_t* qa = &S.Qs[(16 * wave + l16) * QP + 8 * g16];
+                    const uint16_t* nbp = &S.nb[cur][l16 & 1][p * DB + 8 * g16];
 #pragma unroll
-                for (int i = 0; i < DQT; ++i) {
-                    const int tt = wave + kWaves * i;
-                    if (tt < L / 16) {
-                        const uint16_t* qa = &S.Qs[(16 * tt + l16) * QP + 8 * g16];
-                        const uint16_t* nbp = &S.nb[cur][l16 & 1][p * DB + 8 * g16];
-#pragma unroll
-                        for (int ks = 0; ks < DB / 32; ++ks) {
-                            const u32x4_t nbv = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(nbp + 32 * ks)
-                                                          : u32x4_t{0u, 0u, 0u, 0u};
-                            dqacc[i] = mfma16(*reinterpret_cast<const u32x4_t*>(qa + 32 * ks), nbv, dqacc[i]);
-                        }
+                    for (int ks = 0; ks < DB / 32; ++ks) {
+                        const u32x4_t nbv = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(nbp + 32 * ks)
+                                                      : u32x4_t{0u, 0u, 0u, 0u};
+                        dqacc = mfma16(*reinterpret_cast<const u32x4_t*>(qa + 32 * ks), nbv, dqacc);
                     }
                 }
-                // (iii) N^T += C_p^T Q_p^T, A operand straight from the C accumulators
+                // (iii) N^T += C_p^T Q_p^T: A from two C tiles (rows 4 g16 + j of each), converted
+                // to bf16 in registers; B = Q rows with the same d permutation
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
+                for (int pt = 0; pt < DT / 2; ++pt) {
+                    const f32x4_t& c0 = Cacc[p * DT + 2 * pt];
+                    const f32x4_t& c1 = Cacc[p * DT + 2 * pt + 1];
+                    u32x4_t a;
+                    a[0] = pack_bf16x2(acc_read(c0[0]), acc_read(c0[1]));
+                    a[1] = pack_bf16x2(acc_read(c0[2]), acc_read(c0[3]));
+                    a[2] = pack_bf16x2(acc_read(c1[0]), acc_read(c1[1]));
+                    a[3] = pack_bf16x2(acc_read(c1[2]), acc_read(c1[3]));
+                    const int dl = 32 * pt + 4 * g16;
 #pragma unroll
-                    for (int hh = 0; hh < 2; ++hh) {
-                        const f32x16_t& cc = Cacc[p * DT + dt];
-                        u32x4_t a;
-                        a[0] = pack_bf16x2(acc_read(cc[8 * hh + 0]), acc_read(cc[8 * hh + 1]));
-                        a[1] = pack_bf16x2(acc_read(cc[8 * hh + 2]), acc_read(cc[8 * hh + 3]));
-                        a[2] = pack_bf16x2(acc_read(cc[8 * hh + 4]), acc_read(cc[8 * hh + 5]));
-                        a[3] = pack_bf16x2(acc_read(cc[8 * hh + 6]), acc_read(cc[8 * hh + 7]));
-                        const int dl = 32 * dt + 16 * hh + 4 * kg;
-#pragma unroll
-                        for (int T = 0; T < NTT; ++T) {
-                            const uint16_t* qrow = &S.Qs[(32 * T + l32) * QP + dl];
-                            const u32x2_t b0 = *reinterpret_cast<const u32x2_t*>(qrow);
-                            const u32x2_t b1 = *reinterpret_cast<const u32x2_t*>(qrow + 8);
-                            Nacc[T] = mfma32(a, cat(b0, b1), Nacc[T]);
-                        }
+                    for (int T = 0; T < NTT; ++T) {
+                        const uint16_t* qrow = &S.Qs[(16 * T + l16) * QP + dl];
+                        const u32x2_t b0 = *reinterpret_cast<const u32x2_t*>(qrow);
+                        const u32x2_t b1 = *reinterpret_cast<const u32x2_t*>(qrow + 16);
+                        Nacc[T] = mfma16(a, cat(b0, b1), Nacc[T]);
                     }
                 }
             }
@@ -536,26 +552,27 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             // (iv) C_p += K_p^T (w e^{-s} V): A = K read transposed, B = the scaled V operands
             if (c_scale != 1.0f) {
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) scale_acc(Cacc[p * DT + dt], c_scale);
+                for (int dt = 0; dt < DT; ++dt) scale_acc4(Cacc[p * DT + dt], c_scale);
             }
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) {
-                    const uint16_t* kb = &S.Ks[(16 * ks + tr_row) * QP + 32 * dt + tr_col];
-                    Cacc[p * DT + dt] = mfma32(cat(tr_read(kb), tr_read(kb + 4 * QP)), Vw[ks], Cacc[p * DT + dt]);
+                    const uint16_t* kb = &S.Ks[(32 * ks + tr_row) * QP + 16 * dt + tr_col];
+                    Cacc[p * DT + dt] = mfma16(cat(tr_read(kb), tr_read(kb + 4 * QP)), Vw[ks], Cacc[p * DT + dt]);
                 }
             }
             // n_p = decay n_p + K_p^T w: A = w as bf16 hi / lo rows, B = K read transposed
 #pragma unroll
             for (int j = 0; j < NUT; ++j) {
                 const int ut = wave * NUT + j;   // 16-column tile of this d block
+                if (ut >= DB / 16) break;
                 f32x4_t nacc = f32x4_t{};
 #pragma unroll
-                for (int ks = 0; ks < L / 32; ++ks) {
+                for (int ks = 0; ks < NKS; ++ks) {
                     const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&S.wb[l16 & 1][32 * ks + 8 * g16])
                                                  : u32x4_t{0u, 0u, 0u, 0u};
-                    const uint16_t* kb = &S.Ks[(32 * ks + tr_row16) * QP + 16 * ut + tr_col16];
+                    const uint16_t* kb = &S.Ks[(32 * ks + tr_row) * QP + 16 * ut + tr_col];
                     nacc = mfma16(wa, cat(tr_read(kb), tr_read(kb + 4 * QP)), nacc);
                 }
                 // rows 0 and 1 (hi and lo weights) of column l16 sit in lanes 0..15
@@ -573,13 +590,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         if constexpr (FULL) {
             // finish Q n: columns 0 and 1 of the 16x16 tile are lanes l16 = 0 and 1
 #pragma unroll
-            for (int i = 0; i < DQT; ++i) {
-                const int tt = wave + kWaves * i;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const float other = __shfl_down(dqacc[i][j], 1, 64);
-                    if (tt < L / 16 && l16 == 0) S.dq[16 * tt + 4 * g16 + j] = dqacc[i][j] + other;
-                }
+            for (int j = 0; j < 4; ++j) {
+                const float other = __shfl_down(dqacc[j], 1, 64);
+                if (wave < NTT && l16 == 0) S.dq[16 * wave + 4 * g16 + j] = dqacc[j] + other;
             }
             // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums
 #pragma unroll
@@ -610,10 +623,11 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     if (g16 == 0) S.rs[sb][tau] = rsum;
                 }
             }
-            // zero the masked 16x16 tiles inside each diagonal 32x32 block
-            for (int T = wave; T < NTT; T += kWaves) {
-                const int tau = 32 * T + l16;
-                *reinterpret_cast<u32x2_t*>(&S.St[tau * SP + 32 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
+            // zero the masked 16x16 tiles (sigma block T+1, tau block T) for even T: the k steps
+            // of (ii) are 32 wide
+            for (int T = 2 * wave; T < NTT; T += 2 * kWaves) {
+                const int tau = 16 * T + l16;
+                *reinterpret_cast<u32x2_t*>(&S.St[tau * SP + 16 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
             }
             __syncthreads();
             // denominators
@@ -627,23 +641,19 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             // (ii) N^T = interC * N^T + V^T S~^T, then h
 #pragma unroll
             for (int T = 0; T < NTT; ++T) {
-                const int tau = 32 * T + l32;
-                scale_acc(Nacc[T], S.interC[tau]);
+                const int tau = 16 * T + l16;
+                scale_acc4(Nacc[T], S.interC[tau]);
 #pragma unroll
-                for (int ks = 0; ks < 2 * T + 2; ++ks) {
-                    const uint16_t* vb = &S.Vs[(16 * ks + tr_row) * VP + 32 * wave + tr_col];
-                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&S.St[tau * SP + 16 * ks + 8 * kg]);
-                    Nacc[T] = mfma32(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, Nacc[T]);
+                for (int ks = 0; ks <= T / 2; ++ks) {
+                    const uint16_t* vb = &S.Vs[(32 * ks + tr_row) * VP + vc + tr_col];
+                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&S.St[tau * SP + 32 * ks + 8 * g16]);
+                    Nacc[T] = mfma16(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, Nacc[T]);
                 }
                 const float hv = S.hinv[tau];
-                uint16_t* hrow = A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + 32 * wave + 4 * kg;
-#pragma unroll
-                for (int jg = 0; jg < 4; ++jg) {
-                    u32x2_t o;
-                    o[0] = pack_bf16x2(Nacc[T][4 * jg + 0] * hv, Nacc[T][4 * jg + 1] * hv);
-                    o[1] = pack_bf16x2(Nacc[T][4 * jg + 2] * hv, Nacc[T][4 * jg + 3] * hv);
-                    *reinterpret_cast<u32x2_t*>(hrow + 8 * jg) = o;
-                }
+                u32x2_t o;
+                o[0] = pack_bf16x2(Nacc[T][0] * hv, Nacc[T][1] * hv);
+                o[1] = pack_bf16x2(Nacc[T][2] * hv, Nacc[T][3] * hv);
+                *reinterpret_cast<u32x2_t*>(A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + vc + 4 * g16) = o;
             }
         }
         s_off = s_new;
@@ -671,14 +681,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     }
     const float esc = expf(s_off);
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
+    for (int t = 0; t < NCT; ++t) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const int d = 32 * dt + 8 * (j >> 2) + 4 * kg + (j & 3);
-            Cout[static_cast<int64_t>(d) * kDV + v0 + 32 * wave + l32] = acc_read(Cacc[dt][j]) * esc;
+        for (int j = 0; j < 4; ++j) {
+            const int d = 16 * t + 4 * g16 + j;
+            Cout[static_cast<int64_t>(d) * kDV + v0 + vc + l16] = acc_read(Cacc[t][j]) * esc;
         }
     }
-    if (write_nm) {
+    if (write_nm && tid < kDQK) {
         nout[tid] = S.n[nfinal][tid];
         if (tid == 0) mout[0] = m_prev;
     }

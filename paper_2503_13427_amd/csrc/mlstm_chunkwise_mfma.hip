@@ -148,31 +148,42 @@ struct Cfg {
     static constexpr int VP = kDVT + 8;             // row pitch of V
     static constexpr int SP = L + 8;                // row pitch of S~
     static constexpr int NB = L / 16;               // 16-wide blocks along the chunk
+    static constexpr int QKE = L * QP;              // elements of one Q or K block buffer
+    // L = 128: S~ lives in the second Q/K buffer set, which is free from the end of the
+    // chunk's last d block to the next chunk's first store into it; this keeps the
+    // workgroup within the 160 KB of LDS
+    static constexpr bool ST_ALIAS = (L == 128);
+};
+
+// Per-chunk gate quantities, written one chunk ahead by the gate wave.
+template <int L>
+struct GateBuf {
+    float x2[L];        // (i~ - b) * log2 e
+    float M2[L];        // M * log2 e
+    float interC[L];    // exp(m_prev - M + s) / sqrt(DQK): scale of C_acc^T Q^T
+    float interN[L];    // exp(m_prev - M) / sqrt(DQK):     scale of Q n
+    float floorv[L];    // exp(-(b + M))
+    float wC[L];        // C-update weights exp(x - M_L - s_new)
+    uint16_t wb[2][L];  // n-update weights exp(x - M_L) as bf16 hi / lo rows
+    float scal[4];      // [0] n decay, [1] m_next, [2] s_new, [3] eager C scale (1: none)
 };
 
 template <int L>
 struct Smem {
     using C = Cfg<L>;
-    uint16_t Qs[L * C::QP];        // Q[tau][d]  (current d block)
-    uint16_t Ks[L * C::QP];        // K[tau][d]
-    uint16_t Vs[L * C::VP];        // V[tau][v]  (this workgroup's 128 columns)
-    uint16_t St[L * C::SP];        // S~[tau][sig]
-    uint16_t nb[2][2][kDQK];       // normaliser as bf16 hi / lo rows, double-buffered
-    uint16_t wb[2][L];             // n-update weights as bf16 hi / lo rows
-    float n[2][kDQK];              // fp32 normaliser, double-buffered across chunks
-    float x2[L];                   // (i~ - b) * log2 e
-    float M2[L];                   // M * log2 e
-    float interC[L];               // exp(m_prev - M + s) / sqrt(DQK): scale of C_acc^T Q^T
-    float interN[L];               // exp(m_prev - M) / sqrt(DQK):     scale of Q n
-    float floorv[L];               // exp(-(b + M))
-    float wC[L];                   // C-update weights exp(x - M_L - s_new)
-    float dq[L];                   // Q n_{k-1} (unscaled q)
-    float hinv[L];                 // 1 / max(|den|, floor)
-    float rs[L / 16][L];           // row sums of S~ per 16-wide sigma block
-    float scal[8];                 // [0] n decay, [1] m_next, [2] gsum, [3] s_new, [4] eager C scale
+    uint16_t QK[2][2][C::QKE];                     // [set][0: Q, 1: K][tau * QP + d]; d block p uses set p % 2
+    uint16_t Vs[2][L * C::VP];                     // V[tau][v] (this workgroup's 128 columns), by chunk parity
+    uint16_t St_own[C::ST_ALIAS ? 8 : L * C::SP];  // S~[tau][sig] when it has its own buffer
+    uint16_t nb[2][2][kDQK];                       // normaliser as bf16 hi / lo rows, double-buffered
+    float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
+    float dq[L];                                   // Q n_{k-1} (unscaled q)
+    float rs[L / 16][L];                           // row sums of S~ per 16-wide sigma block
+    GateBuf<L> G[2];                               // by chunk parity
 };
+static_assert(Cfg<128>::ST_ALIAS && 128 * Cfg<128>::SP <= 2 * Cfg<128>::QKE, "S~ must fit in one Q/K set");
+static_assert(sizeof(Smem<64>) <= 160 * 1024 && sizeof(Smem<128>) <= 160 * 1024, "LDS budget");
 
-// Per-thread staging registers.
+// Per-thread staging registers: one Q/K d block and one chunk of V in flight.
 template <int L>
 struct QKRegs {
     static constexpr int N = (L * Cfg<L>::DB / 8) / kThreads;   // 16-byte pieces per thread per matrix
@@ -183,7 +194,6 @@ template <int L>
 struct VRegs {
     static constexpr int N = (L * kDVT / 8) / kThreads;
     u32x4_t v[N];
-    float ig, fg, ig2, fg2;   // gates (wave 0; two per lane when L == 128)
 };
 
 // Buffer resources (SGPRs) for one sequence's inputs: loads need one 32-bit VGPR
@@ -219,14 +229,14 @@ __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, 
     }
 }
 template <int L, bool FULL>
-__device__ __forceinline__ void store_qk(Smem<L>& S, const QKRegs<L>& r, int tid) {
+__device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKRegs<L>& r, int tid) {
     constexpr int PR = Cfg<L>::DB / 8, QP = Cfg<L>::QP;
 #pragma unroll
     for (int i = 0; i < QKRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
         const int off = (item / PR) * QP + 8 * (item % PR);
-        if constexpr (FULL) *reinterpret_cast<u32x4_t*>(&S.Qs[off]) = r.q[i];
-        *reinterpret_cast<u32x4_t*>(&S.Ks[off]) = r.k[i];
+        if constexpr (FULL) *reinterpret_cast<u32x4_t*>(&Qd[off]) = r.q[i];
+        *reinterpret_cast<u32x4_t*>(&Kd[off]) = r.k[i];
     }
 }
 template <int L>
@@ -237,42 +247,54 @@ __device__ __forceinline__ void load_v(VRegs<L>& r, const SeqRsrc& R, int t0, in
         const int item = tid + i * kThreads;
         r.v[i] = bload128(R.v, (item / 16) * (kDV * 2) + 16 * (item % 16), soff);
     }
-    if ((tid >> 6) == kGateWave) {
-        const uint32_t goff = static_cast<uint32_t>(t0) * 4;
-        const int lane = tid & 63;
-        r.ig = bloadf(R.ig, 4 * lane, goff);
-        r.fg = bloadf(R.fg, 4 * lane, goff);
-        if constexpr (L == 128) {
-            r.ig2 = bloadf(R.ig, 4 * lane + 256, goff);
-            r.fg2 = bloadf(R.fg, 4 * lane + 256, goff);
-        }
-    }
 }
 template <int L>
-__device__ __forceinline__ void store_v(Smem<L>& S, const VRegs<L>& r, int tid) {
+__device__ __forceinline__ void store_v(uint16_t* Vd, const VRegs<L>& r, int tid) {
 #pragma unroll
     for (int i = 0; i < VRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
-        *reinterpret_cast<u32x4_t*>(&S.Vs[(item / 16) * Cfg<L>::VP + 8 * (item % 16)]) = r.v[i];
+        *reinterpret_cast<u32x4_t*>(&Vd[(item / 16) * Cfg<L>::VP + 8 * (item % 16)]) = r.v[i];
+    }
+}
+// Gate pre-activations of one chunk, one (L = 64) or two (L = 128) per lane of the gate wave.
+template <int L>
+__device__ __forceinline__ void load_gates(float (&gi)[2], float (&gf)[2], const SeqRsrc& R, int t0, int lane) {
+    const uint32_t goff = static_cast<uint32_t>(t0) * 4;
+    gi[0] = bloadf(R.ig, 4 * lane, goff);
+    gf[0] = bloadf(R.fg, 4 * lane, goff);
+    if constexpr (L == 128) {
+        gi[1] = bloadf(R.ig, 4 * lane + 256, goff);
+        gf[1] = bloadf(R.fg, 4 * lane + 256, goff);
     }
 }
 
-// Inclusive wave-wide scans over 64 lanes.
-__device__ __forceinline__ float wave_incl_sum(float x, int lane) {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const float y = __shfl_up(x, o, 64);
-        if (lane >= o) x += y;
-    }
+// Inclusive scans over the 64 lanes of a wave with DPP: shifts inside 16-lane rows,
+// then the row_bcast steps carry row totals forward.  Lanes without a source take the
+// identity (0 for the sum, -inf for the max).
+#define MLSTM_DPP(old, x, ctrl, rmask)                                                                   \
+    __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, (old)),                 \
+                                                          __builtin_bit_cast(int, (x)), (ctrl), (rmask), 0xf, false))
+__device__ __forceinline__ float wave_incl_sum(float x) {
+    x += MLSTM_DPP(0.0f, x, 0x111, 0xf);   // row_shr:1
+    x += MLSTM_DPP(0.0f, x, 0x112, 0xf);   // row_shr:2
+    x += MLSTM_DPP(0.0f, x, 0x114, 0xf);   // row_shr:4
+    x += MLSTM_DPP(0.0f, x, 0x118, 0xf);   // row_shr:8
+    x += MLSTM_DPP(0.0f, x, 0x142, 0xa);   // row_bcast:15 into rows 1 and 3
+    x += MLSTM_DPP(0.0f, x, 0x143, 0xc);   // row_bcast:31 into rows 2 and 3
     return x;
 }
-__device__ __forceinline__ float wave_incl_max(float x, int lane) {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const float y = __shfl_up(x, o, 64);
-        if (lane >= o) x = fmaxf(x, y);
-    }
+__device__ __forceinline__ float wave_incl_max(float x) {
+    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x111, 0xf));
+    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x112, 0xf));
+    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x114, 0xf));
+    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x118, 0xf));
+    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x142, 0xa));
+    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x143, 0xc));
     return x;
+}
+#undef MLSTM_DPP
+__device__ __forceinline__ float lane63(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
 }
 
 // exp and log sigmoid through the hardware exp2 / log2 (v_exp_f32, v_log_f32).
@@ -281,54 +303,56 @@ __device__ __forceinline__ float flogsig(float x) {
     return fminf(x, 0.0f) - 0.6931471805599453f * __builtin_amdgcn_logf(1.0f + fexp(-fabsf(x)));
 }
 
-// Gate phase (one wave): chunkwise gates, max state, the lazy scale, and every per-row
-// scale of the chunk.
+// Gate phase of one chunk (run by one wave): in-chunk prefix sums and maxima, the max
+// state, the lazy C scale, and every per-row scale of the chunk.  m_prev and s_cur
+// carry the max state and the lazy log-scale from chunk to chunk; gsum accumulates b_L.
 template <int L>
-__device__ __forceinline__ void gate_phase(Smem<L>& S, const VRegs<L>& r, float m_prev, float s_old, int lane) {
-    float a = flogsig(r.fg);
-    float b = wave_incl_sum(a, lane);
-    float x = r.ig - b;
-    float p = wave_incl_max(x, lane);
+__device__ __forceinline__ void gate_phase(GateBuf<L>& Gb, const float (&gi)[2], const float (&gf)[2], float& m_prev,
+                                           float& s_cur, float& gsum, int lane) {
+    const float b = wave_incl_sum(flogsig(gf[0]));
+    const float x = gi[0] - b;
+    const float p = wave_incl_max(x);
     float b2 = 0.f, x2 = 0.f, p2 = 0.f;
     if constexpr (L == 128) {
-        const float btot = __shfl(b, 63, 64);
-        const float ptot = __shfl(p, 63, 64);
-        b2 = btot + wave_incl_sum(flogsig(r.fg2), lane);
-        x2 = r.ig2 - b2;
-        p2 = fmaxf(ptot, wave_incl_max(x2, lane));
+        b2 = lane63(b) + wave_incl_sum(flogsig(gf[1]));
+        x2 = gi[1] - b2;
+        p2 = fmaxf(lane63(p), wave_incl_max(x2));
     }
-    const float pL = (L == 128) ? __shfl(p2, 63, 64) : __shfl(p, 63, 64);
-    const float bL = (L == 128) ? __shfl(b2, 63, 64) : __shfl(b, 63, 64);
+    const float pL = lane63(L == 128 ? p2 : p);
+    const float bL = lane63(L == 128 ? b2 : b);
     const float ML = fmaxf(m_prev, pL);
     // an empty state (m = -inf, local-state pass only) has nothing to decay
     const bool empty = (m_prev == -INFINITY);
     const float dlog = empty ? 0.0f : m_prev - ML;
-    const float s_try = s_old + dlog;
+    const float s_try = s_cur + dlog;
     const bool eager = s_try < kRenorm;
     const float s_new = eager ? 0.0f : s_try;
     auto emit = [&](int tau, float bb, float xx, float pp) {
         const float M = fmaxf(m_prev, pp);
-        S.x2[tau] = xx * kLog2e;
-        S.M2[tau] = M * kLog2e;
-        S.interC[tau] = (M == -INFINITY) ? 0.0f : fexp(m_prev - M + s_old) * kQScale;
-        S.interN[tau] = (M == -INFINITY) ? 0.0f : fexp(m_prev - M) * kQScale;
-        S.floorv[tau] = fexp(-(bb + M));
+        Gb.x2[tau] = xx * kLog2e;
+        Gb.M2[tau] = M * kLog2e;
+        Gb.interC[tau] = (M == -INFINITY) ? 0.0f : fexp(m_prev - M + s_cur) * kQScale;
+        Gb.interN[tau] = (M == -INFINITY) ? 0.0f : fexp(m_prev - M) * kQScale;
+        Gb.floorv[tau] = fexp(-(bb + M));
         const bool none = (xx == -INFINITY);
-        S.wC[tau] = none ? 0.0f : fexp(xx - ML - s_new);
+        Gb.wC[tau] = none ? 0.0f : fexp(xx - ML - s_new);
         const float wn = none ? 0.0f : fexp(xx - ML);
         const uint16_t whi = f32_to_bf16(wn);
-        S.wb[0][tau] = whi;
-        S.wb[1][tau] = f32_to_bf16(wn - bf16_to_f32(whi));
+        Gb.wb[0][tau] = whi;
+        Gb.wb[1][tau] = f32_to_bf16(wn - bf16_to_f32(whi));
     };
     emit(lane, b, x, p);
     if constexpr (L == 128) emit(64 + lane, b2, x2, p2);
+    const float m_next = bL + ML;
     if (lane == 0) {
-        S.scal[0] = (empty || ML == -INFINITY) ? 0.0f : fexp(m_prev - ML);
-        S.scal[1] = bL + ML;
-        S.scal[2] += bL;
-        S.scal[3] = s_new;
-        S.scal[4] = eager ? fexp(s_try) : 1.0f;
+        Gb.scal[0] = (empty || ML == -INFINITY) ? 0.0f : fexp(m_prev - ML);
+        Gb.scal[1] = m_next;
+        Gb.scal[2] = s_new;
+        Gb.scal[3] = eager ? fexp(s_try) : 1.0f;
     }
+    m_prev = m_next;
+    s_cur = s_new;
+    gsum += bL;
 }
 
 // XCD-aware block order: the hardware deals consecutive workgroups round-robin to
@@ -362,18 +386,21 @@ struct ChunkKernelArgs {
 // workspace slot of (sequence s, segment g): C [DQK*DV], n [DQK], then m_loc, gsum, m_in, pad
 constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
 
+// Staging order (one Q/K block and one V chunk in registers at a time): block 0 of a
+// chunk and its V are stored during the previous chunk (before its last d block), block 1
+// at the top of the chunk, block p + 1 (p >= 1) at the barrier that opens block p.
 template <int L, bool FULL>
 __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     Smem<L>& S = *reinterpret_cast<Smem<L>*>(smem_raw);
     using CF = Cfg<L>;
-    constexpr int QP = CF::QP, VP = CF::VP, SP = CF::SP, NB = CF::NB, DB = CF::DB, DT = CF::DT;
+    constexpr int QP = CF::QP, VP = CF::VP, SP = CF::SP, NB = CF::NB, DB = CF::DB, DT = CF::DT, NDB = CF::NDB;
     constexpr int NT_S = NB * (NB + 1) / 2;          // causal 16x16 tiles of S^T
     constexpr int MAXT = (NT_S + kWaves - 1) / kWaves;
     constexpr int NTT = L / 16;                       // 16-wide tau tiles
     constexpr int NKS = L / 32;                       // k steps of 32 along the chunk
     constexpr int NCT = kDQK / 16;                    // 16-row tiles of this wave's C slice
-    constexpr int NUT = (DB / 16 + kWaves - 1) / kWaves;           // 16-col n-update tiles per wave per block
+    constexpr int NUT = (DB / 16 + kWaves - 1) / kWaves;   // 16-col n-update tiles per wave per block
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -384,6 +411,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     const int tr_row = (l16 >> 2) + 8 * g16;   // + 4r + k base
     const int tr_col = 4 * (l16 & 3);           // + m/n base
     const int vc = kVW * wave;                  // this wave's first column of the dv tile
+    const bool gate_wave = (wave == kGateWave);
+    uint16_t* const St = CF::ST_ALIAS ? &S.QK[1][0][0] : S.St_own;
 
     const int wi = work_index();
     const int tile = wi % kNTile;
@@ -438,14 +467,26 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         S.nb[0][0][tid] = hi;
         S.nb[0][1][tid] = f32_to_bf16(nv - bf16_to_f32(hi));
     }
-    if (tid == 0) S.scal[2] = 0.0f;
     float s_off = 0.0f;   // C = C_acc * e^{s_off}
 
-    VRegs<L> rv;
+    // gate wave state: max state and lazy scale after the last chunk whose gates it computed
+    float g_m = m_prev, g_s = 0.0f, g_sum = 0.0f;
+    float gi[2] = {0.f, 0.f}, gf[2] = {0.f, 0.f};
+
     QKRegs<L> rqk;
+    VRegs<L> rv;
     if (c_begin < c_end) {
-        load_v<L>(rv, P, c_begin * L, v0, tid);
-        load_qk<L, FULL>(rqk, P, c_begin * L, 0, tid);
+        const int t0 = c_begin * L;
+        load_qk<L, FULL>(rqk, P, t0, 0, tid);
+        load_v<L>(rv, P, t0, v0, tid);
+        if (gate_wave) {
+            load_gates<L>(gi, gf, P, t0, lane);
+            gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, g_sum, lane);
+        }
+        store_qk<L, FULL>(S.QK[0][0], S.QK[0][1], rqk, tid);
+        store_v<L>(S.Vs[c_begin & 1], rv, tid);
+        load_qk<L, FULL>(rqk, P, t0, 1, tid);
+        if (c_begin + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid);
     }
 
     f32x4_t Nacc[NTT];
@@ -455,28 +496,30 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * L;
         const int cur = (c - c_begin) & 1;
-        __syncthreads();   // the previous chunk's LDS reads are done
-        if (wave == kGateWave) gate_phase<L>(S, rv, m_prev, s_off, lane);
-        store_v<L>(S, rv, tid);
-        store_qk<L, FULL>(S, rqk, tid);
-        __syncthreads();
-        if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid);
-        load_qk<L, FULL>(rqk, P, t0, 1, tid);
-        const float decay_n = S.scal[0];
-        const float m_next = S.scal[1];
-        const float s_new = S.scal[3];
-        const float c_scale = S.scal[4];   // != 1: apply this chunk's decay to C_acc eagerly
+        const int par = c & 1;
+        const GateBuf<L>& Gc = S.G[par];
+        __syncthreads();   // the previous chunk is done; block 0, V and the gates of this chunk are visible
+        // block 1 -> set 1 (its readers in the previous chunk, the last d block and S~, are done)
+        store_qk<L, FULL>(S.QK[1][0], S.QK[1][1], rqk, tid);
+        if constexpr (NDB > 2) load_qk<L, FULL>(rqk, P, t0, 2, tid);
+        else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
+        if (gate_wave && c + 1 < c_end) load_gates<L>(gi, gf, P, t0 + L, lane);
+        const float decay_n = Gc.scal[0];
+        const float m_next = Gc.scal[1];
+        const float s_new = Gc.scal[2];
+        const float c_scale = Gc.scal[3];   // != 1: apply this chunk's decay to C_acc eagerly
         const float* n_old = S.n[cur];
         float* n_new = S.n[cur ^ 1];
+        const uint16_t* Vc = S.Vs[par];
 
         // B operands of (iv): V read transposed once per chunk and scaled by the C-update key
         // weights; lane (n = column vc + l16, k group g16) holds tau = 32 ks + 8 g16 + 0..7
         u32x4_t Vw[NKS];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
-            const uint16_t* vb = &S.Vs[(32 * ks + tr_row) * VP + vc + tr_col];
+            const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vc + tr_col];
             const u32x4_t raw = cat(tr_read(vb), tr_read(vb + 4 * VP));
-            const float* wv = &S.wC[32 * ks + 8 * g16];
+            const float* wv = &Gc.wC[32 * ks + 8 * g16];
 #pragma unroll
             for (int u = 0; u < 4; ++u)
                 Vw[ks][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
@@ -491,16 +534,26 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         }
 
 #pragma unroll
-        for (int p = 0; p < CF::NDB; ++p) {
+        for (int p = 0; p < NDB; ++p) {
+            const uint16_t* Qs = S.QK[p & 1][0];
+            const uint16_t* Ks = S.QK[p & 1][1];
             if (p > 0) {
-                __syncthreads();   // block p-1 fully read
-                store_qk<L, FULL>(S, rqk, tid);
-                __syncthreads();
-                if (p + 1 < CF::NDB) load_qk<L, FULL>(rqk, P, t0, p + 1, tid);
-                else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
+                __syncthreads();   // block p visible, block p - 1 fully read
+                if (p + 1 < NDB) {
+                    store_qk<L, FULL>(S.QK[(p + 1) & 1][0], S.QK[(p + 1) & 1][1], rqk, tid);
+                    if (p + 2 < NDB) load_qk<L, FULL>(rqk, P, t0, p + 2, tid);
+                    else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
+                } else if (c + 1 < c_end) {
+                    // block 0 and V of the next chunk
+                    store_qk<L, FULL>(S.QK[0][0], S.QK[0][1], rqk, tid);
+                    load_qk<L, FULL>(rqk, P, t0 + L, 1, tid);
+                    store_v<L>(S.Vs[par ^ 1], rv, tid);
+                    if (c + 2 < c_end) load_v<L>(rv, P, t0 + 2 * L, v0, tid);
+                }
             }
             if constexpr (FULL) {
-                // (i) S^T += K_p Q_p^T on this wave's causal tiles
+                // (i) S^T += K_p Q_p^T on this wave's causal tiles (L = 128: a fixed tile count per
+                // wave; the surplus tiles repeat the last one and are not used)
 #pragma unroll
                 for (int i = 0; i < MAXT; ++i) {
                     const int t = (L == 128) ? min(wave + kWaves * i, NT_S - 1) : wave + kWaves * i;
@@ -508,8 +561,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                         int tb = 0, rem = t;
                         while (rem > tb) { rem -= tb + 1; ++tb; }
                         const int sb = rem;
-                        const uint16_t* ka = &S.Ks[(16 * sb + l16) * QP + 8 * g16];
-                        const uint16_t* qb = &S.Qs[(16 * tb + l16) * QP + 8 * g16];
+                        const uint16_t* ka = &Ks[(16 * sb + l16) * QP + 8 * g16];
+                        const uint16_t* qb = &Qs[(16 * tb + l16) * QP + 8 * g16];
 #pragma unroll
                         for (int ks = 0; ks < DB / 32; ++ks)
                             Sacc[i] = mfma16(*reinterpret_cast<const u32x4_t*>(ka + 32 * ks),
@@ -518,7 +571,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 }
                 // Q n_{k-1} over this d block: A = Q rows, B = n as bf16 hi / lo columns
                 if (wave < NTT) {
-                    const uint16_t* qa = &S.Qs[(16 * wave + l16) * QP + 8 * g16];
+                    const uint16_t* qa = &Qs[(16 * wave + l16) * QP + 8 * g16];
                     const uint16_t* nbp = &S.nb[cur][l16 & 1][p * DB + 8 * g16];
 #pragma unroll
                     for (int ks = 0; ks < DB / 32; ++ks) {
@@ -541,7 +594,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     const int dl = 32 * pt + 4 * g16;
 #pragma unroll
                     for (int T = 0; T < NTT; ++T) {
-                        const uint16_t* qrow = &S.Qs[(16 * T + l16) * QP + dl];
+                        const uint16_t* qrow = &Qs[(16 * T + l16) * QP + dl];
                         const u32x2_t b0 = *reinterpret_cast<const u32x2_t*>(qrow);
                         const u32x2_t b1 = *reinterpret_cast<const u32x2_t*>(qrow + 16);
                         Nacc[T] = mfma16(a, cat(b0, b1), Nacc[T]);
@@ -558,7 +611,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) {
-                    const uint16_t* kb = &S.Ks[(32 * ks + tr_row) * QP + 16 * dt + tr_col];
+                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * dt + tr_col];
                     Cacc[p * DT + dt] = mfma16(cat(tr_read(kb), tr_read(kb + 4 * QP)), Vw[ks], Cacc[p * DT + dt]);
                 }
             }
@@ -570,9 +623,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 f32x4_t nacc = f32x4_t{};
 #pragma unroll
                 for (int ks = 0; ks < NKS; ++ks) {
-                    const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&S.wb[l16 & 1][32 * ks + 8 * g16])
+                    const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&Gc.wb[l16 & 1][32 * ks + 8 * g16])
                                                  : u32x4_t{0u, 0u, 0u, 0u};
-                    const uint16_t* kb = &S.Ks[(32 * ks + tr_row) * QP + 16 * ut + tr_col];
+                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * ut + tr_col];
                     nacc = mfma16(wa, cat(tr_read(kb), tr_read(kb + 4 * QP)), nacc);
                 }
                 // rows 0 and 1 (hi and lo weights) of column l16 sit in lanes 0..15
@@ -587,6 +640,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             }
         }
 
+        // gates of the next chunk, one chunk ahead
+        if (gate_wave && c + 1 < c_end) gate_phase<L>(S.G[par ^ 1], gi, gf, g_m, g_s, g_sum, lane);
+
         if constexpr (FULL) {
             // finish Q n: columns 0 and 1 of the 16x16 tile are lanes l16 = 0 and 1
 #pragma unroll
@@ -594,6 +650,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 const float other = __shfl_down(dqacc[j], 1, 64);
                 if (wave < NTT && l16 == 0) S.dq[16 * wave + 4 * g16 + j] = dqacc[j] + other;
             }
+            if constexpr (CF::ST_ALIAS) __syncthreads();   // the last d block is fully read before S~ overwrites it
             // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
@@ -603,21 +660,21 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     while (rem > tb) { rem -= tb + 1; ++tb; }
                     const int sb = rem;
                     const int tau = 16 * tb + l16;
-                    const float Mt = S.M2[tau];
+                    const float Mt = Gc.M2[tau];
                     float vals[4];
                     float rsum = 0.f;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const int sig = 16 * sb + 4 * g16 + j;
                         float val = 0.f;
-                        if (sig <= tau) val = Sacc[i][j] * kQScale * fast_exp2(S.x2[sig] - Mt);
+                        if (sig <= tau) val = Sacc[i][j] * kQScale * fast_exp2(Gc.x2[sig] - Mt);
                         vals[j] = val;
                         rsum += val;
                     }
                     u32x2_t o;
                     o[0] = pack_bf16x2(vals[0], vals[1]);
                     o[1] = pack_bf16x2(vals[2], vals[3]);
-                    *reinterpret_cast<u32x2_t*>(&S.St[tau * SP + 16 * sb + 4 * g16]) = o;
+                    *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
                     rsum += __shfl_xor(rsum, 16, 64);
                     rsum += __shfl_xor(rsum, 32, 64);
                     if (g16 == 0) S.rs[sb][tau] = rsum;
@@ -627,29 +684,24 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             // of (ii) are 32 wide
             for (int T = 2 * wave; T < NTT; T += 2 * kWaves) {
                 const int tau = 16 * T + l16;
-                *reinterpret_cast<u32x2_t*>(&S.St[tau * SP + 16 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
+                *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
             }
             __syncthreads();
-            // denominators
-            if (tid < L) {
-                const int tau = tid;
-                float den = S.interN[tau] * S.dq[tau];
-                for (int sb = 0; sb <= tau / 16; ++sb) den += S.rs[sb][tau];
-                S.hinv[tau] = 1.0f / fmaxf(fabsf(den), S.floorv[tau]);
-            }
-            __syncthreads();
-            // (ii) N^T = interC * N^T + V^T S~^T, then h
+            // (ii) N^T = interC * N^T + V^T S~^T, then h = N^T / max(|den|, floor)
 #pragma unroll
             for (int T = 0; T < NTT; ++T) {
                 const int tau = 16 * T + l16;
-                scale_acc4(Nacc[T], S.interC[tau]);
+                float den = Gc.interN[tau] * S.dq[tau];
+#pragma unroll
+                for (int sb = 0; sb <= T; ++sb) den += S.rs[sb][tau];
+                const float hv = __builtin_amdgcn_rcpf(fmaxf(fabsf(den), Gc.floorv[tau]));
+                scale_acc4(Nacc[T], Gc.interC[tau]);
 #pragma unroll
                 for (int ks = 0; ks <= T / 2; ++ks) {
-                    const uint16_t* vb = &S.Vs[(32 * ks + tr_row) * VP + vc + tr_col];
-                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&S.St[tau * SP + 32 * ks + 8 * g16]);
+                    const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vc + tr_col];
+                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&St[tau * SP + 32 * ks + 8 * g16]);
                     Nacc[T] = mfma16(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, Nacc[T]);
                 }
-                const float hv = S.hinv[tau];
                 u32x2_t o;
                 o[0] = pack_bf16x2(Nacc[T][0] * hv, Nacc[T][1] * hv);
                 o[1] = pack_bf16x2(Nacc[T][2] * hv, Nacc[T][3] * hv);
@@ -677,7 +729,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         Cout = slot;
         nout = slot + kDQK * kDV;
         mout = nout + kDQK;   // m_loc, then gsum
-        if (write_nm && tid == 0) mout[1] = S.scal[2];
+        if (write_nm && gate_wave && lane == 0) mout[1] = g_sum;
     }
     const float esc = expf(s_off);
 #pragma unroll

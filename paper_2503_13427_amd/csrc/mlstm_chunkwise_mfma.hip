@@ -17,8 +17,8 @@
 //
 // Lazily scaled matrix memory.  The accumulators hold C_acc with C = C_acc e^{s}.
 // A chunk's decay is folded into s (s += m_prev - M_L) and into the key weights
-// of the update (w e^{-s} <= e^{-kRenorm}), so the 128 accumulator registers of a
-// wave are not rescaled by VALU work in most chunks; when s would fall below
+// of the update (w e^{-s} <= e^{-kRenorm}), so the 64 accumulator registers of C in
+// a wave are not rescaled by VALU work in most chunks; when s would fall below
 // kRenorm the chunk applies the decay eagerly instead (C_acc *= e^{s + m_prev - M_L},
 // between the read-out (iii) and the update (iv)) and s returns to 0.  The
 // inter-chunk term uses exp(m_prev - M_tau + s); the exit state is C_acc e^{s}.
@@ -79,17 +79,12 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x4_t mfma16(u32x4_t a, u32x4_t b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
-                                                   c, 0, 0, 0);
-}
-__device__ __forceinline__ f32x16_t mfma32(u32x4_t a, u32x4_t b, f32x16_t c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
                                                    c, 0, 0, 0);
 }
 
@@ -100,37 +95,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float lo_f32(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_f32(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// Accumulator access through single instructions: keeps the register allocator from
-// parking copies of whole accumulator tiles in VGPRs across the chunk loop.
-__device__ __forceinline__ float acc_read(float x) {
-    float t;
-    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(t) : "a"(x));
-    return t;
-}
-__device__ __forceinline__ void scale_acc(f32x16_t& acc, float s) {
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        float x = acc[j];
-        float t;
-        asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
-                     : "+a"(x), "=&v"(t)
-                     : "v"(s));
-        acc[j] = x;
-    }
-}
-
-__device__ __forceinline__ void scale_acc4(f32x4_t& acc, float s) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        float x = acc[j];
-        float t;
-        asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
-                     : "+a"(x), "=&v"(t)
-                     : "v"(s));
-        acc[j] = x;
-    }
-}
 
 // LDS transpose read: 4 bf16 per lane (see the header comment for the lane mapping).
 __device__ __forceinline__ u32x2_t tr_read(const uint16_t* p) {
@@ -456,9 +420,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         for (int j = 0; j < 4; ++j) {
             const int d = 16 * t + 4 * g16 + j;
             const float x = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + vc + l16] : 0.0f;
-            asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(Cacc[t][j]) : "v"(x));
+            Cacc[t][j] = x;
         }
-        if ((t & 3) == 3) __builtin_amdgcn_sched_barrier(0);
     }
     if (tid < kDQK) {
         const float nv = nin ? nin[tid] : 0.0f;
@@ -587,10 +550,10 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     const f32x4_t& c0 = Cacc[p * DT + 2 * pt];
                     const f32x4_t& c1 = Cacc[p * DT + 2 * pt + 1];
                     u32x4_t a;
-                    a[0] = pack_bf16x2(acc_read(c0[0]), acc_read(c0[1]));
-                    a[1] = pack_bf16x2(acc_read(c0[2]), acc_read(c0[3]));
-                    a[2] = pack_bf16x2(acc_read(c1[0]), acc_read(c1[1]));
-                    a[3] = pack_bf16x2(acc_read(c1[2]), acc_read(c1[3]));
+                    a[0] = pack_bf16x2((c0[0]), (c0[1]));
+                    a[1] = pack_bf16x2((c0[2]), (c0[3]));
+                    a[2] = pack_bf16x2((c1[0]), (c1[1]));
+                    a[3] = pack_bf16x2((c1[2]), (c1[3]));
                     const int dl = 32 * pt + 4 * g16;
 #pragma unroll
                     for (int T = 0; T < NTT; ++T) {
@@ -605,7 +568,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             // (iv) C_p += K_p^T (w e^{-s} V): A = K read transposed, B = the scaled V operands
             if (c_scale != 1.0f) {
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) scale_acc4(Cacc[p * DT + dt], c_scale);
+                for (int dt = 0; dt < DT; ++dt) Cacc[p * DT + dt] *= c_scale;
             }
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks) {
@@ -695,7 +658,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 #pragma unroll
                 for (int sb = 0; sb <= T; ++sb) den += S.rs[sb][tau];
                 const float hv = __builtin_amdgcn_rcpf(fmaxf(fabsf(den), Gc.floorv[tau]));
-                scale_acc4(Nacc[T], Gc.interC[tau]);
+                Nacc[T] *= Gc.interC[tau];
 #pragma unroll
                 for (int ks = 0; ks <= T / 2; ++ks) {
                     const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vc + tr_col];
@@ -737,7 +700,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int d = 16 * t + 4 * g16 + j;
-            Cout[static_cast<int64_t>(d) * kDV + v0 + vc + l16] = acc_read(Cacc[t][j]) * esc;
+            Cout[static_cast<int64_t>(d) * kDV + v0 + vc + l16] = (Cacc[t][j]) * esc;
         }
     }
     if (write_nm && tid < kDQK) {

@@ -87,6 +87,30 @@ class Prefill:
         return acc.prefill_bytes(w.B, w.NH, w.T, w.DQK, w.DV, with_initial_state=w.state is not None)
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "chunkwise_traffic_B1_NH8_T2048_L64.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2503_13427_amd", "csrc", "mlstm_chunkwise_mfma.hip")
+
+
+def measured_traffic():
+    """HBM bytes per headline call from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary, or None
+    when that summary is missing or was taken on a different chunkwise kernel source."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+        src = open(KERNEL_SOURCE, "rb").read()
+    except OSError:
+        return None
+    nbytes = sha = None
+    for line in text.splitlines():
+        if line.startswith("traffic_bytes_per_call:"):
+            nbytes = float(line.split(":")[1])
+        elif line.startswith("kernel_source_sha256_16:"):
+            sha = line.split(":")[1].split()[0]
+    if nbytes is None or sha != hashlib.sha256(src).hexdigest()[:16]:
+        return None
+    return nbytes
+
+
 def time_steps(fn, steps, warmup, stream):
     """Wall time and HIP-event time (on the launch stream) of ``steps`` calls of fn."""
     for _ in range(warmup):
@@ -237,9 +261,10 @@ def main():
         line["value"] = hp["tokens_per_s"]
         line["ms_per_step"] = hp["us_per_call"] / 1e3
         line["roofline"] = {"bound": "mfma", "achieved": hp["tflops"], "peak": acc.PEAK_BF16_MFMA_TFLOPS,
-                            "unit": "TFLOP/s", "frac": hp["mfma_frac"], "traffic": None,
-                            "kernel": "chunk_mfma_kernel<64, FULL> (+ local-state and combine kernels of the "
-                                      "segment schedule; achieved uses the whole call's duration)",
+                            "unit": "TFLOP/s", "frac": hp["mfma_frac"], "traffic": measured_traffic(),
+                            "kernel": "mlstm_chunkwise_fwd call: chunk_mfma_kernel<64,false> + combine_kernel + "
+                                      "chunk_mfma_kernel<64,true> (segment schedule); achieved and traffic are per "
+                                      "call, over the call's duration",
                             "flops_per_call": hp["flops_per_call"], "hbm_frac": hp["hbm_frac"]}
         line["prefill"] = hp
     if "prefill_large" in res:

@@ -214,8 +214,14 @@ def main():
     ap.add_argument("--skip-decode", action="store_true")
     ap.add_argument("--skip-large", action="store_true")
     ap.add_argument("--skip-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=["prefill", "decode", "large"], default=None,
-                    help="run one part only (profiling runs)")
+    ap.add_argument("--only", choices=["prefill", "decode", "large", "calls"], default=None,
+                    help="run one part only (profiling runs); 'calls' makes --calls untimed prefill calls of "
+                         "--workload and then one --copy-mib MiB device copy, for counter runs")
+    ap.add_argument("--workload", default=configs.PREFILL_T2048.name,
+                    help="workload name for --only calls")
+    ap.add_argument("--calls", type=int, default=3)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="size of the calibration copy after the calls (0: none)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported (every (batch, head) "
@@ -227,6 +233,20 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     w = configs.PREFILL_T2048
+
+    if args.only == "calls":
+        wl = {x.name: x for x in configs.ALL}[args.workload]
+        p = Prefill(wl, 1)
+        for _ in range(args.calls):
+            p.step(stream)
+        torch.cuda.synchronize()
+        if args.copy_mib:
+            src = torch.ones(args.copy_mib * (1 << 18), dtype=torch.float32, device="cuda")
+            dst = torch.empty_like(src)
+            dst.copy_(src)
+            torch.cuda.synchronize()
+        log(f"calls: {args.calls} x {wl.name}, copy {args.copy_mib} MiB")
+        return
 
     res = {}
     if args.only in (None, "prefill"):

@@ -69,7 +69,6 @@ constexpr int kDVT = 128;             // dv columns per workgroup
 constexpr int kNTile = kDV / kDVT;    // 4 dv tiles per sequence
 constexpr int kThreads = 512;
 constexpr int kWaves = 8;
-constexpr int kVW = kDVT / kWaves;    // 16 dv columns of C per wave
 constexpr int kGateWave = kWaves - 1; // the wave with the least MFMA work runs the gate scans
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kQScale = 0.0625f;    // 1 / sqrt(256), exact
@@ -117,6 +116,13 @@ struct Cfg {
     // chunk's last d block to the next chunk's first store into it; this keeps the
     // workgroup within the 160 KB of LDS
     static constexpr bool ST_ALIAS = (L == 128);
+    // Wave split of the workgroup's 256 x 128 slice of C: DH d partitions x (8 / DH) column
+    // groups of VT = DH 16-column tiles.  DH = 2 (L = 64) halves the Q and K^T operand reads of
+    // (iii) and (iv) at the price of summing the two partial read-outs of (iii) through LDS;
+    // L = 128 keeps DH = 1 (its read-out accumulators would not fit twice).
+    static constexpr int DH = (L == 64) ? 2 : 1;
+    static constexpr int VT = DH;
+    static constexpr int NVG = kWaves / DH;
 };
 
 // Per-chunk gate quantities, written one chunk ahead by the gate wave.
@@ -143,6 +149,9 @@ struct Smem {
     float dq[L];                                   // Q n_{k-1} (unscaled q)
     float rs[L / 16][L];                           // row sums of S~ per 16-wide sigma block
     GateBuf<L> G[2];                               // by chunk parity
+    // partial read-outs exchanged between the two d partitions of a column group (DH = 2):
+    // [column group][v tile][tau tile][lane] as float4
+    float X[C::DH == 2 ? C::NVG * C::VT * (L / 16) * 64 * 4 : 4];
 };
 static_assert(Cfg<128>::ST_ALIAS && 128 * Cfg<128>::SP <= 2 * Cfg<128>::QKE, "S~ must fit in one Q/K set");
 static_assert(sizeof(Smem<64>) <= 160 * 1024 && sizeof(Smem<128>) <= 160 * 1024, "LDS budget");
@@ -352,7 +361,9 @@ constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
 
 // Staging order (one Q/K block and one V chunk in registers at a time): block 0 of a
 // chunk and its V are stored during the previous chunk (before its last d block), block 1
-// at the top of the chunk, block p + 1 (p >= 1) at the barrier that opens block p.
+// at the top of the chunk, block p + 1 (p >= 1) at the barrier that opens block p.  The V
+// load is issued at the top of the previous chunk, so its registers are free from the last
+// d block on.
 template <int L, bool FULL>
 __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
@@ -374,9 +385,17 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     // transpose-read lane roles inside a 16-lane group (16x16x32 operands)
     const int tr_row = (l16 >> 2) + 8 * g16;   // + 4r + k base
     const int tr_col = 4 * (l16 & 3);           // + m/n base
-    const int vc = kVW * wave;                  // this wave's first column of the dv tile
+    constexpr int DH = CF::DH, VT = CF::VT, NVG = CF::NVG;
+    constexpr int NQ = DT / DH;                 // this wave's 16-row C tiles per d block
+    const int vg = wave % NVG;                  // column group
+    const int dh = wave / NVG;                  // d partition: tiles dt = q DH + dh of every d block
+    auto vcol = [&](int vt) { return 16 * (vg * VT + vt); };   // first column of v tile vt
     const bool gate_wave = (wave == kGateWave);
     uint16_t* const St = CF::ST_ALIAS ? &S.QK[1][0][0] : S.St_own;
+    // Q n tile of this wave (>= NTT: none): with fewer tau tiles than waves, the waves after
+    // the two that hold two S tiles take it
+    const int dqt = (NTT < kWaves) ? wave - 2 : wave;
+    const bool dq_wave = (dqt >= 0 && dqt < NTT);
 
     const int wi = work_index();
     const int tile = wi % kNTile;
@@ -397,8 +416,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
 
     // ---- entry state ------------------------------------------------------------------------
-    // Cacc[t] lane holds C[16 t + 4 g16 + j][vc + l16], j = 0..3
-    f32x4_t Cacc[NCT];
+    // Cacc[p NQ + q][vt] lane holds C[p DB + 16 (q DH + dh) + 4 g16 + j][vcol(vt) + l16], j = 0..3
+    f32x4_t Cacc[NDB * NQ][VT];
     const float* Cin = nullptr;
     const float* nin = nullptr;
     float m_prev;
@@ -415,12 +434,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         m_prev = slot[kDQK * kDV + kDQK + 2];
     }
 #pragma unroll
-    for (int t = 0; t < NCT; ++t) {
+    for (int t = 0; t < NDB * NQ; ++t) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int d = 16 * t + 4 * g16 + j;
-            const float x = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + vc + l16] : 0.0f;
-            Cacc[t][j] = x;
+        for (int vt = 0; vt < VT; ++vt) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int d = (t / NQ) * DB + 16 * ((t % NQ) * DH + dh) + 4 * g16 + j;
+                Cacc[t][vt][j] = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + vcol(vt) + l16] : 0.0f;
+            }
         }
     }
     if (tid < kDQK) {
@@ -449,10 +470,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         store_qk<L, FULL>(S.QK[0][0], S.QK[0][1], rqk, tid);
         store_v<L>(S.Vs[c_begin & 1], rv, tid);
         load_qk<L, FULL>(rqk, P, t0, 1, tid);
-        if (c_begin + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid);
     }
 
-    f32x4_t Nacc[NTT];
+    f32x4_t Nacc[VT][NTT];
     f32x4_t Sacc[MAXT];
     f32x4_t dqacc;
 
@@ -467,6 +487,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         if constexpr (NDB > 2) load_qk<L, FULL>(rqk, P, t0, 2, tid);
         else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
         if (gate_wave && c + 1 < c_end) load_gates<L>(gi, gf, P, t0 + L, lane);
+        // V of the next chunk, stored at the barrier that opens this chunk's last d block
+        if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid);
         const float decay_n = Gc.scal[0];
         const float m_next = Gc.scal[1];
         const float s_new = Gc.scal[2];
@@ -475,22 +497,11 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         float* n_new = S.n[cur ^ 1];
         const uint16_t* Vc = S.Vs[par];
 
-        // B operands of (iv): V read transposed once per chunk and scaled by the C-update key
-        // weights; lane (n = column vc + l16, k group g16) holds tau = 32 ks + 8 g16 + 0..7
-        u32x4_t Vw[NKS];
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-            const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vc + tr_col];
-            const u32x4_t raw = cat(tr_read(vb), tr_read(vb + 4 * VP));
-            const float* wv = &Gc.wC[32 * ks + 8 * g16];
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                Vw[ks][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
-        }
-
         if constexpr (FULL) {
 #pragma unroll
-            for (int T = 0; T < NTT; ++T) Nacc[T] = f32x4_t{};
+            for (int vt = 0; vt < VT; ++vt)
+#pragma unroll
+                for (int T = 0; T < NTT; ++T) Nacc[vt][T] = f32x4_t{};
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) Sacc[i] = f32x4_t{};
             dqacc = f32x4_t{};
@@ -511,7 +522,6 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     store_qk<L, FULL>(S.QK[0][0], S.QK[0][1], rqk, tid);
                     load_qk<L, FULL>(rqk, P, t0 + L, 1, tid);
                     store_v<L>(S.Vs[par ^ 1], rv, tid);
-                    if (c + 2 < c_end) load_v<L>(rv, P, t0 + 2 * L, v0, tid);
                 }
             }
             if constexpr (FULL) {
@@ -533,8 +543,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     }
                 }
                 // Q n_{k-1} over this d block: A = Q rows, B = n as bf16 hi / lo columns
-                if (wave < NTT) {
-                    const uint16_t* qa = &Qs[(16 * wave + l16) * QP + 8 * g16];
+                if (dq_wave) {
+                    const uint16_t* qa = &Qs[(16 * dqt + l16) * QP + 8 * g16];
                     const uint16_t* nbp = &S.nb[cur][l16 & 1][p * DB + 8 * g16];
 #pragma unroll
                     for (int ks = 0; ks < DB / 32; ++ks) {
@@ -543,39 +553,65 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                         dqacc = mfma16(*reinterpret_cast<const u32x4_t*>(qa + 32 * ks), nbv, dqacc);
                     }
                 }
-                // (iii) N^T += C_p^T Q_p^T: A from two C tiles (rows 4 g16 + j of each), converted
-                // to bf16 in registers; B = Q rows with the same d permutation
+                // (iii) N^T += C_p^T Q_p^T over this wave's d tiles: A from two C tiles (rows
+                // 4 g16 + j of each), converted to bf16 in registers; B = Q rows with the same d
+                // permutation, shared by the VT column tiles
 #pragma unroll
-                for (int pt = 0; pt < DT / 2; ++pt) {
-                    const f32x4_t& c0 = Cacc[p * DT + 2 * pt];
-                    const f32x4_t& c1 = Cacc[p * DT + 2 * pt + 1];
-                    u32x4_t a;
-                    a[0] = pack_bf16x2((c0[0]), (c0[1]));
-                    a[1] = pack_bf16x2((c0[2]), (c0[3]));
-                    a[2] = pack_bf16x2((c1[0]), (c1[1]));
-                    a[3] = pack_bf16x2((c1[2]), (c1[3]));
-                    const int dl = 32 * pt + 4 * g16;
+                for (int pt = 0; pt < NQ / 2; ++pt) {
+                    const int q0 = p * NQ + 2 * pt;
+                    u32x4_t a[VT];
+#pragma unroll
+                    for (int vt = 0; vt < VT; ++vt) {
+                        const f32x4_t& c0 = Cacc[q0][vt];
+                        const f32x4_t& c1 = Cacc[q0 + 1][vt];
+                        a[vt][0] = pack_bf16x2(c0[0], c0[1]);
+                        a[vt][1] = pack_bf16x2(c0[2], c0[3]);
+                        a[vt][2] = pack_bf16x2(c1[0], c1[1]);
+                        a[vt][3] = pack_bf16x2(c1[2], c1[3]);
+                    }
+                    const int d0 = 16 * ((2 * pt) * DH + dh) + 4 * g16;       // within the block
+                    const int d1 = 16 * ((2 * pt + 1) * DH + dh) + 4 * g16;
 #pragma unroll
                     for (int T = 0; T < NTT; ++T) {
-                        const uint16_t* qrow = &Qs[(16 * T + l16) * QP + dl];
-                        const u32x2_t b0 = *reinterpret_cast<const u32x2_t*>(qrow);
-                        const u32x2_t b1 = *reinterpret_cast<const u32x2_t*>(qrow + 16);
-                        Nacc[T] = mfma16(a, cat(b0, b1), Nacc[T]);
+                        const uint16_t* qrow = &Qs[(16 * T + l16) * QP];
+                        const u32x2_t b0 = *reinterpret_cast<const u32x2_t*>(qrow + d0);
+                        const u32x2_t b1 = *reinterpret_cast<const u32x2_t*>(qrow + d1);
+                        const u32x4_t b = cat(b0, b1);
+#pragma unroll
+                        for (int vt = 0; vt < VT; ++vt) Nacc[vt][T] = mfma16(a[vt], b, Nacc[vt][T]);
                     }
                 }
             }
 
-            // (iv) C_p += K_p^T (w e^{-s} V): A = K read transposed, B = the scaled V operands
+            // (iv) C_p += K_p^T (w e^{-s} V): A = K read transposed (this wave's d tiles),
+            // B = V read transposed and scaled by the C-update key weights in registers (rebuilt
+            // per d block: a short live range is worth the extra transposed reads)
             if (c_scale != 1.0f) {
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) Cacc[p * DT + dt] *= c_scale;
+                for (int q = 0; q < NQ; ++q)
+#pragma unroll
+                    for (int vt = 0; vt < VT; ++vt) Cacc[p * NQ + q][vt] *= c_scale;
             }
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks) {
+                // lane (n = column vcol(vt) + l16, k group g16) holds tau = 32 ks + 8 g16 + 0..7
+                u32x4_t Vw[VT];
+                const float* wv = &Gc.wC[32 * ks + 8 * g16];
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * dt + tr_col];
-                    Cacc[p * DT + dt] = mfma16(cat(tr_read(kb), tr_read(kb + 4 * QP)), Vw[ks], Cacc[p * DT + dt]);
+                for (int vt = 0; vt < VT; ++vt) {
+                    const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
+                    const u32x4_t raw = cat(tr_read(vb), tr_read(vb + 4 * VP));
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        Vw[vt][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
+                }
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * (q * DH + dh) + tr_col];
+                    const u32x4_t a = cat(tr_read(kb), tr_read(kb + 4 * QP));
+#pragma unroll
+                    for (int vt = 0; vt < VT; ++vt)
+                        Cacc[p * NQ + q][vt] = mfma16(a, Vw[vt], Cacc[p * NQ + q][vt]);
                 }
             }
             // n_p = decay n_p + K_p^T w: A = w as bf16 hi / lo rows, B = K read transposed
@@ -611,7 +647,16 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const float other = __shfl_down(dqacc[j], 1, 64);
-                if (wave < NTT && l16 == 0) S.dq[16 * wave + 4 * g16 + j] = dqacc[j] + other;
+                if (dq_wave && l16 == 0) S.dq[16 * dqt + 4 * g16 + j] = dqacc[j] + other;
+            }
+            // DH = 2: hand the partial read-out of the tau tiles the other d partition finishes
+            if constexpr (DH == 2) {
+#pragma unroll
+                for (int vt = 0; vt < VT; ++vt)
+#pragma unroll
+                    for (int T = 0; T < NTT; ++T)
+                        if ((T & 1) != dh)
+                            *reinterpret_cast<f32x4_t*>(&S.X[(((vg * VT + vt) * NTT + T) * 64 + lane) * 4]) = Nacc[vt][T];
             }
             if constexpr (CF::ST_ALIAS) __syncthreads();   // the last d block is fully read before S~ overwrites it
             // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums
@@ -650,25 +695,35 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
             }
             __syncthreads();
-            // (ii) N^T = interC * N^T + V^T S~^T, then h = N^T / max(|den|, floor)
+            // (ii) N^T = interC * N^T + V^T S~^T, then h = N^T / max(|den|, floor); with DH = 2 each
+            // d partition finishes the tau tiles T with T % 2 == dh, after adding the other's partial
 #pragma unroll
             for (int T = 0; T < NTT; ++T) {
+                if (DH == 2 && (T & 1) != dh) continue;
                 const int tau = 16 * T + l16;
                 float den = Gc.interN[tau] * S.dq[tau];
 #pragma unroll
                 for (int sb = 0; sb <= T; ++sb) den += S.rs[sb][tau];
                 const float hv = __builtin_amdgcn_rcpf(fmaxf(fabsf(den), Gc.floorv[tau]));
-                Nacc[T] *= Gc.interC[tau];
+                const float ic = Gc.interC[tau];
 #pragma unroll
-                for (int ks = 0; ks <= T / 2; ++ks) {
-                    const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vc + tr_col];
-                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&St[tau * SP + 32 * ks + 8 * g16]);
-                    Nacc[T] = mfma16(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, Nacc[T]);
+                for (int vt = 0; vt < VT; ++vt) {
+                    f32x4_t acc = Nacc[vt][T];
+                    if constexpr (DH == 2)
+                        acc += *reinterpret_cast<const f32x4_t*>(&S.X[(((vg * VT + vt) * NTT + T) * 64 + lane) * 4]);
+                    acc *= ic;
+#pragma unroll
+                    for (int ks = 0; ks <= T / 2; ++ks) {
+                        const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
+                        const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&St[tau * SP + 32 * ks + 8 * g16]);
+                        acc = mfma16(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, acc);
+                    }
+                    u32x2_t o;
+                    o[0] = pack_bf16x2(acc[0] * hv, acc[1] * hv);
+                    o[1] = pack_bf16x2(acc[2] * hv, acc[3] * hv);
+                    *reinterpret_cast<u32x2_t*>(A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + vcol(vt) +
+                                                4 * g16) = o;
                 }
-                u32x2_t o;
-                o[0] = pack_bf16x2(Nacc[T][0] * hv, Nacc[T][1] * hv);
-                o[1] = pack_bf16x2(Nacc[T][2] * hv, Nacc[T][3] * hv);
-                *reinterpret_cast<u32x2_t*>(A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + vc + 4 * g16) = o;
             }
         }
         s_off = s_new;
@@ -696,11 +751,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     }
     const float esc = expf(s_off);
 #pragma unroll
-    for (int t = 0; t < NCT; ++t) {
+    for (int t = 0; t < NDB * NQ; ++t) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int d = 16 * t + 4 * g16 + j;
-            Cout[static_cast<int64_t>(d) * kDV + v0 + vc + l16] = (Cacc[t][j]) * esc;
+        for (int vt = 0; vt < VT; ++vt) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int d = (t / NQ) * DB + 16 * ((t % NQ) * DH + dh) + 4 * g16 + j;
+                Cout[static_cast<int64_t>(d) * kDV + v0 + vcol(vt) + l16] = Cacc[t][vt][j] * esc;
+            }
         }
     }
     if (write_nm && tid < kDQK) {

@@ -107,9 +107,11 @@ struct Cfg {
     static constexpr int NDB = (L == 128) ? 4 : 2;  // d blocks staged per chunk
     static constexpr int DB = kDQK / NDB;           // 128 or 64
     static constexpr int DT = DB / 16;              // 16-row C tiles per d block
-    static constexpr int QP = DB + 8;               // row pitch (elements) of Q and K blocks
+    // row pitch (elements) of Q and K blocks: 288 bytes at L = 64 keeps the 16-byte row reads of 16
+    // consecutive rows free of bank conflicts (the L = 128 blocks keep 144 bytes for LDS space)
+    static constexpr int QP = (L == 64) ? DB + 16 : DB + 8;
     static constexpr int VP = kDVT + 8;             // row pitch of V
-    static constexpr int SP = L + 8;                // row pitch of S~
+    static constexpr int SP = (L == 64) ? L + 16 : L + 8;   // row pitch of S~ (160 bytes at L = 64)
     static constexpr int NB = L / 16;               // 16-wide blocks along the chunk
     static constexpr int QKE = L * QP;              // elements of one Q or K block buffer
     // L = 128: S~ lives in the second Q/K buffer set, which is free from the end of the
@@ -390,6 +392,11 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     const int vg = wave % NVG;                  // column group
     const int dh = wave / NVG;                  // d partition: tiles dt = q DH + dh of every d block
     auto vcol = [&](int vt) { return 16 * (vg * VT + vt); };   // first column of v tile vt
+    // d row of element j of accumulator tile t (see the entry state)
+    auto cdrow = [&](int t, int j) {
+        const int q = t % NQ;
+        return (t / NQ) * DB + 32 * ((q / 2) * DH + dh) + 8 * g16 + 4 * (q % 2) + j;
+    };
     const bool gate_wave = (wave == kGateWave);
     uint16_t* const St = CF::ST_ALIAS ? &S.QK[1][0][0] : S.St_own;
     // Q n tile of this wave (>= NTT: none): with fewer tau tiles than waves, the waves after
@@ -416,7 +423,10 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
 
     // ---- entry state ------------------------------------------------------------------------
-    // Cacc[p NQ + q][vt] lane holds C[p DB + 16 (q DH + dh) + 4 g16 + j][vcol(vt) + l16], j = 0..3
+    // C tiles come in pairs over 32 consecutive d: in pair pp of a d block, tile e (0, 1) holds the d
+    // with (d mod 8) / 4 == e.  This wave owns pairs pp = pq DH + dh; Cacc[p NQ + 2 pq + e][vt] lane
+    // holds C[p DB + 32 pp + 8 g16 + 4 e + j][vcol(vt) + l16], j = 0..3, so the read-out (iii) finds
+    // the 8 d of its k slots contiguous in Q.
     f32x4_t Cacc[NDB * NQ][VT];
     const float* Cin = nullptr;
     const float* nin = nullptr;
@@ -439,7 +449,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         for (int vt = 0; vt < VT; ++vt) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int d = (t / NQ) * DB + 16 * ((t % NQ) * DH + dh) + 4 * g16 + j;
+                const int d = cdrow(t, j);
                 Cacc[t][vt][j] = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + vcol(vt) + l16] : 0.0f;
             }
         }
@@ -553,9 +563,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                         dqacc = mfma16(*reinterpret_cast<const u32x4_t*>(qa + 32 * ks), nbv, dqacc);
                     }
                 }
-                // (iii) N^T += C_p^T Q_p^T over this wave's d tiles: A from two C tiles (rows
-                // 4 g16 + j of each), converted to bf16 in registers; B = Q rows with the same d
-                // permutation, shared by the VT column tiles
+                // (iii) N^T += C_p^T Q_p^T over this wave's tile pairs: A from the two C tiles of a
+                // pair (rows 4 g16 + j of each), converted to bf16 in registers, is k slot 8 g16 + i
+                // = d 32 pp + 8 g16 + i; B = 16 bytes of a Q row, shared by the VT column tiles
 #pragma unroll
                 for (int pt = 0; pt < NQ / 2; ++pt) {
                     const int q0 = p * NQ + 2 * pt;
@@ -569,14 +579,10 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                         a[vt][2] = pack_bf16x2(c1[0], c1[1]);
                         a[vt][3] = pack_bf16x2(c1[2], c1[3]);
                     }
-                    const int d0 = 16 * ((2 * pt) * DH + dh) + 4 * g16;       // within the block
-                    const int d1 = 16 * ((2 * pt + 1) * DH + dh) + 4 * g16;
+                    const int dq0 = 32 * (pt * DH + dh) + 8 * g16;   // within the block
 #pragma unroll
                     for (int T = 0; T < NTT; ++T) {
-                        const uint16_t* qrow = &Qs[(16 * T + l16) * QP];
-                        const u32x2_t b0 = *reinterpret_cast<const u32x2_t*>(qrow + d0);
-                        const u32x2_t b1 = *reinterpret_cast<const u32x2_t*>(qrow + d1);
-                        const u32x4_t b = cat(b0, b1);
+                        const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&Qs[(16 * T + l16) * QP + dq0]);
 #pragma unroll
                         for (int vt = 0; vt < VT; ++vt) Nacc[vt][T] = mfma16(a[vt], b, Nacc[vt][T]);
                     }
@@ -607,7 +613,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 }
 #pragma unroll
                 for (int q = 0; q < NQ; ++q) {
-                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * (q * DH + dh) + tr_col];
+                    // tile (pair q / 2, half q % 2): columns 32 pp + 8 (l16 & 3) + 4 (q % 2) + 0..3
+                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * ((q / 2) * DH + dh) + 2 * tr_col + 4 * (q % 2)];
                     const u32x4_t a = cat(tr_read(kb), tr_read(kb + 4 * QP));
 #pragma unroll
                     for (int vt = 0; vt < VT; ++vt)
@@ -756,7 +763,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         for (int vt = 0; vt < VT; ++vt) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int d = (t / NQ) * DB + 16 * ((t % NQ) * DH + dh) + 4 * g16 + j;
+                const int d = cdrow(t, j);
                 Cout[static_cast<int64_t>(d) * kDV + v0 + vcol(vt) + l16] = Cacc[t][vt][j] * esc;
             }
         }
@@ -784,24 +791,39 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
             cur = reinterpret_cast<const float4*>(n0 + static_cast<int64_t>(s) * kDQK)[e4 - kDQK * kDV / 4];
         }
     }
-    for (int gg = 0; gg < G - 1; ++gg) {
-        float* slot = base + static_cast<int64_t>(gg) * kSlotFloats;
-        const float m_loc = slot[kDQK * kDV + kDQK];
-        const float gsum = slot[kDQK * kDV + kDQK + 1];
-        const float m_new = fmaxf(gsum + m_in, m_loc);
-        const float a = expf(gsum + m_in - m_new);
-        const float b = expf(m_loc - m_new);
-        if (e4 < kE4) {
-            float4* p4 = reinterpret_cast<float4*>(slot) + e4;
-            const float4 loc = *p4;
-            cur.x = a * cur.x + b * loc.x;
-            cur.y = a * cur.y + b * loc.y;
-            cur.z = a * cur.z + b * loc.z;
-            cur.w = a * cur.w + b * loc.w;
-            *p4 = cur;
+    // slots in batches: all loads of a batch are issued before its dependent chain of updates
+    constexpr int kBatch = 8;
+    for (int g0 = 0; g0 < G - 1; g0 += kBatch) {
+        const int nbat = min(kBatch, G - 1 - g0);
+        float4 loc[kBatch];
+        float mloc[kBatch], gs[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (u < nbat) {
+                const float* slot = base + static_cast<int64_t>(g0 + u) * kSlotFloats;
+                mloc[u] = slot[kDQK * kDV + kDQK];
+                gs[u] = slot[kDQK * kDV + kDQK + 1];
+                if (e4 < kE4) loc[u] = reinterpret_cast<const float4*>(slot)[e4];
+            }
         }
-        if (blockIdx.x == 0 && threadIdx.x == 0) slot[kDQK * kDV + kDQK + 2] = m_new;
-        m_in = m_new;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (u < nbat) {
+                float* slot = base + static_cast<int64_t>(g0 + u) * kSlotFloats;
+                const float m_new = fmaxf(gs[u] + m_in, mloc[u]);
+                const float a = expf(gs[u] + m_in - m_new);
+                const float b = expf(mloc[u] - m_new);
+                if (e4 < kE4) {
+                    cur.x = a * cur.x + b * loc[u].x;
+                    cur.y = a * cur.y + b * loc[u].y;
+                    cur.z = a * cur.z + b * loc[u].z;
+                    cur.w = a * cur.w + b * loc[u].w;
+                    reinterpret_cast<float4*>(slot)[e4] = cur;
+                }
+                if (blockIdx.x == 0 && threadIdx.x == 0) slot[kDQK * kDV + kDQK + 2] = m_new;
+                m_in = m_new;
+            }
+        }
     }
 }
 

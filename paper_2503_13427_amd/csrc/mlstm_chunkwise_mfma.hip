@@ -129,7 +129,7 @@ struct Cfg {
 
 // Per-chunk gate quantities, written one chunk ahead by the gate wave.
 template <int L>
-struct GateBuf {
+struct alignas(16) GateBuf {
     float x2[L];        // (i~ - b) * log2 e
     float M2[L];        // M * log2 e
     float interC[L];    // exp(m_prev - M + s) / sqrt(DQK): scale of C_acc^T Q^T
@@ -149,7 +149,9 @@ struct Smem {
     uint16_t nb[2][2][kDQK];                       // normaliser as bf16 hi / lo rows, double-buffered
     float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
     float dq[L];                                   // Q n_{k-1} (unscaled q)
-    float rs[L / 16][L];                           // row sums of S~ per 16-wide sigma block
+    // row sums of S~: L = 64 keeps one partial per (sigma block, tau, sigma quarter) so no
+    // cross-lane reduction is needed; L = 128 (no LDS to spare) reduces over the quarters first
+    float rs[L / 16][L][L == 64 ? 4 : 1];
     GateBuf<L> G[2];                               // by chunk parity
     // partial read-outs exchanged between the two d partitions of a column group (DH = 2):
     // [column group][v tile][tau tile][lane] as float4
@@ -666,7 +668,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                             *reinterpret_cast<f32x4_t*>(&S.X[(((vg * VT + vt) * NTT + T) * 64 + lane) * 4]) = Nacc[vt][T];
             }
             if constexpr (CF::ST_ALIAS) __syncthreads();   // the last d block is fully read before S~ overwrites it
-            // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums
+            // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums (fp32, before the
+            // bf16 rounding); branch-free, one 16-byte read of the four sigma exponents per lane
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
                 const int t = wave + kWaves * i;
@@ -676,23 +679,27 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     const int sb = rem;
                     const int tau = 16 * tb + l16;
                     const float Mt = Gc.M2[tau];
+                    const f32x4_t xs = *reinterpret_cast<const f32x4_t*>(&Gc.x2[16 * sb + 4 * g16]);
                     float vals[4];
                     float rsum = 0.f;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const int sig = 16 * sb + 4 * g16 + j;
-                        float val = 0.f;
-                        if (sig <= tau) val = Sacc[i][j] * kQScale * fast_exp2(Gc.x2[sig] - Mt);
-                        vals[j] = val;
-                        rsum += val;
+                        const float val = Sacc[i][j] * kQScale * fast_exp2(xs[j] - Mt);
+                        vals[j] = (sig <= tau) ? val : 0.f;
+                        rsum += vals[j];
                     }
                     u32x2_t o;
                     o[0] = pack_bf16x2(vals[0], vals[1]);
                     o[1] = pack_bf16x2(vals[2], vals[3]);
                     *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
-                    rsum += __shfl_xor(rsum, 16, 64);
-                    rsum += __shfl_xor(rsum, 32, 64);
-                    if (g16 == 0) S.rs[sb][tau] = rsum;
+                    if constexpr (L == 64) {
+                        S.rs[sb][tau][g16] = rsum;
+                    } else {
+                        rsum += __shfl_xor(rsum, 16, 64);
+                        rsum += __shfl_xor(rsum, 32, 64);
+                        if (g16 == 0) S.rs[sb][tau][0] = rsum;
+                    }
                 }
             }
             // zero the masked 16x16 tiles (sigma block T+1, tau block T) for even T: the k steps
@@ -710,7 +717,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 const int tau = 16 * T + l16;
                 float den = Gc.interN[tau] * S.dq[tau];
 #pragma unroll
-                for (int sb = 0; sb <= T; ++sb) den += S.rs[sb][tau];
+                for (int sb = 0; sb <= T; ++sb) {
+                    if constexpr (L == 64) {
+                        const f32x4_t r4 = *reinterpret_cast<const f32x4_t*>(&S.rs[sb][tau][0]);
+                        den += (r4[0] + r4[1]) + (r4[2] + r4[3]);
+                    } else {
+                        den += S.rs[sb][tau][0];
+                    }
+                }
                 const float hv = __builtin_amdgcn_rcpf(fmaxf(fabsf(den), Gc.floorv[tau]));
                 const float ic = Gc.interC[tau];
 #pragma unroll

@@ -167,9 +167,12 @@ struct QKRegs {
     u32x4_t q[N];
     u32x4_t k[N];
 };
+// V is staged in VPARTS parts (two at L = 128, whose four d blocks leave time for it) so
+// that fewer registers hold it at once.
 template <int L>
 struct VRegs {
-    static constexpr int N = (L * kDVT / 8) / kThreads;
+    static constexpr int PARTS = (Cfg<L>::NDB >= 3) ? 2 : 1;
+    static constexpr int N = (L * kDVT / 8) / kThreads / PARTS;   // pieces per thread per part
     u32x4_t v[N];
 };
 
@@ -217,19 +220,19 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
     }
 }
 template <int L>
-__device__ __forceinline__ void load_v(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int tid) {
+__device__ __forceinline__ void load_v(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int tid, int part) {
     const uint32_t soff = static_cast<uint32_t>(t0) * (kDV * 2) + v0 * 2;
 #pragma unroll
     for (int i = 0; i < VRegs<L>::N; ++i) {
-        const int item = tid + i * kThreads;
+        const int item = tid + (part * VRegs<L>::N + i) * kThreads;
         r.v[i] = bload128(R.v, (item / 16) * (kDV * 2) + 16 * (item % 16), soff);
     }
 }
 template <int L>
-__device__ __forceinline__ void store_v(uint16_t* Vd, const VRegs<L>& r, int tid) {
+__device__ __forceinline__ void store_v(uint16_t* Vd, const VRegs<L>& r, int tid, int part) {
 #pragma unroll
     for (int i = 0; i < VRegs<L>::N; ++i) {
-        const int item = tid + i * kThreads;
+        const int item = tid + (part * VRegs<L>::N + i) * kThreads;
         *reinterpret_cast<u32x4_t*>(&Vd[(item / 16) * Cfg<L>::VP + 8 * (item % 16)]) = r.v[i];
     }
 }
@@ -363,11 +366,11 @@ struct ChunkKernelArgs {
 // workspace slot of (sequence s, segment g): C [DQK*DV], n [DQK], then m_loc, gsum, m_in, pad
 constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
 
-// Staging order (one Q/K block and one V chunk in registers at a time): block 0 of a
-// chunk and its V are stored during the previous chunk (before its last d block), block 1
-// at the top of the chunk, block p + 1 (p >= 1) at the barrier that opens block p.  The V
-// load is issued at the top of the previous chunk, so its registers are free from the last
-// d block on.
+// Staging order (one Q/K block and one part of a V chunk in registers at a time): block 0
+// of a chunk is stored during the previous chunk (at the barrier that opens its last d
+// block), block 1 at the top of the chunk, block p + 1 (p >= 1) at the barrier that opens
+// block p.  The next chunk's V is loaded from the top of a chunk on, part k stored at the
+// barrier that opens d block k + 1.
 template <int L, bool FULL>
 __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
@@ -474,13 +477,16 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     if (c_begin < c_end) {
         const int t0 = c_begin * L;
         load_qk<L, FULL>(rqk, P, t0, 0, tid);
-        load_v<L>(rv, P, t0, v0, tid);
         if (gate_wave) {
             load_gates<L>(gi, gf, P, t0, lane);
             gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, g_sum, lane);
         }
         store_qk<L, FULL>(S.QK[0][0], S.QK[0][1], rqk, tid);
-        store_v<L>(S.Vs[c_begin & 1], rv, tid);
+#pragma unroll
+        for (int part = 0; part < VRegs<L>::PARTS; ++part) {
+            load_v<L>(rv, P, t0, v0, tid, part);
+            store_v<L>(S.Vs[c_begin & 1], rv, tid, part);
+        }
         load_qk<L, FULL>(rqk, P, t0, 1, tid);
     }
 
@@ -499,8 +505,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         if constexpr (NDB > 2) load_qk<L, FULL>(rqk, P, t0, 2, tid);
         else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
         if (gate_wave && c + 1 < c_end) load_gates<L>(gi, gf, P, t0 + L, lane);
-        // V of the next chunk, stored at the barrier that opens this chunk's last d block
-        if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid);
+        // V of the next chunk: part 0 now, part k stored at the barrier that opens d block k + 1
+        if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid, 0);
         const float decay_n = Gc.scal[0];
         const float m_next = Gc.scal[1];
         const float s_new = Gc.scal[2];
@@ -530,10 +536,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     if (p + 2 < NDB) load_qk<L, FULL>(rqk, P, t0, p + 2, tid);
                     else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
                 } else if (c + 1 < c_end) {
-                    // block 0 and V of the next chunk
+                    // block 0 of the next chunk
                     store_qk<L, FULL>(S.QK[0][0], S.QK[0][1], rqk, tid);
                     load_qk<L, FULL>(rqk, P, t0 + L, 1, tid);
-                    store_v<L>(S.Vs[par ^ 1], rv, tid);
+                }
+                // V of the next chunk, part p - 1 (its buffer was last read by the previous chunk)
+                if (p <= VRegs<L>::PARTS && c + 1 < c_end) {
+                    store_v<L>(S.Vs[par ^ 1], rv, tid, p - 1);
+                    if (p < VRegs<L>::PARTS) load_v<L>(rv, P, t0 + L, v0, tid, p);
                 }
             }
             if constexpr (FULL) {

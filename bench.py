@@ -282,8 +282,8 @@ def main():
         line["ms_per_step"] = hp["us_per_call"] / 1e3
         line["roofline"] = {"bound": "mfma", "achieved": hp["tflops"], "peak": acc.PEAK_BF16_MFMA_TFLOPS,
                             "unit": "TFLOP/s", "frac": hp["mfma_frac"], "traffic": measured_traffic(),
-                            "kernel": "mlstm_chunkwise_fwd call: chunk_mfma_kernel<64,false> + combine_kernel + "
-                                      "chunk_mfma_kernel<64,true> (segment schedule); achieved and traffic are per "
+                            "kernel": "mlstm_chunkwise_fwd call: local_state_kernel + combine_kernel + "
+                                      "chunk_mfma_kernel<64> (segment schedule); achieved and traffic are per "
                                       "call, over the call's duration",
                             "flops_per_call": hp["flops_per_call"], "hbm_frac": hp["hbm_frac"]}
         line["prefill"] = hp

@@ -42,21 +42,23 @@
 //
 // Work decomposition.  One workgroup of 8 waves (two per SIMD, so one wave's
 // LDS and memory waits are covered by the other's MFMAs) owns one (sequence,
-// 128-column dv tile, segment) and walks the segment's chunks in order.  Wave w
-// owns the 256 x 16 slice C[:, 16w:16w+16] in its accumulators (64 registers) for
-// the whole segment; S~, Q n and the gates are computed once per workgroup.
+// 128-column dv tile, segment) and walks the segment's chunks in order.  Each wave
+// owns 64 accumulator registers of C for the whole segment (L = 64: a 128 x 32 slice,
+// one of two d partitions of a 32-column group; L = 128: a 256 x 16 slice); S~, Q n
+// and the gates are computed once per workgroup.
 // Q and K are staged in d blocks (two of 128 for L = 64, four of 64 for L = 128);
 // the next block (and the next chunk's V and gates) is prefetched into registers
 // while the current block is multiplied.  The four dv tiles of a (sequence,
 // segment) are dispatched consecutively onto one XCD so their shared Q/K reads
 // hit one L2.
 //
-// Segment-parallel schedule (optional workspace).  With G segments per
-// sequence: (1) the LOCAL variant computes each of the first G-1 segments' state
-// from an empty state (C = 0, n = 0, m = -inf) -- gates, the C and n updates only;
-// (2) a combine kernel scans those local states into each segment's entry state,
-// m_in' = max(gsum + m_in, m_loc), C_in' = e^{gsum + m_in - m_in'} C_in + e^{m_loc - m_in'} C_loc;
-// (3) the FULL variant runs every segment from its entry state.
+// Segment-parallel schedule (optional workspace).  With G segments per sequence:
+// (1) local_state_kernel computes the state of each of the first G-1 segments (split
+// into R sub-segments of at most kLocMax tokens) from an empty state, as one weighted
+// contraction over its tokens; (2) a combine kernel scans those local states into each
+// segment's entry state, m_in' = max(gsum + m_in, m_loc),
+// C_in' = e^{gsum + m_in - m_in'} C_in + e^{m_loc - m_in'} C_loc; (3) the chunkwise
+// kernel runs every segment from its entry state.
 #include "device_common.h"
 #include "launch.h"
 
@@ -196,7 +198,7 @@ __device__ __forceinline__ float bloadf(__amdgpu_buffer_rsrc_t r, uint32_t voff,
 }
 
 // Q and K rows are 512 bytes, V rows 1024 bytes; offsets are in bytes.
-template <int L, bool FULL>
+template <int L>
 __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, int p, int tid) {
     constexpr int DB = Cfg<L>::DB, PR = DB / 8;   // 16-byte pieces per row
     const uint32_t soff = static_cast<uint32_t>(t0) * (kDQK * 2) + p * (DB * 2);
@@ -204,18 +206,18 @@ __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, 
     for (int i = 0; i < QKRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
         const uint32_t voff = (item / PR) * (kDQK * 2) + 16 * (item % PR);
-        if constexpr (FULL) r.q[i] = bload128(R.q, voff, soff);
+        r.q[i] = bload128(R.q, voff, soff);
         r.k[i] = bload128(R.k, voff, soff);
     }
 }
-template <int L, bool FULL>
+template <int L>
 __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKRegs<L>& r, int tid) {
     constexpr int PR = Cfg<L>::DB / 8, QP = Cfg<L>::QP;
 #pragma unroll
     for (int i = 0; i < QKRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
         const int off = (item / PR) * QP + 8 * (item % PR);
-        if constexpr (FULL) *reinterpret_cast<u32x4_t*>(&Qd[off]) = r.q[i];
+        *reinterpret_cast<u32x4_t*>(&Qd[off]) = r.q[i];
         *reinterpret_cast<u32x4_t*>(&Kd[off]) = r.k[i];
     }
 }
@@ -285,10 +287,10 @@ __device__ __forceinline__ float flogsig(float x) {
 
 // Gate phase of one chunk (run by one wave): in-chunk prefix sums and maxima, the max
 // state, the lazy C scale, and every per-row scale of the chunk.  m_prev and s_cur
-// carry the max state and the lazy log-scale from chunk to chunk; gsum accumulates b_L.
+// carry the max state and the lazy log-scale from chunk to chunk.
 template <int L>
 __device__ __forceinline__ void gate_phase(GateBuf<L>& Gb, const float (&gi)[2], const float (&gf)[2], float& m_prev,
-                                           float& s_cur, float& gsum, int lane) {
+                                           float& s_cur, int lane) {
     const float b = wave_incl_sum(flogsig(gf[0]));
     const float x = gi[0] - b;
     const float p = wave_incl_max(x);
@@ -301,7 +303,7 @@ __device__ __forceinline__ void gate_phase(GateBuf<L>& Gb, const float (&gi)[2],
     const float pL = lane63(L == 128 ? p2 : p);
     const float bL = lane63(L == 128 ? b2 : b);
     const float ML = fmaxf(m_prev, pL);
-    // an empty state (m = -inf, local-state pass only) has nothing to decay
+    // an empty state (m = -inf) has nothing to decay
     const bool empty = (m_prev == -INFINITY);
     const float dlog = empty ? 0.0f : m_prev - ML;
     const float s_try = s_cur + dlog;
@@ -332,7 +334,6 @@ __device__ __forceinline__ void gate_phase(GateBuf<L>& Gb, const float (&gi)[2],
     }
     m_prev = m_next;
     s_cur = s_new;
-    gsum += bL;
 }
 
 // XCD-aware block order: the hardware deals consecutive workgroups round-robin to
@@ -356,6 +357,8 @@ struct ChunkKernelArgs {
     float* ws;         // segment slots (NULL when G == 1)
     int T;
     int G;             // segments per sequence
+    int R;             // local sub-segments per segment; segment g >= 1 enters from slot g R - 1
+    int NS;            // local slots per sequence, (G - 1) R
     int seg_chunks;    // chunks per segment (last may be shorter)
     uint16_t* h;
     float* CT;
@@ -363,7 +366,8 @@ struct ChunkKernelArgs {
     float* mT;
 };
 
-// workspace slot of (sequence s, segment g): C [DQK*DV], n [DQK], then m_loc, gsum, m_in, pad
+// workspace slot of (sequence s, local sub-segment j): C [DQK*DV], n [DQK], then m_loc, gsum
+// (sum of logsig over the sub-segment), m_in (entry max state, in segment-boundary slots), pad
 constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
 
 // Staging order (one Q/K block and one part of a V chunk in registers at a time): block 0
@@ -371,7 +375,7 @@ constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
 // block), block 1 at the top of the chunk, block p + 1 (p >= 1) at the barrier that opens
 // block p.  The next chunk's V is loaded from the top of a chunk on, part k stored at the
 // barrier that opens d block k + 1.
-template <int L, bool FULL>
+template <int L>
 __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     Smem<L>& S = *reinterpret_cast<Smem<L>*>(smem_raw);
@@ -412,9 +416,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     const int wi = work_index();
     const int tile = wi % kNTile;
     const int sg = wi / kNTile;
-    const int G_run = FULL ? A.G : A.G - 1;
-    const int g = sg % G_run;
-    const int s = sg / G_run;
+    const int g = sg % A.G;
+    const int s = sg / A.G;
     const int v0 = tile * kDVT;
     const int nc_total = A.T / L;
     const int c_begin = g * A.seg_chunks;
@@ -436,14 +439,12 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     const float* Cin = nullptr;
     const float* nin = nullptr;
     float m_prev;
-    if (!FULL) {
-        m_prev = -INFINITY;
-    } else if (g == 0) {
+    if (g == 0) {
         Cin = A.C0 ? A.C0 + static_cast<int64_t>(s) * kDQK * kDV : nullptr;
         nin = A.n0 ? A.n0 + static_cast<int64_t>(s) * kDQK : nullptr;
         m_prev = A.m0 ? A.m0[s] : 0.0f;
     } else {
-        const float* slot = A.ws + (static_cast<int64_t>(s) * (A.G - 1) + (g - 1)) * kSlotFloats;
+        const float* slot = A.ws + (static_cast<int64_t>(s) * A.NS + g * A.R - 1) * kSlotFloats;
         Cin = slot;
         nin = slot + kDQK * kDV;
         m_prev = slot[kDQK * kDV + kDQK + 2];
@@ -469,25 +470,25 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     float s_off = 0.0f;   // C = C_acc * e^{s_off}
 
     // gate wave state: max state and lazy scale after the last chunk whose gates it computed
-    float g_m = m_prev, g_s = 0.0f, g_sum = 0.0f;
+    float g_m = m_prev, g_s = 0.0f;
     float gi[2] = {0.f, 0.f}, gf[2] = {0.f, 0.f};
 
     QKRegs<L> rqk;
     VRegs<L> rv;
     if (c_begin < c_end) {
         const int t0 = c_begin * L;
-        load_qk<L, FULL>(rqk, P, t0, 0, tid);
+        load_qk<L>(rqk, P, t0, 0, tid);
         if (gate_wave) {
             load_gates<L>(gi, gf, P, t0, lane);
-            gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, g_sum, lane);
+            gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane);
         }
-        store_qk<L, FULL>(S.QK[0][0], S.QK[0][1], rqk, tid);
+        store_qk<L>(S.QK[0][0], S.QK[0][1], rqk, tid);
 #pragma unroll
         for (int part = 0; part < VRegs<L>::PARTS; ++part) {
             load_v<L>(rv, P, t0, v0, tid, part);
             store_v<L>(S.Vs[c_begin & 1], rv, tid, part);
         }
-        load_qk<L, FULL>(rqk, P, t0, 1, tid);
+        load_qk<L>(rqk, P, t0, 1, tid);
     }
 
     f32x4_t Nacc[VT][NTT];
@@ -501,9 +502,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         const GateBuf<L>& Gc = S.G[par];
         __syncthreads();   // the previous chunk is done; block 0, V and the gates of this chunk are visible
         // block 1 -> set 1 (its readers in the previous chunk, the last d block and S~, are done)
-        store_qk<L, FULL>(S.QK[1][0], S.QK[1][1], rqk, tid);
-        if constexpr (NDB > 2) load_qk<L, FULL>(rqk, P, t0, 2, tid);
-        else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
+        store_qk<L>(S.QK[1][0], S.QK[1][1], rqk, tid);
+        if constexpr (NDB > 2) load_qk<L>(rqk, P, t0, 2, tid);
+        else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid);
         if (gate_wave && c + 1 < c_end) load_gates<L>(gi, gf, P, t0 + L, lane);
         // V of the next chunk: part 0 now, part k stored at the barrier that opens d block k + 1
         if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid, 0);
@@ -515,15 +516,13 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         float* n_new = S.n[cur ^ 1];
         const uint16_t* Vc = S.Vs[par];
 
-        if constexpr (FULL) {
 #pragma unroll
-            for (int vt = 0; vt < VT; ++vt)
+        for (int vt = 0; vt < VT; ++vt)
 #pragma unroll
-                for (int T = 0; T < NTT; ++T) Nacc[vt][T] = f32x4_t{};
+            for (int T = 0; T < NTT; ++T) Nacc[vt][T] = f32x4_t{};
 #pragma unroll
-            for (int i = 0; i < MAXT; ++i) Sacc[i] = f32x4_t{};
-            dqacc = f32x4_t{};
-        }
+        for (int i = 0; i < MAXT; ++i) Sacc[i] = f32x4_t{};
+        dqacc = f32x4_t{};
 
 #pragma unroll
         for (int p = 0; p < NDB; ++p) {
@@ -532,13 +531,13 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             if (p > 0) {
                 __syncthreads();   // block p visible, block p - 1 fully read
                 if (p + 1 < NDB) {
-                    store_qk<L, FULL>(S.QK[(p + 1) & 1][0], S.QK[(p + 1) & 1][1], rqk, tid);
-                    if (p + 2 < NDB) load_qk<L, FULL>(rqk, P, t0, p + 2, tid);
-                    else if (c + 1 < c_end) load_qk<L, FULL>(rqk, P, t0 + L, 0, tid);
+                    store_qk<L>(S.QK[(p + 1) & 1][0], S.QK[(p + 1) & 1][1], rqk, tid);
+                    if (p + 2 < NDB) load_qk<L>(rqk, P, t0, p + 2, tid);
+                    else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid);
                 } else if (c + 1 < c_end) {
                     // block 0 of the next chunk
-                    store_qk<L, FULL>(S.QK[0][0], S.QK[0][1], rqk, tid);
-                    load_qk<L, FULL>(rqk, P, t0 + L, 1, tid);
+                    store_qk<L>(S.QK[0][0], S.QK[0][1], rqk, tid);
+                    load_qk<L>(rqk, P, t0 + L, 1, tid);
                 }
                 // V of the next chunk, part p - 1 (its buffer was last read by the previous chunk)
                 if (p <= VRegs<L>::PARTS && c + 1 < c_end) {
@@ -546,58 +545,56 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     if (p < VRegs<L>::PARTS) load_v<L>(rv, P, t0 + L, v0, tid, p);
                 }
             }
-            if constexpr (FULL) {
-                // (i) S^T += K_p Q_p^T on this wave's causal tiles (L = 128: a fixed tile count per
-                // wave; the surplus tiles repeat the last one and are not used)
+            // (i) S^T += K_p Q_p^T on this wave's causal tiles (L = 128: a fixed tile count per
+            // wave; the surplus tiles repeat the last one and are not used)
 #pragma unroll
-                for (int i = 0; i < MAXT; ++i) {
-                    const int t = (L == 128) ? min(wave + kWaves * i, NT_S - 1) : wave + kWaves * i;
-                    if (L == 128 || t < NT_S) {
-                        int tb = 0, rem = t;
-                        while (rem > tb) { rem -= tb + 1; ++tb; }
-                        const int sb = rem;
-                        const uint16_t* ka = &Ks[(16 * sb + l16) * QP + 8 * g16];
-                        const uint16_t* qb = &Qs[(16 * tb + l16) * QP + 8 * g16];
+            for (int i = 0; i < MAXT; ++i) {
+                const int t = (L == 128) ? min(wave + kWaves * i, NT_S - 1) : wave + kWaves * i;
+                if (L == 128 || t < NT_S) {
+                    int tb = 0, rem = t;
+                    while (rem > tb) { rem -= tb + 1; ++tb; }
+                    const int sb = rem;
+                    const uint16_t* ka = &Ks[(16 * sb + l16) * QP + 8 * g16];
+                    const uint16_t* qb = &Qs[(16 * tb + l16) * QP + 8 * g16];
 #pragma unroll
-                        for (int ks = 0; ks < DB / 32; ++ks)
-                            Sacc[i] = mfma16(*reinterpret_cast<const u32x4_t*>(ka + 32 * ks),
-                                             *reinterpret_cast<const u32x4_t*>(qb + 32 * ks), Sacc[i]);
-                    }
+                    for (int ks = 0; ks < DB / 32; ++ks)
+                        Sacc[i] = mfma16(*reinterpret_cast<const u32x4_t*>(ka + 32 * ks),
+                                         *reinterpret_cast<const u32x4_t*>(qb + 32 * ks), Sacc[i]);
                 }
-                // Q n_{k-1} over this d block: A = Q rows, B = n as bf16 hi / lo columns
-                if (dq_wave) {
-                    const uint16_t* qa = &Qs[(16 * dqt + l16) * QP + 8 * g16];
-                    const uint16_t* nbp = &S.nb[cur][l16 & 1][p * DB + 8 * g16];
+            }
+            // Q n_{k-1} over this d block: A = Q rows, B = n as bf16 hi / lo columns
+            if (dq_wave) {
+                const uint16_t* qa = &Qs[(16 * dqt + l16) * QP + 8 * g16];
+                const uint16_t* nbp = &S.nb[cur][l16 & 1][p * DB + 8 * g16];
 #pragma unroll
-                    for (int ks = 0; ks < DB / 32; ++ks) {
-                        const u32x4_t nbv = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(nbp + 32 * ks)
-                                                      : u32x4_t{0u, 0u, 0u, 0u};
-                        dqacc = mfma16(*reinterpret_cast<const u32x4_t*>(qa + 32 * ks), nbv, dqacc);
-                    }
+                for (int ks = 0; ks < DB / 32; ++ks) {
+                    const u32x4_t nbv = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(nbp + 32 * ks)
+                                                  : u32x4_t{0u, 0u, 0u, 0u};
+                    dqacc = mfma16(*reinterpret_cast<const u32x4_t*>(qa + 32 * ks), nbv, dqacc);
                 }
-                // (iii) N^T += C_p^T Q_p^T over this wave's tile pairs: A from the two C tiles of a
-                // pair (rows 4 g16 + j of each), converted to bf16 in registers, is k slot 8 g16 + i
-                // = d 32 pp + 8 g16 + i; B = 16 bytes of a Q row, shared by the VT column tiles
+            }
+            // (iii) N^T += C_p^T Q_p^T over this wave's tile pairs: A from the two C tiles of a
+            // pair (rows 4 g16 + j of each), converted to bf16 in registers, is k slot 8 g16 + i
+            // = d 32 pp + 8 g16 + i; B = 16 bytes of a Q row, shared by the VT column tiles
 #pragma unroll
-                for (int pt = 0; pt < NQ / 2; ++pt) {
-                    const int q0 = p * NQ + 2 * pt;
-                    u32x4_t a[VT];
+            for (int pt = 0; pt < NQ / 2; ++pt) {
+                const int q0 = p * NQ + 2 * pt;
+                u32x4_t a[VT];
 #pragma unroll
-                    for (int vt = 0; vt < VT; ++vt) {
-                        const f32x4_t& c0 = Cacc[q0][vt];
-                        const f32x4_t& c1 = Cacc[q0 + 1][vt];
-                        a[vt][0] = pack_bf16x2(c0[0], c0[1]);
-                        a[vt][1] = pack_bf16x2(c0[2], c0[3]);
-                        a[vt][2] = pack_bf16x2(c1[0], c1[1]);
-                        a[vt][3] = pack_bf16x2(c1[2], c1[3]);
-                    }
-                    const int dq0 = 32 * (pt * DH + dh) + 8 * g16;   // within the block
+                for (int vt = 0; vt < VT; ++vt) {
+                    const f32x4_t& c0 = Cacc[q0][vt];
+                    const f32x4_t& c1 = Cacc[q0 + 1][vt];
+                    a[vt][0] = pack_bf16x2(c0[0], c0[1]);
+                    a[vt][1] = pack_bf16x2(c0[2], c0[3]);
+                    a[vt][2] = pack_bf16x2(c1[0], c1[1]);
+                    a[vt][3] = pack_bf16x2(c1[2], c1[3]);
+                }
+                const int dq0 = 32 * (pt * DH + dh) + 8 * g16;   // within the block
 #pragma unroll
-                    for (int T = 0; T < NTT; ++T) {
-                        const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&Qs[(16 * T + l16) * QP + dq0]);
+                for (int T = 0; T < NTT; ++T) {
+                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&Qs[(16 * T + l16) * QP + dq0]);
 #pragma unroll
-                        for (int vt = 0; vt < VT; ++vt) Nacc[vt][T] = mfma16(a[vt], b, Nacc[vt][T]);
-                    }
+                    for (int vt = 0; vt < VT; ++vt) Nacc[vt][T] = mfma16(a[vt], b, Nacc[vt][T]);
                 }
             }
 
@@ -659,102 +656,100 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         }
 
         // gates of the next chunk, one chunk ahead
-        if (gate_wave && c + 1 < c_end) gate_phase<L>(S.G[par ^ 1], gi, gf, g_m, g_s, g_sum, lane);
+        if (gate_wave && c + 1 < c_end) gate_phase<L>(S.G[par ^ 1], gi, gf, g_m, g_s, lane);
 
-        if constexpr (FULL) {
-            // finish Q n: columns 0 and 1 of the 16x16 tile are lanes l16 = 0 and 1
+        // finish Q n: columns 0 and 1 of the 16x16 tile are lanes l16 = 0 and 1
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const float other = __shfl_down(dqacc[j], 1, 64);
-                if (dq_wave && l16 == 0) S.dq[16 * dqt + 4 * g16 + j] = dqacc[j] + other;
-            }
-            // DH = 2: hand the partial read-out of the tau tiles the other d partition finishes
-            if constexpr (DH == 2) {
+        for (int j = 0; j < 4; ++j) {
+            const float other = __shfl_down(dqacc[j], 1, 64);
+            if (dq_wave && l16 == 0) S.dq[16 * dqt + 4 * g16 + j] = dqacc[j] + other;
+        }
+        // DH = 2: hand the partial read-out of the tau tiles the other d partition finishes
+        if constexpr (DH == 2) {
 #pragma unroll
-                for (int vt = 0; vt < VT; ++vt)
+            for (int vt = 0; vt < VT; ++vt)
 #pragma unroll
-                    for (int T = 0; T < NTT; ++T)
-                        if ((T & 1) != dh)
-                            *reinterpret_cast<f32x4_t*>(&S.X[(((vg * VT + vt) * NTT + T) * 64 + lane) * 4]) = Nacc[vt][T];
-            }
-            if constexpr (CF::ST_ALIAS) __syncthreads();   // the last d block is fully read before S~ overwrites it
-            // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums (fp32, before the
-            // bf16 rounding); branch-free, one 16-byte read of the four sigma exponents per lane
+                for (int T = 0; T < NTT; ++T)
+                    if ((T & 1) != dh)
+                        *reinterpret_cast<f32x4_t*>(&S.X[(((vg * VT + vt) * NTT + T) * 64 + lane) * 4]) = Nacc[vt][T];
+        }
+        if constexpr (CF::ST_ALIAS) __syncthreads();   // the last d block is fully read before S~ overwrites it
+        // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums (fp32, before the
+        // bf16 rounding); branch-free, one 16-byte read of the four sigma exponents per lane
 #pragma unroll
-            for (int i = 0; i < MAXT; ++i) {
-                const int t = wave + kWaves * i;
-                if (t < NT_S) {
-                    int tb = 0, rem = t;
-                    while (rem > tb) { rem -= tb + 1; ++tb; }
-                    const int sb = rem;
-                    const int tau = 16 * tb + l16;
-                    const float Mt = Gc.M2[tau];
-                    const f32x4_t xs = *reinterpret_cast<const f32x4_t*>(&Gc.x2[16 * sb + 4 * g16]);
-                    float vals[4];
-                    float rsum = 0.f;
+        for (int i = 0; i < MAXT; ++i) {
+            const int t = wave + kWaves * i;
+            if (t < NT_S) {
+                int tb = 0, rem = t;
+                while (rem > tb) { rem -= tb + 1; ++tb; }
+                const int sb = rem;
+                const int tau = 16 * tb + l16;
+                const float Mt = Gc.M2[tau];
+                const f32x4_t xs = *reinterpret_cast<const f32x4_t*>(&Gc.x2[16 * sb + 4 * g16]);
+                float vals[4];
+                float rsum = 0.f;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int sig = 16 * sb + 4 * g16 + j;
-                        const float val = Sacc[i][j] * kQScale * fast_exp2(xs[j] - Mt);
-                        vals[j] = (sig <= tau) ? val : 0.f;
-                        rsum += vals[j];
-                    }
-                    u32x2_t o;
-                    o[0] = pack_bf16x2(vals[0], vals[1]);
-                    o[1] = pack_bf16x2(vals[2], vals[3]);
-                    *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
-                    if constexpr (L == 64) {
-                        S.rs[sb][tau][g16] = rsum;
-                    } else {
-                        rsum += __shfl_xor(rsum, 16, 64);
-                        rsum += __shfl_xor(rsum, 32, 64);
-                        if (g16 == 0) S.rs[sb][tau][0] = rsum;
-                    }
+                for (int j = 0; j < 4; ++j) {
+                    const int sig = 16 * sb + 4 * g16 + j;
+                    const float val = Sacc[i][j] * kQScale * fast_exp2(xs[j] - Mt);
+                    vals[j] = (sig <= tau) ? val : 0.f;
+                    rsum += vals[j];
+                }
+                u32x2_t o;
+                o[0] = pack_bf16x2(vals[0], vals[1]);
+                o[1] = pack_bf16x2(vals[2], vals[3]);
+                *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
+                if constexpr (L == 64) {
+                    S.rs[sb][tau][g16] = rsum;
+                } else {
+                    rsum += __shfl_xor(rsum, 16, 64);
+                    rsum += __shfl_xor(rsum, 32, 64);
+                    if (g16 == 0) S.rs[sb][tau][0] = rsum;
                 }
             }
-            // zero the masked 16x16 tiles (sigma block T+1, tau block T) for even T: the k steps
-            // of (ii) are 32 wide
-            for (int T = 2 * wave; T < NTT; T += 2 * kWaves) {
-                const int tau = 16 * T + l16;
-                *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
+        }
+        // zero the masked 16x16 tiles (sigma block T+1, tau block T) for even T: the k steps
+        // of (ii) are 32 wide
+        for (int T = 2 * wave; T < NTT; T += 2 * kWaves) {
+            const int tau = 16 * T + l16;
+            *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
+        }
+        __syncthreads();
+        // (ii) N^T = interC * N^T + V^T S~^T, then h = N^T / max(|den|, floor); with DH = 2 each
+        // d partition finishes the tau tiles T with T % 2 == dh, after adding the other's partial
+#pragma unroll
+        for (int T = 0; T < NTT; ++T) {
+            if (DH == 2 && (T & 1) != dh) continue;
+            const int tau = 16 * T + l16;
+            float den = Gc.interN[tau] * S.dq[tau];
+#pragma unroll
+            for (int sb = 0; sb <= T; ++sb) {
+                if constexpr (L == 64) {
+                    const f32x4_t r4 = *reinterpret_cast<const f32x4_t*>(&S.rs[sb][tau][0]);
+                    den += (r4[0] + r4[1]) + (r4[2] + r4[3]);
+                } else {
+                    den += S.rs[sb][tau][0];
+                }
             }
-            __syncthreads();
-            // (ii) N^T = interC * N^T + V^T S~^T, then h = N^T / max(|den|, floor); with DH = 2 each
-            // d partition finishes the tau tiles T with T % 2 == dh, after adding the other's partial
+            const float hv = __builtin_amdgcn_rcpf(fmaxf(fabsf(den), Gc.floorv[tau]));
+            const float ic = Gc.interC[tau];
 #pragma unroll
-            for (int T = 0; T < NTT; ++T) {
-                if (DH == 2 && (T & 1) != dh) continue;
-                const int tau = 16 * T + l16;
-                float den = Gc.interN[tau] * S.dq[tau];
+            for (int vt = 0; vt < VT; ++vt) {
+                f32x4_t acc = Nacc[vt][T];
+                if constexpr (DH == 2)
+                    acc += *reinterpret_cast<const f32x4_t*>(&S.X[(((vg * VT + vt) * NTT + T) * 64 + lane) * 4]);
+                acc *= ic;
 #pragma unroll
-                for (int sb = 0; sb <= T; ++sb) {
-                    if constexpr (L == 64) {
-                        const f32x4_t r4 = *reinterpret_cast<const f32x4_t*>(&S.rs[sb][tau][0]);
-                        den += (r4[0] + r4[1]) + (r4[2] + r4[3]);
-                    } else {
-                        den += S.rs[sb][tau][0];
-                    }
+                for (int ks = 0; ks <= T / 2; ++ks) {
+                    const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
+                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&St[tau * SP + 32 * ks + 8 * g16]);
+                    acc = mfma16(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, acc);
                 }
-                const float hv = __builtin_amdgcn_rcpf(fmaxf(fabsf(den), Gc.floorv[tau]));
-                const float ic = Gc.interC[tau];
-#pragma unroll
-                for (int vt = 0; vt < VT; ++vt) {
-                    f32x4_t acc = Nacc[vt][T];
-                    if constexpr (DH == 2)
-                        acc += *reinterpret_cast<const f32x4_t*>(&S.X[(((vg * VT + vt) * NTT + T) * 64 + lane) * 4]);
-                    acc *= ic;
-#pragma unroll
-                    for (int ks = 0; ks <= T / 2; ++ks) {
-                        const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
-                        const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&St[tau * SP + 32 * ks + 8 * g16]);
-                        acc = mfma16(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, acc);
-                    }
-                    u32x2_t o;
-                    o[0] = pack_bf16x2(acc[0] * hv, acc[1] * hv);
-                    o[1] = pack_bf16x2(acc[2] * hv, acc[3] * hv);
-                    *reinterpret_cast<u32x2_t*>(A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + vcol(vt) +
-                                                4 * g16) = o;
-                }
+                u32x2_t o;
+                o[0] = pack_bf16x2(acc[0] * hv, acc[1] * hv);
+                o[1] = pack_bf16x2(acc[2] * hv, acc[3] * hv);
+                *reinterpret_cast<u32x2_t*>(A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + vcol(vt) +
+                                            4 * g16) = o;
             }
         }
         s_off = s_new;
@@ -768,18 +763,10 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     float* nout;
     float* mout;
     const bool write_nm = (tile == 0);
-    if (FULL) {
-        if (g != A.G - 1) return;
-        Cout = A.CT + static_cast<int64_t>(s) * kDQK * kDV;
-        nout = A.nT + static_cast<int64_t>(s) * kDQK;
-        mout = A.mT + s;
-    } else {
-        float* slot = A.ws + (static_cast<int64_t>(s) * (A.G - 1) + g) * kSlotFloats;
-        Cout = slot;
-        nout = slot + kDQK * kDV;
-        mout = nout + kDQK;   // m_loc, then gsum
-        if (write_nm && gate_wave && lane == 0) mout[1] = g_sum;
-    }
+    if (g != A.G - 1) return;
+    Cout = A.CT + static_cast<int64_t>(s) * kDQK * kDV;
+    nout = A.nT + static_cast<int64_t>(s) * kDQK;
+    mout = A.mT + s;
     const float esc = expf(s_off);
 #pragma unroll
     for (int t = 0; t < NDB * NQ; ++t) {
@@ -798,11 +785,237 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     }
 }
 
-// Entry states of segments 1..G-1 from the local segment states (in place).
+// ---- local segment states as one weighted contraction ------------------------------------------
+//
+// From an empty state (C = 0, n = 0, m = -inf) the recurrence of Eq. 2-4 over tokens 1..N unrolls to
+// a closed form: with b_t the prefix sums of logsig(f~_t) and x_t = i~_t - b_t,
+//   m_N = b_N + X,  X = max_t x_t,   C_N = sum_t w_t k_t v_t^T,  n_N = sum_t w_t k_t,  w_t = exp(x_t - X)
+// (every weight is <= 1).  A (sub-)segment's local state is therefore one contraction over its
+// tokens, with no chunk recurrence: the gates are scanned once over the whole sub-segment, then
+// 64-token tiles of K^T and V^T stream through LDS into the MFMA accumulators.  C and n are the
+// same quantities the chunkwise update accumulates (bf16 w V operand, bf16 hi / lo weights for n).
+constexpr int kLocTile = 64;                  // tokens per tile
+constexpr int kLocMax = 4096;                 // tokens per sub-segment (weights held in LDS)
+constexpr int kLocP = kLocTile + 8;           // K^T / V^T row pitch: 144 bytes
+
+struct LocSmem {
+    uint16_t Kt[2][kDQK * kLocP];             // K^T[d][tau] of a tile, double-buffered
+    uint16_t Vt[2][kDVT * kLocP];             // V^T[v][tau] (this workgroup's 128 columns)
+    float w[kLocMax];                         // x_t, then the weights w_t
+    uint16_t wb[2][kLocMax];                  // w_t as bf16 hi / lo
+    float red[2][kWaves];                     // per-wave scan totals and maxima
+};
+static_assert(sizeof(LocSmem) <= 160 * 1024, "LDS budget");
+
+__device__ __forceinline__ uint32_t bload32(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+// Column item regrouping: r[j] holds columns (c, c + 1) of row j as a bf16 pair; c0 / c1 receive
+// column c / c + 1 over rows 0..7, in row order.
+__device__ __forceinline__ void regroup(const uint32_t (&r)[8], u32x4_t& c0, u32x4_t& c1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        c0[i] = __builtin_amdgcn_perm(r[2 * i + 1], r[2 * i], 0x05040100u);   // low halves
+        c1[i] = __builtin_amdgcn_perm(r[2 * i + 1], r[2 * i], 0x07060302u);   // high halves
+    }
+}
+// One tile in flight: two K column items (2 d x 8 tau) and one V column item (2 v x 8 tau) per
+// thread, each read as eight 4-byte loads so the store side can write whole transposed rows.
+struct LocRegs {
+    uint32_t k[2][8];
+    uint32_t v[8];
+};
+__device__ __forceinline__ void loc_load(LocRegs& r, const SeqRsrc& R, int t, int v0, int tid) {
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int item = tid + it * kThreads;
+        const uint32_t vo = (8 * (item / (kDQK / 2))) * (kDQK * 2) + 4 * (item % (kDQK / 2));
+#pragma unroll
+        for (int j = 0; j < 8; ++j) r.k[it][j] = bload32(R.k, vo, static_cast<uint32_t>(t + j) * (kDQK * 2));
+    }
+    const uint32_t vo = (8 * (tid / (kDVT / 2))) * (kDV * 2) + 4 * (tid % (kDVT / 2));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) r.v[j] = bload32(R.v, vo, static_cast<uint32_t>(t + j) * (kDV * 2) + v0 * 2);
+}
+__device__ __forceinline__ void loc_store(uint16_t* Kt, uint16_t* Vt, const LocRegs& r, int tid) {
+    u32x4_t c0, c1;
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int item = tid + it * kThreads;
+        regroup(r.k[it], c0, c1);
+        uint16_t* dst = &Kt[(2 * (item % (kDQK / 2))) * kLocP + 8 * (item / (kDQK / 2))];
+        *reinterpret_cast<u32x4_t*>(dst) = c0;
+        *reinterpret_cast<u32x4_t*>(dst + kLocP) = c1;
+    }
+    regroup(r.v, c0, c1);
+    uint16_t* dst = &Vt[(2 * (tid % (kDVT / 2))) * kLocP + 8 * (tid / (kDVT / 2))];
+    *reinterpret_cast<u32x4_t*>(dst) = c0;
+    *reinterpret_cast<u32x4_t*>(dst + kLocP) = c1;
+}
+
+struct LocalArgs {
+    const uint16_t* k;
+    const uint16_t* v;
+    const float* ipre;
+    const float* fpre;
+    float* ws;
+    int T;
+    int NS;            // local slots per sequence: (G - 1) segments x R sub-segments
+    int R;             // sub-segments per segment
+    int seg_tokens;    // tokens per local segment (a multiple of kLocTile)
+};
+
+// One workgroup per (sequence, local segment, sub-segment, dv tile); its slot receives C[:, tile],
+// and (dv tile 0) n, m_loc and the segment's logsig sum.
+// (the LDS footprint allows one workgroup per CU, two waves per SIMD: registers are not worth
+// saving for a higher occupancy)
+__global__ void __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(2, 2)))
+local_state_kernel(LocalArgs A) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+    LocSmem& S = *reinterpret_cast<LocSmem*>(smem_raw);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g16 = lane >> 4, l16 = lane & 15;
+    const int wi = work_index();
+    const int tile = wi % kNTile;
+    const int rest = wi / kNTile;
+    const int sl = rest % A.NS;                 // local slot of the sequence
+    const int s = rest / A.NS;
+    const int g = sl / A.R, r = sl % A.R;
+    const int v0 = tile * kDVT;
+    const int ntiles = A.seg_tokens / kLocTile;
+    const int tps = (ntiles + A.R - 1) / A.R;
+    const int tile_b = min(ntiles, r * tps), tile_e = min(ntiles, tile_b + tps);
+    const int tb = g * A.seg_tokens + tile_b * kLocTile;
+    const int ntok = (tile_e - tile_b) * kLocTile;
+
+    SeqRsrc P;
+    P.k = make_rsrc(A.k + static_cast<int64_t>(s) * A.T * kDQK, static_cast<uint32_t>(A.T) * kDQK * 2);
+    P.v = make_rsrc(A.v + static_cast<int64_t>(s) * A.T * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
+    P.ig = make_rsrc(A.ipre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
+    P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
+
+    LocRegs rg;
+    if (ntok > 0) loc_load(rg, P, tb, v0, tid);   // first tile, in flight during the gate pass
+
+    // gates: block-wide prefix sums of logsig(f~) in rounds of 512 tokens, x_t into LDS, then X
+    float carry = 0.0f, xmax = -INFINITY;
+    for (int j0 = 0; j0 < ntok; j0 += kThreads) {
+        const int t = j0 + tid;
+        const bool valid = t < ntok;
+        const float fv = valid ? bloadf(P.fg, 4 * t, 4 * tb) : 0.0f;
+        const float iv = valid ? bloadf(P.ig, 4 * t, 4 * tb) : 0.0f;
+        const float incl = wave_incl_sum(valid ? flogsig(fv) : 0.0f);
+        if (lane == 63) S.red[0][wave] = incl;
+        __syncthreads();
+        float before = carry, total = 0.0f;
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) {
+            const float tw = S.red[0][w2];
+            if (w2 < wave) before += tw;
+            total += tw;
+        }
+        carry += total;
+        const float x = valid ? iv - (before + incl) : -INFINITY;
+        if (valid) S.w[t] = x;
+        xmax = fmaxf(xmax, x);
+        __syncthreads();   // red[0] is rewritten by the next round
+    }
+    const float wm = lane63(wave_incl_max(xmax));
+    if (lane == 0) S.red[1][wave] = wm;
+    __syncthreads();
+    float X = -INFINITY;
+#pragma unroll
+    for (int w2 = 0; w2 < kWaves; ++w2) X = fmaxf(X, S.red[1][w2]);
+    for (int t = tid; t < ntok; t += kThreads) {
+        const float wv = fexp(S.w[t] - X);
+        S.w[t] = wv;
+        const uint16_t hi = f32_to_bf16(wv);
+        S.wb[0][t] = hi;
+        S.wb[1][t] = f32_to_bf16(wv - bf16_to_f32(hi));
+    }
+
+    // contraction: wave (dh, vg) owns C[128 dh + 0..127][32 vg + 0..31] as 8 x 2 tiles; it also
+    // accumulates n over its d tiles 2 vg and 2 vg + 1
+    const int dh = wave >> 2, vg = wave & 3;
+    f32x4_t Cacc[8][2];
+    f32x4_t nacc[2];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) Cacc[q][0] = Cacc[q][1] = f32x4_t{};
+    nacc[0] = nacc[1] = f32x4_t{};
+    const int nt = ntok / kLocTile;
+    if (nt > 0) {
+        loc_store(S.Kt[0], S.Vt[0], rg, tid);
+        if (nt > 1) loc_load(rg, P, tb + kLocTile, v0, tid);
+    }
+    for (int i = 0; i < nt; ++i) {
+        __syncthreads();   // tile i and the weights are visible; the other buffer's readers are done
+        if (i + 1 < nt) {
+            loc_store(S.Kt[(i + 1) & 1], S.Vt[(i + 1) & 1], rg, tid);
+            if (i + 2 < nt) loc_load(rg, P, tb + (i + 2) * kLocTile, v0, tid);
+        }
+        const uint16_t* Kt = S.Kt[i & 1];
+        const uint16_t* Vt = S.Vt[i & 1];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int t0 = i * kLocTile + 32 * ks + 8 * g16;   // this lane's 8 k slots
+            const f32x4_t wa0 = *reinterpret_cast<const f32x4_t*>(&S.w[t0]);
+            const f32x4_t wa1 = *reinterpret_cast<const f32x4_t*>(&S.w[t0 + 4]);
+            const float wv[8] = {wa0[0], wa0[1], wa0[2], wa0[3], wa1[0], wa1[1], wa1[2], wa1[3]};
+            u32x4_t Vw[2];
+#pragma unroll
+            for (int vt = 0; vt < 2; ++vt) {
+                const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(&Vt[(32 * vg + 16 * vt + l16) * kLocP + 32 * ks + 8 * g16]);
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    Vw[vt][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
+            }
+            const uint16_t* kb = &Kt[(128 * dh + l16) * kLocP + 32 * ks + 8 * g16];
+            u32x4_t a[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) a[q] = *reinterpret_cast<const u32x4_t*>(kb + 16 * q * kLocP);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                Cacc[q][0] = mfma16(a[q], Vw[0], Cacc[q][0]);
+                Cacc[q][1] = mfma16(a[q], Vw[1], Cacc[q][1]);
+            }
+            // n over d tiles 2 vg and 2 vg + 1 (rows re-read by address: no wave-dependent branch)
+            const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&S.wb[l16 & 1][t0]) : u32x4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int e = 0; e < 2; ++e)
+                nacc[e] = mfma16(wa, *reinterpret_cast<const u32x4_t*>(kb + 16 * (2 * vg + e) * kLocP), nacc[e]);
+        }
+    }
+
+    // slot (s, local slot sl): C [DQK x DV] row-major, then n, m_loc, logsig sum
+    float* slot = A.ws + (static_cast<int64_t>(s) * A.NS + sl) * kSlotFloats;
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+        for (int vt = 0; vt < 2; ++vt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                slot[static_cast<int64_t>(128 * dh + 16 * q + 4 * g16 + j) * kDV + v0 + 32 * vg + 16 * vt + l16] = Cacc[q][vt][j];
+    if (tile == 0) {
+        if (g16 == 0) {
+#pragma unroll
+            for (int e = 0; e < 2; ++e) slot[kDQK * kDV + 128 * dh + 16 * (2 * vg + e) + l16] = nacc[e][0] + nacc[e][1];
+        }
+        if (tid == 0) {
+            slot[kDQK * kDV + kDQK] = carry + X;      // m_loc (-inf for an empty sub-segment)
+            slot[kDQK * kDV + kDQK + 1] = carry;      // sum of logsig(f~)
+        }
+    }
+}
+
+// Running entry states from the local (sub-)segment states, in place: the last slot of segment g
+// (slot g R + R - 1) receives the state after local slots 0..g R + R - 1, the entry state of
+// segment g + 1; the other sub-segment slots are only read.
 __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0, const float* n0, const float* m0,
-                                                      int G) {
+                                                      int NS, int R) {
     const int s = blockIdx.y;
-    float* base = ws + static_cast<int64_t>(s) * (G - 1) * kSlotFloats;
+    float* base = ws + static_cast<int64_t>(s) * NS * kSlotFloats;
     // scalar chain of entry max states (every block computes it; block 0 stores it)
     float m_in = m0 ? m0[s] : 0.0f;
     constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
@@ -817,8 +1030,8 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
     }
     // slots in batches: all loads of a batch are issued before its dependent chain of updates
     constexpr int kBatch = 8;
-    for (int g0 = 0; g0 < G - 1; g0 += kBatch) {
-        const int nbat = min(kBatch, G - 1 - g0);
+    for (int g0 = 0; g0 < NS; g0 += kBatch) {
+        const int nbat = min(kBatch, NS - g0);
         float4 loc[kBatch];
         float mloc[kBatch], gs[kBatch];
 #pragma unroll
@@ -837,24 +1050,25 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
                 const float m_new = fmaxf(gs[u] + m_in, mloc[u]);
                 const float a = expf(gs[u] + m_in - m_new);
                 const float b = expf(mloc[u] - m_new);
+                const bool entry = ((g0 + u) % R) == R - 1;
                 if (e4 < kE4) {
                     cur.x = a * cur.x + b * loc[u].x;
                     cur.y = a * cur.y + b * loc[u].y;
                     cur.z = a * cur.z + b * loc[u].z;
                     cur.w = a * cur.w + b * loc[u].w;
-                    reinterpret_cast<float4*>(slot)[e4] = cur;
+                    if (entry) reinterpret_cast<float4*>(slot)[e4] = cur;
                 }
-                if (blockIdx.x == 0 && threadIdx.x == 0) slot[kDQK * kDV + kDQK + 2] = m_new;
+                if (entry && blockIdx.x == 0 && threadIdx.x == 0) slot[kDQK * kDV + kDQK + 2] = m_new;
                 m_in = m_new;
             }
         }
     }
 }
 
-template <int L, bool FULL>
+template <int L>
 hipError_t launch_variant(const ChunkKernelArgs& a, int S, hipStream_t stream) {
     const size_t lds = sizeof(Smem<L>);
-    auto kern = chunk_mfma_kernel<L, FULL>;
+    auto kern = chunk_mfma_kernel<L>;
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -862,11 +1076,27 @@ hipError_t launch_variant(const ChunkKernelArgs& a, int S, hipStream_t stream) {
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const int G_run = FULL ? a.G : a.G - 1;
-    const dim3 grid(static_cast<unsigned>(S * G_run * kNTile));
+    const dim3 grid(static_cast<unsigned>(S * a.G * kNTile));
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, stream, a);
     return hipGetLastError();
 }
+
+hipError_t launch_local(const LocalArgs& a, int S, hipStream_t stream) {
+    const size_t lds = sizeof(LocSmem);
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(local_state_kernel),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    hipLaunchKernelGGL(local_state_kernel, dim3(static_cast<unsigned>(S * a.NS * kNTile)), dim3(kThreads), lds, stream,
+                       a);
+    return hipGetLastError();
+}
+
+// sub-segments of a local segment: at most kLocMax tokens each
+int local_subsegments(int seg_tokens) { return (seg_tokens + kLocMax - 1) / kLocMax; }
 
 }  // namespace
 
@@ -892,7 +1122,9 @@ size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L) 
     (void)DV;
     const int G = chunk_mfma_segments(B, NH, T, L);
     if (G <= 1) return 0;
-    return static_cast<size_t>(B) * NH * (G - 1) * kSlotFloats * sizeof(float);
+    const int nc = T / L;
+    const int seg_tokens = ((nc + G - 1) / G) * L;
+    return static_cast<size_t>(B) * NH * (G - 1) * local_subsegments(seg_tokens) * kSlotFloats * sizeof(float);
 }
 
 hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream) {
@@ -902,6 +1134,7 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
     if (G > 1 && workspace_bytes < chunk_mfma_workspace_bytes(a.B, a.NH, a.T, a.DQK, a.DV, a.L)) G = 1;
     if (nc == 0) G = 1;
     const int seg_chunks = G > 1 ? (nc + G - 1) / G : nc;
+    const int R = G > 1 ? local_subsegments(seg_chunks * a.L) : 1;
 
     ChunkKernelArgs k{};
     k.q = static_cast<const uint16_t*>(a.q);
@@ -915,6 +1148,8 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
     k.ws = static_cast<float*>(workspace);
     k.T = a.T;
     k.G = G;
+    k.R = R;
+    k.NS = (G - 1) * R;
     k.seg_chunks = seg_chunks;
     k.h = static_cast<uint16_t*>(a.h);
     k.CT = a.CT;
@@ -923,15 +1158,25 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
 
     hipError_t e;
     if (G > 1) {
-        e = (a.L == 64) ? launch_variant<64, false>(k, S, stream) : launch_variant<128, false>(k, S, stream);
+        LocalArgs la{};
+        la.k = k.k;
+        la.v = k.v;
+        la.ipre = a.ipre;
+        la.fpre = a.fpre;
+        la.ws = k.ws;
+        la.T = a.T;
+        la.NS = k.NS;
+        la.R = R;
+        la.seg_tokens = seg_chunks * a.L;
+        e = launch_local(la, S, stream);
         if (e != hipSuccess) return e;
         constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
         hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, k.ws, a.C0, a.n0, a.m0,
-                           G);
+                           k.NS, R);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    return (a.L == 64) ? launch_variant<64, true>(k, S, stream) : launch_variant<128, true>(k, S, stream);
+    return (a.L == 64) ? launch_variant<64>(k, S, stream) : launch_variant<128>(k, S, stream);
 }
 
 }  // namespace mlstm

@@ -183,7 +183,7 @@ struct VRegs {
 constexpr int kRsrcWord3 = 0x00020000;
 
 struct SeqRsrc {
-    __amdgpu_buffer_rsrc_t q, k, v, ig, fg;
+    __amdgpu_buffer_rsrc_t q, k, v, ig, fg, h;
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -429,6 +429,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     P.v = make_rsrc(A.v + static_cast<int64_t>(s) * A.T * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
     P.ig = make_rsrc(A.ipre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
     P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
+    P.h = make_rsrc(A.h + static_cast<int64_t>(s) * A.T * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
 
     // ---- entry state ------------------------------------------------------------------------
     // C tiles come in pairs over 32 consecutive d: in pair pp of a d block, tile e (0, 1) holds the d
@@ -495,7 +496,20 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     f32x4_t Sacc[MAXT];
     f32x4_t dqacc;
 
+    const int tid_outer = tid;
     for (int c = c_begin; c < c_end; ++c) {
+        // L = 128: the lane quantities are re-derived from an opaque copy of the thread index in
+        // every chunk.  Otherwise the compiler hoists every lane-dependent address out of the loop
+        // and, with the larger accumulator set resident, spills them and reloads them through
+        // memory each chunk (a reload waits for every staging load in flight).  At L = 64 the
+        // recomputation costs more than it saves.
+        int tid = tid_outer;
+        if constexpr (L == 128) asm volatile("" : "+v"(tid));
+        const int lane = tid & 63;
+        const int g16 = lane >> 4;
+        const int l16 = lane & 15;
+        const int tr_row = (l16 >> 2) + 8 * g16;
+        const int tr_col = 4 * (l16 & 3);
         const int t0 = c * L;
         const int cur = (c - c_begin) & 1;
         const int par = c & 1;
@@ -748,8 +762,15 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 u32x2_t o;
                 o[0] = pack_bf16x2(acc[0] * hv, acc[1] * hv);
                 o[1] = pack_bf16x2(acc[2] * hv, acc[3] * hv);
-                *reinterpret_cast<u32x2_t*>(A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + vcol(vt) +
-                                            4 * g16) = o;
+                if constexpr (L == 128) {
+                    // 32-bit offsets into the sequence's h: no 64-bit addresses to keep per tau tile
+                    __builtin_amdgcn_raw_buffer_store_b64(o, P.h,
+                                                          static_cast<uint32_t>(tau * kDV + v0 + vcol(vt) + 4 * g16) * 2,
+                                                          static_cast<uint32_t>(t0) * (kDV * 2), 0);
+                } else {
+                    *reinterpret_cast<u32x2_t*>(A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + vcol(vt) +
+                                                4 * g16) = o;
+                }
             }
         }
         s_off = s_new;

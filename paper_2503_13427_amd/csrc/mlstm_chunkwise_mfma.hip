@@ -366,6 +366,11 @@ struct ChunkKernelArgs {
     float* mT;
 };
 
+// row pitch (floats) of the entry-state staging of a 256 x 128 tile in LDS: 528 bytes puts the
+// rows 8 apart that one read of the accumulator pickup touches in different banks
+constexpr int kStageP = kDVT + 4;
+static_assert(kDQK * kStageP * 4 <= sizeof(Smem<64>) && kDQK * kStageP * 4 <= sizeof(Smem<128>), "staging");
+
 // workspace slot of (sequence s, local sub-segment j): C [DQK*DV], n [DQK], then m_loc, gsum
 // (sum of logsig over the sub-segment), m_in (entry max state, in segment-boundary slots), pad
 constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
@@ -450,16 +455,31 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         nin = slot + kDQK * kDV;
         m_prev = slot[kDQK * kDV + kDQK + 2];
     }
-#pragma unroll
-    for (int t = 0; t < NDB * NQ; ++t) {
-#pragma unroll
-        for (int vt = 0; vt < VT; ++vt) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int d = cdrow(t, j);
-                Cacc[t][vt][j] = Cin ? Cin[static_cast<int64_t>(d) * kDV + v0 + vcol(vt) + l16] : 0.0f;
-            }
+    if (Cin) {
+        // the workgroup's 256 x 128 tile of the entry state in coalesced 16-byte pieces, staged in
+        // LDS (rows of kStageP floats, before the chunk loop uses it) and picked up in the
+        // accumulator layout
+        float* stage = reinterpret_cast<float*>(smem_raw);
+#pragma unroll 4
+        for (int i = 0; i < (kDQK * kDVT / 4) / kThreads; ++i) {
+            const int f = tid + kThreads * i;
+            const int row = f / (kDVT / 4), c4 = f % (kDVT / 4);
+            *reinterpret_cast<f32x4_t*>(&stage[row * kStageP + 4 * c4]) =
+                *reinterpret_cast<const f32x4_t*>(Cin + static_cast<int64_t>(row) * kDV + v0 + 4 * c4);
         }
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < NDB * NQ; ++t)
+#pragma unroll
+            for (int vt = 0; vt < VT; ++vt)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) Cacc[t][vt][j] = stage[cdrow(t, j) * kStageP + vcol(vt) + l16];
+        __syncthreads();   // the staging area is the LDS of the chunk loop
+    } else {
+#pragma unroll
+        for (int t = 0; t < NDB * NQ; ++t)
+#pragma unroll
+            for (int vt = 0; vt < VT; ++vt) Cacc[t][vt] = f32x4_t{};
     }
     if (tid < kDQK) {
         const float nv = nin ? nin[tid] : 0.0f;

@@ -260,9 +260,9 @@ def main():
     if args.only in (None, "large") and not args.skip_large:
         res["prefill_large"] = []
         for wl, steps in ((configs.PREFILL_T8192, max(3, args.steps // 20)),
-                          (configs.CONT_PREFILL_T32768, max(2, args.steps // 40))):
+                          (configs.CONT_PREFILL_T32768, max(2, args.steps // 20))):
             log(f"prefill {wl.name}: {steps} timed steps")
-            r, p = bench_prefill(wl, steps, 1, 1, stream)
+            r, p = bench_prefill(wl, steps, 2, 1, stream)
             res["prefill_large"].append(r)
             del p
             torch.cuda.empty_cache()

@@ -643,6 +643,16 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             }
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks) {
+                // the K^T operands first: their reads are in flight while the weighted V operand is
+                // built (the fence keeps the compiler from sinking them below that VALU work)
+                u32x4_t a[NQ];
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    // tile (pair q / 2, half q % 2): columns 32 pp + 8 (l16 & 3) + 4 (q % 2) + 0..3
+                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * ((q / 2) * DH + dh) + 2 * tr_col + 4 * (q % 2)];
+                    a[q] = cat(tr_read(kb), tr_read(kb + 4 * QP));
+                }
+                if constexpr (L == 64) __builtin_amdgcn_sched_barrier(0);
                 // lane (n = column vcol(vt) + l16, k group g16) holds tau = 32 ks + 8 g16 + 0..7
                 u32x4_t Vw[VT];
                 const float* wv = &Gc.wC[32 * ks + 8 * g16];
@@ -655,14 +665,10 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                         Vw[vt][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
                 }
 #pragma unroll
-                for (int q = 0; q < NQ; ++q) {
-                    // tile (pair q / 2, half q % 2): columns 32 pp + 8 (l16 & 3) + 4 (q % 2) + 0..3
-                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * ((q / 2) * DH + dh) + 2 * tr_col + 4 * (q % 2)];
-                    const u32x4_t a = cat(tr_read(kb), tr_read(kb + 4 * QP));
+                for (int q = 0; q < NQ; ++q)
 #pragma unroll
                     for (int vt = 0; vt < VT; ++vt)
-                        Cacc[p * NQ + q][vt] = mfma16(a, Vw[vt], Cacc[p * NQ + q][vt]);
-                }
+                        Cacc[p * NQ + q][vt] = mfma16(a[q], Vw[vt], Cacc[p * NQ + q][vt]);
             }
             // n_p = decay n_p + K_p^T w: A = w as bf16 hi / lo rows, B = K read transposed
 #pragma unroll

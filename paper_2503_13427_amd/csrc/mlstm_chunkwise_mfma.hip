@@ -372,7 +372,10 @@ constexpr int kStageP = kDVT + 4;
 static_assert(kDQK * kStageP * 4 <= sizeof(Smem<64>) && kDQK * kStageP * 4 <= sizeof(Smem<128>), "staging");
 
 // workspace slot of (sequence s, local sub-segment j): C [DQK*DV], n [DQK], then m_loc, gsum
-// (sum of logsig over the sub-segment), m_in (entry max state, in segment-boundary slots), pad
+// (sum of logsig over the sub-segment), m_in (entry max state, in segment-boundary slots), pad.
+// C is stored four rows interleaved: element (d, v) at ((d / 4) DV + v) 4 + d % 4, so the four
+// consecutive d one accumulator lane holds for one v are one 16-byte piece
+__host__ __device__ constexpr int64_t slot_c4(int d4, int v) { return (static_cast<int64_t>(d4) * kDV + v) * 4; }
 constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
 
 // Staging order (one Q/K block and one part of a V chunk in registers at a time): block 0
@@ -455,10 +458,16 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         nin = slot + kDQK * kDV;
         m_prev = slot[kDQK * kDV + kDQK + 2];
     }
-    if (Cin) {
-        // the workgroup's 256 x 128 tile of the entry state in coalesced 16-byte pieces, staged in
-        // LDS (rows of kStageP floats, before the chunk loop uses it) and picked up in the
-        // accumulator layout
+    if (Cin && g > 0) {
+        // a segment entry slot (four rows interleaved): each accumulator tile is one 16-byte load
+#pragma unroll
+        for (int t = 0; t < NDB * NQ; ++t)
+#pragma unroll
+            for (int vt = 0; vt < VT; ++vt)
+                Cacc[t][vt] = *reinterpret_cast<const f32x4_t*>(Cin + slot_c4(cdrow(t, 0) / 4, v0 + vcol(vt) + l16));
+    } else if (Cin) {
+        // C0: the workgroup's 256 x 128 tile in coalesced 16-byte pieces, staged in LDS (rows of
+        // kStageP floats, before the chunk loop uses it) and picked up in the accumulator layout
         float* stage = reinterpret_cast<float*>(smem_raw);
 #pragma unroll 4
         for (int i = 0; i < (kDQK * kDVT / 4) / kThreads; ++i) {
@@ -1041,9 +1050,7 @@ local_state_kernel(LocalArgs A) {
     for (int q = 0; q < 8; ++q)
 #pragma unroll
         for (int vt = 0; vt < 2; ++vt)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                slot[static_cast<int64_t>(128 * dh + 16 * q + 4 * g16 + j) * kDV + v0 + 32 * vg + 16 * vt + l16] = Cacc[q][vt][j];
+            *reinterpret_cast<f32x4_t*>(slot + slot_c4(32 * dh + 4 * q + g16, v0 + 32 * vg + 16 * vt + l16)) = Cacc[q][vt];
     if (tile == 0) {
         if (g16 == 0) {
 #pragma unroll
@@ -1070,7 +1077,11 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
     float4 cur = make_float4(0.f, 0.f, 0.f, 0.f);
     if (e4 < kE4) {
         if (e4 < kDQK * kDV / 4) {
-            if (C0) cur = reinterpret_cast<const float4*>(C0 + static_cast<int64_t>(s) * kDQK * kDV)[e4];
+            if (C0) {
+                // slot float4 e4 holds rows 4 (e4 / DV) + 0..3 of column e4 % DV; C0 is row-major
+                const float* c0 = C0 + static_cast<int64_t>(s) * kDQK * kDV + static_cast<int64_t>(4 * (e4 / kDV)) * kDV + e4 % kDV;
+                cur = make_float4(c0[0], c0[kDV], c0[2 * kDV], c0[3 * kDV]);
+            }
         } else if (n0) {
             cur = reinterpret_cast<const float4*>(n0 + static_cast<int64_t>(s) * kDQK)[e4 - kDQK * kDV / 4];
         }

@@ -111,8 +111,25 @@ def measured_traffic():
     return nbytes
 
 
+SETTLE_S = 0.25
+
+
+def settle(fn, seconds=SETTLE_S):
+    """Untimed calls of fn until ``seconds`` of wall time have passed: the GPU raises its clocks over
+    the first milliseconds under load, so short warm-ups alone time a partly idle-clocked chip."""
+    t0 = time.perf_counter()
+    n = 1
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(n):
+            fn()
+        torch.cuda.synchronize()
+        n = min(2 * n, 64)
+
+
 def time_steps(fn, steps, warmup, stream):
-    """Wall time and HIP-event time (on the launch stream) of ``steps`` calls of fn."""
+    """Wall time and HIP-event time (on the launch stream) of ``steps`` calls of fn, after the clock
+    settle phase and ``warmup`` untimed calls."""
+    settle(fn)
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
@@ -167,6 +184,7 @@ def bench_decode(w, steps, stream, warm=16):
                            hpre, C, n, m, stream=stream)
     h = torch.empty(w.B, w.NH, w.DV, dtype=torch.bfloat16, device="cuda")
     C0, n0, m0 = C.clone(), n.clone(), m.clone()
+    settle(lambda: mb.mlstm_step(qs[0], ks[0], vs[0], ips[0], fps[0], C0, n0, m0, h, C0, n0, m0, stream=stream))
     for t in range(warm):   # warm-up on a copy of the state
         mb.mlstm_step(qs[t], ks[t], vs[t], ips[t], fps[t], C0, n0, m0, h, C0, n0, m0, stream=stream)
     del C0, n0, m0

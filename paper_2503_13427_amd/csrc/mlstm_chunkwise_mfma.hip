@@ -127,6 +127,10 @@ struct Cfg {
     static constexpr int DH = (L == 64) ? 2 : 1;
     static constexpr int VT = DH;
     static constexpr int NVG = kWaves / DH;
+    // L = 64: V is kept in LDS transposed (rows v, tau contiguous, pitch TP), once plain for (ii) and
+    // once scaled by the C-update key weights for (iv), so both read it with plain 16-byte row reads
+    static constexpr bool VTR = (L == 64);
+    static constexpr int TP = L + 8;
 };
 
 // Per-chunk gate quantities, written one chunk ahead by the gate wave.
@@ -146,14 +150,14 @@ template <int L>
 struct Smem {
     using C = Cfg<L>;
     uint16_t QK[2][2][C::QKE];                     // [set][0: Q, 1: K][tau * QP + d]; d block p uses set p % 2
-    uint16_t Vs[2][L * C::VP];                     // V[tau][v] (this workgroup's 128 columns), by chunk parity
+    // L = 128: V[tau][v] (this workgroup's 128 columns) by chunk parity; L = 64: [0] V^T[v][tau] and
+    // [1] (w e^{-s} V)^T[v][tau] of the current chunk
+    uint16_t Vs[2][C::VTR ? kDVT * C::TP : L * C::VP];
     uint16_t St_own[C::ST_ALIAS ? 8 : L * C::SP];  // S~[tau][sig] when it has its own buffer
     uint16_t nb[2][2][kDQK];                       // normaliser as bf16 hi / lo rows, double-buffered
     float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
     float dq[L];                                   // Q n_{k-1} (unscaled q)
-    // row sums of S~: L = 64 keeps one partial per (sigma block, tau, sigma quarter) so no
-    // cross-lane reduction is needed; L = 128 (no LDS to spare) reduces over the quarters first
-    float rs[L / 16][L][L == 64 ? 4 : 1];
+    float rs[L / 16][L];                           // row sums of S~ per (sigma block, tau)
     GateBuf<L> G[2];                               // by chunk parity
     // partial read-outs exchanged between the two d partitions of a column group (DH = 2):
     // [column group][v tile][tau tile][lane] as float4
@@ -238,6 +242,81 @@ __device__ __forceinline__ void store_v(uint16_t* Vd, const VRegs<L>& r, int tid
         *reinterpret_cast<u32x4_t*>(&Vd[(item / 16) * Cfg<L>::VP + 8 * (item % 16)]) = r.v[i];
     }
 }
+// L = 64: V pieces in the MFMA A-operand layout for vt_transpose: lane (l16, g16) of wave w, piece i
+// holds V[tau 16 a + l16][v 32 b + 8 g16 + 0..7] with (a, b) = ((w + 8 i) % 4, (w + 8 i) / 4), so the
+// 16 pieces of the workgroup cover the 64 x 128 chunk once.
+template <int L>
+__device__ __forceinline__ void load_v_tr(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane) {
+    static_assert(VRegs<L>::PARTS == 1 && VRegs<L>::N * kWaves == 16, "pieces of one 64 x 128 chunk");
+    const uint32_t soff = static_cast<uint32_t>(t0) * (kDV * 2) + v0 * 2;
+    int ln = lane;   // opaque: the offsets are recomputed per call rather than held across the loop
+    asm volatile("" : "+v"(ln));
+#pragma unroll
+    for (int i = 0; i < VRegs<L>::N; ++i) {
+        const int pc = wave + kWaves * i, a = pc & 3, b = pc >> 2;
+        r.v[i] = bload128(R.v, (16 * a + (ln & 15)) * (kDV * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
+    }
+}
+// The transposition on the matrix cores: D = A E_h with A a piece (16 tau x 32 v) and E_h the 32 x 16
+// one-hot selection of its columns 16 h + 0..15 (exact in fp32).  Lane (n = l16, g16) of D holds
+// V[tau 16 a + 4 g16 + j][v 32 b + 16 h + n], j = 0..3: four consecutive tau of one row of V^T, kept
+// packed in pv until the stores below.
+template <int L>
+__device__ __forceinline__ void vt_transpose(u32x2_t (&pv)[2 * VRegs<L>::N], const VRegs<L>& r, int lane) {
+    // E_h in the B-operand layout: lane (l16, g16) holds k slots 8 g16 + 0..7 of column l16, whose
+    // one (if any) is slot 16 h + l16.  Built from an opaque copy of the lane index so that it is not
+    // hoisted out of the chunk loop (eight more registers held across the loop would spill).
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    u32x4_t E[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int pos = 16 * h + (ln & 15) - 8 * (ln >> 4);
+        const uint32_t one = (pos & 1) ? 0x3F800000u : 0x3F80u;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) E[h][d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < VRegs<L>::N; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const f32x4_t d = mfma16(r.v[i], E[h], f32x4_t{});
+            pv[2 * i + h] = u32x2_t{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
+        }
+}
+// (w V)^T from the packed V^T: row weights wC of the chunk, rounded to bf16 once
+template <int L>
+__device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const u32x2_t (&pv)[2 * VRegs<L>::N], const float* wC,
+                                                int wave, int lane) {
+    constexpr int TP = Cfg<L>::TP;
+    const int l16 = lane & 15, g16 = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < VRegs<L>::N; ++i) {
+        const int pc = wave + kWaves * i, a = pc & 3, b = pc >> 2;
+        const int tau = 16 * a + 4 * g16;
+        const f32x4_t w = *reinterpret_cast<const f32x4_t*>(&wC[tau]);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const u32x2_t x = pv[2 * i + h];
+            u32x2_t o;
+            o[0] = pack_bf16x2(lo_f32(x[0]) * w[0], hi_f32(x[0]) * w[1]);
+            o[1] = pack_bf16x2(lo_f32(x[1]) * w[2], hi_f32(x[1]) * w[3]);
+            *reinterpret_cast<u32x2_t*>(&VwT[(32 * b + 16 * h + l16) * TP + tau]) = o;
+        }
+    }
+}
+template <int L>
+__device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const u32x2_t (&pv)[2 * VRegs<L>::N], int wave, int lane) {
+    constexpr int TP = Cfg<L>::TP;
+    const int l16 = lane & 15, g16 = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < VRegs<L>::N; ++i) {
+        const int pc = wave + kWaves * i, a = pc & 3, b = pc >> 2;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            *reinterpret_cast<u32x2_t*>(&VtT[(32 * b + 16 * h + l16) * TP + 16 * a + 4 * g16]) = pv[2 * i + h];
+    }
+}
 // Gate pre-activations of one chunk, one (L = 64) or two (L = 128) per lane of the gate wave.
 template <int L>
 __device__ __forceinline__ void load_gates(float (&gi)[2], float (&gf)[2], const SeqRsrc& R, int t0, int lane) {
@@ -275,6 +354,15 @@ __device__ __forceinline__ float wave_incl_max(float x) {
     return x;
 }
 #undef MLSTM_DPP
+// sum over the four 16-lane rows of a wave, in every lane (gfx950 cross-row lane swaps, no LDS)
+__device__ __forceinline__ float sum_rows4(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);   // rows (0, 1) <-> (2, 3)
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const uint32_t w = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane16_swap(w, w, false, false);   // rows 0 <-> 1, 2 <-> 3
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 __device__ __forceinline__ float lane63(float x) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
 }
@@ -505,6 +593,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 
     QKRegs<L> rqk;
     VRegs<L> rv;
+    u32x2_t pv[2 * VRegs<L>::N];   // L = 64: the next chunk's V^T, packed, until its store
     if (c_begin < c_end) {
         const int t0 = c_begin * L;
         load_qk<L>(rqk, P, t0, 0, tid);
@@ -513,10 +602,18 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane);
         }
         store_qk<L>(S.QK[0][0], S.QK[0][1], rqk, tid);
+        if constexpr (CF::VTR) {
+            load_v_tr<L>(rv, P, t0, v0, wave, lane);
+            vt_transpose<L>(pv, rv, lane);
+            __syncthreads();   // the first chunk's gates are visible
+            vt_store_scaled<L>(S.Vs[1], pv, S.G[c_begin & 1].wC, wave, lane);
+            vt_store_plain<L>(S.Vs[0], pv, wave, lane);
+        } else {
 #pragma unroll
-        for (int part = 0; part < VRegs<L>::PARTS; ++part) {
-            load_v<L>(rv, P, t0, v0, tid, part);
-            store_v<L>(S.Vs[c_begin & 1], rv, tid, part);
+            for (int part = 0; part < VRegs<L>::PARTS; ++part) {
+                load_v<L>(rv, P, t0, v0, tid, part);
+                store_v<L>(S.Vs[c_begin & 1], rv, tid, part);
+            }
         }
         load_qk<L>(rqk, P, t0, 1, tid);
     }
@@ -549,15 +646,22 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         if constexpr (NDB > 2) load_qk<L>(rqk, P, t0, 2, tid);
         else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid);
         if (gate_wave && c + 1 < c_end) load_gates<L>(gi, gf, P, t0 + L, lane);
-        // V of the next chunk: part 0 now, part k stored at the barrier that opens d block k + 1
-        if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid, 0);
+        if constexpr (CF::VTR) {
+            // this chunk's plain V^T (its readers in the previous chunk are done); the next chunk's V
+            if (c > c_begin) vt_store_plain<L>(S.Vs[0], pv, wave, lane);
+            if (c + 1 < c_end) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane);
+        } else {
+            // V of the next chunk: part 0 now, part k stored at the barrier that opens d block k + 1
+            if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid, 0);
+        }
         const float decay_n = Gc.scal[0];
         const float m_next = Gc.scal[1];
         const float s_new = Gc.scal[2];
         const float c_scale = Gc.scal[3];   // != 1: apply this chunk's decay to C_acc eagerly
         const float* n_old = S.n[cur];
         float* n_new = S.n[cur ^ 1];
-        const uint16_t* Vc = S.Vs[par];
+        const uint16_t* Vc = S.Vs[CF::VTR ? 0 : par];   // L = 64: V^T
+        const uint16_t* VwT = S.Vs[1];
 
 #pragma unroll
         for (int vt = 0; vt < VT; ++vt)
@@ -583,7 +687,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     load_qk<L>(rqk, P, t0 + L, 1, tid);
                 }
                 // V of the next chunk, part p - 1 (its buffer was last read by the previous chunk)
-                if (p <= VRegs<L>::PARTS && c + 1 < c_end) {
+                if (CF::VTR && p == 1 && c + 1 < c_end) vt_transpose<L>(pv, rv, lane);
+                if (!CF::VTR && p <= VRegs<L>::PARTS && c + 1 < c_end) {
                     store_v<L>(S.Vs[par ^ 1], rv, tid, p - 1);
                     if (p < VRegs<L>::PARTS) load_v<L>(rv, P, t0 + L, v0, tid, p);
                 }
@@ -667,11 +772,15 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 const float* wv = &Gc.wC[32 * ks + 8 * g16];
 #pragma unroll
                 for (int vt = 0; vt < VT; ++vt) {
-                    const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
-                    const u32x4_t raw = cat(tr_read(vb), tr_read(vb + 4 * VP));
+                    if constexpr (CF::VTR) {
+                        Vw[vt] = *reinterpret_cast<const u32x4_t*>(&VwT[(vcol(vt) + l16) * CF::TP + 32 * ks + 8 * g16]);
+                    } else {
+                        const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
+                        const u32x4_t raw = cat(tr_read(vb), tr_read(vb + 4 * VP));
 #pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        Vw[vt][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
+                        for (int u = 0; u < 4; ++u)
+                            Vw[vt][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
+                    }
                 }
 #pragma unroll
                 for (int q = 0; q < NQ; ++q)
@@ -748,13 +857,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 o[0] = pack_bf16x2(vals[0], vals[1]);
                 o[1] = pack_bf16x2(vals[2], vals[3]);
                 *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
-                if constexpr (L == 64) {
-                    S.rs[sb][tau][g16] = rsum;
-                } else {
-                    rsum += __shfl_xor(rsum, 16, 64);
-                    rsum += __shfl_xor(rsum, 32, 64);
-                    if (g16 == 0) S.rs[sb][tau][0] = rsum;
-                }
+                rsum = sum_rows4(rsum);
+                if (g16 == 0) S.rs[sb][tau] = rsum;
             }
         }
         // zero the masked 16x16 tiles (sigma block T+1, tau block T) for even T: the k steps
@@ -764,6 +868,11 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
         }
         __syncthreads();
+        // L = 64: the next chunk's scaled V^T (its readers, (iv) of this chunk, are done; the next
+        // chunk's weights are visible)
+        if constexpr (CF::VTR) {
+            if (c + 1 < c_end) vt_store_scaled<L>(S.Vs[1], pv, S.G[par ^ 1].wC, wave, lane);
+        }
         // (ii) N^T = interC * N^T + V^T S~^T, then h = N^T / max(|den|, floor); with DH = 2 each
         // d partition finishes the tau tiles T with T % 2 == dh, after adding the other's partial
 #pragma unroll
@@ -772,14 +881,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             const int tau = 16 * T + l16;
             float den = Gc.interN[tau] * S.dq[tau];
 #pragma unroll
-            for (int sb = 0; sb <= T; ++sb) {
-                if constexpr (L == 64) {
-                    const f32x4_t r4 = *reinterpret_cast<const f32x4_t*>(&S.rs[sb][tau][0]);
-                    den += (r4[0] + r4[1]) + (r4[2] + r4[3]);
-                } else {
-                    den += S.rs[sb][tau][0];
-                }
-            }
+            for (int sb = 0; sb <= T; ++sb) den += S.rs[sb][tau];
             const float hv = __builtin_amdgcn_rcpf(fmaxf(fabsf(den), Gc.floorv[tau]));
             const float ic = Gc.interC[tau];
 #pragma unroll
@@ -790,9 +892,15 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 acc *= ic;
 #pragma unroll
                 for (int ks = 0; ks <= T / 2; ++ks) {
-                    const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
                     const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&St[tau * SP + 32 * ks + 8 * g16]);
-                    acc = mfma16(cat(tr_read(vb), tr_read(vb + 4 * VP)), b, acc);
+                    u32x4_t va;
+                    if constexpr (CF::VTR) {
+                        va = *reinterpret_cast<const u32x4_t*>(&Vc[(vcol(vt) + l16) * CF::TP + 32 * ks + 8 * g16]);
+                    } else {
+                        const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
+                        va = cat(tr_read(vb), tr_read(vb + 4 * VP));
+                    }
+                    acc = mfma16(va, b, acc);
                 }
                 u32x2_t o;
                 o[0] = pack_bf16x2(acc[0] * hv, acc[1] * hv);

@@ -25,17 +25,19 @@
 //
 // Products and their MFMA mapping (gfx950 bf16 16x16x32 MFMA, fp32 accumulate):
 //   (i)   S^T = K Q^T             A = K rows, B = Q rows (both d-contiguous)
-//   (ii)  N^T += V^T S~^T         A = V read transposed, B = S~ rows
+//   (ii)  N^T += V^T S~^T         A = V^T rows, B = S~ rows
 //   (iii) N^T += C^T Q^T          A = the C accumulators of (iv), converted to bf16 in
 //                                 registers, B = Q rows
-//   (iv)  C += K^T (w e^{-s} V)   A = K read transposed, B = V read transposed and scaled
-//                                 by the key weights in registers
+//   (iv)  C += K^T (w e^{-s} V)   A = K read transposed, B = (w e^{-s} V)^T rows
 //   Q n and K^T w                 the fp32 normaliser and weights split into bf16 hi + lo
 //                                 rows (relative error ~2^-17)
 // "Read transposed" is the LDS transpose read of gfx950 (ds_read_b64_tr_b16): in each
 // 16-lane group, lane 4s+q supplies 4 consecutive elements of row s of a 4 x 16 tile and
 // lane c receives column c, so a row-major [k][m] tile arrives k-contiguous, as an MFMA
-// operand wants it.  Q, K and V therefore live in LDS only in their natural layout.
+// operand wants it.  Q and K live in LDS in their natural layout.  V is transposed once per
+// chunk on the matrix cores instead (a piece in the A-operand layout times a one-hot
+// selection, exact) and kept in LDS as V^T and as the key-weighted (w e^{-s} V)^T, so (ii)
+// and (iv) read it with plain 16-byte row reads.
 // (iii) consumes C in the accumulator layout of (iv): the contraction index d is
 // permuted consistently in both operands.  Outputs come out transposed (rows v,
 // columns tau), so each lane stores runs of four consecutive v of one h row.
@@ -112,7 +114,6 @@ struct Cfg {
     // row pitch (elements) of Q and K blocks: 288 bytes at L = 64 keeps the 16-byte row reads of 16
     // consecutive rows free of bank conflicts (the L = 128 blocks keep 144 bytes for LDS space)
     static constexpr int QP = (L == 64) ? DB + 16 : DB + 8;
-    static constexpr int VP = kDVT + 8;             // row pitch of V
     static constexpr int SP = (L == 64) ? L + 16 : L + 8;   // row pitch of S~ (160 bytes at L = 64)
     static constexpr int NB = L / 16;               // 16-wide blocks along the chunk
     static constexpr int QKE = L * QP;              // elements of one Q or K block buffer
@@ -127,9 +128,8 @@ struct Cfg {
     static constexpr int DH = (L == 64) ? 2 : 1;
     static constexpr int VT = DH;
     static constexpr int NVG = kWaves / DH;
-    // L = 64: V is kept in LDS transposed (rows v, tau contiguous, pitch TP), once plain for (ii) and
-    // once scaled by the C-update key weights for (iv), so both read it with plain 16-byte row reads
-    static constexpr bool VTR = (L == 64);
+    // V is kept in LDS transposed (rows v, tau contiguous, pitch TP), once plain for (ii) and once
+    // scaled by the C-update key weights for (iv), so both read it with plain 16-byte row reads
     static constexpr int TP = L + 8;
 };
 
@@ -150,9 +150,8 @@ template <int L>
 struct Smem {
     using C = Cfg<L>;
     uint16_t QK[2][2][C::QKE];                     // [set][0: Q, 1: K][tau * QP + d]; d block p uses set p % 2
-    // L = 128: V[tau][v] (this workgroup's 128 columns) by chunk parity; L = 64: [0] V^T[v][tau] and
-    // [1] (w e^{-s} V)^T[v][tau] of the current chunk
-    uint16_t Vs[2][C::VTR ? kDVT * C::TP : L * C::VP];
+    // [0] V^T[v][tau] and [1] (w e^{-s} V)^T[v][tau] of the current chunk (this workgroup's 128 columns)
+    uint16_t Vs[2][kDVT * C::TP];
     uint16_t St_own[C::ST_ALIAS ? 8 : L * C::SP];  // S~[tau][sig] when it has its own buffer
     uint16_t nb[2][2][kDQK];                       // normaliser as bf16 hi / lo rows, double-buffered
     float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
@@ -225,44 +224,30 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
         *reinterpret_cast<u32x4_t*>(&Kd[off]) = r.k[i];
     }
 }
+// V pieces in the MFMA A-operand layout for vt_transpose: for piece i of part `part`, lane (l16, g16)
+// of wave w holds V[tau 16 a + l16][v 32 b + 8 g16 + 0..7] with pc = w + 8 (part N + i) and
+// (a, b) = (pc % (L / 16), pc / (L / 16)), so the workgroup's pieces cover the L x 128 chunk once.
 template <int L>
-__device__ __forceinline__ void load_v(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int tid, int part) {
-    const uint32_t soff = static_cast<uint32_t>(t0) * (kDV * 2) + v0 * 2;
-#pragma unroll
-    for (int i = 0; i < VRegs<L>::N; ++i) {
-        const int item = tid + (part * VRegs<L>::N + i) * kThreads;
-        r.v[i] = bload128(R.v, (item / 16) * (kDV * 2) + 16 * (item % 16), soff);
-    }
-}
-template <int L>
-__device__ __forceinline__ void store_v(uint16_t* Vd, const VRegs<L>& r, int tid, int part) {
-#pragma unroll
-    for (int i = 0; i < VRegs<L>::N; ++i) {
-        const int item = tid + (part * VRegs<L>::N + i) * kThreads;
-        *reinterpret_cast<u32x4_t*>(&Vd[(item / 16) * Cfg<L>::VP + 8 * (item % 16)]) = r.v[i];
-    }
-}
-// L = 64: V pieces in the MFMA A-operand layout for vt_transpose: lane (l16, g16) of wave w, piece i
-// holds V[tau 16 a + l16][v 32 b + 8 g16 + 0..7] with (a, b) = ((w + 8 i) % 4, (w + 8 i) / 4), so the
-// 16 pieces of the workgroup cover the 64 x 128 chunk once.
-template <int L>
-__device__ __forceinline__ void load_v_tr(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane) {
-    static_assert(VRegs<L>::PARTS == 1 && VRegs<L>::N * kWaves == 16, "pieces of one 64 x 128 chunk");
+__device__ __forceinline__ void load_v_tr(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane, int part) {
+    static_assert(VRegs<L>::PARTS * VRegs<L>::N * kWaves == (L / 16) * (kDVT / 32), "pieces of one L x 128 chunk");
+    constexpr int NA = L / 16;
     const uint32_t soff = static_cast<uint32_t>(t0) * (kDV * 2) + v0 * 2;
     int ln = lane;   // opaque: the offsets are recomputed per call rather than held across the loop
     asm volatile("" : "+v"(ln));
 #pragma unroll
     for (int i = 0; i < VRegs<L>::N; ++i) {
-        const int pc = wave + kWaves * i, a = pc & 3, b = pc >> 2;
+        const int pc = wave + kWaves * (part * VRegs<L>::N + i), a = pc % NA, b = pc / NA;
         r.v[i] = bload128(R.v, (16 * a + (ln & 15)) * (kDV * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
     }
 }
+template <int L>
+using VtPacked = u32x2_t[2 * VRegs<L>::N * VRegs<L>::PARTS];
 // The transposition on the matrix cores: D = A E_h with A a piece (16 tau x 32 v) and E_h the 32 x 16
 // one-hot selection of its columns 16 h + 0..15 (exact in fp32).  Lane (n = l16, g16) of D holds
 // V[tau 16 a + 4 g16 + j][v 32 b + 16 h + n], j = 0..3: four consecutive tau of one row of V^T, kept
 // packed in pv until the stores below.
 template <int L>
-__device__ __forceinline__ void vt_transpose(u32x2_t (&pv)[2 * VRegs<L>::N], const VRegs<L>& r, int lane) {
+__device__ __forceinline__ void vt_transpose(VtPacked<L>& pv, const VRegs<L>& r, int lane, int part) {
     // E_h in the B-operand layout: lane (l16, g16) holds k slots 8 g16 + 0..7 of column l16, whose
     // one (if any) is slot 16 h + l16.  Built from an opaque copy of the lane index so that it is not
     // hoisted out of the chunk loop (eight more registers held across the loop would spill).
@@ -281,18 +266,17 @@ __device__ __forceinline__ void vt_transpose(u32x2_t (&pv)[2 * VRegs<L>::N], con
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const f32x4_t d = mfma16(r.v[i], E[h], f32x4_t{});
-            pv[2 * i + h] = u32x2_t{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
+            pv[2 * (part * VRegs<L>::N + i) + h] = u32x2_t{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
         }
 }
 // (w V)^T from the packed V^T: row weights wC of the chunk, rounded to bf16 once
 template <int L>
-__device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const u32x2_t (&pv)[2 * VRegs<L>::N], const float* wC,
-                                                int wave, int lane) {
-    constexpr int TP = Cfg<L>::TP;
+__device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const VtPacked<L>& pv, const float* wC, int wave, int lane) {
+    constexpr int TP = Cfg<L>::TP, NA = L / 16;
     const int l16 = lane & 15, g16 = lane >> 4;
 #pragma unroll
-    for (int i = 0; i < VRegs<L>::N; ++i) {
-        const int pc = wave + kWaves * i, a = pc & 3, b = pc >> 2;
+    for (int i = 0; i < VRegs<L>::N * VRegs<L>::PARTS; ++i) {
+        const int pc = wave + kWaves * i, a = pc % NA, b = pc / NA;
         const int tau = 16 * a + 4 * g16;
         const f32x4_t w = *reinterpret_cast<const f32x4_t*>(&wC[tau]);
 #pragma unroll
@@ -306,12 +290,12 @@ __device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const u32x2_t (&p
     }
 }
 template <int L>
-__device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const u32x2_t (&pv)[2 * VRegs<L>::N], int wave, int lane) {
-    constexpr int TP = Cfg<L>::TP;
+__device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const VtPacked<L>& pv, int wave, int lane) {
+    constexpr int TP = Cfg<L>::TP, NA = L / 16;
     const int l16 = lane & 15, g16 = lane >> 4;
 #pragma unroll
-    for (int i = 0; i < VRegs<L>::N; ++i) {
-        const int pc = wave + kWaves * i, a = pc & 3, b = pc >> 2;
+    for (int i = 0; i < VRegs<L>::N * VRegs<L>::PARTS; ++i) {
+        const int pc = wave + kWaves * i, a = pc % NA, b = pc / NA;
 #pragma unroll
         for (int h = 0; h < 2; ++h)
             *reinterpret_cast<u32x2_t*>(&VtT[(32 * b + 16 * h + l16) * TP + 16 * a + 4 * g16]) = pv[2 * i + h];
@@ -469,14 +453,16 @@ constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
 // Staging order (one Q/K block and one part of a V chunk in registers at a time): block 0
 // of a chunk is stored during the previous chunk (at the barrier that opens its last d
 // block), block 1 at the top of the chunk, block p + 1 (p >= 1) at the barrier that opens
-// block p.  The next chunk's V is loaded from the top of a chunk on, part k stored at the
-// barrier that opens d block k + 1.
+// block p.  The next chunk's V is loaded from the top of a chunk on, part k transposed in
+// registers at the barrier that opens d block k + 1; its weighted copy goes to LDS after the
+// S~ barrier (once this chunk's (iv) is done and the next chunk's weights are known), its
+// plain copy at the top of the next chunk (once this chunk's (ii) is done).
 template <int L>
 __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     Smem<L>& S = *reinterpret_cast<Smem<L>*>(smem_raw);
     using CF = Cfg<L>;
-    constexpr int QP = CF::QP, VP = CF::VP, SP = CF::SP, NB = CF::NB, DB = CF::DB, DT = CF::DT, NDB = CF::NDB;
+    constexpr int QP = CF::QP, SP = CF::SP, NB = CF::NB, DB = CF::DB, DT = CF::DT, NDB = CF::NDB;
     constexpr int NT_S = NB * (NB + 1) / 2;          // causal 16x16 tiles of S^T
     constexpr int MAXT = (NT_S + kWaves - 1) / kWaves;
     constexpr int NTT = L / 16;                       // 16-wide tau tiles
@@ -593,7 +579,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 
     QKRegs<L> rqk;
     VRegs<L> rv;
-    u32x2_t pv[2 * VRegs<L>::N];   // L = 64: the next chunk's V^T, packed, until its store
+    VtPacked<L> pv;   // the next chunk's V^T, packed, until its stores
     if (c_begin < c_end) {
         const int t0 = c_begin * L;
         load_qk<L>(rqk, P, t0, 0, tid);
@@ -602,19 +588,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane);
         }
         store_qk<L>(S.QK[0][0], S.QK[0][1], rqk, tid);
-        if constexpr (CF::VTR) {
-            load_v_tr<L>(rv, P, t0, v0, wave, lane);
-            vt_transpose<L>(pv, rv, lane);
-            __syncthreads();   // the first chunk's gates are visible
-            vt_store_scaled<L>(S.Vs[1], pv, S.G[c_begin & 1].wC, wave, lane);
-            vt_store_plain<L>(S.Vs[0], pv, wave, lane);
-        } else {
 #pragma unroll
-            for (int part = 0; part < VRegs<L>::PARTS; ++part) {
-                load_v<L>(rv, P, t0, v0, tid, part);
-                store_v<L>(S.Vs[c_begin & 1], rv, tid, part);
-            }
+        for (int part = 0; part < VRegs<L>::PARTS; ++part) {
+            load_v_tr<L>(rv, P, t0, v0, wave, lane, part);
+            vt_transpose<L>(pv, rv, lane, part);
         }
+        __syncthreads();   // the first chunk's gates are visible
+        vt_store_scaled<L>(S.Vs[1], pv, S.G[c_begin & 1].wC, wave, lane);
+        vt_store_plain<L>(S.Vs[0], pv, wave, lane);
         load_qk<L>(rqk, P, t0, 1, tid);
     }
 
@@ -646,21 +627,17 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         if constexpr (NDB > 2) load_qk<L>(rqk, P, t0, 2, tid);
         else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid);
         if (gate_wave && c + 1 < c_end) load_gates<L>(gi, gf, P, t0 + L, lane);
-        if constexpr (CF::VTR) {
-            // this chunk's plain V^T (its readers in the previous chunk are done); the next chunk's V
-            if (c > c_begin) vt_store_plain<L>(S.Vs[0], pv, wave, lane);
-            if (c + 1 < c_end) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane);
-        } else {
-            // V of the next chunk: part 0 now, part k stored at the barrier that opens d block k + 1
-            if (c + 1 < c_end) load_v<L>(rv, P, t0 + L, v0, tid, 0);
-        }
+        // this chunk's plain V^T (its readers in the previous chunk are done); the next chunk's V,
+        // part 0 now, part k at the barrier that opens d block k + 1
+        if (c > c_begin) vt_store_plain<L>(S.Vs[0], pv, wave, lane);
+        if (c + 1 < c_end) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane, 0);
         const float decay_n = Gc.scal[0];
         const float m_next = Gc.scal[1];
         const float s_new = Gc.scal[2];
         const float c_scale = Gc.scal[3];   // != 1: apply this chunk's decay to C_acc eagerly
         const float* n_old = S.n[cur];
         float* n_new = S.n[cur ^ 1];
-        const uint16_t* Vc = S.Vs[CF::VTR ? 0 : par];   // L = 64: V^T
+        const uint16_t* VtT = S.Vs[0];
         const uint16_t* VwT = S.Vs[1];
 
 #pragma unroll
@@ -686,11 +663,10 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     store_qk<L>(S.QK[0][0], S.QK[0][1], rqk, tid);
                     load_qk<L>(rqk, P, t0 + L, 1, tid);
                 }
-                // V of the next chunk, part p - 1 (its buffer was last read by the previous chunk)
-                if (CF::VTR && p == 1 && c + 1 < c_end) vt_transpose<L>(pv, rv, lane);
-                if (!CF::VTR && p <= VRegs<L>::PARTS && c + 1 < c_end) {
-                    store_v<L>(S.Vs[par ^ 1], rv, tid, p - 1);
-                    if (p < VRegs<L>::PARTS) load_v<L>(rv, P, t0 + L, v0, tid, p);
+                // the next chunk's V, part p - 1, transposed in registers; part p requested
+                if (p <= VRegs<L>::PARTS && c + 1 < c_end) {
+                    vt_transpose<L>(pv, rv, lane, p - 1);
+                    if (p < VRegs<L>::PARTS) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane, p);
                 }
             }
             // (i) S^T += K_p Q_p^T on this wave's causal tiles (L = 128: a fixed tile count per
@@ -769,19 +745,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 if constexpr (L == 64) __builtin_amdgcn_sched_barrier(0);
                 // lane (n = column vcol(vt) + l16, k group g16) holds tau = 32 ks + 8 g16 + 0..7
                 u32x4_t Vw[VT];
-                const float* wv = &Gc.wC[32 * ks + 8 * g16];
 #pragma unroll
-                for (int vt = 0; vt < VT; ++vt) {
-                    if constexpr (CF::VTR) {
-                        Vw[vt] = *reinterpret_cast<const u32x4_t*>(&VwT[(vcol(vt) + l16) * CF::TP + 32 * ks + 8 * g16]);
-                    } else {
-                        const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
-                        const u32x4_t raw = cat(tr_read(vb), tr_read(vb + 4 * VP));
-#pragma unroll
-                        for (int u = 0; u < 4; ++u)
-                            Vw[vt][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
-                    }
-                }
+                for (int vt = 0; vt < VT; ++vt)
+                    Vw[vt] = *reinterpret_cast<const u32x4_t*>(&VwT[(vcol(vt) + l16) * CF::TP + 32 * ks + 8 * g16]);
 #pragma unroll
                 for (int q = 0; q < NQ; ++q)
 #pragma unroll
@@ -868,11 +834,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * T + 16 + 4 * g16]) = u32x2_t{0u, 0u};
         }
         __syncthreads();
-        // L = 64: the next chunk's scaled V^T (its readers, (iv) of this chunk, are done; the next
-        // chunk's weights are visible)
-        if constexpr (CF::VTR) {
-            if (c + 1 < c_end) vt_store_scaled<L>(S.Vs[1], pv, S.G[par ^ 1].wC, wave, lane);
-        }
+        // the next chunk's scaled V^T (its readers, (iv) of this chunk, are done; the next chunk's
+        // weights are visible)
+        if (c + 1 < c_end) vt_store_scaled<L>(S.Vs[1], pv, S.G[par ^ 1].wC, wave, lane);
         // (ii) N^T = interC * N^T + V^T S~^T, then h = N^T / max(|den|, floor); with DH = 2 each
         // d partition finishes the tau tiles T with T % 2 == dh, after adding the other's partial
 #pragma unroll
@@ -893,13 +857,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 #pragma unroll
                 for (int ks = 0; ks <= T / 2; ++ks) {
                     const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&St[tau * SP + 32 * ks + 8 * g16]);
-                    u32x4_t va;
-                    if constexpr (CF::VTR) {
-                        va = *reinterpret_cast<const u32x4_t*>(&Vc[(vcol(vt) + l16) * CF::TP + 32 * ks + 8 * g16]);
-                    } else {
-                        const uint16_t* vb = &Vc[(32 * ks + tr_row) * VP + vcol(vt) + tr_col];
-                        va = cat(tr_read(vb), tr_read(vb + 4 * VP));
-                    }
+                    const u32x4_t va = *reinterpret_cast<const u32x4_t*>(&VtT[(vcol(vt) + l16) * CF::TP + 32 * ks + 8 * g16]);
                     acc = mfma16(va, b, acc);
                 }
                 u32x2_t o;

@@ -45,7 +45,7 @@ extern "C" {
 typedef enum {
     MLSTM_OK = 0,
     MLSTM_ERR_NULL_PTR = 1,     /* a required pointer is NULL                         */
-    MLSTM_ERR_BAD_SHAPE = 2,    /* negative/zero size, or T % L != 0                  */
+    MLSTM_ERR_BAD_SHAPE = 2,    /* negative/zero size, or a size product overflows    */
     MLSTM_ERR_UNSUPPORTED = 3,  /* (dtype, DQK, DV, L) combination not built          */
     MLSTM_ERR_MISALIGNED = 4,   /* a tensor base pointer is not 16-byte aligned       */
     MLSTM_ERR_ALIAS = 5,        /* outputs overlap inputs in a way that is not allowed */
@@ -72,7 +72,10 @@ typedef enum {
  *   h  [B, NH, T, DV]       (dt)       output h~ for every step
  *   CT [B, NH, DQK, DV], nT [B, NH, DQK], mT [B, NH]   fp32 final state
  *
- * L is the chunk size; T % L == 0 is required (else MLSTM_ERR_BAD_SHAPE).
+ * L is the chunk size.  T need not be a multiple of L: the last chunk is
+ * then partial, its missing tokens taken as neutral (no input, no decay:
+ * i~ = -inf, f~ = +inf), which leaves the state unchanged, and their h rows
+ * are not written.
  * T == 0 copies the initial state to the final state; q, k, v, ipre, fpre
  * and h are then not accessed and may be NULL.  The result does not
  * depend on L except through rounding; mT equals the recurrent m_T of Eq. 2.

@@ -42,7 +42,7 @@ const char* mlstm_status_string(mlstm_status s) {
     switch (s) {
         case MLSTM_OK: return "MLSTM_OK";
         case MLSTM_ERR_NULL_PTR: return "MLSTM_ERR_NULL_PTR: a required pointer is NULL, or the initial state is partially given";
-        case MLSTM_ERR_BAD_SHAPE: return "MLSTM_ERR_BAD_SHAPE: invalid size, or T is not a multiple of L";
+        case MLSTM_ERR_BAD_SHAPE: return "MLSTM_ERR_BAD_SHAPE: invalid size";
         case MLSTM_ERR_UNSUPPORTED: return "MLSTM_ERR_UNSUPPORTED: this (dtype, DQK, DV, L) combination is not built";
         case MLSTM_ERR_MISALIGNED: return "MLSTM_ERR_MISALIGNED: a tensor pointer is not 16-byte aligned";
         case MLSTM_ERR_ALIAS: return "MLSTM_ERR_ALIAS: an output overlaps an input or another output";
@@ -55,7 +55,7 @@ const char* mlstm_status_string(mlstm_status s) {
 int mlstm_version(void) { return 100; }
 
 size_t mlstm_chunkwise_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L, mlstm_dtype dt) {
-    if (B <= 0 || NH <= 0 || T < 0 || L <= 0 || (T % L)) return 0;
+    if (B <= 0 || NH <= 0 || T < 0 || L <= 0) return 0;
     if (!mlstm::chunk_mfma_supported(dt, DQK, DV, L)) return 0;
     return mlstm::chunk_mfma_workspace_bytes(B, NH, T, DQK, DV, L);
 }
@@ -73,7 +73,6 @@ mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, ml
     if (workspace_bytes > 0 && !workspace) return MLSTM_ERR_NULL_PTR;
     if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
     if (B <= 0 || NH <= 0 || T < 0 || DQK <= 0 || DV <= 0 || L <= 0) return MLSTM_ERR_BAD_SHAPE;
-    if (T % L) return MLSTM_ERR_BAD_SHAPE;
 
     int64_t S, ST, nq, nv, nC, nn;
     if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &ST) || !mul_ok(ST, DQK, &nq) || !mul_ok(ST, DV, &nv) ||

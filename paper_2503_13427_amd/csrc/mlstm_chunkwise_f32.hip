@@ -89,14 +89,18 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
     TIn* hb = h + seq * static_cast<int64_t>(T) * DV;
 
     for (int t0 = 0; t0 < T; t0 += L) {
+        // rows lc..L-1 of a partial last chunk are neutral tokens: zero q, k, v, no input
+        // (x = -inf) and no decay, so they leave the state unchanged; their h is not written
+        const int lc = min(L, T - t0);
         // stage the chunk
         for (int e = tid; e < L * DQK; e += kF32Threads) {
-            Qs[e] = io<TIn>::load(qb, static_cast<int64_t>(t0) * DQK + e) * qscale;
-            Ks[e] = io<TIn>::load(kb, static_cast<int64_t>(t0) * DQK + e);
+            const bool ok = e < lc * DQK;
+            Qs[e] = ok ? io<TIn>::load(qb, static_cast<int64_t>(t0) * DQK + e) * qscale : 0.0f;
+            Ks[e] = ok ? io<TIn>::load(kb, static_cast<int64_t>(t0) * DQK + e) : 0.0f;
         }
         for (int e = tid; e < L * DVT; e += kF32Threads) {
             const int t = e / DVT, j = e % DVT;
-            Vs[e] = io<TIn>::load(vb, static_cast<int64_t>(t0 + t) * DV + v0 + j);
+            Vs[e] = t < lc ? io<TIn>::load(vb, static_cast<int64_t>(t0 + t) * DV + v0 + j) : 0.0f;
         }
         // chunkwise gates and max state: a short serial scan (L <= 64)
         if (tid == 0) {
@@ -105,8 +109,8 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
             const float* fb = fpre + seq * static_cast<int64_t>(T) + t0;
             float b = 0.0f, p = -INFINITY;
             for (int t = 0; t < L; ++t) {
-                b += logsigmoid(fb[t]);
-                const float x = ib[t] - b;
+                if (t < lc) b += logsigmoid(fb[t]);
+                const float x = t < lc ? ib[t] - b : -INFINITY;
                 p = fmaxf(p, x);
                 const float M = fmaxf(mprev, p);
                 g_ib[t] = x;
@@ -146,7 +150,7 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
         __syncthreads();
 
         // numerators and output combination
-        for (int e = tid; e < L * DVT; e += kF32Threads) {
+        for (int e = tid; e < lc * DVT; e += kF32Threads) {
             const int t = e / DVT, j = e % DVT;
             float inter = 0.0f;
             for (int d = 0; d < DQK; ++d) inter += Qs[t * DQK + d] * Cs[d * DVT + j];

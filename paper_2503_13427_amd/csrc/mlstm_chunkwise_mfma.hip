@@ -359,17 +359,21 @@ __device__ __forceinline__ float flogsig(float x) {
 
 // Gate phase of one chunk (run by one wave): in-chunk prefix sums and maxima, the max
 // state, the lazy C scale, and every per-row scale of the chunk.  m_prev and s_cur
-// carry the max state and the lazy log-scale from chunk to chunk.
+// carry the max state and the lazy log-scale from chunk to chunk.  Rows at or beyond
+// nvalid (the partial last chunk of a sequence) are neutral tokens: no input (x = -inf)
+// and no decay (logsig f~ = 0), so they leave the state unchanged.
 template <int L>
 __device__ __forceinline__ void gate_phase(GateBuf<L>& Gb, const float (&gi)[2], const float (&gf)[2], float& m_prev,
-                                           float& s_cur, int lane) {
-    const float b = wave_incl_sum(flogsig(gf[0]));
-    const float x = gi[0] - b;
+                                           float& s_cur, int lane, int nvalid) {
+    const bool ok0 = lane < nvalid;
+    const float b = wave_incl_sum(ok0 ? flogsig(gf[0]) : 0.0f);
+    const float x = ok0 ? gi[0] - b : -INFINITY;
     const float p = wave_incl_max(x);
     float b2 = 0.f, x2 = 0.f, p2 = 0.f;
     if constexpr (L == 128) {
-        b2 = lane63(b) + wave_incl_sum(flogsig(gf[1]));
-        x2 = gi[1] - b2;
+        const bool ok1 = 64 + lane < nvalid;
+        b2 = lane63(b) + wave_incl_sum(ok1 ? flogsig(gf[1]) : 0.0f);
+        x2 = ok1 ? gi[1] - b2 : -INFINITY;
         p2 = fmaxf(lane63(p), wave_incl_max(x2));
     }
     const float pL = lane63(L == 128 ? p2 : p);
@@ -501,7 +505,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     const int g = sg % A.G;
     const int s = sg / A.G;
     const int v0 = tile * kDVT;
-    const int nc_total = A.T / L;
+    const int nc_total = (A.T + L - 1) / L;   // the last chunk may be partial
     const int c_begin = g * A.seg_chunks;
     const int c_end = min(nc_total, c_begin + A.seg_chunks);
 
@@ -585,7 +589,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         load_qk<L>(rqk, P, t0, 0, tid);
         if (gate_wave) {
             load_gates<L>(gi, gf, P, t0, lane);
-            gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane);
+            gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane, A.T - t0);
         }
         store_qk<L>(S.QK[0][0], S.QK[0][1], rqk, tid);
 #pragma unroll
@@ -780,7 +784,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         }
 
         // gates of the next chunk, one chunk ahead
-        if (gate_wave && c + 1 < c_end) gate_phase<L>(S.G[par ^ 1], gi, gf, g_m, g_s, lane);
+        if (gate_wave && c + 1 < c_end) gate_phase<L>(S.G[par ^ 1], gi, gf, g_m, g_s, lane, A.T - (t0 + L));
 
         // finish Q n: columns 0 and 1 of the 16x16 tile are lanes l16 = 0 and 1
 #pragma unroll
@@ -864,11 +868,12 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 o[0] = pack_bf16x2(acc[0] * hv, acc[1] * hv);
                 o[1] = pack_bf16x2(acc[2] * hv, acc[3] * hv);
                 if constexpr (L == 128) {
-                    // 32-bit offsets into the sequence's h: no 64-bit addresses to keep per tau tile
+                    // 32-bit offsets into the sequence's h: no 64-bit addresses to keep per tau tile; rows
+                    // beyond T (a partial last chunk) fall outside the buffer range and are dropped
                     __builtin_amdgcn_raw_buffer_store_b64(o, P.h,
                                                           static_cast<uint32_t>(tau * kDV + v0 + vcol(vt) + 4 * g16) * 2,
                                                           static_cast<uint32_t>(t0) * (kDV * 2), 0);
-                } else {
+                } else if (t0 + tau < A.T) {
                     *reinterpret_cast<u32x2_t*>(A.h + (static_cast<int64_t>(s) * A.T + t0 + tau) * kDV + v0 + vcol(vt) +
                                                 4 * g16) = o;
                 }
@@ -1230,7 +1235,7 @@ bool chunk_mfma_supported(mlstm_dtype dt, int DQK, int DV, int L) {
 
 int chunk_mfma_segments(int B, int NH, int T, int L) {
     const int S = B * NH;
-    const int nc = T / L;
+    const int nc = (T + L - 1) / L;
     if (nc <= 1) return 1;
     const int wgs = S * kNTile;
     constexpr int kTargetWGs = 256;
@@ -1246,14 +1251,14 @@ size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L) 
     (void)DV;
     const int G = chunk_mfma_segments(B, NH, T, L);
     if (G <= 1) return 0;
-    const int nc = T / L;
+    const int nc = (T + L - 1) / L;
     const int seg_tokens = ((nc + G - 1) / G) * L;
     return static_cast<size_t>(B) * NH * (G - 1) * local_subsegments(seg_tokens) * kSlotFloats * sizeof(float);
 }
 
 hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream) {
     const int S = a.B * a.NH;
-    const int nc = a.T / a.L;
+    const int nc = (a.T + a.L - 1) / a.L;
     int G = workspace ? chunk_mfma_segments(a.B, a.NH, a.T, a.L) : 1;
     if (G > 1 && workspace_bytes < chunk_mfma_workspace_bytes(a.B, a.NH, a.T, a.DQK, a.DV, a.L)) G = 1;
     if (nc == 0) G = 1;

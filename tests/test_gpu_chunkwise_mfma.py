@@ -3,9 +3,10 @@ fp64 recurrent oracle.
 
 Parity bar: max relative error <= 2e-2 per (batch, head) slice for h and the final state
 (bf16 q/k/v/h, fp32 state).  Covers several chunks and segments, an initial state, the
-floor branch, short and long memory, the soft-capped gates, T = 0, the segment-parallel
-schedule (workspace), chunk-size independence, state carry, decode steps == prefill,
-run-to-run determinism, and the three prefill workloads at full size (sampled heads).
+floor branch, short and long memory, the soft-capped gates, T = 0, a partial last chunk
+(T not a multiple of L: no h row beyond T is written), the segment-parallel schedule
+(workspace), chunk-size independence, state carry, decode steps == prefill, run-to-run
+determinism, and the three prefill workloads at full size (sampled heads).
 """
 import numpy as np
 import pytest
@@ -69,6 +70,12 @@ CASES = [
     (1, 2, 256, 64, GateDist(f_mu=-1.0, f_sd=2.0), StateDist()),  # short memory
     (1, 1, 64, 64, GateDist(), StateDist()),                     # a single chunk
     (1, 1, 128, 128, GateDist(i_mu=2.0, i_sd=3.0), None),        # large input gates
+    # partial last chunk
+    (1, 2, 100, 64, GateDist(), None),
+    (1, 1, 17, 64, GateDist(), StateDist()),                     # one partial chunk
+    (1, 2, 300, 128, GateDist(f_mu=5, f_sd=2, cap=15.0), StateDist()),
+    (1, 2, 1000, 64, GateDist(), StateDist()),                   # 8 segments, the last one ragged
+    (1, 1, 700, 128, GateDist(), None),
 ]
 
 
@@ -79,6 +86,28 @@ def test_mfma_matches_oracle(case, workspace):
     inp = make_prefill(workload=95, B=B, NH=NH, T=T, DQK=256, DV=512, dtype="bf16", gates=g, state=st)
     o = run(inp, L, workspace=workspace)
     check(inp, o, label=str(case))
+
+
+@pytest.mark.parametrize("T,L", [(100, 64), (300, 128), (1000, 64)])
+def test_partial_chunk_writes_no_row_beyond_T(T, L):
+    """h is a view of the first T rows of a larger buffer: the rows after it keep their
+    sentinel, and the chunk-size-independent result matches the oracle."""
+    inp = make_prefill(workload=97, B=1, NH=1, T=T, DQK=256, DV=512, dtype="bf16", gates=GateDist(),
+                       state=StateDist())
+    d = upload_prefill(inp)
+    o = alloc_prefill_outputs(inp)
+    big = torch.full((T + 128, 512), -7.0, dtype=torch.bfloat16, device="cuda")
+    h = big[:T].view(1, 1, T, 512)
+    for workspace in (False, True):
+        ws = None
+        nb = _mb().mlstm_chunkwise_workspace_bytes(1, 1, T, 256, 512, L)
+        if workspace and nb:
+            ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        _mb().mlstm_chunkwise_fwd(d["q"], d["k"], d["v"], d["ipre"], d["fpre"], d["C0"], d["n0"], d["m0"], L,
+                                  h, o["CT"], o["nT"], o["mT"], workspace=ws)
+        torch.cuda.synchronize()
+        assert bool((big[T:] == -7.0).all()), "a row beyond T was written"
+        check(inp, dict(h=h, CT=o["CT"], nT=o["nT"], mT=o["mT"]), label=f"T{T}L{L}ws{workspace}")
 
 
 def test_segment_schedule_is_used_and_agrees():

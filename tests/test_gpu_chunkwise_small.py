@@ -57,6 +57,9 @@ SMALL = [
     (1, 4, 192, 16, 128, 64, "f32", True, GateDist(f_mu=-1, f_sd=2)),
     (1, 2, 64, 128, 16, 16, "f32", False, GateDist()),
     (3, 2, 128, 32, 32, 32, "bf16", True, GateDist()),
+    # partial last chunk
+    (1, 2, 50, 16, 16, 16, "f32", True, GateDist()),
+    (2, 1, 70, 32, 64, 32, "f32", False, GateDist(f_mu=5, f_sd=2, cap=15.0)),
 ]
 
 

@@ -28,6 +28,9 @@ Forms, each written from the paper's statement of the cell (Sec. 2):
                              matrix, gated logits, intra-chunk numerator and
                              denominator, output combination), for any chunk size;
                              the last chunk may be shorter.
+* ``output_gate_norm``       the hidden-state output h = o * Norm(h~) with o = sigmoid(o~)
+                             (Eq. 6 with Eq. 9), Norm the headwise LayerNorm or RMSNorm that
+                             Sec. 2 allows; it takes [B, NH, T, DV] rows, not the S axis.
 """
 from __future__ import annotations
 
@@ -194,3 +197,37 @@ def chunkwise(q, k, v, ipre, fpre, C0=None, n0=None, m0=None, L=64):
             mp = m_k
         C[s], n[s], m[s] = Cs, ns, mp
     return h, C, n, m
+
+
+def sigmoid(x):
+    """1 / (1 + exp(-x)), written so that neither branch overflows."""
+    x = np.asarray(x, dtype=np.float64)
+    e = np.exp(-np.abs(x))
+    return np.where(x >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+
+
+def output_gate_norm(h_tilde, o_pre, weight=None, bias=None, eps=1e-6, norm="layer"):
+    """Hidden-state output h = o * Norm(h~), o = sigmoid(o~) (Eq. 6 with Eq. 9).
+
+    Norm acts on each row of DV values, one head at one step (the headwise norm of Sec. 2 and
+    of the 7B model's cell), then scales by ``weight`` and shifts by ``bias`` (both [NH, DV],
+    None meaning 1 and 0):
+      layer: (x - mean(x)) / sqrt(var(x) + eps), var the mean squared deviation;
+      rms:   x / sqrt(mean(x^2) + eps).
+    h_tilde, o_pre: [B, NH, T, DV].  Returns h [B, NH, T, DV] in fp64.
+    """
+    x = np.asarray(h_tilde, dtype=np.float64)
+    o = np.asarray(o_pre, dtype=np.float64)
+    assert x.ndim == 4 and o.shape == x.shape
+    if norm == "layer":
+        mu = x.mean(axis=-1, keepdims=True)
+        y = (x - mu) / np.sqrt(((x - mu) ** 2).mean(axis=-1, keepdims=True) + eps)
+    elif norm == "rms":
+        y = x / np.sqrt((x * x).mean(axis=-1, keepdims=True) + eps)
+    else:
+        raise ValueError(norm)
+    if weight is not None:
+        y = y * np.asarray(weight, dtype=np.float64)[None, :, None, :]
+    if bias is not None:
+        y = y + np.asarray(bias, dtype=np.float64)[None, :, None, :]
+    return sigmoid(o) * y

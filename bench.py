@@ -14,8 +14,12 @@ Extra objects on the same line:
   cpu_baseline  the fp64 CPU oracle on the same workload (host cores);
   decode        1024 consecutive mlstm_step calls at B=256, NH=8: us per step,
                 us per sequence-token, achieved GB/s vs 8 TB/s;
-  prefill       the two larger prefill workloads (B=8 x T=8192 soft-capped,
-                and B=4 x T=32768 from a nonzero state, L=128).
+  prefill_large the two larger prefill workloads (B=8 x T=8192 soft-capped,
+                and B=4 x T=32768 from a nonzero state, L=128);
+  output_norm   the hidden-state output h = sigmoid(o~) * LayerNorm(h~) w + b
+                (mlstm_output_norm) on the headline prefill's h shape and the
+                decode step's h shape: us per call and achieved GB/s vs 8 TB/s.
+Every timed section is preceded by 0.25 s of untimed calls (clock settle).
 """
 from __future__ import annotations
 
@@ -206,6 +210,24 @@ def bench_decode(w, steps, stream, warm=16):
                 wall_s=wall, state_finite=finite)
 
 
+def bench_output_norm(B, NH, T, DV, steps, stream, label):
+    """h = sigmoid(o~) * LayerNorm(h~) * w + b on bf16 rows already in HBM (HBM-bound)."""
+    from paper_2503_13427_amd import binding as mb
+    g = torch.Generator(device="cuda").manual_seed(5)
+    shape = (B, NH, T, DV)
+    x = torch.randn(shape, generator=g, device="cuda").bfloat16()
+    o = torch.randn(shape, generator=g, device="cuda").bfloat16()
+    w = torch.randn(NH, DV, generator=g, device="cuda") * 0.2 + 1
+    b = torch.randn(NH, DV, generator=g, device="cuda") * 0.2
+    h = torch.empty_like(x)
+    fn = lambda: mb.mlstm_output_norm(x, o, w, b, 1e-6, "layer", h, stream=stream)
+    _, ev = time_steps(fn, steps, 10, stream)
+    t = ev / steps
+    by = acc.output_norm_bytes(B, NH, T, DV)
+    return dict(workload=label, rows=B * NH * T, dv=DV, us_per_call=t * 1e6, bytes_per_call=by,
+                gbs=by / t / 1e9, hbm_frac=by / t / 1e9 / acc.PEAK_HBM_GBS)
+
+
 def cpu_baseline(w, max_seconds=30.0):
     """The fp64 oracle on the headline workload, timed on the host.  Heads are independent, so
     the sample is a subset of heads over the full sequence (all heads if they fit the budget)."""
@@ -231,8 +253,9 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=1024)
     ap.add_argument("--skip-decode", action="store_true")
     ap.add_argument("--skip-large", action="store_true")
+    ap.add_argument("--skip-output-norm", action="store_true")
     ap.add_argument("--skip-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=["prefill", "decode", "large", "calls"], default=None,
+    ap.add_argument("--only", choices=["prefill", "decode", "large", "output_norm", "calls"], default=None,
                     help="run one part only (profiling runs); 'calls' makes --calls untimed prefill calls of "
                          "--workload and then one --copy-mib MiB device copy, for counter runs")
     ap.add_argument("--workload", default=configs.PREFILL_T2048.name,
@@ -284,6 +307,11 @@ def main():
             res["prefill_large"].append(r)
             del p
             torch.cuda.empty_cache()
+    if args.only in (None, "output_norm") and not args.skip_output_norm:
+        log("output gate + headwise LayerNorm on the prefill and decode h shapes")
+        res["output_norm"] = [bench_output_norm(w.B, w.NH, w.T, w.DV, args.steps, stream, "prefill_B1_NH8_T2048_DV512"),
+                              bench_output_norm(256, 8, 1, 512, args.steps, stream, "decode_B256_NH8_DV512")]
+        torch.cuda.empty_cache()
     if args.only in (None, "decode") and not args.skip_decode:
         log(f"decode {configs.DECODE_B256.name}: {args.decode_steps} steps")
         res["decode"] = bench_decode(configs.DECODE_B256, args.decode_steps, stream)
@@ -309,6 +337,8 @@ def main():
         line["prefill_large"] = res["prefill_large"]
     if "decode" in res:
         line["decode"] = res["decode"]
+    if "output_norm" in res:
+        line["output_norm"] = res["output_norm"]
     if not args.skip_cpu_baseline and args.only in (None, "prefill"):
         log("cpu baseline: fp64 oracle")
         line["cpu_baseline"] = cpu_baseline(w)

@@ -11,7 +11,8 @@
  *   n_t  = f_t n_{t-1} + i_t k_t                (DQK, fp32)
  *   h_t  = C_t^T q^_t / max(|n_t^T q^_t|, exp(-m_t))
  *
- * h is the h~ of Eq. 5: the output gate and Norm of Eq. 6 are not applied.
+ * h is the h~ of Eq. 5.  The output gate and Norm of Eq. 6 are a separate
+ * entry point, mlstm_output_norm, applied to h~ and o~ afterwards.
  * h_{t-1} is not an input (Eq. 1 lists it, Eqs. 2-9 never use it).
  *
  * Conventions shared by every entry point:
@@ -129,6 +130,34 @@ mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype
                         const float* C, const float* n, const float* m,
                         int B, int NH, int DQK, int DV,
                         void* h, float* C_out, float* n_out, float* m_out, void* hip_stream);
+
+typedef enum {
+    MLSTM_NORM_LAYER = 0,   /* LayerNorm: (x - mean(x)) / sqrt(var(x) + eps)  */
+    MLSTM_NORM_RMS = 1      /* RMSNorm:   x / sqrt(mean(x^2) + eps)           */
+} mlstm_norm;
+
+/*
+ * Hidden-state output of the cell (Eq. 6 with the output gate of Eq. 9):
+ * for every (b, head, t) row of DV values
+ *
+ *   h_row = sigmoid(o~_row) * (Norm(h~_row) * weight[head] + bias[head])
+ *
+ * Norm is the headwise norm (Sec. 2 allows RMSNorm or LayerNorm; the 7B
+ * model uses LayerNorm), computed in fp32 over the row; var is the mean
+ * squared deviation.
+ *
+ *   h_tilde, o_pre, h [B, NH, T, DV] (dt)   (a decode step is T = 1)
+ *   weight, bias [NH, DV] fp32, either may be NULL (weight 1, bias 0)
+ *
+ * eps must be finite and > 0; norm is MLSTM_NORM_LAYER or MLSTM_NORM_RMS
+ * (else MLSTM_ERR_BAD_SHAPE).  Built: DV a multiple of 4, DV <= 2048 (else
+ * MLSTM_ERR_UNSUPPORTED).  T == 0 launches nothing.  h may equal h_tilde
+ * (in place: each row is read before it is written); any other overlap of h
+ * with an input is MLSTM_ERR_ALIAS.
+ */
+mlstm_status mlstm_output_norm(const void* h_tilde, const void* o_pre, mlstm_dtype dt,
+                               const float* weight, const float* bias, float eps, mlstm_norm norm,
+                               int B, int NH, int T, int DV, void* h, void* hip_stream);
 
 /* Static, human-readable name of a status code. */
 const char* mlstm_status_string(mlstm_status s);

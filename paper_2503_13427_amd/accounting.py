@@ -90,3 +90,9 @@ def step_flops(B: int, NH: int, dqk: int, dv: int) -> int:
     read-out C'^T q^ one multiply-add (2 FLOPs) per element; n and its dot product add 6 per row."""
     S = B * NH
     return S * (5 * dqk * dv + 6 * dqk)
+
+
+def output_norm_bytes(B: int, NH: int, T: int, dv: int, elem_bytes: int = 2, affine: bool = True) -> int:
+    """Algorithmic HBM bytes of the hidden-state output h = sigmoid(o~) * (Norm(h~) w + b): every
+    row of h~ and o~ read once and of h written once, plus the per-head weight and bias once."""
+    return 3 * B * NH * T * dv * elem_bytes + (2 * NH * dv * 4 if affine else 0)

@@ -26,6 +26,8 @@ lib = ctypes.CDLL(LIB_PATH)
 MLSTM_OK = 0
 MLSTM_F32 = 0
 MLSTM_BF16 = 1
+MLSTM_NORM_LAYER = 0
+MLSTM_NORM_RMS = 1
 STATUS_NAMES = {0: "MLSTM_OK", 1: "MLSTM_ERR_NULL_PTR", 2: "MLSTM_ERR_BAD_SHAPE", 3: "MLSTM_ERR_UNSUPPORTED",
                 4: "MLSTM_ERR_MISALIGNED", 5: "MLSTM_ERR_ALIAS", 6: "MLSTM_ERR_WORKSPACE", 7: "MLSTM_ERR_HIP"}
 
@@ -38,6 +40,8 @@ lib.mlstm_chunkwise_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i]
 lib.mlstm_chunkwise_workspace_bytes.restype = ctypes.c_size_t
 lib.mlstm_step.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp]
 lib.mlstm_step.restype = _i
+lib.mlstm_output_norm.argtypes = [_vp, _vp, _i, _vp, _vp, ctypes.c_float, _i, _i, _i, _i, _i, _vp, _vp]
+lib.mlstm_output_norm.restype = _i
 lib.mlstm_status_string.argtypes = [_i]
 lib.mlstm_status_string.restype = ctypes.c_char_p
 lib.mlstm_version.argtypes = []
@@ -114,3 +118,18 @@ def mlstm_step(q, k, v, ipre, fpre, C, n, m, h, C_out, n_out, m_out, stream=None
     _check(lib.mlstm_step(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre), _ptr(C),
                           _ptr(n), _ptr(m), B, NH, DQK, DV, _ptr(h), _ptr(C_out), _ptr(n_out), _ptr(m_out),
                           _stream(stream)))
+
+
+def mlstm_output_norm(h_tilde, o_pre, weight, bias, eps: float, norm: str, h, stream=None) -> None:
+    """Hidden-state output h = sigmoid(o~) * (Norm(h~) * weight + bias) over the rows of
+    h_tilde / o_pre / h [B, NH, T, DV] (a decode step: [B, NH, DV], taken as T = 1); weight and
+    bias [NH, DV] fp32 or None; norm "layer" or "rms".  h may be h_tilde (in place)."""
+    shape = h_tilde.shape
+    if len(shape) == 3:
+        B, NH, DV = shape
+        T = 1
+    else:
+        B, NH, T, DV = shape
+    code = {"layer": MLSTM_NORM_LAYER, "rms": MLSTM_NORM_RMS}[norm]
+    _check(lib.mlstm_output_norm(_ptr(h_tilde), _ptr(o_pre), _dtype_code(h_tilde), _ptr(weight), _ptr(bias),
+                                 float(eps), code, B, NH, T, DV, _ptr(h), _stream(stream)))

@@ -19,7 +19,8 @@ OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmlstm.so")
 ARCH = "gfx950"
 
-SOURCES = ["mlstm_abi.cpp", "mlstm_step.hip", "mlstm_chunkwise_f32.hip", "mlstm_chunkwise_mfma.hip"]
+SOURCES = ["mlstm_abi.cpp", "mlstm_step.hip", "mlstm_chunkwise_f32.hip", "mlstm_chunkwise_mfma.hip",
+           "mlstm_output_norm.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Wall", "-Wno-unused-result"]
 NO_PACKED_FP32 = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

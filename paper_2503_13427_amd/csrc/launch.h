@@ -15,6 +15,12 @@ hipError_t launch_step(mlstm_dtype dt, const void* q, const void* k, const void*
                        hipStream_t stream);
 size_t step_lds_bytes(int DQK, int DV);
 
+// --- hidden-state output: output gate and headwise norm ----------------------
+constexpr int kOutNormMaxDV = 2048;
+hipError_t launch_output_norm(mlstm_dtype dt, const void* h_tilde, const void* o_pre, const float* weight,
+                              const float* bias, float eps, int rms, int64_t rows, int NH, int T, int DV, void* h,
+                              hipStream_t stream);
+
 // --- chunkwise prefill, fp32 VALU kernel (small heads) -----------------------
 struct ChunkArgs {
     const void* q;

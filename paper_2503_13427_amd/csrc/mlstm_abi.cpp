@@ -161,4 +161,32 @@ mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype
     return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
 }
 
+mlstm_status mlstm_output_norm(const void* h_tilde, const void* o_pre, mlstm_dtype dt, const float* weight,
+                               const float* bias, float eps, mlstm_norm norm, int B, int NH, int T, int DV,
+                               void* h, void* hip_stream) {
+    if (T != 0 && (!h_tilde || !o_pre || !h)) return MLSTM_ERR_NULL_PTR;
+    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (B <= 0 || NH <= 0 || T < 0 || DV <= 0) return MLSTM_ERR_BAD_SHAPE;
+    if (!(eps > 0.0f) || eps > 3.0e38f) return MLSTM_ERR_BAD_SHAPE;   // rejects NaN and inf too
+    if (norm != MLSTM_NORM_LAYER && norm != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
+    if ((DV % 4) || DV > mlstm::kOutNormMaxDV) return MLSTM_ERR_UNSUPPORTED;
+    int64_t S, rows, nel, nw;
+    if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &rows) || !mul_ok(rows, DV, &nel) || !mul_ok(NH, DV, &nw) ||
+        rows / 4 >= INT32_MAX)
+        return MLSTM_ERR_BAD_SHAPE;
+    const void* ptrs[] = {h_tilde, o_pre, weight, bias, h};
+    for (const void* p : ptrs)
+        if (misaligned(p)) return MLSTM_ERR_MISALIGNED;
+    const size_t eb = elem_bytes(dt);
+    const Range rx = range_of(h_tilde, nel * eb), ro = range_of(o_pre, nel * eb), rh = range_of(h, nel * eb);
+    const Range rw = range_of(weight, weight ? nw * 4 : 0), rb = range_of(bias, bias ? nw * 4 : 0);
+    // h may be h_tilde exactly (in place) and overlaps nothing else
+    if ((overlap(rh, rx) && h != h_tilde) || overlap(rh, ro) || overlap(rh, rw) || overlap(rh, rb))
+        return MLSTM_ERR_ALIAS;
+    if (rows == 0) return MLSTM_OK;
+    hipError_t e = mlstm::launch_output_norm(dt, h_tilde, o_pre, weight, bias, eps, norm == MLSTM_NORM_RMS, rows, NH,
+                                             T, DV, h, static_cast<hipStream_t>(hip_stream));
+    return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
 }  // extern "C"

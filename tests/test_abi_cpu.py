@@ -25,7 +25,7 @@ def declared_functions():
 
 def test_header_declares_expected_entry_points():
     assert declared_functions() == sorted(["mlstm_chunkwise_fwd", "mlstm_chunkwise_workspace_bytes", "mlstm_step",
-                                           "mlstm_status_string", "mlstm_version"])
+                                           "mlstm_output_norm", "mlstm_status_string", "mlstm_version"])
 
 
 @pytest.mark.parametrize("name", declared_functions())
@@ -168,3 +168,52 @@ def test_step_alias(out, inp, off):
     a = step_args()
     a[out] = a[inp] + off
     assert call_step(a) == 5
+
+
+# ---- output gate + norm validation ---------------------------------------------------------------
+
+def norm_args(**over):
+    a = dict(x=fake(0), o=fake(1), dt=Bd.MLSTM_BF16, w=fake(2), b=fake(3), eps=1e-6, norm=Bd.MLSTM_NORM_LAYER,
+             B=1, NH=8, T=2048, DV=512, h=fake(4), stream=None)
+    a.update(over)
+    return a
+
+
+def call_norm(a):
+    return lib.mlstm_output_norm(a["x"], a["o"], a["dt"], a["w"], a["b"], a["eps"], a["norm"], a["B"], a["NH"],
+                                 a["T"], a["DV"], a["h"], a["stream"])
+
+
+@pytest.mark.parametrize("field", ["x", "o", "h"])
+def test_norm_null_pointer(field):
+    assert call_norm(norm_args(**{field: None})) == 1
+
+
+def test_norm_empty_rows_is_ok_without_pointers():
+    # T == 0: nothing to do, no row pointer needed, nothing launched
+    assert call_norm(norm_args(T=0, x=None, o=None, h=None)) == 0
+
+
+@pytest.mark.parametrize("over", [dict(B=0), dict(NH=-1), dict(T=-1), dict(DV=0), dict(eps=0.0), dict(eps=-1e-6),
+                                  dict(eps=float("nan")), dict(eps=float("inf")), dict(norm=2)])
+def test_norm_bad_shape(over):
+    assert call_norm(norm_args(**over)) == 2
+
+
+@pytest.mark.parametrize("over", [dict(dt=3), dict(DV=6), dict(DV=4096)])
+def test_norm_unsupported(over):
+    assert call_norm(norm_args(**over)) == 3
+
+
+@pytest.mark.parametrize("field", ["x", "o", "w", "b", "h"])
+def test_norm_misaligned(field):
+    a = norm_args()
+    a[field] += 8
+    assert call_norm(a) == 4
+
+
+@pytest.mark.parametrize("inp,off", [("x", 16), ("o", 0), ("o", 4096), ("w", 0), ("b", 16)])
+def test_norm_alias(inp, off):
+    a = norm_args()
+    a["h"] = a[inp] + off
+    assert call_norm(a) == 5

@@ -479,9 +479,6 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g16 = lane >> 4;  // k group of the 16x16x32 operands, also the transpose-read group
     const int l16 = lane & 15;
-    // transpose-read lane roles inside a 16-lane group (16x16x32 operands)
-    const int tr_row = (l16 >> 2) + 8 * g16;   // + 4r + k base
-    const int tr_col = 4 * (l16 & 3);           // + m/n base
     constexpr int DH = CF::DH, VT = CF::VT, NVG = CF::NVG;
     constexpr int NQ = DT / DH;                 // this wave's 16-row C tiles per d block
     const int vg = wave % NVG;                  // column group
@@ -619,8 +616,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         const int lane = tid & 63;
         const int g16 = lane >> 4;
         const int l16 = lane & 15;
-        const int tr_row = (l16 >> 2) + 8 * g16;
-        const int tr_col = 4 * (l16 & 3);
+        // transpose-read lane roles inside a 16-lane group (16x16x32 operands)
+        const int tr_row = (l16 >> 2) + 8 * g16;   // + 4r + k base
+        const int tr_col = 4 * (l16 & 3);           // + m/n base
         const int t0 = c * L;
         const int cur = (c - c_begin) & 1;
         const int par = c & 1;

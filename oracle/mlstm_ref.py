@@ -31,6 +31,10 @@ Forms, each written from the paper's statement of the cell (Sec. 2):
 * ``output_gate_norm``       the hidden-state output h = o * Norm(h~) with o = sigmoid(o~)
                              (Eq. 6 with Eq. 9), Norm the headwise LayerNorm or RMSNorm that
                              Sec. 2 allows; it takes [B, NH, T, DV] rows, not the S axis.
+* ``mlstm_layer``            the multi-head mLSTM layer (Eq. 11): dense projections of x to
+                             q, k, v, the gate pre-activations (soft-capped, Eq. 13) and o~,
+                             one cell per head, the output gate and norm, concatenation and
+                             the output projection; it takes x [B, T, d].
 """
 from __future__ import annotations
 
@@ -231,3 +235,46 @@ def output_gate_norm(h_tilde, o_pre, weight=None, bias=None, eps=1e-6, norm="lay
     if bias is not None:
         y = y + np.asarray(bias, dtype=np.float64)[None, :, None, :]
     return sigmoid(o) * y
+
+
+def soft_cap(x, cap):
+    """cap * tanh(x / cap) (Eq. 13); cap = None leaves x unchanged."""
+    x = np.asarray(x, dtype=np.float64)
+    return x if cap is None else cap * np.tanh(x / cap)
+
+
+def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, cap=15.0,
+                C0=None, n0=None, m0=None):
+    """Multi-head mLSTM layer (Eq. 11), x [B, T, d] -> y [B, T, d] and the final cell state.
+
+    W_in [d, NH * (2 DQK + 2 DV + 2)] holds, in column order, the q, k, v projections (head-major:
+    the DQK or DV columns of head 0, then head 1, ...), the input and forget gate projections
+    (one column per head) and the output gate projection (head-major); gate_bias [2, NH] is added
+    to the two gate pre-activations before the soft-cap.  Each head runs the cell of Sec. 2 from
+    (C0, n0, m0) ([B * NH, ...], None: zero state), its h~ goes through the output gate and the
+    headwise LayerNorm (weight norm_weight [NH, DV]), the heads are concatenated and projected by
+    W_proj [NH * DV, d].
+    """
+    x = np.asarray(x, dtype=np.float64)
+    B, T, d = x.shape
+    P = x @ np.asarray(W_in, dtype=np.float64)                      # [B, T, N_in]
+    o0 = 0
+    def take(width):
+        nonlocal o0
+        part = P[..., o0:o0 + width]
+        o0 += width
+        return part
+    q = take(NH * DQK).reshape(B, T, NH, DQK)
+    k = take(NH * DQK).reshape(B, T, NH, DQK)
+    v = take(NH * DV).reshape(B, T, NH, DV)
+    ig = soft_cap(take(NH) + np.asarray(gate_bias, dtype=np.float64)[0], cap)   # [B, T, NH]
+    fg = soft_cap(take(NH) + np.asarray(gate_bias, dtype=np.float64)[1], cap)
+    og = take(NH * DV).reshape(B, T, NH, DV)
+    assert o0 == P.shape[-1]
+    heads = lambda a: np.ascontiguousarray(np.moveaxis(a, 2, 1))    # [B, T, NH, D] -> [B, NH, T, D]
+    S = B * NH
+    h, C, n, m = recurrent(heads(q).reshape(S, T, DQK), heads(k).reshape(S, T, DQK), heads(v).reshape(S, T, DV),
+                           np.moveaxis(ig, 2, 1).reshape(S, T), np.moveaxis(fg, 2, 1).reshape(S, T), C0, n0, m0)
+    hy = output_gate_norm(h.reshape(B, NH, T, DV), heads(og), norm_weight, None, eps=eps, norm="layer")
+    y = np.moveaxis(hy, 1, 2).reshape(B, T, NH * DV) @ np.asarray(W_proj, dtype=np.float64)
+    return y, (C, n, m)

@@ -70,3 +70,45 @@ def test_sigmoid_is_stable_and_symmetric():
     assert np.isfinite(s).all() and s[0] == 0.0 and s[-1] == 1.0 and s[3] == 0.5
     np.testing.assert_allclose(s + R.sigmoid(-z), 1.0, rtol=0, atol=1e-15)
     np.testing.assert_allclose(s[1:-1], torch.sigmoid(torch.from_numpy(z[1:-1])).numpy(), rtol=1e-15)
+
+
+# ---- the layer (Eq. 11) --------------------------------------------------------------------------
+
+def _layer_weights(seed, d, NH, DQK, DV):
+    rng = np.random.default_rng(seed)
+    N = NH * (2 * DQK + 2 * DV + 2)
+    return (rng.normal(0, d ** -0.5, (d, N)), rng.normal(0, (NH * DV) ** -0.5, (NH * DV, d)),
+            np.stack([rng.normal(-2.0, 1.0, NH), rng.normal(3.0, 1.0, NH)]), rng.normal(1, 0.1, (NH, DV)))
+
+
+def test_layer_equals_a_loop_over_heads():
+    """Head h uses exactly its own columns of W_in (q, k, v, o head-major; gates one column
+    each) and its own rows of W_proj: the layer equals the sum over heads of separate cells."""
+    B, T, d, NH, DQK, DV = 2, 7, 12, 3, 4, 5
+    Win, Wp, gb, nw = _layer_weights(3, d, NH, DQK, DV)
+    x = np.random.default_rng(4).normal(0, 1, (B, T, d))
+    y, _ = R.mlstm_layer(x, Win, Wp, gb, nw, NH, DQK, DV, eps=1e-5, cap=15.0)
+    off = np.cumsum([0, NH * DQK, NH * DQK, NH * DV, NH, NH, NH * DV])
+    acc = np.zeros((B, T, d))
+    for hd in range(NH):
+        cols = lambda blk, w: Win[:, off[blk] + hd * w: off[blk] + (hd + 1) * w]
+        q, k, v, o = x @ cols(0, DQK), x @ cols(1, DQK), x @ cols(2, DV), x @ cols(5, DV)
+        ig = 15 * np.tanh((x @ cols(3, 1) + gb[0, hd]) / 15)[..., 0]
+        fg = 15 * np.tanh((x @ cols(4, 1) + gb[1, hd]) / 15)[..., 0]
+        h, *_ = R.recurrent(q, k, v, ig, fg)
+        hn = R.output_gate_norm(h[:, None], o[:, None], nw[hd:hd + 1], None, eps=1e-5)[:, 0]
+        acc += hn @ Wp[hd * DV:(hd + 1) * DV]
+    np.testing.assert_allclose(y, acc, rtol=1e-12, atol=1e-12)
+
+
+def test_layer_soft_cap_limits():
+    """cap -> infinity is no cap; the capped gates stay inside (-cap, cap)."""
+    B, T, d, NH, DQK, DV = 1, 6, 8, 2, 3, 4
+    Win, Wp, gb, nw = _layer_weights(5, d, NH, DQK, DV)
+    x = np.random.default_rng(6).normal(0, 1, (B, T, d))
+    a, _ = R.mlstm_layer(x, Win, Wp, gb, nw, NH, DQK, DV, cap=1e9)
+    b, _ = R.mlstm_layer(x, Win, Wp, gb, nw, NH, DQK, DV, cap=None)
+    np.testing.assert_allclose(a, b, rtol=1e-9, atol=1e-12)
+    z = np.linspace(-200, 200, 41)
+    assert (np.abs(R.soft_cap(z, 15.0)) < 15.0).all()
+    np.testing.assert_allclose(R.soft_cap(1e-3, 15.0), 1e-3, rtol=1e-8)

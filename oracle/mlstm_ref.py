@@ -34,7 +34,10 @@ Forms, each written from the paper's statement of the cell (Sec. 2):
 * ``mlstm_layer``            the multi-head mLSTM layer (Eq. 11): dense projections of x to
                              q, k, v, the gate pre-activations (soft-capped, Eq. 13) and o~,
                              one cell per head, the output gate and norm, concatenation and
-                             the output projection; it takes x [B, T, d].
+                             the output projection; it takes x [B, T, d].  With
+                             proj_dtype="bf16" the projections q, k, v and o~ are stored in
+                             bf16 (``round_bf16``) before the cell, as a bf16 model holds them.
+* ``round_bf16``             fp64 -> nearest bf16 value (ties to even), returned as fp64.
 """
 from __future__ import annotations
 
@@ -243,8 +246,20 @@ def soft_cap(x, cap):
     return x if cap is None else cap * np.tanh(x / cap)
 
 
+def round_bf16(x):
+    """Nearest bf16 value of each element (ties to even), as fp64.  bf16 keeps 8 significant bits
+    and fp32's exponent range: a normal |x| in [2^E, 2^(E+1)) has the quantum 2^(E-7), and below
+    the smallest normal 2^-126 the quantum stays 2^-133 (subnormals).  Dividing by a power of two
+    and multiplying back are exact in fp64, and np.round rounds halves to even.  Overflow past the
+    largest bf16 value is not handled (no caller comes near it)."""
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)                       # x = f 2^e, f in [0.5, 1): leading bit 2^(e-1)
+    quantum = np.ldexp(1.0, np.maximum(e - 1, -126) - 7)
+    return np.round(x / quantum) * quantum
+
+
 def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, cap=15.0,
-                C0=None, n0=None, m0=None):
+                C0=None, n0=None, m0=None, proj_dtype=None):
     """Multi-head mLSTM layer (Eq. 11), x [B, T, d] -> y [B, T, d] and the final cell state.
 
     W_in [d, NH * (2 DQK + 2 DV + 2)] holds, in column order, the q, k, v projections (head-major:
@@ -253,7 +268,8 @@ def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, 
     to the two gate pre-activations before the soft-cap.  Each head runs the cell of Sec. 2 from
     (C0, n0, m0) ([B * NH, ...], None: zero state), its h~ goes through the output gate and the
     headwise LayerNorm (weight norm_weight [NH, DV]), the heads are concatenated and projected by
-    W_proj [NH * DV, d].
+    W_proj [NH * DV, d].  proj_dtype="bf16" rounds q, k, v and o~ to bf16 after the projection
+    (the gates stay in full precision); None keeps every projection in fp64.
     """
     x = np.asarray(x, dtype=np.float64)
     B, T, d = x.shape
@@ -271,6 +287,10 @@ def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, 
     fg = soft_cap(take(NH) + np.asarray(gate_bias, dtype=np.float64)[1], cap)
     og = take(NH * DV).reshape(B, T, NH, DV)
     assert o0 == P.shape[-1]
+    if proj_dtype == "bf16":
+        q, k, v, og = round_bf16(q), round_bf16(k), round_bf16(v), round_bf16(og)
+    elif proj_dtype is not None:
+        raise ValueError(proj_dtype)
     heads = lambda a: np.ascontiguousarray(np.moveaxis(a, 2, 1))    # [B, T, NH, D] -> [B, NH, T, D]
     S = B * NH
     h, C, n, m = recurrent(heads(q).reshape(S, T, DQK), heads(k).reshape(S, T, DQK), heads(v).reshape(S, T, DV),

@@ -112,3 +112,41 @@ def test_layer_soft_cap_limits():
     z = np.linspace(-200, 200, 41)
     assert (np.abs(R.soft_cap(z, 15.0)) < 15.0).all()
     np.testing.assert_allclose(R.soft_cap(1e-3, 15.0), 1e-3, rtol=1e-8)
+
+
+def test_round_bf16_matches_torch_conversion():
+    """The oracle's bf16 rounding against torch's fp32 -> bf16 conversion (round to nearest even)
+    on fp32 values spread over the exponent range, exact ties, and subnormals."""
+    import torch
+    rng = np.random.default_rng(5)
+    one = np.float32(1.0)
+    ties = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -(1 + 2.0 ** -8), 3 * 2.0 ** -9 + 2.0 ** -1,
+                     2.0 ** -130 + 2.0 ** -134, 2.0 ** -130 + 3 * 2.0 ** -134], dtype=np.float32)
+    vals = np.concatenate([
+        (rng.standard_normal(20000) * np.exp2(rng.integers(-140, 120, 20000))).astype(np.float32),
+        ties, np.array([0.0, -0.0, one, 2.0 ** -126, 2.0 ** -133, 3.0e38], dtype=np.float32)])
+    want = torch.from_numpy(vals).bfloat16().double().numpy()
+    got = R.round_bf16(vals.astype(np.float64))
+    np.testing.assert_array_equal(got, want)
+    assert R.round_bf16(1 + 2.0 ** -8) == 1.0 and R.round_bf16(1 + 3 * 2.0 ** -8) == 1 + 2.0 ** -6
+
+
+def test_layer_bf16_projections_only_round_q_k_v_o():
+    """proj_dtype="bf16" moves a generic output by about bf16 rounding, and leaves it bit for
+    bit unchanged when every projection is already a bf16 value (x a one-hot row per step,
+    W_in on the bf16 grid): the rounding touches only the projections."""
+    rng = np.random.default_rng(6)
+    B, T, NH, DQK, DV, d = 1, 5, 2, 4, 4, 8
+    x = rng.standard_normal((B, T, d))
+    Win = rng.standard_normal((d, NH * (2 * DQK + 2 * DV + 2))) * 0.3
+    Wp = rng.standard_normal((NH * DV, d)) * 0.3
+    gb = np.array([[-1.0, 0.5], [2.0, 3.0]]); nw = 1 + 0.1 * rng.standard_normal((NH, DV))
+    a, _ = R.mlstm_layer(x, Win, Wp, gb, nw, NH, DQK, DV)
+    b, _ = R.mlstm_layer(x, Win, Wp, gb, nw, NH, DQK, DV, proj_dtype="bf16")
+    assert 0 < np.abs(a - b).max() < 0.05 * np.abs(a).max()
+    # a projection already on the bf16 grid is left alone: x = e_j, W_in columns on the grid
+    Wg = R.round_bf16(Win)
+    xe = np.zeros((B, T, d)); xe[0, np.arange(T), np.arange(T)] = 1.0
+    c, _ = R.mlstm_layer(xe, Wg, Wp, gb, nw, NH, DQK, DV)
+    e, _ = R.mlstm_layer(xe, Wg, Wp, gb, nw, NH, DQK, DV, proj_dtype="bf16")
+    np.testing.assert_array_equal(c, e)

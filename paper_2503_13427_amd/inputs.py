@@ -211,3 +211,36 @@ def make_decode_steps(*, workload: int, B: int, NH: int, steps: int, DQK: int, D
     ids, so the first s steps of a longer run are identical."""
     return make_prefill(workload=workload, B=B, NH=NH, T=steps, DQK=DQK, DV=DV, dtype=dtype,
                         gates=gates, state=None, seed=seed, heads=heads, tensor_base=_DEC_OFFSET)
+
+
+@dataclass
+class LayerInputs:
+    """Synthetic weights and input of one mLSTM layer (bf16 arrays as uint16 bit patterns).
+
+    W_in [d, NH (2 DQK + 2 DV + 2)]: q, k, v projections (head-major), the input and forget
+    gate projections (one column per head), the output gate projection (head-major);
+    W_proj [NH DV, d]; gate_bias [2, NH] fp32 (input gate around -2, forget gate around +3);
+    norm_weight [NH, DV] fp32; x [B, T, d] bf16.
+    """
+    d: int
+    NH: int
+    DQK: int
+    DV: int
+    W_in: np.ndarray
+    W_proj: np.ndarray
+    gate_bias: np.ndarray
+    norm_weight: np.ndarray
+    x: np.ndarray
+
+
+def make_layer(*, workload: int, B: int, T: int, NH: int, DQK: int, DV: int, seed: int = 0) -> LayerInputs:
+    """Weights drawn N(0, 1/sqrt(fan_in)), norm weights N(1, 0.1), x N(0, 1)."""
+    d = NH * DV
+    n_in = NH * (2 * DQK + 2 * DV + 2)
+    r = lambda t: _rng(seed, workload, 1 << 20, t)
+    W_in = r(0).standard_normal((d, n_in), dtype=np.float32) * np.float32(d ** -0.5)
+    W_proj = r(1).standard_normal((NH * DV, d), dtype=np.float32) * np.float32((NH * DV) ** -0.5)
+    gb = np.stack([r(2).normal(-2.0, 1.0, NH), r(3).normal(3.0, 1.0, NH)]).astype(np.float32)
+    nw = r(4).normal(1.0, 0.1, (NH, DV)).astype(np.float32)
+    x = r(5).standard_normal((B, T, d), dtype=np.float32)
+    return LayerInputs(d, NH, DQK, DV, f32_to_bf16_bits(W_in), f32_to_bf16_bits(W_proj), gb, nw, f32_to_bf16_bits(x))

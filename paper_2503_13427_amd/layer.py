@@ -1,0 +1,115 @@
+"""Multi-head mLSTM layer of xLSTM 7B (Eq. 11) around libmlstm, with synthetic weights.
+
+x [B, T, d] -> y [B, T, d], d = NH * DV:
+
+1. input projection: one bf16 GEMM for q, k, v and o~ (head-major columns) and one fp32 GEMM
+   for the two gate pre-activations (one column per head each), both through torch.matmul,
+   which is hipBLASLt on ROCm;
+2. gate biases and the soft-cap a * tanh(x / a) of Eq. 13 (a = 15) on the fp32 gates;
+3. head-major copies, since the C ABI takes [B, NH, T, D] rows;
+4. the cell: ``mlstm_chunkwise_fwd`` for a prefill, ``mlstm_step`` for one decode step;
+5. ``mlstm_output_norm``: h = sigmoid(o~) * LayerNorm(h~) * weight, per head;
+6. concatenation of the heads and the output projection (bf16 GEMM).
+
+The projections are plain library GEMMs around the cell; every step of the cell and of the
+output norm runs in libmlstm.  The layer's pre-norm (Norm(x) in the block, Eq. 12) belongs to
+the block, not to the layer, and is not applied.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import torch
+
+from . import binding as mb
+
+State = Tuple[torch.Tensor, torch.Tensor, torch.Tensor]   # C [B, NH, DQK, DV], n [B, NH, DQK], m [B, NH]
+
+
+@dataclass
+class LayerWeights:
+    W_qkvo: torch.Tensor      # [d, NH (2 DQK + 2 DV)] bf16: q, k, v, o~ columns, head-major
+    W_gates: torch.Tensor     # [d, 2 NH] fp32: input gate columns, then forget gate columns
+    W_proj: torch.Tensor      # [NH DV, d] bf16
+    gate_bias: torch.Tensor   # [2, NH] fp32
+    norm_weight: torch.Tensor # [NH, DV] fp32
+    NH: int
+    DQK: int
+    DV: int
+
+    @staticmethod
+    def from_inputs(li, device="cuda") -> "LayerWeights":
+        """From ``inputs.LayerInputs`` (bf16 bit patterns): the gate columns of W_in are taken
+        out (upcast exactly to fp32), the rest kept in bf16."""
+        import numpy as np
+        NH, DQK, DV = li.NH, li.DQK, li.DV
+        W = torch.from_numpy(np.ascontiguousarray(li.W_in)).view(torch.bfloat16)
+        a = NH * (2 * DQK + DV)
+        W_qkvo = torch.cat([W[:, :a], W[:, a + 2 * NH:]], dim=1).contiguous()
+        W_gates = W[:, a:a + 2 * NH].float().contiguous()
+        Wp = torch.from_numpy(np.ascontiguousarray(li.W_proj)).view(torch.bfloat16)
+        return LayerWeights(W_qkvo.to(device), W_gates.to(device), Wp.to(device),
+                            torch.from_numpy(li.gate_bias).to(device), torch.from_numpy(li.norm_weight).to(device),
+                            NH, DQK, DV)
+
+
+class MLSTMLayer:
+    def __init__(self, w: LayerWeights, L: int = 64, eps: float = 1e-6, cap: Optional[float] = 15.0):
+        self.w, self.L, self.eps, self.cap = w, L, eps, cap
+
+    def _project(self, x2: torch.Tensor):
+        """x2 [R, d] bf16 -> q, k [R, NH, DQK], v, o [R, NH, DV] bf16, i, f [R, NH] fp32."""
+        w = self.w
+        NH, DQK, DV = w.NH, w.DQK, w.DV
+        P = torch.matmul(x2, w.W_qkvo)
+        G = torch.matmul(x2.float(), w.W_gates) + w.gate_bias.reshape(1, 2 * NH)
+        if self.cap is not None:
+            G = self.cap * torch.tanh(G / self.cap)
+        R = x2.shape[0]
+        c = [0, NH * DQK, 2 * NH * DQK, NH * (2 * DQK + DV), NH * (2 * DQK + 2 * DV)]
+        q = P[:, c[0]:c[1]].view(R, NH, DQK)
+        k = P[:, c[1]:c[2]].view(R, NH, DQK)
+        v = P[:, c[2]:c[3]].view(R, NH, DV)
+        o = P[:, c[3]:c[4]].view(R, NH, DV)
+        return q, k, v, o, G[:, :NH], G[:, NH:]
+
+    def project_heads(self, x: torch.Tensor):
+        """Steps 1-3 for a prefill: x [B, T, d] -> head-major q, k [B, NH, T, DQK], v, o~
+        [B, NH, T, DV] (bf16) and the capped gate pre-activations i~, f~ [B, NH, T] (fp32)."""
+        w = self.w
+        B, T, d = x.shape
+        NH, DQK, DV = w.NH, w.DQK, w.DV
+        q, k, v, o, ig, fg = self._project(x.reshape(B * T, d))
+        hm = lambda a, D: a.view(B, T, NH, D).transpose(1, 2).contiguous()   # head-major [B, NH, T, D]
+        gm = lambda a: a.reshape(B, T, NH).transpose(1, 2).contiguous()
+        return hm(q, DQK), hm(k, DQK), hm(v, DV), hm(o, DV), gm(ig), gm(fg)
+
+    def prefill(self, x: torch.Tensor, state: Optional[State] = None,
+                workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, State]:
+        """x [B, T, d] bf16 -> (y [B, T, d] bf16, the cell state after the T tokens)."""
+        w = self.w
+        B, T, d = x.shape
+        NH, DQK, DV = w.NH, w.DQK, w.DV
+        q, k, v, o, ig, fg = self.project_heads(x)
+        h = torch.empty(B, NH, T, DV, dtype=torch.bfloat16, device=x.device)
+        C = torch.empty(B, NH, DQK, DV, device=x.device)
+        n = torch.empty(B, NH, DQK, device=x.device)
+        m = torch.empty(B, NH, device=x.device)
+        C0, n0, m0 = state if state is not None else (None, None, None)
+        mb.mlstm_chunkwise_fwd(q, k, v, ig, fg, C0, n0, m0, self.L, h, C, n, m, workspace=workspace)
+        mb.mlstm_output_norm(h, o, w.norm_weight, None, self.eps, "layer", h)   # in place
+        y = torch.matmul(h.transpose(1, 2).reshape(B * T, NH * DV), w.W_proj)
+        return y.view(B, T, d), (C, n, m)
+
+    def step(self, x: torch.Tensor, state: State) -> torch.Tensor:
+        """One decode step: x [B, d] bf16 -> y [B, d]; the state is updated in place."""
+        w = self.w
+        B, d = x.shape
+        q, k, v, o, ig, fg = self._project(x)
+        q, k, v, o = q.contiguous(), k.contiguous(), v.contiguous(), o.contiguous()
+        C, n, m = state
+        h = torch.empty(B, w.NH, w.DV, dtype=torch.bfloat16, device=x.device)
+        mb.mlstm_step(q, k, v, ig.contiguous(), fg.contiguous(), C, n, m, h, C, n, m)
+        mb.mlstm_output_norm(h, o, w.norm_weight, None, self.eps, "layer", h)
+        return torch.matmul(h.reshape(B, w.NH * w.DV), w.W_proj)

@@ -1,0 +1,63 @@
+"""The mLSTM layer (Eq. 11) around libmlstm against the fp64 oracle.
+
+bf16 weights and input.  The layer stores q, k, v and o~ in bf16 after its projections, as a bf16
+model does, and keeps the gates in fp32; the oracle takes the same storage step
+(``proj_dtype="bf16"``: its own fp64 projections rounded to bf16), so the comparison holds y to
+the cell's bar, max relative error <= 2e-2 per batch slice.  The projections are checked
+against the oracle's rounded ones to one bf16 rounding step.  Decode steps after a prefill are
+checked against the whole sequence."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import mlstm_ref as R
+from paper_2503_13427_amd.inputs import bf16_bits_to_f32, make_layer
+from tests.helpers import TOL_BF16, host_f64, rel_err, state_errs
+
+pytestmark = pytest.mark.gpu
+
+
+def _layer(li, L=64):
+    from paper_2503_13427_amd.layer import LayerWeights, MLSTMLayer
+    return MLSTMLayer(LayerWeights.from_inputs(li), L=L, eps=1e-6, cap=15.0)
+
+
+def _oracle(li, proj_dtype="bf16"):
+    return R.mlstm_layer(bf16_bits_to_f32(li.x), bf16_bits_to_f32(li.W_in), bf16_bits_to_f32(li.W_proj),
+                         li.gate_bias, li.norm_weight, li.NH, li.DQK, li.DV, eps=1e-6, cap=15.0,
+                         proj_dtype=proj_dtype)
+
+
+@pytest.mark.parametrize("B,T,NH,L", [(1, 192, 2, 64), (2, 160, 1, 128)])
+def test_layer_prefill_matches_oracle(B, T, NH, L):
+    li = make_layer(workload=70, B=B, T=T, NH=NH, DQK=256, DV=512)
+    layer = _layer(li, L)
+    x = torch.from_numpy(li.x).view(torch.bfloat16).cuda()
+    q = host_f64(layer.project_heads(x)[0])
+    y, (C, n, m) = layer.prefill(x)
+    torch.cuda.synchronize()
+    yr, (Cr, nr, mr) = _oracle(li)
+    err = rel_err(host_f64(y), yr, 1)
+    xw = bf16_bits_to_f32(li.x).astype(np.float64) @ bf16_bits_to_f32(li.W_in).astype(np.float64)
+    q_ref = R.round_bf16(np.moveaxis(xw[..., :NH * 256].reshape(B, T, NH, 256), 2, 1))
+    e_q = rel_err(q, q_ref, 2)
+    e_C, e_n, e_m = state_errs(host_f64(C).reshape(B * NH, 256, 512), host_f64(n).reshape(B * NH, 256),
+                               host_f64(m).reshape(B * NH), Cr, nr, mr)
+    print(f"layer B{B} T{T} NH{NH} L{L}: y {err:.3e}, state C {e_C:.3e} n {e_n:.3e} m {e_m:.3e}, q {e_q:.3e}")
+    assert np.isfinite(host_f64(y)).all() and err <= TOL_BF16
+    assert max(e_C, e_n) <= TOL_BF16 and e_m <= TOL_BF16
+    assert e_q <= 2 ** -8
+
+
+def test_layer_decode_continues_the_prefill():
+    li = make_layer(workload=71, B=2, T=132, NH=2, DQK=256, DV=512)
+    layer = _layer(li)
+    x = torch.from_numpy(li.x).view(torch.bfloat16).cuda()
+    _, state = layer.prefill(x[:, :128].contiguous())
+    ys = [layer.step(x[:, t].contiguous(), state) for t in range(128, 132)]
+    torch.cuda.synchronize()
+    yr, _ = _oracle(li)
+    got = np.stack([host_f64(y) for y in ys], axis=1)      # [B, 4, d]
+    err = rel_err(got, yr[:, 128:], 1)
+    print(f"layer decode: y {err:.3e}")
+    assert err <= TOL_BF16

@@ -18,7 +18,11 @@ Extra objects on the same line:
                 and B=4 x T=32768 from a nonzero state, L=128);
   output_norm   the hidden-state output h = sigmoid(o~) * LayerNorm(h~) w + b
                 (mlstm_output_norm) on the headline prefill's h shape and the
-                decode step's h shape: us per call and achieved GB/s vs 8 TB/s.
+                decode step's h shape: us per call and achieved GB/s vs 8 TB/s;
+  layer         one xLSTM-7B-shaped mLSTM layer (d = 4096, random weights): prefill
+                of 65536 tokens as batch x context (1 x 65536, 8 x 8192, 64 x 1024)
+                with the time of each stage, and decode steps at B = 1 and 256,
+                eager and as a captured HIP graph.
 Every timed section is preceded by 0.25 s of untimed calls (clock settle).
 """
 from __future__ import annotations
@@ -228,6 +232,95 @@ def bench_output_norm(B, NH, T, DV, steps, stream, label):
                 gbs=by / t / 1e9, hbm_frac=by / t / 1e9 / acc.PEAK_HBM_GBS)
 
 
+LAYER_D, LAYER_NH, LAYER_DQK, LAYER_DV = 4096, 8, 256, 512
+LAYER_PREFILL_SPLITS = ((1, 65536), (8, 8192), (64, 1024))   # 65536 tokens as batch x context
+
+
+def synthetic_layer(seed=11, L=64):
+    """An xLSTM-7B-shaped mLSTM layer (d = 4096, 8 heads, dqk = 256, dv = 512) with random weights:
+    projections N(0, 1/fan_in) in bf16, input/forget gate biases around
+    -2 and +3, norm weight around 1."""
+    from paper_2503_13427_amd.layer import LayerWeights, MLSTMLayer
+    d, NH, DQK, DV = LAYER_D, LAYER_NH, LAYER_DQK, LAYER_DV
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    rn = lambda *shape: torch.randn(*shape, generator=g, device="cuda")
+    w = LayerWeights(W_qkvo=(rn(d, NH * (2 * DQK + 2 * DV)) * d ** -0.5).bfloat16(),
+                     W_gates=(rn(d, 2 * NH) * d ** -0.5).bfloat16(),
+                     W_proj=(rn(NH * DV, d) * (NH * DV) ** -0.5).bfloat16(),
+                     gate_bias=rn(2, NH) + torch.tensor([[-2.0], [3.0]], device="cuda"),
+                     norm_weight=1 + 0.1 * rn(NH, DV), NH=NH, DQK=DQK, DV=DV)
+    return MLSTMLayer(w, L=L, eps=1e-6, cap=15.0)
+
+
+def bench_layer_prefill(layer, B, T, steps, stream):
+    """One layer forward over B x T tokens (x resident in HBM), and the same work stage by stage."""
+    from paper_2503_13427_amd import binding as mb
+    w = layer.w
+    NH, DQK, DV, d = w.NH, w.DQK, w.DV, LAYER_D
+    g = torch.Generator(device="cuda").manual_seed(12)
+    x = torch.randn(B, T, d, generator=g, device="cuda").bfloat16()
+    nb = mb.mlstm_chunkwise_workspace_bytes(B, NH, T, DQK, DV, layer.L)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda") if nb else None
+    run = lambda fn: time_steps(fn, steps, 1, stream)[1] / steps
+    t_total = run(lambda: layer.prefill(x, workspace=ws))
+    x2 = x.reshape(B * T, d)
+    t_proj = run(lambda: layer._project(x2))
+    t_heads = run(lambda: layer.project_heads(x)) - t_proj
+    q, k, v, o, ig, fg = layer.project_heads(x)
+    h = torch.empty(B, NH, T, DV, dtype=torch.bfloat16, device="cuda")
+    C = torch.empty(B, NH, DQK, DV, device="cuda")
+    n = torch.empty(B, NH, DQK, device="cuda")
+    m = torch.empty(B, NH, device="cuda")
+    t_cell = run(lambda: mb.mlstm_chunkwise_fwd(q, k, v, ig, fg, None, None, None, layer.L, h, C, n, m,
+                                                 workspace=ws, stream=stream))
+    hn = torch.empty_like(h)
+    t_norm = run(lambda: mb.mlstm_output_norm(h, o, w.norm_weight, None, layer.eps, "layer", hn, stream=stream))
+    t_out = run(lambda: torch.matmul(hn.transpose(1, 2).reshape(B * T, NH * DV), w.W_proj))
+    tok = B * T
+    fl_proj = acc.flops_layer_projections(tok, d, NH, DQK, DV)
+    fl_cell = acc.flops_chunkwise(B * NH, T, layer.L, DQK, DV).total
+    stages = dict(projections=t_proj, head_major_copies=t_heads, cell=t_cell, output_norm=t_norm,
+                  output_projection=t_out)
+    return dict(workload=f"layer_prefill_B{B}_T{T}_d{d}_NH{NH}", B=B, T=T, tokens_per_s=tok / t_total,
+                ms_per_call=t_total * 1e3, tflops=(fl_proj + fl_cell) / t_total / 1e12,
+                flops_projections=fl_proj, flops_cell=fl_cell,
+                stages_ms={k: v * 1e3 for k, v in stages.items()},
+                stages_share={k: v / t_total for k, v in stages.items()})
+
+
+def bench_layer_decode(layer, B, steps, stream):
+    """Consecutive decode steps of B tokens through one layer: eager launches, then the same step
+    replayed as a captured HIP graph; algorithmic bytes per step against HBM bandwidth."""
+    from paper_2503_13427_amd.layer import GraphedDecode
+    w = layer.w
+    NH, DQK, DV, d = w.NH, w.DQK, w.DV, LAYER_D
+    g = torch.Generator(device="cuda").manual_seed(13)
+    x = torch.randn(B, d, generator=g, device="cuda").bfloat16()
+    state = (torch.zeros(B, NH, DQK, DV, device="cuda"), torch.zeros(B, NH, DQK, device="cuda"),
+             torch.zeros(B, NH, device="cuda"))
+    t_eager = time_steps(lambda: layer.step(x, state), steps, 10, stream)[1] / steps
+    gd = GraphedDecode(layer, tuple(t.clone() for t in state), B)
+    gd.x.copy_(x)
+    t_graph = time_steps(gd.graph.replay, steps, 10, stream)[1] / steps
+    by = acc.layer_step_bytes(B, d, NH, DQK, DV)
+    return dict(workload=f"layer_decode_B{B}_d{d}_NH{NH}", B=B, us_per_step_eager=t_eager * 1e6,
+                us_per_step_graph=t_graph * 1e6, tokens_per_s_graph=B / t_graph, bytes_per_step=by,
+                gbs_graph=by / t_graph / 1e9, hbm_frac_graph=by / t_graph / 1e9 / acc.PEAK_HBM_GBS)
+
+
+def bench_layer(steps, decode_steps, stream):
+    layer = synthetic_layer()
+    out = {"prefill": [], "decode": []}
+    for B, T in LAYER_PREFILL_SPLITS:
+        log(f"layer prefill B={B} T={T}")
+        out["prefill"].append(bench_layer_prefill(layer, B, T, steps, stream))
+        torch.cuda.empty_cache()
+    for B in (1, 256):
+        log(f"layer decode B={B}")
+        out["decode"].append(bench_layer_decode(layer, B, decode_steps, stream))
+    return out
+
+
 def cpu_baseline(w, max_seconds=30.0):
     """The fp64 oracle on the headline workload, timed on the host.  Heads are independent, so
     the sample is a subset of heads over the full sequence (all heads if they fit the budget)."""
@@ -255,7 +348,8 @@ def main():
     ap.add_argument("--skip-large", action="store_true")
     ap.add_argument("--skip-output-norm", action="store_true")
     ap.add_argument("--skip-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=["prefill", "decode", "large", "output_norm", "calls"], default=None,
+    ap.add_argument("--skip-layer", action="store_true")
+    ap.add_argument("--only", choices=["prefill", "decode", "large", "output_norm", "layer", "calls"], default=None,
                     help="run one part only (profiling runs); 'calls' makes --calls untimed prefill calls of "
                          "--workload and then one --copy-mib MiB device copy, for counter runs")
     ap.add_argument("--workload", default=configs.PREFILL_T2048.name,
@@ -312,6 +406,10 @@ def main():
         res["output_norm"] = [bench_output_norm(w.B, w.NH, w.T, w.DV, args.steps, stream, "prefill_B1_NH8_T2048_DV512"),
                               bench_output_norm(256, 8, 1, 512, args.steps, stream, "decode_B256_NH8_DV512")]
         torch.cuda.empty_cache()
+    if args.only in (None, "layer") and not args.skip_layer:
+        log("mLSTM layer (projections + cell + output norm + output projection)")
+        res["layer"] = bench_layer(max(3, args.steps // 20), max(50, args.decode_steps // 4), stream)
+        torch.cuda.empty_cache()
     if args.only in (None, "decode") and not args.skip_decode:
         log(f"decode {configs.DECODE_B256.name}: {args.decode_steps} steps")
         res["decode"] = bench_decode(configs.DECODE_B256, args.decode_steps, stream)
@@ -339,6 +437,8 @@ def main():
         line["decode"] = res["decode"]
     if "output_norm" in res:
         line["output_norm"] = res["output_norm"]
+    if "layer" in res:
+        line["layer"] = res["layer"]
     if not args.skip_cpu_baseline and args.only in (None, "prefill"):
         log("cpu baseline: fp64 oracle")
         line["cpu_baseline"] = cpu_baseline(w)

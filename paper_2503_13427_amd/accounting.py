@@ -7,6 +7,10 @@
   (#blocks x #heads x d_qk x d_hv x 4 bytes).
 * ``prefill_bytes`` / ``step_bytes``: algorithmic HBM bytes of one call, i.e.
   every input read once and every output written once, at the call's dtypes.
+* ``flops_layer_projections``: the dense projections of one mLSTM layer, App. D.2
+  ("FLOPs for the mLSTM in a Transformer Backbone"), per token count.
+* ``layer_step_bytes``: algorithmic HBM bytes of one layer decode step (weights,
+  state, token in and out).
 """
 from __future__ import annotations
 
@@ -96,3 +100,23 @@ def output_norm_bytes(B: int, NH: int, T: int, dv: int, elem_bytes: int = 2, aff
     """Algorithmic HBM bytes of the hidden-state output h = sigmoid(o~) * (Norm(h~) w + b): every
     row of h~ and o~ read once and of h written once, plus the per-head weight and bias once."""
     return 3 * B * NH * T * dv * elem_bytes + (2 * NH * dv * 4 if affine else 0)
+
+
+def flops_layer_projections(tokens: int, d: int, NH: int, dqk: int, dv: int, F_sig: int = 1) -> int:
+    """App. D.2, one mLSTM layer without the cell: the q, k, v, input and forget gate projections,
+    2 tokens d NH (2 dqk + dv + 2), and the output gate with the output projection,
+    4 tokens d NH dv + tokens NH dv F_sig."""
+    return 2 * tokens * d * NH * (2 * dqk + dv + 2) + 4 * tokens * d * NH * dv + tokens * NH * dv * F_sig
+
+
+def layer_weight_bytes(d: int, NH: int, dqk: int, dv: int) -> int:
+    """The layer's weights as stored: q, k, v, o~ projection and output projection in bf16, the gate
+    projection (2 NH columns), the gate biases and the norm weight in fp32."""
+    return 2 * d * NH * (2 * dqk + 2 * dv) + 2 * NH * dv * d + 4 * (2 * d * NH + 2 * NH + NH * dv)
+
+
+def layer_step_bytes(B: int, d: int, NH: int, dqk: int, dv: int) -> int:
+    """Algorithmic HBM bytes of one layer decode step of B tokens: every weight read once, the fp32
+    state (C, n, m) read and written once, x read and y written once (bf16)."""
+    state = 4 * B * NH * (dqk * dv + dqk + 1)
+    return layer_weight_bytes(d, NH, dqk, dv) + 2 * state + 2 * 2 * B * d

@@ -2,9 +2,9 @@
 
 x [B, T, d] -> y [B, T, d], d = NH * DV:
 
-1. input projection: one bf16 GEMM for q, k, v and o~ (head-major columns) and one fp32 GEMM
-   for the two gate pre-activations (one column per head each), both through torch.matmul,
-   which is hipBLASLt on ROCm;
+1. input projection: one bf16 GEMM for q, k, v and o~ (head-major columns, bf16 output) and one
+   bf16 GEMM with fp32 output for the two gate pre-activations (one column per head each), both
+   hipBLASLt on ROCm;
 2. gate biases and the soft-cap a * tanh(x / a) of Eq. 13 (a = 15) on the fp32 gates;
 3. head-major copies, since the C ABI takes [B, NH, T, D] rows;
 4. the cell: ``mlstm_chunkwise_fwd`` for a prefill, ``mlstm_step`` for one decode step;
@@ -30,7 +30,7 @@ State = Tuple[torch.Tensor, torch.Tensor, torch.Tensor]   # C [B, NH, DQK, DV], 
 @dataclass
 class LayerWeights:
     W_qkvo: torch.Tensor      # [d, NH (2 DQK + 2 DV)] bf16: q, k, v, o~ columns, head-major
-    W_gates: torch.Tensor     # [d, 2 NH] fp32: input gate columns, then forget gate columns
+    W_gates: torch.Tensor     # [d, 2 NH] bf16: input gate columns, then forget gate columns
     W_proj: torch.Tensor      # [NH DV, d] bf16
     gate_bias: torch.Tensor   # [2, NH] fp32
     norm_weight: torch.Tensor # [NH, DV] fp32
@@ -40,14 +40,14 @@ class LayerWeights:
 
     @staticmethod
     def from_inputs(li, device="cuda") -> "LayerWeights":
-        """From ``inputs.LayerInputs`` (bf16 bit patterns): the gate columns of W_in are taken
-        out (upcast exactly to fp32), the rest kept in bf16."""
+        """From ``inputs.LayerInputs`` (bf16 bit patterns): W_in split into the q, k, v, o~ columns
+        and the gate columns."""
         import numpy as np
         NH, DQK, DV = li.NH, li.DQK, li.DV
         W = torch.from_numpy(np.ascontiguousarray(li.W_in)).view(torch.bfloat16)
         a = NH * (2 * DQK + DV)
         W_qkvo = torch.cat([W[:, :a], W[:, a + 2 * NH:]], dim=1).contiguous()
-        W_gates = W[:, a:a + 2 * NH].float().contiguous()
+        W_gates = W[:, a:a + 2 * NH].contiguous()
         Wp = torch.from_numpy(np.ascontiguousarray(li.W_proj)).view(torch.bfloat16)
         return LayerWeights(W_qkvo.to(device), W_gates.to(device), Wp.to(device),
                             torch.from_numpy(li.gate_bias).to(device), torch.from_numpy(li.norm_weight).to(device),
@@ -63,7 +63,8 @@ class MLSTMLayer:
         w = self.w
         NH, DQK, DV = w.NH, w.DQK, w.DV
         P = torch.matmul(x2, w.W_qkvo)
-        G = torch.matmul(x2.float(), w.W_gates) + w.gate_bias.reshape(1, 2 * NH)
+        # bf16 products accumulated and returned in fp32: the gates never pass through bf16
+        G = torch.mm(x2, w.W_gates, out_dtype=torch.float32) + w.gate_bias.reshape(1, 2 * NH)
         if self.cap is not None:
             G = self.cap * torch.tanh(G / self.cap)
         R = x2.shape[0]
@@ -87,7 +88,8 @@ class MLSTMLayer:
 
     def prefill(self, x: torch.Tensor, state: Optional[State] = None,
                 workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, State]:
-        """x [B, T, d] bf16 -> (y [B, T, d] bf16, the cell state after the T tokens)."""
+        """x [B, T, d] bf16 -> (y [B, T, d] bf16, the cell state after the T tokens).  ``workspace``
+        (uint8, ``mlstm_chunkwise_workspace_bytes``) is allocated per call when not given."""
         w = self.w
         B, T, d = x.shape
         NH, DQK, DV = w.NH, w.DQK, w.DV
@@ -97,6 +99,9 @@ class MLSTMLayer:
         n = torch.empty(B, NH, DQK, device=x.device)
         m = torch.empty(B, NH, device=x.device)
         C0, n0, m0 = state if state is not None else (None, None, None)
+        if workspace is None:   # the segment schedule needs one; without it the call runs one block per sequence
+            nb = mb.mlstm_chunkwise_workspace_bytes(B, NH, T, DQK, DV, self.L)
+            workspace = torch.empty(nb, dtype=torch.uint8, device=x.device) if nb else None
         mb.mlstm_chunkwise_fwd(q, k, v, ig, fg, C0, n0, m0, self.L, h, C, n, m, workspace=workspace)
         mb.mlstm_output_norm(h, o, w.norm_weight, None, self.eps, "layer", h)   # in place
         y = torch.matmul(h.transpose(1, 2).reshape(B * T, NH * DV), w.W_proj)
@@ -113,3 +118,39 @@ class MLSTMLayer:
         mb.mlstm_step(q, k, v, ig.contiguous(), fg.contiguous(), C, n, m, h, C, n, m)
         mb.mlstm_output_norm(h, o, w.norm_weight, None, self.eps, "layer", h)
         return torch.matmul(h.reshape(B, w.NH * w.DV), w.W_proj)
+
+
+class GraphedDecode:
+    """One decode step of ``layer`` captured as a HIP graph, for batch B and the given state.
+
+    A single-token step is a dozen small launches (projections, gate cap, the cell, the norm, the
+    output projection); replaying them as one graph removes the per-launch host cost.  The graph
+    reads ``self.x`` and the state tensors it was captured with, updates that state in place and
+    writes ``self.y``: call it with the next token's x [B, d]; the returned y is overwritten by the
+    next call.  Nothing in the captured work clears memory with a memset node."""
+
+    def __init__(self, layer: MLSTMLayer, state: State, B: int):
+        w = layer.w
+        d = w.W_proj.shape[1]
+        dev = w.W_proj.device
+        self.x = torch.zeros(B, d, dtype=torch.bfloat16, device=dev)
+        self.state = state
+        # library set-up (GEMM handles, workspaces) happens on warm-up calls before capture; they run
+        # on a copy of the state so the caller's state is untouched
+        scratch = tuple(t.clone() for t in state)
+        side = torch.cuda.Stream(device=dev)
+        side.wait_stream(torch.cuda.current_stream(dev))
+        with torch.cuda.stream(side):
+            for _ in range(2):
+                layer.step(self.x, scratch)
+        torch.cuda.current_stream(dev).wait_stream(side)
+        torch.cuda.synchronize(dev)
+        del scratch
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self.y = layer.step(self.x, state)
+
+    def __call__(self, x: torch.Tensor) -> torch.Tensor:
+        self.x.copy_(x)
+        self.graph.replay()
+        return self.y

@@ -4,7 +4,8 @@ bf16 weights and input.  The layer stores q, k, v and o~ in bf16 after its proje
 model does, and keeps the gates in fp32; the oracle takes the same storage step
 (``proj_dtype="bf16"``: its own fp64 projections rounded to bf16), so the comparison holds y to
 the cell's bar, max relative error <= 2e-2 per batch slice.  The projections are checked
-against the oracle's rounded ones to one bf16 rounding step.  Decode steps after a prefill are
+against the oracle's rounded ones to one bf16 rounding step, and the capped gate pre-activations
+(fp32 throughout) against the oracle's to fp32 accumulation error.  Decode steps after a prefill are
 checked against the whole sequence."""
 import numpy as np
 import pytest
@@ -33,7 +34,8 @@ def test_layer_prefill_matches_oracle(B, T, NH, L):
     li = make_layer(workload=70, B=B, T=T, NH=NH, DQK=256, DV=512)
     layer = _layer(li, L)
     x = torch.from_numpy(li.x).view(torch.bfloat16).cuda()
-    q = host_f64(layer.project_heads(x)[0])
+    heads = layer.project_heads(x)
+    q, ig, fg = host_f64(heads[0]), host_f64(heads[4]), host_f64(heads[5])
     y, (C, n, m) = layer.prefill(x)
     torch.cuda.synchronize()
     yr, (Cr, nr, mr) = _oracle(li)
@@ -41,12 +43,17 @@ def test_layer_prefill_matches_oracle(B, T, NH, L):
     xw = bf16_bits_to_f32(li.x).astype(np.float64) @ bf16_bits_to_f32(li.W_in).astype(np.float64)
     q_ref = R.round_bf16(np.moveaxis(xw[..., :NH * 256].reshape(B, T, NH, 256), 2, 1))
     e_q = rel_err(q, q_ref, 2)
+    a = NH * (2 * 256 + 512)
+    gates = [np.moveaxis(R.soft_cap(xw[..., a + j * NH:a + (j + 1) * NH] + li.gate_bias[j], 15.0), 2, 1) for j in (0, 1)]
+    e_g = max(float(np.abs(got - ref).max()) for got, ref in zip((ig, fg), gates))
     e_C, e_n, e_m = state_errs(host_f64(C).reshape(B * NH, 256, 512), host_f64(n).reshape(B * NH, 256),
                                host_f64(m).reshape(B * NH), Cr, nr, mr)
-    print(f"layer B{B} T{T} NH{NH} L{L}: y {err:.3e}, state C {e_C:.3e} n {e_n:.3e} m {e_m:.3e}, q {e_q:.3e}")
+    print(f"layer B{B} T{T} NH{NH} L{L}: y {err:.3e}, state C {e_C:.3e} n {e_n:.3e} m {e_m:.3e}, q {e_q:.3e}, "
+          f"gates {e_g:.3e}")
     assert np.isfinite(host_f64(y)).all() and err <= TOL_BF16
     assert max(e_C, e_n) <= TOL_BF16 and e_m <= TOL_BF16
     assert e_q <= 2 ** -8
+    assert e_g <= 1e-4     # fp32 accumulation of bf16 products; a bf16 round trip would show ~1e-2
 
 
 def test_layer_decode_continues_the_prefill():
@@ -61,3 +68,25 @@ def test_layer_decode_continues_the_prefill():
     err = rel_err(got, yr[:, 128:], 1)
     print(f"layer decode: y {err:.3e}")
     assert err <= TOL_BF16
+
+
+def test_graphed_decode_replays_match_eager():
+    """Four replays of the captured decode step, with eager work and synchronisations between them,
+    each against the eager step from the same state (same kernels on the same data)."""
+    from paper_2503_13427_amd.layer import GraphedDecode
+    li = make_layer(workload=72, B=2, T=68, NH=2, DQK=256, DV=512)
+    layer = _layer(li)
+    x = torch.from_numpy(li.x).view(torch.bfloat16).cuda()
+    _, st_e = layer.prefill(x[:, :64].contiguous())
+    st_g = tuple(t.clone() for t in st_e)
+    gd = GraphedDecode(layer, st_g, B=2)
+    for t in range(64, 68):
+        ye = layer.step(x[:, t].contiguous(), st_e)
+        junk = torch.randn(1 << 20, device="cuda").sum()          # eager work between replays
+        yg = gd(x[:, t].contiguous()).clone()
+        torch.cuda.synchronize()
+        e_y = rel_err(host_f64(yg), host_f64(ye), 1)
+        e_C = rel_err(host_f64(st_g[0]), host_f64(st_e[0]), 2)
+        print(f"graphed decode t={t}: y {e_y:.3e}, C {e_C:.3e}, junk {float(junk):.1f}")
+        assert e_y <= 1e-3 and e_C <= 1e-5
+        np.testing.assert_allclose(host_f64(st_g[2]), host_f64(st_e[2]), rtol=1e-6, atol=1e-6)

@@ -27,11 +27,14 @@
  *    and the call returns after enqueue.  Launch failures are reported as
  *    MLSTM_ERR_HIP; faults during execution surface at the caller's next
  *    synchronisation.
- *  - Inputs are assumed finite, except that i~ = -inf (nothing written) and
- *    f~ = +inf (nothing forgotten) are allowed.  f~ = -inf (a forget gate of
- *    exactly zero) is supported by mlstm_step only; the chunkwise form takes
- *    differences of in-chunk prefix sums of logsig(f~).  NaN/Inf are not
- *    checked on the hot path and propagate.
+ *  - Inputs are assumed finite, except that i~ = -inf (nothing written),
+ *    f~ = +inf (nothing forgotten) and f~ = -inf are allowed.  f~ = -inf is a
+ *    forget gate of exactly zero: the state restarts from the zero matrix at
+ *    that token, the reset at document borders of packed sequences (App. B,
+ *    "Sequence packing"); both entry points support it.  A restart token with
+ *    i~ = -inf as well leaves an empty state (m = -inf), for which Eqs. 7-8
+ *    are undefined; such rows get h = 0.  NaN/Inf are not checked on the hot
+ *    path and propagate.
  *  - The library is stateless and re-entrant.
  */
 #ifndef LIBMLSTM_MLSTM_H

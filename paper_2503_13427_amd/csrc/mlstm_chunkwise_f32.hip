@@ -19,6 +19,12 @@
 //   floor                        exp(-(b_tau + M_tau))
 // and the chunk's exit max state is b_L + M_L.
 //
+// A forget gate of exactly zero (f~ = -inf, a document border) restarts the state.  The prefix
+// sum b skips the restart token, each row keeps its last restart R_tau, the gate matrix keeps
+// only R_tau <= sig <= tau, p restarts at R_tau, a row at or after a restart has no entry-state
+// term, and a chunk that holds a restart drops its entry state (decay 0) and weights only the
+// keys from its last restart on.
+//
 // One workgroup owns a (sequence, dv tile) pair and walks the chunks in order
 // with its C tile, n and m in LDS.  Everything is fp32; q, k, v may be fp32 or
 // bf16.  This kernel is the fp32 path and the reference schedule; the bf16
@@ -66,6 +72,7 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
     float* g_w = g_floor + L;                           // [L]  key weights
     float* g_den = g_w + L;                             // [L]  1 / max(|den|, floor)
     float* g_sc = g_den + 2 * L;                        // scalars: [0] m_prev, [1] decay
+    float* g_R = g_sc + 8;                              // [L]  last restart at or before the row (-1: none)
 
     const int ntiles = DV / DVT;
     const int64_t seq = blockIdx.x / ntiles;
@@ -108,19 +115,27 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
             const float* ib = ipre + seq * static_cast<int64_t>(T) + t0;
             const float* fb = fpre + seq * static_cast<int64_t>(T) + t0;
             float b = 0.0f, p = -INFINITY;
+            int R = -1;
             for (int t = 0; t < L; ++t) {
-                if (t < lc) b += logsigmoid(fb[t]);
+                const float lg = t < lc ? logsigmoid(fb[t]) : 0.0f;
+                if (lg == -INFINITY) {
+                    R = t;
+                    p = -INFINITY;
+                } else {
+                    b += lg;
+                }
                 const float x = t < lc ? ib[t] - b : -INFINITY;
                 p = fmaxf(p, x);
-                const float M = fmaxf(mprev, p);
+                const float M = R >= 0 ? p : fmaxf(mprev, p);
                 g_ib[t] = x;
                 g_M[t] = M;
-                g_inter[t] = expf(mprev - M);
+                g_R[t] = static_cast<float>(R);
+                g_inter[t] = (R >= 0 || M == -INFINITY) ? 0.0f : expf(mprev - M);
                 g_floor[t] = expf(-(b + M));
             }
             const float ML = g_M[L - 1];
-            for (int t = 0; t < L; ++t) g_w[t] = expf(g_ib[t] - ML);
-            g_sc[1] = expf(mprev - ML);
+            for (int t = 0; t < L; ++t) g_w[t] = (t < R || ML == -INFINITY) ? 0.0f : expf(g_ib[t] - ML);
+            g_sc[1] = (R >= 0 || ML == -INFINITY) ? 0.0f : expf(mprev - ML);
             g_sc[0] = b + ML;  // exit max state m_k
         }
         __syncthreads();
@@ -129,7 +144,7 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
         for (int e = tid; e < L * L; e += kF32Threads) {
             const int t = e / L, s = e % L;
             float val = 0.0f;
-            if (s <= t) {
+            if (s <= t && s >= static_cast<int>(g_R[t]) && g_M[t] != -INFINITY) {
                 float acc = 0.0f;
                 for (int d = 0; d < DQK; ++d) acc += Qs[t * DQK + d] * Ks[s * DQK + d];
                 val = acc * expf(g_ib[s] - g_M[t]);

@@ -137,7 +137,8 @@ struct Cfg {
 template <int L>
 struct alignas(16) GateBuf {
     float x2[L];        // (i~ - b) * log2 e
-    float M2[L];        // M * log2 e
+    float M2[L];        // M * log2 e (0 for a row with no input at all)
+    int R[L];           // last restart (forget gate exactly zero) at or before the row, -1: none
     float interC[L];    // exp(m_prev - M + s) / sqrt(DQK): scale of C_acc^T Q^T
     float interN[L];    // exp(m_prev - M) / sqrt(DQK):     scale of Q n
     float floorv[L];    // exp(-(b + M))
@@ -337,6 +338,27 @@ __device__ __forceinline__ float wave_incl_max(float x) {
     x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x143, 0xc));
     return x;
 }
+// Segmented inclusive max: a lane with ``start`` set begins a new segment, so every lane gets the
+// maximum over the lanes from the last start at or before it (all lanes before it if none).  Each
+// step combines (flag, value) pairs with the associative rule "a later start discards the left".
+__device__ __forceinline__ float wave_seg_incl_max(float x, bool start) {
+    int f = start ? 1 : 0;
+#define MLSTM_SEG_STEP(ctrl, rmask)                                                                        \
+    {                                                                                                     \
+        const float y = MLSTM_DPP(-INFINITY, x, ctrl, rmask);                                             \
+        const int fy = __builtin_amdgcn_update_dpp(0, f, (ctrl), (rmask), 0xf, false);                    \
+        x = f ? x : fmaxf(x, y);                                                                          \
+        f |= fy;                                                                                          \
+    }
+    MLSTM_SEG_STEP(0x111, 0xf)
+    MLSTM_SEG_STEP(0x112, 0xf)
+    MLSTM_SEG_STEP(0x114, 0xf)
+    MLSTM_SEG_STEP(0x118, 0xf)
+    MLSTM_SEG_STEP(0x142, 0xa)
+    MLSTM_SEG_STEP(0x143, 0xc)
+#undef MLSTM_SEG_STEP
+    return x;
+}
 #undef MLSTM_DPP
 // sum over the four 16-lane rows of a wave, in every lane (gfx950 cross-row lane swaps, no LDS)
 __device__ __forceinline__ float sum_rows4(float x) {
@@ -362,51 +384,85 @@ __device__ __forceinline__ float flogsig(float x) {
 // carry the max state and the lazy log-scale from chunk to chunk.  Rows at or beyond
 // nvalid (the partial last chunk of a sequence) are neutral tokens: no input (x = -inf)
 // and no decay (logsig f~ = 0), so they leave the state unchanged.
+//
+// A forget gate of exactly zero (f~ = -inf, a document border) restarts the state: nothing
+// before that token reaches it or any later token.  The prefix sum b skips the restart token
+// (the decay from s to t over tokens s+1..t never includes a restart for the pairs that
+// survive), every row keeps R, its last restart at or before it, and the row's maxima, weights
+// and entry-state terms cover only the tokens from R on.  A chunk that holds a restart drops
+// its entry state: C and n are scaled by zero before this chunk's keys are added.
 template <int L>
 __device__ __forceinline__ void gate_phase(GateBuf<L>& Gb, const float (&gi)[2], const float (&gf)[2], float& m_prev,
                                            float& s_cur, int lane, int nvalid) {
     const bool ok0 = lane < nvalid;
-    const float b = wave_incl_sum(ok0 ? flogsig(gf[0]) : 0.0f);
+    const float lg0 = ok0 ? flogsig(gf[0]) : 0.0f;
+    const bool rs0 = (lg0 == -INFINITY);
+    bool rs1 = false;
+    float lg1 = 0.f;
+    if constexpr (L == 128) {
+        lg1 = (64 + lane < nvalid) ? flogsig(gf[1]) : 0.0f;
+        rs1 = (lg1 == -INFINITY);
+    }
+    // restarts are rare: a chunk without one (a wave-uniform test) takes the plain scans
+    const bool any_restart = __builtin_amdgcn_ballot_w64(rs0 || rs1) != 0;
+    const float b = wave_incl_sum(rs0 ? 0.0f : lg0);
     const float x = ok0 ? gi[0] - b : -INFINITY;
-    const float p = wave_incl_max(x);
-    float b2 = 0.f, x2 = 0.f, p2 = 0.f;
+    float r = -1.f, p;
+    if (any_restart) {
+        r = wave_incl_max(rs0 ? static_cast<float>(lane) : -1.0f);
+        p = wave_seg_incl_max(x, rs0);
+    } else {
+        p = wave_incl_max(x);
+    }
+    float b2 = 0.f, x2 = 0.f, p2 = 0.f, r2 = -1.f;
     if constexpr (L == 128) {
         const bool ok1 = 64 + lane < nvalid;
-        b2 = lane63(b) + wave_incl_sum(ok1 ? flogsig(gf[1]) : 0.0f);
+        b2 = lane63(b) + wave_incl_sum(rs1 ? 0.0f : lg1);
         x2 = ok1 ? gi[1] - b2 : -INFINITY;
-        p2 = fmaxf(lane63(p), wave_incl_max(x2));
+        if (any_restart) {
+            const float r_own = wave_incl_max(rs1 ? static_cast<float>(64 + lane) : -1.0f);
+            r2 = fmaxf(lane63(r), r_own);
+            const float q2 = wave_seg_incl_max(x2, rs1);
+            p2 = (r_own >= 0.0f) ? q2 : fmaxf(lane63(p), q2);
+        } else {
+            p2 = fmaxf(lane63(p), wave_incl_max(x2));
+        }
     }
     const float pL = lane63(L == 128 ? p2 : p);
     const float bL = lane63(L == 128 ? b2 : b);
-    const float ML = fmaxf(m_prev, pL);
-    // an empty state (m = -inf) has nothing to decay
-    const bool empty = (m_prev == -INFINITY);
+    const float rL = lane63(L == 128 ? r2 : r);
+    const bool restart = (rL >= 0.0f);
+    const float ML = restart ? pL : fmaxf(m_prev, pL);
+    // an empty state (m = -inf) has nothing to decay, and a restart drops the state
+    const bool empty = restart || (m_prev == -INFINITY);
     const float dlog = empty ? 0.0f : m_prev - ML;
     const float s_try = s_cur + dlog;
-    const bool eager = s_try < kRenorm;
+    const bool eager = restart || s_try < kRenorm;
     const float s_new = eager ? 0.0f : s_try;
-    auto emit = [&](int tau, float bb, float xx, float pp) {
-        const float M = fmaxf(m_prev, pp);
+    auto emit = [&](int tau, float bb, float xx, float pp, float rr) {
+        const bool fresh = (rr >= 0.0f);   // a restart at or before this row: no entry-state term
+        const float M = fresh ? pp : fmaxf(m_prev, pp);
         Gb.x2[tau] = xx * kLog2e;
-        Gb.M2[tau] = M * kLog2e;
-        Gb.interC[tau] = (M == -INFINITY) ? 0.0f : fexp(m_prev - M + s_cur) * kQScale;
-        Gb.interN[tau] = (M == -INFINITY) ? 0.0f : fexp(m_prev - M) * kQScale;
+        Gb.M2[tau] = (M == -INFINITY) ? 0.0f : M * kLog2e;
+        Gb.R[tau] = static_cast<int>(rr);
+        Gb.interC[tau] = (fresh || M == -INFINITY) ? 0.0f : fexp(m_prev - M + s_cur) * kQScale;
+        Gb.interN[tau] = (fresh || M == -INFINITY) ? 0.0f : fexp(m_prev - M) * kQScale;
         Gb.floorv[tau] = fexp(-(bb + M));
-        const bool none = (xx == -INFINITY);
+        const bool none = (xx == -INFINITY) || (static_cast<float>(tau) < rL);
         Gb.wC[tau] = none ? 0.0f : fexp(xx - ML - s_new);
         const float wn = none ? 0.0f : fexp(xx - ML);
         const uint16_t whi = f32_to_bf16(wn);
         Gb.wb[0][tau] = whi;
         Gb.wb[1][tau] = f32_to_bf16(wn - bf16_to_f32(whi));
     };
-    emit(lane, b, x, p);
-    if constexpr (L == 128) emit(64 + lane, b2, x2, p2);
+    emit(lane, b, x, p, r);
+    if constexpr (L == 128) emit(64 + lane, b2, x2, p2, r2);
     const float m_next = bL + ML;
     if (lane == 0) {
         Gb.scal[0] = (empty || ML == -INFINITY) ? 0.0f : fexp(m_prev - ML);
         Gb.scal[1] = m_next;
         Gb.scal[2] = s_new;
-        Gb.scal[3] = eager ? fexp(s_try) : 1.0f;
+        Gb.scal[3] = restart ? 0.0f : (eager ? fexp(s_try) : 1.0f);
     }
     m_prev = m_next;
     s_cur = s_new;
@@ -811,6 +867,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 const int sb = rem;
                 const int tau = 16 * tb + l16;
                 const float Mt = Gc.M2[tau];
+                const int Rt = Gc.R[tau];
                 const f32x4_t xs = *reinterpret_cast<const f32x4_t*>(&Gc.x2[16 * sb + 4 * g16]);
                 float vals[4];
                 float rsum = 0.f;
@@ -818,7 +875,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 for (int j = 0; j < 4; ++j) {
                     const int sig = 16 * sb + 4 * g16 + j;
                     const float val = Sacc[i][j] * kQScale * fast_exp2(xs[j] - Mt);
-                    vals[j] = (sig <= tau) ? val : 0.f;
+                    // Rt <= sig <= tau as one unsigned comparison (Rt <= tau always)
+                    vals[j] = (static_cast<unsigned>(sig - Rt) <= static_cast<unsigned>(tau - Rt)) ? val : 0.f;
                     rsum += vals[j];
                 }
                 u32x2_t o;
@@ -915,7 +973,10 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 // From an empty state (C = 0, n = 0, m = -inf) the recurrence of Eq. 2-4 over tokens 1..N unrolls to
 // a closed form: with b_t the prefix sums of logsig(f~_t) and x_t = i~_t - b_t,
 //   m_N = b_N + X,  X = max_t x_t,   C_N = sum_t w_t k_t v_t^T,  n_N = sum_t w_t k_t,  w_t = exp(x_t - X)
-// (every weight is <= 1).  A (sub-)segment's local state is therefore one contraction over its
+// (every weight is <= 1).  With restarts (f~ = -inf) the prefix sums skip the restart tokens, only
+// the tokens from the last restart R on carry weight (X is their maximum), and the sub-segment's
+// logsig sum is -inf, so the combine drops whatever state entered it.
+// A (sub-)segment's local state is therefore one contraction over its
 // tokens, with no chunk recurrence: the gates are scanned once over the whole sub-segment, then
 // 64-token tiles of K^T and V^T stream through LDS into the MFMA accumulators.  C and n are the
 // same quantities the chunkwise update accumulates (bf16 w V operand, bf16 hi / lo weights for n).
@@ -928,7 +989,7 @@ struct LocSmem {
     uint16_t Vt[2][kDVT * kLocP];             // V^T[v][tau] (this workgroup's 128 columns)
     float w[kLocMax];                         // x_t, then the weights w_t
     uint16_t wb[2][kLocMax];                  // w_t as bf16 hi / lo
-    float red[2][kWaves];                     // per-wave scan totals and maxima
+    float red[3][kWaves];                     // per-wave scan totals, maxima, last restarts
 };
 static_assert(sizeof(LocSmem) <= 160 * 1024, "LDS budget");
 
@@ -1024,14 +1085,18 @@ local_state_kernel(LocalArgs A) {
     LocRegs rg;
     if (ntok > 0) loc_load(rg, P, tb, v0, tid);   // first tile, in flight during the gate pass
 
-    // gates: block-wide prefix sums of logsig(f~) in rounds of 512 tokens, x_t into LDS, then X
-    float carry = 0.0f, xmax = -INFINITY;
+    // gates: block-wide prefix sums of logsig(f~) in rounds of 512 tokens (restart tokens add
+    // nothing), x_t into LDS, the last restart R, then X over the tokens from R on
+    float carry = 0.0f, rmax = -1.0f, xall = -INFINITY;
     for (int j0 = 0; j0 < ntok; j0 += kThreads) {
         const int t = j0 + tid;
         const bool valid = t < ntok;
         const float fv = valid ? bloadf(P.fg, 4 * t, 4 * tb) : 0.0f;
         const float iv = valid ? bloadf(P.ig, 4 * t, 4 * tb) : 0.0f;
-        const float incl = wave_incl_sum(valid ? flogsig(fv) : 0.0f);
+        const float lg = valid ? flogsig(fv) : 0.0f;
+        const bool rs = (lg == -INFINITY);
+        if (rs) rmax = static_cast<float>(t);
+        const float incl = wave_incl_sum(rs ? 0.0f : lg);
         if (lane == 63) S.red[0][wave] = incl;
         __syncthreads();
         float before = carry, total = 0.0f;
@@ -1044,8 +1109,20 @@ local_state_kernel(LocalArgs A) {
         carry += total;
         const float x = valid ? iv - (before + incl) : -INFINITY;
         if (valid) S.w[t] = x;
-        xmax = fmaxf(xmax, x);
+        xall = fmaxf(xall, x);
         __syncthreads();   // red[0] is rewritten by the next round
+    }
+    const float wr = lane63(wave_incl_max(rmax));
+    if (lane == 0) S.red[2][wave] = wr;
+    __syncthreads();   // the x_t and the restarts of every wave are visible
+    float Rf = -1.0f;
+#pragma unroll
+    for (int w2 = 0; w2 < kWaves; ++w2) Rf = fmaxf(Rf, S.red[2][w2]);
+    const int Rl = static_cast<int>(Rf);   // last restart of the sub-segment, -1: none
+    float xmax = xall;   // no restart: the maximum over every token
+    if (Rl >= 0) {       // block-uniform: only the tokens from the restart on
+        xmax = -INFINITY;
+        for (int t = Rl + tid; t < ntok; t += kThreads) xmax = fmaxf(xmax, S.w[t]);
     }
     const float wm = lane63(wave_incl_max(xmax));
     if (lane == 0) S.red[1][wave] = wm;
@@ -1054,7 +1131,7 @@ local_state_kernel(LocalArgs A) {
 #pragma unroll
     for (int w2 = 0; w2 < kWaves; ++w2) X = fmaxf(X, S.red[1][w2]);
     for (int t = tid; t < ntok; t += kThreads) {
-        const float wv = fexp(S.w[t] - X);
+        const float wv = (t < Rl || X == -INFINITY) ? 0.0f : fexp(S.w[t] - X);
         S.w[t] = wv;
         const uint16_t hi = f32_to_bf16(wv);
         S.wb[0][t] = hi;
@@ -1127,7 +1204,7 @@ local_state_kernel(LocalArgs A) {
         }
         if (tid == 0) {
             slot[kDQK * kDV + kDQK] = carry + X;      // m_loc (-inf for an empty sub-segment)
-            slot[kDQK * kDV + kDQK + 1] = carry;      // sum of logsig(f~)
+            slot[kDQK * kDV + kDQK + 1] = Rl >= 0 ? -INFINITY : carry;   // sum of logsig(f~)
         }
     }
 }
@@ -1174,9 +1251,12 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
         for (int u = 0; u < kBatch; ++u) {
             if (u < nbat) {
                 float* slot = base + static_cast<int64_t>(g0 + u) * kSlotFloats;
-                const float m_new = fmaxf(gs[u] + m_in, mloc[u]);
-                const float a = expf(gs[u] + m_in - m_new);
-                const float b = expf(mloc[u] - m_new);
+                // a restart inside the slot (gs = -inf) drops the running state; an empty slot
+                // (m_loc = -inf) adds nothing
+                const float carried = gs[u] + m_in;
+                const float m_new = fmaxf(carried, mloc[u]);
+                const float a = (carried == -INFINITY) ? 0.0f : expf(carried - m_new);
+                const float b = (mloc[u] == -INFINITY) ? 0.0f : expf(mloc[u] - m_new);
                 const bool entry = ((g0 + u) % R) == R - 1;
                 if (e4 < kE4) {
                     cur.x = a * cur.x + b * loc[u].x;

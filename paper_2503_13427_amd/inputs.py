@@ -33,6 +33,7 @@ import numpy as np
 # tensor ids inside a head's key
 _Q, _K, _V, _I, _F, _C0, _N0, _M0 = 0, 1, 2, 3, 4, 5, 6, 7
 _DEC_OFFSET = 10  # decode-step tensors use ids 10..14
+_DOC = 20         # document lengths of a packed sequence
 
 
 def _rng(seed: int, workload: int, head: int, tensor: int) -> np.random.Generator:
@@ -200,6 +201,29 @@ def make_prefill(*, workload: int, B: int, NH: int, T: int, DQK: int, DV: int, d
         out.C0 = C0.reshape(*shp, DQK, DV)
         out.n0 = n0.reshape(*shp, DQK)
         out.m0 = m0.reshape(*shp)
+    return out
+
+
+def pack_documents(inp: Inputs, mean_len: float, *, workload: int, seed: int = 0,
+                   first: bool = False) -> list:
+    """Mark document borders in ``inp.fpre`` in place: each sequence is a run of packed documents
+    with i.i.d. geometric lengths of mean ``mean_len`` (at least one token), and the first token
+    of every document after the first gets f~ = -inf, a forget gate of exactly zero (the reset at
+    document borders of sequence packing, App. B).  ``first`` also marks token 0, which drops an
+    initial state.  Returns the marked positions per sequence (global head order)."""
+    fp = inp.fpre.reshape(-1, inp.T)
+    heads = np.arange(fp.shape[0]) if inp.heads is None else inp.heads
+    out = []
+    for j, hg in enumerate(heads):
+        rng = _rng(seed, workload, int(hg), _DOC)
+        pos, t = [0] if first else [], 0
+        while True:
+            t += int(rng.geometric(1.0 / mean_len))
+            if t >= inp.T:
+                break
+            pos.append(t)
+        fp[j, pos] = -np.inf
+        out.append(np.asarray(pos, dtype=np.int64))
     return out
 
 

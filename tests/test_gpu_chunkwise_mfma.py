@@ -5,8 +5,9 @@ Parity bar: max relative error <= 2e-2 per (batch, head) slice for h and the fin
 (bf16 q/k/v/h, fp32 state).  Covers several chunks and segments, an initial state, the
 floor branch, short and long memory, the soft-capped gates, T = 0, a partial last chunk
 (T not a multiple of L: no h row beyond T is written), the segment-parallel schedule
-(workspace), chunk-size independence, state carry, decode steps == prefill, run-to-run
-determinism, and the three prefill workloads at full size (sampled heads).
+(workspace), document resets (f~ = -inf) at chunk edges, consecutive tokens, segment starts
+and packed-document borders, chunk-size independence, state carry, decode steps == prefill,
+run-to-run determinism, and the three prefill workloads at full size (sampled heads).
 """
 import numpy as np
 import pytest
@@ -86,6 +87,42 @@ def test_mfma_matches_oracle(case, workspace):
     inp = make_prefill(workload=95, B=B, NH=NH, T=T, DQK=256, DV=512, dtype="bf16", gates=g, state=st)
     o = run(inp, L, workspace=workspace)
     check(inp, o, label=str(case))
+
+
+def _edge_borders(T, L):
+    """Restarts at the first token (drops an initial state), at the last and first rows of a
+    chunk, on consecutive tokens, at a segment's start and at the last token."""
+    pos = [0, L - 1, L, L + 1, 2 * L + 2, 2 * L + 3, T // 2, T - 1]
+    return sorted({p for p in pos if 0 <= p < T})
+
+
+RESET_CASES = [
+    # (B, NH, T, L, gates, state, borders: "edges", "every" or a mean document length)
+    (1, 2, 1000, 64, GateDist(), StateDist(), "edges"),
+    (1, 2, 700, 128, GateDist(f_mu=5, f_sd=2, cap=15.0), StateDist(), "edges"),
+    (1, 2, 2048, 64, GateDist(), None, 150.0),
+    (2, 1, 3000, 128, GateDist(f_mu=5, f_sd=2, cap=15.0), StateDist(), 400.0),
+    (1, 2, 4096, 64, GateDist(f_mu=5, f_sd=2, cap=15.0), None, 1500.0),   # few borders, long memory
+    (1, 1, 256, 64, GateDist(), StateDist(), "every"),
+]
+
+
+@pytest.mark.parametrize("case", RESET_CASES, ids=lambda c: f"B{c[0]}NH{c[1]}T{c[2]}L{c[3]}-{c[6]}")
+@pytest.mark.parametrize("workspace", [False, True], ids=["fused", "segments"])
+def test_document_resets_match_oracle(case, workspace):
+    """f~ = -inf at document borders (sequence packing, App. B): the state restarts there, in the
+    chunk loop, in the local segment states and in their combination."""
+    from paper_2503_13427_amd.inputs import pack_documents
+    B, NH, T, L, g, st, borders = case
+    inp = make_prefill(workload=98, B=B, NH=NH, T=T, DQK=256, DV=512, dtype="bf16", gates=g, state=st)
+    if borders == "edges":
+        inp.fpre[..., _edge_borders(T, L)] = -np.inf
+    elif borders == "every":
+        inp.fpre[...] = -np.inf
+    else:
+        pack_documents(inp, borders, workload=98)
+    o = run(inp, L, workspace=workspace)
+    check(inp, o, label=f"resets {case[:4]} {borders}")
 
 
 @pytest.mark.parametrize("T,L", [(100, 64), (300, 128), (1000, 64)])

@@ -1,8 +1,8 @@
 """mlstm_chunkwise_fwd on small heads (the fp32 VALU kernel) against the fp64 oracle.
 
 Covers the tiny fp32 workload (B=1, NH=1, T=64, d=16, L=16) at the fp32 bar of
-1e-5, chunk-size independence, an initial state, T = 0, bf16 inputs through
-the same kernel, and T decode steps == one prefill of T tokens.
+1e-5, chunk-size independence, an initial state, T = 0, document resets (f~ = -inf),
+bf16 inputs through the same kernel, and T decode steps == one prefill of T tokens.
 """
 import numpy as np
 import pytest
@@ -70,6 +70,24 @@ def test_small_heads_match_oracle(case):
                        state=StateDist() if st else None, k_scale=1 / np.sqrt(DQK))
     out = run_chunk(inp, L)
     compare(inp, out, TOL_F32 if dt == "f32" else TOL_BF16)
+
+
+@pytest.mark.parametrize("borders", ["edges", "every", 20.0])
+@pytest.mark.parametrize("L", [16, 32])
+def test_document_resets_fp32(borders, L):
+    """f~ = -inf (a document border, App. B) restarts the state; fp32 bar."""
+    from paper_2503_13427_amd.inputs import pack_documents
+    T = 150
+    inp = make_prefill(workload=93, B=1, NH=3, T=T, DQK=16, DV=32, dtype="f32", gates=GateDist(),
+                       state=StateDist(), k_scale=0.25)
+    if borders == "edges":
+        inp.fpre[..., [0, L - 1, L, L + 1, 2 * L + 5, 2 * L + 6, T - 1]] = -np.inf
+    elif borders == "every":
+        inp.fpre[...] = -np.inf
+    else:
+        pack_documents(inp, borders, workload=93)
+    out = run_chunk(inp, L)
+    compare(inp, out, TOL_F32, f"resets L{L} {borders}")
 
 
 def test_chunk_size_independence_fp32():

@@ -55,3 +55,18 @@ def test_decode_steps_prefix():
     b = w.decode_inputs(steps=8, heads=[100])
     np.testing.assert_array_equal(a.q[0, 0], b.q[0, 0, :4])
     assert a.q.shape == (1, 1, 4, 256) and a.v.shape == (1, 1, 4, 512)
+
+
+def test_pack_documents_marks_borders():
+    """Borders are f~ = -inf exactly at the returned positions, reproducible per head, with the
+    requested mean document length on a long sequence."""
+    from paper_2503_13427_amd.inputs import GateDist, make_prefill, pack_documents
+    a = make_prefill(workload=5, B=1, NH=2, T=20000, DQK=4, DV=4, dtype="f32", gates=GateDist())
+    pos = pack_documents(a, 100.0, workload=5)
+    for j in range(2):
+        fp = a.fpre.reshape(2, -1)[j]
+        assert np.array_equal(np.flatnonzero(np.isneginf(fp)), pos[j])
+        assert pos[j][0] > 0 and 80 < 20000 / (len(pos[j]) + 1) < 125
+    b = make_prefill(workload=5, B=1, NH=2, T=20000, DQK=4, DV=4, dtype="f32", gates=GateDist())
+    pos_b = pack_documents(b, 100.0, workload=5, first=True)
+    assert pos_b[1][0] == 0 and np.array_equal(pos_b[1][1:], pos[1])

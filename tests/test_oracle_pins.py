@@ -115,6 +115,26 @@ def test_forget_gate_zero_resets_every_step(impl):
     np.testing.assert_allclose(m, ip[:, -1], rtol=1e-15)
 
 
+@pytest.mark.parametrize("impl", IMPLS_RESET)
+def test_document_border_restarts_from_the_zero_state(impl):
+    """App. B (sequence packing): a forget gate of zero at a document border resets the memory
+    to the zero matrix.  With restarts at tokens r (an initial state given), h over each
+    document and the final state equal a fresh run over that document alone from the zero
+    state; h from the zero state does not depend on m_0, so the fresh run's m_0 = 0 is no
+    assumption."""
+    q, k, v, ip, fp, C0, n0, m0 = rand_inputs(21, S=2, T=31, DQK=5, DV=4, state=True)
+    borders = [0, 7, 8, 19, 30]
+    fp[:, borders] = -np.inf
+    h, C, n, m = IMPLS[impl](q, k, v, ip, fp, C0, n0, m0)
+    ends = borders[1:] + [31]
+    for r, e in zip(borders, ends):
+        hf, Cf, nf, mf = IMPLS[impl](q[:, r:e], k[:, r:e], v[:, r:e], ip[:, r:e], fp[:, r:e])
+        np.testing.assert_allclose(h[:, r:e], hf, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(C, Cf, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(n, nf, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(m, mf, rtol=1e-14)
+
+
 @pytest.mark.parametrize("impl", list(IMPLS))
 @pytest.mark.parametrize("i_sd", [0.0, 1.0])
 def test_forget_gate_one_is_weighted_linear_attention(impl, i_sd):

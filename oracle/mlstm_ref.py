@@ -38,6 +38,9 @@ Forms, each written from the paper's statement of the cell (Sec. 2):
                              proj_dtype="bf16" the projections q, k, v and o~ are stored in
                              bf16 (``round_bf16``) before the cell, as a bf16 model holds them.
 * ``round_bf16``             fp64 -> nearest bf16 value (ties to even), returned as fp64.
+* ``gate_preact``            the gate pre-activations of the layer: i~, f~ = softcap(x W + b)
+                             per head (Eq. 11 with the soft-cap of Eq. 13), f~ = -inf on
+                             document-border tokens (the reset of App. B), head-major [B, NH, T].
 """
 from __future__ import annotations
 
@@ -256,6 +259,26 @@ def round_bf16(x):
     _, e = np.frexp(x)                       # x = f 2^e, f in [0.5, 1): leading bit 2^(e-1)
     quantum = np.ldexp(1.0, np.maximum(e - 1, -126) - 7)
     return np.round(x / quantum) * quantum
+
+
+def gate_preact(x, W_gates, gate_bias, cap=15.0, border=None):
+    """Gate pre-activations of one layer, head-major.
+
+    x [B, T, d]; W_gates [d, 2 NH]: the input gate column of each head, then the forget gate
+    column of each head; gate_bias [2, NH].  i~ = softcap(x w_i + b_i), f~ = softcap(x w_f + b_f)
+    (cap None: no cap).  ``border`` [B, T] (bool, optional) marks the first token of a new
+    document, whose forget gate is exactly zero: f~ = -inf there.  Returns ipre, fpre [B, NH, T]
+    in fp64."""
+    x = np.asarray(x, dtype=np.float64)
+    W = np.asarray(W_gates, dtype=np.float64)
+    NH = W.shape[1] // 2
+    b = np.asarray(gate_bias, dtype=np.float64)
+    z = x @ W                                                        # [B, T, 2 NH]
+    ig = soft_cap(z[..., :NH] + b[0], cap)
+    fg = soft_cap(z[..., NH:] + b[1], cap)
+    if border is not None:
+        fg = np.where(np.asarray(border, dtype=bool)[..., None], -np.inf, fg)
+    return np.ascontiguousarray(np.moveaxis(ig, 2, 1)), np.ascontiguousarray(np.moveaxis(fg, 2, 1))
 
 
 def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, cap=15.0,

@@ -150,3 +150,29 @@ def test_layer_bf16_projections_only_round_q_k_v_o():
     c, _ = R.mlstm_layer(xe, Wg, Wp, gb, nw, NH, DQK, DV)
     e, _ = R.mlstm_layer(xe, Wg, Wp, gb, nw, NH, DQK, DV, proj_dtype="bf16")
     np.testing.assert_array_equal(c, e)
+
+
+def test_gate_preact_one_hot_rows_and_borders():
+    """A one-hot token e_j selects row j of W: i~ = softcap(W[j, :NH] + b_i) exactly; the output
+    is head-major; border tokens get f~ = -inf and keep their i~; cap None leaves x W + b."""
+    rng = np.random.default_rng(8)
+    B, T, d, NH = 2, 5, 7, 3
+    W = rng.standard_normal((d, 2 * NH)) * 4
+    b = rng.standard_normal((2, NH))
+    x = np.zeros((B, T, d))
+    js = rng.integers(0, d, (B, T))
+    for bb in range(B):
+        for t in range(T):
+            x[bb, t, js[bb, t]] = 1.0
+    border = np.zeros((B, T), bool); border[0, 2] = border[1, 0] = True
+    ip, fp = R.gate_preact(x, W, b, cap=15.0, border=border)
+    assert ip.shape == (B, NH, T) and fp.shape == (B, NH, T)
+    for bb in range(B):
+        for t in range(T):
+            for h in range(NH):
+                assert ip[bb, h, t] == 15.0 * np.tanh((W[js[bb, t], h] + b[0, h]) / 15.0)
+                want_f = -np.inf if border[bb, t] else 15.0 * np.tanh((W[js[bb, t], NH + h] + b[1, h]) / 15.0)
+                assert fp[bb, h, t] == want_f
+    ip0, fp0 = R.gate_preact(x, W, b, cap=None)
+    np.testing.assert_allclose(ip0[0, :, 1], W[js[0, 1], :NH] + b[0], rtol=1e-15)
+    assert np.abs(ip).max() < 15.0

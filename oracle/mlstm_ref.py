@@ -282,7 +282,7 @@ def gate_preact(x, W_gates, gate_bias, cap=15.0, border=None):
 
 
 def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, cap=15.0,
-                C0=None, n0=None, m0=None, proj_dtype=None):
+                C0=None, n0=None, m0=None, proj_dtype=None, border=None):
     """Multi-head mLSTM layer (Eq. 11), x [B, T, d] -> y [B, T, d] and the final cell state.
 
     W_in [d, NH * (2 DQK + 2 DV + 2)] holds, in column order, the q, k, v projections (head-major:
@@ -292,7 +292,9 @@ def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, 
     (C0, n0, m0) ([B * NH, ...], None: zero state), its h~ goes through the output gate and the
     headwise LayerNorm (weight norm_weight [NH, DV]), the heads are concatenated and projected by
     W_proj [NH * DV, d].  proj_dtype="bf16" rounds q, k, v and o~ to bf16 after the projection
-    (the gates stay in full precision); None keeps every projection in fp64.
+    (the gates stay in full precision); None keeps every projection in fp64.  ``border`` [B, T]
+    (optional) marks document borders of a packed sequence: the forget gate is zero there
+    (``gate_preact``), so each document runs as if from the zero state.
     """
     x = np.asarray(x, dtype=np.float64)
     B, T, d = x.shape
@@ -306,8 +308,10 @@ def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, 
     q = take(NH * DQK).reshape(B, T, NH, DQK)
     k = take(NH * DQK).reshape(B, T, NH, DQK)
     v = take(NH * DV).reshape(B, T, NH, DV)
-    ig = soft_cap(take(NH) + np.asarray(gate_bias, dtype=np.float64)[0], cap)   # [B, T, NH]
-    fg = soft_cap(take(NH) + np.asarray(gate_bias, dtype=np.float64)[1], cap)
+    o_gates = o0
+    take(2 * NH)
+    ig, fg = gate_preact(x, np.asarray(W_in, dtype=np.float64)[:, o_gates:o_gates + 2 * NH], gate_bias, cap,
+                         border)                                    # [B, NH, T] each
     og = take(NH * DV).reshape(B, T, NH, DV)
     assert o0 == P.shape[-1]
     if proj_dtype == "bf16":
@@ -317,7 +321,7 @@ def mlstm_layer(x, W_in, W_proj, gate_bias, norm_weight, NH, DQK, DV, eps=1e-6, 
     heads = lambda a: np.ascontiguousarray(np.moveaxis(a, 2, 1))    # [B, T, NH, D] -> [B, NH, T, D]
     S = B * NH
     h, C, n, m = recurrent(heads(q).reshape(S, T, DQK), heads(k).reshape(S, T, DQK), heads(v).reshape(S, T, DV),
-                           np.moveaxis(ig, 2, 1).reshape(S, T), np.moveaxis(fg, 2, 1).reshape(S, T), C0, n0, m0)
+                           ig.reshape(S, T), fg.reshape(S, T), C0, n0, m0)
     hy = output_gate_norm(h.reshape(B, NH, T, DV), heads(og), norm_weight, None, eps=eps, norm="layer")
     y = np.moveaxis(hy, 1, 2).reshape(B, T, NH * DV) @ np.asarray(W_proj, dtype=np.float64)
     return y, (C, n, m)

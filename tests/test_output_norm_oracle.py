@@ -176,3 +176,28 @@ def test_gate_preact_one_hot_rows_and_borders():
     ip0, fp0 = R.gate_preact(x, W, b, cap=None)
     np.testing.assert_allclose(ip0[0, :, 1], W[js[0, 1], :NH] + b[0], rtol=1e-15)
     assert np.abs(ip).max() < 15.0
+
+
+def test_layer_packed_documents_equal_separate_runs():
+    """App. B at the layer level: a sequence of two packed documents with a border at the second
+    one's first token gives, token for token, the outputs of the layer run on each document alone
+    from the zero state."""
+    rng = np.random.default_rng(9)
+    NH, DQK, DV = 2, 3, 4
+    d = NH * DV
+    T1, T2 = 6, 5
+    x = rng.standard_normal((1, T1 + T2, d))
+    Win = rng.standard_normal((d, NH * (2 * DQK + 2 * DV + 2))) * 0.4
+    Wp = rng.standard_normal((NH * DV, d)) * 0.4
+    gb = np.array([[-1.0, 0.5], [2.0, 3.0]]); nw = 1 + 0.1 * rng.standard_normal((NH, DV))
+    border = np.zeros((1, T1 + T2), bool); border[0, T1] = True
+    y, (C, n, m) = R.mlstm_layer(x, Win, Wp, gb, nw, NH, DQK, DV, border=border)
+    y1, _ = R.mlstm_layer(x[:, :T1], Win, Wp, gb, nw, NH, DQK, DV)
+    y2, (C2, n2, m2) = R.mlstm_layer(x[:, T1:], Win, Wp, gb, nw, NH, DQK, DV)
+    np.testing.assert_allclose(y[:, :T1], y1, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(y[:, T1:], y2, rtol=1e-12, atol=1e-13)
+    # the state scale-free (the separate run starts from m_0 = 0, the packed one restarts at m = i~)
+    np.testing.assert_allclose(C * np.exp(m)[:, None, None], C2 * np.exp(m2)[:, None, None], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(n * np.exp(m)[:, None], n2 * np.exp(m2)[:, None], rtol=1e-12, atol=1e-13)
+    y0, _ = R.mlstm_layer(x, Win, Wp, gb, nw, NH, DQK, DV)
+    assert np.abs(y0[:, T1:] - y2).max() > 1e-3     # without the border the second document sees the first

@@ -162,6 +162,35 @@ mlstm_status mlstm_output_norm(const void* h_tilde, const void* o_pre, mlstm_dty
                                const float* weight, const float* bias, float eps, mlstm_norm norm,
                                int B, int NH, int T, int DV, void* h, void* hip_stream);
 
+/*
+ * Gate pre-activations of an mLSTM layer, the inputs ipre and fpre of the two
+ * cell entry points (Eq. 11: one input and one forget gate column per head,
+ * each with a bias; Eq. 13: the soft-cap; App. B: the reset at document
+ * borders of packed sequences).  For token (b, t) with x = x[b, t, :] and head h:
+ *
+ *   ipre[b, h, t] = softcap(x . w_t[h, :]      + bias[0, h])
+ *   fpre[b, h, t] = softcap(x . w_t[NH + h, :] + bias[1, h]),  or -inf where
+ *                   border[b, t] != 0 (a forget gate of exactly zero)
+ *
+ * with softcap(z) = cap * tanh(z / cap), or z itself when cap == 0.  The
+ * products are bf16 with fp32 accumulation; the gates stay fp32.
+ *
+ *   x      [B, T, d] (dt, MLSTM_BF16 only)
+ *   w_t    [2 NH, d] bf16: row h holds head h's input gate weights, row NH + h
+ *          its forget gate weights (the transpose of a [d, 2 NH] projection)
+ *   bias   [2, NH] fp32, or NULL (zero)
+ *   border [B, T] uint8, or NULL (no document borders)
+ *   ipre, fpre [B, NH, T] fp32 outputs (head-major: the cell's layout)
+ *
+ * cap must be finite and >= 0 (else MLSTM_ERR_BAD_SHAPE).  Built: d a
+ * multiple of 128 and 2 NH <= 64 (else MLSTM_ERR_UNSUPPORTED).  B T == 0
+ * launches nothing.  The outputs may not overlap each other or any input
+ * (MLSTM_ERR_ALIAS).
+ */
+mlstm_status mlstm_gate_preact(const void* x, mlstm_dtype dt, const void* w_t, const float* bias, float cap,
+                               const unsigned char* border, int B, int T, int d, int NH,
+                               float* ipre, float* fpre, void* hip_stream);
+
 /* Static, human-readable name of a status code. */
 const char* mlstm_status_string(mlstm_status s);
 

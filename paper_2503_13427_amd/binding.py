@@ -42,6 +42,8 @@ lib.mlstm_step.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _
 lib.mlstm_step.restype = _i
 lib.mlstm_output_norm.argtypes = [_vp, _vp, _i, _vp, _vp, ctypes.c_float, _i, _i, _i, _i, _i, _vp, _vp]
 lib.mlstm_output_norm.restype = _i
+lib.mlstm_gate_preact.argtypes = [_vp, _i, _vp, _vp, ctypes.c_float, _vp, _i, _i, _i, _i, _vp, _vp, _vp]
+lib.mlstm_gate_preact.restype = _i
 lib.mlstm_status_string.argtypes = [_i]
 lib.mlstm_status_string.restype = ctypes.c_char_p
 lib.mlstm_version.argtypes = []
@@ -133,3 +135,20 @@ def mlstm_output_norm(h_tilde, o_pre, weight, bias, eps: float, norm: str, h, st
     code = {"layer": MLSTM_NORM_LAYER, "rms": MLSTM_NORM_RMS}[norm]
     _check(lib.mlstm_output_norm(_ptr(h_tilde), _ptr(o_pre), _dtype_code(h_tilde), _ptr(weight), _ptr(bias),
                                  float(eps), code, B, NH, T, DV, _ptr(h), _stream(stream)))
+
+
+def mlstm_gate_preact(x, w_t, bias, cap: float, border, ipre, fpre, stream=None) -> None:
+    """Gate pre-activations of a layer: x [B, T, d] bf16 (a decode step: [B, d], taken as T = 1),
+    w_t [2 NH, d] bf16 (input gate rows, then forget gate rows), bias [2, NH] fp32 or None,
+    cap (0: none), border [B, T] uint8/bool or None -> ipre, fpre [B, NH, T] fp32 (decode:
+    [B, NH])."""
+    if x.dim() == 2:
+        B, d = x.shape
+        T = 1
+    else:
+        B, T, d = x.shape
+    NH = w_t.shape[0] // 2
+    if border is not None and border.dtype == torch.bool:
+        border = border.view(torch.uint8)
+    _check(lib.mlstm_gate_preact(_ptr(x), _dtype_code(x), _ptr(w_t), _ptr(bias), float(cap), _ptr(border), B, T, d,
+                                 NH, _ptr(ipre), _ptr(fpre), _stream(stream)))

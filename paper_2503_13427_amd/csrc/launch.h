@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 #include <stddef.h>
+#include <stdint.h>
 
 #include "mlstm.h"
 
@@ -20,6 +21,12 @@ constexpr int kOutNormMaxDV = 2048;
 hipError_t launch_output_norm(mlstm_dtype dt, const void* h_tilde, const void* o_pre, const float* weight,
                               const float* bias, float eps, int rms, int64_t rows, int NH, int T, int DV, void* h,
                               hipStream_t stream);
+
+// --- gate pre-activations of a layer (bf16 x, W^T [2 NH, d]) -----------------
+constexpr int kGateMaxCols = 64;   // 2 NH
+constexpr int kGateDMultiple = 128;
+hipError_t launch_gate_preact(const void* x, const void* w_t, const float* bias, float cap, const uint8_t* border,
+                              int B, int T, int d, int NH, float* ipre, float* fpre, hipStream_t stream);
 
 // --- chunkwise prefill, fp32 VALU kernel (small heads) -----------------------
 struct ChunkArgs {

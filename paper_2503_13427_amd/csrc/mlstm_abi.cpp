@@ -189,4 +189,35 @@ mlstm_status mlstm_output_norm(const void* h_tilde, const void* o_pre, mlstm_dty
     return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
 }
 
+mlstm_status mlstm_gate_preact(const void* x, mlstm_dtype dt, const void* w_t, const float* bias, float cap,
+                               const unsigned char* border, int B, int T, int d, int NH, float* ipre, float* fpre,
+                               void* hip_stream) {
+    if (B < 0 || T < 0 || d <= 0 || NH <= 0) return MLSTM_ERR_BAD_SHAPE;
+    int64_t M, nx, ng, nw;
+    if (!mul_ok(B, T, &M) || !mul_ok(M, d, &nx) || !mul_ok(M, NH, &ng) || !mul_ok(2 * static_cast<int64_t>(NH), d, &nw))
+        return MLSTM_ERR_BAD_SHAPE;
+    if (M != 0 && (!x || !w_t || !ipre || !fpre)) return MLSTM_ERR_NULL_PTR;
+    if (!(cap >= 0.0f) || cap > 3.0e38f) return MLSTM_ERR_BAD_SHAPE;   // rejects NaN and inf too
+    if (dt != MLSTM_BF16 || d % mlstm::kGateDMultiple || 2 * static_cast<int64_t>(NH) > mlstm::kGateMaxCols)
+        return MLSTM_ERR_UNSUPPORTED;
+    // a workgroup addresses its 64 rows of x, and all of w_t, through 32-bit byte offsets
+    if (64 * static_cast<int64_t>(d) * 2 >= (int64_t(1) << 31) || nw * 2 >= (int64_t(1) << 31))
+        return MLSTM_ERR_UNSUPPORTED;
+    const void* ptrs[] = {x, w_t, bias, border, ipre, fpre};
+    for (const void* p : ptrs)
+        if (misaligned(p)) return MLSTM_ERR_MISALIGNED;
+    const Range rx = range_of(x, nx * 2), rw = range_of(w_t, nw * 2);
+    const Range rb = range_of(bias, bias ? 2 * static_cast<size_t>(NH) * 4 : 0);
+    const Range rd = range_of(border, border ? static_cast<size_t>(M) : 0);
+    const Range ri = range_of(ipre, ng * 4), rf = range_of(fpre, ng * 4);
+    if (overlap(ri, rf)) return MLSTM_ERR_ALIAS;
+    for (const Range& o : {ri, rf})
+        for (const Range& r : {rx, rw, rb, rd})
+            if (overlap(o, r)) return MLSTM_ERR_ALIAS;
+    if (M == 0) return MLSTM_OK;
+    hipError_t e = mlstm::launch_gate_preact(x, w_t, bias, cap, border, B, T, d, NH, ipre, fpre,
+                                             static_cast<hipStream_t>(hip_stream));
+    return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
 }  // extern "C"

@@ -25,7 +25,8 @@ def declared_functions():
 
 def test_header_declares_expected_entry_points():
     assert declared_functions() == sorted(["mlstm_chunkwise_fwd", "mlstm_chunkwise_workspace_bytes", "mlstm_step",
-                                           "mlstm_output_norm", "mlstm_status_string", "mlstm_version"])
+                                           "mlstm_output_norm", "mlstm_gate_preact", "mlstm_status_string",
+                                           "mlstm_version"])
 
 
 @pytest.mark.parametrize("name", declared_functions())
@@ -217,3 +218,54 @@ def test_norm_alias(inp, off):
     a = norm_args()
     a["h"] = a[inp] + off
     assert call_norm(a) == 5
+
+
+# ---- gate pre-activation validation ------------------------------------------------------------
+
+def gate_args(**over):
+    a = dict(x=fake(0), dt=Bd.MLSTM_BF16, w=fake(1), b=fake(2), cap=15.0, border=fake(3), B=2, T=2048, d=4096,
+             NH=8, ip=fake(4), fp=fake(5), stream=None)
+    a.update(over)
+    return a
+
+
+def call_gate(a):
+    return lib.mlstm_gate_preact(a["x"], a["dt"], a["w"], a["b"], a["cap"], a["border"], a["B"], a["T"], a["d"],
+                                 a["NH"], a["ip"], a["fp"], a["stream"])
+
+
+@pytest.mark.parametrize("field", ["x", "w", "ip", "fp"])
+def test_gate_null_pointer(field):
+    assert call_gate(gate_args(**{field: None})) == 1
+
+
+def test_gate_optional_pointers_and_empty_batch():
+    # bias and border are optional; B T == 0 needs no pointer and launches nothing
+    assert call_gate(gate_args(B=0, x=None, w=None, ip=None, fp=None)) == 0
+    assert call_gate(gate_args(T=0, x=None, w=None, ip=None, fp=None, b=None, border=None)) == 0
+
+
+@pytest.mark.parametrize("over", [dict(B=-1), dict(T=-1), dict(d=0), dict(NH=0), dict(cap=-1.0),
+                                  dict(cap=float("nan")), dict(cap=float("inf"))])
+def test_gate_bad_shape(over):
+    assert call_gate(gate_args(**over)) == 2
+
+
+@pytest.mark.parametrize("over", [dict(dt=Bd.MLSTM_F32), dict(d=4000), dict(d=64), dict(NH=33)])
+def test_gate_unsupported(over):
+    assert call_gate(gate_args(**over)) == 3
+
+
+@pytest.mark.parametrize("field", ["x", "w", "b", "border", "ip", "fp"])
+def test_gate_misaligned(field):
+    a = gate_args()
+    a[field] += 4
+    assert call_gate(a) == 4
+
+
+@pytest.mark.parametrize("out,inp,off", [("fp", "ip", 16), ("ip", "x", 4096), ("fp", "w", 0), ("ip", "b", 0),
+                                         ("fp", "border", 16)])
+def test_gate_alias(out, inp, off):
+    a = gate_args()
+    a[out] = a[inp] + off
+    assert call_gate(a) == 5

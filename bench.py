@@ -14,6 +14,7 @@ Extra objects on the same line:
   cpu_baseline  the fp64 CPU oracle on the same workload (host cores);
   decode        1024 consecutive mlstm_step calls at B=256, NH=8: us per step,
                 us per sequence-token, achieved GB/s vs 8 TB/s;
+  decode_b1     mlstm_step at B=1, NH=8 (single-sequence generation), in place;
   prefill_large the two larger prefill workloads (B=8 x T=8192 soft-capped,
                 and B=4 x T=32768 from a nonzero state, L=128);
   output_norm   the hidden-state output h = sigmoid(o~) * LayerNorm(h~) w + b
@@ -214,6 +215,30 @@ def bench_decode(w, steps, stream, warm=16):
                 wall_s=wall, state_finite=finite)
 
 
+def bench_step_small(B, NH, steps, stream):
+    """mlstm_step for a small batch (B = 1: the single-sequence generation of the paper's speed
+    benchmarks), the state updated in place; the C stream is split over many workgroups per
+    sequence.  us per step and the step's algorithmic bytes against HBM bandwidth."""
+    from paper_2503_13427_amd import binding as mb
+    DQK, DV = 256, 512
+    g = torch.Generator(device="cuda").manual_seed(7)
+    q = torch.randn(B, NH, DQK, generator=g, device="cuda").bfloat16()
+    k = torch.randn(B, NH, DQK, generator=g, device="cuda").bfloat16()
+    v = torch.randn(B, NH, DV, generator=g, device="cuda").bfloat16()
+    ip = torch.randn(B, NH, generator=g, device="cuda")
+    fp = torch.randn(B, NH, generator=g, device="cuda") + 3
+    C = torch.randn(B, NH, DQK, DV, generator=g, device="cuda") * 0.1
+    n = torch.randn(B, NH, DQK, generator=g, device="cuda").abs()
+    m = torch.zeros(B, NH, device="cuda")
+    h = torch.empty(B, NH, DV, dtype=torch.bfloat16, device="cuda")
+    fn = lambda: mb.mlstm_step(q, k, v, ip, fp, C, n, m, h, C, n, m, stream=stream)
+    _, ev = time_steps(fn, steps, 10, stream)
+    t = ev / steps
+    by = acc.step_bytes(B, NH, DQK, DV)
+    return dict(workload=f"decode_B{B}_NH{NH}", us_per_step=t * 1e6, bytes_per_step=by, gbs=by / t / 1e9,
+                hbm_frac=by / t / 1e9 / acc.PEAK_HBM_GBS)
+
+
 def bench_output_norm(B, NH, T, DV, steps, stream, label):
     """h = sigmoid(o~) * LayerNorm(h~) * w + b on bf16 rows already in HBM (HBM-bound)."""
     from paper_2503_13427_amd import binding as mb
@@ -245,7 +270,7 @@ def synthetic_layer(seed=11, L=64):
     g = torch.Generator(device="cuda").manual_seed(seed)
     rn = lambda *shape: torch.randn(*shape, generator=g, device="cuda")
     w = LayerWeights(W_qkvo=(rn(d, NH * (2 * DQK + 2 * DV)) * d ** -0.5).bfloat16(),
-                     W_gates=(rn(d, 2 * NH) * d ** -0.5).bfloat16(),
+                     W_gates_t=(rn(2 * NH, d) * d ** -0.5).bfloat16(),
                      W_proj=(rn(NH * DV, d) * (NH * DV) ** -0.5).bfloat16(),
                      gate_bias=rn(2, NH) + torch.tensor([[-2.0], [3.0]], device="cuda"),
                      norm_weight=1 + 0.1 * rn(NH, DV), NH=NH, DQK=DQK, DV=DV)
@@ -265,7 +290,8 @@ def bench_layer_prefill(layer, B, T, steps, stream):
     t_total = run(lambda: layer.prefill(x, workspace=ws))
     x2 = x.reshape(B * T, d)
     t_proj = run(lambda: layer._project(x2))
-    t_heads = run(lambda: layer.project_heads(x)) - t_proj
+    t_gates = run(lambda: layer.gates(x))
+    t_heads = run(lambda: layer.project_heads(x)) - t_proj - t_gates
     q, k, v, o, ig, fg = layer.project_heads(x)
     h = torch.empty(B, NH, T, DV, dtype=torch.bfloat16, device="cuda")
     C = torch.empty(B, NH, DQK, DV, device="cuda")
@@ -279,7 +305,7 @@ def bench_layer_prefill(layer, B, T, steps, stream):
     tok = B * T
     fl_proj = acc.flops_layer_projections(tok, d, NH, DQK, DV)
     fl_cell = acc.flops_chunkwise(B * NH, T, layer.L, DQK, DV).total
-    stages = dict(projections=t_proj, head_major_copies=t_heads, cell=t_cell, output_norm=t_norm,
+    stages = dict(projections=t_proj, gates=t_gates, head_major_copies=t_heads, cell=t_cell, output_norm=t_norm,
                   output_projection=t_out)
     return dict(workload=f"layer_prefill_B{B}_T{T}_d{d}_NH{NH}", B=B, T=T, tokens_per_s=tok / t_total,
                 ms_per_call=t_total * 1e3, tflops=(fl_proj + fl_cell) / t_total / 1e12,
@@ -413,6 +439,7 @@ def main():
     if args.only in (None, "decode") and not args.skip_decode:
         log(f"decode {configs.DECODE_B256.name}: {args.decode_steps} steps")
         res["decode"] = bench_decode(configs.DECODE_B256, args.decode_steps, stream)
+        res["decode_b1"] = bench_step_small(1, 8, args.decode_steps, stream)
         torch.cuda.empty_cache()
 
     line = {"metric": METRIC, "value": None, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -435,6 +462,7 @@ def main():
         line["prefill_large"] = res["prefill_large"]
     if "decode" in res:
         line["decode"] = res["decode"]
+        line["decode_b1"] = res["decode_b1"]
     if "output_norm" in res:
         line["output_norm"] = res["output_norm"]
     if "layer" in res:

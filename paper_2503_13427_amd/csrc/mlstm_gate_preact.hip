@@ -10,8 +10,9 @@
 // The projection is a skinny product: M = B T tokens by K = d by N = 2 NH gate
 // columns.  It runs on bf16 MFMA (16x16x32, fp32 accumulation) so that the kernel
 // stays bound by reading x once from HBM:
-//   - a workgroup of four waves owns MT 16-token tiles; each wave takes a quarter of
-//     K, and the four partial sums meet in LDS;
+//   - a workgroup of NW waves owns MT 16-token tiles; each wave takes 1 / NW of K,
+//     and the partial sums meet in LDS (four waves and four tiles for many tokens;
+//     sixteen waves and one tile for a decode step, whose K walk is then short);
 //   - both operands are 16-byte row reads: x rows as they are stored, the weights as
 //     W^T [2 NH, d] (one row of d weights per gate column), which the caller stores
 //     in that layout; W^T is small and stays in L2;
@@ -27,8 +28,6 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kGpWaves = 4;
-constexpr int kGpThreads = 64 * kGpWaves;
 constexpr int kGpUnroll = 4;          // k steps whose loads are issued together
 constexpr int kRsrcWord3 = 0x00020000;
 
@@ -57,10 +56,11 @@ struct GateArgs {
     float* fpre;
 };
 
-// MT 16-token tiles per workgroup, NCT 16-column tiles of the 2 NH gate columns.
-template <int MT, int NCT>
-__global__ void __launch_bounds__(kGpThreads) gate_preact_kernel(GateArgs A) {
-    __shared__ f32x4_t red[kGpWaves][MT * NCT][64];
+// MT 16-token tiles per workgroup, NCT 16-column tiles of the 2 NH gate columns, NW waves.
+template <int MT, int NCT, int NW>
+__global__ void __launch_bounds__(64 * NW) gate_preact_kernel(GateArgs A) {
+    constexpr int kThreadsW = 64 * NW;
+    __shared__ f32x4_t red[NW][MT * NCT][64];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -71,7 +71,7 @@ __global__ void __launch_bounds__(kGpThreads) gate_preact_kernel(GateArgs A) {
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(A.x + r0 * A.d, static_cast<uint32_t>(rows * A.d * 2));
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(A.wt, static_cast<uint32_t>(2 * A.NH) * A.d * 2);
 
-    const int kq = A.d / kGpWaves;   // this wave's quarter of K (a multiple of 32)
+    const int kq = A.d / NW;         // this wave's share of K (a multiple of 32)
     const int k0 = wave * kq;
     const int steps = kq / 32;
     f32x4_t acc[MT][NCT];
@@ -113,14 +113,14 @@ __global__ void __launch_bounds__(kGpThreads) gate_preact_kernel(GateArgs A) {
 
     // lane group (tile mt, column tile ct, lane ln): column 16 ct + ln % 16, rows 4 (ln / 16) + 0..3
     const int ncol = 2 * A.NH;
-    for (int it = tid; it < MT * NCT * 64; it += kGpThreads) {
+    for (int it = tid; it < MT * NCT * 64; it += kThreadsW) {
         const int mc = it >> 6, ln = it & 63;
         const int mt = mc / NCT, ct = mc % NCT;
         const int j = 16 * ct + (ln & 15);
         if (j >= ncol) continue;
         f32x4_t z = red[0][mc][ln];
 #pragma unroll
-        for (int w = 1; w < kGpWaves; ++w) z += red[w][mc][ln];
+        for (int w = 1; w < NW; ++w) z += red[w][mc][ln];
         const bool forget = j >= A.NH;
         const int hd = forget ? j - A.NH : j;
         const float bj = A.bias ? A.bias[j] : 0.0f;
@@ -138,14 +138,15 @@ __global__ void __launch_bounds__(kGpThreads) gate_preact_kernel(GateArgs A) {
     }
 }
 
-template <int MT>
+template <int MT, int NW>
 void launch_mt(const GateArgs& a, int nct, hipStream_t stream) {
     const dim3 grid(static_cast<unsigned>((a.M + 16 * MT - 1) / (16 * MT)));
+    const dim3 block(64 * NW);
     switch (nct) {
-        case 1: hipLaunchKernelGGL((gate_preact_kernel<MT, 1>), grid, dim3(kGpThreads), 0, stream, a); break;
-        case 2: hipLaunchKernelGGL((gate_preact_kernel<MT, 2>), grid, dim3(kGpThreads), 0, stream, a); break;
-        case 3: hipLaunchKernelGGL((gate_preact_kernel<MT, 3>), grid, dim3(kGpThreads), 0, stream, a); break;
-        default: hipLaunchKernelGGL((gate_preact_kernel<MT, 4>), grid, dim3(kGpThreads), 0, stream, a); break;
+        case 1: hipLaunchKernelGGL((gate_preact_kernel<MT, 1, NW>), grid, block, 0, stream, a); break;
+        case 2: hipLaunchKernelGGL((gate_preact_kernel<MT, 2, NW>), grid, block, 0, stream, a); break;
+        case 3: hipLaunchKernelGGL((gate_preact_kernel<MT, 3, NW>), grid, block, 0, stream, a); break;
+        default: hipLaunchKernelGGL((gate_preact_kernel<MT, 4, NW>), grid, block, 0, stream, a); break;
     }
 }
 
@@ -166,9 +167,11 @@ hipError_t launch_gate_preact(const void* x, const void* w_t, const float* bias,
     a.ipre = ipre;
     a.fpre = fpre;
     const int nct = (2 * NH + 15) / 16;
-    // four tiles per workgroup once there are enough tokens to fill the chip with them
-    if (a.M >= 4096) launch_mt<4>(a, nct, stream);
-    else launch_mt<1>(a, nct, stream);
+    // four tiles per workgroup once there are enough tokens to fill the chip with them; a decode
+    // step's few tokens get sixteen waves on one tile (K walks of d / 512 steps)
+    if (a.M >= 4096) launch_mt<4, 4>(a, nct, stream);
+    else if (a.M <= 16 && d % (32 * 16) == 0) launch_mt<1, 16>(a, nct, stream);
+    else launch_mt<1, 4>(a, nct, stream);
     return hipGetLastError();
 }
 

@@ -3,9 +3,17 @@
 // Generation Kernels": the outer product, the dot products and the pointwise
 // gate math run in one kernel so C is read once and written once).
 //
-// One workgroup owns one (batch, head) sequence, so n and m may be updated in
-// place: every element of C and n is read and written by the same thread, and
-// m is written only after a barrier that follows every read of it.
+// With enough sequences to fill the chip, one workgroup owns one (batch, head)
+// sequence, so n and m may be updated in place: every element of C and n is read
+// and written by the same thread, and m is written only after a barrier that
+// follows every read of it.
+//
+// With few sequences (a decode step at batch 1 has 8), P workgroups split a
+// sequence's DV columns so that the C stream runs on many CUs.  Each of them owns
+// all DQK rows of its columns (the read-out C'^T q^ needs no exchange) and
+// recomputes the scalar n'.q^ from n, which no workgroup of this launch writes;
+// n' and m' are written by a second, small kernel that runs after it on the same
+// stream, so an in-place update stays exact.
 //
 // The kernel is HBM-bound: C is streamed as float4 (128-bit) non-temporal loads
 // and stores along DV; each thread walks a column group down the DQK rows with
@@ -26,16 +34,22 @@ __global__ void __launch_bounds__(kStepThreads)
 step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __restrict__ v,
             const float* __restrict__ ipre, const float* __restrict__ fpre,
             const float* C, const float* n, const float* m,
-            int DQK, int DV, TIn* __restrict__ h, float* C_out, float* n_out, float* m_out) {
+            int DQK, int DV, int P, TIn* __restrict__ h, float* C_out, float* n_out, float* m_out) {
     extern __shared__ float smem[];
     float* qs = smem;                 // [DQK]   q / sqrt(DQK)
     float* iks = qs + DQK;            // [DQK]   i * k
-    float* red = iks + DQK;           // [RG * DV] partial read-outs
+    float* red = iks + DQK;           // [RG * DVs] partial read-outs
     __shared__ float wsum[kStepThreads / 64];
 
-    const int64_t head = blockIdx.x;
+    // P workgroups per sequence, each owning DV / P columns (P = 1: the whole row and n, m)
+    const int64_t head = blockIdx.x / P;
+    const int part = blockIdx.x % P;
+    const bool write_nm = (P == 1);
+    const int DVs = DV / P;
+    const int cv0 = part * DVs;       // first column of this workgroup
     const int tid = threadIdx.x;
-    const int NC4 = DV >> 2;
+    const int NC4 = DVs >> 2;         // float4 columns of this workgroup
+    const int ROW4 = DV >> 2;         // float4 pitch of a C row
     const int RG = NC4 >= kStepThreads ? 1 : kStepThreads / NC4;
     const int rg = RG == 1 ? 0 : tid / NC4;    // row group: rows rg, rg + RG, ...
     const int c4_first = tid % NC4;            // first float4 column
@@ -47,13 +61,20 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
     // C_out may be C itself, so the compiler cannot hoist loads over stores; the next batch
     // is loaded explicitly before the current one is stored (disjoint rows, so the order is
     // exact).  The first batch is issued before the gate prologue, which it does not need.
-    const f4_t* Ch = reinterpret_cast<const f4_t*>(C + head * static_cast<int64_t>(DQK) * DV);
-    f4_t* Ch_out = reinterpret_cast<f4_t*>(C_out + head * static_cast<int64_t>(DQK) * DV);
-    auto row = [&](int r) { return static_cast<int64_t>(rg + r * RG) * NC4; };
+    const f4_t* Ch = reinterpret_cast<const f4_t*>(C + head * static_cast<int64_t>(DQK) * DV + cv0);
+    f4_t* Ch_out = reinterpret_cast<f4_t*>(C_out + head * static_cast<int64_t>(DQK) * DV + cv0);
+    auto row = [&](int r) { return static_cast<int64_t>(rg + r * RG) * ROW4; };
     f4_t cur[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u)
         if (u < nrows) cur[u] = __builtin_nontemporal_load(&Ch[row(u) + c4_first]);
+    // v of the first column group rides along with the first batch (it does not wait for the gates)
+    const TIn* vh = v + head * DV + cv0;
+    float vf[4] = {0.f, 0.f, 0.f, 0.f};
+    if (active && c4_first < NC4) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) vf[e] = io<TIn>::load(vh, 4 * c4_first + e);
+    }
 
     // s1: scalar gates (Eqs. 2, 7, 8), computed redundantly by every thread
     const float mprev = m[head];
@@ -70,18 +91,18 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
     float* nh_out = n_out + head * DQK;
 
     // s3: n' = f n + i k, and the partial n'.q^ (Eq. 4, denominator of Eq. 5)
-    float part = 0.0f;
+    float dot = 0.0f;
     for (int d = tid; d < DQK; d += kStepThreads) {
         const float qd = io<TIn>::load(qh, d) * qscale;
         const float ikd = ig * io<TIn>::load(kh, d);
         qs[d] = qd;
         iks[d] = ikd;
         const float nn = fg * nh[d] + ikd;
-        nh_out[d] = nn;
-        part += nn * qd;
+        if (write_nm) nh_out[d] = nn;
+        dot += nn * qd;
     }
-    part = wave_sum(part);
-    if ((tid & 63) == 0) wsum[tid >> 6] = part;
+    dot = wave_sum(dot);
+    if ((tid & 63) == 0) wsum[tid >> 6] = dot;
     __syncthreads();  // also orders every read of m[head] before the write below
     float qn = 0.0f;
 #pragma unroll
@@ -89,15 +110,17 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
     const float inv = 1.0f / fmaxf(fabsf(qn), expf(-mnew));
 
     // s2 + s4: the C stream and num = C'^T q^ (Eqs. 3, 5)
-    const TIn* vh = v + head * DV;
     for (int c4 = c4_first; active && c4 < NC4; c4 += c4_stride) {
         if (c4 != c4_first) {
 #pragma unroll
             for (int u = 0; u < kBatch; ++u)
                 if (u < nrows) cur[u] = __builtin_nontemporal_load(&Ch[row(u) + c4]);
         }
-        const float v0 = io<TIn>::load(vh, 4 * c4 + 0), v1 = io<TIn>::load(vh, 4 * c4 + 1);
-        const float v2 = io<TIn>::load(vh, 4 * c4 + 2), v3 = io<TIn>::load(vh, 4 * c4 + 3);
+        const bool first = (c4 == c4_first);
+        const float v0 = first ? vf[0] : io<TIn>::load(vh, 4 * c4 + 0);
+        const float v1 = first ? vf[1] : io<TIn>::load(vh, 4 * c4 + 1);
+        const float v2 = first ? vf[2] : io<TIn>::load(vh, 4 * c4 + 2);
+        const float v3 = first ? vf[3] : io<TIn>::load(vh, 4 * c4 + 3);
         float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
         for (int r0 = 0; r0 < nrows; r0 += kBatch) {
             f4_t nxt[kBatch];
@@ -130,7 +153,7 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
         }
         if (RG == 1) {
             // s5: h = num / max(|n'.q^|, exp(-m'))
-            TIn* hh = h + head * DV;
+            TIn* hh = h + head * DV + cv0;
             io<TIn>::store(hh, 4 * c4 + 0, a0 * inv);
             io<TIn>::store(hh, 4 * c4 + 1, a1 * inv);
             io<TIn>::store(hh, 4 * c4 + 2, a2 * inv);
@@ -141,14 +164,42 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
     }
     if (RG > 1) {
         __syncthreads();
-        TIn* hh = h + head * DV;
-        for (int j = tid; j < DV; j += kStepThreads) {
+        TIn* hh = h + head * DV + cv0;
+        for (int j = tid; j < DVs; j += kStepThreads) {
             float s = 0.0f;
-            for (int r = 0; r < RG; ++r) s += red[r * DV + j];
+            for (int r = 0; r < RG; ++r) s += red[r * DVs + j];
             io<TIn>::store(hh, j, s * inv);
         }
     }
-    if (tid == 0) m_out[head] = mnew;
+    if (write_nm && tid == 0) m_out[head] = mnew;
+}
+
+// n' = f n + i k and m' for each sequence (the split launch's second kernel); every element of
+// n is read and written by one thread, and m' is written after the barrier that follows every
+// read of m, so n_out and m_out may be n and m.
+template <typename TIn>
+__global__ void __launch_bounds__(256)
+step_state_kernel(const TIn* __restrict__ k, const float* __restrict__ ipre, const float* __restrict__ fpre,
+                  const float* n, const float* m, int DQK, float* n_out, float* m_out) {
+    const int64_t head = blockIdx.x;
+    const float mprev = m[head];
+    const float a = logsigmoid(fpre[head]);
+    const float it = ipre[head];
+    const float mnew = fmaxf(a + mprev, it);
+    const float fg = expf(a + mprev - mnew);
+    const float ig = expf(it - mnew);
+    for (int d = threadIdx.x; d < DQK; d += blockDim.x)
+        n_out[head * DQK + d] = fg * n[head * DQK + d] + ig * io<TIn>::load(k + head * DQK, d);
+    __syncthreads();
+    if (threadIdx.x == 0) m_out[head] = mnew;
+}
+
+// Column splits per sequence: enough workgroups for the 256 CUs, at least 32 columns each (every
+// row access then covers whole 128-byte lines).
+static int step_splits(int heads, int DV) {
+    int P = 1;
+    while (static_cast<int64_t>(heads) * P < 256 && DV % (8 * P) == 0 && DV / (2 * P) >= 32) P *= 2;
+    return P;
 }
 
 hipError_t launch_step(mlstm_dtype dt, const void* q, const void* k, const void* v, const float* ipre,
@@ -156,27 +207,34 @@ hipError_t launch_step(mlstm_dtype dt, const void* q, const void* k, const void*
                        int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
                        hipStream_t stream) {
     const int heads = B * NH;
-    const int NC4 = DV / 4;
-    const int RG = NC4 >= kStepThreads ? 1 : kStepThreads / NC4;
-    const size_t lds = sizeof(float) * (2 * static_cast<size_t>(DQK) + (RG > 1 ? static_cast<size_t>(RG) * DV : 0));
+    const int P = step_splits(heads, DV);
+    const size_t lds = step_lds_bytes(DQK, DV / P);
+    const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(heads) * P));
     if (dt == MLSTM_BF16) {
-        hipLaunchKernelGGL(step_kernel<bf16_t>, dim3(heads), dim3(kStepThreads), lds, stream,
+        hipLaunchKernelGGL(step_kernel<bf16_t>, grid, dim3(kStepThreads), lds, stream,
                            static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
-                           static_cast<const bf16_t*>(v), ipre, fpre, C, n, m, DQK, DV,
+                           static_cast<const bf16_t*>(v), ipre, fpre, C, n, m, DQK, DV, P,
                            static_cast<bf16_t*>(h), C_out, n_out, m_out);
+        if (P > 1)
+            hipLaunchKernelGGL(step_state_kernel<bf16_t>, dim3(heads), dim3(256), 0, stream,
+                               static_cast<const bf16_t*>(k), ipre, fpre, n, m, DQK, n_out, m_out);
     } else {
-        hipLaunchKernelGGL(step_kernel<float>, dim3(heads), dim3(kStepThreads), lds, stream,
+        hipLaunchKernelGGL(step_kernel<float>, grid, dim3(kStepThreads), lds, stream,
                            static_cast<const float*>(q), static_cast<const float*>(k),
-                           static_cast<const float*>(v), ipre, fpre, C, n, m, DQK, DV,
+                           static_cast<const float*>(v), ipre, fpre, C, n, m, DQK, DV, P,
                            static_cast<float*>(h), C_out, n_out, m_out);
+        if (P > 1)
+            hipLaunchKernelGGL(step_state_kernel<float>, dim3(heads), dim3(256), 0, stream,
+                               static_cast<const float*>(k), ipre, fpre, n, m, DQK, n_out, m_out);
     }
     return hipGetLastError();
 }
 
-size_t step_lds_bytes(int DQK, int DV) {
-    const int NC4 = DV / 4;
+// LDS of one workgroup owning DVs columns: q^ and i k, then the partial read-outs of its row groups
+size_t step_lds_bytes(int DQK, int DVs) {
+    const int NC4 = DVs / 4;
     const int RG = NC4 >= kStepThreads ? 1 : kStepThreads / NC4;
-    return sizeof(float) * (2 * static_cast<size_t>(DQK) + (RG > 1 ? static_cast<size_t>(RG) * DV : 0));
+    return sizeof(float) * (2 * static_cast<size_t>(DQK) + (RG > 1 ? static_cast<size_t>(RG) * DVs : 0));
 }
 
 }  // namespace mlstm

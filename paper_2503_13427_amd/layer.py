@@ -2,17 +2,18 @@
 
 x [B, T, d] -> y [B, T, d], d = NH * DV:
 
-1. input projection: one bf16 GEMM for q, k, v and o~ (head-major columns, bf16 output) and one
-   bf16 GEMM with fp32 output for the two gate pre-activations (one column per head each), both
-   hipBLASLt on ROCm;
-2. gate biases and the soft-cap a * tanh(x / a) of Eq. 13 (a = 15) on the fp32 gates;
-3. head-major copies, since the C ABI takes [B, NH, T, D] rows;
+1. input projection: one bf16 GEMM for q, k, v and o~ (head-major columns, bf16 output;
+   hipBLASLt on ROCm);
+2. ``mlstm_gate_preact``: the two gate pre-activations per head (bf16 products, fp32), their
+   biases, the soft-cap a * tanh(x / a) of Eq. 13 (a = 15) and the document borders of a packed
+   sequence (f~ = -inf, App. B), written head-major;
+3. head-major copies of q, k, v and o~, since the C ABI takes [B, NH, T, D] rows;
 4. the cell: ``mlstm_chunkwise_fwd`` for a prefill, ``mlstm_step`` for one decode step;
 5. ``mlstm_output_norm``: h = sigmoid(o~) * LayerNorm(h~) * weight, per head;
 6. concatenation of the heads and the output projection (bf16 GEMM).
 
-The projections are plain library GEMMs around the cell; every step of the cell and of the
-output norm runs in libmlstm.  The layer's pre-norm (Norm(x) in the block, Eq. 12) belongs to
+The q, k, v, o~ and output projections are plain library GEMMs around the cell; the gates, the
+cell and the output norm run in libmlstm.  The layer's pre-norm (Norm(x) in the block, Eq. 12) belongs to
 the block, not to the layer, and is not applied.
 """
 from __future__ import annotations
@@ -30,7 +31,7 @@ State = Tuple[torch.Tensor, torch.Tensor, torch.Tensor]   # C [B, NH, DQK, DV], 
 @dataclass
 class LayerWeights:
     W_qkvo: torch.Tensor      # [d, NH (2 DQK + 2 DV)] bf16: q, k, v, o~ columns, head-major
-    W_gates: torch.Tensor     # [d, 2 NH] bf16: input gate columns, then forget gate columns
+    W_gates_t: torch.Tensor   # [2 NH, d] bf16: input gate rows, then forget gate rows
     W_proj: torch.Tensor      # [NH DV, d] bf16
     gate_bias: torch.Tensor   # [2, NH] fp32
     norm_weight: torch.Tensor # [NH, DV] fp32
@@ -47,9 +48,9 @@ class LayerWeights:
         W = torch.from_numpy(np.ascontiguousarray(li.W_in)).view(torch.bfloat16)
         a = NH * (2 * DQK + DV)
         W_qkvo = torch.cat([W[:, :a], W[:, a + 2 * NH:]], dim=1).contiguous()
-        W_gates = W[:, a:a + 2 * NH].contiguous()
+        W_gates_t = W[:, a:a + 2 * NH].t().contiguous()
         Wp = torch.from_numpy(np.ascontiguousarray(li.W_proj)).view(torch.bfloat16)
-        return LayerWeights(W_qkvo.to(device), W_gates.to(device), Wp.to(device),
+        return LayerWeights(W_qkvo.to(device), W_gates_t.to(device), Wp.to(device),
                             torch.from_numpy(li.gate_bias).to(device), torch.from_numpy(li.norm_weight).to(device),
                             NH, DQK, DV)
 
@@ -59,41 +60,49 @@ class MLSTMLayer:
         self.w, self.L, self.eps, self.cap = w, L, eps, cap
 
     def _project(self, x2: torch.Tensor):
-        """x2 [R, d] bf16 -> q, k [R, NH, DQK], v, o [R, NH, DV] bf16, i, f [R, NH] fp32."""
+        """x2 [R, d] bf16 -> q, k [R, NH, DQK], v, o [R, NH, DV] bf16 (views of one GEMM output)."""
         w = self.w
         NH, DQK, DV = w.NH, w.DQK, w.DV
         P = torch.matmul(x2, w.W_qkvo)
-        # bf16 products accumulated and returned in fp32: the gates never pass through bf16
-        G = torch.mm(x2, w.W_gates, out_dtype=torch.float32) + w.gate_bias.reshape(1, 2 * NH)
-        if self.cap is not None:
-            G = self.cap * torch.tanh(G / self.cap)
         R = x2.shape[0]
         c = [0, NH * DQK, 2 * NH * DQK, NH * (2 * DQK + DV), NH * (2 * DQK + 2 * DV)]
         q = P[:, c[0]:c[1]].view(R, NH, DQK)
         k = P[:, c[1]:c[2]].view(R, NH, DQK)
         v = P[:, c[2]:c[3]].view(R, NH, DV)
         o = P[:, c[3]:c[4]].view(R, NH, DV)
-        return q, k, v, o, G[:, :NH], G[:, NH:]
+        return q, k, v, o
 
-    def project_heads(self, x: torch.Tensor):
+    def gates(self, x: torch.Tensor, border: Optional[torch.Tensor] = None):
+        """i~, f~ head-major, fp32: [B, NH, T] for x [B, T, d], [B, NH] for a decode step x [B, d];
+        ``border`` [B, T] (bool or uint8) marks the first token of each new document."""
+        w = self.w
+        shape = (x.shape[0], w.NH) if x.dim() == 2 else (x.shape[0], w.NH, x.shape[1])
+        ig = torch.empty(shape, dtype=torch.float32, device=x.device)
+        fg = torch.empty(shape, dtype=torch.float32, device=x.device)
+        mb.mlstm_gate_preact(x, w.W_gates_t, w.gate_bias, self.cap or 0.0, border, ig, fg)
+        return ig, fg
+
+    def project_heads(self, x: torch.Tensor, border: Optional[torch.Tensor] = None):
         """Steps 1-3 for a prefill: x [B, T, d] -> head-major q, k [B, NH, T, DQK], v, o~
         [B, NH, T, DV] (bf16) and the capped gate pre-activations i~, f~ [B, NH, T] (fp32)."""
         w = self.w
         B, T, d = x.shape
         NH, DQK, DV = w.NH, w.DQK, w.DV
-        q, k, v, o, ig, fg = self._project(x.reshape(B * T, d))
+        q, k, v, o = self._project(x.reshape(B * T, d))
         hm = lambda a, D: a.view(B, T, NH, D).transpose(1, 2).contiguous()   # head-major [B, NH, T, D]
-        gm = lambda a: a.reshape(B, T, NH).transpose(1, 2).contiguous()
-        return hm(q, DQK), hm(k, DQK), hm(v, DV), hm(o, DV), gm(ig), gm(fg)
+        ig, fg = self.gates(x, border)
+        return hm(q, DQK), hm(k, DQK), hm(v, DV), hm(o, DV), ig, fg
 
     def prefill(self, x: torch.Tensor, state: Optional[State] = None,
-                workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, State]:
+                workspace: Optional[torch.Tensor] = None,
+                border: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, State]:
         """x [B, T, d] bf16 -> (y [B, T, d] bf16, the cell state after the T tokens).  ``workspace``
-        (uint8, ``mlstm_chunkwise_workspace_bytes``) is allocated per call when not given."""
+        (uint8, ``mlstm_chunkwise_workspace_bytes``) is allocated per call when not given;
+        ``border`` [B, T] marks document borders of packed sequences (the state restarts there)."""
         w = self.w
         B, T, d = x.shape
         NH, DQK, DV = w.NH, w.DQK, w.DV
-        q, k, v, o, ig, fg = self.project_heads(x)
+        q, k, v, o, ig, fg = self.project_heads(x, border)
         h = torch.empty(B, NH, T, DV, dtype=torch.bfloat16, device=x.device)
         C = torch.empty(B, NH, DQK, DV, device=x.device)
         n = torch.empty(B, NH, DQK, device=x.device)
@@ -111,11 +120,12 @@ class MLSTMLayer:
         """One decode step: x [B, d] bf16 -> y [B, d]; the state is updated in place."""
         w = self.w
         B, d = x.shape
-        q, k, v, o, ig, fg = self._project(x)
+        q, k, v, o = self._project(x)
         q, k, v, o = q.contiguous(), k.contiguous(), v.contiguous(), o.contiguous()
+        ig, fg = self.gates(x)
         C, n, m = state
         h = torch.empty(B, w.NH, w.DV, dtype=torch.bfloat16, device=x.device)
-        mb.mlstm_step(q, k, v, ig.contiguous(), fg.contiguous(), C, n, m, h, C, n, m)
+        mb.mlstm_step(q, k, v, ig, fg, C, n, m, h, C, n, m)
         mb.mlstm_output_norm(h, o, w.norm_weight, None, self.eps, "layer", h)
         return torch.matmul(h.reshape(B, w.NH * w.DV), w.W_proj)
 

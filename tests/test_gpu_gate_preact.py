@@ -3,8 +3,8 @@ against the fp64 oracle ``gate_preact``.
 
 bf16 x and weights (the oracle upcasts the same bf16 values exactly), fp32 accumulation and
 fp32 gates: the bar is the fp32 one, max relative error <= 1e-5 per (batch, head) slice, and
-border tokens must hold exactly -inf in f~ while keeping their i~.  Covers both tile paths
-(fewer and more than 4096 tokens), ragged token tiles, a partial gate-column tile (2 NH = 6),
+border tokens must hold exactly -inf in f~ while keeping their i~.  Covers the three launch shapes
+(at most 16 tokens, fewer and more than 4096 tokens), ragged token tiles, a partial gate-column tile (2 NH = 6),
 several column tiles (NH = 16, 32), a decode step ([B, d] input), no cap, no bias, and the
 65 536-token layer shape on sampled tokens.
 """
@@ -72,6 +72,8 @@ CASES = [
     (1, 300, 384, 16, 0.0, False, True),     # two column tiles, no cap, no bias
     (1, 64, 128, 32, 15.0, True, True),      # four column tiles
     (3, 4100, 128, 8, 0.0, True, False),     # tiles crossing batch boundaries
+    (1, 1, 4096, 8, 15.0, True, True),       # one token: sixteen-wave path
+    (3, 5, 512, 16, 15.0, True, True),       # 15 tokens, two column tiles: sixteen-wave path
 ]
 
 
@@ -84,7 +86,7 @@ def test_gate_preact_matches_oracle(case):
     got = run(x, w_t, bias, cap, border)
     want = R.gate_preact(bf16_bits_to_f32(x), bf16_bits_to_f32(w_t).T, np.zeros((2, NH)) if bias is None else bias,
                          cap=cap if cap > 0 else None, border=border)
-    compare(got, want, str(case))
+    compare(got, want, str(case), per_head=T >= 16)
 
 
 def test_gate_preact_decode_step():

@@ -56,6 +56,27 @@ def test_layer_prefill_matches_oracle(B, T, NH, L):
     assert e_g <= 1e-4     # fp32 accumulation of bf16 products; a bf16 round trip would show ~1e-2
 
 
+def test_layer_prefill_with_document_borders():
+    """A packed sequence: borders (f~ = -inf from the gate kernel) restart the state per document
+    (App. B); against the oracle layer with the same border mask."""
+    from paper_2503_13427_amd.layer import MLSTMLayer  # noqa: F401  (import check)
+    B, T, NH = 2, 300, 2
+    li = make_layer(workload=73, B=B, T=T, NH=NH, DQK=256, DV=512)
+    border = np.zeros((B, T), bool)
+    border[0, [40, 64, 65, 200]] = True
+    border[1, [0, 128, 299]] = True
+    layer = _layer(li)
+    x = torch.from_numpy(li.x).view(torch.bfloat16).cuda()
+    y, _ = layer.prefill(x, border=torch.from_numpy(border).cuda())
+    torch.cuda.synchronize()
+    yr, _ = R.mlstm_layer(bf16_bits_to_f32(li.x), bf16_bits_to_f32(li.W_in), bf16_bits_to_f32(li.W_proj),
+                          li.gate_bias, li.norm_weight, NH, 256, 512, eps=1e-6, cap=15.0, proj_dtype="bf16",
+                          border=border)
+    err = rel_err(host_f64(y), yr, 1)
+    print(f"layer with borders: y {err:.3e}")
+    assert np.isfinite(host_f64(y)).all() and err <= TOL_BF16
+
+
 def test_layer_decode_continues_the_prefill():
     li = make_layer(workload=71, B=2, T=132, NH=2, DQK=256, DV=512)
     layer = _layer(li)

@@ -1,7 +1,10 @@
 """mlstm_step on the GPU against the fp64 recurrent oracle (Eqs. 2-5, 7-8).
 
 Parity bar: max relative error (per (batch, head) slice, see helpers) <= 1e-5
-for fp32 q/k/v/h and <= 2e-2 for bf16 q/k/v/h, fp32 state in both cases.
+for fp32 q/k/v/h and <= 2e-2 for bf16 q/k/v/h, fp32 state in both cases.  Few
+sequences take the column-split launch (several workgroups per sequence, n' and
+m' from a second kernel), many take one workgroup per sequence; both run in
+place and out of place.
 """
 import os
 
@@ -43,11 +46,14 @@ def run_steps(q, k, v, ip, fp, C, n, m, dtype, in_place=True):
         C2, n2, m2 = torch.empty_like(Cd), torch.empty_like(nd), torch.empty_like(md)
     for t in range(steps):
         hs = torch.empty(B, S, DV, dtype=tdt, device="cuda")
-        qt = tq[:, t].contiguous().reshape(B, S, DQK)
-        kt = tk[:, t].contiguous().reshape(B, S, DQK)
-        vt = tv[:, t].contiguous().reshape(B, S, DV)
-        it = tip[:, t].contiguous().reshape(B, S)
-        ft = tfp[:, t].contiguous().reshape(B, S)
+        # fresh copies: with one sequence a step's slice is contiguous already, and a view of it
+        # would start mid-buffer (the library requires 16-byte aligned tensors)
+        cp = lambda a: a.clone(memory_format=torch.contiguous_format)
+        qt = cp(tq[:, t]).reshape(B, S, DQK)
+        kt = cp(tk[:, t]).reshape(B, S, DQK)
+        vt = cp(tv[:, t]).reshape(B, S, DV)
+        it = cp(tip[:, t]).reshape(B, S)
+        ft = cp(tfp[:, t]).reshape(B, S)
         if in_place:
             mb.mlstm_step(qt, kt, vt, it, ft, Cd, nd, md, hs, Cd, nd, md)
         else:
@@ -105,6 +111,21 @@ def test_step_bf16_xlstm_head_matches_oracle(dist):
         fp[::3, 2] = -np.inf     # forget gate exactly zero: the state restarts
         ip[1::3, 4] = -np.inf    # nothing written ...
         fp[1::3, 4] = np.inf     # ... and nothing forgotten: a neutral token
+    check(q, k, v, ip, fp, *rand_state(rng, S, DQK, DV), "bf16", TOL_BF16)
+
+
+@pytest.mark.parametrize("S", [1, 8, 300])
+def test_step_bf16_head_counts(S):
+    """One sequence and B = 1 x 8 heads split each head's columns over many workgroups (n', m'
+    from the second kernel); 300 heads keep one workgroup per head.  In place, several steps."""
+    rng = np.random.default_rng(100 + S)
+    steps, DQK, DV = 4, 256, 512
+    q = bf16(rng.standard_normal((S, steps, DQK)))
+    k = bf16(rng.standard_normal((S, steps, DQK)))
+    v = bf16(rng.standard_normal((S, steps, DV)))
+    ip = rng.standard_normal((S, steps)).astype(np.float32)
+    fp = rng.normal(3, 1, (S, steps)).astype(np.float32)
+    fp[0, 2] = -np.inf
     check(q, k, v, ip, fp, *rand_state(rng, S, DQK, DV), "bf16", TOL_BF16)
 
 

@@ -589,13 +589,16 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         nin = slot + kDQK * kDV;
         m_prev = slot[kDQK * kDV + kDQK + 2];
     }
-    if (Cin && g > 0) {
-        // a segment entry slot (four rows interleaved): each accumulator tile is one 16-byte load
+    // L = 64: a segment entry slot is loaded after the first chunk's staging loads, so that their
+    // waits do not include it (at L = 128 the early load measured faster)
+    const bool slot_entry = (Cin && g > 0);
+    if (slot_entry && L == 128) {
 #pragma unroll
         for (int t = 0; t < NDB * NQ; ++t)
 #pragma unroll
             for (int vt = 0; vt < VT; ++vt)
                 Cacc[t][vt] = *reinterpret_cast<const f32x4_t*>(Cin + slot_c4(cdrow(t, 0) / 4, v0 + vcol(vt) + l16));
+    } else if (slot_entry) {
     } else if (Cin) {
         // C0: the workgroup's 256 x 128 tile in coalesced 16-byte pieces, staged in LDS (rows of
         // kStageP floats, before the chunk loop uses it) and picked up in the accumulator layout
@@ -654,6 +657,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         vt_store_scaled<L>(S.Vs[1], pv, S.G[c_begin & 1].wC, wave, lane);
         vt_store_plain<L>(S.Vs[0], pv, wave, lane);
         load_qk<L>(rqk, P, t0, 1, tid);
+    }
+    if (slot_entry && L == 64) {
+        // a segment entry slot (four rows interleaved): each accumulator tile is one 16-byte load
+#pragma unroll
+        for (int t = 0; t < NDB * NQ; ++t)
+#pragma unroll
+            for (int vt = 0; vt < VT; ++vt)
+                Cacc[t][vt] = *reinterpret_cast<const f32x4_t*>(Cin + slot_c4(cdrow(t, 0) / 4, v0 + vcol(vt) + l16));
     }
 
     f32x4_t Nacc[VT][NTT];

@@ -1,0 +1,91 @@
+"""Pins of the backward-pass oracle (CPU only).
+
+``recurrent_grad`` (autograd over the step-by-step cell) is tied to central finite differences of
+the NumPy recurrent form, an independent implementation; ``parallel_grad`` (the closed form over
+the parallel form) is tied to ``recurrent_grad``.  A planted mistake in a copy of the closed form
+(a dropped term, a wrong sign) must fail the comparison.
+"""
+import numpy as np
+import pytest
+
+from oracle import mlstm_grad as G
+from oracle import mlstm_ref as R
+
+
+def inputs(seed, S=2, T=7, DQK=3, DV=2, i_mu=0.0, f_mu=3.0, f_sd=1.0):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((S, T, DQK))
+    k = rng.standard_normal((S, T, DQK))
+    v = rng.standard_normal((S, T, DV))
+    ip = rng.normal(i_mu, 1.0, (S, T))
+    fp = rng.normal(f_mu, f_sd, (S, T))
+    dh = rng.standard_normal((S, T, DV))
+    return q, k, v, ip, fp, dh
+
+
+def loss(q, k, v, ip, fp, dh):
+    h, *_ = R.recurrent(q, k, v, ip, fp)
+    return float((h * dh).sum())
+
+
+DISTS = {"standard": dict(), "floor_active": dict(i_mu=-6.0), "short_memory": dict(f_mu=-1.0, f_sd=2.0)}
+
+
+@pytest.mark.parametrize("dist", list(DISTS))
+def test_recurrent_grad_matches_finite_differences(dist):
+    q, k, v, ip, fp, dh = inputs(1, **DISTS[dist])
+    grads = G.recurrent_grad(q, k, v, ip, fp, dh)
+    args = [q, k, v, ip, fp]
+    eps = 1e-6
+    for j, (x, g) in enumerate(zip(args, grads)):
+        fd = np.zeros_like(x)
+        for idx in np.ndindex(x.shape):
+            xp = x.copy(); xp[idx] += eps
+            xm = x.copy(); xm[idx] -= eps
+            ap = list(args); ap[j] = xp
+            am = list(args); am[j] = xm
+            fd[idx] = (loss(*ap, dh) - loss(*am, dh)) / (2 * eps)
+        np.testing.assert_allclose(g, fd, rtol=1e-6, atol=1e-8, err_msg=f"input {j}")
+
+
+@pytest.mark.parametrize("dist", list(DISTS))
+@pytest.mark.parametrize("shape", [(2, 7, 3, 2), (1, 40, 5, 4)])
+def test_parallel_grad_matches_recurrent_grad(dist, shape):
+    S, T, DQK, DV = shape
+    q, k, v, ip, fp, dh = inputs(2, S, T, DQK, DV, **DISTS[dist])
+    a = G.recurrent_grad(q, k, v, ip, fp, dh)
+    b = G.parallel_grad(q, k, v, ip, fp, dh)
+    for j, (x, y) in enumerate(zip(a, b)):
+        np.testing.assert_allclose(y, x, rtol=1e-9, atol=1e-11, err_msg=f"input {j}")
+
+
+def test_v_gradient_is_linear_in_dh_and_closed_form_at_one_token():
+    """T = 1 from the zero state: h = (q^.k) v / max(|q^.k|, exp(-i~)) (with the weight e^{i~}
+    and m_1 = max(logsig f~, i~) cancelling), so dh/dv is that scalar ratio."""
+    q, k, v, ip, fp, dh = inputs(3, S=3, T=1, DQK=4, DV=2)
+    dq, dk, dv, di, df = G.parallel_grad(q, k, v, ip, fp, dh)
+    qk = (q[:, 0] * k[:, 0]).sum(-1) / 2.0
+    m = np.maximum(R.logsigmoid(fp[:, 0]), ip[:, 0])
+    w = np.exp(ip[:, 0] - m)
+    ratio = w * qk / np.maximum(np.abs(w * qk), np.exp(-m))
+    np.testing.assert_allclose(dv[:, 0], ratio[:, None] * dh[:, 0], rtol=1e-12)
+    np.testing.assert_allclose(df[:, 0], 0.0, atol=1e-15)   # nothing before the first token to decay
+
+
+def test_planted_mistakes_fail():
+    """A copy of the closed form with the denominator term dropped, or the forget-gate sign
+    flipped, no longer matches the definition."""
+    q, k, v, ip, fp, dh = inputs(4, S=1, T=9, DQK=3, DV=2)   # |D~| above the floor: dD~ is live
+    ref = G.recurrent_grad(q, k, v, ip, fp, dh)
+    good = G.parallel_grad(q, k, v, ip, fp, dh)
+    assert all(np.allclose(x, y, rtol=1e-9, atol=1e-11) for x, y in zip(ref, good))
+    src = open(G.__file__).read()
+    ns = {}
+    bad1 = src.replace("W = (dN @ v[s].T + dD[:, None]) * Ft", "W = (dN @ v[s].T) * Ft")
+    bad2 = src.replace("da = np.cumsum((P - di)[::-1])[::-1]", "da = np.cumsum((P + di)[::-1])[::-1]")
+    for bad in (bad1, bad2):
+        assert bad != src
+        ns = {}
+        exec(compile(bad, "planted", "exec"), ns)
+        got = ns["parallel_grad"](q, k, v, ip, fp, dh)
+        assert not all(np.allclose(x, y, rtol=1e-6, atol=1e-9) for x, y in zip(ref, got))

@@ -23,7 +23,9 @@ Extra objects on the same line:
   layer         one xLSTM-7B-shaped mLSTM layer (d = 4096, random weights): prefill
                 of 65536 tokens as batch x context (1 x 65536, 8 x 8192, 64 x 1024)
                 with the time of each stage, and decode steps at B = 1 and 256,
-                eager and as a captured HIP graph.
+                eager and as a captured HIP graph;
+  backward      mlstm_parallel_bwd (training-mode gradients over the parallel form) on
+                the headline prefill shape: ms per call, FLOP/s vs the fp32 VALU peak.
 Every timed section is preceded by 0.25 s of untimed calls (clock settle).
 """
 from __future__ import annotations
@@ -347,6 +349,32 @@ def bench_layer(steps, decode_steps, stream):
     return out
 
 
+def bench_backward(w, steps, stream):
+    """mlstm_parallel_bwd on the headline prefill shape (bf16 q/k/v, fp32 gates and dh): ms per call
+    and FLOP/s (the parallel form's count) against the fp32 VALU peak."""
+    from paper_2503_13427_amd import binding as mb
+    g = torch.Generator(device="cuda").manual_seed(17)
+    B, NH, T, DQK, DV = w.B, w.NH, w.T, w.DQK, w.DV
+    q = torch.randn(B, NH, T, DQK, generator=g, device="cuda").bfloat16()
+    k = (torch.randn(B, NH, T, DQK, generator=g, device="cuda") / 4).bfloat16()
+    v = torch.randn(B, NH, T, DV, generator=g, device="cuda").bfloat16()
+    ip = torch.randn(B, NH, T, generator=g, device="cuda")
+    fp = torch.randn(B, NH, T, generator=g, device="cuda") + 3
+    dh = torch.randn(B, NH, T, DV, generator=g, device="cuda")
+    outs = [torch.empty(B, NH, T, DQK, device="cuda"), torch.empty(B, NH, T, DQK, device="cuda"),
+            torch.empty(B, NH, T, DV, device="cuda"), torch.empty(B, NH, T, device="cuda"),
+            torch.empty(B, NH, T, device="cuda")]
+    ws = torch.empty(mb.mlstm_parallel_bwd_workspace_bytes(B, NH, T, DV), dtype=torch.uint8, device="cuda")
+    fn = lambda: mb.mlstm_parallel_bwd(q, k, v, ip, fp, dh, *outs, ws, stream=stream)
+    _, ev = time_steps(fn, steps, 2, stream)
+    t = ev / steps
+    fl = acc.flops_parallel_bwd(B * NH, T, DQK, DV)
+    fl_d2 = 2 * acc.flops_chunkwise(B * NH, T, w.L, DQK, DV).total   # App. D.2: backward = 2 x forward
+    return dict(workload=f"backward_{w.name}", ms_per_call=t * 1e3, tokens_per_s=B * T / t, flops_per_call=fl,
+                tflops=fl / t / 1e12, valu_frac=fl / t / 1e12 / acc.PEAK_FP32_VALU_TFLOPS,
+                app_d2_flops=fl_d2, app_d2_tflops=fl_d2 / t / 1e12)
+
+
 def cpu_baseline(w, max_seconds=30.0):
     """The fp64 oracle on the headline workload, timed on the host.  Heads are independent, so
     the sample is a subset of heads over the full sequence (all heads if they fit the budget)."""
@@ -375,7 +403,9 @@ def main():
     ap.add_argument("--skip-output-norm", action="store_true")
     ap.add_argument("--skip-cpu-baseline", action="store_true")
     ap.add_argument("--skip-layer", action="store_true")
-    ap.add_argument("--only", choices=["prefill", "decode", "large", "output_norm", "layer", "calls"], default=None,
+    ap.add_argument("--skip-backward", action="store_true")
+    ap.add_argument("--only", choices=["prefill", "decode", "large", "output_norm", "layer", "backward", "calls"],
+                    default=None,
                     help="run one part only (profiling runs); 'calls' makes --calls untimed prefill calls of "
                          "--workload and then one --copy-mib MiB device copy, for counter runs")
     ap.add_argument("--workload", default=configs.PREFILL_T2048.name,
@@ -436,6 +466,10 @@ def main():
         log("mLSTM layer (projections + cell + output norm + output projection)")
         res["layer"] = bench_layer(max(3, args.steps // 20), max(50, args.decode_steps // 4), stream)
         torch.cuda.empty_cache()
+    if args.only in (None, "backward") and not args.skip_backward:
+        log(f"backward over the parallel form, {w.name}")
+        res["backward"] = bench_backward(w, max(3, args.steps // 20), stream)
+        torch.cuda.empty_cache()
     if args.only in (None, "decode") and not args.skip_decode:
         log(f"decode {configs.DECODE_B256.name}: {args.decode_steps} steps")
         res["decode"] = bench_decode(configs.DECODE_B256, args.decode_steps, stream)
@@ -467,6 +501,8 @@ def main():
         line["output_norm"] = res["output_norm"]
     if "layer" in res:
         line["layer"] = res["layer"]
+    if "backward" in res:
+        line["backward"] = res["backward"]
     if not args.skip_cpu_baseline and args.only in (None, "prefill"):
         log("cpu baseline: fp64 oracle")
         line["cpu_baseline"] = cpu_baseline(w)

@@ -191,6 +191,34 @@ mlstm_status mlstm_gate_preact(const void* x, mlstm_dtype dt, const void* w_t, c
                                const unsigned char* border, int B, int T, int d, int NH,
                                float* ipre, float* fpre, void* hip_stream);
 
+/*
+ * Backward pass of the cell for training (Sec. 2, "Training Mode"): the
+ * gradients of a loss with respect to q, k, v, ipre and fpre, given its
+ * gradient dh with respect to the outputs h~ of a forward call from the zero
+ * initial state (C0, n0, m0 all NULL in mlstm_chunkwise_fwd).  It works on the
+ * parallel form (Eq. 10): h~_t = N_t / max(|D_t|, 1) in unscaled units with
+ * N_t, D_t sums over s <= t of exp(b_t - b_s + i~_s) (k_s . q^_t) (times v_s
+ * for N), b the prefix sums of logsig(f~), every exponential evaluated
+ * relative to the max state of Eq. 2.  Work is O(T^2 (DQK + DV)) per
+ * sequence, in fp32.
+ *
+ *   q, k [B, NH, T, DQK], v [B, NH, T, DV] (dt)   ipre, fpre [B, NH, T] fp32
+ *   dh [B, NH, T, DV] fp32
+ *   dq, dk [B, NH, T, DQK], dv [B, NH, T, DV], dipre, dfpre [B, NH, T] fp32
+ *   workspace: device scratch of at least mlstm_parallel_bwd_workspace_bytes
+ *   bytes (else MLSTM_ERR_WORKSPACE); its contents on entry do not matter.
+ *
+ * Built: DQK and DV multiples of 16, DQK <= 256, DV <= 512 (else
+ * MLSTM_ERR_UNSUPPORTED).  T == 0 launches nothing.  No output may overlap
+ * an input, another output or the workspace (MLSTM_ERR_ALIAS).
+ */
+size_t mlstm_parallel_bwd_workspace_bytes(int B, int NH, int T, int DV);
+mlstm_status mlstm_parallel_bwd(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                                const float* ipre, const float* fpre, const float* dh,
+                                int B, int NH, int T, int DQK, int DV,
+                                float* dq, float* dk, float* dv, float* dipre, float* dfpre,
+                                void* workspace, size_t workspace_bytes, void* hip_stream);
+
 /* Static, human-readable name of a status code. */
 const char* mlstm_status_string(mlstm_status s);
 

@@ -11,6 +11,8 @@
   ("FLOPs for the mLSTM in a Transformer Backbone"), per token count.
 * ``layer_step_bytes``: algorithmic HBM bytes of one layer decode step (weights,
   state, token in and out).
+* ``flops_parallel_bwd``: the FLOP count of the backward pass over the parallel
+  form, per causal (t, s) pair.
 """
 from __future__ import annotations
 
@@ -120,3 +122,10 @@ def layer_step_bytes(B: int, d: int, NH: int, dqk: int, dv: int) -> int:
     state (C, n, m) read and written once, x read and y written once (bf16)."""
     state = 4 * B * NH * (dqk * dv + dqk + 1)
     return layer_weight_bytes(d, NH, dqk, dv) + 2 * state + 2 * 2 * B * d
+
+
+def flops_parallel_bwd(heads: int, T: int, dqk: int, dv: int) -> int:
+    """FLOPs of the backward pass over the parallel form (Eq. 10) as the library computes it: per
+    causal pair (t, s <= t) the dot products q^_t . k_s (twice), dN~_t . v_s (twice) and the
+    accumulations into N~_t, dq_t, dk_s and dv_s, each 2 FLOP per element: 8 (dqk + dv)."""
+    return heads * (T * (T + 1) // 2) * 8 * (dqk + dv)

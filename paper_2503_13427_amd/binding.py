@@ -44,6 +44,11 @@ lib.mlstm_output_norm.argtypes = [_vp, _vp, _i, _vp, _vp, ctypes.c_float, _i, _i
 lib.mlstm_output_norm.restype = _i
 lib.mlstm_gate_preact.argtypes = [_vp, _i, _vp, _vp, ctypes.c_float, _vp, _i, _i, _i, _i, _vp, _vp, _vp]
 lib.mlstm_gate_preact.restype = _i
+lib.mlstm_parallel_bwd_workspace_bytes.argtypes = [_i, _i, _i, _i]
+lib.mlstm_parallel_bwd_workspace_bytes.restype = ctypes.c_size_t
+lib.mlstm_parallel_bwd.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp,
+                                   ctypes.c_size_t, _vp]
+lib.mlstm_parallel_bwd.restype = _i
 lib.mlstm_status_string.argtypes = [_i]
 lib.mlstm_status_string.restype = ctypes.c_char_p
 lib.mlstm_version.argtypes = []
@@ -152,3 +157,19 @@ def mlstm_gate_preact(x, w_t, bias, cap: float, border, ipre, fpre, stream=None)
         border = border.view(torch.uint8)
     _check(lib.mlstm_gate_preact(_ptr(x), _dtype_code(x), _ptr(w_t), _ptr(bias), float(cap), _ptr(border), B, T, d,
                                  NH, _ptr(ipre), _ptr(fpre), _stream(stream)))
+
+
+def mlstm_parallel_bwd_workspace_bytes(B: int, NH: int, T: int, DV: int) -> int:
+    return int(lib.mlstm_parallel_bwd_workspace_bytes(B, NH, T, DV))
+
+
+def mlstm_parallel_bwd(q, k, v, ipre, fpre, dh, dq, dk, dv, dipre, dfpre, workspace, stream=None) -> None:
+    """Gradients of a loss with respect to q, k, v [B, NH, T, D] (bf16 or fp32) and ipre, fpre
+    [B, NH, T] given dh [B, NH, T, DV] fp32, from the zero initial state; outputs fp32 of the
+    input shapes; workspace: uint8 tensor of mlstm_parallel_bwd_workspace_bytes bytes."""
+    B, NH, T, DQK = q.shape
+    DV = v.shape[3]
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.mlstm_parallel_bwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre), _ptr(dh), B, NH, T,
+                                  DQK, DV, _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dipre), _ptr(dfpre), _ptr(workspace),
+                                  ws_bytes, _stream(stream)))

@@ -28,6 +28,13 @@ constexpr int kGateDMultiple = 128;
 hipError_t launch_gate_preact(const void* x, const void* w_t, const float* bias, float cap, const uint8_t* border,
                               int B, int T, int d, int NH, float* ipre, float* fpre, hipStream_t stream);
 
+// --- backward pass over the parallel form (fp32 VALU) ------------------------
+bool parallel_bwd_supported(int DQK, int DV);
+size_t parallel_bwd_workspace_bytes(int B, int NH, int T, int DV);
+hipError_t launch_parallel_bwd(mlstm_dtype dt, const void* q, const void* k, const void* v, const float* ipre,
+                               const float* fpre, const float* dh, int B, int NH, int T, int DQK, int DV, float* dq,
+                               float* dk, float* dv, float* dipre, float* dfpre, void* workspace, hipStream_t stream);
+
 // --- chunkwise prefill, fp32 VALU kernel (small heads) -----------------------
 struct ChunkArgs {
     const void* q;

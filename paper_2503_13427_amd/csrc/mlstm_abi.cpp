@@ -220,4 +220,48 @@ mlstm_status mlstm_gate_preact(const void* x, mlstm_dtype dt, const void* w_t, c
     return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
 }
 
+size_t mlstm_parallel_bwd_workspace_bytes(int B, int NH, int T, int DV) {
+    if (B <= 0 || NH <= 0 || T < 0 || DV <= 0) return 0;
+    return mlstm::parallel_bwd_workspace_bytes(B, NH, T, DV);
+}
+
+mlstm_status mlstm_parallel_bwd(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,
+                                const float* fpre, const float* dh, int B, int NH, int T, int DQK, int DV, float* dq,
+                                float* dk, float* dv, float* dipre, float* dfpre, void* workspace,
+                                size_t workspace_bytes, void* hip_stream) {
+    if (B <= 0 || NH <= 0 || T < 0 || DQK <= 0 || DV <= 0) return MLSTM_ERR_BAD_SHAPE;
+    int64_t S, nt, nqk, nv;
+    if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &nt) || !mul_ok(nt, DQK, &nqk) || !mul_ok(nt, DV, &nv) ||
+        S * ((static_cast<int64_t>(T) + 15) / 16) > INT32_MAX)
+        return MLSTM_ERR_BAD_SHAPE;
+    if (T != 0) {
+        const void* req[] = {q, k, v, ipre, fpre, dh, dq, dk, dv, dipre, dfpre, workspace};
+        for (const void* p : req)
+            if (!p) return MLSTM_ERR_NULL_PTR;
+    }
+    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (!mlstm::parallel_bwd_supported(DQK, DV)) return MLSTM_ERR_UNSUPPORTED;
+    const size_t ws_need = mlstm::parallel_bwd_workspace_bytes(B, NH, T, DV);
+    if (T != 0 && workspace_bytes < ws_need) return MLSTM_ERR_WORKSPACE;
+    const void* ptrs[] = {q, k, v, ipre, fpre, dh, dq, dk, dv, dipre, dfpre, workspace};
+    for (const void* p : ptrs)
+        if (misaligned(p)) return MLSTM_ERR_MISALIGNED;
+    const size_t eb = elem_bytes(dt);
+    const Range ins[] = {range_of(q, nqk * eb), range_of(k, nqk * eb), range_of(v, nv * eb), range_of(ipre, nt * 4),
+                         range_of(fpre, nt * 4), range_of(dh, nv * 4)};
+    const Range outs[] = {range_of(dq, nqk * 4), range_of(dk, nqk * 4), range_of(dv, nv * 4),
+                          range_of(dipre, nt * 4), range_of(dfpre, nt * 4), range_of(workspace, ws_need)};
+    const size_t nouts = sizeof(outs) / sizeof(outs[0]);
+    for (size_t a = 0; a < nouts; ++a) {
+        for (const Range& r : ins)
+            if (overlap(outs[a], r)) return MLSTM_ERR_ALIAS;
+        for (size_t b = a + 1; b < nouts; ++b)
+            if (overlap(outs[a], outs[b])) return MLSTM_ERR_ALIAS;
+    }
+    if (T == 0) return MLSTM_OK;
+    hipError_t e = mlstm::launch_parallel_bwd(dt, q, k, v, ipre, fpre, dh, B, NH, T, DQK, DV, dq, dk, dv, dipre,
+                                              dfpre, workspace, static_cast<hipStream_t>(hip_stream));
+    return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
 }  // extern "C"

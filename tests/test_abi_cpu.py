@@ -25,7 +25,8 @@ def declared_functions():
 
 def test_header_declares_expected_entry_points():
     assert declared_functions() == sorted(["mlstm_chunkwise_fwd", "mlstm_chunkwise_workspace_bytes", "mlstm_step",
-                                           "mlstm_output_norm", "mlstm_gate_preact", "mlstm_status_string",
+                                           "mlstm_output_norm", "mlstm_gate_preact", "mlstm_parallel_bwd",
+                                           "mlstm_parallel_bwd_workspace_bytes", "mlstm_status_string",
                                            "mlstm_version"])
 
 
@@ -269,3 +270,66 @@ def test_gate_alias(out, inp, off):
     a = gate_args()
     a[out] = a[inp] + off
     assert call_gate(a) == 5
+
+
+# ---- backward validation -------------------------------------------------------------------------
+
+def bwd_args(**over):
+    a = dict(q=fake(0), k=fake(1), v=fake(2), dt=Bd.MLSTM_BF16, ip=fake(3), fp=fake(4), dh=fake(5), B=1, NH=8,
+             T=2048, DQK=256, DV=512, dq=fake(6), dk=fake(7), dv=fake(8), di=fake(9), df=fake(10), ws=fake(11),
+             ws_bytes=1 << 30, stream=None)
+    a.update(over)
+    return a
+
+
+def call_bwd(a):
+    return lib.mlstm_parallel_bwd(a["q"], a["k"], a["v"], a["dt"], a["ip"], a["fp"], a["dh"], a["B"], a["NH"], a["T"],
+                                  a["DQK"], a["DV"], a["dq"], a["dk"], a["dv"], a["di"], a["df"], a["ws"],
+                                  a["ws_bytes"], a["stream"])
+
+
+def test_bwd_workspace_size():
+    # per sequence: five fp32 vectors of T and dN~ [T][DV]
+    assert lib.mlstm_parallel_bwd_workspace_bytes(2, 8, 100, 512) == 2 * 8 * 100 * (5 + 512) * 4
+    assert lib.mlstm_parallel_bwd_workspace_bytes(0, 8, 100, 512) == 0
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "ip", "fp", "dh", "dq", "dk", "dv", "di", "df", "ws"])
+def test_bwd_null_pointer(field):
+    assert call_bwd(bwd_args(**{field: None})) == 1
+
+
+def test_bwd_empty_sequence_is_ok_without_pointers():
+    assert call_bwd(bwd_args(T=0, q=None, k=None, v=None, dh=None, dq=None, ws=None, ws_bytes=0)) == 0
+
+
+@pytest.mark.parametrize("over", [dict(B=0), dict(NH=-1), dict(T=-1), dict(DQK=0), dict(DV=0)])
+def test_bwd_bad_shape(over):
+    assert call_bwd(bwd_args(**over)) == 2
+
+
+@pytest.mark.parametrize("over", [dict(dt=3), dict(DQK=24), dict(DV=520), dict(DQK=272), dict(DV=1024)])
+def test_bwd_unsupported(over):
+    assert call_bwd(bwd_args(**over)) == 3
+
+
+def test_bwd_workspace_too_small():
+    need = lib.mlstm_parallel_bwd_workspace_bytes(1, 8, 2048, 512)
+    assert call_bwd(bwd_args(ws_bytes=need - 1)) == 6
+    # enough workspace passes that check and stops at the next one (no call here may launch)
+    assert call_bwd(bwd_args(ws_bytes=need, q=fake(0, 4))) == 4
+
+
+@pytest.mark.parametrize("field", ["q", "dh", "dq", "df", "ws"])
+def test_bwd_misaligned(field):
+    a = bwd_args()
+    a[field] += 4
+    assert call_bwd(a) == 4
+
+
+@pytest.mark.parametrize("out,other,off", [("dq", "q", 0), ("dv", "dh", 4096), ("dk", "dq", 16), ("df", "di", 0),
+                                           ("ws", "dv", 64), ("di", "ip", 0)])
+def test_bwd_alias(out, other, off):
+    a = bwd_args()
+    a[out] = a[other] + off
+    assert call_bwd(a) == 5

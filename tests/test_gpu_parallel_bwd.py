@@ -1,0 +1,99 @@
+"""mlstm_parallel_bwd (the training-mode backward pass over the parallel form) against the fp64
+gradient oracle: ``recurrent_grad`` (autograd over the step-by-step cell) for small shapes and
+``parallel_grad`` (its closed form, pinned to it) for the xLSTM-7B head shape.
+
+Bars, per (batch, head) slice of each gradient: max relative error <= 1e-4 for fp32 q/k/v,
+<= 2e-2 for bf16 q/k/v (the oracle upcasts the same bf16 values).  No bar is stated for gradients;
+1e-4 comes from the arithmetic: df~ is a reverse cumulative sum of P_t - di~_t, each an fp32 sum
+over up to T pair terms, and the two nearly cancel, so fp32 rounding of order T 2^-24 on each is
+amplified by that cancellation (1e-5 is reached at T = 64 with short memory).  Covers ragged T (not a
+multiple of the 16-token tile), one token, the floor branch and short memory."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import mlstm_grad as G
+from paper_2503_13427_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
+from tests.helpers import TOL_BF16, rel_err
+
+TOL_BWD_F32 = 1e-4
+
+pytestmark = pytest.mark.gpu
+
+
+def _mb():
+    from paper_2503_13427_amd import binding
+    return binding
+
+
+def draw(seed, B, NH, T, DQK, DV, dtype, i_mu=0.0, f_mu=3.0, f_sd=1.0):
+    rng = np.random.default_rng(seed)
+    S = B * NH
+    q = rng.standard_normal((S, T, DQK)).astype(np.float32)
+    k = (rng.standard_normal((S, T, DQK)) / np.sqrt(DQK) * 4).astype(np.float32)
+    v = rng.standard_normal((S, T, DV)).astype(np.float32)
+    if dtype == "bf16":
+        q, k, v = (bf16_bits_to_f32(f32_to_bf16_bits(x)) for x in (q, k, v))
+    ip = rng.normal(i_mu, 1.0, (S, T)).astype(np.float32)
+    fp = rng.normal(f_mu, f_sd, (S, T)).astype(np.float32)
+    dh = rng.standard_normal((S, T, DV)).astype(np.float32)
+    return q, k, v, ip, fp, dh
+
+
+def run(B, NH, q, k, v, ip, fp, dh, dtype):
+    S, T, DQK = q.shape
+    DV = v.shape[2]
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dev = lambda x, *shape: torch.from_numpy(np.ascontiguousarray(x)).reshape(*shape).cuda()
+    qd, kd = dev(q, B, NH, T, DQK).to(tdt), dev(k, B, NH, T, DQK).to(tdt)
+    vd = dev(v, B, NH, T, DV).to(tdt)
+    ipd, fpd, dhd = dev(ip, B, NH, T), dev(fp, B, NH, T), dev(dh, B, NH, T, DV)
+    outs = [torch.full_like(qd, 9.0, dtype=torch.float32), torch.full_like(kd, 9.0, dtype=torch.float32),
+            torch.full_like(vd, 9.0, dtype=torch.float32), torch.full_like(ipd, 9.0), torch.full_like(fpd, 9.0)]
+    ws = torch.empty(_mb().mlstm_parallel_bwd_workspace_bytes(B, NH, T, DV), dtype=torch.uint8, device="cuda")
+    _mb().mlstm_parallel_bwd(qd, kd, vd, ipd, fpd, dhd, *outs, ws)
+    torch.cuda.synchronize()
+    return [o.cpu().numpy().astype(np.float64).reshape(S, T, -1) for o in outs]
+
+
+def compare(got, ref, tol, label):
+    names = ["dq", "dk", "dv", "di", "df"]
+    errs = []
+    for n, g, r in zip(names, got, ref):
+        S, T = r.shape[0], r.shape[1]
+        e = rel_err(g.reshape(S, -1), r.reshape(S, -1), 1)
+        errs.append(e)
+        assert np.isfinite(g).all(), n
+    print(label + " " + " ".join(f"{n} {e:.2e}" for n, e in zip(names, errs)))
+    assert max(errs) <= tol, dict(zip(names, errs))
+
+
+SMALL = [
+    # (B, NH, T, DQK, DV, dist)
+    (1, 2, 40, 16, 16, "standard"),       # ragged: 40 = 2 x 16 + 8
+    (2, 1, 64, 32, 48, "short_memory"),
+    (1, 1, 17, 16, 32, "floor_active"),
+    (1, 1, 1, 16, 16, "standard"),        # one token
+    (1, 2, 100, 64, 128, "standard"),
+]
+DIST = {"standard": {}, "short_memory": dict(f_mu=-1.0, f_sd=2.0), "floor_active": dict(i_mu=-6.0)}
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: f"B{c[0]}NH{c[1]}T{c[2]}d{c[3]}x{c[4]}-{c[5]}")
+def test_parallel_bwd_fp32_matches_oracle(case):
+    B, NH, T, DQK, DV, dist = case
+    q, k, v, ip, fp, dh = draw(300 + SMALL.index(case), B, NH, T, DQK, DV, "f32", **DIST[dist])
+    got = run(B, NH, q, k, v, ip, fp, dh, "f32")
+    ref = G.recurrent_grad(q, k, v, ip, fp, dh)
+    ref = [r.reshape(r.shape[0], r.shape[1], -1) for r in ref]
+    compare(got, ref, TOL_BWD_F32, str(case))
+
+
+@pytest.mark.parametrize("T", [128, 300])
+def test_parallel_bwd_bf16_xlstm_head(T):
+    B, NH, DQK, DV = 1, 2, 256, 512
+    q, k, v, ip, fp, dh = draw(310 + T, B, NH, T, DQK, DV, "bf16")
+    got = run(B, NH, q, k, v, ip, fp, dh, "bf16")
+    ref = G.parallel_grad(q, k, v, ip, fp, dh)
+    ref = [r.reshape(r.shape[0], r.shape[1], -1) for r in ref]
+    compare(got, ref, TOL_BF16, f"7B head T{T}")

@@ -13,14 +13,16 @@
 //   df~_j = sigmoid(-f~_j) sum_{t >= j} (P_t - di~_t).
 //
 // Four launches per call:
-//   gate pass    one thread per sequence: b, x, M, m into the workspace (a serial scan);
+//   gate pass    one wave per sequence: b, x, M, m into the workspace (wave scans);
 //   row pass     one workgroup per 16 rows t: a sweep over s <= t rebuilds N~ and D~ (so h),
 //                gives dN~, dD~ and P (dN~ into the workspace); a second sweep accumulates dq;
 //   column pass  one workgroup per 16 columns s: a sweep over t >= s accumulates dk, dv, di~;
-//   forget pass  one thread per sequence: the reverse sum for df~.
+//   forget pass  one wave per sequence: the reverse sum for df~.
 // Tiles of 16 x 16 (t, s) pairs: one thread per pair for the dot products, then each thread of a
 // row (or column) owns every 16th of its DV (or DQK) outputs.  LDS rows are padded by one float
 // so that a row read across threads spreads over the banks.  Work is O(T^2 (DQK + DV)).
+#include <utility>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -45,15 +47,36 @@ struct BwdArgs {
     float* dv;
     float* dipre;
     float* dfpre;
-    float* ws;          // per sequence: x, M, m, dD, P [T] then dN [T][DV]
+    float* ws;          // per sequence: x, M, m, dD, P [T], then from dn_off(T) dN [T][DV]
 };
 
-__host__ __device__ inline int64_t ws_floats(int T, int DV) { return static_cast<int64_t>(T) * (5 + DV); }
+// dN starts on a 16-byte boundary (the passes stage it with 16-byte loads); DV is a multiple of 16,
+// so every sequence's block is a multiple of four floats too
+__host__ __device__ inline int64_t dn_off(int T) { return (5 * static_cast<int64_t>(T) + 3) & ~int64_t(3); }
+__host__ __device__ inline int64_t ws_floats(int T, int DV) { return dn_off(T) + static_cast<int64_t>(T) * DV; }
 
 // ---- gate pass ---------------------------------------------------------------------------------
+// Inclusive scans over a wave (shift-and-combine, 6 steps).
+__device__ __forceinline__ float wave_scan_sum(float x, int lane) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const float y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+__device__ __forceinline__ float wave_scan_max(float x, int lane) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const float y = __shfl_up(x, o, 64);
+        if (lane >= o) x = fmaxf(x, y);
+    }
+    return x;
+}
+// one wave per sequence, 64 tokens per step: b, x = i~ - b, M = max(0, prefix max of x), m = b + M
 __global__ void bwd_gate_kernel(BwdArgs A, int S) {
-    const int s = blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= S) return;
+    const int s = blockIdx.x;
+    const int lane = threadIdx.x;
     const int T = A.T;
     float* w = A.ws + s * ws_floats(T, A.DV);
     float* x = w;
@@ -61,14 +84,20 @@ __global__ void bwd_gate_kernel(BwdArgs A, int S) {
     float* m = w + 2 * T;
     const float* ib = A.ipre + static_cast<int64_t>(s) * T;
     const float* fb = A.fpre + static_cast<int64_t>(s) * T;
-    float b = 0.0f, p = 0.0f;   // running prefix sum of logsig f~ and max(0, prefix max of x)
-    for (int t = 0; t < T; ++t) {
-        b += logsigmoid(fb[t]);
-        const float xv = ib[t] - b;
-        p = fmaxf(p, xv);
-        x[t] = xv;
-        M[t] = p;
-        m[t] = b + p;
+    float b_carry = 0.0f, p_carry = 0.0f;
+    for (int t0 = 0; t0 < T; t0 += 64) {
+        const int t = t0 + lane;
+        const bool ok = t < T;
+        const float b = b_carry + wave_scan_sum(ok ? logsigmoid(fb[t]) : 0.0f, lane);
+        const float xv = ok ? ib[t] - b : -INFINITY;
+        const float p = fmaxf(p_carry, wave_scan_max(xv, lane));
+        if (ok) {
+            x[t] = xv;
+            M[t] = p;
+            m[t] = b + p;
+        }
+        b_carry = __shfl(b, 63, 64);
+        p_carry = __shfl(p, 63, 64);
     }
 }
 
@@ -100,7 +129,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_kernel(BwdArgs A) {
     const float* mw = wsq + 2 * T;
     float* dDw = const_cast<float*>(wsq) + 3 * T;
     float* Pw = const_cast<float*>(wsq) + 4 * T;
-    float* dNw = const_cast<float*>(wsq) + 5 * T;
+    float* dNw = const_cast<float*>(wsq) + dn_off(T);
     const float qscale = rsqrtf(static_cast<float>(DQK));
 
     for (int e = tid; e < kBT * DQK; e += kBwdThreads) {
@@ -256,7 +285,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_kernel(BwdArgs A) {
     const float* xw = wsq;
     const float* Mw = wsq + T;
     const float* dDw = wsq + 3 * T;
-    const float* dNw = wsq + 5 * T;
+    const float* dNw = wsq + dn_off(T);
     const float qscale = rsqrtf(static_cast<float>(DQK));
 
     for (int e = tid; e < kBT * DQK; e += kBwdThreads) {
@@ -328,22 +357,408 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_kernel(BwdArgs A) {
     }
 }
 
+// ---- MFMA row and column passes (DQK and DV multiples of 64) ----------------------------------
+//
+// The same passes with the tile products on fp32 MFMA 16x16x4 (lane l: A[l % 16][l / 16],
+// B[l / 16][l % 16], D[4 (l / 16) + j][l % 16]).  Per 16 x 16 tile of (t, s) pairs:
+//   - the logits S = Q^ K^T (or U = dN~ V^T) are split over the four waves along the contraction
+//     and their partial tiles summed through LDS;
+//   - one thread per pair applies the gates (F~, the causal mask) and writes the operand tile;
+//   - the accumulating products (N~ += A~ V, dq += W K; dk += W^T Q^, dv += A~^T dN~) give each
+//     wave a quarter of the output columns, one 16 x 16 accumulator per 16 columns.
+// LDS rows are padded to a pitch of 4 (mod 32) floats.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+constexpr int kMaxNT = kMaxDV / 64;     // 16-column output tiles per wave, at most (DV = 512)
+constexpr int kTP = kBT + 4;            // pitch of a 16 x 16 operand tile
+
+__device__ __forceinline__ f32x4_t mfma4(float a, float b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Partial logits over this wave's quarter of a contraction of length n: rows of X (pitch xp) against
+// rows of Y (pitch yp), both 16 x n in LDS; returns the 16 x 16 partial in D layout.
+__device__ __forceinline__ f32x4_t partial_logits(const float* X, int xp, const float* Y, int yp, int n, int wave,
+                                                  int l16, int g) {
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int q = n / 4;
+    for (int k = wave * q; k < (wave + 1) * q; k += 4) acc = mfma4(X[l16 * xp + k + g], Y[l16 * yp + k + g], acc);
+    return acc;
+}
+
+// 16 rows of n values (n a multiple of 64) from global memory into LDS as fp32, rows at or beyond
+// nrows_total as zeros: 16-byte loads, every load of the thread issued before the first store.
+template <typename TIn> struct Vec16;
+template <> struct Vec16<float> {
+    static constexpr int N = 4;
+    typedef float4 type;
+    static __device__ __forceinline__ void widen(const type& v, float (&o)[4]) { o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w; }
+};
+template <> struct Vec16<bf16_t> {
+    static constexpr int N = 8;
+    typedef uint4 type;
+    static __device__ __forceinline__ void widen(const type& v, float (&o)[8]) {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            o[2 * i] = __uint_as_float(w[i] << 16);
+            o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
+};
+template <typename TIn>
+__device__ __forceinline__ void stage_rows(float* dst, int pitch, const TIn* src, int r0, int nrows_total, int n,
+                                           float scale, int tid) {
+    typedef Vec16<TIn> V;
+    constexpr int kMaxPer = kBT * kMaxDV / V::N / kBwdThreads;   // vectors per thread, at most
+    const int nvec = kBT * n / V::N;
+    typename V::type buf[kMaxPer];
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+        const int idx = tid + kBwdThreads * i;
+        const int r = (idx * V::N) / n;
+        if (idx < nvec && r0 + r < nrows_total)
+            buf[i] = reinterpret_cast<const typename V::type*>(src + static_cast<int64_t>(r0) * n)[idx];
+    }
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+        const int idx = tid + kBwdThreads * i;
+        if (idx < nvec) {
+            const int e = idx * V::N, r = e / n, d = e % n;
+            float o[V::N];
+            if (r0 + r < nrows_total) {
+                V::widen(buf[i], o);
+            } else {
+#pragma unroll
+                for (int j = 0; j < V::N; ++j) o[j] = 0.0f;
+            }
+#pragma unroll
+            for (int j = 0; j < V::N; ++j) dst[r * pitch + d + j] = o[j] * scale;
+        }
+    }
+}
+// the same for fp32 rows of the workspace
+__device__ __forceinline__ void stage_rows_f32(float* dst, int pitch, const float* src, int r0, int nrows_total, int n,
+                                               int tid) {
+    stage_rows<float>(dst, pitch, src, r0, nrows_total, n, 1.0f, tid);
+}
+
+template <typename TIn>
+__global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
+    extern __shared__ float sm[];
+    const int DQK = A.DQK, DV = A.DV, T = A.T;
+    const int KP = DQK + 4, VP = DV + 4;
+    float* Qs = sm;                      // [kBT][KP]
+    float* Ks = Qs + kBT * KP;           // [kBT][KP]
+    float* Vs = Ks + kBT * KP;           // [kBT][VP]
+    float* dN = Vs + kBT * VP;           // [kBT][VP]
+    float* Pr = dN + kBT * VP;           // [4 waves][kBT][kBT] partial logits
+    float* Op = Pr + 4 * kBT * kBT;      // [kBT][kTP] operand tile (A~ or W), rows t
+    float* red = Op + kBT * kTP;         // [4][kBT][kBT] row partial sums
+    float* rowv = red + 4 * kBT * kBT;   // [kBT][4] per row: M, m, dD
+    const int ntile = (T + kBT - 1) / kBT;
+    const int64_t seq = blockIdx.x / ntile;
+    const int t0 = (blockIdx.x % ntile) * kBT;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, g = lane >> 4;
+    const int pr = tid / kBT, pc = tid % kBT;
+    const TIn* q = static_cast<const TIn*>(A.q) + seq * T * DQK;
+    const TIn* k = static_cast<const TIn*>(A.k) + seq * T * DQK;
+    const TIn* v = static_cast<const TIn*>(A.v) + seq * T * DV;
+    float* wsq = A.ws + seq * ws_floats(T, DV);
+    const float* xw = wsq;
+    const float* Mw = wsq + T;
+    const float* mw = wsq + 2 * T;
+    float* dDw = wsq + 3 * T;
+    float* Pw = wsq + 4 * T;
+    float* dNw = wsq + dn_off(T);
+    const float qscale = rsqrtf(static_cast<float>(DQK));
+    const int nvt = DV / 64, nkt = DQK / 64;   // 16-column output tiles per wave
+    const int vc0 = wave * (DV / 4), kc0 = wave * (DQK / 4);
+
+    stage_rows<TIn>(Qs, KP, q, t0, T, DQK, qscale, tid);
+    if (tid < kBT) {
+        const int t = t0 + tid;
+        rowv[4 * tid + 0] = t < T ? Mw[t] : 0.0f;
+        rowv[4 * tid + 1] = t < T ? mw[t] : 0.0f;
+    }
+    f32x4_t accN[kMaxNT];
+#pragma unroll
+    for (int c = 0; c < kMaxNT; ++c) accN[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float accD = 0.0f;   // this thread's (t, s) column of A~, summed over s tiles
+    const int t_pair = t0 + pr;
+    const int last_tile = t0 / kBT;
+
+    for (int st = 0; st <= last_tile; ++st) {
+        const int s0 = st * kBT;
+        __syncthreads();
+        stage_rows<TIn>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
+        stage_rows<TIn>(Vs, VP, v, s0, T, DV, 1.0f, tid);
+        __syncthreads();
+        const f32x4_t part = partial_logits(Qs, KP, Ks, KP, DQK, wave, l16, g);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) Pr[(wave * kBT + 4 * g + j) * kBT + l16] = part[j];
+        __syncthreads();
+        {
+            const int s = s0 + pc;
+            float a = 0.0f;
+            if (s <= t_pair && t_pair < T) {
+                const float sv = Pr[pr * kBT + pc] + Pr[(kBT + pr) * kBT + pc] + Pr[(2 * kBT + pr) * kBT + pc] +
+                                 Pr[(3 * kBT + pr) * kBT + pc];
+                a = expf(xw[s] - rowv[4 * pr]) * sv;
+            }
+            Op[pr * kTP + pc] = a;
+            accD += a;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const float a = Op[l16 * kTP + 4 * kk + g];
+#pragma unroll
+            for (int c = 0; c < kMaxNT; ++c)
+                if (c < nvt) accN[c] = mfma4(a, Vs[(4 * kk + g) * VP + vc0 + 16 * c + l16], accN[c]);
+        }
+    }
+    // D~ per row, then dN~, dD~ and P
+    red[pr * kBT + pc] = accD;
+    __syncthreads();
+    if (tid < kBT) {
+        float d = 0.0f;
+        for (int j = 0; j < kBT; ++j) d += red[tid * kBT + j];
+        rowv[4 * tid + 3] = d;
+    }
+    __syncthreads();
+    float part_hh[4] = {0.f, 0.f, 0.f, 0.f}, part_nn[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int r = 4 * g + j, t = t0 + r;
+        const float Dt = rowv[4 * r + 3];
+        const float den = fmaxf(fabsf(Dt), expf(-rowv[4 * r + 1]));
+#pragma unroll
+        for (int c = 0; c < kMaxNT; ++c) {
+            if (c < nvt) {
+                const int col = vc0 + 16 * c + l16;
+                const float gh = t < T ? A.dh[(seq * T + t) * DV + col] : 0.0f;
+                const float nv = accN[c][j];
+                const float dn = gh / den;
+                part_hh[j] += gh * (nv / den);
+                part_nn[j] += dn * nv;
+                dN[r * VP + col] = dn;
+                if (t < T) dNw[static_cast<int64_t>(t) * DV + col] = dn;
+            }
+        }
+    }
+    // row sums over the 16 lanes of a row group and the four waves
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        red[(wave * kBT + 4 * g + j) * kBT + l16] = part_hh[j];
+    }
+    __syncthreads();
+    if (tid < kBT) {
+        float sdh = 0.0f;
+        for (int w = 0; w < 4; ++w)
+            for (int j = 0; j < kBT; ++j) sdh += red[(w * kBT + tid) * kBT + j];
+        const float Dt = rowv[4 * tid + 3];
+        const float fl = expf(-rowv[4 * tid + 1]);
+        const float den = fmaxf(fabsf(Dt), fl);
+        rowv[4 * tid + 2] = (fabsf(Dt) > fl) ? -sdh / den * (Dt > 0.0f ? 1.0f : -1.0f) : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) red[(wave * kBT + 4 * g + j) * kBT + l16] = part_nn[j];
+    __syncthreads();
+    if (tid < kBT && t0 + tid < T) {
+        float sdn = 0.0f;
+        for (int w = 0; w < 4; ++w)
+            for (int j = 0; j < kBT; ++j) sdn += red[(w * kBT + tid) * kBT + j];
+        const float dD = rowv[4 * tid + 2];
+        dDw[t0 + tid] = dD;
+        Pw[t0 + tid] = sdn + dD * rowv[4 * tid + 3];
+    }
+
+    // sweep 2: dq
+    f32x4_t accQ[kMaxDQK / 64];
+#pragma unroll
+    for (int c = 0; c < kMaxDQK / 64; ++c) accQ[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int st = 0; st <= last_tile; ++st) {
+        const int s0 = st * kBT;
+        __syncthreads();
+        stage_rows<TIn>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
+        stage_rows<TIn>(Vs, VP, v, s0, T, DV, 1.0f, tid);
+        __syncthreads();
+        const f32x4_t part = partial_logits(dN, VP, Vs, VP, DV, wave, l16, g);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) Pr[(wave * kBT + 4 * g + j) * kBT + l16] = part[j];
+        __syncthreads();
+        {
+            const int s = s0 + pc;
+            float w = 0.0f;
+            if (s <= t_pair && t_pair < T) {
+                const float u = Pr[pr * kBT + pc] + Pr[(kBT + pr) * kBT + pc] + Pr[(2 * kBT + pr) * kBT + pc] +
+                                Pr[(3 * kBT + pr) * kBT + pc];
+                w = (u + rowv[4 * pr + 2]) * expf(xw[s] - rowv[4 * pr]);
+            }
+            Op[pr * kTP + pc] = w;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const float a = Op[l16 * kTP + 4 * kk + g];
+#pragma unroll
+            for (int c = 0; c < kMaxDQK / 64; ++c)
+                if (c < nkt) accQ[c] = mfma4(a, Ks[(4 * kk + g) * KP + kc0 + 16 * c + l16], accQ[c]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int t = t0 + 4 * g + j;
+        if (t < T) {
+#pragma unroll
+            for (int c = 0; c < kMaxDQK / 64; ++c)
+                if (c < nkt) A.dq[(seq * T + t) * DQK + kc0 + 16 * c + l16] = accQ[c][j] * qscale;
+        }
+    }
+}
+
+template <typename TIn>
+__global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
+    extern __shared__ float sm[];
+    const int DQK = A.DQK, DV = A.DV, T = A.T;
+    const int KP = DQK + 4, VP = DV + 4;
+    float* Ks = sm;                      // [kBT][KP] this tile's k
+    float* Vs = Ks + kBT * KP;           // [kBT][VP] this tile's v
+    float* Qs = Vs + kBT * VP;           // [kBT][KP] a tile of q^
+    float* dN = Qs + kBT * KP;           // [kBT][VP] a tile of dN~
+    float* Ps = dN + kBT * VP;           // [4][kBT][kBT] partial S
+    float* Pu = Ps + 4 * kBT * kBT;      // [4][kBT][kBT] partial U
+    float* Wt = Pu + 4 * kBT * kBT;      // [kBT][kTP] W^T (rows s)
+    float* At = Wt + kBT * kTP;          // [kBT][kTP] A~^T (rows s)
+    float* red = At + kBT * kTP;         // [kBT][kBT]
+    float* rowv = red + kBT * kBT;       // [kBT][2] per row t of the t tile: M, dD
+    const int ntile = (T + kBT - 1) / kBT;
+    const int64_t seq = blockIdx.x / ntile;
+    const int s0 = (blockIdx.x % ntile) * kBT;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, g = lane >> 4;
+    const int pr = tid / kBT, pc = tid % kBT;   // pair (t row pr, s column pc)
+    const TIn* q = static_cast<const TIn*>(A.q) + seq * T * DQK;
+    const TIn* k = static_cast<const TIn*>(A.k) + seq * T * DQK;
+    const TIn* v = static_cast<const TIn*>(A.v) + seq * T * DV;
+    const float* wsq = A.ws + seq * ws_floats(T, DV);
+    const float* xw = wsq;
+    const float* Mw = wsq + T;
+    const float* dDw = wsq + 3 * T;
+    const float* dNw = wsq + dn_off(T);
+    const float qscale = rsqrtf(static_cast<float>(DQK));
+    const int nvt = DV / 64, nkt = DQK / 64;
+    const int vc0 = wave * (DV / 4), kc0 = wave * (DQK / 4);
+
+    stage_rows<TIn>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
+    stage_rows<TIn>(Vs, VP, v, s0, T, DV, 1.0f, tid);
+    f32x4_t accK[kMaxDQK / 64], accV[kMaxNT];
+#pragma unroll
+    for (int c = 0; c < kMaxDQK / 64; ++c) accK[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < kMaxNT; ++c) accV[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float accI = 0.0f;   // this thread's (t, s) entry of G, summed over t tiles
+    for (int tt = s0 / kBT; tt < ntile; ++tt) {
+        const int t0 = tt * kBT;
+        __syncthreads();
+        stage_rows<TIn>(Qs, KP, q, t0, T, DQK, qscale, tid);
+        stage_rows_f32(dN, VP, dNw, t0, T, DV, tid);
+        if (tid < kBT) {
+            const int t = t0 + tid;
+            rowv[2 * tid + 0] = t < T ? Mw[t] : 0.0f;
+            rowv[2 * tid + 1] = t < T ? dDw[t] : 0.0f;
+        }
+        __syncthreads();
+        const f32x4_t ps = partial_logits(Qs, KP, Ks, KP, DQK, wave, l16, g);   // S[t][s]
+        const f32x4_t pu = partial_logits(dN, VP, Vs, VP, DV, wave, l16, g);    // U[t][s]
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            Ps[(wave * kBT + 4 * g + j) * kBT + l16] = ps[j];
+            Pu[(wave * kBT + 4 * g + j) * kBT + l16] = pu[j];
+        }
+        __syncthreads();
+        {
+            const int t = t0 + pr, s = s0 + pc;
+            float w = 0.0f, a = 0.0f;
+            if (s <= t && t < T && s < T) {
+                float sv = 0.0f, u = 0.0f;
+#pragma unroll
+                for (int w4 = 0; w4 < 4; ++w4) {
+                    sv += Ps[(w4 * kBT + pr) * kBT + pc];
+                    u += Pu[(w4 * kBT + pr) * kBT + pc];
+                }
+                const float F = expf(xw[s] - rowv[2 * pr]);
+                w = (u + rowv[2 * pr + 1]) * F;
+                a = F * sv;
+                accI += w * sv;
+            }
+            Wt[pc * kTP + pr] = w;
+            At[pc * kTP + pr] = a;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const float aw = Wt[l16 * kTP + 4 * kk + g];
+            const float aa = At[l16 * kTP + 4 * kk + g];
+#pragma unroll
+            for (int c = 0; c < kMaxDQK / 64; ++c)
+                if (c < nkt) accK[c] = mfma4(aw, Qs[(4 * kk + g) * KP + kc0 + 16 * c + l16], accK[c]);
+#pragma unroll
+            for (int c = 0; c < kMaxNT; ++c)
+                if (c < nvt) accV[c] = mfma4(aa, dN[(4 * kk + g) * VP + vc0 + 16 * c + l16], accV[c]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int s = s0 + 4 * g + j;
+        if (s < T) {
+#pragma unroll
+            for (int c = 0; c < kMaxDQK / 64; ++c)
+                if (c < nkt) A.dk[(seq * T + s) * DQK + kc0 + 16 * c + l16] = accK[c][j];
+#pragma unroll
+            for (int c = 0; c < kMaxNT; ++c)
+                if (c < nvt) A.dv[(seq * T + s) * DV + vc0 + 16 * c + l16] = accV[c][j];
+        }
+    }
+    red[pr * kBT + pc] = accI;
+    __syncthreads();
+    if (tid < kBT && s0 + tid < T) {
+        float d = 0.0f;
+        for (int r = 0; r < kBT; ++r) d += red[r * kBT + tid];
+        A.dipre[seq * T + s0 + tid] = d;
+    }
+}
+
 // ---- forget pass -------------------------------------------------------------------------------
+// one wave per sequence, from the last token backwards, 64 tokens per step (lane 0 the latest)
 __global__ void bwd_forget_kernel(BwdArgs A, int S) {
-    const int s = blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= S) return;
+    const int s = blockIdx.x;
+    const int lane = threadIdx.x;
     const int T = A.T;
     const float* Pw = A.ws + s * ws_floats(T, A.DV) + 4 * T;
     const float* di = A.dipre + static_cast<int64_t>(s) * T;
     const float* fb = A.fpre + static_cast<int64_t>(s) * T;
     float* df = A.dfpre + static_cast<int64_t>(s) * T;
-    float acc = 0.0f;
-    for (int j = T - 1; j >= 0; --j) {
-        acc += Pw[j] - di[j];
-        df[j] = acc / (1.0f + expf(fb[j]));   // sigmoid(-f~)
+    float carry = 0.0f;
+    for (int e0 = T - 1; e0 >= 0; e0 -= 64) {
+        const int j = e0 - lane;
+        const bool ok = j >= 0;
+        const float acc = carry + wave_scan_sum(ok ? Pw[j] - di[j] : 0.0f, lane);
+        if (ok) df[j] = acc / (1.0f + expf(fb[j]));   // sigmoid(-f~)
+        carry = __shfl(acc, 63, 64);
     }
 }
 
+size_t row_mfma_lds(int DQK, int DV) {
+    return sizeof(float) * (2 * kBT * (DQK + 4) + 2 * kBT * (DV + 4) + 4 * kBT * kBT + kBT * kTP + 4 * kBT * kBT +
+                            4 * kBT);
+}
+size_t col_mfma_lds(int DQK, int DV) {
+    return sizeof(float) * (2 * kBT * (DQK + 4) + 2 * kBT * (DV + 4) + 8 * kBT * kBT + 2 * kBT * kTP + kBT * kBT +
+                            2 * kBT);
+}
 size_t row_lds(int DQK, int DV) {
     return sizeof(float) * (2 * kBT * (DQK + 1) + 2 * kBT * (DV + 1) + 2 * kBT * kBT + 4 * kBT);
 }
@@ -353,23 +768,33 @@ size_t col_lds(int DQK, int DV) {
 
 template <typename TIn>
 hipError_t launch_typed(const BwdArgs& a, int S, hipStream_t stream) {
-    const size_t lr = row_lds(a.DQK, a.DV), lc = col_lds(a.DQK, a.DV);
     static bool attr = false;
     if (!attr) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_row_kernel<TIn>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(row_lds(kMaxDQK, kMaxDV)));
-        if (e != hipSuccess) return e;
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_col_kernel<TIn>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(col_lds(kMaxDQK, kMaxDV)));
-        if (e != hipSuccess) return e;
+        const std::pair<const void*, size_t> kernels[] = {
+            {reinterpret_cast<const void*>(bwd_row_kernel<TIn>), row_lds(kMaxDQK, kMaxDV)},
+            {reinterpret_cast<const void*>(bwd_col_kernel<TIn>), col_lds(kMaxDQK, kMaxDV)},
+            {reinterpret_cast<const void*>(bwd_row_mfma_kernel<TIn>), row_mfma_lds(kMaxDQK, kMaxDV)},
+            {reinterpret_cast<const void*>(bwd_col_mfma_kernel<TIn>), col_mfma_lds(kMaxDQK, kMaxDV)}};
+        for (const auto& kl : kernels) {
+            hipError_t e = hipFuncSetAttribute(kl.first, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               static_cast<int>(kl.second));
+            if (e != hipSuccess) return e;
+        }
         attr = true;
     }
     const int ntile = (a.T + kBT - 1) / kBT;
     const dim3 tiles(static_cast<unsigned>(static_cast<int64_t>(S) * ntile));
-    const dim3 seqs(static_cast<unsigned>((S + 63) / 64));
+    const dim3 seqs(static_cast<unsigned>(S));   // the scans: one wave per sequence
+    // the MFMA passes need each wave to own whole 16-column tiles of DQK and DV
+    const bool mfma = (a.DQK % 64 == 0) && (a.DV % 64 == 0);
     hipLaunchKernelGGL(bwd_gate_kernel, seqs, dim3(64), 0, stream, a, S);
-    hipLaunchKernelGGL(bwd_row_kernel<TIn>, tiles, dim3(kBwdThreads), lr, stream, a);
-    hipLaunchKernelGGL(bwd_col_kernel<TIn>, tiles, dim3(kBwdThreads), lc, stream, a);
+    if (mfma) {
+        hipLaunchKernelGGL(bwd_row_mfma_kernel<TIn>, tiles, dim3(kBwdThreads), row_mfma_lds(a.DQK, a.DV), stream, a);
+        hipLaunchKernelGGL(bwd_col_mfma_kernel<TIn>, tiles, dim3(kBwdThreads), col_mfma_lds(a.DQK, a.DV), stream, a);
+    } else {
+        hipLaunchKernelGGL(bwd_row_kernel<TIn>, tiles, dim3(kBwdThreads), row_lds(a.DQK, a.DV), stream, a);
+        hipLaunchKernelGGL(bwd_col_kernel<TIn>, tiles, dim3(kBwdThreads), col_lds(a.DQK, a.DV), stream, a);
+    }
     hipLaunchKernelGGL(bwd_forget_kernel, seqs, dim3(64), 0, stream, a, S);
     return hipGetLastError();
 }

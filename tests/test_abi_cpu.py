@@ -289,8 +289,9 @@ def call_bwd(a):
 
 
 def test_bwd_workspace_size():
-    # per sequence: five fp32 vectors of T and dN~ [T][DV]
-    assert lib.mlstm_parallel_bwd_workspace_bytes(2, 8, 100, 512) == 2 * 8 * 100 * (5 + 512) * 4
+    # per sequence: five fp32 vectors of T (rounded up to four floats) and dN~ [T][DV]
+    assert lib.mlstm_parallel_bwd_workspace_bytes(2, 8, 100, 512) == 2 * 8 * (500 + 100 * 512) * 4
+    assert lib.mlstm_parallel_bwd_workspace_bytes(1, 1, 3, 16) == (16 + 3 * 16) * 4
     assert lib.mlstm_parallel_bwd_workspace_bytes(0, 8, 100, 512) == 0
 
 

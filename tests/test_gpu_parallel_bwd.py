@@ -7,7 +7,8 @@ Bars, per (batch, head) slice of each gradient: max relative error <= 1e-4 for f
 1e-4 comes from the arithmetic: df~ is a reverse cumulative sum of P_t - di~_t, each an fp32 sum
 over up to T pair terms, and the two nearly cancel, so fp32 rounding of order T 2^-24 on each is
 amplified by that cancellation (1e-5 is reached at T = 64 with short memory).  Covers ragged T (not a
-multiple of the 16-token tile), one token, the floor branch and short memory."""
+multiple of the 16-token tile), one token, the floor branch and short memory, on both the VALU
+passes (DQK or DV not a multiple of 64) and the MFMA passes."""
 import numpy as np
 import pytest
 import torch
@@ -74,7 +75,9 @@ SMALL = [
     (2, 1, 64, 32, 48, "short_memory"),
     (1, 1, 17, 16, 32, "floor_active"),
     (1, 1, 1, 16, 16, "standard"),        # one token
-    (1, 2, 100, 64, 128, "standard"),
+    (1, 2, 100, 64, 128, "standard"),     # DQK, DV multiples of 64: the MFMA passes
+    (2, 1, 77, 64, 64, "short_memory"),   # MFMA passes, ragged T
+    (1, 1, 50, 128, 192, "floor_active"), # MFMA passes, three 16-column tiles per wave
 ]
 DIST = {"standard": {}, "short_memory": dict(f_mu=-1.0, f_sd=2.0), "floor_active": dict(i_mu=-6.0)}
 

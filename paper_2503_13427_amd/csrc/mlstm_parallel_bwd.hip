@@ -357,12 +357,14 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_kernel(BwdArgs A) {
     }
 }
 
-// ---- MFMA row and column passes (DQK and DV multiples of 64) ----------------------------------
+// ---- MFMA row and column passes (instantiated head shapes) ------------------------------------
 //
 // The same passes with the tile products on fp32 MFMA 16x16x4 (lane l: A[l % 16][l / 16],
 // B[l / 16][l % 16], D[4 (l / 16) + j][l % 16]).  Per 16 x 16 tile of (t, s) pairs:
 //   - the logits S = Q^ K^T (or U = dN~ V^T) are split over the four waves along the contraction
-//     and their partial tiles summed through LDS;
+//     and their partial tiles summed through LDS; the operand that stays fixed over a sweep (the
+//     row pass's q^ and dN~ rows, the column pass's k and v rows) is held in registers, which
+//     keeps a workgroup near 60 KB of LDS and lets two share a CU;
 //   - one thread per pair applies the gates (F~, the causal mask) and writes the operand tile;
 //   - the accumulating products (N~ += A~ V, dq += W K; dk += W^T Q^, dv += A~^T dN~) give each
 //     wave a quarter of the output columns, one 16 x 16 accumulator per 16 columns.
@@ -375,18 +377,6 @@ __device__ __forceinline__ f32x4_t mfma4(float a, float b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-// Partial logits over this wave's quarter of a contraction of length n: rows of X (pitch xp) against
-// rows of Y (pitch yp), both 16 x n in LDS; returns the 16 x 16 partial in D layout.
-__device__ __forceinline__ f32x4_t partial_logits(const float* X, int xp, const float* Y, int yp, int n, int wave,
-                                                  int l16, int g) {
-    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    const int q = n / 4;
-    for (int k = wave * q; k < (wave + 1) * q; k += 4) acc = mfma4(X[l16 * xp + k + g], Y[l16 * yp + k + g], acc);
-    return acc;
-}
-
-// 16 rows of n values (n a multiple of 64) from global memory into LDS as fp32, rows at or beyond
-// nrows_total as zeros: 16-byte loads, every load of the thread issued before the first store.
 template <typename TIn> struct Vec16;
 template <> struct Vec16<float> {
     static constexpr int N = 4;
@@ -405,11 +395,11 @@ template <> struct Vec16<bf16_t> {
         }
     }
 };
-template <typename TIn>
+template <typename TIn, int NMAX = kMaxDV>
 __device__ __forceinline__ void stage_rows(float* dst, int pitch, const TIn* src, int r0, int nrows_total, int n,
                                            float scale, int tid) {
     typedef Vec16<TIn> V;
-    constexpr int kMaxPer = kBT * kMaxDV / V::N / kBwdThreads;   // vectors per thread, at most
+    constexpr int kMaxPer = (kBT * NMAX / V::N + kBwdThreads - 1) / kBwdThreads;   // vectors per thread, at most
     const int nvec = kBT * n / V::N;
     typename V::type buf[kMaxPer];
 #pragma unroll
@@ -437,21 +427,21 @@ __device__ __forceinline__ void stage_rows(float* dst, int pitch, const TIn* src
     }
 }
 // the same for fp32 rows of the workspace
+template <int NMAX>
 __device__ __forceinline__ void stage_rows_f32(float* dst, int pitch, const float* src, int r0, int nrows_total, int n,
                                                int tid) {
-    stage_rows<float>(dst, pitch, src, r0, nrows_total, n, 1.0f, tid);
+    stage_rows<float, NMAX>(dst, pitch, src, r0, nrows_total, n, 1.0f, tid);
 }
 
-template <typename TIn>
+template <typename TIn, int NK, int NV>   // DQK = 64 NK, DV = 64 NV
 __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     extern __shared__ float sm[];
-    const int DQK = A.DQK, DV = A.DV, T = A.T;
-    const int KP = DQK + 4, VP = DV + 4;
-    float* Qs = sm;                      // [kBT][KP]
-    float* Ks = Qs + kBT * KP;           // [kBT][KP]
-    float* Vs = Ks + kBT * KP;           // [kBT][VP]
-    float* dN = Vs + kBT * VP;           // [kBT][VP]
-    float* Pr = dN + kBT * VP;           // [4 waves][kBT][kBT] partial logits
+    constexpr int DQK = 64 * NK, DV = 64 * NV;
+    const int T = A.T;
+    constexpr int KP = DQK + 4, VP = DV + 4;
+    float* Ks = sm;                      // [kBT][KP]
+    float* Vs = Ks + kBT * KP;           // [kBT][VP]; between the sweeps it passes dN~ to the registers
+    float* Pr = Vs + kBT * VP;           // [4 waves][kBT][kBT] partial logits
     float* Op = Pr + 4 * kBT * kBT;      // [kBT][kTP] operand tile (A~ or W), rows t
     float* red = Op + kBT * kTP;         // [4][kBT][kBT] row partial sums
     float* rowv = red + 4 * kBT * kBT;   // [kBT][4] per row: M, m, dD
@@ -472,18 +462,25 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     float* Pw = wsq + 4 * T;
     float* dNw = wsq + dn_off(T);
     const float qscale = rsqrtf(static_cast<float>(DQK));
-    const int nvt = DV / 64, nkt = DQK / 64;   // 16-column output tiles per wave
+    constexpr int nvt = NV, nkt = NK;   // 16-column output tiles per wave
     const int vc0 = wave * (DV / 4), kc0 = wave * (DQK / 4);
 
-    stage_rows<TIn>(Qs, KP, q, t0, T, DQK, qscale, tid);
+    // this wave's quarter of the q^ rows, as the A operand of the logits (lane: row l16, k 4 kk + g)
+    constexpr int kq = DQK / 4;
+    float qreg[(4 * NK)];
+#pragma unroll
+    for (int kk = 0; kk < (4 * NK); ++kk)
+        qreg[kk] = (kk < kq / 4 && t0 + l16 < T)
+                       ? io<TIn>::load(q, static_cast<int64_t>(t0 + l16) * DQK + wave * kq + 4 * kk + g) * qscale
+                       : 0.0f;
     if (tid < kBT) {
         const int t = t0 + tid;
         rowv[4 * tid + 0] = t < T ? Mw[t] : 0.0f;
         rowv[4 * tid + 1] = t < T ? mw[t] : 0.0f;
     }
-    f32x4_t accN[kMaxNT];
+    f32x4_t accN[NV];
 #pragma unroll
-    for (int c = 0; c < kMaxNT; ++c) accN[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < NV; ++c) accN[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float accD = 0.0f;   // this thread's (t, s) column of A~, summed over s tiles
     const int t_pair = t0 + pr;
     const int last_tile = t0 / kBT;
@@ -491,10 +488,13 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     for (int st = 0; st <= last_tile; ++st) {
         const int s0 = st * kBT;
         __syncthreads();
-        stage_rows<TIn>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
-        stage_rows<TIn>(Vs, VP, v, s0, T, DV, 1.0f, tid);
+        stage_rows<TIn, DQK>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
+        stage_rows<TIn, DV>(Vs, VP, v, s0, T, DV, 1.0f, tid);
         __syncthreads();
-        const f32x4_t part = partial_logits(Qs, KP, Ks, KP, DQK, wave, l16, g);
+        f32x4_t part = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < (4 * NK); ++kk)
+            if (kk < kq / 4) part = mfma4(qreg[kk], Ks[l16 * KP + wave * kq + 4 * kk + g], part);
 #pragma unroll
         for (int j = 0; j < 4; ++j) Pr[(wave * kBT + 4 * g + j) * kBT + l16] = part[j];
         __syncthreads();
@@ -514,11 +514,11 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
         for (int kk = 0; kk < 4; ++kk) {
             const float a = Op[l16 * kTP + 4 * kk + g];
 #pragma unroll
-            for (int c = 0; c < kMaxNT; ++c)
+            for (int c = 0; c < NV; ++c)
                 if (c < nvt) accN[c] = mfma4(a, Vs[(4 * kk + g) * VP + vc0 + 16 * c + l16], accN[c]);
         }
     }
-    // D~ per row, then dN~, dD~ and P
+    // D~ per row, then dN~, dD~ and P (the barrier also ends every read of the last V tile)
     red[pr * kBT + pc] = accD;
     __syncthreads();
     if (tid < kBT) {
@@ -534,7 +534,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
         const float Dt = rowv[4 * r + 3];
         const float den = fmaxf(fabsf(Dt), expf(-rowv[4 * r + 1]));
 #pragma unroll
-        for (int c = 0; c < kMaxNT; ++c) {
+        for (int c = 0; c < NV; ++c) {
             if (c < nvt) {
                 const int col = vc0 + 16 * c + l16;
                 const float gh = t < T ? A.dh[(seq * T + t) * DV + col] : 0.0f;
@@ -542,7 +542,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
                 const float dn = gh / den;
                 part_hh[j] += gh * (nv / den);
                 part_nn[j] += dn * nv;
-                dN[r * VP + col] = dn;
+                Vs[r * VP + col] = dn;   // the last sweep-1 reads of Vs are done (barrier below)
                 if (t < T) dNw[static_cast<int64_t>(t) * DV + col] = dn;
             }
         }
@@ -575,17 +575,28 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
         Pw[t0 + tid] = sdn + dD * rowv[4 * tid + 3];
     }
 
-    // sweep 2: dq
-    f32x4_t accQ[kMaxDQK / 64];
+    // dN~ rows into registers as the A operand of U = dN~ V^T (lane: row l16, d = this wave's
+    // quarter, 4 kk + g); Vs held them since the barriers above
+    constexpr int dq4 = DV / 4;
+    __syncthreads();
+    float dnreg[(4 * NV)];
 #pragma unroll
-    for (int c = 0; c < kMaxDQK / 64; ++c) accQ[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < (4 * NV); ++kk) dnreg[kk] = (kk < dq4 / 4) ? Vs[l16 * VP + wave * dq4 + 4 * kk + g] : 0.0f;
+
+    // sweep 2: dq
+    f32x4_t accQ[NK];
+#pragma unroll
+    for (int c = 0; c < NK; ++c) accQ[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     for (int st = 0; st <= last_tile; ++st) {
         const int s0 = st * kBT;
         __syncthreads();
-        stage_rows<TIn>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
-        stage_rows<TIn>(Vs, VP, v, s0, T, DV, 1.0f, tid);
+        stage_rows<TIn, DQK>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
+        stage_rows<TIn, DV>(Vs, VP, v, s0, T, DV, 1.0f, tid);
         __syncthreads();
-        const f32x4_t part = partial_logits(dN, VP, Vs, VP, DV, wave, l16, g);
+        f32x4_t part = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < (4 * NV); ++kk)
+            if (kk < dq4 / 4) part = mfma4(dnreg[kk], Vs[l16 * VP + wave * dq4 + 4 * kk + g], part);
 #pragma unroll
         for (int j = 0; j < 4; ++j) Pr[(wave * kBT + 4 * g + j) * kBT + l16] = part[j];
         __syncthreads();
@@ -604,7 +615,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
         for (int kk = 0; kk < 4; ++kk) {
             const float a = Op[l16 * kTP + 4 * kk + g];
 #pragma unroll
-            for (int c = 0; c < kMaxDQK / 64; ++c)
+            for (int c = 0; c < NK; ++c)
                 if (c < nkt) accQ[c] = mfma4(a, Ks[(4 * kk + g) * KP + kc0 + 16 * c + l16], accQ[c]);
         }
     }
@@ -613,20 +624,19 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
         const int t = t0 + 4 * g + j;
         if (t < T) {
 #pragma unroll
-            for (int c = 0; c < kMaxDQK / 64; ++c)
+            for (int c = 0; c < NK; ++c)
                 if (c < nkt) A.dq[(seq * T + t) * DQK + kc0 + 16 * c + l16] = accQ[c][j] * qscale;
         }
     }
 }
 
-template <typename TIn>
+template <typename TIn, int NK, int NV>   // DQK = 64 NK, DV = 64 NV
 __global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
     extern __shared__ float sm[];
-    const int DQK = A.DQK, DV = A.DV, T = A.T;
-    const int KP = DQK + 4, VP = DV + 4;
-    float* Ks = sm;                      // [kBT][KP] this tile's k
-    float* Vs = Ks + kBT * KP;           // [kBT][VP] this tile's v
-    float* Qs = Vs + kBT * VP;           // [kBT][KP] a tile of q^
+    constexpr int DQK = 64 * NK, DV = 64 * NV;
+    const int T = A.T;
+    constexpr int KP = DQK + 4, VP = DV + 4;
+    float* Qs = sm;                      // [kBT][KP] a tile of q^
     float* dN = Qs + kBT * KP;           // [kBT][VP] a tile of dN~
     float* Ps = dN + kBT * VP;           // [4][kBT][kBT] partial S
     float* Pu = Ps + 4 * kBT * kBT;      // [4][kBT][kBT] partial U
@@ -649,30 +659,45 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
     const float* dDw = wsq + 3 * T;
     const float* dNw = wsq + dn_off(T);
     const float qscale = rsqrtf(static_cast<float>(DQK));
-    const int nvt = DV / 64, nkt = DQK / 64;
+    constexpr int nvt = NV, nkt = NK;
     const int vc0 = wave * (DV / 4), kc0 = wave * (DQK / 4);
 
-    stage_rows<TIn>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
-    stage_rows<TIn>(Vs, VP, v, s0, T, DV, 1.0f, tid);
-    f32x4_t accK[kMaxDQK / 64], accV[kMaxNT];
+    // this tile's k and v rows, as the B operands of S and U (lane: column s = l16, the wave's
+    // quarter of the contraction, 4 kk + g)
+    constexpr int kq = DQK / 4, dq4 = DV / 4;
+    float kreg[(4 * NK)], vreg[(4 * NV)];
 #pragma unroll
-    for (int c = 0; c < kMaxDQK / 64; ++c) accK[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < (4 * NK); ++kk)
+        kreg[kk] = (kk < kq / 4 && s0 + l16 < T)
+                       ? io<TIn>::load(k, static_cast<int64_t>(s0 + l16) * DQK + wave * kq + 4 * kk + g) : 0.0f;
 #pragma unroll
-    for (int c = 0; c < kMaxNT; ++c) accV[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < (4 * NV); ++kk)
+        vreg[kk] = (kk < dq4 / 4 && s0 + l16 < T)
+                       ? io<TIn>::load(v, static_cast<int64_t>(s0 + l16) * DV + wave * dq4 + 4 * kk + g) : 0.0f;
+    f32x4_t accK[NK], accV[NV];
+#pragma unroll
+    for (int c = 0; c < NK; ++c) accK[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NV; ++c) accV[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float accI = 0.0f;   // this thread's (t, s) entry of G, summed over t tiles
     for (int tt = s0 / kBT; tt < ntile; ++tt) {
         const int t0 = tt * kBT;
         __syncthreads();
-        stage_rows<TIn>(Qs, KP, q, t0, T, DQK, qscale, tid);
-        stage_rows_f32(dN, VP, dNw, t0, T, DV, tid);
+        stage_rows<TIn, DQK>(Qs, KP, q, t0, T, DQK, qscale, tid);
+        stage_rows_f32<DV>(dN, VP, dNw, t0, T, DV, tid);
         if (tid < kBT) {
             const int t = t0 + tid;
             rowv[2 * tid + 0] = t < T ? Mw[t] : 0.0f;
             rowv[2 * tid + 1] = t < T ? dDw[t] : 0.0f;
         }
         __syncthreads();
-        const f32x4_t ps = partial_logits(Qs, KP, Ks, KP, DQK, wave, l16, g);   // S[t][s]
-        const f32x4_t pu = partial_logits(dN, VP, Vs, VP, DV, wave, l16, g);    // U[t][s]
+        f32x4_t ps = f32x4_t{0.f, 0.f, 0.f, 0.f}, pu = f32x4_t{0.f, 0.f, 0.f, 0.f};   // S[t][s], U[t][s]
+#pragma unroll
+        for (int kk = 0; kk < (4 * NK); ++kk)
+            if (kk < kq / 4) ps = mfma4(Qs[l16 * KP + wave * kq + 4 * kk + g], kreg[kk], ps);
+#pragma unroll
+        for (int kk = 0; kk < (4 * NV); ++kk)
+            if (kk < dq4 / 4) pu = mfma4(dN[l16 * VP + wave * dq4 + 4 * kk + g], vreg[kk], pu);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             Ps[(wave * kBT + 4 * g + j) * kBT + l16] = ps[j];
@@ -703,10 +728,10 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
             const float aw = Wt[l16 * kTP + 4 * kk + g];
             const float aa = At[l16 * kTP + 4 * kk + g];
 #pragma unroll
-            for (int c = 0; c < kMaxDQK / 64; ++c)
+            for (int c = 0; c < NK; ++c)
                 if (c < nkt) accK[c] = mfma4(aw, Qs[(4 * kk + g) * KP + kc0 + 16 * c + l16], accK[c]);
 #pragma unroll
-            for (int c = 0; c < kMaxNT; ++c)
+            for (int c = 0; c < NV; ++c)
                 if (c < nvt) accV[c] = mfma4(aa, dN[(4 * kk + g) * VP + vc0 + 16 * c + l16], accV[c]);
         }
     }
@@ -715,10 +740,10 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
         const int s = s0 + 4 * g + j;
         if (s < T) {
 #pragma unroll
-            for (int c = 0; c < kMaxDQK / 64; ++c)
+            for (int c = 0; c < NK; ++c)
                 if (c < nkt) A.dk[(seq * T + s) * DQK + kc0 + 16 * c + l16] = accK[c][j];
 #pragma unroll
-            for (int c = 0; c < kMaxNT; ++c)
+            for (int c = 0; c < NV; ++c)
                 if (c < nvt) A.dv[(seq * T + s) * DV + vc0 + 16 * c + l16] = accV[c][j];
         }
     }
@@ -752,12 +777,10 @@ __global__ void bwd_forget_kernel(BwdArgs A, int S) {
 }
 
 size_t row_mfma_lds(int DQK, int DV) {
-    return sizeof(float) * (2 * kBT * (DQK + 4) + 2 * kBT * (DV + 4) + 4 * kBT * kBT + kBT * kTP + 4 * kBT * kBT +
-                            4 * kBT);
+    return sizeof(float) * (kBT * (DQK + 4) + kBT * (DV + 4) + 4 * kBT * kBT + kBT * kTP + 4 * kBT * kBT + 4 * kBT);
 }
 size_t col_mfma_lds(int DQK, int DV) {
-    return sizeof(float) * (2 * kBT * (DQK + 4) + 2 * kBT * (DV + 4) + 8 * kBT * kBT + 2 * kBT * kTP + kBT * kBT +
-                            2 * kBT);
+    return sizeof(float) * (kBT * (DQK + 4) + kBT * (DV + 4) + 8 * kBT * kBT + 2 * kBT * kTP + kBT * kBT + 2 * kBT);
 }
 size_t row_lds(int DQK, int DV) {
     return sizeof(float) * (2 * kBT * (DQK + 1) + 2 * kBT * (DV + 1) + 2 * kBT * kBT + 4 * kBT);
@@ -766,15 +789,38 @@ size_t col_lds(int DQK, int DV) {
     return sizeof(float) * (2 * kBT * (DQK + 1) + 2 * kBT * (DV + 1) + 3 * kBT * kBT + 2 * kBT);
 }
 
+// The MFMA passes for one (DQK, DV) = (64 NK, 64 NV); their dynamic LDS limit is raised on first use.
+template <typename TIn, int NK, int NV>
+hipError_t launch_mfma_passes(const BwdArgs& a, dim3 tiles, hipStream_t stream) {
+    static bool attr = false;
+    const size_t lr = row_mfma_lds(64 * NK, 64 * NV), lc = col_mfma_lds(64 * NK, 64 * NV);
+    if (!attr) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_row_mfma_kernel<TIn, NK, NV>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lr));
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_col_mfma_kernel<TIn, NK, NV>),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lc));
+        if (e != hipSuccess) return e;
+        attr = true;
+    }
+    hipLaunchKernelGGL((bwd_row_mfma_kernel<TIn, NK, NV>), tiles, dim3(kBwdThreads), lr, stream, a);
+    hipLaunchKernelGGL((bwd_col_mfma_kernel<TIn, NK, NV>), tiles, dim3(kBwdThreads), lc, stream, a);
+    return hipSuccess;
+}
+
+// head shapes with MFMA passes: the xLSTM-7B head and three smaller ones
+bool bwd_mfma_shape(int DQK, int DV) {
+    return (DQK == 256 && DV == 512) || (DQK == 64 && DV == 64) || (DQK == 64 && DV == 128) ||
+           (DQK == 128 && DV == 192);
+}
+
 template <typename TIn>
 hipError_t launch_typed(const BwdArgs& a, int S, hipStream_t stream) {
     static bool attr = false;
     if (!attr) {
         const std::pair<const void*, size_t> kernels[] = {
             {reinterpret_cast<const void*>(bwd_row_kernel<TIn>), row_lds(kMaxDQK, kMaxDV)},
-            {reinterpret_cast<const void*>(bwd_col_kernel<TIn>), col_lds(kMaxDQK, kMaxDV)},
-            {reinterpret_cast<const void*>(bwd_row_mfma_kernel<TIn>), row_mfma_lds(kMaxDQK, kMaxDV)},
-            {reinterpret_cast<const void*>(bwd_col_mfma_kernel<TIn>), col_mfma_lds(kMaxDQK, kMaxDV)}};
+            {reinterpret_cast<const void*>(bwd_col_kernel<TIn>), col_lds(kMaxDQK, kMaxDV)}};
         for (const auto& kl : kernels) {
             hipError_t e = hipFuncSetAttribute(kl.first, hipFuncAttributeMaxDynamicSharedMemorySize,
                                                static_cast<int>(kl.second));
@@ -785,16 +831,17 @@ hipError_t launch_typed(const BwdArgs& a, int S, hipStream_t stream) {
     const int ntile = (a.T + kBT - 1) / kBT;
     const dim3 tiles(static_cast<unsigned>(static_cast<int64_t>(S) * ntile));
     const dim3 seqs(static_cast<unsigned>(S));   // the scans: one wave per sequence
-    // the MFMA passes need each wave to own whole 16-column tiles of DQK and DV
-    const bool mfma = (a.DQK % 64 == 0) && (a.DV % 64 == 0);
     hipLaunchKernelGGL(bwd_gate_kernel, seqs, dim3(64), 0, stream, a, S);
-    if (mfma) {
-        hipLaunchKernelGGL(bwd_row_mfma_kernel<TIn>, tiles, dim3(kBwdThreads), row_mfma_lds(a.DQK, a.DV), stream, a);
-        hipLaunchKernelGGL(bwd_col_mfma_kernel<TIn>, tiles, dim3(kBwdThreads), col_mfma_lds(a.DQK, a.DV), stream, a);
-    } else {
+    hipError_t e = hipSuccess;
+    if (a.DQK == 256 && a.DV == 512) e = launch_mfma_passes<TIn, 4, 8>(a, tiles, stream);
+    else if (a.DQK == 64 && a.DV == 64) e = launch_mfma_passes<TIn, 1, 1>(a, tiles, stream);
+    else if (a.DQK == 64 && a.DV == 128) e = launch_mfma_passes<TIn, 1, 2>(a, tiles, stream);
+    else if (a.DQK == 128 && a.DV == 192) e = launch_mfma_passes<TIn, 2, 3>(a, tiles, stream);
+    else {
         hipLaunchKernelGGL(bwd_row_kernel<TIn>, tiles, dim3(kBwdThreads), row_lds(a.DQK, a.DV), stream, a);
         hipLaunchKernelGGL(bwd_col_kernel<TIn>, tiles, dim3(kBwdThreads), col_lds(a.DQK, a.DV), stream, a);
     }
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bwd_forget_kernel, seqs, dim3(64), 0, stream, a, S);
     return hipGetLastError();
 }

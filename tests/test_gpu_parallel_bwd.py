@@ -78,6 +78,7 @@ SMALL = [
     (1, 2, 100, 64, 128, "standard"),     # DQK, DV multiples of 64: the MFMA passes
     (2, 1, 77, 64, 64, "short_memory"),   # MFMA passes, ragged T
     (1, 1, 50, 128, 192, "floor_active"), # MFMA passes, three 16-column tiles per wave
+    (1, 1, 40, 256, 512, "standard"),     # the xLSTM-7B head in fp32: MFMA passes
 ]
 DIST = {"standard": {}, "short_memory": dict(f_mu=-1.0, f_sd=2.0), "floor_active": dict(i_mu=-6.0)}
 

@@ -101,3 +101,26 @@ def test_parallel_bwd_bf16_xlstm_head(T):
     ref = G.parallel_grad(q, k, v, ip, fp, dh)
     ref = [r.reshape(r.shape[0], r.shape[1], -1) for r in ref]
     compare(got, ref, TOL_BF16, f"7B head T{T}")
+
+
+@pytest.mark.parametrize("dtype,DQK,DV", [("f32", 64, 128), ("bf16", 256, 512)])
+def test_autograd_cell_gradients(dtype, DQK, DV):
+    """Gradients through ``mlstm_cell`` (forward on the chunkwise kernels, backward on the parallel-form
+    kernels) for a loss sum(h * w), against the fp64 gradient oracle with dh = w (for bf16 the forward
+    output h, and so dh = w, enter in bf16, and the gradients return in bf16: the bf16 bar)."""
+    from paper_2503_13427_amd.cell import mlstm_cell
+    B, NH, T = 1, 2, 90
+    q, k, v, ip, fp, w = draw(330, B, NH, T, DQK, DV, dtype)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dev = lambda x, dt, *shape: torch.from_numpy(np.ascontiguousarray(x)).reshape(*shape).cuda().to(dt).requires_grad_(True)
+    tq, tk, tv = dev(q, tdt, B, NH, T, DQK), dev(k, tdt, B, NH, T, DQK), dev(v, tdt, B, NH, T, DV)
+    tip, tfp = dev(ip, torch.float32, B, NH, T), dev(fp, torch.float32, B, NH, T)
+    h = mlstm_cell(tq, tk, tv, tip, tfp, L=64)
+    assert h.dtype == tdt
+    (h * torch.from_numpy(w).reshape(B, NH, T, DV).cuda().to(tdt)).sum().backward()
+    torch.cuda.synchronize()
+    got = [t.grad.float().cpu().numpy().astype(np.float64).reshape(B * NH, T, -1) for t in (tq, tk, tv, tip, tfp)]
+    wr = w if dtype == "f32" else bf16_bits_to_f32(f32_to_bf16_bits(w))
+    ref = G.recurrent_grad(q, k, v, ip, fp, wr)
+    ref = [r.reshape(r.shape[0], r.shape[1], -1) for r in ref]
+    compare(got, ref, TOL_BWD_F32 if dtype == "f32" else TOL_BF16, f"autograd cell {dtype}")

@@ -262,3 +262,43 @@ def test_prefill_full_size_sampled_heads(wl):
     heads = [0, wl.heads - 1]
     sub = wl.prefill_inputs(heads=heads)
     check(sub, o, heads=heads, label=wl.name)
+
+
+def test_maximum_sequence_length():
+    """The longest sequence the MFMA prefill takes: T = 2^21 - 64, whose h spans just under the 2^31
+    bytes a buffer resource addresses.  A document border every 4096 tokens makes every document a
+    fresh run (App. B; pinned on the oracle), so sampled documents, including the ragged last one
+    that ends at the last token, and the final state are checked against the oracle run on that
+    document alone."""
+    T = (1 << 21) - 64
+    L, doc = 64, 4096
+    assert T * 512 * 2 < (1 << 31) and (T + 64) * 512 * 2 >= (1 << 31)
+    g = torch.Generator(device="cuda").manual_seed(90)
+    q = torch.randn(1, 1, T, 256, generator=g, device="cuda").bfloat16()
+    k = (torch.randn(1, 1, T, 256, generator=g, device="cuda") / 16).bfloat16()
+    v = torch.randn(1, 1, T, 512, generator=g, device="cuda").bfloat16()
+    ip = torch.randn(1, 1, T, generator=g, device="cuda")
+    fp = torch.randn(1, 1, T, generator=g, device="cuda") + 3
+    fp[..., ::doc] = float("-inf")
+    h = torch.empty(1, 1, T, 512, dtype=torch.bfloat16, device="cuda")
+    CT = torch.empty(1, 1, 256, 512, device="cuda")
+    nT = torch.empty(1, 1, 256, device="cuda")
+    mT = torch.empty(1, 1, device="cuda")
+    nb = _mb().mlstm_chunkwise_workspace_bytes(1, 1, T, 256, 512, L)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    _mb().mlstm_chunkwise_fwd(q, k, v, ip, fp, None, None, None, L, h, CT, nT, mT, workspace=ws)
+    torch.cuda.synchronize()
+    starts = [0, doc * 257, (T - 1) // doc * doc]
+    for s0 in starts:
+        e0 = min(T, s0 + doc)
+        sl = lambda x: host_f64(x[0, 0, s0:e0]).reshape(1, e0 - s0, -1)
+        qd, kd, vd = sl(q), sl(k), sl(v)
+        ipd, fpd = host_f64(ip[0, 0, s0:e0]).reshape(1, -1), host_f64(fp[0, 0, s0:e0]).reshape(1, -1)
+        hr, Cr, nr, mr = coracle.recurrent(qd, kd, vd, ipd, fpd, None, None, None)
+        eh = rel_err(sl(h).reshape(1, -1), hr.reshape(1, -1), 1)
+        print(f"T = {T}: document at {s0} ({e0 - s0} tokens): h {eh:.3e}")
+        assert np.isfinite(sl(h)).all() and eh <= TOL_BF16
+    eC, en, em = state_errs(host_f64(CT).reshape(1, 256, 512), host_f64(nT).reshape(1, 256), host_f64(mT).reshape(1),
+                            Cr, nr, mr)
+    print(f"final state: C {eC:.3e} n {en:.3e} m {em:.3e}")
+    assert max(eC, en, em) <= TOL_BF16

@@ -5,9 +5,25 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "mlstm.h"
 
 namespace mlstm {
+
+// Raises a kernel's dynamic LDS limit to `bytes` on the current device, once per device;
+// `done` is that kernel's mask of devices already raised (devices 64 and up are raised on
+// every call).  Safe to call from several host threads: the attribute call is idempotent.
+inline hipError_t raise_dynamic_lds(const void* kernel, size_t bytes, std::atomic<uint64_t>& done) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = dev < 64 ? (uint64_t{1} << dev) : 0;
+    if (bit != 0 && (done.load(std::memory_order_acquire) & bit) != 0) return hipSuccess;
+    e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
+    if (e == hipSuccess && bit != 0) done.fetch_or(bit, std::memory_order_release);
+    return e;
+}
 
 // --- decode step -----------------------------------------------------------
 hipError_t launch_step(mlstm_dtype dt, const void* q, const void* k, const void* v, const float* ipre,

@@ -1287,13 +1287,9 @@ template <int L>
 hipError_t launch_variant(const ChunkKernelArgs& a, int S, hipStream_t stream) {
     const size_t lds = sizeof(Smem<L>);
     auto kern = chunk_mfma_kernel<L>;
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
+    static std::atomic<uint64_t> raised{0};
+    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(kern), lds, raised);
+    if (e != hipSuccess) return e;
     const dim3 grid(static_cast<unsigned>(S * a.G * kNTile));
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, stream, a);
     return hipGetLastError();
@@ -1301,13 +1297,9 @@ hipError_t launch_variant(const ChunkKernelArgs& a, int S, hipStream_t stream) {
 
 hipError_t launch_local(const LocalArgs& a, int S, hipStream_t stream) {
     const size_t lds = sizeof(LocSmem);
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(local_state_kernel),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
+    static std::atomic<uint64_t> raised{0};
+    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(local_state_kernel), lds, raised);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(local_state_kernel, dim3(static_cast<unsigned>(S * a.NS * kNTile)), dim3(kThreads), lds, stream,
                        a);
     return hipGetLastError();

@@ -789,20 +789,15 @@ size_t col_lds(int DQK, int DV) {
     return sizeof(float) * (2 * kBT * (DQK + 1) + 2 * kBT * (DV + 1) + 3 * kBT * kBT + 2 * kBT);
 }
 
-// The MFMA passes for one (DQK, DV) = (64 NK, 64 NV); their dynamic LDS limit is raised on first use.
+// The MFMA passes for one (DQK, DV) = (64 NK, 64 NV); their dynamic LDS limit is raised once per device.
 template <typename TIn, int NK, int NV>
 hipError_t launch_mfma_passes(const BwdArgs& a, dim3 tiles, hipStream_t stream) {
-    static bool attr = false;
+    static std::atomic<uint64_t> raised_row{0}, raised_col{0};
     const size_t lr = row_mfma_lds(64 * NK, 64 * NV), lc = col_mfma_lds(64 * NK, 64 * NV);
-    if (!attr) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_row_mfma_kernel<TIn, NK, NV>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lr));
-        if (e == hipSuccess)
-            e = hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_col_mfma_kernel<TIn, NK, NV>),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lc));
-        if (e != hipSuccess) return e;
-        attr = true;
-    }
+    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_row_mfma_kernel<TIn, NK, NV>), lr, raised_row);
+    if (e == hipSuccess)
+        e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_col_mfma_kernel<TIn, NK, NV>), lc, raised_col);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((bwd_row_mfma_kernel<TIn, NK, NV>), tiles, dim3(kBwdThreads), lr, stream, a);
     hipLaunchKernelGGL((bwd_col_mfma_kernel<TIn, NK, NV>), tiles, dim3(kBwdThreads), lc, stream, a);
     return hipSuccess;
@@ -816,17 +811,14 @@ bool bwd_mfma_shape(int DQK, int DV) {
 
 template <typename TIn>
 hipError_t launch_typed(const BwdArgs& a, int S, hipStream_t stream) {
-    static bool attr = false;
-    if (!attr) {
-        const std::pair<const void*, size_t> kernels[] = {
-            {reinterpret_cast<const void*>(bwd_row_kernel<TIn>), row_lds(kMaxDQK, kMaxDV)},
-            {reinterpret_cast<const void*>(bwd_col_kernel<TIn>), col_lds(kMaxDQK, kMaxDV)}};
-        for (const auto& kl : kernels) {
-            hipError_t e = hipFuncSetAttribute(kl.first, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                               static_cast<int>(kl.second));
-            if (e != hipSuccess) return e;
-        }
-        attr = true;
+    static std::atomic<uint64_t> raised_row{0}, raised_col{0};
+    {
+        hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_row_kernel<TIn>), row_lds(kMaxDQK, kMaxDV),
+                                         raised_row);
+        if (e == hipSuccess)
+            e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_col_kernel<TIn>), col_lds(kMaxDQK, kMaxDV),
+                                  raised_col);
+        if (e != hipSuccess) return e;
     }
     const int ntile = (a.T + kBT - 1) / kBT;
     const dim3 tiles(static_cast<unsigned>(static_cast<int64_t>(S) * ntile));

@@ -363,12 +363,14 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_kernel(BwdArgs A) {
 // B[l / 16][l % 16], D[4 (l / 16) + j][l % 16]).  Per 16 x 16 tile of (t, s) pairs:
 //   - the logits S = Q^ K^T (or U = dN~ V^T) are split over the four waves along the contraction
 //     and their partial tiles summed through LDS; the operand that stays fixed over a sweep (the
-//     row pass's q^ and dN~ rows, the column pass's k and v rows) is held in registers, which
-//     keeps a workgroup near 60 KB of LDS and lets two share a CU;
+//     row pass's q^ and dN~ rows, the column pass's k and v rows) is held in registers;
+//   - the k, v and q tiles stay in the input type in LDS, so with bf16 inputs a row-pass
+//     workgroup takes 34 KB of LDS and a column-pass workgroup 52 KB (dN~ stays fp32), and
+//     three share a CU;
 //   - one thread per pair applies the gates (F~, the causal mask) and writes the operand tile;
 //   - the accumulating products (N~ += A~ V, dq += W K; dk += W^T Q^, dv += A~^T dN~) give each
 //     wave a quarter of the output columns, one 16 x 16 accumulator per 16 columns.
-// LDS rows are padded to a pitch of 4 (mod 32) floats.
+// fp32 LDS rows are padded to a pitch of 4 (mod 32) floats.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kMaxNT = kMaxDV / 64;     // 16-column output tiles per wave, at most (DV = 512)
 constexpr int kTP = kBT + 4;            // pitch of a 16 x 16 operand tile
@@ -433,15 +435,46 @@ __device__ __forceinline__ void stage_rows_f32(float* dst, int pitch, const floa
     stage_rows<float, NMAX>(dst, pitch, src, r0, nrows_total, n, 1.0f, tid);
 }
 
+// k, v and q tiles stay in the input type in LDS (half the bytes for bf16, so more workgroups
+// share a CU); rows beyond T are zero.  A bf16 row pitch of n + 8 elements keeps the 16-byte
+// stores aligned and the row and column reads of the passes at most 2-way bank-conflicted.
+template <typename TIn> constexpr int lds_pad() { return sizeof(TIn) == 2 ? 8 : 4; }
+__device__ __forceinline__ float lds_ld(const float* p, int i) { return p[i]; }
+__device__ __forceinline__ float lds_ld(const bf16_t* p, int i) { return bf16_to_f32(p[i].bits); }
+template <typename TIn, int NMAX>
+__device__ __forceinline__ void stage_raw(TIn* dst, int pitch, const TIn* src, int r0, int nrows_total, int n,
+                                          int tid) {
+    typedef typename Vec16<TIn>::type V;
+    constexpr int kN = Vec16<TIn>::N;
+    constexpr int kMaxPer = (kBT * NMAX / kN + kBwdThreads - 1) / kBwdThreads;
+    const int nvec = kBT * n / kN;
+    V buf[kMaxPer];
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+        const int idx = tid + kBwdThreads * i;
+        buf[i] = V{};
+        if (idx < nvec && r0 + (idx * kN) / n < nrows_total)
+            buf[i] = reinterpret_cast<const V*>(src + static_cast<int64_t>(r0) * n)[idx];
+    }
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+        const int idx = tid + kBwdThreads * i;
+        if (idx < nvec) {
+            const int e = idx * kN;
+            *reinterpret_cast<V*>(dst + (e / n) * pitch + e % n) = buf[i];
+        }
+    }
+}
+
 template <typename TIn, int NK, int NV>   // DQK = 64 NK, DV = 64 NV
 __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     extern __shared__ float sm[];
     constexpr int DQK = 64 * NK, DV = 64 * NV;
     const int T = A.T;
-    constexpr int KP = DQK + 4, VP = DV + 4;
-    float* Ks = sm;                      // [kBT][KP]
-    float* Vs = Ks + kBT * KP;           // [kBT][VP]; between the sweeps it passes dN~ to the registers
-    float* Pr = Vs + kBT * VP;           // [4 waves][kBT][kBT] partial logits
+    constexpr int KP = DQK + lds_pad<TIn>(), VP = DV + lds_pad<TIn>();
+    TIn* Ks = reinterpret_cast<TIn*>(sm);                // [kBT][KP]
+    TIn* Vs = Ks + kBT * KP;                             // [kBT][VP]
+    float* Pr = reinterpret_cast<float*>(Vs + kBT * VP); // [4 waves][kBT][kBT] partial logits
     float* Op = Pr + 4 * kBT * kBT;      // [kBT][kTP] operand tile (A~ or W), rows t
     float* red = Op + kBT * kTP;         // [4][kBT][kBT] row partial sums
     float* rowv = red + 4 * kBT * kBT;   // [kBT][4] per row: M, m, dD
@@ -488,13 +521,13 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     for (int st = 0; st <= last_tile; ++st) {
         const int s0 = st * kBT;
         __syncthreads();
-        stage_rows<TIn, DQK>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
-        stage_rows<TIn, DV>(Vs, VP, v, s0, T, DV, 1.0f, tid);
+        stage_raw<TIn, DQK>(Ks, KP, k, s0, T, DQK, tid);
+        stage_raw<TIn, DV>(Vs, VP, v, s0, T, DV, tid);
         __syncthreads();
         f32x4_t part = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < (4 * NK); ++kk)
-            if (kk < kq / 4) part = mfma4(qreg[kk], Ks[l16 * KP + wave * kq + 4 * kk + g], part);
+            if (kk < kq / 4) part = mfma4(qreg[kk], lds_ld(Ks, l16 * KP + wave * kq + 4 * kk + g), part);
 #pragma unroll
         for (int j = 0; j < 4; ++j) Pr[(wave * kBT + 4 * g + j) * kBT + l16] = part[j];
         __syncthreads();
@@ -515,10 +548,10 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
             const float a = Op[l16 * kTP + 4 * kk + g];
 #pragma unroll
             for (int c = 0; c < NV; ++c)
-                if (c < nvt) accN[c] = mfma4(a, Vs[(4 * kk + g) * VP + vc0 + 16 * c + l16], accN[c]);
+                if (c < nvt) accN[c] = mfma4(a, lds_ld(Vs, (4 * kk + g) * VP + vc0 + 16 * c + l16), accN[c]);
         }
     }
-    // D~ per row, then dN~, dD~ and P (the barrier also ends every read of the last V tile)
+    // D~ per row, then dN~, dD~ and P
     red[pr * kBT + pc] = accD;
     __syncthreads();
     if (tid < kBT) {
@@ -542,7 +575,6 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
                 const float dn = gh / den;
                 part_hh[j] += gh * (nv / den);
                 part_nn[j] += dn * nv;
-                Vs[r * VP + col] = dn;   // the last sweep-1 reads of Vs are done (barrier below)
                 if (t < T) dNw[static_cast<int64_t>(t) * DV + col] = dn;
             }
         }
@@ -576,12 +608,15 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     }
 
     // dN~ rows into registers as the A operand of U = dN~ V^T (lane: row l16, d = this wave's
-    // quarter, 4 kk + g); Vs held them since the barriers above
+    // quarter, 4 kk + g), read back from the workspace: the wave stored exactly these columns
+    // above, and the barriers since then order the stores before the loads
     constexpr int dq4 = DV / 4;
     __syncthreads();
     float dnreg[(4 * NV)];
 #pragma unroll
-    for (int kk = 0; kk < (4 * NV); ++kk) dnreg[kk] = (kk < dq4 / 4) ? Vs[l16 * VP + wave * dq4 + 4 * kk + g] : 0.0f;
+    for (int kk = 0; kk < (4 * NV); ++kk)
+        dnreg[kk] = (kk < dq4 / 4 && t0 + l16 < T)
+                        ? dNw[static_cast<int64_t>(t0 + l16) * DV + wave * dq4 + 4 * kk + g] : 0.0f;
 
     // sweep 2: dq
     f32x4_t accQ[NK];
@@ -590,13 +625,13 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     for (int st = 0; st <= last_tile; ++st) {
         const int s0 = st * kBT;
         __syncthreads();
-        stage_rows<TIn, DQK>(Ks, KP, k, s0, T, DQK, 1.0f, tid);
-        stage_rows<TIn, DV>(Vs, VP, v, s0, T, DV, 1.0f, tid);
+        stage_raw<TIn, DQK>(Ks, KP, k, s0, T, DQK, tid);
+        stage_raw<TIn, DV>(Vs, VP, v, s0, T, DV, tid);
         __syncthreads();
         f32x4_t part = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < (4 * NV); ++kk)
-            if (kk < dq4 / 4) part = mfma4(dnreg[kk], Vs[l16 * VP + wave * dq4 + 4 * kk + g], part);
+            if (kk < dq4 / 4) part = mfma4(dnreg[kk], lds_ld(Vs, l16 * VP + wave * dq4 + 4 * kk + g), part);
 #pragma unroll
         for (int j = 0; j < 4; ++j) Pr[(wave * kBT + 4 * g + j) * kBT + l16] = part[j];
         __syncthreads();
@@ -616,7 +651,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
             const float a = Op[l16 * kTP + 4 * kk + g];
 #pragma unroll
             for (int c = 0; c < NK; ++c)
-                if (c < nkt) accQ[c] = mfma4(a, Ks[(4 * kk + g) * KP + kc0 + 16 * c + l16], accQ[c]);
+                if (c < nkt) accQ[c] = mfma4(a, lds_ld(Ks, (4 * kk + g) * KP + kc0 + 16 * c + l16), accQ[c]);
         }
     }
 #pragma unroll
@@ -630,14 +665,18 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     }
 }
 
+// With bf16 inputs three workgroups fit a CU's LDS; the register budget is capped to match (a few
+// registers spill, and it is still faster than two workgroups).  fp32 tiles allow two.
+template <typename TIn> constexpr int col_waves() { return sizeof(TIn) == 2 ? 3 : 2; }
 template <typename TIn, int NK, int NV>   // DQK = 64 NK, DV = 64 NV
-__global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
+__global__ void __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(col_waves<TIn>())))
+bwd_col_mfma_kernel(BwdArgs A) {
     extern __shared__ float sm[];
     constexpr int DQK = 64 * NK, DV = 64 * NV;
     const int T = A.T;
-    constexpr int KP = DQK + 4, VP = DV + 4;
-    float* Qs = sm;                      // [kBT][KP] a tile of q^
-    float* dN = Qs + kBT * KP;           // [kBT][VP] a tile of dN~
+    constexpr int KP = DQK + lds_pad<TIn>(), VP = DV + 4;
+    TIn* Qs = reinterpret_cast<TIn*>(sm);                // [kBT][KP] a tile of q (unscaled)
+    float* dN = reinterpret_cast<float*>(Qs + kBT * KP); // [kBT][VP] a tile of dN~
     float* Ps = dN + kBT * VP;           // [4][kBT][kBT] partial S
     float* Pu = Ps + 4 * kBT * kBT;      // [4][kBT][kBT] partial U
     float* Wt = Pu + 4 * kBT * kBT;      // [kBT][kTP] W^T (rows s)
@@ -683,7 +722,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
     for (int tt = s0 / kBT; tt < ntile; ++tt) {
         const int t0 = tt * kBT;
         __syncthreads();
-        stage_rows<TIn, DQK>(Qs, KP, q, t0, T, DQK, qscale, tid);
+        stage_raw<TIn, DQK>(Qs, KP, q, t0, T, DQK, tid);
         stage_rows_f32<DV>(dN, VP, dNw, t0, T, DV, tid);
         if (tid < kBT) {
             const int t = t0 + tid;
@@ -694,13 +733,13 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
         f32x4_t ps = f32x4_t{0.f, 0.f, 0.f, 0.f}, pu = f32x4_t{0.f, 0.f, 0.f, 0.f};   // S[t][s], U[t][s]
 #pragma unroll
         for (int kk = 0; kk < (4 * NK); ++kk)
-            if (kk < kq / 4) ps = mfma4(Qs[l16 * KP + wave * kq + 4 * kk + g], kreg[kk], ps);
+            if (kk < kq / 4) ps = mfma4(lds_ld(Qs, l16 * KP + wave * kq + 4 * kk + g), kreg[kk], ps);
 #pragma unroll
         for (int kk = 0; kk < (4 * NV); ++kk)
             if (kk < dq4 / 4) pu = mfma4(dN[l16 * VP + wave * dq4 + 4 * kk + g], vreg[kk], pu);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            Ps[(wave * kBT + 4 * g + j) * kBT + l16] = ps[j];
+            Ps[(wave * kBT + 4 * g + j) * kBT + l16] = ps[j] * qscale;
             Pu[(wave * kBT + 4 * g + j) * kBT + l16] = pu[j];
         }
         __syncthreads();
@@ -729,7 +768,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
             const float aa = At[l16 * kTP + 4 * kk + g];
 #pragma unroll
             for (int c = 0; c < NK; ++c)
-                if (c < nkt) accK[c] = mfma4(aw, Qs[(4 * kk + g) * KP + kc0 + 16 * c + l16], accK[c]);
+                if (c < nkt) accK[c] = mfma4(aw, lds_ld(Qs, (4 * kk + g) * KP + kc0 + 16 * c + l16), accK[c]);
 #pragma unroll
             for (int c = 0; c < NV; ++c)
                 if (c < nvt) accV[c] = mfma4(aa, dN[(4 * kk + g) * VP + vc0 + 16 * c + l16], accV[c]);
@@ -741,7 +780,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_col_mfma_kernel(BwdArgs A) {
         if (s < T) {
 #pragma unroll
             for (int c = 0; c < NK; ++c)
-                if (c < nkt) A.dk[(seq * T + s) * DQK + kc0 + 16 * c + l16] = accK[c][j];
+                if (c < nkt) A.dk[(seq * T + s) * DQK + kc0 + 16 * c + l16] = accK[c][j] * qscale;
 #pragma unroll
             for (int c = 0; c < NV; ++c)
                 if (c < nvt) A.dv[(seq * T + s) * DV + vc0 + 16 * c + l16] = accV[c][j];
@@ -776,11 +815,15 @@ __global__ void bwd_forget_kernel(BwdArgs A, int S) {
     }
 }
 
+template <typename TIn>
 size_t row_mfma_lds(int DQK, int DV) {
-    return sizeof(float) * (kBT * (DQK + 4) + kBT * (DV + 4) + 4 * kBT * kBT + kBT * kTP + 4 * kBT * kBT + 4 * kBT);
+    return sizeof(TIn) * (kBT * (DQK + lds_pad<TIn>()) + kBT * (DV + lds_pad<TIn>())) +
+           sizeof(float) * (4 * kBT * kBT + kBT * kTP + 4 * kBT * kBT + 4 * kBT);
 }
+template <typename TIn>
 size_t col_mfma_lds(int DQK, int DV) {
-    return sizeof(float) * (kBT * (DQK + 4) + kBT * (DV + 4) + 8 * kBT * kBT + 2 * kBT * kTP + kBT * kBT + 2 * kBT);
+    return sizeof(TIn) * kBT * (DQK + lds_pad<TIn>()) +
+           sizeof(float) * (kBT * (DV + 4) + 8 * kBT * kBT + 2 * kBT * kTP + kBT * kBT + 2 * kBT);
 }
 size_t row_lds(int DQK, int DV) {
     return sizeof(float) * (2 * kBT * (DQK + 1) + 2 * kBT * (DV + 1) + 2 * kBT * kBT + 4 * kBT);
@@ -793,7 +836,7 @@ size_t col_lds(int DQK, int DV) {
 template <typename TIn, int NK, int NV>
 hipError_t launch_mfma_passes(const BwdArgs& a, dim3 tiles, hipStream_t stream) {
     static std::atomic<uint64_t> raised_row{0}, raised_col{0};
-    const size_t lr = row_mfma_lds(64 * NK, 64 * NV), lc = col_mfma_lds(64 * NK, 64 * NV);
+    const size_t lr = row_mfma_lds<TIn>(64 * NK, 64 * NV), lc = col_mfma_lds<TIn>(64 * NK, 64 * NV);
     hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_row_mfma_kernel<TIn, NK, NV>), lr, raised_row);
     if (e == hipSuccess)
         e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_col_mfma_kernel<TIn, NK, NV>), lc, raised_col);

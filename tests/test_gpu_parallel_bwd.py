@@ -8,7 +8,8 @@ Bars, per (batch, head) slice of each gradient: max relative error <= 1e-4 for f
 over up to T pair terms, and the two nearly cancel, so fp32 rounding of order T 2^-24 on each is
 amplified by that cancellation (1e-5 is reached at T = 64 with short memory).  Covers ragged T (not a
 multiple of the 16-token tile), one token, the floor branch and short memory, on both the VALU
-passes (DQK or DV not a multiple of 64) and the MFMA passes."""
+passes (DQK or DV not a multiple of 64) and the MFMA passes, and the benchmarked shape (8 heads,
+T = 2048) with sampled heads."""
 import numpy as np
 import pytest
 import torch
@@ -124,3 +125,17 @@ def test_autograd_cell_gradients(dtype, DQK, DV):
     ref = G.recurrent_grad(q, k, v, ip, fp, wr)
     ref = [r.reshape(r.shape[0], r.shape[1], -1) for r in ref]
     compare(got, ref, TOL_BWD_F32 if dtype == "f32" else TOL_BF16, f"autograd cell {dtype}")
+
+
+def test_parallel_bwd_full_size_sampled_heads():
+    """The benchmarked backward shape (8 heads of 256 x 512, T = 2048, bf16) in one call; two
+    heads are checked against the closed-form oracle run on those heads alone."""
+    B, NH, T, DQK, DV = 1, 8, 2048, 256, 512
+    q, k, v, ip, fp, dh = draw(330, B, NH, T, DQK, DV, "bf16")
+    got = run(B, NH, q, k, v, ip, fp, dh, "bf16")
+    for h in (0, 5):
+        sl = slice(h, h + 1)
+        ref = G.parallel_grad(q[sl], k[sl], v[sl], ip[sl], fp[sl], dh[sl])
+        ref = [r.reshape(1, T, -1) for r in ref]
+        compare([g[sl] for g in got], ref, TOL_BF16, f"T{T} head {h}")
+    assert all(np.isfinite(g).all() for g in got)

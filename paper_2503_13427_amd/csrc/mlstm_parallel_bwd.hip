@@ -73,6 +73,8 @@ __device__ __forceinline__ float wave_scan_max(float x, int lane) {
     }
     return x;
 }
+constexpr int kScanBatch = 8;   // 64-token steps of a scan whose loads are issued together
+
 // one wave per sequence, 64 tokens per step: b, x = i~ - b, M = max(0, prefix max of x), m = b + M
 __global__ void bwd_gate_kernel(BwdArgs A, int S) {
     const int s = blockIdx.x;
@@ -85,19 +87,38 @@ __global__ void bwd_gate_kernel(BwdArgs A, int S) {
     const float* ib = A.ipre + static_cast<int64_t>(s) * T;
     const float* fb = A.fpre + static_cast<int64_t>(s) * T;
     float b_carry = 0.0f, p_carry = 0.0f;
-    for (int t0 = 0; t0 < T; t0 += 64) {
-        const int t = t0 + lane;
-        const bool ok = t < T;
-        const float b = b_carry + wave_scan_sum(ok ? logsigmoid(fb[t]) : 0.0f, lane);
-        const float xv = ok ? ib[t] - b : -INFINITY;
-        const float p = fmaxf(p_carry, wave_scan_max(xv, lane));
-        if (ok) {
-            x[t] = xv;
-            M[t] = p;
-            m[t] = b + p;
+    for (int tb = 0; tb < T; tb += 64 * kScanBatch) {
+        float fv[kScanBatch], iv[kScanBatch];
+#pragma unroll
+        for (int u = 0; u < kScanBatch; ++u) {
+            const int t = tb + 64 * u + lane;
+            fv[u] = t < T ? fb[t] : 0.0f;
+            iv[u] = t < T ? ib[t] : 0.0f;
         }
-        b_carry = __shfl(b, 63, 64);
-        p_carry = __shfl(p, 63, 64);
+        // the sum scans of the batch do not depend on one another: run them first, then add the
+        // carries in order (the same roundings as one scan after another)
+        float ls[kScanBatch], lt[kScanBatch];
+#pragma unroll
+        for (int u = 0; u < kScanBatch; ++u) {
+            const int t = tb + 64 * u + lane;
+            ls[u] = wave_scan_sum(t < T ? logsigmoid(fv[u]) : 0.0f, lane);
+            lt[u] = __shfl(ls[u], 63, 64);
+        }
+#pragma unroll
+        for (int u = 0; u < kScanBatch; ++u) {
+            const int t = tb + 64 * u + lane;
+            const bool ok = t < T;
+            const float b = b_carry + ls[u];
+            const float xv = ok ? iv[u] - b : -INFINITY;
+            const float p = fmaxf(p_carry, wave_scan_max(xv, lane));
+            if (ok) {
+                x[t] = xv;
+                M[t] = p;
+                m[t] = b + p;
+            }
+            b_carry += lt[u];
+            p_carry = __shfl(p, 63, 64);
+        }
     }
 }
 
@@ -806,12 +827,26 @@ __global__ void bwd_forget_kernel(BwdArgs A, int S) {
     const float* fb = A.fpre + static_cast<int64_t>(s) * T;
     float* df = A.dfpre + static_cast<int64_t>(s) * T;
     float carry = 0.0f;
-    for (int e0 = T - 1; e0 >= 0; e0 -= 64) {
-        const int j = e0 - lane;
-        const bool ok = j >= 0;
-        const float acc = carry + wave_scan_sum(ok ? Pw[j] - di[j] : 0.0f, lane);
-        if (ok) df[j] = acc / (1.0f + expf(fb[j]));   // sigmoid(-f~)
-        carry = __shfl(acc, 63, 64);
+    for (int eb = T - 1; eb >= 0; eb -= 64 * kScanBatch) {
+        float pv[kScanBatch], fv[kScanBatch];
+#pragma unroll
+        for (int u = 0; u < kScanBatch; ++u) {
+            const int j = eb - 64 * u - lane;
+            pv[u] = j >= 0 ? Pw[j] - di[j] : 0.0f;
+            fv[u] = j >= 0 ? fb[j] : 0.0f;
+        }
+        float ls[kScanBatch], lt[kScanBatch];   // independent scans first, then the carries in order
+#pragma unroll
+        for (int u = 0; u < kScanBatch; ++u) {
+            ls[u] = wave_scan_sum(pv[u], lane);
+            lt[u] = __shfl(ls[u], 63, 64);
+        }
+#pragma unroll
+        for (int u = 0; u < kScanBatch; ++u) {
+            const int j = eb - 64 * u - lane;
+            if (j >= 0) df[j] = (carry + ls[u]) / (1.0f + expf(fv[u]));   // sigmoid(-f~)
+            carry += lt[u];
+        }
     }
 }
 

@@ -41,6 +41,7 @@
 #define LIBMLSTM_MLSTM_H
 
 #include <stddef.h>
+#include <stdint.h>
 
 #ifdef __cplusplus
 extern "C" {
@@ -161,6 +162,27 @@ typedef enum {
 mlstm_status mlstm_output_norm(const void* h_tilde, const void* o_pre, mlstm_dtype dt,
                                const float* weight, const float* bias, float eps, mlstm_norm norm,
                                int B, int NH, int T, int DV, void* h, void* hip_stream);
+
+/*
+ * The same output (Eq. 6 with the output gate of Eq. 9) in the token-major
+ * layouts of a layer's projections, so that neither o~ nor the result needs a
+ * head-major copy:
+ *
+ *   h_tilde [B, NH, T, DV] (dt)        the cell output, head-major
+ *   o_pre   row (b, h, t) at element (b T + t) o_token_stride + h DV: the
+ *           o~ columns of a token-major projection output (o_token_stride is
+ *           its row length in elements, >= NH DV, a multiple of 4)
+ *   y       [B, T, NH, DV] (dt)        token-major, the input layout of the
+ *           output projection
+ *
+ * Same arithmetic, norms, limits and errors as mlstm_output_norm; y may not
+ * overlap any input (MLSTM_ERR_ALIAS), and a bad o_token_stride is
+ * MLSTM_ERR_BAD_SHAPE.
+ */
+mlstm_status mlstm_output_norm_tokens(const void* h_tilde, const void* o_pre, int64_t o_token_stride,
+                                      mlstm_dtype dt, const float* weight, const float* bias, float eps,
+                                      mlstm_norm norm, int B, int NH, int T, int DV, void* y,
+                                      void* hip_stream);
 
 /*
  * Gate pre-activations of an mLSTM layer, the inputs ipre and fpre of the two

@@ -42,6 +42,9 @@ lib.mlstm_step.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _
 lib.mlstm_step.restype = _i
 lib.mlstm_output_norm.argtypes = [_vp, _vp, _i, _vp, _vp, ctypes.c_float, _i, _i, _i, _i, _i, _vp, _vp]
 lib.mlstm_output_norm.restype = _i
+lib.mlstm_output_norm_tokens.argtypes = [_vp, _vp, ctypes.c_int64, _i, _vp, _vp, ctypes.c_float, _i, _i, _i, _i,
+                                         _i, _vp, _vp]
+lib.mlstm_output_norm_tokens.restype = _i
 lib.mlstm_gate_preact.argtypes = [_vp, _i, _vp, _vp, ctypes.c_float, _vp, _i, _i, _i, _i, _vp, _vp, _vp]
 lib.mlstm_gate_preact.restype = _i
 lib.mlstm_parallel_bwd_workspace_bytes.argtypes = [_i, _i, _i, _i]
@@ -140,6 +143,23 @@ def mlstm_output_norm(h_tilde, o_pre, weight, bias, eps: float, norm: str, h, st
     code = {"layer": MLSTM_NORM_LAYER, "rms": MLSTM_NORM_RMS}[norm]
     _check(lib.mlstm_output_norm(_ptr(h_tilde), _ptr(o_pre), _dtype_code(h_tilde), _ptr(weight), _ptr(bias),
                                  float(eps), code, B, NH, T, DV, _ptr(h), _stream(stream)))
+
+
+def mlstm_output_norm_tokens(h_tilde, o_pre, weight, bias, eps: float, norm: str, y, stream=None) -> None:
+    """The output norm in token-major layouts: h_tilde [B, NH, T, DV] head-major, o_pre a
+    [B, T, NH, DV] view whose tokens are ``o_pre.stride(1)`` elements apart (columns of a
+    projection output), y [B, T, NH, DV] contiguous."""
+    B, NH, T, DV = h_tilde.shape
+    if tuple(o_pre.shape) != (B, T, NH, DV) or o_pre.stride(3) != 1 or o_pre.stride(2) != DV or \
+            (B > 1 and o_pre.stride(0) != T * o_pre.stride(1)):
+        raise ValueError("o_pre must be a [B, T, NH, DV] view with contiguous heads and evenly spaced tokens")
+    if tuple(y.shape) != (B, T, NH, DV) or not y.is_contiguous():
+        raise ValueError("y must be a contiguous [B, T, NH, DV] tensor")
+    code = {"layer": MLSTM_NORM_LAYER, "rms": MLSTM_NORM_RMS}[norm]
+    # o_pre is a strided view by design: its layout was checked above, so its pointer is taken as is
+    _check(lib.mlstm_output_norm_tokens(_ptr(h_tilde), o_pre.data_ptr(), o_pre.stride(1), _dtype_code(h_tilde),
+                                        _ptr(weight), _ptr(bias), float(eps), code, B, NH, T, DV, _ptr(y),
+                                        _stream(stream)))
 
 
 def mlstm_gate_preact(x, w_t, bias, cap: float, border, ipre, fpre, stream=None) -> None:

@@ -34,8 +34,13 @@ size_t step_lds_bytes(int DQK, int DV);
 
 // --- hidden-state output: output gate and headwise norm ----------------------
 constexpr int kOutNormMaxDV = 2048;
+// element offset of row (b, head, t) is b * b + head * h + t * t; a row is DV contiguous elements
+struct RowStrides {
+    int64_t b, h, t;
+};
 hipError_t launch_output_norm(mlstm_dtype dt, const void* h_tilde, const void* o_pre, const float* weight,
                               const float* bias, float eps, int rms, int64_t rows, int NH, int T, int DV, void* h,
+                              RowStrides so, RowStrides sy,
                               hipStream_t stream);
 
 // --- gate pre-activations of a layer (bf16 x, W^T [2 NH, d]) -----------------

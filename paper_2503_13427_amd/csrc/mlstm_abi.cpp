@@ -184,8 +184,41 @@ mlstm_status mlstm_output_norm(const void* h_tilde, const void* o_pre, mlstm_dty
     if ((overlap(rh, rx) && h != h_tilde) || overlap(rh, ro) || overlap(rh, rw) || overlap(rh, rb))
         return MLSTM_ERR_ALIAS;
     if (rows == 0) return MLSTM_OK;
+    const mlstm::RowStrides hm{static_cast<int64_t>(NH) * T * DV, static_cast<int64_t>(T) * DV, DV};
     hipError_t e = mlstm::launch_output_norm(dt, h_tilde, o_pre, weight, bias, eps, norm == MLSTM_NORM_RMS, rows, NH,
-                                             T, DV, h, static_cast<hipStream_t>(hip_stream));
+                                             T, DV, h, hm, hm, static_cast<hipStream_t>(hip_stream));
+    return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
+mlstm_status mlstm_output_norm_tokens(const void* h_tilde, const void* o_pre, int64_t o_token_stride, mlstm_dtype dt,
+                                      const float* weight, const float* bias, float eps, mlstm_norm norm, int B,
+                                      int NH, int T, int DV, void* y, void* hip_stream) {
+    if (T != 0 && (!h_tilde || !o_pre || !y)) return MLSTM_ERR_NULL_PTR;
+    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (B <= 0 || NH <= 0 || T < 0 || DV <= 0) return MLSTM_ERR_BAD_SHAPE;
+    if (!(eps > 0.0f) || eps > 3.0e38f) return MLSTM_ERR_BAD_SHAPE;
+    if (norm != MLSTM_NORM_LAYER && norm != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
+    if ((DV % 4) || DV > mlstm::kOutNormMaxDV) return MLSTM_ERR_UNSUPPORTED;
+    int64_t S, rows, nel, nw, toks, ospan;
+    if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &rows) || !mul_ok(rows, DV, &nel) || !mul_ok(NH, DV, &nw) ||
+        !mul_ok(B, T, &toks) || rows / 4 >= INT32_MAX)
+        return MLSTM_ERR_BAD_SHAPE;
+    // o~ rows of one token may not overlap one another; the stride keeps rows DV-aligned like the others
+    if (o_token_stride < nw || o_token_stride % 4) return MLSTM_ERR_BAD_SHAPE;
+    if (toks > 0 && (!mul_ok(toks - 1, o_token_stride, &ospan) || ospan > INT64_MAX - nw)) return MLSTM_ERR_BAD_SHAPE;
+    const void* ptrs[] = {h_tilde, o_pre, weight, bias, y};
+    for (const void* p : ptrs)
+        if (misaligned(p)) return MLSTM_ERR_MISALIGNED;
+    const size_t eb = elem_bytes(dt);
+    const int64_t oel = toks > 0 ? ospan + nw : 0;
+    const Range rx = range_of(h_tilde, nel * eb), ro = range_of(o_pre, oel * eb), ry = range_of(y, nel * eb);
+    const Range rw = range_of(weight, weight ? nw * 4 : 0), rb = range_of(bias, bias ? nw * 4 : 0);
+    if (overlap(ry, rx) || overlap(ry, ro) || overlap(ry, rw) || overlap(ry, rb)) return MLSTM_ERR_ALIAS;
+    if (rows == 0) return MLSTM_OK;
+    const mlstm::RowStrides so{static_cast<int64_t>(T) * o_token_stride, DV, o_token_stride};
+    const mlstm::RowStrides sy{static_cast<int64_t>(T) * NH * DV, DV, static_cast<int64_t>(NH) * DV};
+    hipError_t e = mlstm::launch_output_norm(dt, h_tilde, o_pre, weight, bias, eps, norm == MLSTM_NORM_RMS, rows, NH,
+                                             T, DV, y, so, sy, static_cast<hipStream_t>(hip_stream));
     return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
 }
 

@@ -87,15 +87,17 @@ template <typename TIn, int NS>
 __global__ void __launch_bounds__(kNormThreads)
 output_norm_kernel(const TIn* ht, const TIn* __restrict__ op, const float* __restrict__ weight,
                    const float* __restrict__ bias, float eps, int rms, int64_t rows, int NH, int T, int DV,
-                   TIn* h) {
+                   TIn* h, RowStrides so, RowStrides sy) {
     const int lane = threadIdx.x & 63;
     const int64_t row = static_cast<int64_t>(blockIdx.x) * (kNormThreads / 64) + (threadIdx.x >> 6);
     if (row >= rows) return;   // whole waves; the kernel has no barrier
-    const int head = static_cast<int>((row / T) % NH);
+    const int64_t bh = row / T, t = row - bh * T;
+    const int64_t bb = bh / NH;
+    const int head = static_cast<int>(bh - bb * NH);
     const int ng = DV / 4;
     const TIn* x = ht + row * DV;
-    const TIn* o = op + row * DV;
-    TIn* y = h + row * DV;
+    const TIn* o = op + bb * so.b + head * so.h + t * so.t;
+    TIn* y = h + bb * sy.b + head * sy.h + t * sy.t;
 
     // both rows are requested before the reductions, so their latencies overlap
     float v[NS][8], og[NS][8];
@@ -168,7 +170,7 @@ output_norm_kernel(const TIn* ht, const TIn* __restrict__ op, const float* __res
 
 hipError_t launch_output_norm(mlstm_dtype dt, const void* h_tilde, const void* o_pre, const float* weight,
                               const float* bias, float eps, int rms, int64_t rows, int NH, int T, int DV, void* h,
-                              hipStream_t stream) {
+                              RowStrides so, RowStrides sy, hipStream_t stream) {
     constexpr int rpb = kNormThreads / 64;
     const dim3 grid(static_cast<unsigned>((rows + rpb - 1) / rpb));
     const int need = (DV + 511) / 512;
@@ -176,7 +178,7 @@ hipError_t launch_output_norm(mlstm_dtype dt, const void* h_tilde, const void* o
         using T_ = decltype(tag);
         hipLaunchKernelGGL((output_norm_kernel<T_, decltype(ns)::value>), grid, dim3(kNormThreads), 0, stream,
                            static_cast<const T_*>(h_tilde), static_cast<const T_*>(o_pre), weight, bias, eps, rms, rows,
-                           NH, T, DV, static_cast<T_*>(h));
+                           NH, T, DV, static_cast<T_*>(h), so, sy);
     };
     auto by_width = [&](auto tag) {
         if (need <= 1) go(tag, std::integral_constant<int, 1>{});

@@ -25,7 +25,7 @@ def declared_functions():
 
 def test_header_declares_expected_entry_points():
     assert declared_functions() == sorted(["mlstm_chunkwise_fwd", "mlstm_chunkwise_workspace_bytes", "mlstm_step",
-                                           "mlstm_output_norm", "mlstm_gate_preact", "mlstm_parallel_bwd",
+                                           "mlstm_output_norm", "mlstm_output_norm_tokens", "mlstm_gate_preact", "mlstm_parallel_bwd",
                                            "mlstm_parallel_bwd_workspace_bytes", "mlstm_status_string",
                                            "mlstm_version"])
 
@@ -212,6 +212,53 @@ def test_norm_misaligned(field):
     a = norm_args()
     a[field] += 8
     assert call_norm(a) == 4
+
+
+# ---- the token-major output norm: the same checks plus the o~ token stride -----------------------
+
+def call_norm_tokens(a, stride=None):
+    ostride = 4 * a["NH"] * a["DV"] if stride is None else stride
+    return lib.mlstm_output_norm_tokens(a["x"], a["o"], ostride, a["dt"], a["w"], a["b"], a["eps"], a["norm"],
+                                        a["B"], a["NH"], a["T"], a["DV"], a["h"], a["stream"])
+
+
+@pytest.mark.parametrize("field", ["x", "o", "h"])
+def test_norm_tokens_null_pointer(field):
+    assert call_norm_tokens(norm_args(**{field: None})) == 1
+
+
+def test_norm_tokens_empty_rows_is_ok_without_pointers():
+    assert call_norm_tokens(norm_args(T=0, x=None, o=None, h=None)) == 0
+
+
+@pytest.mark.parametrize("over", [dict(B=0), dict(NH=-1), dict(DV=0), dict(eps=0.0), dict(norm=2)])
+def test_norm_tokens_bad_shape(over):
+    assert call_norm_tokens(norm_args(**over)) == 2
+
+
+@pytest.mark.parametrize("stride", [8 * 512 - 4, 8 * 512 + 2, -4, 0])
+def test_norm_tokens_bad_stride(stride):
+    # the o~ rows of one token would overlap, or rows would lose their 4-element alignment
+    assert call_norm_tokens(norm_args(), stride) == 2
+
+
+@pytest.mark.parametrize("over", [dict(dt=3), dict(DV=6), dict(DV=4096)])
+def test_norm_tokens_unsupported(over):
+    assert call_norm_tokens(norm_args(**over)) == 3
+
+
+@pytest.mark.parametrize("field", ["x", "o", "w", "b", "h"])
+def test_norm_tokens_misaligned(field):
+    a = norm_args()
+    a[field] += 8
+    assert call_norm_tokens(a) == 4
+
+
+def test_norm_tokens_output_may_not_overlap_inputs():
+    # unlike the head-major call, y may not be h~ itself: the two layouts differ
+    a = norm_args()
+    a["h"] = a["x"]
+    assert call_norm_tokens(a) == 5
 
 
 @pytest.mark.parametrize("inp,off", [("x", 16), ("o", 0), ("o", 4096), ("w", 0), ("b", 16)])

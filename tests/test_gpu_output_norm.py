@@ -66,6 +66,39 @@ def test_output_norm_matches_oracle(case):
     assert err <= (TOL_F32 if dt == "f32" else TOL_BF16), err
 
 
+TOKEN_CASES = [
+    # (B, NH, T, DV, dtype, norm, affine, extra columns per projection row)
+    (2, 8, 64, 512, "bf16", "layer", True, 8 * (2 * 256 + 512)),
+    (3, 2, 33, 512, "bf16", "rms", False, 8),   # base 16-byte aligned, rows 8-byte aligned
+    (1, 3, 17, 2048, "f32", "layer", True, 0),
+    (2, 4, 9, 64, "f32", "rms", True, 12),
+]
+
+
+@pytest.mark.parametrize("case", TOKEN_CASES, ids=lambda c: "B{}NH{}T{}DV{}-{}-{}-{}-pad{}".format(*c))
+def test_output_norm_tokens_matches_oracle(case):
+    """o~ as columns of a wider token-major projection output, y token-major: element by element
+    the same result as the head-major oracle, transposed."""
+    B, NH, T, DV, dt, norm, affine, pad = case
+    xt, ot, w, b = _inputs(300 + TOKEN_CASES.index(case), B, NH, T, DV, dt, affine)
+    P = torch.full((B * T, pad + NH * DV + 4), 7.0, dtype=xt.dtype, device="cuda")
+    o_view = P[:, pad:pad + NH * DV].view(B, T, NH, DV)
+    o_view.copy_(ot.transpose(1, 2))
+    y = torch.full((B, T, NH, DV + 0), -5.0, dtype=xt.dtype, device="cuda")
+    eps = 1e-6 if dt == "f32" else 1e-5
+    _mb().mlstm_output_norm_tokens(xt, o_view, w, b, eps, norm, y)
+    torch.cuda.synchronize()
+    ref = _oracle(xt, ot, w, b, eps, norm).transpose(0, 2, 1, 3)
+    err = rel_err(host_f64(y), ref, 2)
+    print(case, f"{err:.3e}")
+    assert err <= (TOL_F32 if dt == "f32" else TOL_BF16), err
+    # the head-major call on the same rows gives the same bits
+    h = torch.empty_like(xt)
+    _mb().mlstm_output_norm(xt, ot, w, b, eps, norm, h)
+    torch.cuda.synchronize()
+    assert torch.equal(h.transpose(1, 2), y)
+
+
 def test_decode_shape_and_in_place():
     xt, ot, w, b = _inputs(7, 256, 8, 1, 512, "bf16", True)
     x3, o3 = xt[:, :, 0].contiguous(), ot[:, :, 0].contiguous()

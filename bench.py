@@ -293,17 +293,23 @@ def bench_layer_prefill(layer, B, T, steps, stream):
     x2 = x.reshape(B * T, d)
     t_proj = run(lambda: layer._project(x2))
     t_gates = run(lambda: layer.gates(x))
-    t_heads = run(lambda: layer.project_heads(x)) - t_proj - t_gates
-    q, k, v, o, ig, fg = layer.project_heads(x)
+    # the stages as the prefill runs them: head-major copies of q, k, v; o~ read in place by the norm
+    q4, k4, v4, o4 = layer._project(x2)
+    hm = lambda a, D: a.view(B, T, NH, D).transpose(1, 2).contiguous()
+    t_heads = run(lambda: (hm(q4, DQK), hm(k4, DQK), hm(v4, DV)))
+    q, k, v = hm(q4, DQK), hm(k4, DQK), hm(v4, DV)
+    ig, fg = layer.gates(x)
     h = torch.empty(B, NH, T, DV, dtype=torch.bfloat16, device="cuda")
     C = torch.empty(B, NH, DQK, DV, device="cuda")
     n = torch.empty(B, NH, DQK, device="cuda")
     m = torch.empty(B, NH, device="cuda")
     t_cell = run(lambda: mb.mlstm_chunkwise_fwd(q, k, v, ig, fg, None, None, None, layer.L, h, C, n, m,
                                                  workspace=ws, stream=stream))
-    hn = torch.empty_like(h)
-    t_norm = run(lambda: mb.mlstm_output_norm(h, o, w.norm_weight, None, layer.eps, "layer", hn, stream=stream))
-    t_out = run(lambda: torch.matmul(hn.transpose(1, 2).reshape(B * T, NH * DV), w.W_proj))
+    yh = torch.empty(B, T, NH, DV, dtype=torch.bfloat16, device="cuda")
+    o_view = o4.view(B, T, NH, DV)
+    t_norm = run(lambda: mb.mlstm_output_norm_tokens(h, o_view, w.norm_weight, None, layer.eps, "layer", yh,
+                                                     stream=stream))
+    t_out = run(lambda: torch.matmul(yh.view(B * T, NH * DV), w.W_proj))
     tok = B * T
     fl_proj = acc.flops_layer_projections(tok, d, NH, DQK, DV)
     fl_cell = acc.flops_chunkwise(B * NH, T, layer.L, DQK, DV).total

@@ -1,37 +1,45 @@
 #!/usr/bin/env python3
 """Benchmark of libmlstm on one MI355X: prefill tokens/s (%MFMA) and decode step us (%HBM).
 
-One JSON line on stdout.  The headline ``value`` is the chunkwise prefill of
-the xLSTM-7B-shaped workload B=1, NH=8, T=2048, DQK=256, DV=512, L=64 (bf16
-q/k/v, fp32 gates and state, zero initial state): one "step" is one
-mlstm_chunkwise_fwd call over that batch, all of its kernels included.
-Inputs are seeded synthetic data already resident in HBM; NINPUT copies are
-rotated so consecutive steps do not hit a warm Infinity Cache.
+One JSON line on stdout.  The headline ``value`` is the chunkwise prefill of the
+largest xLSTM-7B-shaped workload, the continued prefill B=4, NH=8, T=32768,
+DQK=256, DV=512, L=128 from a nonzero fp32 initial state (bf16 q/k/v, fp32 gates
+soft-capped at 15, fp32 state): one "step" is one mlstm_chunkwise_fwd call over
+that batch, all of its kernels included.  Inputs are seeded synthetic data
+already resident in HBM (the working set, 3.3 GB, is far beyond the 256 MB
+Infinity Cache).  Every timed call is bracketed by HIP events on the launch
+stream: ``ms_per_step`` is the mean over the K timed calls, and the median,
+p10 and p90 of the per-call times are reported beside it.
 
 Extra objects on the same line:
-  roofline      achieved bf16 TFLOP/s (App. D.1 FLOP count per call / call
-                duration from HIP events on the launch stream) vs 2.5 PFLOP/s;
-  cpu_baseline  the fp64 CPU oracle on the same workload (host cores);
+  roofline      achieved bf16 TFLOP/s (App. D.1 FLOP count per call / mean call
+                duration) vs 2.5 PFLOP/s, and the HBM bytes per call from the
+                committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary;
+  cpu_baseline  the fp64 CPU oracle on a sample of the same workload (host
+                cores), plus every other workload and a 1-thread run;
+  prefill_other the two other prefill workloads (B=1 x T=2048, L=64, with rotated
+                input copies and warm-cache figure; B=8 x T=8192 soft-capped, L=64),
+                each >= 20 calls with median, p10, p90;
   decode        1024 consecutive mlstm_step calls at B=256, NH=8: us per step,
                 us per sequence-token, achieved GB/s vs 8 TB/s;
   decode_b1     mlstm_step at B=1, NH=8 (single-sequence generation), in place;
-  prefill_large the two larger prefill workloads (B=8 x T=8192 soft-capped,
-                and B=4 x T=32768 from a nonzero state, L=128);
   output_norm   the hidden-state output h = sigmoid(o~) * LayerNorm(h~) w + b
-                (mlstm_output_norm) on the headline prefill's h shape and the
+                (mlstm_output_norm) on the T=2048 prefill's h shape and the
                 decode step's h shape: us per call and achieved GB/s vs 8 TB/s;
   layer         one xLSTM-7B-shaped mLSTM layer (d = 4096, random weights): prefill
                 of 65536 tokens as batch x context (1 x 65536, 8 x 8192, 64 x 1024)
                 with the time of each stage, and decode steps at B = 1 and 256,
                 eager and as a captured HIP graph;
-  backward      mlstm_parallel_bwd (training-mode gradients over the parallel form) on
-                the headline prefill shape: ms per call, FLOP/s vs the fp32 VALU peak.
+  backward      the training-mode backward pass on the T=2048 prefill shape;
+  env           GPU, ROCm and torch versions, git commit when available, and a
+                hash of the kernel sources.
 Every timed section is preceded by 0.25 s of untimed calls (clock settle).
 """
 from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -98,8 +106,9 @@ class Prefill:
         return acc.prefill_bytes(w.B, w.NH, w.T, w.DQK, w.DV, with_initial_state=w.state is not None)
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "chunkwise_traffic_B1_NH8_T2048_L64.md")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "chunkwise_traffic_B4_NH8_T32768_L128.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2503_13427_amd", "csrc", "mlstm_chunkwise_mfma.hip")
+CSRC = os.path.join(ROOT, "paper_2503_13427_amd", "csrc")
 
 
 def measured_traffic():
@@ -157,15 +166,33 @@ def time_steps(fn, steps, warmup, stream):
 
 
 def bench_prefill(w, steps, warmup, ninput, stream):
+    """``steps`` calls, each bracketed by HIP events on the launch stream: mean, median, p10 and
+    p90 of the per-call times; the throughput and roofline figures use the mean."""
     p = Prefill(w, ninput)
-    wall, ev = time_steps(lambda: p.step(stream), steps, warmup, stream)
-    t = ev / steps
+    fn = lambda: p.step(stream)
+    settle(fn)
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i].record(stream)
+        fn()
+    ev[steps].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]) / 1e3
+    t = ev[0].elapsed_time(ev[steps]) / 1e3 / steps
     fl = p.flops()
     tok = w.B * w.T
-    out = dict(workload=w.name, tokens_per_s=tok / t, us_per_call=t * 1e6, tflops=fl / t / 1e12,
-               mfma_frac=fl / t / 1e12 / acc.PEAK_BF16_MFMA_TFLOPS, gbs=p.bytes() / t / 1e9,
-               hbm_frac=p.bytes() / t / 1e9 / acc.PEAK_HBM_GBS, wall_s=wall, steps=steps,
-               flops_per_call=fl, bytes_per_call=p.bytes(),
+    out = dict(workload=w.name, tokens_per_s=tok / t, us_per_call=t * 1e6,
+               us_per_call_median=float(np.median(per)) * 1e6, us_per_call_p10=float(np.quantile(per, 0.1)) * 1e6,
+               us_per_call_p90=float(np.quantile(per, 0.9)) * 1e6, tflops=fl / t / 1e12,
+               mfma_frac=fl / t / 1e12 / acc.PEAK_BF16_MFMA_TFLOPS,
+               mfma_frac_median=fl / float(np.median(per)) / 1e12 / acc.PEAK_BF16_MFMA_TFLOPS,
+               gbs=p.bytes() / t / 1e9, hbm_frac=p.bytes() / t / 1e9 / acc.PEAK_HBM_GBS, wall_s=wall, steps=steps,
+               flops_per_call=fl, bytes_per_call=p.bytes(), input_sets=ninput,
                workspace_bytes=0 if p.ws is None else p.ws.numel())
     return out, p
 
@@ -381,40 +408,146 @@ def bench_backward(w, steps, stream):
                 app_d2_flops=fl_d2, app_d2_tflops=fl_d2 / t / 1e12)
 
 
-def cpu_baseline(w, max_seconds=30.0):
-    """The fp64 oracle on the headline workload, timed on the host.  Heads are independent, so
-    the sample is a subset of heads over the full sequence (all heads if they fit the budget)."""
+def cpu_model():
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_prefill(w, heads, threads, T=None):
+    """Seconds the fp64 oracle takes on ``heads`` of workload w (full sequence, or its first T tokens)."""
     from oracle import coracle
-    aff = len(os.sched_getaffinity(0))
-    heads = list(range(w.heads))
-    threads = max(1, min(aff, len(heads), 16))
-    inp = w.prefill_inputs()
+    inp = w.prefill_inputs(heads=heads, T=T)
     t0 = time.perf_counter()
     coracle.recurrent_inputs(inp, nthreads=threads)
-    dt = time.perf_counter() - t0
-    return dict(value=w.B * w.T / dt, unit="tokens/s", cores=threads, kind="oracle",
-                sample=f"full workload {w.name} (all {w.heads} heads x {w.T} tokens), fp64 recurrent form, "
-                       f"{dt:.2f} s wall on {threads} threads", seconds=dt)
+    return time.perf_counter() - t0
+
+
+def _oracle_decode(w, heads, steps, threads):
+    """Seconds the fp64 oracle takes for ``steps`` decode steps of ``heads`` sequences from a state."""
+    from oracle import coracle
+    rng = np.random.default_rng(3)
+    S = len(heads)
+    C = rng.normal(0, 0.1, (S, w.DQK, w.DV))
+    n = np.abs(rng.standard_normal((S, w.DQK)))
+    m = rng.standard_normal(S)
+    dec = w.decode_inputs(steps=steps, heads=heads)
+    args = [dec.as_f64(x)[0] for x in ("q", "k", "v", "ipre", "fpre")]
+    t0 = time.perf_counter()
+    coracle.recurrent(*args, C, n, m, nthreads=threads)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(w):
+    """The fp64 recurrent oracle (the CPU baseline, never tuned) timed on the host.  Heads are
+    independent sequences, so each workload's sample is a subset of its heads over the full
+    sequence; token rates are scaled to whole-workload tokens (B T per call) by the sampled share
+    of the heads.  The headline entry is workload w; ``per_workload`` holds every workload, and the
+    T=2048 prefill is also timed on one thread."""
+    aff = len(os.sched_getaffinity(0))
+    threads = max(1, min(aff, 16))
+
+    def prefill_entry(wl, nheads, nthreads=threads):
+        heads = list(range(min(nheads, wl.heads)))
+        dt = _oracle_prefill(wl, heads, nthreads)
+        share = len(heads) / wl.heads
+        return dict(workload=wl.name, tokens_per_s=wl.B * wl.T * share / dt, seconds=dt, threads=nthreads,
+                    sample=f"{len(heads)} of {wl.heads} heads x {wl.T} tokens")
+
+    log(f"cpu baseline: fp64 oracle on {threads} threads")
+    w2 = configs.PREFILL_T2048
+    first = prefill_entry(w2, 8)
+    # heads for a budget of about ``seconds`` of oracle time, from the T=2048 rate (threads work on
+    # one head each)
+    per_head_token = first["seconds"] / min(8, threads) / w2.T / math.ceil(8 / threads)
+
+    def budget_heads(wl, seconds):
+        rounds = max(1, int(seconds / (per_head_token * wl.T)))
+        return max(1, min(wl.heads, rounds * threads))
+
+    head = prefill_entry(w, budget_heads(w, 12.0))
+    per = [prefill_entry(configs.TINY_F32, 1, 1), first, prefill_entry(w2, 8, 1),
+           prefill_entry(configs.PREFILL_T8192, budget_heads(configs.PREFILL_T8192, 4.0))]
+    dw = configs.DECODE_B256
+    dheads = list(range(2 * threads))
+    dt = _oracle_decode(dw, dheads, dw.steps, threads)
+    us_step = dt / dw.steps * dw.heads / len(dheads) * 1e6
+    per.append(dict(workload=dw.name, us_per_step=us_step, us_per_token=us_step / dw.B, seconds=dt, threads=threads,
+                    sample=f"{len(dheads)} of {dw.heads} heads x {dw.steps} steps, scaled to all heads"))
+    per.append(head)
+    return dict(value=head["tokens_per_s"], unit="tokens/s", cores=threads, kind="oracle",
+                sample=f"{head['sample']} of {w.name} (fp64 recurrent form, {head['seconds']:.2f} s wall); "
+                       "tokens/s scaled to the whole workload by the sampled share of heads",
+                seconds=head["seconds"], cpu_model=cpu_model(), affinity_cpus=aff, per_workload=per)
+
+
+def env_info():
+    """What produced the numbers: GPU, ROCm, torch, git commit (when the tree has one) and a hash of
+    the HIP sources and the built library."""
+    import hashlib
+    import subprocess
+    info = dict(torch=torch.__version__, hip=getattr(torch.version, "hip", None))
+    try:
+        props = torch.cuda.get_device_properties(0)
+        info.update(gpu=props.name, arch=getattr(props, "gcnArchName", None), cus=props.multi_processor_count)
+    except RuntimeError:
+        pass
+    for path in ("/opt/rocm/.info/version", "/opt/rocm/.info/version-dev"):
+        try:
+            info["rocm"] = open(path).read().strip()
+            break
+        except OSError:
+            pass
+    try:
+        r = subprocess.run(["git", "-C", ROOT, "rev-parse", "HEAD"], capture_output=True, text=True, timeout=10)
+        info["git_commit"] = r.stdout.strip() if r.returncode == 0 else None
+    except (OSError, subprocess.SubprocessError):
+        info["git_commit"] = None
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        h.update(name.encode())
+        h.update(open(os.path.join(CSRC, name), "rb").read())
+    info["csrc_sha256_16"] = h.hexdigest()[:16]
+    lib = os.path.join(ROOT, "paper_2503_13427_amd", "libmlstm.so")
+    if os.path.exists(lib):
+        info["libmlstm_sha256_16"] = hashlib.sha256(open(lib, "rb").read()).hexdigest()[:16]
+    return info
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--ninput", type=int, default=8, help="rotated input copies (defeats a warm MALL)")
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--ninput", type=int, default=8, help="rotated input copies of the T=2048 prefill (defeats a "
+                                                            "warm Infinity Cache)")
+    ap.add_argument("--other-steps", type=int, default=50, help="timed calls of each other prefill workload")
     ap.add_argument("--decode-steps", type=int, default=1024)
     ap.add_argument("--skip-decode", action="store_true")
-    ap.add_argument("--skip-large", action="store_true")
+    ap.add_argument("--skip-other", action="store_true")
     ap.add_argument("--skip-output-norm", action="store_true")
     ap.add_argument("--skip-cpu-baseline", action="store_true")
     ap.add_argument("--skip-layer", action="store_true")
     ap.add_argument("--skip-backward", action="store_true")
-    ap.add_argument("--only", choices=["prefill", "decode", "large", "output_norm", "layer", "backward", "calls"],
+    ap.add_argument("--only", choices=["prefill", "other", "decode", "decode_b1", "output_norm", "layer", "backward",
+                                       "calls", "cpu"],
                     default=None,
                     help="run one part only (profiling runs); 'calls' makes --calls untimed prefill calls of "
                          "--workload and then one --copy-mib MiB device copy, for counter runs")
-    ap.add_argument("--workload", default=configs.PREFILL_T2048.name,
+    ap.add_argument("--workload", default=configs.CONT_PREFILL_T32768.name,
                     help="workload name for --only calls")
     ap.add_argument("--calls", type=int, default=3)
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -424,18 +557,34 @@ def main():
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported (every (batch, head) "
               "sequence is independent, so more GPUs would shard B*NH with no exchange)", file=sys.stderr)
         sys.exit(2)
+    if args.only == "cpu":
+        print(json.dumps(cpu_baseline(configs.CONT_PREFILL_T32768)), flush=True)
+        return
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = configs.PREFILL_T2048
+    w = configs.CONT_PREFILL_T32768
 
     if args.only == "calls":
         wl = {x.name: x for x in configs.ALL}[args.workload]
-        p = Prefill(wl, 1)
-        for _ in range(args.calls):
-            p.step(stream)
+        if wl.kind == "decode":
+            # in-place steps of the full decode batch from a random state (counter runs of the step)
+            from paper_2503_13427_amd import binding as mb
+            g = torch.Generator(device="cuda").manual_seed(7)
+            rn = lambda *shape: torch.randn(*shape, generator=g, device="cuda")
+            q, k, v = rn(wl.B, wl.NH, wl.DQK).bfloat16(), rn(wl.B, wl.NH, wl.DQK).bfloat16(), rn(wl.B, wl.NH, wl.DV).bfloat16()
+            ip, fp = rn(wl.B, wl.NH), rn(wl.B, wl.NH) + 3
+            C, n, m = rn(wl.B, wl.NH, wl.DQK, wl.DV) * 0.1, rn(wl.B, wl.NH, wl.DQK).abs(), torch.zeros(wl.B, wl.NH, device="cuda")
+            h = torch.empty(wl.B, wl.NH, wl.DV, dtype=torch.bfloat16, device="cuda")
+            torch.cuda.synchronize()
+            for _ in range(args.calls):
+                mb.mlstm_step(q, k, v, ip, fp, C, n, m, h, C, n, m, stream=stream)
+        else:
+            p = Prefill(wl, 1)
+            for _ in range(args.calls):
+                p.step(stream)
         torch.cuda.synchronize()
         if args.copy_mib:
             src = torch.ones(args.copy_mib * (1 << 18), dtype=torch.float32, device="cuda")
@@ -447,71 +596,70 @@ def main():
 
     res = {}
     if args.only in (None, "prefill"):
-        log(f"prefill {w.name}: {args.warmup} warm-up + {args.steps} timed steps, {args.ninput} rotated inputs")
-        head, p = bench_prefill(w, args.steps, args.warmup, args.ninput, stream)
-        # warm-cache figure for reference: one input set
-        warm, _ = bench_prefill(w, args.steps, args.warmup, 1, stream)
-        head["warm_mall_us_per_call"] = warm["us_per_call"]
-        res["prefill"] = head
+        log(f"prefill {w.name}: {args.warmup} warm-up + {args.steps} timed calls")
+        res["prefill"], p = bench_prefill(w, args.steps, args.warmup, 1, stream)
         del p
-    if args.only in (None, "large") and not args.skip_large:
-        res["prefill_large"] = []
-        for wl, steps in ((configs.PREFILL_T8192, max(3, args.steps // 20)),
-                          (configs.CONT_PREFILL_T32768, max(2, args.steps // 20))):
-            log(f"prefill {wl.name}: {steps} timed steps")
-            r, p = bench_prefill(wl, steps, 2, 1, stream)
-            res["prefill_large"].append(r)
-            del p
-            torch.cuda.empty_cache()
+        torch.cuda.empty_cache()
+    if args.only in (None, "other") and not args.skip_other:
+        res["prefill_other"] = []
+        w2 = configs.PREFILL_T2048
+        log(f"prefill {w2.name}: {args.other_steps} timed calls, {args.ninput} rotated inputs")
+        r, p = bench_prefill(w2, args.other_steps, 5, args.ninput, stream)
+        del p
+        warm, p = bench_prefill(w2, args.other_steps, 5, 1, stream)   # warm-cache figure: one input set
+        del p
+        r["warm_mall_us_per_call_median"] = warm["us_per_call_median"]
+        res["prefill_other"].append(r)
+        w3 = configs.PREFILL_T8192
+        log(f"prefill {w3.name}: {args.other_steps} timed calls")
+        r, p = bench_prefill(w3, args.other_steps, 3, 1, stream)
+        res["prefill_other"].append(r)
+        del p
+        torch.cuda.empty_cache()
     if args.only in (None, "output_norm") and not args.skip_output_norm:
         log("output gate + headwise LayerNorm on the prefill and decode h shapes")
-        res["output_norm"] = [bench_output_norm(w.B, w.NH, w.T, w.DV, args.steps, stream, "prefill_B1_NH8_T2048_DV512"),
-                              bench_output_norm(256, 8, 1, 512, args.steps, stream, "decode_B256_NH8_DV512")]
+        w2 = configs.PREFILL_T2048
+        res["output_norm"] = [bench_output_norm(w2.B, w2.NH, w2.T, w2.DV, 200, stream, "prefill_B1_NH8_T2048_DV512"),
+                              bench_output_norm(256, 8, 1, 512, 200, stream, "decode_B256_NH8_DV512")]
         torch.cuda.empty_cache()
     if args.only in (None, "layer") and not args.skip_layer:
         log("mLSTM layer (projections + cell + output norm + output projection)")
-        res["layer"] = bench_layer(max(3, args.steps // 20), max(50, args.decode_steps // 4), stream)
+        res["layer"] = bench_layer(10, max(50, args.decode_steps // 4), stream)
         torch.cuda.empty_cache()
     if args.only in (None, "backward") and not args.skip_backward:
-        log(f"backward over the parallel form, {w.name}")
-        res["backward"] = bench_backward(w, max(3, args.steps // 20), stream)
+        log(f"backward, {configs.PREFILL_T2048.name}")
+        res["backward"] = bench_backward(configs.PREFILL_T2048, 10, stream)
         torch.cuda.empty_cache()
     if args.only in (None, "decode") and not args.skip_decode:
         log(f"decode {configs.DECODE_B256.name}: {args.decode_steps} steps")
         res["decode"] = bench_decode(configs.DECODE_B256, args.decode_steps, stream)
-        res["decode_b1"] = bench_step_small(1, 8, args.decode_steps, stream)
         torch.cuda.empty_cache()
+    if args.only in (None, "decode_b1") and not args.skip_decode:
+        res["decode_b1"] = bench_step_small(1, 8, args.decode_steps, stream)
 
     line = {"metric": METRIC, "value": None, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": None, "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
             "config": {"workload": w.name, "B": w.B, "NH": w.NH, "T": w.T, "dqk": w.DQK, "dv": w.DV, "L": w.L,
-                       "qkv": "bf16", "gates_state": "fp32", "initial_state": "zero"}}
+                       "qkv": "bf16", "gates_state": "fp32", "initial_state": "C0~N(0,0.1), n0~|N(0,1)|, m0~N(0,1)",
+                       "gates": "ipre~N(0,1), fpre~N(5,2), both soft-capped at 15"}}
     if "prefill" in res:
         hp = res["prefill"]
         line["value"] = hp["tokens_per_s"]
         line["ms_per_step"] = hp["us_per_call"] / 1e3
         line["roofline"] = {"bound": "mfma", "achieved": hp["tflops"], "peak": acc.PEAK_BF16_MFMA_TFLOPS,
                             "unit": "TFLOP/s", "frac": hp["mfma_frac"], "traffic": measured_traffic(),
-                            "kernel": "mlstm_chunkwise_fwd call: local_state_kernel + combine_kernel + "
-                                      "chunk_mfma_kernel<64> (segment schedule); achieved and traffic are per "
-                                      "call, over the call's duration",
+                            "kernel": "mlstm_chunkwise_fwd call (every kernel of the call: the segment schedule's "
+                                      "local-state and combine passes and the chunkwise pass); achieved and traffic "
+                                      "are per call, over the call's mean duration",
                             "flops_per_call": hp["flops_per_call"], "hbm_frac": hp["hbm_frac"]}
         line["prefill"] = hp
-    if "prefill_large" in res:
-        line["prefill_large"] = res["prefill_large"]
-    if "decode" in res:
-        line["decode"] = res["decode"]
-        line["decode_b1"] = res["decode_b1"]
-    if "output_norm" in res:
-        line["output_norm"] = res["output_norm"]
-    if "layer" in res:
-        line["layer"] = res["layer"]
-    if "backward" in res:
-        line["backward"] = res["backward"]
+    for key in ("prefill_other", "decode", "decode_b1", "output_norm", "layer", "backward"):
+        if key in res:
+            line[key] = res[key]
     if not args.skip_cpu_baseline and args.only in (None, "prefill"):
-        log("cpu baseline: fp64 oracle")
         line["cpu_baseline"] = cpu_baseline(w)
+    line["env"] = env_info()
     print(json.dumps(line), flush=True)
 
 

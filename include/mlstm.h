@@ -230,6 +230,10 @@ mlstm_status mlstm_gate_preact(const void* x, mlstm_dtype dt, const void* w_t, c
  *   workspace: device scratch of at least mlstm_parallel_bwd_workspace_bytes
  *   bytes (else MLSTM_ERR_WORKSPACE); its contents on entry do not matter.
  *
+ * fpre must not hold -inf (a document border): the parallel form's prefix
+ * sums cannot restart there, and every gradient of that sequence would be
+ * NaN.  The chunkwise backward takes borders.
+ *
  * Built: DQK and DV multiples of 16, DQK <= 256, DV <= 512 (else
  * MLSTM_ERR_UNSUPPORTED).  T == 0 launches nothing.  No output may overlap
  * an input, another output or the workspace (MLSTM_ERR_ALIAS).

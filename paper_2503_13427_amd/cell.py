@@ -26,11 +26,15 @@ class _MLSTMCell(torch.autograd.Function):
         ws = torch.empty(nb, dtype=torch.uint8, device=dev) if nb else None
         mb.mlstm_chunkwise_fwd(q, k, v, ipre, fpre, None, None, None, L, h, CT, nT, mT, workspace=ws)
         ctx.save_for_backward(q, k, v, ipre, fpre)
+        ctx.has_borders = bool(torch.isneginf(fpre).any())
         return h
 
     @staticmethod
     def backward(ctx, dh):
         q, k, v, ipre, fpre = ctx.saved_tensors
+        if ctx.has_borders:
+            raise ValueError("mlstm_parallel_bwd does not take document borders (f~ = -inf); "
+                             "its gradients would be NaN")
         B, NH, T, DQK = q.shape
         DV = v.shape[3]
         dev = q.device

@@ -26,8 +26,9 @@
 // keys from its last restart on.
 //
 // One workgroup owns a (sequence, dv tile) pair and walks the chunks in order
-// with its C tile, n and m in LDS.  Everything is fp32; q, k, v may be fp32 or
-// bf16.  This kernel is the fp32 path and the reference schedule; the bf16
+// with its C tile, n and m in LDS.  Storage and the gate arithmetic are fp32; q, k, v may be
+// fp32 or bf16.  The dot products (logits, read-outs, state updates) accumulate in fp64, so a
+// row whose sum cancels keeps the accuracy of its fp32 operands rather than of an fp32 sum.  This kernel is the fp32 path and the reference schedule; the bf16
 // xLSTM-7B head shape runs on the MFMA kernel.
 #include "device_common.h"
 #include "launch.h"
@@ -145,9 +146,9 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
             const int t = e / L, s = e % L;
             float val = 0.0f;
             if (s <= t && s >= static_cast<int>(g_R[t]) && g_M[t] != -INFINITY) {
-                float acc = 0.0f;
-                for (int d = 0; d < DQK; ++d) acc += Qs[t * DQK + d] * Ks[s * DQK + d];
-                val = acc * expf(g_ib[s] - g_M[t]);
+                double acc = 0.0;
+                for (int d = 0; d < DQK; ++d) acc += static_cast<double>(Qs[t * DQK + d]) * Ks[s * DQK + d];
+                val = static_cast<float>(acc) * expf(g_ib[s] - g_M[t]);
             }
             Sm[e] = val;
         }
@@ -155,11 +156,11 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
 
         // denominators: exp(m_prev - M) q^.n + rowsum(S~), floored
         for (int t = tid; t < L; t += kF32Threads) {
-            float qn = 0.0f;
-            for (int d = 0; d < DQK; ++d) qn += Qs[t * DQK + d] * ns[d];
-            float rs = 0.0f;
+            double qn = 0.0;
+            for (int d = 0; d < DQK; ++d) qn += static_cast<double>(Qs[t * DQK + d]) * ns[d];
+            double rs = 0.0;
             for (int s = 0; s <= t; ++s) rs += Sm[t * L + s];
-            const float den = g_inter[t] * qn + rs;
+            const float den = static_cast<float>(g_inter[t] * qn + rs);
             g_den[t] = 1.0f / fmaxf(fabsf(den), g_floor[t]);
         }
         __syncthreads();
@@ -167,11 +168,12 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
         // numerators and output combination
         for (int e = tid; e < lc * DVT; e += kF32Threads) {
             const int t = e / DVT, j = e % DVT;
-            float inter = 0.0f;
-            for (int d = 0; d < DQK; ++d) inter += Qs[t * DQK + d] * Cs[d * DVT + j];
-            float intra = 0.0f;
-            for (int s = 0; s <= t; ++s) intra += Sm[t * L + s] * Vs[s * DVT + j];
-            io<TIn>::store(hb, static_cast<int64_t>(t0 + t) * DV + v0 + j, (g_inter[t] * inter + intra) * g_den[t]);
+            double inter = 0.0;
+            for (int d = 0; d < DQK; ++d) inter += static_cast<double>(Qs[t * DQK + d]) * Cs[d * DVT + j];
+            double intra = 0.0;
+            for (int s = 0; s <= t; ++s) intra += static_cast<double>(Sm[t * L + s]) * Vs[s * DVT + j];
+            io<TIn>::store(hb, static_cast<int64_t>(t0 + t) * DV + v0 + j,
+                           static_cast<float>((g_inter[t] * inter + intra) * g_den[t]));
         }
         __syncthreads();
 
@@ -179,14 +181,14 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
         const float decay = g_sc[1];
         for (int e = tid; e < DQK * DVT; e += kF32Threads) {
             const int d = e / DVT, j = e % DVT;
-            float acc = 0.0f;
-            for (int t = 0; t < L; ++t) acc += g_w[t] * Ks[t * DQK + d] * Vs[t * DVT + j];
-            Cs[e] = decay * Cs[e] + acc;
+            double acc = 0.0;
+            for (int t = 0; t < L; ++t) acc += static_cast<double>(g_w[t] * Ks[t * DQK + d]) * Vs[t * DVT + j];
+            Cs[e] = static_cast<float>(decay * static_cast<double>(Cs[e]) + acc);
         }
         for (int d = tid; d < DQK; d += kF32Threads) {
-            float acc = 0.0f;
-            for (int t = 0; t < L; ++t) acc += g_w[t] * Ks[t * DQK + d];
-            ns[d] = decay * ns[d] + acc;
+            double acc = 0.0;
+            for (int t = 0; t < L; ++t) acc += static_cast<double>(g_w[t]) * Ks[t * DQK + d];
+            ns[d] = static_cast<float>(decay * static_cast<double>(ns[d]) + acc);
         }
         __syncthreads();
     }

@@ -768,11 +768,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             }
             // (iii) N^T += C_p^T Q_p^T over this wave's tile pairs: A from the two C tiles of a
             // pair (rows 4 g16 + j of each), converted to bf16 in registers, is k slot 8 g16 + i
-            // = d 32 pp + 8 g16 + i; B = 16 bytes of a Q row, shared by the VT column tiles
+            // = d 32 pp + 8 g16 + i; B = 16 bytes of a Q row, shared by the VT column tiles.
+            // C goes in as a bf16 pair hi + lo (lo = C - hi, rounded again), so the read-out sees C
+            // to about 2^-16: a single bf16 rounding of the state (2^-9) is what a row whose
+            // read-out cancels (|C^T q| much smaller than the terms it sums) would amplify
 #pragma unroll
             for (int pt = 0; pt < NQ / 2; ++pt) {
                 const int q0 = p * NQ + 2 * pt;
-                u32x4_t a[VT];
+                u32x4_t a[VT], alo[VT];
 #pragma unroll
                 for (int vt = 0; vt < VT; ++vt) {
                     const f32x4_t& c0 = Cacc[q0][vt];
@@ -781,13 +784,20 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     a[vt][1] = pack_bf16x2(c0[2], c0[3]);
                     a[vt][2] = pack_bf16x2(c1[0], c1[1]);
                     a[vt][3] = pack_bf16x2(c1[2], c1[3]);
+                    alo[vt][0] = pack_bf16x2(c0[0] - lo_f32(a[vt][0]), c0[1] - hi_f32(a[vt][0]));
+                    alo[vt][1] = pack_bf16x2(c0[2] - lo_f32(a[vt][1]), c0[3] - hi_f32(a[vt][1]));
+                    alo[vt][2] = pack_bf16x2(c1[0] - lo_f32(a[vt][2]), c1[1] - hi_f32(a[vt][2]));
+                    alo[vt][3] = pack_bf16x2(c1[2] - lo_f32(a[vt][3]), c1[3] - hi_f32(a[vt][3]));
                 }
                 const int dq0 = 32 * (pt * DH + dh) + 8 * g16;   // within the block
 #pragma unroll
                 for (int T = 0; T < NTT; ++T) {
                     const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&Qs[(16 * T + l16) * QP + dq0]);
 #pragma unroll
-                    for (int vt = 0; vt < VT; ++vt) Nacc[vt][T] = mfma16(a[vt], b, Nacc[vt][T]);
+                    for (int vt = 0; vt < VT; ++vt) {
+                        Nacc[vt][T] = mfma16(a[vt], b, Nacc[vt][T]);
+                        Nacc[vt][T] = mfma16(alo[vt], b, Nacc[vt][T]);
+                    }
                 }
             }
 

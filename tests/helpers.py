@@ -1,10 +1,15 @@
 """Shared test helpers: device upload, the error metric, oracle runs on workloads.
 
-Error metric (the reading adopted for "max relative error"): for an output
-tensor, take each (batch, head) slice, compute max|x - x_ref| / max|x_ref|
-over the slice, and report the maximum over slices.  The max state m is
-compared absolutely, |dm| <= tol * max(1, |m_ref|), and the matrix state is
-compared scale-free, C * exp(m - m_ref) against C_ref.
+Error metric (the reading adopted for "max relative error"), per row: an
+output row is the vector one (batch, head, step) produces (an h row of DV
+values), or one d-row of the matrix state C (DV values).  Each row's error is
+max|x - x_ref| / max|x_ref| over that row, and the bar applies to the largest
+row error, so every row is held to its own magnitude (a row of small values
+cannot hide under a large one elsewhere in its sequence).  A row whose
+reference is exactly zero is held to max|x|.  The max state m is compared
+absolutely, |dm| <= tol * max(1, |m_ref|), and the matrix state is compared
+scale-free, C * exp(m - m_ref) against C_ref.  The normaliser n of a sequence
+is one row.
 """
 from __future__ import annotations
 
@@ -45,19 +50,60 @@ def rel_err(x: np.ndarray, ref: np.ndarray, slice_dims: int) -> float:
     return float((num / den).max()) if lead else 0.0
 
 
+def row_errs(x: np.ndarray, ref: np.ndarray, row_len: int, floor: float = 0.0) -> np.ndarray:
+    """Per-row errors over rows of ``row_len`` consecutive values: max|x-ref| / max|ref| per row,
+    max|x| for a row whose reference is all zero.  ``floor`` > 0 (gradient checks only) holds a
+    row to at least that fraction of the largest row of its tensor: a gradient row that is zero
+    in exact arithmetic has no relative error to speak of."""
+    x = np.asarray(x, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert x.shape == ref.shape, (x.shape, ref.shape)
+    if ref.size == 0:
+        return np.zeros(0)
+    xs = x.reshape(-1, row_len)
+    rs = ref.reshape(-1, row_len)
+    num = np.abs(xs - rs).max(axis=1)
+    den = np.maximum(np.abs(rs).max(axis=1), floor * np.abs(rs).max())
+    return np.where(den > 0, num / np.where(den > 0, den, 1.0), num)
+
+
+def row_err(x: np.ndarray, ref: np.ndarray, row_len: int, label: str = None, floor: float = 0.0) -> float:
+    """Largest per-row error (see ``row_errs``); with a label, prints the row count, median,
+    99.9th percentile and maximum."""
+    e = row_errs(x, ref, row_len, floor)
+    if not e.size:
+        return 0.0
+    if label is not None:
+        print(f"{label}: {e.size} rows of {row_len}, median {np.median(e):.2e}, "
+              f"p99.9 {np.quantile(e, 0.999):.2e}, max {e.max():.2e}")
+    return float(e.max())
+
+
 def m_err(m: np.ndarray, m_ref: np.ndarray) -> float:
     m = np.asarray(m, np.float64).ravel()
     r = np.asarray(m_ref, np.float64).ravel()
     return float((np.abs(m - r) / np.maximum(1.0, np.abs(r))).max()) if r.size else 0.0
 
 
-def state_errs(C, n, m, C_ref, n_ref, m_ref):
-    """Errors of (C, n, m) against the oracle, C and n compared scale-free."""
+def state_errs(C, n, m, C_ref, n_ref, m_ref, label=None):
+    """Errors of (C, n, m) against the oracle, C and n compared scale-free: C per d-row (DV
+    values), n per sequence."""
     S = C_ref.shape[0]
+    DV = C_ref.shape[-1]
     sc = np.exp(np.asarray(m, np.float64).reshape(S) - np.asarray(m_ref, np.float64).reshape(S))
-    eC = rel_err(np.asarray(C, np.float64).reshape(S, -1) * sc[:, None], C_ref.reshape(S, -1), 1)
-    en = rel_err(np.asarray(n, np.float64).reshape(S, -1) * sc[:, None], n_ref.reshape(S, -1), 1)
+    eC = row_err(np.asarray(C, np.float64).reshape(S, -1) * sc[:, None], C_ref.reshape(S, -1), DV,
+                 None if label is None else f"{label} C")
+    en = row_err(np.asarray(n, np.float64).reshape(S, -1) * sc[:, None], n_ref.reshape(S, -1), n_ref.reshape(S, -1).shape[1])
     return eC, en, m_err(m, m_ref)
+
+
+def subset(inp: Inputs, heads) -> Inputs:
+    """The inputs of the given global heads (b * NH + h), shaped [1, len(heads), ...]."""
+    sel = np.asarray(heads, dtype=np.int64)
+    S = inp.B * inp.NH
+    pick = lambda a: None if a is None else a.reshape(S, *a.shape[2:])[sel][None]
+    return Inputs(dtype=inp.dtype, q=pick(inp.q), k=pick(inp.k), v=pick(inp.v), ipre=pick(inp.ipre),
+                  fpre=pick(inp.fpre), C0=pick(inp.C0), n0=pick(inp.n0), m0=pick(inp.m0), heads=sel)
 
 
 def upload_prefill(inp: Inputs, device="cuda"):

@@ -11,7 +11,7 @@ import torch
 from oracle import coracle
 from paper_2503_13427_amd import configs
 from paper_2503_13427_amd.inputs import GateDist, StateDist, make_prefill
-from tests.helpers import (TOL_BF16, TOL_F32, alloc_prefill_outputs, host_f64, rel_err, state_errs,
+from tests.helpers import (TOL_BF16, TOL_F32, alloc_prefill_outputs, host_f64, row_err, state_errs,
                            upload_prefill)
 
 pytestmark = pytest.mark.gpu
@@ -34,7 +34,7 @@ def run_chunk(inp, L, workspace=None):
 def compare(inp, out, tol, label=""):
     S = inp.B * inp.NH
     hr, Cr, nr, mr = coracle.recurrent_inputs(inp)
-    eh = rel_err(out["h"].reshape(S, -1), hr.reshape(S, -1), 1)
+    eh = row_err(out["h"].reshape(S, inp.T, inp.DV), hr, inp.DV, f"{label} h")
     eC, en, em = state_errs(out["CT"].reshape(S, inp.DQK, inp.DV), out["nT"].reshape(S, inp.DQK),
                             out["mT"].reshape(S), Cr, nr, mr)
     print(f"{label} h {eh:.3e} C {eC:.3e} n {en:.3e} m {em:.3e}")
@@ -95,7 +95,7 @@ def test_chunk_size_independence_fp32():
                        state=StateDist(), k_scale=0.25)
     outs = [run_chunk(inp, L) for L in (16, 32, 64)]
     for o in outs[1:]:
-        assert rel_err(o["h"].reshape(3, -1), outs[0]["h"].reshape(3, -1), 1) < 2e-6
+        assert row_err(o["h"], outs[0]["h"], 32, "L vs L16") < 2e-6
         np.testing.assert_allclose(o["mT"], outs[0]["mT"], rtol=1e-6, atol=1e-6)
 
 
@@ -123,7 +123,7 @@ def test_decode_steps_equal_prefill_fp32():
         hs.append(h)
     torch.cuda.synchronize()
     hstep = host_f64(torch.stack(hs, dim=2))
-    assert rel_err(hstep.reshape(2, -1), out["h"].reshape(2, -1), 1) < 2e-6
+    assert row_err(hstep, out["h"].reshape(hstep.shape), 16, "steps vs prefill") < 2e-6
     eC, en, em = state_errs(host_f64(C).reshape(2, 16, 16), host_f64(n).reshape(2, 16), host_f64(m).reshape(2),
                             out["CT"].reshape(2, 16, 16), out["nT"].reshape(2, 16), out["mT"].reshape(2))
     assert max(eC, en, em) < 2e-6

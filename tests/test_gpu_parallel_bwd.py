@@ -16,7 +16,7 @@ import torch
 
 from oracle import mlstm_grad as G
 from paper_2503_13427_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
-from tests.helpers import TOL_BF16, rel_err
+from tests.helpers import TOL_BF16, rel_err, row_err
 
 TOL_BWD_F32 = 1e-4
 
@@ -63,7 +63,11 @@ def compare(got, ref, tol, label):
     errs = []
     for n, g, r in zip(names, got, ref):
         S, T = r.shape[0], r.shape[1]
-        e = rel_err(g.reshape(S, -1), r.reshape(S, -1), 1)
+        # dq, dk, dv per token row (a row that is zero in exact arithmetic, such as dq of a first
+        # token whose denominator is above the floor, held to 1e-3 of the tensor's largest row);
+        # the gate gradients (one value per token) per sequence
+        e = row_err(g, r, r.shape[2], f"{label} {n}", floor=1e-3) if n in ("dq", "dk", "dv") else \
+            rel_err(g.reshape(S, -1), r.reshape(S, -1), 1)
         errs.append(e)
         assert np.isfinite(g).all(), n
     print(label + " " + " ".join(f"{n} {e:.2e}" for n, e in zip(names, errs)))

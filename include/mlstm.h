@@ -111,6 +111,29 @@ mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, ml
                                  void* workspace, size_t workspace_bytes, void* hip_stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * mlstm_chunkwise_fwd with no workspace argument and no allocation.  Same
+ * arguments (less the workspace), validation, kernels and results as
+ * mlstm_chunkwise_fwd given a workspace of mlstm_chunkwise_workspace_bytes
+ * bytes: the segment slots live in a fixed device array of
+ * mlstm_chunkwise_scratch_bytes() bytes (64 MiB), one per device, which the
+ * library holds from the first call on that device until the process ends.
+ * A call whose segment schedule needs more than that returns
+ * MLSTM_ERR_WORKSPACE and does nothing (mlstm_chunkwise_fwd serves it).
+ * Nothing in the array needs clearing between calls (every slot a call
+ * reads is written earlier in that call), but calls that overlap in time on
+ * one device share it and race: order them (one stream, or events).
+ * It calls no hipMalloc or hipFree.
+ */
+mlstm_status mlstm_chunkwise_fwd_noalloc(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                                         const float* ipre, const float* fpre,
+                                         const float* C0, const float* n0, const float* m0,
+                                         int B, int NH, int T, int DQK, int DV, int L,
+                                         void* h, float* CT, float* nT, float* mT, void* hip_stream);
+size_t mlstm_chunkwise_scratch_bytes(void);
+
+/*
  * Workspace size (bytes) for the segment-parallel schedule of
  * mlstm_chunkwise_fwd with these arguments; 0 when that schedule would not be
  * used (the call then runs the fused kernel whatever workspace is given).

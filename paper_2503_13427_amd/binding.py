@@ -36,6 +36,11 @@ _i = ctypes.c_int
 lib.mlstm_chunkwise_fwd.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                     _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
 lib.mlstm_chunkwise_fwd.restype = _i
+lib.mlstm_chunkwise_fwd_noalloc.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                                            _vp, _vp, _vp, _vp, _vp]
+lib.mlstm_chunkwise_fwd_noalloc.restype = _i
+lib.mlstm_chunkwise_scratch_bytes.argtypes = []
+lib.mlstm_chunkwise_scratch_bytes.restype = ctypes.c_size_t
 lib.mlstm_chunkwise_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i]
 lib.mlstm_chunkwise_workspace_bytes.restype = ctypes.c_size_t
 lib.mlstm_step.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp]
@@ -119,6 +124,20 @@ def mlstm_chunkwise_fwd(q, k, v, ipre, fpre, C0, n0, m0, L, h, CT, nT, mT,
                                    _ptr(C0), _ptr(n0), _ptr(m0), B, NH, T, DQK, DV, int(L),
                                    _ptr(h), _ptr(CT), _ptr(nT), _ptr(mT), _ptr(workspace), ws_bytes,
                                    _stream(stream)))
+
+
+def mlstm_chunkwise_scratch_bytes() -> int:
+    return int(lib.mlstm_chunkwise_scratch_bytes())
+
+
+def mlstm_chunkwise_fwd_noalloc(q, k, v, ipre, fpre, C0, n0, m0, L, h, CT, nT, mT, stream=None) -> None:
+    """Chunkwise prefill without a workspace and without allocating: the segment slots live in the
+    library's fixed device scratch (``mlstm_chunkwise_scratch_bytes``)."""
+    B, NH, T, DQK = q.shape
+    DV = v.shape[3]
+    _check(lib.mlstm_chunkwise_fwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre),
+                                           _ptr(C0), _ptr(n0), _ptr(m0), B, NH, T, DQK, DV, int(L),
+                                           _ptr(h), _ptr(CT), _ptr(nT), _ptr(mT), _stream(stream)))
 
 
 def mlstm_step(q, k, v, ipre, fpre, C, n, m, h, C_out, n_out, m_out, stream=None) -> None:

@@ -83,5 +83,10 @@ bool chunk_mfma_supported(mlstm_dtype dt, int DQK, int DV, int L);
 int chunk_mfma_segments(int B, int NH, int T, int L);
 size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L);
 hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream);
+// Fixed device scratch of mlstm_chunkwise_fwd_noalloc: a file-scope device array of this many bytes,
+// one copy per device.  chunk_scratch gives its address on the current device (looked up once per
+// device, then cached).
+constexpr size_t kChunkScratchBytes = size_t(64) << 20;
+hipError_t chunk_scratch(void** ptr);
 
 }  // namespace mlstm

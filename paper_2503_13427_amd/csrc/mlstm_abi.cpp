@@ -46,7 +46,9 @@ const char* mlstm_status_string(mlstm_status s) {
         case MLSTM_ERR_UNSUPPORTED: return "MLSTM_ERR_UNSUPPORTED: this (dtype, DQK, DV, L) combination is not built";
         case MLSTM_ERR_MISALIGNED: return "MLSTM_ERR_MISALIGNED: a tensor pointer is not 16-byte aligned";
         case MLSTM_ERR_ALIAS: return "MLSTM_ERR_ALIAS: an output overlaps an input or another output";
-        case MLSTM_ERR_WORKSPACE: return "MLSTM_ERR_WORKSPACE: workspace smaller than mlstm_chunkwise_workspace_bytes";
+        case MLSTM_ERR_WORKSPACE:
+            return "MLSTM_ERR_WORKSPACE: workspace smaller than mlstm_chunkwise_workspace_bytes, or (no-allocation "
+                   "variant) more than the library's fixed scratch of mlstm_chunkwise_scratch_bytes";
         case MLSTM_ERR_HIP: return "MLSTM_ERR_HIP: the HIP runtime reported an error at launch";
     }
     return "MLSTM_UNKNOWN_STATUS";
@@ -60,11 +62,13 @@ size_t mlstm_chunkwise_workspace_bytes(int B, int NH, int T, int DQK, int DV, in
     return mlstm::chunk_mfma_workspace_bytes(B, NH, T, DQK, DV, L);
 }
 
-mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, mlstm_dtype dt,
-                                 const float* ipre, const float* fpre, const float* C0, const float* n0,
-                                 const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
-                                 float* CT, float* nT, float* mT, void* workspace, size_t workspace_bytes,
-                                 void* hip_stream) {
+// Validation and launch shared by mlstm_chunkwise_fwd (caller workspace) and
+// mlstm_chunkwise_fwd_noalloc (the library's fixed device scratch, use_scratch).
+static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                                       const float* ipre, const float* fpre, const float* C0, const float* n0,
+                                       const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
+                                       float* CT, float* nT, float* mT, void* workspace, size_t workspace_bytes,
+                                       bool use_scratch, void* hip_stream) {
     // per-token buffers are empty (and may be NULL) when T == 0
     if (T != 0 && (!q || !k || !v || !ipre || !fpre || !h)) return MLSTM_ERR_NULL_PTR;
     if (!CT || !nT || !mT) return MLSTM_ERR_NULL_PTR;
@@ -105,13 +109,38 @@ mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, ml
     size_t ws_need = 0;
     if (mfma) ws_need = mlstm::chunk_mfma_workspace_bytes(B, NH, T, DQK, DV, L);
     if (workspace_bytes > 0 && workspace_bytes < ws_need) return MLSTM_ERR_WORKSPACE;
+    if (use_scratch && ws_need > mlstm::kChunkScratchBytes) return MLSTM_ERR_WORKSPACE;
 
     mlstm::ChunkArgs a{q, k, v, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT};
     hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+    if (use_scratch && ws_need > 0) {
+        hipError_t e = mlstm::chunk_scratch(&workspace);
+        if (e != hipSuccess) return MLSTM_ERR_HIP;
+        workspace_bytes = ws_need;
+    }
     hipError_t e = mfma ? mlstm::launch_chunk_mfma(a, workspace_bytes ? workspace : nullptr,
                                                    workspace_bytes, stream)
                         : mlstm::launch_chunk_f32(dt, a, stream);
     return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
+mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                                 const float* ipre, const float* fpre, const float* C0, const float* n0,
+                                 const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
+                                 float* CT, float* nT, float* mT, void* workspace, size_t workspace_bytes,
+                                 void* hip_stream) {
+    return chunkwise_fwd_impl(q, k, v, dt, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, workspace,
+                              workspace_bytes, false, hip_stream);
+}
+
+size_t mlstm_chunkwise_scratch_bytes(void) { return mlstm::kChunkScratchBytes; }
+
+mlstm_status mlstm_chunkwise_fwd_noalloc(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                                         const float* ipre, const float* fpre, const float* C0, const float* n0,
+                                         const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
+                                         float* CT, float* nT, float* mT, void* hip_stream) {
+    return chunkwise_fwd_impl(q, k, v, dt, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, nullptr, 0,
+                              true, hip_stream);
 }
 
 mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,

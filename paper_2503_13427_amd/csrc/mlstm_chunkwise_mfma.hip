@@ -61,6 +61,8 @@
 // segment's entry state, m_in' = max(gsum + m_in, m_loc),
 // C_in' = e^{gsum + m_in - m_in'} C_in + e^{m_loc - m_in'} C_loc; (3) the chunkwise
 // kernel runs every segment from its entry state.
+#include <mutex>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -1397,6 +1399,34 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
         if (e != hipSuccess) return e;
     }
     return (a.L == 64) ? launch_variant<64>(k, S, stream) : launch_variant<128>(k, S, stream);
+}
+
+// ---- fixed scratch for callers that cannot allocate ---------------------------------------------
+// The segment slots of mlstm_chunkwise_fwd_noalloc.  Every slot a call reads is written earlier in
+// the same call (local pass, then combine), so nothing needs clearing between calls; calls that
+// overlap on one device share this array and race.
+namespace {
+__device__ __attribute__((aligned(256))) unsigned char scratch[kChunkScratchBytes];
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+}  // namespace
+
+hipError_t chunk_scratch(void** ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        // the device address of this device's copy (the host-side name is not a device address)
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 }  // namespace mlstm

@@ -25,6 +25,7 @@ def declared_functions():
 
 def test_header_declares_expected_entry_points():
     assert declared_functions() == sorted(["mlstm_chunkwise_fwd", "mlstm_chunkwise_workspace_bytes", "mlstm_step",
+                                           "mlstm_chunkwise_fwd_noalloc", "mlstm_chunkwise_scratch_bytes",
                                            "mlstm_output_norm", "mlstm_output_norm_tokens", "mlstm_gate_preact", "mlstm_parallel_bwd",
                                            "mlstm_parallel_bwd_workspace_bytes", "mlstm_status_string",
                                            "mlstm_version"])
@@ -381,3 +382,34 @@ def test_bwd_alias(out, other, off):
     a = bwd_args()
     a[out] = a[other] + off
     assert call_bwd(a) == 5
+
+
+# ---- the no-allocation prefill (fixed device scratch) ---------------------------------------------
+
+def call_chunk_noalloc(a):
+    return lib.mlstm_chunkwise_fwd_noalloc(a["q"], a["k"], a["v"], a["dt"], a["ipre"], a["fpre"], a["C0"], a["n0"],
+                                           a["m0"], a["B"], a["NH"], a["T"], a["DQK"], a["DV"], a["L"], a["h"],
+                                           a["CT"], a["nT"], a["mT"], a["stream"])
+
+
+def test_noalloc_scratch_size():
+    assert Bd.mlstm_chunkwise_scratch_bytes() == 64 << 20
+
+
+def test_noalloc_rejects_a_schedule_larger_than_the_scratch():
+    """The B=4 x T=32768 prefill's segment schedule needs 67.2 MB of slots, more than the 64 MiB
+    scratch: rejected on the host, nothing launched."""
+    a = chunk_args(B=4, NH=8, T=32768, L=128)
+    assert Bd.mlstm_chunkwise_workspace_bytes(4, 8, 32768, 256, 512, 128) > Bd.mlstm_chunkwise_scratch_bytes()
+    assert call_chunk_noalloc(a) == 6
+    assert "scratch" in Bd.mlstm_status_string(6)
+
+
+@pytest.mark.parametrize("field", ["q", "fpre", "h", "mT"])
+def test_noalloc_validates_like_the_workspace_entry_point(field):
+    assert call_chunk_noalloc(chunk_args(**{field: None})) == 1
+    a = chunk_args()
+    a[field] = a[field] + 2
+    assert call_chunk_noalloc(a) == 4
+    assert call_chunk_noalloc(chunk_args(B=0)) == 2
+    assert call_chunk_noalloc(chunk_args(h=fake(1, 64))) == 5

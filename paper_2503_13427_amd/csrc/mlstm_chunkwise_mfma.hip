@@ -133,7 +133,20 @@ struct Cfg {
     // V is kept in LDS transposed (rows v, tau contiguous, pitch TP), once plain for (ii) and once
     // scaled by the C-update key weights for (iv), so both read it with plain 16-byte row reads
     static constexpr int TP = L + 8;
+    // L = 128 stages K only transposed (K^T rows [d][tau], pitch KTP, transposed on the matrix cores
+    // like V): (iv) and the n update read it with 16-byte row reads, (i) with transpose reads.  L = 64
+    // stages K rows (its LDS holds no room for a second layout next to the read-out exchange).
+    static constexpr bool KT = (L == 128);
+    static constexpr int KTP = L + 8;
+    static constexpr int KTE = DB * KTP;
+    static constexpr int SETE = QKE + (KT ? KTE : QKE);   // elements of one d-block set: Q, then K
 };
+
+// Physical K^T row of d (within a d block): bit 2 flipped when bit 4 is set, so that the 16 rows an
+// (iv) operand reads (d = 32 pp + 8 i + 4 e + 0..3, i = 0..3) and the 16 consecutive rows an n-update
+// operand reads fall in 16 different 4-bank groups at a 272-byte pitch; four consecutive d stay
+// consecutive (the transpose reads of (i) take them four at a time).
+__device__ __forceinline__ int kt_row(int d) { return d ^ (((d >> 4) & 1) << 2); }
 
 // Per-chunk gate quantities, written one chunk ahead by the gate wave.
 template <int L>
@@ -152,7 +165,9 @@ struct alignas(16) GateBuf {
 template <int L>
 struct Smem {
     using C = Cfg<L>;
-    uint16_t QK[2][2][C::QKE];                     // [set][0: Q, 1: K][tau * QP + d]; d block p uses set p % 2
+    // d-block set s: Q [tau * QP + d], then K (L = 64: rows [tau * QP + d]; L = 128: K^T
+    // [kt_row(d) * KTP + tau]); d block p uses set p % 2
+    uint16_t QK[2][C::SETE];
     // [0] V^T[v][tau] and [1] (w e^{-s} V)^T[v][tau] of the current chunk (this workgroup's 128 columns)
     uint16_t Vs[2][kDVT * C::TP];
     uint16_t St_own[C::ST_ALIAS ? 8 : L * C::SP];  // S~[tau][sig] when it has its own buffer
@@ -165,7 +180,7 @@ struct Smem {
     // [column group][v tile][tau tile][lane] as float4
     float X[C::DH == 2 ? C::NVG * C::VT * (L / 16) * 64 * 4 : 4];
 };
-static_assert(Cfg<128>::ST_ALIAS && 128 * Cfg<128>::SP <= 2 * Cfg<128>::QKE, "S~ must fit in one Q/K set");
+static_assert(Cfg<128>::ST_ALIAS && 128 * Cfg<128>::SP <= Cfg<128>::SETE, "S~ must fit in one Q/K set");
 static_assert(sizeof(Smem<64>) <= 160 * 1024 && sizeof(Smem<128>) <= 160 * 1024, "LDS budget");
 
 // Per-thread staging registers: one Q/K d block and one chunk of V in flight.
@@ -204,6 +219,9 @@ __device__ __forceinline__ float bloadf(__amdgpu_buffer_rsrc_t r, uint32_t voff,
 }
 
 // Q and K rows are 512 bytes, V rows 1024 bytes; offsets are in bytes.
+// With K^T staging (L = 128) K is loaded in pieces in the MFMA A-operand layout: piece i of wave w
+// (pc = w + 8 i, a = pc % (L / 16), b = pc / (L / 16)) has lane (l16, g16) holding
+// K[tau 16 a + l16][d 32 b + 8 g16 + 0..7] of the d block.
 template <int L>
 __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, int p, int tid) {
     constexpr int DB = Cfg<L>::DB, PR = DB / 8;   // 16-byte pieces per row
@@ -213,7 +231,32 @@ __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, 
         const int item = tid + i * kThreads;
         const uint32_t voff = (item / PR) * (kDQK * 2) + 16 * (item % PR);
         r.q[i] = bload128(R.q, voff, soff);
-        r.k[i] = bload128(R.k, voff, soff);
+        if constexpr (!Cfg<L>::KT) r.k[i] = bload128(R.k, voff, soff);
+    }
+    if constexpr (Cfg<L>::KT) {
+        static_assert(QKRegs<L>::N * kWaves == (L / 16) * (DB / 32), "pieces of one K block");
+        int ln = tid & 63;   // opaque: recomputed per call rather than held across the loop
+        asm volatile("" : "+v"(ln));
+        const int wave = tid >> 6;
+#pragma unroll
+        for (int i = 0; i < QKRegs<L>::N; ++i) {
+            const int pc = wave + kWaves * i, a = pc % (L / 16), b = pc / (L / 16);
+            r.k[i] = bload128(R.k, (16 * a + (ln & 15)) * (kDQK * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
+        }
+    }
+}
+// One-hot selection E_h (32 x 16, columns 16 h + 0..15 of a 32-column piece) in the B-operand layout:
+// lane (l16, g16) holds k slots 8 g16 + 0..7 of column l16, whose one (if any) is slot 16 h + l16.
+// Built from an opaque copy of the lane index so that it is not held across the chunk loop.
+__device__ __forceinline__ void onehot_pair(u32x4_t (&E)[2], int lane) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int pos = 16 * h + (ln & 15) - 8 * (ln >> 4);
+        const uint32_t one = (pos & 1) ? 0x3F800000u : 0x3F80u;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) E[h][d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
     }
 }
 template <int L>
@@ -224,7 +267,26 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
         const int item = tid + i * kThreads;
         const int off = (item / PR) * QP + 8 * (item % PR);
         *reinterpret_cast<u32x4_t*>(&Qd[off]) = r.q[i];
-        *reinterpret_cast<u32x4_t*>(&Kd[off]) = r.k[i];
+        if constexpr (!Cfg<L>::KT) *reinterpret_cast<u32x4_t*>(&Kd[off]) = r.k[i];
+    }
+    if constexpr (Cfg<L>::KT) {
+        // K^T on the matrix cores: D = (piece) E_h holds, in lane (n = l16, g16), K[tau 16 a + 4 g16 + j]
+        // [d 32 b + 16 h + n], j = 0..3 (exact), stored as four consecutive tau of K^T row d
+        constexpr int KTP = Cfg<L>::KTP;
+        const int lane = tid & 63, wave = tid >> 6;
+        u32x4_t E[2];
+        onehot_pair(E, lane);
+        const int l16 = lane & 15, g16 = lane >> 4;
+#pragma unroll
+        for (int i = 0; i < QKRegs<L>::N; ++i) {
+            const int pc = wave + kWaves * i, a = pc % (L / 16), b = pc / (L / 16);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const f32x4_t d = mfma16(r.k[i], E[h], f32x4_t{});
+                const u32x2_t o{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
+                *reinterpret_cast<u32x2_t*>(&Kd[kt_row(32 * b + 16 * h + l16) * KTP + 16 * a + 4 * g16]) = o;
+            }
+        }
     }
 }
 // V pieces in the MFMA A-operand layout for vt_transpose: for piece i of part `part`, lane (l16, g16)
@@ -548,7 +610,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         return (t / NQ) * DB + 32 * ((q / 2) * DH + dh) + 8 * g16 + 4 * (q % 2) + j;
     };
     const bool gate_wave = (wave == kGateWave);
-    uint16_t* const St = CF::ST_ALIAS ? &S.QK[1][0][0] : S.St_own;
+    uint16_t* const St = CF::ST_ALIAS ? &S.QK[1][0] : S.St_own;
     // Q n tile of this wave (>= NTT: none): with fewer tau tiles than waves, the waves after
     // the two that hold two S tiles take it
     const int dqt = (NTT < kWaves) ? wave - 2 : wave;
@@ -649,7 +711,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             load_gates<L>(gi, gf, P, t0, lane);
             gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane, A.T - t0);
         }
-        store_qk<L>(S.QK[0][0], S.QK[0][1], rqk, tid);
+        store_qk<L>(S.QK[0], S.QK[0] + CF::QKE, rqk, tid);
 #pragma unroll
         for (int part = 0; part < VRegs<L>::PARTS; ++part) {
             load_v_tr<L>(rv, P, t0, v0, wave, lane, part);
@@ -694,7 +756,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         const GateBuf<L>& Gc = S.G[par];
         __syncthreads();   // the previous chunk is done; block 0, V and the gates of this chunk are visible
         // block 1 -> set 1 (its readers in the previous chunk, the last d block and S~, are done)
-        store_qk<L>(S.QK[1][0], S.QK[1][1], rqk, tid);
+        store_qk<L>(S.QK[1], S.QK[1] + CF::QKE, rqk, tid);
         if constexpr (NDB > 2) load_qk<L>(rqk, P, t0, 2, tid);
         else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid);
         if (gate_wave && c + 1 < c_end) load_gates<L>(gi, gf, P, t0 + L, lane);
@@ -721,17 +783,17 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
 
 #pragma unroll
         for (int p = 0; p < NDB; ++p) {
-            const uint16_t* Qs = S.QK[p & 1][0];
-            const uint16_t* Ks = S.QK[p & 1][1];
+            const uint16_t* Qs = S.QK[p & 1];
+            const uint16_t* Ks = S.QK[p & 1] + CF::QKE;   // K rows, or K^T at L = 128
             if (p > 0) {
                 __syncthreads();   // block p visible, block p - 1 fully read
                 if (p + 1 < NDB) {
-                    store_qk<L>(S.QK[(p + 1) & 1][0], S.QK[(p + 1) & 1][1], rqk, tid);
+                    store_qk<L>(S.QK[(p + 1) & 1], S.QK[(p + 1) & 1] + CF::QKE, rqk, tid);
                     if (p + 2 < NDB) load_qk<L>(rqk, P, t0, p + 2, tid);
                     else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid);
                 } else if (c + 1 < c_end) {
                     // block 0 of the next chunk
-                    store_qk<L>(S.QK[0][0], S.QK[0][1], rqk, tid);
+                    store_qk<L>(S.QK[0], S.QK[0] + CF::QKE, rqk, tid);
                     load_qk<L>(rqk, P, t0 + L, 1, tid);
                 }
                 // the next chunk's V, part p - 1, transposed in registers; part p requested
@@ -740,21 +802,31 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     if (p < VRegs<L>::PARTS) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane, p);
                 }
             }
-            // (i) S^T += K_p Q_p^T on this wave's causal tiles (L = 128: a fixed tile count per
-            // wave; the surplus tiles repeat the last one and are not used)
+            // (i) S^T += K_p Q_p^T on this wave's causal tiles.  K^T staging (L = 128): the A operand
+            // (K rows sigma, 8 consecutive d) is two transpose reads of 4 K^T rows x 16 tau
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
-                const int t = (L == 128) ? min(wave + kWaves * i, NT_S - 1) : wave + kWaves * i;
-                if (L == 128 || t < NT_S) {
+                const int t = wave + kWaves * i;
+                if (t < NT_S) {
                     int tb = 0, rem = t;
                     while (rem > tb) { rem -= tb + 1; ++tb; }
                     const int sb = rem;
-                    const uint16_t* ka = &Ks[(16 * sb + l16) * QP + 8 * g16];
                     const uint16_t* qb = &Qs[(16 * tb + l16) * QP + 8 * g16];
+                    if constexpr (CF::KT) {
 #pragma unroll
-                    for (int ks = 0; ks < DB / 32; ++ks)
-                        Sacc[i] = mfma16(*reinterpret_cast<const u32x4_t*>(ka + 32 * ks),
-                                         *reinterpret_cast<const u32x4_t*>(qb + 32 * ks), Sacc[i]);
+                        for (int ks = 0; ks < DB / 32; ++ks) {
+                            const int d0 = 32 * ks + 8 * g16 + (l16 >> 2);
+                            const u32x4_t a = cat(tr_read(&Ks[kt_row(d0) * CF::KTP + 16 * sb + tr_col]),
+                                                  tr_read(&Ks[kt_row(d0 + 4) * CF::KTP + 16 * sb + tr_col]));
+                            Sacc[i] = mfma16(a, *reinterpret_cast<const u32x4_t*>(qb + 32 * ks), Sacc[i]);
+                        }
+                    } else {
+                        const uint16_t* ka = &Ks[(16 * sb + l16) * QP + 8 * g16];
+#pragma unroll
+                        for (int ks = 0; ks < DB / 32; ++ks)
+                            Sacc[i] = mfma16(*reinterpret_cast<const u32x4_t*>(ka + 32 * ks),
+                                             *reinterpret_cast<const u32x4_t*>(qb + 32 * ks), Sacc[i]);
+                    }
                 }
             }
             // Q n_{k-1} over this d block: A = Q rows, B = n as bf16 hi / lo columns
@@ -792,14 +864,20 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                     alo[vt][3] = pack_bf16x2(c1[2] - lo_f32(a[vt][3]), c1[3] - hi_f32(a[vt][3]));
                 }
                 const int dq0 = 32 * (pt * DH + dh) + 8 * g16;   // within the block
+                // the Q operand of the next tau tile is requested before this one's MFMAs are issued
+                // (the scheduling fence keeps the compiler from waiting on each read in turn)
+                u32x4_t b = *reinterpret_cast<const u32x4_t*>(&Qs[l16 * QP + dq0]);
 #pragma unroll
                 for (int T = 0; T < NTT; ++T) {
-                    const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&Qs[(16 * T + l16) * QP + dq0]);
+                    u32x4_t bn = b;
+                    if (T + 1 < NTT) bn = *reinterpret_cast<const u32x4_t*>(&Qs[(16 * (T + 1) + l16) * QP + dq0]);
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int vt = 0; vt < VT; ++vt) {
                         Nacc[vt][T] = mfma16(a[vt], b, Nacc[vt][T]);
                         Nacc[vt][T] = mfma16(alo[vt], b, Nacc[vt][T]);
                     }
+                    b = bn;
                 }
             }
 
@@ -819,9 +897,15 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 u32x4_t a[NQ];
 #pragma unroll
                 for (int q = 0; q < NQ; ++q) {
-                    // tile (pair q / 2, half q % 2): columns 32 pp + 8 (l16 & 3) + 4 (q % 2) + 0..3
-                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * ((q / 2) * DH + dh) + 2 * tr_col + 4 * (q % 2)];
-                    a[q] = cat(tr_read(kb), tr_read(kb + 4 * QP));
+                    if constexpr (CF::KT) {
+                        // row m = l16 of tile (pair q / 2, half q % 2) is d = 32 pp + 8 (m / 4) + 4 (q % 2) + m % 4
+                        const int d = 32 * ((q / 2) * DH + dh) + 8 * (l16 >> 2) + 4 * (q % 2) + (l16 & 3);
+                        a[q] = *reinterpret_cast<const u32x4_t*>(&Ks[kt_row(d) * CF::KTP + 32 * ks + 8 * g16]);
+                    } else {
+                        // tile (pair q / 2, half q % 2): columns 32 pp + 8 (l16 & 3) + 4 (q % 2) + 0..3
+                        const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * ((q / 2) * DH + dh) + 2 * tr_col + 4 * (q % 2)];
+                        a[q] = cat(tr_read(kb), tr_read(kb + 4 * QP));
+                    }
                 }
                 if constexpr (L == 64) __builtin_amdgcn_sched_barrier(0);
                 // lane (n = column vcol(vt) + l16, k group g16) holds tau = 32 ks + 8 g16 + 0..7
@@ -845,8 +929,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 for (int ks = 0; ks < NKS; ++ks) {
                     const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&Gc.wb[l16 & 1][32 * ks + 8 * g16])
                                                  : u32x4_t{0u, 0u, 0u, 0u};
-                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * ut + tr_col];
-                    nacc = mfma16(wa, cat(tr_read(kb), tr_read(kb + 4 * QP)), nacc);
+                    u32x4_t kt;
+                    if constexpr (CF::KT) {
+                        kt = *reinterpret_cast<const u32x4_t*>(&Ks[kt_row(16 * ut + l16) * CF::KTP + 32 * ks + 8 * g16]);
+                    } else {
+                        const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * ut + tr_col];
+                        kt = cat(tr_read(kb), tr_read(kb + 4 * QP));
+                    }
+                    nacc = mfma16(wa, kt, nacc);
                 }
                 // rows 0 and 1 (hi and lo weights) of column l16 sit in lanes 0..15
                 if (g16 == 0) {

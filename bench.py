@@ -23,6 +23,9 @@ Extra objects on the same line:
   decode        1024 consecutive mlstm_step calls at B=256, NH=8: us per step,
                 us per sequence-token, achieved GB/s vs 8 TB/s;
   decode_b1     mlstm_step at B=1, NH=8 (single-sequence generation), in place;
+  decode_output the step returning h = sigmoid(o~) * LayerNorm(h~) w: mlstm_step_output
+                (fused epilogue at B=256; column split + output pass at B=1) against
+                mlstm_step followed by mlstm_output_norm;
   output_norm   the hidden-state output h = sigmoid(o~) * LayerNorm(h~) w + b
                 (mlstm_output_norm) on the T=2048 prefill's h shape and the
                 decode step's h shape: us per call and achieved GB/s vs 8 TB/s;
@@ -266,6 +269,33 @@ def bench_step_small(B, NH, steps, stream):
     by = acc.step_bytes(B, NH, DQK, DV)
     return dict(workload=f"decode_B{B}_NH{NH}", us_per_step=t * 1e6, bytes_per_step=by, gbs=by / t / 1e9,
                 hbm_frac=by / t / 1e9 / acc.PEAK_HBM_GBS)
+
+
+def bench_step_output(B, NH, steps, stream):
+    """The decode step returning the hidden-state output h = sigmoid(o~) * LayerNorm(h~) w (Eq. 6, 9):
+    mlstm_step_output (the norm in the step's epilogue at this batch) against mlstm_step followed by
+    mlstm_output_norm, both in place on the same state; us per step."""
+    from paper_2503_13427_amd import binding as mb
+    DQK, DV = 256, 512
+    g = torch.Generator(device="cuda").manual_seed(9)
+    rn = lambda *shape: torch.randn(*shape, generator=g, device="cuda")
+    q, k, v = rn(B, NH, DQK).bfloat16(), rn(B, NH, DQK).bfloat16(), rn(B, NH, DV).bfloat16()
+    o = rn(B, NH, DV).bfloat16()
+    ip, fp = rn(B, NH), rn(B, NH) + 3
+    C, n, m = rn(B, NH, DQK, DV) * 0.1, rn(B, NH, DQK).abs(), torch.zeros(B, NH, device="cuda")
+    w = 1 + 0.1 * rn(NH, DV)
+    h = torch.empty(B, NH, DV, dtype=torch.bfloat16, device="cuda")
+    fused = lambda: mb.mlstm_step_output(q, k, v, ip, fp, C, n, m, o, w, None, 1e-6, "layer", h, C, n, m, stream=stream)
+
+    def pair():
+        mb.mlstm_step(q, k, v, ip, fp, C, n, m, h, C, n, m, stream=stream)
+        mb.mlstm_output_norm(h, o, w, None, 1e-6, "layer", h, stream=stream)
+    t_f = time_steps(fused, steps, 10, stream)[1] / steps
+    t_p = time_steps(pair, steps, 10, stream)[1] / steps
+    by = acc.step_bytes(B, NH, DQK, DV) + B * NH * DV * 2   # plus o~ read once
+    return dict(workload=f"decode_output_B{B}_NH{NH}", us_per_step_fused=t_f * 1e6, us_per_step_step_then_norm=t_p * 1e6,
+                saved_us=(t_p - t_f) * 1e6, bytes_per_step=by, gbs_fused=by / t_f / 1e9,
+                hbm_frac_fused=by / t_f / 1e9 / acc.PEAK_HBM_GBS)
 
 
 def bench_output_norm(B, NH, T, DV, steps, stream, label):
@@ -542,7 +572,8 @@ def main():
     ap.add_argument("--skip-cpu-baseline", action="store_true")
     ap.add_argument("--skip-layer", action="store_true")
     ap.add_argument("--skip-backward", action="store_true")
-    ap.add_argument("--only", choices=["prefill", "other", "decode", "decode_b1", "output_norm", "layer", "backward",
+    ap.add_argument("--only", choices=["prefill", "other", "decode", "decode_b1", "decode_output", "output_norm", "layer",
+                                       "backward",
                                        "calls", "cpu"],
                     default=None,
                     help="run one part only (profiling runs); 'calls' makes --calls untimed prefill calls of "
@@ -636,6 +667,10 @@ def main():
         torch.cuda.empty_cache()
     if args.only in (None, "decode_b1") and not args.skip_decode:
         res["decode_b1"] = bench_step_small(1, 8, args.decode_steps, stream)
+    if args.only in (None, "decode_output") and not args.skip_decode:
+        log("decode step with the output gate and norm: fused vs step + output pass")
+        res["decode_output"] = [bench_step_output(256, 8, 256, stream), bench_step_output(1, 8, 256, stream)]
+        torch.cuda.empty_cache()
 
     line = {"metric": METRIC, "value": None, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": None, "higher_is_better": True, "scaling": "weak",
@@ -654,7 +689,7 @@ def main():
                                       "are per call, over the call's mean duration",
                             "flops_per_call": hp["flops_per_call"], "hbm_frac": hp["hbm_frac"]}
         line["prefill"] = hp
-    for key in ("prefill_other", "decode", "decode_b1", "output_norm", "layer", "backward"):
+    for key in ("prefill_other", "decode", "decode_b1", "decode_output", "output_norm", "layer", "backward"):
         if key in res:
             line[key] = res[key]
     if not args.skip_cpu_baseline and args.only in (None, "prefill"):

@@ -208,6 +208,30 @@ mlstm_status mlstm_output_norm_tokens(const void* h_tilde, const void* o_pre, in
                                       void* hip_stream);
 
 /*
+ * One decode step that returns the cell's hidden-state output instead of h~
+ * (Sec. 2, Eqs. 2-5 for the step; Eq. 6 with the output gate of Eq. 9 for the
+ * output; Sec. 3.1, "Fused Generation Kernels"):
+ *
+ *   h_row = sigmoid(o~_row) * (Norm(h~_row) * weight[head] + bias[head])
+ *
+ * with the state update and arguments of mlstm_step, and o~, weight, bias,
+ * eps and norm as in mlstm_output_norm (o_pre [B, NH, DV] in dt).  When one
+ * workgroup owns each sequence (enough sequences to fill the chip, e.g. a
+ * decode batch of 256 x 8 heads) the norm runs on the h~ row in the step
+ * kernel itself, from the unrounded fp32 h~, and h~ never goes to memory;
+ * otherwise the step writes h~ into h and the output pass runs on it in place,
+ * on the same stream.  Limits and state aliasing as mlstm_step, plus DV <=
+ * 2048; h may not overlap o_pre, weight or bias (MLSTM_ERR_ALIAS), a bad eps
+ * or norm is MLSTM_ERR_BAD_SHAPE and a NULL o_pre is MLSTM_ERR_NULL_PTR.
+ */
+mlstm_status mlstm_step_output(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                               const float* ipre, const float* fpre,
+                               const float* C, const float* n, const float* m,
+                               const void* o_pre, const float* weight, const float* bias, float eps,
+                               mlstm_norm norm, int B, int NH, int DQK, int DV,
+                               void* h, float* C_out, float* n_out, float* m_out, void* hip_stream);
+
+/*
  * Gate pre-activations of an mLSTM layer, the inputs ipre and fpre of the two
  * cell entry points (Eq. 11: one input and one forget gate column per head,
  * each with a bias; Eq. 13: the soft-cap; App. B: the reset at document

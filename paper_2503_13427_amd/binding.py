@@ -45,6 +45,9 @@ lib.mlstm_chunkwise_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i]
 lib.mlstm_chunkwise_workspace_bytes.restype = ctypes.c_size_t
 lib.mlstm_step.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp]
 lib.mlstm_step.restype = _i
+lib.mlstm_step_output.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_float, _i, _i, _i,
+                                  _i, _i, _vp, _vp, _vp, _vp, _vp]
+lib.mlstm_step_output.restype = _i
 lib.mlstm_output_norm.argtypes = [_vp, _vp, _i, _vp, _vp, ctypes.c_float, _i, _i, _i, _i, _i, _vp, _vp]
 lib.mlstm_output_norm.restype = _i
 lib.mlstm_output_norm_tokens.argtypes = [_vp, _vp, ctypes.c_int64, _i, _vp, _vp, ctypes.c_float, _i, _i, _i, _i,
@@ -147,6 +150,18 @@ def mlstm_step(q, k, v, ipre, fpre, C, n, m, h, C_out, n_out, m_out, stream=None
     _check(lib.mlstm_step(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre), _ptr(C),
                           _ptr(n), _ptr(m), B, NH, DQK, DV, _ptr(h), _ptr(C_out), _ptr(n_out), _ptr(m_out),
                           _stream(stream)))
+
+
+def mlstm_step_output(q, k, v, ipre, fpre, C, n, m, o_pre, weight, bias, eps: float, norm: str, h, C_out, n_out,
+                      m_out, stream=None) -> None:
+    """One decode step returning h = sigmoid(o~) * (Norm(h~) * weight + bias); o_pre and h [B, NH, DV];
+    weight, bias [NH, DV] fp32 or None; norm "layer" or "rms"; state outputs may be the inputs."""
+    B, NH, DQK = q.shape
+    DV = v.shape[2]
+    code = {"layer": MLSTM_NORM_LAYER, "rms": MLSTM_NORM_RMS}[norm]
+    _check(lib.mlstm_step_output(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre), _ptr(C), _ptr(n),
+                                 _ptr(m), _ptr(o_pre), _ptr(weight), _ptr(bias), float(eps), code, B, NH, DQK, DV,
+                                 _ptr(h), _ptr(C_out), _ptr(n_out), _ptr(m_out), _stream(stream)))
 
 
 def mlstm_output_norm(h_tilde, o_pre, weight, bias, eps: float, norm: str, h, stream=None) -> None:

@@ -31,6 +31,13 @@ hipError_t launch_step(mlstm_dtype dt, const void* q, const void* k, const void*
                        int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
                        hipStream_t stream);
 size_t step_lds_bytes(int DQK, int DV);
+// the step with the output gate and headwise norm of the cell's output (fused when one workgroup
+// owns each sequence's row, else the step and then the output pass in place)
+bool step_output_fused(int B, int NH, int DQK, int DV);
+hipError_t launch_step_output(mlstm_dtype dt, const void* q, const void* k, const void* v, const float* ipre,
+                              const float* fpre, const float* C, const float* n, const float* m, const void* o_pre,
+                              const float* weight, const float* bias, float eps, int rms, int B, int NH, int DQK,
+                              int DV, void* h, float* C_out, float* n_out, float* m_out, hipStream_t stream);
 
 // --- hidden-state output: output gate and headwise norm ----------------------
 constexpr int kOutNormMaxDV = 2048;

@@ -143,10 +143,12 @@ mlstm_status mlstm_chunkwise_fwd_noalloc(const void* q, const void* k, const voi
                               true, hip_stream);
 }
 
-mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,
-                        const float* fpre, const float* C, const float* n, const float* m, int B, int NH,
-                        int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
-                        void* hip_stream) {
+// Validation shared by mlstm_step and mlstm_step_output (extra: the o~, weight and bias ranges
+// of the output variant, which h may not overlap either).
+static mlstm_status step_validate(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,
+                                  const float* fpre, const float* C, const float* n, const float* m, int B, int NH,
+                                  int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
+                                  const Range* extra, int n_extra) {
     if (!q || !k || !v || !ipre || !fpre || !C || !n || !m || !h || !C_out || !n_out || !m_out)
         return MLSTM_ERR_NULL_PTR;
     if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
@@ -169,6 +171,8 @@ mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype
     // h overlaps nothing
     for (const Range& r : {rq, rk, rv, ri, rf, rC, rn, rm, rCo, rno, rmo})
         if (overlap(rh, r)) return MLSTM_ERR_ALIAS;
+    for (int i = 0; i < n_extra; ++i)
+        if (overlap(rh, extra[i])) return MLSTM_ERR_ALIAS;
     // each state output may equal its own input exactly, and overlaps nothing else
     struct Pair {
         Range out;
@@ -180,13 +184,47 @@ mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype
         if (overlap(p.out, p.same) && !p.exact) return MLSTM_ERR_ALIAS;
         for (const Range& r : {rq, rk, rv, ri, rf})
             if (overlap(p.out, r)) return MLSTM_ERR_ALIAS;
+        for (int i = 0; i < n_extra; ++i)
+            if (overlap(p.out, extra[i])) return MLSTM_ERR_ALIAS;
     }
     if (overlap(rCo, rn) || overlap(rCo, rm) || overlap(rno, rC) || overlap(rno, rm) || overlap(rmo, rC) ||
         overlap(rmo, rn) || overlap(rCo, rno) || overlap(rCo, rmo) || overlap(rno, rmo))
         return MLSTM_ERR_ALIAS;
+    return MLSTM_OK;
+}
 
+mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,
+                        const float* fpre, const float* C, const float* n, const float* m, int B, int NH,
+                        int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
+                        void* hip_stream) {
+    const mlstm_status st = step_validate(q, k, v, dt, ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
+                                          nullptr, 0);
+    if (st != MLSTM_OK) return st;
     hipError_t e = mlstm::launch_step(dt, q, k, v, ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
                                       static_cast<hipStream_t>(hip_stream));
+    return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
+mlstm_status mlstm_step_output(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,
+                               const float* fpre, const float* C, const float* n, const float* m,
+                               const void* o_pre, const float* weight, const float* bias, float eps,
+                               mlstm_norm norm, int B, int NH, int DQK, int DV, void* h, float* C_out,
+                               float* n_out, float* m_out, void* hip_stream) {
+    if (!o_pre) return MLSTM_ERR_NULL_PTR;
+    if (!(eps > 0.0f) || eps > 3.0e38f) return MLSTM_ERR_BAD_SHAPE;   // rejects NaN and inf too
+    if (norm != MLSTM_NORM_LAYER && norm != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
+    if (B > 0 && NH > 0 && DV > mlstm::kOutNormMaxDV) return MLSTM_ERR_UNSUPPORTED;
+    if (misaligned(o_pre) || misaligned(weight) || misaligned(bias)) return MLSTM_ERR_MISALIGNED;
+    int64_t S = 0, nw = 0;
+    if (!mul_ok(B, NH, &S) || !mul_ok(NH, DV, &nw)) return MLSTM_ERR_BAD_SHAPE;
+    const Range extra[] = {range_of(o_pre, S * DV * elem_bytes(dt)), range_of(weight, weight ? nw * 4 : 0),
+                           range_of(bias, bias ? nw * 4 : 0)};
+    const mlstm_status st = step_validate(q, k, v, dt, ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
+                                          extra, 3);
+    if (st != MLSTM_OK) return st;
+    hipError_t e = mlstm::launch_step_output(dt, q, k, v, ipre, fpre, C, n, m, o_pre, weight, bias, eps,
+                                             norm == MLSTM_NORM_RMS, B, NH, DQK, DV, h, C_out, n_out, m_out,
+                                             static_cast<hipStream_t>(hip_stream));
     return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
 }
 

@@ -19,6 +19,13 @@
 // and stores along DV; each thread walks a column group down the DQK rows with
 // kBatch rows in flight, and the read-out C'^T q^ is reduced across the row
 // groups in LDS.
+//
+// Output epilogue (mlstm_step_output).  When one workgroup owns a whole sequence and
+// the read-out is reduced in LDS, the workgroup holds the full h~ row, so it can
+// return the cell's hidden-state output instead (Eq. 6 with the output gate of
+// Eq. 9): h = sigmoid(o~) * (Norm(h~) w + b), the headwise LayerNorm or RMSNorm
+// taken over the row in fp32 from the unrounded h~ (two block reductions), and
+// h~ never goes to memory.  Other launches write h~ and the output pass runs after.
 #include "device_common.h"
 #include "launch.h"
 
@@ -29,12 +36,36 @@ constexpr int kBatch = 16;   // rows per pipeline stage
 
 typedef float f4_t __attribute__((ext_vector_type(4)));
 
+// Output epilogue of the fused launch (o == nullptr: the step returns h~)
+template <typename TIn>
+struct StepOut {
+    const TIn* o;        // o~ [heads, DV]
+    const float* w;      // [NH, DV] or nullptr (1)
+    const float* b;      // [NH, DV] or nullptr (0)
+    float eps;
+    int rms;
+    int NH;
+};
+constexpr int kOutPerThread = 4;   // h~ values a thread holds in the epilogue (DV <= 4 * 512)
+
+__device__ __forceinline__ float block_sum(float x, float* wsum) {
+    x = wave_sum(x);
+    __syncthreads();   // wsum may still be read by the previous reduction
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = x;
+    __syncthreads();
+    float t = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kStepThreads / 64; ++w) t += wsum[w];
+    return t;
+}
+
 template <typename TIn>
 __global__ void __launch_bounds__(kStepThreads)
 step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __restrict__ v,
             const float* __restrict__ ipre, const float* __restrict__ fpre,
             const float* C, const float* n, const float* m,
-            int DQK, int DV, int P, TIn* __restrict__ h, float* C_out, float* n_out, float* m_out) {
+            int DQK, int DV, int P, TIn* __restrict__ h, float* C_out, float* n_out, float* m_out,
+            StepOut<TIn> E) {
     extern __shared__ float smem[];
     float* qs = smem;                 // [DQK]   q / sqrt(DQK)
     float* iks = qs + DQK;            // [DQK]   i * k
@@ -162,13 +193,49 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
             reinterpret_cast<float4*>(red)[rg * NC4 + c4] = make_float4(a0, a1, a2, a3);
         }
     }
-    if (RG > 1) {
+    if (RG > 1 && !E.o) {
         __syncthreads();
         TIn* hh = h + head * DV + cv0;
         for (int j = tid; j < DVs; j += kStepThreads) {
             float s = 0.0f;
             for (int r = 0; r < RG; ++r) s += red[r * DVs + j];
             io<TIn>::store(hh, j, s * inv);
+        }
+    } else if (RG > 1) {
+        // the output epilogue (launched only with P == 1, so DVs == DV <= kOutPerThread * 512)
+        __syncthreads();
+        float hv[kOutPerThread];
+        float sum = 0.0f;
+#pragma unroll
+        for (int e = 0; e < kOutPerThread; ++e) {
+            const int j = tid + e * kStepThreads;
+            hv[e] = 0.0f;
+            if (j < DV) {
+                float s = 0.0f;
+                for (int r = 0; r < RG; ++r) s += red[r * DV + j];
+                hv[e] = s * inv;
+                sum += hv[e];
+            }
+        }
+        const float mean = E.rms ? 0.0f : block_sum(sum, wsum) / DV;
+        float sq = 0.0f;
+#pragma unroll
+        for (int e = 0; e < kOutPerThread; ++e)
+            if (tid + e * kStepThreads < DV) sq += (hv[e] - mean) * (hv[e] - mean);
+        const float rstd = rsqrtf(block_sum(sq, wsum) / DV + E.eps);
+        const int hd = static_cast<int>(head % E.NH);
+        TIn* hh = h + head * DV;
+        const TIn* oh = E.o + head * DV;
+#pragma unroll
+        for (int e = 0; e < kOutPerThread; ++e) {
+            const int j = tid + e * kStepThreads;
+            if (j < DV) {
+                float y = (hv[e] - mean) * rstd;
+                if (E.w) y *= E.w[static_cast<int64_t>(hd) * DV + j];
+                if (E.b) y += E.b[static_cast<int64_t>(hd) * DV + j];
+                const float gate = 1.0f / (1.0f + expf(-io<TIn>::load(oh, j)));
+                io<TIn>::store(hh, j, gate * y);
+            }
         }
     }
     if (write_nm && tid == 0) m_out[head] = mnew;
@@ -202,32 +269,60 @@ static int step_splits(int heads, int DV) {
     return P;
 }
 
+template <typename TIn>
+static hipError_t launch_step_t(const void* q, const void* k, const void* v, const float* ipre, const float* fpre,
+                                const float* C, const float* n, const float* m, int heads, int DQK, int DV, int P,
+                                void* h, float* C_out, float* n_out, float* m_out, StepOut<TIn> E,
+                                hipStream_t stream) {
+    const size_t lds = step_lds_bytes(DQK, DV / P);
+    const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(heads) * P));
+    hipLaunchKernelGGL(step_kernel<TIn>, grid, dim3(kStepThreads), lds, stream, static_cast<const TIn*>(q),
+                       static_cast<const TIn*>(k), static_cast<const TIn*>(v), ipre, fpre, C, n, m, DQK, DV, P,
+                       static_cast<TIn*>(h), C_out, n_out, m_out, E);
+    if (P > 1)
+        hipLaunchKernelGGL(step_state_kernel<TIn>, dim3(heads), dim3(256), 0, stream, static_cast<const TIn*>(k),
+                           ipre, fpre, n, m, DQK, n_out, m_out);
+    return hipGetLastError();
+}
+
 hipError_t launch_step(mlstm_dtype dt, const void* q, const void* k, const void* v, const float* ipre,
                        const float* fpre, const float* C, const float* n, const float* m, int B, int NH,
                        int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
                        hipStream_t stream) {
     const int heads = B * NH;
     const int P = step_splits(heads, DV);
-    const size_t lds = step_lds_bytes(DQK, DV / P);
-    const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(heads) * P));
-    if (dt == MLSTM_BF16) {
-        hipLaunchKernelGGL(step_kernel<bf16_t>, grid, dim3(kStepThreads), lds, stream,
-                           static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
-                           static_cast<const bf16_t*>(v), ipre, fpre, C, n, m, DQK, DV, P,
-                           static_cast<bf16_t*>(h), C_out, n_out, m_out);
-        if (P > 1)
-            hipLaunchKernelGGL(step_state_kernel<bf16_t>, dim3(heads), dim3(256), 0, stream,
-                               static_cast<const bf16_t*>(k), ipre, fpre, n, m, DQK, n_out, m_out);
-    } else {
-        hipLaunchKernelGGL(step_kernel<float>, grid, dim3(kStepThreads), lds, stream,
-                           static_cast<const float*>(q), static_cast<const float*>(k),
-                           static_cast<const float*>(v), ipre, fpre, C, n, m, DQK, DV, P,
-                           static_cast<float*>(h), C_out, n_out, m_out);
-        if (P > 1)
-            hipLaunchKernelGGL(step_state_kernel<float>, dim3(heads), dim3(256), 0, stream,
-                               static_cast<const float*>(k), ipre, fpre, n, m, DQK, n_out, m_out);
+    if (dt == MLSTM_BF16)
+        return launch_step_t<bf16_t>(q, k, v, ipre, fpre, C, n, m, heads, DQK, DV, P, h, C_out, n_out, m_out,
+                                     StepOut<bf16_t>{}, stream);
+    return launch_step_t<float>(q, k, v, ipre, fpre, C, n, m, heads, DQK, DV, P, h, C_out, n_out, m_out,
+                                StepOut<float>{}, stream);
+}
+
+bool step_output_fused(int B, int NH, int DQK, int DV) {
+    (void)DQK;
+    const int P = step_splits(B * NH, DV);
+    const int NC4 = DV / 4;
+    return P == 1 && NC4 < kStepThreads && DV <= kOutPerThread * kStepThreads;
+}
+
+hipError_t launch_step_output(mlstm_dtype dt, const void* q, const void* k, const void* v, const float* ipre,
+                              const float* fpre, const float* C, const float* n, const float* m, const void* o_pre,
+                              const float* weight, const float* bias, float eps, int rms, int B, int NH, int DQK,
+                              int DV, void* h, float* C_out, float* n_out, float* m_out, hipStream_t stream) {
+    const int heads = B * NH;
+    if (!step_output_fused(B, NH, DQK, DV)) {
+        // the sequence's row is split over workgroups: h~ into h, then the output pass in place
+        hipError_t e = launch_step(dt, q, k, v, ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out, stream);
+        if (e != hipSuccess) return e;
+        const RowStrides hm{static_cast<int64_t>(NH) * DV, DV, DV};
+        return launch_output_norm(dt, h, o_pre, weight, bias, eps, rms, heads, NH, 1, DV, h, hm, hm, stream);
     }
-    return hipGetLastError();
+    if (dt == MLSTM_BF16)
+        return launch_step_t<bf16_t>(q, k, v, ipre, fpre, C, n, m, heads, DQK, DV, 1, h, C_out, n_out, m_out,
+                                     StepOut<bf16_t>{static_cast<const bf16_t*>(o_pre), weight, bias, eps, rms, NH},
+                                     stream);
+    return launch_step_t<float>(q, k, v, ipre, fpre, C, n, m, heads, DQK, DV, 1, h, C_out, n_out, m_out,
+                                StepOut<float>{static_cast<const float*>(o_pre), weight, bias, eps, rms, NH}, stream);
 }
 
 // LDS of one workgroup owning DVs columns: q^ and i k, then the partial read-outs of its row groups

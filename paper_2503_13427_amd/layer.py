@@ -9,11 +9,11 @@ x [B, T, d] -> y [B, T, d], d = NH * DV:
    sequence (f~ = -inf, App. B), written head-major;
 3. head-major copies of q, k and v, since the cell takes [B, NH, T, D] rows (a decode step,
    with T = 1, takes o~ contiguous as well);
-4. the cell: ``mlstm_chunkwise_fwd`` for a prefill, ``mlstm_step`` for one decode step;
+4. the cell: ``mlstm_chunkwise_fwd`` for a prefill, ``mlstm_step_output`` for one decode step
+   (the step with the output norm of step 5 in its epilogue);
 5. the output norm h = sigmoid(o~) * LayerNorm(h~) * weight, per head: for a prefill
    ``mlstm_output_norm_tokens`` reads o~ in place in the projection output and writes h
-   token-major [B, T, NH, DV], which is already the concatenation of the heads; a decode step
-   uses ``mlstm_output_norm``;
+   token-major [B, T, NH, DV], which is already the concatenation of the heads;
 6. the output projection (bf16 GEMM).
 
 The q, k, v, o~ and output projections are plain library GEMMs around the cell; the gates, the
@@ -134,8 +134,7 @@ class MLSTMLayer:
         ig, fg = self.gates(x)
         C, n, m = state
         h = torch.empty(B, w.NH, w.DV, dtype=torch.bfloat16, device=x.device)
-        mb.mlstm_step(q, k, v, ig, fg, C, n, m, h, C, n, m)
-        mb.mlstm_output_norm(h, o, w.norm_weight, None, self.eps, "layer", h)
+        mb.mlstm_step_output(q, k, v, ig, fg, C, n, m, o, w.norm_weight, None, self.eps, "layer", h, C, n, m)
         return torch.matmul(h.reshape(B, w.NH * w.DV), w.W_proj)
 
 

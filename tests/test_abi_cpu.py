@@ -26,6 +26,7 @@ def declared_functions():
 def test_header_declares_expected_entry_points():
     assert declared_functions() == sorted(["mlstm_chunkwise_fwd", "mlstm_chunkwise_workspace_bytes", "mlstm_step",
                                            "mlstm_chunkwise_fwd_noalloc", "mlstm_chunkwise_scratch_bytes",
+                                           "mlstm_step_output",
                                            "mlstm_output_norm", "mlstm_output_norm_tokens", "mlstm_gate_preact", "mlstm_parallel_bwd",
                                            "mlstm_parallel_bwd_workspace_bytes", "mlstm_status_string",
                                            "mlstm_version"])
@@ -413,3 +414,27 @@ def test_noalloc_validates_like_the_workspace_entry_point(field):
     assert call_chunk_noalloc(a) == 4
     assert call_chunk_noalloc(chunk_args(B=0)) == 2
     assert call_chunk_noalloc(chunk_args(h=fake(1, 64))) == 5
+
+
+# ---- the decode step with the output epilogue ----------------------------------------------------
+
+def step_out_args(**over):
+    a = dict(q=fake(0), k=fake(1), v=fake(2), dt=Bd.MLSTM_BF16, ipre=fake(3), fpre=fake(4), C=fake(5), n=fake(6),
+             m=fake(7), o=fake(8), w=fake(9), b=fake(10), eps=1e-6, norm=0, B=2, NH=8, DQK=256, DV=512, h=fake(11),
+             Co=fake(5), no=fake(6), mo=fake(7), stream=None)
+    a.update(over)
+    return a
+
+
+def call_step_out(a):
+    return lib.mlstm_step_output(a["q"], a["k"], a["v"], a["dt"], a["ipre"], a["fpre"], a["C"], a["n"], a["m"], a["o"],
+                                 a["w"], a["b"], ctypes.c_float(a["eps"]), a["norm"], a["B"], a["NH"], a["DQK"],
+                                 a["DV"], a["h"], a["Co"], a["no"], a["mo"], a["stream"])
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(o=None), 1), (dict(q=None), 1), (dict(eps=0.0), 2), (dict(eps=float("nan")), 2), (dict(norm=5), 2),
+    (dict(DV=4096, DQK=64), 3), (dict(DV=6), 2), (dict(o=fake(8, 2)), 4), (dict(w=fake(9, 4)), 4),
+    (dict(h=fake(8, 16)), 5), (dict(h=fake(9, 64)), 5), (dict(Co=fake(8)), 5)])
+def test_step_output_validation(over, status):
+    assert call_step_out(step_out_args(**over)) == status

@@ -10,6 +10,8 @@ dh [S, T, DV] of the outputs h~ (Eq. 5), from the zero initial state (m_0 = 0):
 * ``recurrent_grad``  the definition: the cell of Sec. 2 (Eqs. 2-5 with Eqs. 7-8) written step
                       by step in torch fp64, differentiated by autograd.  A library primitive
                       (reverse-mode differentiation) supplies the derivative of that code.
+                      ``recurrent_grad_state`` is the same from a given initial state
+                      (C0, n0, m0), and also returns the gradients of C0, n0 and m0.
 * ``parallel_grad``   the same gradients in closed form over the parallel form (Eq. 10), written
                       out from the chain rule (below), with every exponential taken relative to
                       the row's max state so that each weight is <= 1.
@@ -40,13 +42,15 @@ import numpy as np
 import torch
 
 
-def _recurrent_torch(q, k, v, ip, fp):
-    """Eqs. 2-5, 7-8 step by step from the zero state (m_0 = 0), differentiable."""
+def _recurrent_torch(q, k, v, ip, fp, C=None, n=None, m=None):
+    """Eqs. 2-5, 7-8 step by step from (C, n, m), the zero state (m_0 = 0) when not given,
+    differentiable."""
     S, T, DQK = q.shape
     DV = v.shape[2]
-    C = torch.zeros(S, DQK, DV, dtype=torch.float64)
-    n = torch.zeros(S, DQK, dtype=torch.float64)
-    m = torch.zeros(S, dtype=torch.float64)
+    if C is None:
+        C = torch.zeros(S, DQK, DV, dtype=torch.float64)
+        n = torch.zeros(S, DQK, dtype=torch.float64)
+        m = torch.zeros(S, dtype=torch.float64)
     hs = []
     for t in range(T):
         a = torch.nn.functional.logsigmoid(fp[:, t])
@@ -69,6 +73,19 @@ def recurrent_grad(q, k, v, ip, fp, dh):
     h = _recurrent_torch(*ts)
     (h * torch.tensor(np.asarray(dh, dtype=np.float64))).sum().backward()
     return tuple(t.grad.numpy() for t in ts)
+
+
+def recurrent_grad_state(q, k, v, ip, fp, C0, n0, m0, dh):
+    """Gradients of sum(h * dh) with respect to q, k, v, ipre, fpre and the initial state C0 [S, DQK, DV],
+    n0 [S, DQK], m0 [S] (fp64 numpy arrays).  A forget gate of zero (f~ = -inf) restarts the state; its
+    own f~ gradient is zero (sigmoid has zero slope there)."""
+    xs = (q, k, v, ip, fp, C0, n0, m0)
+    ts = [torch.tensor(np.asarray(x, dtype=np.float64), requires_grad=True) for x in xs]
+    h = _recurrent_torch(*ts)
+    (h * torch.tensor(np.asarray(dh, dtype=np.float64))).sum().backward()
+    out = [t.grad.numpy() for t in ts]
+    out[4] = np.where(np.isneginf(np.asarray(fp)), 0.0, out[4])
+    return tuple(out)
 
 
 def _logsigmoid(x):

@@ -89,3 +89,63 @@ def test_planted_mistakes_fail():
         exec(compile(bad, "planted", "exec"), ns)
         got = ns["parallel_grad"](q, k, v, ip, fp, dh)
         assert not all(np.allclose(x, y, rtol=1e-6, atol=1e-9) for x, y in zip(ref, got))
+
+
+def _state(seed, S, DQK, DV):
+    rng = np.random.default_rng(seed)
+    return rng.normal(0, 0.3, (S, DQK, DV)), np.abs(rng.standard_normal((S, DQK))), rng.standard_normal(S)
+
+
+@pytest.mark.parametrize("dist", list(DISTS))
+def test_state_grad_matches_finite_differences(dist):
+    """recurrent_grad_state against central differences of the NumPy recurrent form, for every input
+    including the initial state (C0, n0, m0)."""
+    q, k, v, ip, fp, dh = inputs(3, **DISTS[dist])
+    C0, n0, m0 = _state(4, 2, 3, 2)
+    grads = G.recurrent_grad_state(q, k, v, ip, fp, C0, n0, m0, dh)
+    args = [q, k, v, ip, fp, C0, n0, m0]
+
+    def L(a):
+        h, *_ = R.recurrent(*a[:5], a[5], a[6], a[7])
+        return float((h * dh).sum())
+    eps = 1e-6
+    for j, (x, g) in enumerate(zip(args, grads)):
+        x = np.asarray(x, dtype=np.float64)
+        num = np.zeros_like(x)
+        for idx in np.ndindex(x.shape):
+            xp = x.copy(); xp[idx] += eps
+            xm = x.copy(); xm[idx] -= eps
+            ap = list(args); ap[j] = xp
+            am = list(args); am[j] = xm
+            num[idx] = (L(ap) - L(am)) / (2 * eps)
+        np.testing.assert_allclose(g, num, rtol=1e-6, atol=1e-7 * max(1.0, np.abs(num).max()), err_msg=str(j))
+
+
+def test_state_grad_with_zero_state_is_recurrent_grad():
+    """From (C0, n0, m0) = (0, 0, 0) the five input gradients are those of recurrent_grad."""
+    q, k, v, ip, fp, dh = inputs(5)
+    S, T, DQK = q.shape
+    DV = v.shape[2]
+    a = G.recurrent_grad_state(q, k, v, ip, fp, np.zeros((S, DQK, DV)), np.zeros((S, DQK)), np.zeros(S), dh)
+    b = G.recurrent_grad(q, k, v, ip, fp, dh)
+    for x, y in zip(a[:5], b):
+        np.testing.assert_allclose(x, y, rtol=1e-12, atol=1e-14)
+
+
+def test_state_grad_with_borders():
+    """f~ = -inf (a document border): the gradients stay finite, nothing before the border reaches it
+    (with a border on the first token the initial state gets no gradient), and the gradients of the
+    tokens after the last border equal those of a fresh run of those tokens from the zero state."""
+    q, k, v, ip, fp, dh = inputs(6, S=1, T=9)
+    C0, n0, m0 = _state(7, 1, 3, 2)
+    fp = fp.copy()
+    fp[0, [0, 5]] = -np.inf
+    g = G.recurrent_grad_state(q, k, v, ip, fp, C0, n0, m0, dh)
+    for x in g:
+        assert np.isfinite(x).all()
+    assert np.abs(g[5]).max() == 0 and np.abs(g[6]).max() == 0 and g[7][0] == 0
+    assert g[4][0, 0] == 0 and g[4][0, 5] == 0
+    tail = G.recurrent_grad_state(q[:, 5:], k[:, 5:], v[:, 5:], ip[:, 5:], fp[:, 5:], np.zeros((1, 3, 2)),
+                                  np.zeros((1, 3)), np.zeros(1), dh[:, 5:])
+    for x, y in zip(g[:5], tail[:5]):
+        np.testing.assert_allclose(x[:, 5:], y, rtol=1e-10, atol=1e-12)

@@ -292,6 +292,52 @@ mlstm_status mlstm_parallel_bwd(const void* q, const void* k, const void* v, mls
                                 float* dq, float* dk, float* dv, float* dipre, float* dfpre,
                                 void* workspace, size_t workspace_bytes, void* hip_stream);
 
+/*
+ * Chunkwise backward pass of the cell for training (Sec. 2, "Training Mode";
+ * App. D.2 counts it as twice the forward's work): the gradients of a loss
+ * with respect to q, k, v, ipre, fpre and the initial state, given its
+ * gradient dh with respect to the outputs h~ of mlstm_chunkwise_fwd on the same
+ * inputs.  The entry state of every 64-token chunk is recomputed (the forward's
+ * segment passes), then per chunk the intra-chunk terms, the terms through the
+ * entry state, and the gradient of the state (C, n) carried backwards through
+ * the chunk recurrence of App. D.1; document borders (fpre = -inf, App. B)
+ * restart that recurrence as in the forward.  The forward's output is not
+ * needed: dh . h~ is formed from the recomputed numerator in fp32.  Products
+ * run on bf16 MFMA with fp32 accumulation; the recomputed states and the
+ * state gradients enter them as bf16 hi + lo pairs.  No float atomics: the
+ * result is deterministic.
+ *
+ *   q, k [B, NH, T, DQK], v [B, NH, T, DV] (dt)   ipre, fpre [B, NH, T] fp32
+ *   C0 [B, NH, DQK, DV], n0 [B, NH, DQK], m0 [B, NH] fp32: the forward's
+ *        initial state, or all NULL for the zero state (m0 = 0)
+ *   dh [B, NH, T, DV] (dt): the gradient of the loss with respect to h~
+ *   dq, dk [B, NH, T, DQK], dv [B, NH, T, DV], dipre, dfpre [B, NH, T] fp32
+ *   dC0 [B, NH, DQK, DV], dn0 [B, NH, DQK], dm0 [B, NH] fp32: the gradients
+ *        of the initial state (also of the zero state), or all NULL
+ *   workspace: device scratch of at least mlstm_chunkwise_bwd_workspace_bytes
+ *   bytes (else MLSTM_ERR_WORKSPACE); its contents on entry do not matter.
+ *   About 1 MiB per 64 tokens per (batch, head) plus 36 bytes per token.
+ *
+ * The loss is taken not to depend on the final state (CT, nT, mT).  dfpre is
+ * zero where fpre = -inf.  A partially given initial state or gradient
+ * triple is MLSTM_ERR_NULL_PTR.
+ *
+ * Built: dt = MLSTM_BF16, DQK = 256, DV = 512, L = 64 (the backward's own
+ * chunk length, independent of the forward call's), T DV 2 < 2^31 and
+ * B NH <= 65535 (else MLSTM_ERR_UNSUPPORTED).  T == 0 launches at most a fill
+ * of zeros into dC0, dn0, dm0.  No output may overlap an input, another
+ * output or the workspace (MLSTM_ERR_ALIAS).
+ */
+size_t mlstm_chunkwise_bwd_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L, mlstm_dtype dt);
+mlstm_status mlstm_chunkwise_bwd(const void* q, const void* k, const void* v, mlstm_dtype dt,
+                                 const float* ipre, const float* fpre,
+                                 const float* C0, const float* n0, const float* m0,
+                                 int B, int NH, int T, int DQK, int DV, int L,
+                                 const void* dh,
+                                 float* dq, float* dk, float* dv, float* dipre, float* dfpre,
+                                 float* dC0, float* dn0, float* dm0,
+                                 void* workspace, size_t workspace_bytes, void* hip_stream);
+
 /* Static, human-readable name of a status code. */
 const char* mlstm_status_string(mlstm_status s);
 

@@ -60,6 +60,11 @@ lib.mlstm_parallel_bwd_workspace_bytes.restype = ctypes.c_size_t
 lib.mlstm_parallel_bwd.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp,
                                    ctypes.c_size_t, _vp]
 lib.mlstm_parallel_bwd.restype = _i
+lib.mlstm_chunkwise_bwd_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i]
+lib.mlstm_chunkwise_bwd_workspace_bytes.restype = ctypes.c_size_t
+lib.mlstm_chunkwise_bwd.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp,
+                                    _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+lib.mlstm_chunkwise_bwd.restype = _i
 lib.mlstm_status_string.argtypes = [_i]
 lib.mlstm_status_string.restype = ctypes.c_char_p
 lib.mlstm_version.argtypes = []
@@ -227,3 +232,25 @@ def mlstm_parallel_bwd(q, k, v, ipre, fpre, dh, dq, dk, dv, dipre, dfpre, worksp
     _check(lib.mlstm_parallel_bwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre), _ptr(dh), B, NH, T,
                                   DQK, DV, _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dipre), _ptr(dfpre), _ptr(workspace),
                                   ws_bytes, _stream(stream)))
+
+
+def mlstm_chunkwise_bwd_workspace_bytes(B: int, NH: int, T: int, DQK: int, DV: int, L: int,
+                                        dtype: torch.dtype = torch.bfloat16) -> int:
+    code = MLSTM_BF16 if dtype == torch.bfloat16 else MLSTM_F32
+    return int(lib.mlstm_chunkwise_bwd_workspace_bytes(B, NH, T, DQK, DV, L, code))
+
+
+def mlstm_chunkwise_bwd(q, k, v, ipre, fpre, C0, n0, m0, L, dh, dq, dk, dv, dipre, dfpre, dC0, dn0, dm0,
+                        workspace, stream=None) -> None:
+    """Gradients of a loss with respect to q, k, v [B, NH, T, D] (bf16), ipre, fpre [B, NH, T] and the
+    initial state (C0, n0, m0, or all None), given dh [B, NH, T, DV] (bf16), the loss's gradient with
+    respect to the forward's output h~;
+    outputs fp32 of the input shapes, dC0/dn0/dm0 all None when not wanted; workspace: uint8 tensor
+    of mlstm_chunkwise_bwd_workspace_bytes bytes."""
+    B, NH, T, DQK = q.shape
+    DV = v.shape[3]
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib.mlstm_chunkwise_bwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(ipre), _ptr(fpre), _ptr(C0),
+                                   _ptr(n0), _ptr(m0), B, NH, T, DQK, DV, L, _ptr(dh), _ptr(dq), _ptr(dk),
+                                   _ptr(dv), _ptr(dipre), _ptr(dfpre), _ptr(dC0), _ptr(dn0), _ptr(dm0),
+                                   _ptr(workspace), ws_bytes, _stream(stream)))

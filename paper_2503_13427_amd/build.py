@@ -21,7 +21,7 @@ ARCH = "gfx950"
 
 SOURCES = ["mlstm_abi.cpp", "mlstm_step.hip", "mlstm_chunkwise_f32.hip", "mlstm_chunkwise_mfma.hip",
            "mlstm_output_norm.hip", "mlstm_gate_preact.hip",
-           "mlstm_parallel_bwd.hip"]
+           "mlstm_parallel_bwd.hip", "mlstm_chunkwise_bwd.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Wall", "-Wno-unused-result"]
 NO_PACKED_FP32 = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -90,6 +90,26 @@ bool chunk_mfma_supported(mlstm_dtype dt, int DQK, int DV, int L);
 int chunk_mfma_segments(int B, int NH, int T, int L);
 size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L);
 hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream);
+// State entering every 64-token chunk c >= 1 (slots: S (NC - 1) segment slots; rowhl: the same C as
+// bf16 hi + lo rows, S (NC - 1) x 2 x DQK x DV)
+hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, uint16_t* rowhl, hipStream_t stream);
+// --- chunkwise backward (bf16, DQK = 256, DV = 512, L = 64) --------------------
+bool chunk_bwd_supported(mlstm_dtype dt, int DQK, int DV, int L);
+size_t chunk_bwd_workspace_bytes(int B, int NH, int T);
+struct ChunkBwdArgs {
+    ChunkArgs f;             // forward inputs (q, k, v, gates, initial state), sizes, L
+    const void* dh;          // [B, NH, T, DV] (dt)
+    float* dq;
+    float* dk;
+    float* dv;
+    float* dipre;
+    float* dfpre;
+    float* dC0;              // NULL: the initial-state gradients are not wanted
+    float* dn0;
+    float* dm0;
+};
+hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t stream);
+
 // Fixed device scratch of mlstm_chunkwise_fwd_noalloc: a file-scope device array of this many bytes,
 // one copy per device.  chunk_scratch gives its address on the current device (looked up once per
 // device, then cached).

@@ -47,7 +47,7 @@ const char* mlstm_status_string(mlstm_status s) {
         case MLSTM_ERR_MISALIGNED: return "MLSTM_ERR_MISALIGNED: a tensor pointer is not 16-byte aligned";
         case MLSTM_ERR_ALIAS: return "MLSTM_ERR_ALIAS: an output overlaps an input or another output";
         case MLSTM_ERR_WORKSPACE:
-            return "MLSTM_ERR_WORKSPACE: workspace smaller than mlstm_chunkwise_workspace_bytes, or (no-allocation "
+            return "MLSTM_ERR_WORKSPACE: workspace smaller than the call's *_workspace_bytes, or (no-allocation "
                    "variant) more than the library's fixed scratch of mlstm_chunkwise_scratch_bytes";
         case MLSTM_ERR_HIP: return "MLSTM_ERR_HIP: the HIP runtime reported an error at launch";
     }
@@ -361,6 +361,71 @@ mlstm_status mlstm_parallel_bwd(const void* q, const void* k, const void* v, mls
     if (T == 0) return MLSTM_OK;
     hipError_t e = mlstm::launch_parallel_bwd(dt, q, k, v, ipre, fpre, dh, B, NH, T, DQK, DV, dq, dk, dv, dipre,
                                               dfpre, workspace, static_cast<hipStream_t>(hip_stream));
+    return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
+}
+
+size_t mlstm_chunkwise_bwd_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L, mlstm_dtype dt) {
+    if (B <= 0 || NH <= 0 || T < 0 || !mlstm::chunk_bwd_supported(dt, DQK, DV, L)) return 0;
+    return mlstm::chunk_bwd_workspace_bytes(B, NH, T);
+}
+
+mlstm_status mlstm_chunkwise_bwd(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,
+                                 const float* fpre, const float* C0, const float* n0, const float* m0, int B, int NH,
+                                 int T, int DQK, int DV, int L, const void* dh, float* dq, float* dk,
+                                 float* dv, float* dipre, float* dfpre, float* dC0, float* dn0, float* dm0,
+                                 void* workspace, size_t workspace_bytes, void* hip_stream) {
+    if (B <= 0 || NH <= 0 || T < 0 || DQK <= 0 || DV <= 0 || L <= 0) return MLSTM_ERR_BAD_SHAPE;
+    if (T != 0) {
+        const void* req[] = {q, k, v, ipre, fpre, dh, dq, dk, dv, dipre, dfpre, workspace};
+        for (const void* p : req)
+            if (!p) return MLSTM_ERR_NULL_PTR;
+    }
+    const int n_init = (C0 != nullptr) + (n0 != nullptr) + (m0 != nullptr);
+    const int n_grad = (dC0 != nullptr) + (dn0 != nullptr) + (dm0 != nullptr);
+    if ((n_init != 0 && n_init != 3) || (n_grad != 0 && n_grad != 3)) return MLSTM_ERR_NULL_PTR;
+    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    int64_t S, nt, nqk, nv, nC, nn;
+    if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &nt) || !mul_ok(nt, DQK, &nqk) || !mul_ok(nt, DV, &nv) ||
+        !mul_ok(S, static_cast<int64_t>(DQK) * DV, &nC) || !mul_ok(S, DQK, &nn))
+        return MLSTM_ERR_BAD_SHAPE;
+    if (!mlstm::chunk_bwd_supported(dt, DQK, DV, L)) return MLSTM_ERR_UNSUPPORTED;
+    // one sequence's rows are addressed through 32-bit buffer ranges; the state scan has one grid row
+    // per sequence; the chunk passes launch 4 workgroups per (sequence, chunk)
+    if (static_cast<int64_t>(T) * DV * 2 >= (int64_t(1) << 31) || S > 65535 ||
+        S * ((static_cast<int64_t>(T) + 63) / 64) * 4 > INT32_MAX)
+        return MLSTM_ERR_UNSUPPORTED;
+    const size_t ws_need = mlstm::chunk_bwd_workspace_bytes(B, NH, T);
+    if (T != 0 && workspace_bytes < ws_need) return MLSTM_ERR_WORKSPACE;
+    const void* ptrs[] = {q, k, v, ipre, fpre, C0, n0, m0, dh, dq, dk, dv, dipre, dfpre, dC0, dn0, dm0, workspace};
+    for (const void* p : ptrs)
+        if (misaligned(p)) return MLSTM_ERR_MISALIGNED;
+    const size_t eb = elem_bytes(dt);
+    const Range ins[] = {range_of(q, nqk * eb), range_of(k, nqk * eb), range_of(v, nv * eb), range_of(ipre, nt * 4),
+                         range_of(fpre, nt * 4), range_of(C0, C0 ? nC * 4 : 0), range_of(n0, n0 ? nn * 4 : 0),
+                         range_of(m0, m0 ? S * 4 : 0), range_of(dh, nv * eb)};
+    const Range outs[] = {range_of(dq, nqk * 4), range_of(dk, nqk * 4), range_of(dv, nv * 4),
+                          range_of(dipre, nt * 4), range_of(dfpre, nt * 4), range_of(dC0, dC0 ? nC * 4 : 0),
+                          range_of(dn0, dn0 ? nn * 4 : 0), range_of(dm0, dm0 ? S * 4 : 0),
+                          range_of(workspace, T != 0 ? ws_need : 0)};
+    const size_t nouts = sizeof(outs) / sizeof(outs[0]);
+    for (size_t a = 0; a < nouts; ++a) {
+        for (const Range& r : ins)
+            if (overlap(outs[a], r)) return MLSTM_ERR_ALIAS;
+        for (size_t b = a + 1; b < nouts; ++b)
+            if (overlap(outs[a], outs[b])) return MLSTM_ERR_ALIAS;
+    }
+    mlstm::ChunkBwdArgs a{};
+    a.f = mlstm::ChunkArgs{q, k, v, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, nullptr, nullptr, nullptr, nullptr};
+    a.dh = dh;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.dipre = dipre;
+    a.dfpre = dfpre;
+    a.dC0 = dC0;
+    a.dn0 = dn0;
+    a.dm0 = dm0;
+    hipError_t e = mlstm::launch_chunk_bwd(a, workspace, static_cast<hipStream_t>(hip_stream));
     return e == hipSuccess ? MLSTM_OK : MLSTM_ERR_HIP;
 }
 

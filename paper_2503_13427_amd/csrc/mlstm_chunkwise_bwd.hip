@@ -1,0 +1,926 @@
+// Chunkwise backward of the mLSTM cell on bf16 MFMA for the xLSTM 7B head shape
+// (DQK = 256, DV = 512), chunk length 64: the gradients of sum(h~ . dh) with respect to
+// q, k, v, the gate pre-activations and the initial state (C0, n0, m0).
+//
+// Math.  Per chunk c with entry state (C, n, m_prev) (stabilised by m_prev), the gates of the
+// forward (in-chunk prefix sums b, x = i~ - b, last restart R_tau, M_tau, key weights
+// w_tau = exp(x_tau - M_L), decay = exp(m_prev - M_L)), g_tau = exp(m_prev - M_tau) and
+// floor_tau = exp(-(b_tau + M_tau)) (App. D.1), with q^ = q / sqrt(DQK):
+//
+//   S = Q^ K^T,  E_ts = exp(x_s - M_t) for R_t <= s <= t (else 0),  St = S o E
+//   D_t = g_t (q^_t . n) + sum_s St_ts,  den_t = max(|D_t|, floor_t),  h~_t = N_t / den_t with
+//   N_t = g_t (C^T q^_t) + sum_s St_ts v_s
+//   U = dH / den (rows),  w_t = -(dh_t . N_t) sign(D_t) / den_t^2  where |D_t| > floor_t, else 0
+//   P = E o (U V^T + w 1^T)
+//   dq^ = P K + diag(g) (U C^T + w n^T),   dk = P^T Q^ + diag(wkey) (V Gam^T + 1 gam^T),
+//   dv  = St^T U + diag(wkey) K Gam,
+// where (Gam_c, gam_c) is the gradient reaching chunk c's exit state (C_c, n_c), in the units of
+// its stabiliser, from all later chunks; it runs backwards through the state recurrence of
+// Eqs. 3-4 in chunk form:
+//   Gam_{c-1} = decay_c Gam_c + L_c,   L_c = Q^T diag(g / den) dH,
+//   gam_{c-1} = decay_c gam_c + z_c,   z_c = Q^T (g o w) / sqrt(DQK)
+// (Gam of the last chunk is zero; Gam_{-1}, gam_{-1} are the gradients of C0 and n0, and
+// dm0 = <Gam_{-1}, C0> + gam_{-1} . n0 since the unstabilised state is e^{m0} (C0, n0)).
+// The gate gradients follow from the two row sums r_t = q_t . dq_t and c_t = k_t . dk_t:
+//   di~_t = c_t,  dlogsig(f~_t) = sum_{t' >= t} (r_t' - c_t'),  df~_t = that times sigmoid(-f~_t)
+// (a forget gate of zero, f~ = -inf, is a restart; its own gradient is zero).
+//
+// dh_t . N_t is formed in fp32 from its two parts, g_t q^_t . (C dh_t) and sum_s St_ts (dh_t . v_s),
+// rather than from the forward's rounded h~: where the two terms of dq nearly cancel, the bf16
+// rounding of h~ would dominate the result.  The forward's output is not an input.
+//
+// Passes (one stream, in order):
+//   states  the forward's local-state and combine passes over one-chunk segments leave the entry
+//           state of every chunk c >= 1 (fp32 C, n, m, and C as bf16 hi + lo rows)
+//   dhc     one workgroup per (chunk, 64-row d tile): X = dH C^T on the entry state's hi + lo rows
+//           (kept in dq) and the tile's share of q^_t . X_t
+//   intra   one workgroup per chunk: gates, S, D, den; per 128-column piece of dv, (dH V^T), the
+//           intra term of dv and the piece's columns of L_c; then w, P, dq (complete), the intra
+//           term of dk and z_c; writes the key weights, the chunk's decay and q_t . dq_t
+//   scan    the reverse recurrence of (Gam, gam), elementwise over the state, writing Gam_c as
+//           bf16 hi + lo rows; dC0, dn0 and partial sums of dm0
+//   interkv one workgroup per (chunk, tile): dk of a 64-row d tile and dv of a 128-column v
+//           tile from Gam_c; the partial k . dk of the tile
+//   gates   one workgroup per sequence: the reverse prefix sums of r - c, di~ and df~, dm0
+//
+// MFMA mapping (16x16x32 bf16, fp32 accumulate): lane (l16, g16) holds A[m = l16][k = 8 g16 + 0..7]
+// and B[k = 8 g16 + 0..7][n = l16] and receives D[m = 4 g16 + 0..3][n = l16].  An operand whose
+// contraction index is contiguous in memory is one 16-byte row read; otherwise it comes from a
+// row-major [k][n] tile in LDS through the transpose read.  Every product is arranged so that its
+// output lane holds four consecutive elements of one output row (one 16-byte store).
+//
+// Rows past the end of the sequence (a partial last chunk) are read through buffer resources with
+// the row offset in the range-checked offset, so they read as zero.
+#include "launch.h"
+#include "mfma_common.h"
+
+namespace mlstm {
+namespace {
+
+constexpr int kBL = 64;                                   // tokens per chunk
+constexpr int kBT = 256;                                  // threads per workgroup (4 waves)
+constexpr int kQP = kDQK + 8;                             // LDS pitch of Q, K rows (528 bytes)
+constexpr int kPP = kBL + 8;                              // LDS pitch of [tau][sigma] tiles (144 bytes)
+constexpr int kWP = 128 + 8;                              // LDS pitch of 128-column pieces (272 bytes)
+constexpr int kHP = kDV + 8;                              // LDS pitch of full dv rows (1040 bytes)
+constexpr int64_t kCV = static_cast<int64_t>(kDQK) * kDV; // elements of one state matrix
+constexpr int64_t kLzFloats = kCV + kDQK;                 // L_c then z_c
+constexpr int kScanE4 = static_cast<int>(kLzFloats / 4);  // float4 items of the reverse scan
+constexpr int kScanBlocks = (kScanE4 + 255) / 256;
+constexpr int kTokF = 1;                                  // per-token floats: the key weight
+constexpr int kPartF = 8;                                 // per-token partial sums: q^.X x 4 (then q.dq), k.dk x 4
+
+struct BwdParams {
+    const uint16_t* q;
+    const uint16_t* k;
+    const uint16_t* v;
+    const uint16_t* dh;
+    const float* ipre;
+    const float* fpre;
+    const float* C0;     // NULL: zero initial state (with n0, m0)
+    const float* n0;
+    const float* m0;
+    float* dq;
+    float* dk;
+    float* dv;
+    float* dip;
+    float* dfp;
+    float* dC0;          // NULL: not requested (with dn0, dm0)
+    float* dn0;
+    float* dm0;
+    float* slots;        // S (NC - 1) state slots: entry state of chunk c in slot c - 1, then L_c, z_c
+    uint16_t* hl;        // S (NC - 1) x 2 x DQK x DV: C of slot c as bf16 hi + lo rows, then Gam_c
+    float* lz0;          // S x (DQK DV + DQK): L_0, z_0
+    float* gamn;         // S x NC x DQK: gam_c
+    float* tok;          // S x T x kTokF
+    float* part;         // S x T x kPartF
+    float* chunk;        // S x NC: decay of each chunk
+    float* dmp;          // S x kScanBlocks: partial sums of dm0
+    int T;
+    int NC;
+};
+
+__device__ __forceinline__ float* lz_of(const BwdParams& A, int s, int c) {
+    return c ? A.slots + (static_cast<int64_t>(s) * (A.NC - 1) + c - 1) * kSlotFloats
+             : A.lz0 + static_cast<int64_t>(s) * kLzFloats;
+}
+__device__ __forceinline__ uint16_t* hl_of(const BwdParams& A, int s, int slot) {
+    return A.hl + (static_cast<int64_t>(s) * (A.NC - 1) + slot) * 2 * kCV;
+}
+
+__device__ __forceinline__ u32x4_t lds16(const uint16_t* p) { return *reinterpret_cast<const u32x4_t*>(p); }
+__device__ __forceinline__ u32x2_t lds_u32x2(const uint16_t* p) { return *reinterpret_cast<const u32x2_t*>(p); }
+// operand whose contraction index runs along LDS rows: lane gets row r0 + l16, k = k0 + 8 g16 + 0..7
+__device__ __forceinline__ u32x4_t row_op(const uint16_t* base, int pitch, int r0, int k0, int lane) {
+    return lds16(base + (r0 + (lane & 15)) * pitch + k0 + 8 * (lane >> 4));
+}
+// operand from a row-major [k][n] LDS tile: lane gets column n0 + l16, k = k0 + 8 g16 + 0..7
+__device__ __forceinline__ u32x4_t tr_op(const uint16_t* base, int pitch, int k0, int n0, int lane) {
+    const int g16 = lane >> 4, l16 = lane & 15;
+    const uint16_t* p = base + (k0 + 8 * g16 + (l16 >> 2)) * pitch + n0 + 4 * (l16 & 3);
+    return cat(tr_read(p), tr_read(p + 4 * pitch));
+}
+__device__ __forceinline__ float bf_at(const u32x4_t& w, int e) {
+    return (e & 1) ? hi_f32(w[e >> 1]) : lo_f32(w[e >> 1]);
+}
+// fp32 -> bf16 hi + lo parts of 8 values, packed as two MFMA operands
+__device__ __forceinline__ void split8(const float4& a, const float4& b, u32x4_t& hi, u32x4_t& lo) {
+    const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        hi[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
+        lo[i] = pack_bf16x2(x[2 * i] - lo_f32(hi[i]), x[2 * i + 1] - hi_f32(hi[i]));
+    }
+}
+__device__ __forceinline__ float wave_total(float x) { return lane63(wave_incl_sum(x)); }
+
+// rows t0 .. t0 + 63, columns col0 .. col0 + NCOL - 1 of a [T][row_elems] bf16 matrix into LDS
+template <int NCOL>
+__device__ __forceinline__ void stage_rows(uint16_t* dst, int pitch, __amdgpu_buffer_rsrc_t r, int row_elems, int t0,
+                                           int col0, int tid) {
+    constexpr int PPR = NCOL / 8, N = kBL * PPR / kBT;
+    u32x4_t tmp[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int e = tid + kBT * i, row = e / PPR, pc = e % PPR;
+        tmp[i] = bload128(r, static_cast<uint32_t>((t0 + row) * row_elems + col0 + 8 * pc) * 2u, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int e = tid + kBT * i, row = e / PPR, pc = e % PPR;
+        *reinterpret_cast<u32x4_t*>(dst + row * pitch + 8 * pc) = tmp[i];
+    }
+}
+
+// ---- gates of one chunk (one wave, lane = row) -------------------------------------------------
+struct BGate {
+    float x, M, g, fl, wk;
+    int R;
+};
+__device__ __forceinline__ void bwd_gates(__amdgpu_buffer_rsrc_t ig, __amdgpu_buffer_rsrc_t fg, int T, int t0,
+                                          float m_prev, int lane, BGate& G, float& decay) {
+    const int t = t0 + lane;
+    const bool ok = t < T;
+    const uint32_t off = static_cast<uint32_t>(t) * 4u;
+    const float fv = bloadf(fg, off, 0), iv = bloadf(ig, off, 0);
+    const float lg = ok ? flogsig(fv) : 0.0f;
+    const bool rs = (lg == -INFINITY);
+    const bool any = __builtin_amdgcn_ballot_w64(rs) != 0;
+    const float b = wave_incl_sum(rs ? 0.0f : lg);
+    const float x = ok ? iv - b : -INFINITY;
+    float r = -1.0f, p;
+    if (any) {
+        r = wave_incl_max(rs ? static_cast<float>(lane) : -1.0f);
+        p = wave_seg_incl_max(x, rs);
+    } else {
+        p = wave_incl_max(x);
+    }
+    const float pL = lane63(p), rL = lane63(r);
+    const bool restart = rL >= 0.0f;
+    const float ML = restart ? pL : fmaxf(m_prev, pL);
+    const bool fresh = r >= 0.0f;
+    const float M = fresh ? p : fmaxf(m_prev, p);
+    G.x = x;
+    G.M = M;
+    G.R = static_cast<int>(r);
+    G.g = (fresh || M == -INFINITY) ? 0.0f : fexp(m_prev - M);
+    G.fl = fexp(-(b + M));
+    const bool none = (x == -INFINITY) || (static_cast<float>(lane) < rL);
+    G.wk = none ? 0.0f : fexp(x - ML);
+    decay = (restart || ML == -INFINITY || m_prev == -INFINITY) ? 0.0f : fexp(m_prev - ML);
+}
+
+// ---- dH C^T: the entry state's share of dq ----------------------------------------------------
+struct DhcSmem {
+    uint16_t dH[kBL * kHP];
+    float red[4][kBL];
+};
+static_assert(sizeof(DhcSmem) <= 160 * 1024, "LDS budget");
+
+// One workgroup per (chunk, 64-row d tile): X = dH C^T on the entry state's hi + lo rows, stored in dq
+// (the intra pass scales it by g / den and adds the rest), and the tile's share of q^_t . X_t.
+__global__ void __launch_bounds__(kBT) bwd_dhc_kernel(BwdParams A) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+    DhcSmem& S = *reinterpret_cast<DhcSmem*>(smem_raw);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g16 = lane >> 4, l16 = lane & 15;
+    const int wi = work_index();
+    const int j = wi % 4, c = (wi / 4) % A.NC, s = wi / 4 / A.NC;
+    const int T = A.T, t0 = c * kBL, d0 = 64 * j;
+    const int64_t st = static_cast<int64_t>(s) * T;
+    const auto rdh = make_rsrc(A.dh + st * kDV, static_cast<uint32_t>(T) * kDV * 2);
+    const bool has_c = (c > 0) || (A.C0 != nullptr);
+
+    if (has_c) stage_rows<kDV>(S.dH, kHP, rdh, kDV, t0, 0, tid);
+    __syncthreads();
+    // X^T [d][tau] = sum_v C[d][v] dH[tau][v]; rows d = d0 + 16 wave + l16 of the entry state
+    f32x4_t acc[4];
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) acc[tb] = f32x4_t{};
+    const int drow = d0 + 16 * wave + l16;
+    if (c > 0) {
+        const uint16_t* hi = hl_of(A, s, c - 1) + static_cast<int64_t>(drow) * kDV + 8 * g16;
+        const uint16_t* lo = hi + kCV;
+#pragma unroll 4
+        for (int ks = 0; ks < kDV / 32; ++ks) {
+            const u32x4_t ah = *reinterpret_cast<const u32x4_t*>(hi + 32 * ks);
+            const u32x4_t al = *reinterpret_cast<const u32x4_t*>(lo + 32 * ks);
+#pragma unroll
+            for (int tb = 0; tb < 4; ++tb) {
+                const u32x4_t b = row_op(S.dH, kHP, 16 * tb, 32 * ks, lane);
+                acc[tb] = mfma16(ah, b, acc[tb]);
+                acc[tb] = mfma16(al, b, acc[tb]);
+            }
+        }
+    } else if (A.C0) {
+        const float* c0 = A.C0 + static_cast<int64_t>(s) * kCV + static_cast<int64_t>(drow) * kDV + 8 * g16;
+#pragma unroll 2
+        for (int ks = 0; ks < kDV / 32; ++ks) {
+            u32x4_t ah, al;
+            split8(*reinterpret_cast<const float4*>(c0 + 32 * ks), *reinterpret_cast<const float4*>(c0 + 32 * ks + 4), ah, al);
+#pragma unroll
+            for (int tb = 0; tb < 4; ++tb) {
+                const u32x4_t b = row_op(S.dH, kHP, 16 * tb, 32 * ks, lane);
+                acc[tb] = mfma16(ah, b, acc[tb]);
+                acc[tb] = mfma16(al, b, acc[tb]);
+            }
+        }
+    }
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+        const int tt = 16 * tb + l16;
+        const int d = d0 + 16 * wave + 4 * g16;
+        float qx = 0.0f;
+        if (t0 + tt < T) {
+            *reinterpret_cast<f32x4_t*>(&A.dq[(st + t0 + tt) * kDQK + d]) = acc[tb];
+            const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(&A.q[(st + t0 + tt) * kDQK + d]);
+            qx = lo_f32(qv[0]) * acc[tb][0] + hi_f32(qv[0]) * acc[tb][1] + lo_f32(qv[1]) * acc[tb][2] +
+                 hi_f32(qv[1]) * acc[tb][3];
+        }
+        qx = sum_rows4(qx);
+        if (g16 == 0) S.red[wave][tt] = qx * kQScale;
+    }
+    __syncthreads();
+    if (tid < kBL && t0 + tid < T)
+        A.part[(st + t0 + tid) * kPartF + j] = S.red[0][tid] + S.red[1][tid] + S.red[2][tid] + S.red[3][tid];
+}
+
+// ---- intra pass --------------------------------------------------------------------------------
+struct IntraSmem {
+    uint16_t Q[kBL * kQP];
+    uint16_t K[kBL * kQP];
+    uint16_t dH[kBL * kWP];    // one 128-column piece of dH
+    uint16_t dHg[kBL * kWP];   // the same piece scaled by g / den / sqrt(DQK)
+    uint16_t V[kBL * kWP];     // the same piece of V
+    uint16_t P[2][kBL * kPP];  // P [tau][sigma] as bf16 hi and lo
+    uint16_t Sn[kBL * kPP];    // St / den [tau][sigma]
+    float n[kDQK];
+    float x[kBL];
+    float M[kBL];
+    float gd[kBL];
+    float gw[kBL];
+    int R[kBL];
+    float red[4][kBL];
+};
+static_assert(sizeof(IntraSmem) <= 160 * 1024, "LDS budget");
+
+// One workgroup per chunk (4 waves).  Wave w owns the tau block w of every [sigma][tau] tile.
+__global__ void __launch_bounds__(kBT) bwd_intra_kernel(BwdParams A) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+    IntraSmem& S = *reinterpret_cast<IntraSmem*>(smem_raw);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g16 = lane >> 4, l16 = lane & 15;
+    const int c = blockIdx.x % A.NC, s = blockIdx.x / A.NC;
+    const int T = A.T, t0 = c * kBL;
+    const int64_t st = static_cast<int64_t>(s) * T;
+    const auto rq = make_rsrc(A.q + st * kDQK, static_cast<uint32_t>(T) * kDQK * 2);
+    const auto rk = make_rsrc(A.k + st * kDQK, static_cast<uint32_t>(T) * kDQK * 2);
+    const auto rv = make_rsrc(A.v + st * kDV, static_cast<uint32_t>(T) * kDV * 2);
+    const auto rdh = make_rsrc(A.dh + st * kDV, static_cast<uint32_t>(T) * kDV * 2);
+    float* lz = lz_of(A, s, c);   // chunk >= 1: the slot holding the entry state (n, m read first)
+
+    float m_prev;
+    if (c) {
+        m_prev = lz[kCV + kDQK + 2];
+        S.n[tid] = lz[kCV + tid];
+    } else {
+        m_prev = A.m0 ? A.m0[s] : 0.0f;
+        S.n[tid] = A.n0 ? A.n0[static_cast<int64_t>(s) * kDQK + tid] : 0.0f;
+    }
+    stage_rows<kDQK>(S.Q, kQP, rq, kDQK, t0, 0, tid);
+    stage_rows<kDQK>(S.K, kQP, rk, kDQK, t0, 0, tid);
+    if (wave == 0) {
+        BGate G;
+        float decay;
+        bwd_gates(make_rsrc(A.ipre + st, static_cast<uint32_t>(T) * 4), make_rsrc(A.fpre + st, static_cast<uint32_t>(T) * 4),
+                  T, t0, m_prev, lane, G, decay);
+        S.x[lane] = G.x;
+        S.M[lane] = G.M;
+        S.R[lane] = G.R;
+        S.gw[lane] = G.g;   // g for now; g w below
+        S.gd[lane] = G.fl;  // floor for now; g / den below
+        if (t0 + lane < T) A.tok[(st + t0 + lane) * kTokF] = G.wk;
+        if (lane == 0) A.chunk[static_cast<int64_t>(s) * A.NC + c] = decay;
+    }
+    __syncthreads();
+
+    // S^T tiles of this wave: columns tau = 16 wave + l16, rows sigma = 16 j + 4 g16 + 0..3 (j <= wave)
+    const int tau = 16 * wave + l16;
+    const bool valid = t0 + tau < T;
+    f32x4_t Sa[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) Sa[j] = f32x4_t{};
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if (j <= wave)
+#pragma unroll
+            for (int ks = 0; ks < kDQK / 32; ++ks)
+                Sa[j] = mfma16(row_op(S.K, kQP, 16 * j, 32 * ks, lane), row_op(S.Q, kQP, 16 * wave, 32 * ks, lane), Sa[j]);
+    const float Mt = S.M[tau];
+    const int Rt = S.R[tau];
+    const float gt = S.gw[tau];
+    const float flt = S.gd[tau];
+    float Et[4][4];
+    float rsum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int sg = 16 * j + 4 * g16 + r;
+            const float xs = S.x[sg];
+            const float e = (sg <= tau && sg >= Rt && xs != -INFINITY) ? fexp(xs - Mt) : 0.0f;
+            Et[j][r] = e;
+            Sa[j][r] = Sa[j][r] * kQScale * e;
+            rsum += Sa[j][r];
+        }
+    rsum = sum_rows4(rsum);
+    float qn = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const u32x4_t qv = lds16(&S.Q[tau * kQP + 64 * g16 + 8 * i]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qn += bf_at(qv, e) * S.n[64 * g16 + 8 * i + e];
+    }
+    qn = sum_rows4(qn) * kQScale;
+    const float Dt = gt * qn + rsum;
+    const float den = fmaxf(fabsf(Dt), flt);
+    const bool act = fabsf(Dt) > flt;
+    const float rden = 1.0f / den;
+    const float gd = valid ? gt * rden : 0.0f;
+    __syncthreads();   // floor and g are read by every wave
+    if (g16 == 0) S.gd[tau] = gd;
+    // St / den as bf16 [tau][sigma] (zero above the diagonal)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t p0 = pack_bf16x2(Sa[j][0] * rden, Sa[j][1] * rden);
+        const uint32_t p1 = pack_bf16x2(Sa[j][2] * rden, Sa[j][3] * rden);
+        *reinterpret_cast<u32x2_t*>(&S.Sn[tau * kPP + 16 * j + 4 * g16]) = u32x2_t{p0, p1};
+    }
+
+    // dv pieces of 128 columns: Ap = (V dH^T)^T accumulates;
+    //   dv_i^T [v][sigma] = sum_tau dH^T[v][tau] (St / den)[tau][sigma]
+    //   L_c^T  [v][d]     = sum_tau (g / den dH)^T[v][tau] Q^[tau][d]
+    f32x4_t Ap[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) Ap[j] = f32x4_t{};
+    for (int pc = 0; pc < kDV / 128; ++pc) {
+        __syncthreads();   // the previous piece is consumed; Sn and gd are visible
+        {
+            constexpr int N = kBL * 16 / kBT;
+            u32x4_t tmp[N];
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                const int e = tid + kBT * i, row = e / 16, p8 = e % 16;
+                tmp[i] = bload128(rdh, static_cast<uint32_t>((t0 + row) * kDV + 128 * pc + 8 * p8) * 2u, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                const int e = tid + kBT * i, row = e / 16, p8 = e % 16;
+                *reinterpret_cast<u32x4_t*>(&S.dH[row * kWP + 8 * p8]) = tmp[i];
+                const float sc = S.gd[row] * kQScale;
+                u32x4_t o;
+#pragma unroll
+                for (int w = 0; w < 4; ++w) o[w] = pack_bf16x2(lo_f32(tmp[i][w]) * sc, hi_f32(tmp[i][w]) * sc);
+                *reinterpret_cast<u32x4_t*>(&S.dHg[row * kWP + 8 * p8]) = o;
+            }
+        }
+        stage_rows<128>(S.V, kWP, rv, kDV, t0, 128 * pc, tid);
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (j <= wave)
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+                    Ap[j] = mfma16(row_op(S.V, kWP, 16 * j, 32 * ks, lane), row_op(S.dH, kWP, 16 * wave, 32 * ks, lane), Ap[j]);
+#pragma unroll
+        for (int vb = 0; vb < 2; ++vb) {
+            const int vloc = 16 * (2 * wave + vb);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                f32x4_t acc = f32x4_t{};
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+                    if (32 * ks + 31 >= 16 * j)
+                        acc = mfma16(tr_op(S.dH, kWP, 32 * ks, vloc, lane), tr_op(S.Sn, kPP, 32 * ks, 16 * j, lane), acc);
+                const int sg = 16 * j + l16;
+                if (t0 + sg < T)
+                    *reinterpret_cast<f32x4_t*>(&A.dv[(st + t0 + sg) * kDV + 128 * pc + vloc + 4 * g16]) = acc;
+            }
+        }
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            f32x4_t La[2][8];
+#pragma unroll
+            for (int vb = 0; vb < 2; ++vb)
+#pragma unroll
+                for (int db = 0; db < 8; ++db) La[vb][db] = f32x4_t{};
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                u32x4_t a[2];
+#pragma unroll
+                for (int vb = 0; vb < 2; ++vb) a[vb] = tr_op(S.dHg, kWP, 32 * ks, 16 * (2 * wave + vb), lane);
+#pragma unroll
+                for (int db = 0; db < 8; ++db) {
+                    const u32x4_t b = tr_op(S.Q, kQP, 32 * ks, 16 * (8 * half + db), lane);
+#pragma unroll
+                    for (int vb = 0; vb < 2; ++vb) La[vb][db] = mfma16(a[vb], b, La[vb][db]);
+                }
+            }
+#pragma unroll
+            for (int vb = 0; vb < 2; ++vb)
+#pragma unroll
+                for (int db = 0; db < 8; ++db)
+                    *reinterpret_cast<f32x4_t*>(&lz[static_cast<int64_t>(16 * (8 * half + db) + l16) * kDV + 128 * pc +
+                                                    16 * (2 * wave + vb) + 4 * g16]) = La[vb][db];
+        }
+    }
+    // dh_t . N_t from its two parts: the entry state's g q^_t . (dH C^T)_t (the dhc pass's partial
+    // sums) and the intra sum_sigma St_t,sigma (dh_t . v_sigma); then w_t
+    float dhn = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dhn += Sa[j][r] * Ap[j][r];
+    dhn = sum_rows4(dhn);
+    float qx = 0.0f;
+    if (valid) {
+        const float* pp = &A.part[(st + t0 + tau) * kPartF];
+        qx = (pp[0] + pp[1]) + (pp[2] + pp[3]);
+    }
+    dhn += gt * qx;
+    const float wt = (act && valid) ? -(dhn * rden) * (Dt > 0.0f ? 1.0f : -1.0f) * rden : 0.0f;
+    const float gwt = gt * wt;
+    if (g16 == 0) S.gw[tau] = gwt;
+    // P^T [sigma][tau] = E o (A'^T / den + w), stored as P [tau][sigma] in bf16 hi + lo: where the
+    // numerator and denominator terms of a row nearly cancel, P's own rounding would show
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        float pv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) pv[r] = Et[j][r] * (Ap[j][r] * rden + wt);
+        const uint32_t h01 = pack_bf16x2(pv[0], pv[1]), h23 = pack_bf16x2(pv[2], pv[3]);
+        *reinterpret_cast<u32x2_t*>(&S.P[0][tau * kPP + 16 * j + 4 * g16]) = u32x2_t{h01, h23};
+        *reinterpret_cast<u32x2_t*>(&S.P[1][tau * kPP + 16 * j + 4 * g16]) =
+            u32x2_t{pack_bf16x2(pv[0] - lo_f32(h01), pv[1] - hi_f32(h01)),
+                    pack_bf16x2(pv[2] - lo_f32(h23), pv[3] - hi_f32(h23))};
+    }
+    __syncthreads();
+    // dq^T [d][tau] = (g / den X + sum_sigma K^T[d][sigma] P^T[sigma][tau] + g w n) / sqrt(DQK), X from
+    // the dhc pass; r_t = q_t . dq_t
+    float rpart[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+        const int d0 = 16 * (4 * wave + db);
+#pragma unroll
+        for (int tb = 0; tb < 4; ++tb) {
+            f32x4_t acc = f32x4_t{};
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+                if (32 * ks <= 16 * tb + 15) {
+                    const u32x4_t a = tr_op(S.K, kQP, 32 * ks, d0, lane);
+                    acc = mfma16(a, row_op(S.P[0], kPP, 16 * tb, 32 * ks, lane), acc);
+                    acc = mfma16(a, row_op(S.P[1], kPP, 16 * tb, 32 * ks, lane), acc);
+                }
+            const int tt = 16 * tb + l16;
+            if (t0 + tt < T) {
+                const float gw_t = S.gw[tt], gd_t = S.gd[tt];
+                const int d = d0 + 4 * g16;
+                float* dqp = &A.dq[(st + t0 + tt) * kDQK + d];
+                const f32x4_t x = *reinterpret_cast<const f32x4_t*>(dqp);
+                f32x4_t o;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) o[r] = (gd_t * x[r] + acc[r] + gw_t * S.n[d + r]) * kQScale;
+                *reinterpret_cast<f32x4_t*>(dqp) = o;
+                const u32x2_t qv = lds_u32x2(&S.Q[tt * kQP + d]);
+                rpart[tb] += lo_f32(qv[0]) * o[0] + hi_f32(qv[0]) * o[1] + lo_f32(qv[1]) * o[2] + hi_f32(qv[1]) * o[3];
+            }
+        }
+    }
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+        const float r = sum_rows4(rpart[tb]);
+        if (g16 == 0) S.red[wave][16 * tb + l16] = r;
+    }
+    // dk_i^T [d][sigma] = sum_tau Q^T[d][tau] P[tau][sigma] / sqrt(DQK)
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+        const int d0 = 16 * (4 * wave + db);
+#pragma unroll
+        for (int sb = 0; sb < 4; ++sb) {
+            f32x4_t acc = f32x4_t{};
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+                if (32 * ks + 31 >= 16 * sb) {
+                    const u32x4_t a = tr_op(S.Q, kQP, 32 * ks, d0, lane);
+                    acc = mfma16(a, tr_op(S.P[0], kPP, 32 * ks, 16 * sb, lane), acc);
+                    acc = mfma16(a, tr_op(S.P[1], kPP, 32 * ks, 16 * sb, lane), acc);
+                }
+            const int sg = 16 * sb + l16;
+            if (t0 + sg < T) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[r] *= kQScale;
+                *reinterpret_cast<f32x4_t*>(&A.dk[(st + t0 + sg) * kDQK + d0 + 4 * g16]) = acc;
+            }
+        }
+    }
+    // z_c = Q^T (g o w) / sqrt(DQK) into the chunk's L slot (its n was read at the start)
+    {
+        float z = 0.0f;
+        for (int t = 0; t < kBL; ++t) z += bf16_to_f32(S.Q[t * kQP + tid]) * S.gw[t];
+        lz[kCV + tid] = z * kQScale;
+    }
+    __syncthreads();
+    if (tid < kBL && t0 + tid < T) {
+        float* pp = &A.part[(st + t0 + tid) * kPartF];
+        pp[0] = S.red[0][tid] + S.red[1][tid] + S.red[2][tid] + S.red[3][tid];
+        pp[1] = 0.0f;
+        pp[2] = 0.0f;
+        pp[3] = 0.0f;
+    }
+}
+
+// ---- reverse scan of the state gradient --------------------------------------------------------
+__global__ void __launch_bounds__(256) bwd_scan_kernel(BwdParams A) {
+    const int s = blockIdx.y;
+    const int e4 = blockIdx.x * 256 + threadIdx.x;
+    const bool ok = e4 < kScanE4;
+    const bool isC = e4 < kCV / 4;
+    const int NC = A.NC;
+    f32x4_t G = f32x4_t{};
+    constexpr int kBatch = 8;
+    for (int c1 = NC - 1; c1 >= 0; c1 -= kBatch) {
+        const int nb = min(kBatch, c1 + 1);
+        f32x4_t Lv[kBatch];
+        float dec[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (u < nb) {
+                const int c = c1 - u;
+                dec[u] = A.chunk[static_cast<int64_t>(s) * NC + c];
+                if (ok) Lv[u] = reinterpret_cast<const f32x4_t*>(lz_of(A, s, c))[e4];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (u < nb) {
+                const int c = c1 - u;
+                if (ok && c < NC - 1) {
+                    if (isC) {
+                        uint16_t* hi = hl_of(A, s, c) + 4 * static_cast<int64_t>(e4);
+                        const uint32_t h01 = pack_bf16x2(G[0], G[1]), h23 = pack_bf16x2(G[2], G[3]);
+                        const uint32_t l01 = pack_bf16x2(G[0] - lo_f32(h01), G[1] - hi_f32(h01));
+                        const uint32_t l23 = pack_bf16x2(G[2] - lo_f32(h23), G[3] - hi_f32(h23));
+                        *reinterpret_cast<u32x2_t*>(hi) = u32x2_t{h01, h23};
+                        *reinterpret_cast<u32x2_t*>(hi + kCV) = u32x2_t{l01, l23};
+                    } else {
+                        reinterpret_cast<f32x4_t*>(A.gamn + (static_cast<int64_t>(s) * NC + c) * kDQK)[e4 - kCV / 4] = G;
+                    }
+                }
+                if (ok) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) G[r] = dec[u] * G[r] + Lv[u][r];
+                }
+            }
+        }
+    }
+    // Gam_{-1}, gam_{-1}: the gradients of C0 and n0, and this block's share of dm0
+    if (A.dC0 == nullptr) return;
+    float dm = 0.0f;
+    if (ok) {
+        if (isC) {
+            reinterpret_cast<f32x4_t*>(A.dC0 + static_cast<int64_t>(s) * kCV)[e4] = G;
+            if (A.C0) {
+                const f32x4_t c0 = reinterpret_cast<const f32x4_t*>(A.C0 + static_cast<int64_t>(s) * kCV)[e4];
+                dm = G[0] * c0[0] + G[1] * c0[1] + G[2] * c0[2] + G[3] * c0[3];
+            }
+        } else {
+            reinterpret_cast<f32x4_t*>(A.dn0 + static_cast<int64_t>(s) * kDQK)[e4 - kCV / 4] = G;
+            if (A.n0) {
+                const f32x4_t n0 = reinterpret_cast<const f32x4_t*>(A.n0 + static_cast<int64_t>(s) * kDQK)[e4 - kCV / 4];
+                dm = G[0] * n0[0] + G[1] * n0[1] + G[2] * n0[2] + G[3] * n0[3];
+            }
+        }
+    }
+    __shared__ float red[4];
+    dm = wave_total(dm);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = dm;
+    __syncthreads();
+    if (threadIdx.x == 0) A.dmp[static_cast<int64_t>(s) * kScanBlocks + blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+}
+
+// ---- dk and dv inter terms ---------------------------------------------------------------------
+struct InterKVSmem {
+    uint16_t V[kBL * kHP];
+    uint16_t G[2][kBL * kWP];   // 64 rows d x 128 columns v of Gam_c, hi and lo
+    float wk[kBL];
+    float red[4][kBL];
+};
+static_assert(sizeof(InterKVSmem) <= 160 * 1024, "LDS budget");
+
+__global__ void __launch_bounds__(kBT) bwd_interkv_kernel(BwdParams A) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+    InterKVSmem& S = *reinterpret_cast<InterKVSmem*>(smem_raw);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g16 = lane >> 4, l16 = lane & 15;
+    const int wi = work_index();
+    const int j = wi % 4, c = (wi / 4) % A.NC, s = wi / 4 / A.NC;
+    const int T = A.T, t0 = c * kBL, d0 = 64 * j, v0 = 128 * j;
+    const int64_t st = static_cast<int64_t>(s) * T;
+    const auto rk = make_rsrc(A.k + st * kDQK, static_cast<uint32_t>(T) * kDQK * 2);
+    const auto rv = make_rsrc(A.v + st * kDV, static_cast<uint32_t>(T) * kDV * 2);
+    const bool has_g = c < A.NC - 1;   // the last chunk's exit state receives no gradient
+
+    if (tid < kBL) S.wk[tid] = (t0 + tid < T) ? A.tok[(st + t0 + tid) * kTokF] : 0.0f;
+    if (has_g) stage_rows<kDV>(S.V, kHP, rv, kDV, t0, 0, tid);
+    __syncthreads();
+
+    // dk^T [d][tau] += wk_tau (sum_v Gam[d][v] V[tau][v] + gam[d]); rows d = d0 + 16 wave + l16
+    {
+        f32x4_t acc[4];
+#pragma unroll
+        for (int tb = 0; tb < 4; ++tb) acc[tb] = f32x4_t{};
+        if (has_g) {
+            const uint16_t* hi = hl_of(A, s, c) + static_cast<int64_t>(d0 + 16 * wave + l16) * kDV + 8 * g16;
+            const uint16_t* lo = hi + kCV;
+#pragma unroll 4
+            for (int ks = 0; ks < kDV / 32; ++ks) {
+                const u32x4_t ah = *reinterpret_cast<const u32x4_t*>(hi + 32 * ks);
+                const u32x4_t al = *reinterpret_cast<const u32x4_t*>(lo + 32 * ks);
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb) {
+                    const u32x4_t b = row_op(S.V, kHP, 16 * tb, 32 * ks, lane);
+                    acc[tb] = mfma16(ah, b, acc[tb]);
+                    acc[tb] = mfma16(al, b, acc[tb]);
+                }
+            }
+        }
+        const int d = d0 + 16 * wave + 4 * g16;
+        f32x4_t gam = f32x4_t{};
+        if (has_g) gam = *reinterpret_cast<const f32x4_t*>(&A.gamn[(static_cast<int64_t>(s) * A.NC + c) * kDQK + d]);
+#pragma unroll
+        for (int tb = 0; tb < 4; ++tb) {
+            const int tt = 16 * tb + l16;
+            float cp = 0.0f;
+            if (t0 + tt < T) {
+                float* dkp = &A.dk[(st + t0 + tt) * kDQK + d];
+                f32x4_t o = *reinterpret_cast<const f32x4_t*>(dkp);
+                if (has_g) {
+                    const float w = S.wk[tt];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) o[r] += w * (acc[tb][r] + gam[r]);
+                    *reinterpret_cast<f32x4_t*>(dkp) = o;
+                }
+                const u32x2_t kv = *reinterpret_cast<const u32x2_t*>(&A.k[(st + t0 + tt) * kDQK + d]);
+                cp = lo_f32(kv[0]) * o[0] + hi_f32(kv[0]) * o[1] + lo_f32(kv[1]) * o[2] + hi_f32(kv[1]) * o[3];
+            }
+            cp = sum_rows4(cp);
+            if (g16 == 0) S.red[wave][tt] = cp;
+        }
+    }
+    // dv^T [v][tau] += wk_tau sum_d Gam^T[v][d] K[tau][d]; this wave: v = v0 + 16 (2 wave + vb) + ...
+    if (has_g) {
+        f32x4_t acc[2][4];
+#pragma unroll
+        for (int vb = 0; vb < 2; ++vb)
+#pragma unroll
+            for (int tb = 0; tb < 4; ++tb) acc[vb][tb] = f32x4_t{};
+        const uint16_t* ghi = hl_of(A, s, c);
+        for (int db = 0; db < kDQK / 64; ++db) {
+            __syncthreads();   // the previous block is consumed
+            // rows 64 db .. 64 db + 63, columns v0 .. v0 + 127 of Gam (hi, lo): 2 x 1024 pieces
+#pragma unroll
+            for (int part = 0; part < 2; ++part) {
+                u32x4_t tmp[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int e = tid + kBT * i, row = e / 16, pc = e % 16;
+                    tmp[i] = *reinterpret_cast<const u32x4_t*>(ghi + part * kCV + static_cast<int64_t>(64 * db + row) * kDV +
+                                                             v0 + 8 * pc);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int e = tid + kBT * i, row = e / 16, pc = e % 16;
+                    *reinterpret_cast<u32x4_t*>(&S.G[part][row * kWP + 8 * pc]) = tmp[i];
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                u32x4_t bk[4];
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb)
+                    bk[tb] = bload128(rk, static_cast<uint32_t>((t0 + 16 * tb + l16) * kDQK + 64 * db + 32 * ks + 8 * g16) * 2u, 0);
+#pragma unroll
+                for (int vb = 0; vb < 2; ++vb) {
+                    const int vl = 16 * (2 * wave + vb);
+                    const u32x4_t ah = tr_op(S.G[0], kWP, 32 * ks, vl, lane);
+                    const u32x4_t al = tr_op(S.G[1], kWP, 32 * ks, vl, lane);
+#pragma unroll
+                    for (int tb = 0; tb < 4; ++tb) {
+                        acc[vb][tb] = mfma16(ah, bk[tb], acc[vb][tb]);
+                        acc[vb][tb] = mfma16(al, bk[tb], acc[vb][tb]);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int vb = 0; vb < 2; ++vb)
+#pragma unroll
+            for (int tb = 0; tb < 4; ++tb) {
+                const int tt = 16 * tb + l16;
+                if (t0 + tt < T) {
+                    float* dvp = &A.dv[(st + t0 + tt) * kDV + v0 + 16 * (2 * wave + vb) + 4 * g16];
+                    f32x4_t o = *reinterpret_cast<const f32x4_t*>(dvp);
+                    const float w = S.wk[tt];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) o[r] += w * acc[vb][tb][r];
+                    *reinterpret_cast<f32x4_t*>(dvp) = o;
+                }
+            }
+    }
+    __syncthreads();
+    if (tid < kBL && t0 + tid < T)
+        A.part[(st + t0 + tid) * kPartF + 4 + j] = S.red[0][tid] + S.red[1][tid] + S.red[2][tid] + S.red[3][tid];
+}
+
+// ---- gate gradients ----------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) bwd_gate_kernel(BwdParams A) {
+    const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int T = A.T;
+    const int64_t st = static_cast<int64_t>(s) * T;
+    __shared__ float wsum[4];
+    double carry = 0.0;
+    for (int base = ((T + 255) / 256 - 1) * 256; base >= 0; base -= 256) {
+        const int t = base + tid;
+        float val = 0.0f, ci = 0.0f;
+        if (t < T) {
+            const float* p = &A.part[(st + t) * kPartF];
+            val = (p[0] + p[1]) + (p[2] + p[3]);
+            ci = (p[4] + p[5]) + (p[6] + p[7]);
+            val -= ci;
+        }
+        // inclusive prefix over the block, then the suffix sum from t on
+        const float incl = wave_incl_sum(val);
+        __syncthreads();   // wsum of the previous block is consumed
+        if (lane == 63) wsum[wave] = incl;
+        __syncthreads();
+        float before = 0.0f, total = 0.0f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            if (w < wave) before += wsum[w];
+            total += wsum[w];
+        }
+        const float suffix = total - (before + incl) + val;
+        if (t < T) {
+            const float f = A.fpre[st + t];
+            const double da = carry + static_cast<double>(suffix);
+            A.dfp[st + t] = (f == -INFINITY) ? 0.0f : static_cast<float>(da / (1.0 + exp(static_cast<double>(f))));
+            A.dip[st + t] = ci;
+        }
+        carry += static_cast<double>(total);
+    }
+    if (A.dm0 && tid == 0) {
+        float dm = 0.0f;
+        for (int b = 0; b < kScanBlocks; ++b) dm += A.dmp[static_cast<int64_t>(s) * kScanBlocks + b];
+        A.dm0[s] = dm;
+    }
+}
+
+// T = 0: the initial-state gradients are zero
+__global__ void __launch_bounds__(256) bwd_zero_state_kernel(float* dC0, float* dn0, float* dm0, int S) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i < static_cast<int64_t>(S) * kCV) dC0[i] = 0.0f;
+    if (i < static_cast<int64_t>(S) * kDQK) dn0[i] = 0.0f;
+    if (i < S) dm0[i] = 0.0f;
+}
+
+template <class Smem>
+hipError_t launch_big(const void* kern, const BwdParams& p, unsigned grid, hipStream_t stream,
+                      std::atomic<uint64_t>& raised) {
+    const size_t lds = sizeof(Smem);
+    hipError_t e = raise_dynamic_lds(kern, lds, raised);
+    if (e != hipSuccess) return e;
+    void* args[] = {const_cast<BwdParams*>(&p)};
+    return hipLaunchKernel(kern, dim3(grid), dim3(kBT), args, lds, stream);
+}
+
+size_t align256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
+
+struct BwdLayout {
+    size_t slots, hl, lz0, gamn, tok, part, chunk, dmp, total;
+};
+BwdLayout bwd_layout(int64_t S, int T) {
+    const int64_t NC = (T + kBL - 1) / kBL, NC1 = NC > 0 ? NC - 1 : 0;
+    BwdLayout L{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    L.slots = take(static_cast<size_t>(S * NC1 * kSlotFloats) * 4);
+    L.hl = take(static_cast<size_t>(S * NC1 * 2 * kCV) * 2);
+    L.lz0 = take(static_cast<size_t>(S * kLzFloats) * 4);
+    L.gamn = take(static_cast<size_t>(S * NC * kDQK) * 4);
+    L.tok = take(static_cast<size_t>(S * T * kTokF) * 4);
+    L.part = take(static_cast<size_t>(S * T * kPartF) * 4);
+    L.chunk = take(static_cast<size_t>(S * NC) * 4);
+    L.dmp = take(static_cast<size_t>(S * kScanBlocks) * 4);
+    L.total = off;
+    return L;
+}
+
+}  // namespace
+
+bool chunk_bwd_supported(mlstm_dtype dt, int DQK, int DV, int L) {
+    return dt == MLSTM_BF16 && DQK == kDQK && DV == kDV && L == kBL;
+}
+
+size_t chunk_bwd_workspace_bytes(int B, int NH, int T) {
+    return bwd_layout(static_cast<int64_t>(B) * NH, T).total;
+}
+
+hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t stream) {
+    const int S = a.f.B * a.f.NH, T = a.f.T;
+    if (S == 0) return hipSuccess;
+    if (T == 0) {
+        if (a.dC0) {
+            const int64_t n = static_cast<int64_t>(S) * kCV;
+            hipLaunchKernelGGL(bwd_zero_state_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream,
+                               a.dC0, a.dn0, a.dm0, S);
+            return hipGetLastError();
+        }
+        return hipSuccess;
+    }
+    const BwdLayout L = bwd_layout(S, T);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    BwdParams p{};
+    p.q = static_cast<const uint16_t*>(a.f.q);
+    p.k = static_cast<const uint16_t*>(a.f.k);
+    p.v = static_cast<const uint16_t*>(a.f.v);
+    p.dh = static_cast<const uint16_t*>(a.dh);
+    p.ipre = a.f.ipre;
+    p.fpre = a.f.fpre;
+    p.C0 = a.f.C0;
+    p.n0 = a.f.n0;
+    p.m0 = a.f.m0;
+    p.dq = a.dq;
+    p.dk = a.dk;
+    p.dv = a.dv;
+    p.dip = a.dipre;
+    p.dfp = a.dfpre;
+    p.dC0 = a.dC0;
+    p.dn0 = a.dn0;
+    p.dm0 = a.dm0;
+    p.slots = reinterpret_cast<float*>(ws + L.slots);
+    p.hl = reinterpret_cast<uint16_t*>(ws + L.hl);
+    p.lz0 = reinterpret_cast<float*>(ws + L.lz0);
+    p.gamn = reinterpret_cast<float*>(ws + L.gamn);
+    p.tok = reinterpret_cast<float*>(ws + L.tok);
+    p.part = reinterpret_cast<float*>(ws + L.part);
+    p.chunk = reinterpret_cast<float*>(ws + L.chunk);
+    p.dmp = reinterpret_cast<float*>(ws + L.dmp);
+    p.T = T;
+    p.NC = (T + kBL - 1) / kBL;
+
+    hipError_t e = launch_chunk_states(a.f, p.slots, p.hl, stream);
+    if (e != hipSuccess) return e;
+    const unsigned nchunks = static_cast<unsigned>(S) * p.NC;
+    static std::atomic<uint64_t> r_intra{0}, r_q{0}, r_kv{0};
+    e = launch_big<DhcSmem>(reinterpret_cast<const void*>(bwd_dhc_kernel), p, nchunks * 4, stream, r_q);
+    if (e != hipSuccess) return e;
+    e = launch_big<IntraSmem>(reinterpret_cast<const void*>(bwd_intra_kernel), p, nchunks, stream, r_intra);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bwd_scan_kernel, dim3(kScanBlocks, S), dim3(256), 0, stream, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_big<InterKVSmem>(reinterpret_cast<const void*>(bwd_interkv_kernel), p, nchunks * 4, stream, r_kv);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bwd_gate_kernel, dim3(S), dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
+}  // namespace mlstm

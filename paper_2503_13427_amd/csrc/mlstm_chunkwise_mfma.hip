@@ -63,50 +63,16 @@
 // kernel runs every segment from its entry state.
 #include <mutex>
 
-#include "device_common.h"
 #include "launch.h"
+#include "mfma_common.h"
 
 namespace mlstm {
 namespace {
 
-constexpr int kDQK = 256;
-constexpr int kDV = 512;
-constexpr int kDVT = 128;             // dv columns per workgroup
-constexpr int kNTile = kDV / kDVT;    // 4 dv tiles per sequence
 constexpr int kThreads = 512;
 constexpr int kWaves = 8;
 constexpr int kGateWave = kWaves - 1; // the wave with the least MFMA work runs the gate scans
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kQScale = 0.0625f;    // 1 / sqrt(256), exact
 constexpr float kRenorm = -20.0f;     // rescale C eagerly when its lazy log-scale would drop below this
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-typedef short i16x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f32x4_t mfma16(u32x4_t a, u32x4_t b, f32x4_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
-                                                   c, 0, 0, 0);
-}
-
-// Two fp32 -> packed bf16 pair, round to nearest even (one v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
-}
-__device__ __forceinline__ float lo_f32(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float hi_f32(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// LDS transpose read: 4 bf16 per lane (see the header comment for the lane mapping).
-__device__ __forceinline__ u32x2_t tr_read(const uint16_t* p) {
-    typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
-    return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p)));
-}
-__device__ __forceinline__ u32x4_t cat(u32x2_t a, u32x2_t b) { return u32x4_t{a[0], a[1], b[0], b[1]}; }
 
 template <int L>
 struct Cfg {
@@ -199,24 +165,6 @@ struct VRegs {
     u32x4_t v[N];
 };
 
-// Buffer resources (SGPRs) for one sequence's inputs: loads need one 32-bit VGPR
-// offset per staging item plus immediate offsets.  Out-of-range reads return zero.
-constexpr int kRsrcWord3 = 0x00020000;
-
-struct SeqRsrc {
-    __amdgpu_buffer_rsrc_t q, k, v, ig, fg, h;
-};
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0), static_cast<int>(bytes),
-                                             kRsrcWord3);
-}
-__device__ __forceinline__ u32x4_t bload128(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-    return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
-}
-__device__ __forceinline__ float bloadf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
-}
 
 // Q and K rows are 512 bytes, V rows 1024 bytes; offsets are in bytes.
 // With K^T staging (L = 128) K is loaded in pieces in the MFMA A-operand layout: piece i of wave w
@@ -378,70 +326,6 @@ __device__ __forceinline__ void load_gates(float (&gi)[2], float (&gf)[2], const
     }
 }
 
-// Inclusive scans over the 64 lanes of a wave with DPP: shifts inside 16-lane rows,
-// then the row_bcast steps carry row totals forward.  Lanes without a source take the
-// identity (0 for the sum, -inf for the max).
-#define MLSTM_DPP(old, x, ctrl, rmask)                                                                   \
-    __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, (old)),                 \
-                                                          __builtin_bit_cast(int, (x)), (ctrl), (rmask), 0xf, false))
-__device__ __forceinline__ float wave_incl_sum(float x) {
-    x += MLSTM_DPP(0.0f, x, 0x111, 0xf);   // row_shr:1
-    x += MLSTM_DPP(0.0f, x, 0x112, 0xf);   // row_shr:2
-    x += MLSTM_DPP(0.0f, x, 0x114, 0xf);   // row_shr:4
-    x += MLSTM_DPP(0.0f, x, 0x118, 0xf);   // row_shr:8
-    x += MLSTM_DPP(0.0f, x, 0x142, 0xa);   // row_bcast:15 into rows 1 and 3
-    x += MLSTM_DPP(0.0f, x, 0x143, 0xc);   // row_bcast:31 into rows 2 and 3
-    return x;
-}
-__device__ __forceinline__ float wave_incl_max(float x) {
-    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x111, 0xf));
-    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x112, 0xf));
-    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x114, 0xf));
-    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x118, 0xf));
-    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x142, 0xa));
-    x = fmaxf(x, MLSTM_DPP(-INFINITY, x, 0x143, 0xc));
-    return x;
-}
-// Segmented inclusive max: a lane with ``start`` set begins a new segment, so every lane gets the
-// maximum over the lanes from the last start at or before it (all lanes before it if none).  Each
-// step combines (flag, value) pairs with the associative rule "a later start discards the left".
-__device__ __forceinline__ float wave_seg_incl_max(float x, bool start) {
-    int f = start ? 1 : 0;
-#define MLSTM_SEG_STEP(ctrl, rmask)                                                                        \
-    {                                                                                                     \
-        const float y = MLSTM_DPP(-INFINITY, x, ctrl, rmask);                                             \
-        const int fy = __builtin_amdgcn_update_dpp(0, f, (ctrl), (rmask), 0xf, false);                    \
-        x = f ? x : fmaxf(x, y);                                                                          \
-        f |= fy;                                                                                          \
-    }
-    MLSTM_SEG_STEP(0x111, 0xf)
-    MLSTM_SEG_STEP(0x112, 0xf)
-    MLSTM_SEG_STEP(0x114, 0xf)
-    MLSTM_SEG_STEP(0x118, 0xf)
-    MLSTM_SEG_STEP(0x142, 0xa)
-    MLSTM_SEG_STEP(0x143, 0xc)
-#undef MLSTM_SEG_STEP
-    return x;
-}
-#undef MLSTM_DPP
-// sum over the four 16-lane rows of a wave, in every lane (gfx950 cross-row lane swaps, no LDS)
-__device__ __forceinline__ float sum_rows4(float x) {
-    const uint32_t u = __float_as_uint(x);
-    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);   // rows (0, 1) <-> (2, 3)
-    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    const uint32_t w = __float_as_uint(y);
-    const auto b = __builtin_amdgcn_permlane16_swap(w, w, false, false);   // rows 0 <-> 1, 2 <-> 3
-    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-__device__ __forceinline__ float lane63(float x) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
-}
-
-// exp and log sigmoid through the hardware exp2 / log2 (v_exp_f32, v_log_f32).
-__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
-__device__ __forceinline__ float flogsig(float x) {
-    return fminf(x, 0.0f) - 0.6931471805599453f * __builtin_amdgcn_logf(1.0f + fexp(-fabsf(x)));
-}
 
 // Gate phase of one chunk (run by one wave): in-chunk prefix sums and maxima, the max
 // state, the lazy C scale, and every per-row scale of the chunk.  m_prev and s_cur
@@ -532,14 +416,6 @@ __device__ __forceinline__ void gate_phase(GateBuf<L>& Gb, const float (&gi)[2],
     s_cur = s_new;
 }
 
-// XCD-aware block order: the hardware deals consecutive workgroups round-robin to
-// the 8 XCDs; renumber so that consecutive work items (the four dv tiles of a
-// sequence/segment) run on the same XCD.
-__device__ __forceinline__ int work_index() {
-    const int nb = gridDim.x, b = blockIdx.x;
-    if (nb % 8) return b;
-    return (b % 8) * (nb / 8) + b / 8;
-}
 
 struct ChunkKernelArgs {
     const uint16_t* q;
@@ -567,12 +443,6 @@ struct ChunkKernelArgs {
 constexpr int kStageP = kDVT + 4;
 static_assert(kDQK * kStageP * 4 <= sizeof(Smem<64>) && kDQK * kStageP * 4 <= sizeof(Smem<128>), "staging");
 
-// workspace slot of (sequence s, local sub-segment j): C [DQK*DV], n [DQK], then m_loc, gsum
-// (sum of logsig over the sub-segment), m_in (entry max state, in segment-boundary slots), pad.
-// C is stored four rows interleaved: element (d, v) at ((d / 4) DV + v) 4 + d % 4, so the four
-// consecutive d one accumulator lane holds for one v are one 16-byte piece
-__host__ __device__ constexpr int64_t slot_c4(int d4, int v) { return (static_cast<int64_t>(d4) * kDV + v) * 4; }
-constexpr int64_t kSlotFloats = static_cast<int64_t>(kDQK) * kDV + kDQK + 4;
 
 // Staging order (one Q/K block and one part of a V chunk in registers at a time): block 0
 // of a chunk is stored during the previous chunk (at the barrier that opens its last d
@@ -1165,9 +1035,12 @@ struct LocalArgs {
 };
 
 // One workgroup per (sequence, local segment, sub-segment, dv tile); its slot receives C[:, tile],
-// and (dv tile 0) n, m_loc and the segment's logsig sum.
+// and (dv tile 0) n, m_loc and the segment's logsig sum.  kHiLo: the weighted values w v enter the
+// matrix cores as bf16 hi + lo (twice the products; the state to about 2^-17 instead of the 2^-9
+// of one rounding per term), for the backward pass, whose gradients can cancel against the state.
 // (the LDS footprint allows one workgroup per CU, two waves per SIMD: registers are not worth
 // saving for a higher occupancy)
+template <bool kHiLo>
 __global__ void __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(2, 2)))
 local_state_kernel(LocalArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
@@ -1278,13 +1151,16 @@ local_state_kernel(LocalArgs A) {
             const f32x4_t wa0 = *reinterpret_cast<const f32x4_t*>(&S.w[t0]);
             const f32x4_t wa1 = *reinterpret_cast<const f32x4_t*>(&S.w[t0 + 4]);
             const float wv[8] = {wa0[0], wa0[1], wa0[2], wa0[3], wa1[0], wa1[1], wa1[2], wa1[3]};
-            u32x4_t Vw[2];
+            u32x4_t Vw[2], Vl[2];
 #pragma unroll
             for (int vt = 0; vt < 2; ++vt) {
                 const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(&Vt[(32 * vg + 16 * vt + l16) * kLocP + 32 * ks + 8 * g16]);
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    Vw[vt][u] = pack_bf16x2(lo_f32(raw[u]) * wv[2 * u], hi_f32(raw[u]) * wv[2 * u + 1]);
+                for (int u = 0; u < 4; ++u) {
+                    const float x0 = lo_f32(raw[u]) * wv[2 * u], x1 = hi_f32(raw[u]) * wv[2 * u + 1];
+                    Vw[vt][u] = pack_bf16x2(x0, x1);
+                    if constexpr (kHiLo) Vl[vt][u] = pack_bf16x2(x0 - lo_f32(Vw[vt][u]), x1 - hi_f32(Vw[vt][u]));
+                }
             }
             const uint16_t* kb = &Kt[(128 * dh + l16) * kLocP + 32 * ks + 8 * g16];
             u32x4_t a[8];
@@ -1294,6 +1170,10 @@ local_state_kernel(LocalArgs A) {
             for (int q = 0; q < 8; ++q) {
                 Cacc[q][0] = mfma16(a[q], Vw[0], Cacc[q][0]);
                 Cacc[q][1] = mfma16(a[q], Vw[1], Cacc[q][1]);
+                if constexpr (kHiLo) {
+                    Cacc[q][0] = mfma16(a[q], Vl[0], Cacc[q][0]);
+                    Cacc[q][1] = mfma16(a[q], Vl[1], Cacc[q][1]);
+                }
             }
             // n over d tiles 2 vg and 2 vg + 1 (rows re-read by address: no wave-dependent branch)
             const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&S.wb[l16 & 1][t0]) : u32x4_t{0u, 0u, 0u, 0u};
@@ -1326,7 +1206,7 @@ local_state_kernel(LocalArgs A) {
 // (slot g R + R - 1) receives the state after local slots 0..g R + R - 1, the entry state of
 // segment g + 1; the other sub-segment slots are only read.
 __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0, const float* n0, const float* m0,
-                                                      int NS, int R) {
+                                                      int NS, int R, uint16_t* rowhl) {
     const int s = blockIdx.y;
     float* base = ws + static_cast<int64_t>(s) * NS * kSlotFloats;
     // scalar chain of entry max states (every block computes it; block 0 stores it)
@@ -1377,6 +1257,18 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
                     cur.z = a * cur.z + b * loc[u].z;
                     cur.w = a * cur.w + b * loc[u].w;
                     if (entry) reinterpret_cast<float4*>(slot)[e4] = cur;
+                    if (entry && rowhl && e4 < kDQK * kDV / 4) {
+                        // the entry state also as bf16 hi + lo rows [d][v] (the backward pass's operand)
+                        uint16_t* hl = rowhl + (static_cast<int64_t>(s) * NS + g0 + u) * 2 * kDQK * kDV;
+                        const int d0 = 4 * (e4 / kDV), v = e4 % kDV;
+                        const float cv[4] = {cur.x, cur.y, cur.z, cur.w};
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const uint16_t hi = f32_to_bf16(cv[j]);
+                            hl[(d0 + j) * kDV + v] = hi;
+                            hl[kDQK * kDV + (d0 + j) * kDV + v] = f32_to_bf16(cv[j] - bf16_to_f32(hi));
+                        }
+                    }
                 }
                 if (entry && blockIdx.x == 0 && threadIdx.x == 0) slot[kDQK * kDV + kDQK + 2] = m_new;
                 m_in = m_new;
@@ -1397,13 +1289,13 @@ hipError_t launch_variant(const ChunkKernelArgs& a, int S, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_local(const LocalArgs& a, int S, hipStream_t stream) {
+hipError_t launch_local(const LocalArgs& a, int S, hipStream_t stream, bool hilo = false) {
     const size_t lds = sizeof(LocSmem);
-    static std::atomic<uint64_t> raised{0};
-    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(local_state_kernel), lds, raised);
+    static std::atomic<uint64_t> raised[2]{{0}, {0}};
+    auto kern = hilo ? local_state_kernel<true> : local_state_kernel<false>;
+    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(kern), lds, raised[hilo ? 1 : 0]);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(local_state_kernel, dim3(static_cast<unsigned>(S * a.NS * kNTile)), dim3(kThreads), lds, stream,
-                       a);
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(S * a.NS * kNTile)), dim3(kThreads), lds, stream, a);
     return hipGetLastError();
 }
 
@@ -1484,11 +1376,38 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
         if (e != hipSuccess) return e;
         constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
         hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, k.ws, a.C0, a.n0, a.m0,
-                           k.NS, R);
+                           k.NS, R, static_cast<uint16_t*>(nullptr));
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return (a.L == 64) ? launch_variant<64>(k, S, stream) : launch_variant<128>(k, S, stream);
+}
+
+// ---- chunk-boundary states for the backward pass -----------------------------------------------
+// The state entering every chunk c >= 1 of 64 tokens: the local pass over one-chunk sub-segments
+// (its closed form from an empty state, in the bf16 hi + lo form) and the combine scan, which leaves in slot c - 1 the fp32
+// state (C in the four-row interleaved layout, n, and the entry max state m_in) and writes C as bf16
+// hi + lo rows into rowhl.  ``slots`` holds S (NC - 1) slots, ``rowhl`` S (NC - 1) x 2 x DQK x DV.
+hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, uint16_t* rowhl, hipStream_t stream) {
+    const int S = a.B * a.NH;
+    const int nc = (a.T + 63) / 64;
+    if (nc <= 1) return hipSuccess;
+    LocalArgs la{};
+    la.k = static_cast<const uint16_t*>(a.k);
+    la.v = static_cast<const uint16_t*>(a.v);
+    la.ipre = a.ipre;
+    la.fpre = a.fpre;
+    la.ws = slots;
+    la.T = a.T;
+    la.NS = nc - 1;
+    la.R = 1;
+    la.seg_tokens = 64;
+    hipError_t e = launch_local(la, S, stream, true);
+    if (e != hipSuccess) return e;
+    constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
+    hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, slots, a.C0, a.n0, a.m0, nc - 1,
+                       1, rowhl);
+    return hipGetLastError();
 }
 
 // ---- fixed scratch for callers that cannot allocate ---------------------------------------------

@@ -8,6 +8,7 @@ import os
 import re
 
 import pytest
+import torch
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "mlstm.h")
@@ -26,7 +27,8 @@ def declared_functions():
 def test_header_declares_expected_entry_points():
     assert declared_functions() == sorted(["mlstm_chunkwise_fwd", "mlstm_chunkwise_workspace_bytes", "mlstm_step",
                                            "mlstm_chunkwise_fwd_noalloc", "mlstm_chunkwise_scratch_bytes",
-                                           "mlstm_step_output",
+                                           "mlstm_step_output", "mlstm_chunkwise_bwd",
+                                           "mlstm_chunkwise_bwd_workspace_bytes",
                                            "mlstm_output_norm", "mlstm_output_norm_tokens", "mlstm_gate_preact", "mlstm_parallel_bwd",
                                            "mlstm_parallel_bwd_workspace_bytes", "mlstm_status_string",
                                            "mlstm_version"])
@@ -438,3 +440,86 @@ def call_step_out(a):
     (dict(h=fake(8, 16)), 5), (dict(h=fake(9, 64)), 5), (dict(Co=fake(8)), 5)])
 def test_step_output_validation(over, status):
     assert call_step_out(step_out_args(**over)) == status
+
+
+# ---- the chunkwise backward ----------------------------------------------------------------------
+
+def cbwd_args(**over):
+    a = dict(q=fake(0), k=fake(1), v=fake(2), dt=Bd.MLSTM_BF16, ip=fake(3), fp=fake(4), C0=None, n0=None, m0=None,
+             B=1, NH=8, T=2048, DQK=256, DV=512, L=64, dh=fake(6), dq=fake(7), dk=fake(8), dv=fake(9),
+             di=fake(10), df=fake(11), dC0=None, dn0=None, dm0=None, ws=fake(12), ws_bytes=1 << 40, stream=None)
+    a.update(over)
+    return a
+
+
+def call_cbwd(a):
+    return lib.mlstm_chunkwise_bwd(a["q"], a["k"], a["v"], a["dt"], a["ip"], a["fp"], a["C0"], a["n0"], a["m0"],
+                                   a["B"], a["NH"], a["T"], a["DQK"], a["DV"], a["L"], a["dh"], a["dq"],
+                                   a["dk"], a["dv"], a["di"], a["df"], a["dC0"], a["dn0"], a["dm0"], a["ws"],
+                                   a["ws_bytes"], a["stream"])
+
+
+def test_chunk_bwd_workspace_size():
+    """Entry states (fp32 slot and bf16 hi + lo rows) of every chunk but the first, L_0, gam per chunk,
+    per-token key weights and partial sums, per-chunk decays, dm0 partial sums; each region 256-byte
+    aligned."""
+    al = lambda b: (b + 255) // 256 * 256
+    S, T, NC = 8, 2048, 32
+    slot = 256 * 512 + 256 + 4
+    want = (al(S * (NC - 1) * slot * 4) + al(S * (NC - 1) * 2 * 256 * 512 * 2) + al(S * (256 * 512 + 256) * 4)
+            + al(S * NC * 256 * 4) + al(S * T * 4) + al(S * T * 32) + al(S * NC * 4) + al(S * 129 * 4))
+    assert Bd.mlstm_chunkwise_bwd_workspace_bytes(1, 8, T, 256, 512, 64) == want
+    assert Bd.mlstm_chunkwise_bwd_workspace_bytes(1, 8, T, 256, 512, 128) == 0
+    assert Bd.mlstm_chunkwise_bwd_workspace_bytes(1, 8, T, 256, 512, 64, torch.float32) == 0
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "ip", "fp", "dh", "dq", "dk", "dv", "di", "df", "ws"])
+def test_chunk_bwd_null_pointer(field):
+    assert call_cbwd(cbwd_args(**{field: None})) == 1
+
+
+@pytest.mark.parametrize("over", [dict(C0=fake(13)), dict(C0=fake(13), n0=fake(14)), dict(dC0=fake(13)),
+                                  dict(dn0=fake(13), dm0=fake(14))])
+def test_chunk_bwd_partial_state_triples(over):
+    assert call_cbwd(cbwd_args(**over)) == 1
+
+
+def test_chunk_bwd_empty_sequence_is_ok_without_pointers():
+    assert call_cbwd(cbwd_args(T=0, q=None, k=None, v=None, dh=None, dq=None, ws=None, ws_bytes=0)) == 0
+
+
+@pytest.mark.parametrize("over", [dict(B=0), dict(NH=-1), dict(T=-1), dict(DQK=0), dict(DV=0), dict(L=0)])
+def test_chunk_bwd_bad_shape(over):
+    assert call_cbwd(cbwd_args(**over)) == 2
+
+
+@pytest.mark.parametrize("over", [dict(dt=3), dict(dt=Bd.MLSTM_F32), dict(DQK=128), dict(DV=256), dict(L=128),
+                                  dict(B=65536, NH=1), dict(T=1 << 21)])
+def test_chunk_bwd_unsupported(over):
+    assert call_cbwd(cbwd_args(**over)) == 3
+
+
+def test_chunk_bwd_workspace_too_small():
+    need = Bd.mlstm_chunkwise_bwd_workspace_bytes(1, 8, 2048, 256, 512, 64)
+    assert call_cbwd(cbwd_args(ws_bytes=need - 1)) == 6
+    assert call_cbwd(cbwd_args(ws_bytes=need, q=fake(0, 4))) == 4
+
+
+@pytest.mark.parametrize("field", ["q", "dh", "dq", "df", "ws"])
+def test_chunk_bwd_misaligned(field):
+    a = cbwd_args()
+    a[field] += 4
+    assert call_cbwd(a) == 4
+
+
+@pytest.mark.parametrize("out,other,off", [("dq", "q", 0), ("dv", "dh", 4096), ("dk", "dq", 16), ("df", "di", 0),
+                                           ("ws", "dv", 64), ("di", "ip", 0), ("dq", "k", 1024)])
+def test_chunk_bwd_alias(out, other, off):
+    a = cbwd_args()
+    a[out] = a[other] + off
+    assert call_cbwd(a) == 5
+
+
+def test_chunk_bwd_state_gradient_alias():
+    a = cbwd_args(C0=fake(13), n0=fake(14), m0=fake(15), dC0=fake(13, 64), dn0=fake(16), dm0=fake(17))
+    assert call_cbwd(a) == 5

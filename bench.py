@@ -412,30 +412,64 @@ def bench_layer(steps, decode_steps, stream):
     return out
 
 
-def bench_backward(w, steps, stream):
-    """mlstm_parallel_bwd on the headline prefill shape (bf16 q/k/v, fp32 gates and dh): ms per call
-    and FLOP/s (the parallel form's count) against the fp32 VALU peak."""
+def bench_backward(w, steps, stream, parallel=True):
+    """The training-mode backward on a prefill shape (bf16 q/k/v and dh, fp32 gates, zero initial
+    state): mlstm_chunkwise_bwd (per-call median of ``steps`` calls), the forward on the same inputs
+    for the ratio, and (``parallel``) mlstm_parallel_bwd for comparison.  FLOP figures use App. D.2's
+    count, twice the App. D.1 forward, against the bf16 MFMA peak."""
     from paper_2503_13427_amd import binding as mb
     g = torch.Generator(device="cuda").manual_seed(17)
     B, NH, T, DQK, DV = w.B, w.NH, w.T, w.DQK, w.DV
     q = torch.randn(B, NH, T, DQK, generator=g, device="cuda").bfloat16()
-    k = (torch.randn(B, NH, T, DQK, generator=g, device="cuda") / 4).bfloat16()
+    k = (torch.randn(B, NH, T, DQK, generator=g, device="cuda") / 16).bfloat16()
     v = torch.randn(B, NH, T, DV, generator=g, device="cuda").bfloat16()
     ip = torch.randn(B, NH, T, generator=g, device="cuda")
     fp = torch.randn(B, NH, T, generator=g, device="cuda") + 3
-    dh = torch.randn(B, NH, T, DV, generator=g, device="cuda")
+    dh = torch.randn(B, NH, T, DV, generator=g, device="cuda").bfloat16()
     outs = [torch.empty(B, NH, T, DQK, device="cuda"), torch.empty(B, NH, T, DQK, device="cuda"),
             torch.empty(B, NH, T, DV, device="cuda"), torch.empty(B, NH, T, device="cuda"),
             torch.empty(B, NH, T, device="cuda")]
-    ws = torch.empty(mb.mlstm_parallel_bwd_workspace_bytes(B, NH, T, DV), dtype=torch.uint8, device="cuda")
-    fn = lambda: mb.mlstm_parallel_bwd(q, k, v, ip, fp, dh, *outs, ws, stream=stream)
-    _, ev = time_steps(fn, steps, 2, stream)
-    t = ev / steps
-    fl = acc.flops_parallel_bwd(B * NH, T, DQK, DV)
-    fl_d2 = 2 * acc.flops_chunkwise(B * NH, T, w.L, DQK, DV).total   # App. D.2: backward = 2 x forward
-    return dict(workload=f"backward_{w.name}", ms_per_call=t * 1e3, tokens_per_s=B * T / t, flops_per_call=fl,
-                tflops=fl / t / 1e12, valu_frac=fl / t / 1e12 / acc.PEAK_FP32_VALU_TFLOPS,
-                app_d2_flops=fl_d2, app_d2_tflops=fl_d2 / t / 1e12)
+    wsb = torch.empty(mb.mlstm_chunkwise_bwd_workspace_bytes(B, NH, T, DQK, DV, 64), dtype=torch.uint8, device="cuda")
+
+    def per_call(fn, n):
+        settle(fn)
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        for i in range(n):
+            ev[i].record(stream)
+            fn()
+        ev[n].record(stream)
+        torch.cuda.synchronize()
+        return np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(n)]) / 1e3
+
+    bwd = per_call(lambda: mb.mlstm_chunkwise_bwd(q, k, v, ip, fp, None, None, None, 64, dh, *outs, None, None, None,
+                                                  wsb, stream=stream), steps)
+    del wsb
+    h = torch.empty(B, NH, T, DV, dtype=torch.bfloat16, device="cuda")
+    CT, nT, mT = (torch.empty(B, NH, DQK, DV, device="cuda"), torch.empty(B, NH, DQK, device="cuda"),
+                  torch.empty(B, NH, device="cuda"))
+    nb = mb.mlstm_chunkwise_workspace_bytes(B, NH, T, DQK, DV, w.L)
+    wsf = torch.empty(nb, dtype=torch.uint8, device="cuda") if nb else None
+    fwd = per_call(lambda: mb.mlstm_chunkwise_fwd(q, k, v, ip, fp, None, None, None, w.L, h, CT, nT, mT, workspace=wsf,
+                                                  stream=stream), steps)
+    tb, tf = float(np.median(bwd)), float(np.median(fwd))
+    fl_d2 = 2 * acc.flops_chunkwise(B * NH, T, 64, DQK, DV).total
+    out = dict(workload=f"backward_{w.name}", kernel="mlstm_chunkwise_bwd", calls=steps, ms_per_call=tb * 1e3,
+               ms_per_call_p10=float(np.quantile(bwd, 0.1)) * 1e3, ms_per_call_p90=float(np.quantile(bwd, 0.9)) * 1e3,
+               tokens_per_s=B * T / tb, forward_ms_per_call=tf * 1e3, backward_over_forward=tb / tf,
+               app_d2_flops=fl_d2, app_d2_tflops=fl_d2 / tb / 1e12,
+               mfma_frac=fl_d2 / tb / 1e12 / acc.PEAK_BF16_MFMA_TFLOPS)
+    if parallel:
+        dh32 = dh.float()
+        ws = torch.empty(mb.mlstm_parallel_bwd_workspace_bytes(B, NH, T, DV), dtype=torch.uint8, device="cuda")
+        par = per_call(lambda: mb.mlstm_parallel_bwd(q, k, v, ip, fp, dh32, *outs, ws, stream=stream), max(3, steps // 4))
+        tp = float(np.median(par))
+        fl = acc.flops_parallel_bwd(B * NH, T, DQK, DV)
+        out["parallel_form"] = dict(kernel="mlstm_parallel_bwd", ms_per_call=tp * 1e3, flops_per_call=fl,
+                                    tflops=fl / tp / 1e12, valu_frac=fl / tp / 1e12 / acc.PEAK_FP32_VALU_TFLOPS)
+    return out
 
 
 def cpu_model():
@@ -658,8 +692,9 @@ def main():
         res["layer"] = bench_layer(10, max(50, args.decode_steps // 4), stream)
         torch.cuda.empty_cache()
     if args.only in (None, "backward") and not args.skip_backward:
-        log(f"backward, {configs.PREFILL_T2048.name}")
-        res["backward"] = bench_backward(configs.PREFILL_T2048, 10, stream)
+        log(f"backward, {configs.PREFILL_T2048.name} and {configs.PREFILL_T8192.name}")
+        res["backward"] = [bench_backward(configs.PREFILL_T2048, 20, stream),
+                           bench_backward(configs.PREFILL_T8192, 10, stream, parallel=False)]
         torch.cuda.empty_cache()
     if args.only in (None, "decode") and not args.skip_decode:
         log(f"decode {configs.DECODE_B256.name}: {args.decode_steps} steps")

@@ -17,7 +17,7 @@ _lib = None
 def _load():
     global _lib
     if _lib is None:
-        path = build_oracle.build(force=False)
+        path = os.environ.get("MLSTM_ORACLE_LIBRARY") or build_oracle.build(force=False)
         lib = ctypes.CDLL(path)
         dp = ctypes.POINTER(ctypes.c_double)
         lib.oracle_mlstm_recurrent_f64.argtypes = [dp, dp, dp, dp, dp, dp, dp, dp,

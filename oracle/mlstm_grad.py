@@ -35,6 +35,14 @@ units).  With the stabiliser m_t of Eq. 2 every quantity is carried scaled by ex
 
 The pins in ``tests/test_grad_oracle.py`` tie ``recurrent_grad`` to central finite differences
 of the NumPy recurrent form, and ``parallel_grad`` to ``recurrent_grad``.
+
+``parallel_grad_scales`` gives, for the same closed form, the componentwise magnitude of every term
+an evaluation of dq, dk, dv sums, the inner dot products included:
+    |W|_ts   = (sum_v |dN~_tv v_sv| + sum_v |dh_tv h_tv| / den_t) F~_ts   (second term where |D~_t| > e^{-m_t})
+    |A~|_ts  = sum_d |q^_td k_sd| F~_ts
+    dq: sum_s |W|_ts |k_sd| / sqrt(DQK),  dk: sum_t |W|_ts |q^_td|,  dv: sum_t |A~|_ts |dN~_tv|.
+A gradient element whose terms cancel (W_ts nearly vanishes when h_t is close to v_s) is measured
+against these: a relative error of tol in every term is an error of at most tol times the scale.
 """
 from __future__ import annotations
 
@@ -122,4 +130,33 @@ def parallel_grad(q, k, v, ip, fp, dh):
         da = np.cumsum((P - di)[::-1])[::-1]
         out[3][s] = di
         out[4][s] = da / (1.0 + np.exp(fp[s]))                                    # sigmoid(-f~)
+    return tuple(out)
+
+
+def parallel_grad_scales(q, k, v, ip, fp, dh):
+    """Componentwise term magnitudes of dq, dk, dv in the closed form of ``parallel_grad`` (zero
+    initial state; see the module docstring): arrays of the shapes of q, k, v."""
+    q, k, v, ip, fp, dh = (np.asarray(x, dtype=np.float64) for x in (q, k, v, ip, fp, dh))
+    S, T, DQK = q.shape
+    out = [np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)]
+    tri = np.tril(np.ones((T, T), dtype=bool))
+    for s in range(S):
+        b = np.cumsum(_logsigmoid(fp[s]))
+        logF = np.where(tri, b[:, None] - b[None, :] + ip[s][None, :], -np.inf)
+        m = np.maximum(np.maximum.accumulate(ip[s] - b) + b, b)
+        Ft = np.exp(logF - m[:, None])
+        qh = q[s] / np.sqrt(DQK)
+        At = Ft * (qh @ k[s].T)
+        Nt = At @ v[s]
+        Dt = At.sum(axis=1)
+        den = np.maximum(np.abs(Dt), np.exp(-m))
+        h = Nt / den[:, None]
+        dN = dh[s] / den[:, None]
+        act = np.abs(Dt) > np.exp(-m)
+        dDa = np.where(act, (np.abs(dh[s]) * np.abs(h)).sum(axis=1) / den, 0.0)
+        Wa = (np.abs(dN) @ np.abs(v[s]).T + dDa[:, None]) * Ft
+        Aa = Ft * (np.abs(qh) @ np.abs(k[s]).T)
+        out[0][s] = (Wa @ np.abs(k[s])) / np.sqrt(DQK)
+        out[1][s] = Wa.T @ np.abs(qh)
+        out[2][s] = Aa.T @ np.abs(dN)
     return tuple(out)

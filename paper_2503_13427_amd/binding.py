@@ -15,10 +15,12 @@ from typing import Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmlstm.so")
+# MLSTM_LIBRARY selects another build of the same library (the host-sanitized libmlstm_san.so of
+# build_sanitize.py, for CPU-side checking); the default is the in-tree libmlstm.so
+LIB_PATH = os.environ.get("MLSTM_LIBRARY") or os.path.join(_HERE, "libmlstm.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"libmlstm.so is not built at {LIB_PATH}; run __graft_entry__.build() "
+    raise ImportError(f"libmlstm is not built at {LIB_PATH}; run __graft_entry__.build() "
                       "or python -m paper_2503_13427_amd.build")
 
 lib = ctypes.CDLL(LIB_PATH)

@@ -1,6 +1,7 @@
 // C-ABI layer of libmlstm: argument validation (pure host code, no HIP call
 // before a call is accepted), kernel selection and launch.
 #include <stdint.h>
+#include <string.h>
 
 #include <hip/hip_runtime.h>
 
@@ -32,14 +33,31 @@ inline bool mul_ok(int64_t a, int64_t b, int64_t* out) {
     return true;
 }
 
-inline size_t elem_bytes(mlstm_dtype dt) { return dt == MLSTM_BF16 ? 2 : 4; }
+// A C caller may pass any int as an mlstm_dtype: every test of the argument reads its raw value (a C++ enum
+// load outside the enumerators' range is undefined behaviour).
+// (reading the argument by value is such a load too, so these take its address)
+inline int dtype_code(const mlstm_dtype* d) {
+    int v;
+    memcpy(&v, d, sizeof v);
+    return v;
+}
+inline bool dtype_valid(const mlstm_dtype* d) { return dtype_code(d) == MLSTM_F32 || dtype_code(d) == MLSTM_BF16; }
+inline int norm_code(const mlstm_norm* n) {
+    int v;
+    memcpy(&v, n, sizeof v);
+    return v;
+}
+inline size_t elem_bytes(mlstm_dtype dt) { return dt == MLSTM_BF16 ? 2 : 4; }   // a validated dtype
 
 }  // namespace
 
 extern "C" {
 
 const char* mlstm_status_string(mlstm_status s) {
-    switch (s) {
+    // a C caller may pass any int: read the raw value (an enum load outside its range is undefined in C++)
+    int code;
+    memcpy(&code, &s, sizeof code);
+    switch (code) {
         case MLSTM_OK: return "MLSTM_OK";
         case MLSTM_ERR_NULL_PTR: return "MLSTM_ERR_NULL_PTR: a required pointer is NULL, or the initial state is partially given";
         case MLSTM_ERR_BAD_SHAPE: return "MLSTM_ERR_BAD_SHAPE: invalid size";
@@ -57,14 +75,14 @@ const char* mlstm_status_string(mlstm_status s) {
 int mlstm_version(void) { return 100; }
 
 size_t mlstm_chunkwise_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L, mlstm_dtype dt) {
-    if (B <= 0 || NH <= 0 || T < 0 || L <= 0) return 0;
+    if (B <= 0 || NH <= 0 || T < 0 || L <= 0 || !dtype_valid(&dt)) return 0;
     if (!mlstm::chunk_mfma_supported(dt, DQK, DV, L)) return 0;
     return mlstm::chunk_mfma_workspace_bytes(B, NH, T, DQK, DV, L);
 }
 
 // Validation and launch shared by mlstm_chunkwise_fwd (caller workspace) and
 // mlstm_chunkwise_fwd_noalloc (the library's fixed device scratch, use_scratch).
-static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void* v, mlstm_dtype dt,
+static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void* v, int dtc,
                                        const float* ipre, const float* fpre, const float* C0, const float* n0,
                                        const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
                                        float* CT, float* nT, float* mT, void* workspace, size_t workspace_bytes,
@@ -75,7 +93,8 @@ static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void*
     const int n_init = (C0 != nullptr) + (n0 != nullptr) + (m0 != nullptr);
     if (n_init != 0 && n_init != 3) return MLSTM_ERR_NULL_PTR;
     if (workspace_bytes > 0 && !workspace) return MLSTM_ERR_NULL_PTR;
-    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (dtc != MLSTM_F32 && dtc != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    const mlstm_dtype dt = static_cast<mlstm_dtype>(dtc);
     if (B <= 0 || NH <= 0 || T < 0 || DQK <= 0 || DV <= 0 || L <= 0) return MLSTM_ERR_BAD_SHAPE;
 
     int64_t S, ST, nq, nv, nC, nn;
@@ -129,7 +148,7 @@ mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, ml
                                  const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
                                  float* CT, float* nT, float* mT, void* workspace, size_t workspace_bytes,
                                  void* hip_stream) {
-    return chunkwise_fwd_impl(q, k, v, dt, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, workspace,
+    return chunkwise_fwd_impl(q, k, v, dtype_code(&dt), ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, workspace,
                               workspace_bytes, false, hip_stream);
 }
 
@@ -139,19 +158,20 @@ mlstm_status mlstm_chunkwise_fwd_noalloc(const void* q, const void* k, const voi
                                          const float* ipre, const float* fpre, const float* C0, const float* n0,
                                          const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
                                          float* CT, float* nT, float* mT, void* hip_stream) {
-    return chunkwise_fwd_impl(q, k, v, dt, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, nullptr, 0,
+    return chunkwise_fwd_impl(q, k, v, dtype_code(&dt), ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, nullptr, 0,
                               true, hip_stream);
 }
 
 // Validation shared by mlstm_step and mlstm_step_output (extra: the o~, weight and bias ranges
 // of the output variant, which h may not overlap either).
-static mlstm_status step_validate(const void* q, const void* k, const void* v, mlstm_dtype dt, const float* ipre,
+static mlstm_status step_validate(const void* q, const void* k, const void* v, int dtc, const float* ipre,
                                   const float* fpre, const float* C, const float* n, const float* m, int B, int NH,
                                   int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
                                   const Range* extra, int n_extra) {
     if (!q || !k || !v || !ipre || !fpre || !C || !n || !m || !h || !C_out || !n_out || !m_out)
         return MLSTM_ERR_NULL_PTR;
-    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (dtc != MLSTM_F32 && dtc != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    const mlstm_dtype dt = static_cast<mlstm_dtype>(dtc);
     if (B <= 0 || NH <= 0 || DQK <= 0 || DV <= 0 || (DV % 4)) return MLSTM_ERR_BAD_SHAPE;
     if (static_cast<int64_t>(DQK) * DV > (int64_t(1) << 20) || DQK > 4096) return MLSTM_ERR_UNSUPPORTED;
     int64_t S;
@@ -197,7 +217,7 @@ mlstm_status mlstm_step(const void* q, const void* k, const void* v, mlstm_dtype
                         const float* fpre, const float* C, const float* n, const float* m, int B, int NH,
                         int DQK, int DV, void* h, float* C_out, float* n_out, float* m_out,
                         void* hip_stream) {
-    const mlstm_status st = step_validate(q, k, v, dt, ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
+    const mlstm_status st = step_validate(q, k, v, dtype_code(&dt), ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
                                           nullptr, 0);
     if (st != MLSTM_OK) return st;
     hipError_t e = mlstm::launch_step(dt, q, k, v, ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
@@ -212,14 +232,15 @@ mlstm_status mlstm_step_output(const void* q, const void* k, const void* v, mlst
                                float* n_out, float* m_out, void* hip_stream) {
     if (!o_pre) return MLSTM_ERR_NULL_PTR;
     if (!(eps > 0.0f) || eps > 3.0e38f) return MLSTM_ERR_BAD_SHAPE;   // rejects NaN and inf too
-    if (norm != MLSTM_NORM_LAYER && norm != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
+    if (norm_code(&norm) != MLSTM_NORM_LAYER && norm_code(&norm) != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
     if (B > 0 && NH > 0 && DV > mlstm::kOutNormMaxDV) return MLSTM_ERR_UNSUPPORTED;
     if (misaligned(o_pre) || misaligned(weight) || misaligned(bias)) return MLSTM_ERR_MISALIGNED;
     int64_t S = 0, nw = 0;
     if (!mul_ok(B, NH, &S) || !mul_ok(NH, DV, &nw)) return MLSTM_ERR_BAD_SHAPE;
+    if (!dtype_valid(&dt)) return MLSTM_ERR_UNSUPPORTED;
     const Range extra[] = {range_of(o_pre, S * DV * elem_bytes(dt)), range_of(weight, weight ? nw * 4 : 0),
                            range_of(bias, bias ? nw * 4 : 0)};
-    const mlstm_status st = step_validate(q, k, v, dt, ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
+    const mlstm_status st = step_validate(q, k, v, dtype_code(&dt), ipre, fpre, C, n, m, B, NH, DQK, DV, h, C_out, n_out, m_out,
                                           extra, 3);
     if (st != MLSTM_OK) return st;
     hipError_t e = mlstm::launch_step_output(dt, q, k, v, ipre, fpre, C, n, m, o_pre, weight, bias, eps,
@@ -232,10 +253,10 @@ mlstm_status mlstm_output_norm(const void* h_tilde, const void* o_pre, mlstm_dty
                                const float* bias, float eps, mlstm_norm norm, int B, int NH, int T, int DV,
                                void* h, void* hip_stream) {
     if (T != 0 && (!h_tilde || !o_pre || !h)) return MLSTM_ERR_NULL_PTR;
-    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (!dtype_valid(&dt)) return MLSTM_ERR_UNSUPPORTED;
     if (B <= 0 || NH <= 0 || T < 0 || DV <= 0) return MLSTM_ERR_BAD_SHAPE;
     if (!(eps > 0.0f) || eps > 3.0e38f) return MLSTM_ERR_BAD_SHAPE;   // rejects NaN and inf too
-    if (norm != MLSTM_NORM_LAYER && norm != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
+    if (norm_code(&norm) != MLSTM_NORM_LAYER && norm_code(&norm) != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
     if ((DV % 4) || DV > mlstm::kOutNormMaxDV) return MLSTM_ERR_UNSUPPORTED;
     int64_t S, rows, nel, nw;
     if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &rows) || !mul_ok(rows, DV, &nel) || !mul_ok(NH, DV, &nw) ||
@@ -261,10 +282,10 @@ mlstm_status mlstm_output_norm_tokens(const void* h_tilde, const void* o_pre, in
                                       const float* weight, const float* bias, float eps, mlstm_norm norm, int B,
                                       int NH, int T, int DV, void* y, void* hip_stream) {
     if (T != 0 && (!h_tilde || !o_pre || !y)) return MLSTM_ERR_NULL_PTR;
-    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (!dtype_valid(&dt)) return MLSTM_ERR_UNSUPPORTED;
     if (B <= 0 || NH <= 0 || T < 0 || DV <= 0) return MLSTM_ERR_BAD_SHAPE;
     if (!(eps > 0.0f) || eps > 3.0e38f) return MLSTM_ERR_BAD_SHAPE;
-    if (norm != MLSTM_NORM_LAYER && norm != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
+    if (norm_code(&norm) != MLSTM_NORM_LAYER && norm_code(&norm) != MLSTM_NORM_RMS) return MLSTM_ERR_BAD_SHAPE;
     if ((DV % 4) || DV > mlstm::kOutNormMaxDV) return MLSTM_ERR_UNSUPPORTED;
     int64_t S, rows, nel, nw, toks, ospan;
     if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &rows) || !mul_ok(rows, DV, &nel) || !mul_ok(NH, DV, &nw) ||
@@ -298,7 +319,7 @@ mlstm_status mlstm_gate_preact(const void* x, mlstm_dtype dt, const void* w_t, c
         return MLSTM_ERR_BAD_SHAPE;
     if (M != 0 && (!x || !w_t || !ipre || !fpre)) return MLSTM_ERR_NULL_PTR;
     if (!(cap >= 0.0f) || cap > 3.0e38f) return MLSTM_ERR_BAD_SHAPE;   // rejects NaN and inf too
-    if (dt != MLSTM_BF16 || d % mlstm::kGateDMultiple || 2 * static_cast<int64_t>(NH) > mlstm::kGateMaxCols)
+    if (dtype_code(&dt) != MLSTM_BF16 || d % mlstm::kGateDMultiple || 2 * static_cast<int64_t>(NH) > mlstm::kGateMaxCols)
         return MLSTM_ERR_UNSUPPORTED;
     // a workgroup addresses its 64 rows of x, and all of w_t, through 32-bit byte offsets
     if (64 * static_cast<int64_t>(d) * 2 >= (int64_t(1) << 31) || nw * 2 >= (int64_t(1) << 31))
@@ -339,7 +360,7 @@ mlstm_status mlstm_parallel_bwd(const void* q, const void* k, const void* v, mls
         for (const void* p : req)
             if (!p) return MLSTM_ERR_NULL_PTR;
     }
-    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (!dtype_valid(&dt)) return MLSTM_ERR_UNSUPPORTED;
     if (!mlstm::parallel_bwd_supported(DQK, DV)) return MLSTM_ERR_UNSUPPORTED;
     const size_t ws_need = mlstm::parallel_bwd_workspace_bytes(B, NH, T, DV);
     if (T != 0 && workspace_bytes < ws_need) return MLSTM_ERR_WORKSPACE;
@@ -365,7 +386,7 @@ mlstm_status mlstm_parallel_bwd(const void* q, const void* k, const void* v, mls
 }
 
 size_t mlstm_chunkwise_bwd_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L, mlstm_dtype dt) {
-    if (B <= 0 || NH <= 0 || T < 0 || !mlstm::chunk_bwd_supported(dt, DQK, DV, L)) return 0;
+    if (B <= 0 || NH <= 0 || T < 0 || !dtype_valid(&dt) || !mlstm::chunk_bwd_supported(dt, DQK, DV, L)) return 0;
     return mlstm::chunk_bwd_workspace_bytes(B, NH, T);
 }
 
@@ -383,7 +404,7 @@ mlstm_status mlstm_chunkwise_bwd(const void* q, const void* k, const void* v, ml
     const int n_init = (C0 != nullptr) + (n0 != nullptr) + (m0 != nullptr);
     const int n_grad = (dC0 != nullptr) + (dn0 != nullptr) + (dm0 != nullptr);
     if ((n_init != 0 && n_init != 3) || (n_grad != 0 && n_grad != 3)) return MLSTM_ERR_NULL_PTR;
-    if (dt != MLSTM_F32 && dt != MLSTM_BF16) return MLSTM_ERR_UNSUPPORTED;
+    if (!dtype_valid(&dt)) return MLSTM_ERR_UNSUPPORTED;
     int64_t S, nt, nqk, nv, nC, nn;
     if (!mul_ok(B, NH, &S) || !mul_ok(S, T, &nt) || !mul_ok(nt, DQK, &nqk) || !mul_ok(nt, DV, &nv) ||
         !mul_ok(S, static_cast<int64_t>(DQK) * DV, &nC) || !mul_ok(S, DQK, &nn))

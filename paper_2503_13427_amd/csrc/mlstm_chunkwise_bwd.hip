@@ -632,7 +632,6 @@ __global__ void __launch_bounds__(256) bwd_scan_kernel(BwdParams A) {
 
 // ---- dk and dv inter terms ---------------------------------------------------------------------
 struct InterKVSmem {
-    uint16_t V[kBL * kHP];
     uint16_t G[2][kBL * kWP];   // 64 rows d x 128 columns v of Gam_c, hi and lo
     float wk[kBL];
     float red[4][kBL];
@@ -654,7 +653,6 @@ __global__ void __launch_bounds__(kBT) bwd_interkv_kernel(BwdParams A) {
     const bool has_g = c < A.NC - 1;   // the last chunk's exit state receives no gradient
 
     if (tid < kBL) S.wk[tid] = (t0 + tid < T) ? A.tok[(st + t0 + tid) * kTokF] : 0.0f;
-    if (has_g) stage_rows<kDV>(S.V, kHP, rv, kDV, t0, 0, tid);
     __syncthreads();
 
     // dk^T [d][tau] += wk_tau (sum_v Gam[d][v] V[tau][v] + gam[d]); rows d = d0 + 16 wave + l16
@@ -665,15 +663,20 @@ __global__ void __launch_bounds__(kBT) bwd_interkv_kernel(BwdParams A) {
         if (has_g) {
             const uint16_t* hi = hl_of(A, s, c) + static_cast<int64_t>(d0 + 16 * wave + l16) * kDV + 8 * g16;
             const uint16_t* lo = hi + kCV;
-#pragma unroll 4
+            // V rows (B operands) straight from memory, shared by the chunk's four tiles in L2; the LDS
+            // then holds only the Gam block, so several workgroups share a CU
+#pragma unroll 2
             for (int ks = 0; ks < kDV / 32; ++ks) {
                 const u32x4_t ah = *reinterpret_cast<const u32x4_t*>(hi + 32 * ks);
                 const u32x4_t al = *reinterpret_cast<const u32x4_t*>(lo + 32 * ks);
+                u32x4_t b[4];
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb)
+                    b[tb] = bload128(rv, static_cast<uint32_t>((t0 + 16 * tb + l16) * kDV + 32 * ks + 8 * g16) * 2u, 0);
 #pragma unroll
                 for (int tb = 0; tb < 4; ++tb) {
-                    const u32x4_t b = row_op(S.V, kHP, 16 * tb, 32 * ks, lane);
-                    acc[tb] = mfma16(ah, b, acc[tb]);
-                    acc[tb] = mfma16(al, b, acc[tb]);
+                    acc[tb] = mfma16(ah, b[tb], acc[tb]);
+                    acc[tb] = mfma16(al, b[tb], acc[tb]);
                 }
             }
         }

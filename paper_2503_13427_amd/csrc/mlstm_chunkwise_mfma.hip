@@ -170,14 +170,18 @@ struct VRegs {
 // With K^T staging (L = 128) K is loaded in pieces in the MFMA A-operand layout: piece i of wave w
 // (pc = w + 8 i, a = pc % (L / 16), b = pc / (L / 16)) has lane (l16, g16) holding
 // K[tau 16 a + l16][d 32 b + 8 g16 + 0..7] of the d block.
+// The chunk's row offset t0 rides in the per-lane offset, which the buffer range check covers (the
+// scalar offset is outside it), so rows past the end of a sequence read as zero in a partial last
+// chunk; the scalar offset carries only the column base.
 template <int L>
 __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, int p, int tid) {
     constexpr int DB = Cfg<L>::DB, PR = DB / 8;   // 16-byte pieces per row
-    const uint32_t soff = static_cast<uint32_t>(t0) * (kDQK * 2) + p * (DB * 2);
+    const uint32_t soff = p * (DB * 2);
+    const uint32_t roff = static_cast<uint32_t>(t0) * (kDQK * 2);
 #pragma unroll
     for (int i = 0; i < QKRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
-        const uint32_t voff = (item / PR) * (kDQK * 2) + 16 * (item % PR);
+        const uint32_t voff = roff + (item / PR) * (kDQK * 2) + 16 * (item % PR);
         r.q[i] = bload128(R.q, voff, soff);
         if constexpr (!Cfg<L>::KT) r.k[i] = bload128(R.k, voff, soff);
     }
@@ -189,7 +193,7 @@ __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, 
 #pragma unroll
         for (int i = 0; i < QKRegs<L>::N; ++i) {
             const int pc = wave + kWaves * i, a = pc % (L / 16), b = pc / (L / 16);
-            r.k[i] = bload128(R.k, (16 * a + (ln & 15)) * (kDQK * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
+            r.k[i] = bload128(R.k, roff + (16 * a + (ln & 15)) * (kDQK * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
         }
     }
 }
@@ -244,13 +248,14 @@ template <int L>
 __device__ __forceinline__ void load_v_tr(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane, int part) {
     static_assert(VRegs<L>::PARTS * VRegs<L>::N * kWaves == (L / 16) * (kDVT / 32), "pieces of one L x 128 chunk");
     constexpr int NA = L / 16;
-    const uint32_t soff = static_cast<uint32_t>(t0) * (kDV * 2) + v0 * 2;
+    const uint32_t soff = v0 * 2;   // the row offset goes in the range-checked per-lane offset
+    const uint32_t roff = static_cast<uint32_t>(t0) * (kDV * 2);
     int ln = lane;   // opaque: the offsets are recomputed per call rather than held across the loop
     asm volatile("" : "+v"(ln));
 #pragma unroll
     for (int i = 0; i < VRegs<L>::N; ++i) {
         const int pc = wave + kWaves * (part * VRegs<L>::N + i), a = pc % NA, b = pc / NA;
-        r.v[i] = bload128(R.v, (16 * a + (ln & 15)) * (kDV * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
+        r.v[i] = bload128(R.v, roff + (16 * a + (ln & 15)) * (kDV * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
     }
 }
 template <int L>
@@ -317,12 +322,12 @@ __device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const VtPacked<L>&
 // Gate pre-activations of one chunk, one (L = 64) or two (L = 128) per lane of the gate wave.
 template <int L>
 __device__ __forceinline__ void load_gates(float (&gi)[2], float (&gf)[2], const SeqRsrc& R, int t0, int lane) {
-    const uint32_t goff = static_cast<uint32_t>(t0) * 4;
-    gi[0] = bloadf(R.ig, 4 * lane, goff);
-    gf[0] = bloadf(R.fg, 4 * lane, goff);
+    const uint32_t goff = static_cast<uint32_t>(t0 + lane) * 4;   // range-checked: zero past the end
+    gi[0] = bloadf(R.ig, goff, 0);
+    gf[0] = bloadf(R.fg, goff, 0);
     if constexpr (L == 128) {
-        gi[1] = bloadf(R.ig, 4 * lane + 256, goff);
-        gf[1] = bloadf(R.fg, 4 * lane + 256, goff);
+        gi[1] = bloadf(R.ig, goff + 256, 0);
+        gf[1] = bloadf(R.fg, goff + 256, 0);
     }
 }
 
@@ -1256,7 +1261,8 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
                     cur.y = a * cur.y + b * loc[u].y;
                     cur.z = a * cur.z + b * loc[u].z;
                     cur.w = a * cur.w + b * loc[u].w;
-                    if (entry) reinterpret_cast<float4*>(slot)[e4] = cur;
+                    // (with rowhl, C goes out only as bf16 hi + lo rows; n and m stay in the slot)
+                    if (entry && (!rowhl || e4 >= kDQK * kDV / 4)) reinterpret_cast<float4*>(slot)[e4] = cur;
                     if (entry && rowhl && e4 < kDQK * kDV / 4) {
                         // the entry state also as bf16 hi + lo rows [d][v] (the backward pass's operand)
                         uint16_t* hl = rowhl + (static_cast<int64_t>(s) * NS + g0 + u) * 2 * kDQK * kDV;

@@ -119,3 +119,17 @@ def alloc_prefill_outputs(inp: Inputs, device="cuda"):
                 CT=torch.empty(B, NH, DQK, DV, dtype=torch.float32, device=device),
                 nT=torch.empty(B, NH, DQK, dtype=torch.float32, device=device),
                 mT=torch.empty(B, NH, dtype=torch.float32, device=device))
+
+
+def gate_scales(q, k, fp, ref):
+    """Magnitudes of the summands of the gate gradients, [S, T] each, from the reference gradients
+    ref = (dq, dk, ...): di~_t = k_t . dk_t sums k_td dk_td; dlogsig(f~_t) sums q_t'd dq_t'd - k_t'd dk_t'd
+    over t' >= t, times sigmoid(-f~_t) for df~.  A gate gradient's error is measured against these."""
+    S, T = ref[0].shape[0], ref[0].shape[1]
+    q = np.asarray(q, np.float64).reshape(S, T, -1)
+    k = np.asarray(k, np.float64).reshape(S, T, -1)
+    aq = np.abs(q * ref[0].reshape(S, T, -1)).sum(axis=2)
+    ak = np.abs(k * ref[1].reshape(S, T, -1)).sum(axis=2)
+    tail = np.cumsum((aq + ak)[:, ::-1], axis=1)[:, ::-1]
+    sig = 1.0 / (1.0 + np.exp(np.asarray(fp, np.float64).reshape(S, T)))
+    return ak, sig * tail

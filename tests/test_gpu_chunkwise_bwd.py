@@ -5,8 +5,9 @@ xLSTM-7B prefill shapes from the zero state.
 
 Bars: dq, dk, dv and dC0 per row (a token's row, a
 d-row of C0) at the bf16 bar of 2e-2, a row that is zero in exact arithmetic held to 1e-3 of its
-tensor's largest row; dn0 per sequence; the gate gradients, one value per token, per sequence slice
-at the same bar.  dm0 = <dC0, C0> + dn0 . n0 is a sum of terms of both signs whose total can be far
+tensor's largest row; dn0 per sequence; the gate gradients, sums of terms of both signs, against
+the magnitude of their summands (|err_t| <= tol sum_d |k_td dk_td| for di~, tol sigmoid(-f~_t)
+sum_{t' >= t} sum_d (|q dq| + |k dk|) for df~, from the oracle's gradients).  dm0 = <dC0, C0> + dn0 . n0 is a sum of terms of both signs whose total can be far
 below the terms: its error is held to the bar times the sum of the terms' magnitudes,
 sum |dC0 C0| + sum |dn0 n0| (the error an elementwise relative error of the bar produces)."""
 import numpy as np
@@ -15,7 +16,7 @@ import torch
 
 from oracle import mlstm_grad as G
 from paper_2503_13427_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
-from tests.helpers import TOL_BF16, rel_err, row_err
+from tests.helpers import TOL_BF16, gate_scales, rel_err, row_err
 
 pytestmark = pytest.mark.gpu
 
@@ -83,8 +84,9 @@ def run(B, NH, q, k, v, ip, fp, dh, st, want_state=True):
 NAMES = ["dq", "dk", "dv", "di", "df", "dC0", "dn0", "dm0"]
 
 
-def compare(got, ref, label, tol=TOL_BF16, state=None):
+def compare(got, ref, label, tol=TOL_BF16, state=None, q=None, k=None, fp=None):
     errs = {}
+    sc = gate_scales(q, k, fp, ref)
     for n, g, r in zip(NAMES, got, ref):
         g = np.asarray(g, np.float64)
         r = np.asarray(r, np.float64).reshape(g.shape)
@@ -97,7 +99,11 @@ def compare(got, ref, label, tol=TOL_BF16, state=None):
             scale = (np.abs(np.asarray(ref[5]) * np.asarray(state[0], np.float64)).sum(axis=(1, 2)) +
                      np.abs(np.asarray(ref[6]) * np.asarray(state[1], np.float64)).sum(axis=1))
             errs[n] = float((np.abs(g - r) / np.where(scale > 0, scale, 1.0)).max())
-        else:   # di, df per sequence; dn0 per sequence
+        elif n in ("di", "df"):
+            scale = sc[0] if n == "di" else sc[1]
+            d = np.abs(g.reshape(scale.shape) - r.reshape(scale.shape))
+            errs[n] = float((d / np.where(scale > 0, scale, 1.0)).max()) if d.size else 0.0
+        else:   # dn0 per sequence
             errs[n] = rel_err(g.reshape(g.shape[0], -1), r.reshape(g.shape[0], -1), 1)
     print(label + " " + " ".join(f"{n} {e:.2e}" for n, e in errs.items()))
     assert max(errs.values()) <= tol, errs
@@ -125,7 +131,7 @@ def test_chunk_bwd_matches_recurrent_oracle(case):
     else:
         st0 = st
     ref = G.recurrent_grad_state(q, k, v, ip, fp, *st0, dh)
-    compare(got, ref, label, state=st0)
+    compare(got, ref, label, state=st0, q=q, k=k, fp=fp)
 
 
 @pytest.mark.parametrize("T", [2048, 8192])
@@ -138,4 +144,4 @@ def test_chunk_bwd_prefill_shapes_sampled_heads(T):
     for hd in (0, NH - 1):
         sl = slice(hd, hd + 1)
         ref = G.parallel_grad(q[sl], k[sl], v[sl], ip[sl], fp[sl], dh[sl])
-        compare([g[sl] for g in got], ref, f"T{T} head {hd}")
+        compare([g[sl] for g in got], ref, f"T{T} head {hd}", q=q[sl], k=k[sl], fp=fp[sl])

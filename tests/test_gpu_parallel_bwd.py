@@ -2,23 +2,31 @@
 gradient oracle: ``recurrent_grad`` (autograd over the step-by-step cell) for small shapes and
 ``parallel_grad`` (its closed form, pinned to it) for the xLSTM-7B head shape.
 
-Bars, per (batch, head) slice of each gradient: max relative error <= 1e-4 for fp32 q/k/v,
-<= 2e-2 for bf16 q/k/v (the oracle upcasts the same bf16 values).  No bar is stated for gradients;
-1e-4 comes from the arithmetic: df~ is a reverse cumulative sum of P_t - di~_t, each an fp32 sum
-over up to T pair terms, and the two nearly cancel, so fp32 rounding of order T 2^-24 on each is
-amplified by that cancellation (1e-5 is reached at T = 64 with short memory).  Covers ragged T (not a
-multiple of the 16-token tile), one token, the floor branch and short memory, on both the VALU
-passes (DQK or DV not a multiple of 64) and the MFMA passes, and the benchmarked shape (8 heads,
-T = 2048) with sampled heads."""
+Bars: dq, dk, dv per token row at the spec bars, 1e-5 for fp32 q/k/v and 2e-2 for bf16 (the
+oracle upcasts the same bf16 values), a row that is zero in exact arithmetic held to 1e-3 of its
+tensor's largest row.  A row whose value is far below its terms (dq_t sums W_ts k_s over s with
+W_ts = dh_t . (v_s - sign(D_t) h_t) F~_ts / den_t, which nearly vanishes when h_t is close to v_s, as
+with a short memory) may instead meet the bar elementwise against the magnitudes of all the terms an
+evaluation sums, inner dot products included (``parallel_grad_scales``); a row passes if either
+error is within the bar.  The gate gradients are sums of terms of both signs that cancel:
+di~_t = k_t . dk_t and dlogsig(f~_t) = sum_{t' >= t} (q_t' . dq_t' - k_t' . dk_t'), so an error
+relative to their cancelled value says nothing about the arithmetic.  Their bar is the same
+relative bar applied to the magnitude of the summands, from the oracle's own gradients:
+|di~_t - ref| <= tol sum_d |k_td dk_td| and
+|df~_t - ref| <= tol sigmoid(-f~_t) sum_{t' >= t} sum_d (|q_t'd dq_t'd| + |k_t'd dk_t'd|),
+which is what a relative error of tol in every summand produces.  Covers ragged T (not a multiple
+of the 16-token tile), one token, the floor branch and short memory, on both the VALU passes (DQK or
+DV not a multiple of 64) and the MFMA passes, and the benchmarked shape (8 heads, T = 2048) with
+sampled heads."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import mlstm_grad as G
 from paper_2503_13427_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
-from tests.helpers import TOL_BF16, rel_err, row_err
+from tests.helpers import TOL_BF16, TOL_F32, gate_scales, row_errs
 
-TOL_BWD_F32 = 1e-4
+TOL_BWD_F32 = TOL_F32
 
 pytestmark = pytest.mark.gpu
 
@@ -58,18 +66,28 @@ def run(B, NH, q, k, v, ip, fp, dh, dtype):
     return [o.cpu().numpy().astype(np.float64).reshape(S, T, -1) for o in outs]
 
 
-def compare(got, ref, tol, label):
+def compare(got, ref, tol, label, q, k, fp, term_scales=None):
     names = ["dq", "dk", "dv", "di", "df"]
     errs = []
+    sc = gate_scales(q, k, fp, ref)
     for n, g, r in zip(names, got, ref):
-        S, T = r.shape[0], r.shape[1]
-        # dq, dk, dv per token row (a row that is zero in exact arithmetic, such as dq of a first
-        # token whose denominator is above the floor, held to 1e-3 of the tensor's largest row);
-        # the gate gradients (one value per token) per sequence
-        e = row_err(g, r, r.shape[2], f"{label} {n}", floor=1e-3) if n in ("dq", "dk", "dv") else \
-            rel_err(g.reshape(S, -1), r.reshape(S, -1), 1)
-        errs.append(e)
         assert np.isfinite(g).all(), n
+        if n in ("dq", "dk", "dv"):
+            # per token row; a row that is zero in exact arithmetic (such as dq of a first token whose
+            # denominator is above the floor) is held to 1e-3 of the tensor's largest row
+            er = row_errs(g, r, r.shape[2], floor=1e-3)
+            if term_scales is not None:
+                ts = np.asarray(term_scales[names.index(n)]).reshape(g.shape)
+                et = (np.abs(g - r) / np.where(ts > 0, ts, 1.0)).reshape(er.size, -1).max(axis=1)
+                er = np.minimum(er, et)
+            e = float(er.max()) if er.size else 0.0
+            print(f"{label} {n}: {er.size} rows, median {np.median(er):.2e}, max {e:.2e}")
+        else:
+            S, T = r.shape[0], r.shape[1]
+            scale = sc[0] if n == "di" else sc[1]
+            d = np.abs(g.reshape(S, T) - r.reshape(S, T))
+            e = float((d / np.where(scale > 0, scale, 1.0)).max()) if d.size else 0.0
+        errs.append(e)
     print(label + " " + " ".join(f"{n} {e:.2e}" for n, e in zip(names, errs)))
     assert max(errs) <= tol, dict(zip(names, errs))
 
@@ -95,7 +113,7 @@ def test_parallel_bwd_fp32_matches_oracle(case):
     got = run(B, NH, q, k, v, ip, fp, dh, "f32")
     ref = G.recurrent_grad(q, k, v, ip, fp, dh)
     ref = [r.reshape(r.shape[0], r.shape[1], -1) for r in ref]
-    compare(got, ref, TOL_BWD_F32, str(case))
+    compare(got, ref, TOL_BWD_F32, str(case), q, k, fp, G.parallel_grad_scales(q, k, v, ip, fp, dh))
 
 
 @pytest.mark.parametrize("T", [128, 300])
@@ -105,7 +123,7 @@ def test_parallel_bwd_bf16_xlstm_head(T):
     got = run(B, NH, q, k, v, ip, fp, dh, "bf16")
     ref = G.parallel_grad(q, k, v, ip, fp, dh)
     ref = [r.reshape(r.shape[0], r.shape[1], -1) for r in ref]
-    compare(got, ref, TOL_BF16, f"7B head T{T}")
+    compare(got, ref, TOL_BF16, f"7B head T{T}", q, k, fp)
 
 
 @pytest.mark.parametrize("dtype,DQK,DV", [("f32", 64, 128), ("bf16", 256, 512)])
@@ -128,7 +146,8 @@ def test_autograd_cell_gradients(dtype, DQK, DV):
     wr = w if dtype == "f32" else bf16_bits_to_f32(f32_to_bf16_bits(w))
     ref = G.recurrent_grad(q, k, v, ip, fp, wr)
     ref = [r.reshape(r.shape[0], r.shape[1], -1) for r in ref]
-    compare(got, ref, TOL_BWD_F32 if dtype == "f32" else TOL_BF16, f"autograd cell {dtype}")
+    compare(got, ref, TOL_BWD_F32 if dtype == "f32" else TOL_BF16, f"autograd cell {dtype}", q, k, fp,
+            G.parallel_grad_scales(q, k, v, ip, fp, wr))
 
 
 def test_parallel_bwd_full_size_sampled_heads():
@@ -141,5 +160,5 @@ def test_parallel_bwd_full_size_sampled_heads():
         sl = slice(h, h + 1)
         ref = G.parallel_grad(q[sl], k[sl], v[sl], ip[sl], fp[sl], dh[sl])
         ref = [r.reshape(1, T, -1) for r in ref]
-        compare([g[sl] for g in got], ref, TOL_BF16, f"T{T} head {h}")
+        compare([g[sl] for g in got], ref, TOL_BF16, f"T{T} head {h}", q[sl], k[sl], fp[sl])
     assert all(np.isfinite(g).all() for g in got)

@@ -149,3 +149,33 @@ def test_state_grad_with_borders():
                                   np.zeros((1, 3)), np.zeros(1), dh[:, 5:])
     for x, y in zip(g[:5], tail[:5]):
         np.testing.assert_allclose(x[:, 5:], y, rtol=1e-10, atol=1e-12)
+
+
+def test_term_scales_bound_the_gradients():
+    """parallel_grad_scales sums the magnitudes of every term of each element of dq, dk, dv (inner dot
+    products included), so it bounds the gradient elementwise (triangle inequality) and is strictly
+    larger somewhere."""
+    rng = np.random.default_rng(41)
+    S, T, DQK, DV = 2, 23, 8, 6
+    q, k = rng.standard_normal((S, T, DQK)), rng.standard_normal((S, T, DQK))
+    v, dh = rng.standard_normal((S, T, DV)), rng.standard_normal((S, T, DV))
+    ip, fp = rng.standard_normal((S, T)), rng.normal(1.0, 2.0, (S, T))
+    g = G.parallel_grad(q, k, v, ip, fp, dh)
+    sc = G.parallel_grad_scales(q, k, v, ip, fp, dh)
+    for x, s in zip(g[:3], sc):
+        assert (s >= np.abs(x) - 1e-12 * (1 + np.abs(x))).all()
+        assert (s > np.abs(x) * (1 + 1e-6)).any()
+
+
+def test_term_scales_without_cancellation_are_the_gradient_magnitudes():
+    """One token, one dimension, positive q, k, v, dh and the floor active (no denominator term): every
+    element of dq, dk, dv is a single product of positive factors, so its scale is its magnitude."""
+    rng = np.random.default_rng(42)
+    S, T = 4, 1
+    q, k = rng.uniform(0.5, 1.0, (S, T, 1)), rng.uniform(0.5, 1.0, (S, T, 1))
+    v, dh = rng.uniform(0.5, 1.0, (S, T, 1)), rng.uniform(0.5, 1.0, (S, T, 1))
+    ip, fp = np.full((S, T), -5.0), rng.standard_normal((S, T))
+    g = G.parallel_grad(q, k, v, ip, fp, dh)
+    sc = G.parallel_grad_scales(q, k, v, ip, fp, dh)
+    for x, s in zip(g[:3], sc):
+        np.testing.assert_allclose(s, np.abs(x), rtol=1e-12)

@@ -350,18 +350,23 @@ def bench_layer_prefill(layer, B, T, steps, stream):
     x2 = x.reshape(B * T, d)
     t_proj = run(lambda: layer._project(x2))
     t_gates = run(lambda: layer.gates(x))
-    # the stages as the prefill runs them: head-major copies of q, k, v; o~ read in place by the norm
+    # the stages as the prefill runs them: the cell reads q, k, v as per-head views of the projection
+    # output and the norm reads o~ in place (no head-major copies)
     q4, k4, v4, o4 = layer._project(x2)
-    hm = lambda a, D: a.view(B, T, NH, D).transpose(1, 2).contiguous()
-    t_heads = run(lambda: (hm(q4, DQK), hm(k4, DQK), hm(v4, DV)))
-    q, k, v = hm(q4, DQK), hm(k4, DQK), hm(v4, DV)
+    hv = lambda a, D: a.view(B, T, NH, D).transpose(1, 2)
+    q, k, v = hv(q4, DQK), hv(k4, DQK), hv(v4, DV)
     ig, fg = layer.gates(x)
     h = torch.empty(B, NH, T, DV, dtype=torch.bfloat16, device="cuda")
     C = torch.empty(B, NH, DQK, DV, device="cuda")
     n = torch.empty(B, NH, DQK, device="cuda")
     m = torch.empty(B, NH, device="cuda")
-    t_cell = run(lambda: mb.mlstm_chunkwise_fwd(q, k, v, ig, fg, None, None, None, layer.L, h, C, n, m,
-                                                 workspace=ws, stream=stream))
+    t_cell = run(lambda: mb.mlstm_chunkwise_fwd_strided(q, k, v, ig, fg, None, None, None, layer.L, h, C, n, m,
+                                                         workspace=ws, stream=stream))
+    # for comparison: the cell on head-major copies (what the copies would cost is not in the total)
+    qc, kc, vc = q.contiguous(), k.contiguous(), v.contiguous()
+    t_cell_contig = run(lambda: mb.mlstm_chunkwise_fwd(qc, kc, vc, ig, fg, None, None, None, layer.L, h, C, n, m,
+                                                        workspace=ws, stream=stream))
+    del qc, kc, vc
     yh = torch.empty(B, T, NH, DV, dtype=torch.bfloat16, device="cuda")
     o_view = o4.view(B, T, NH, DV)
     t_norm = run(lambda: mb.mlstm_output_norm_tokens(h, o_view, w.norm_weight, None, layer.eps, "layer", yh,
@@ -370,12 +375,11 @@ def bench_layer_prefill(layer, B, T, steps, stream):
     tok = B * T
     fl_proj = acc.flops_layer_projections(tok, d, NH, DQK, DV)
     fl_cell = acc.flops_chunkwise(B * NH, T, layer.L, DQK, DV).total
-    stages = dict(projections=t_proj, gates=t_gates, head_major_copies=t_heads, cell=t_cell, output_norm=t_norm,
-                  output_projection=t_out)
+    stages = dict(projections=t_proj, gates=t_gates, cell=t_cell, output_norm=t_norm, output_projection=t_out)
     return dict(workload=f"layer_prefill_B{B}_T{T}_d{d}_NH{NH}", B=B, T=T, tokens_per_s=tok / t_total,
                 ms_per_call=t_total * 1e3, tflops=(fl_proj + fl_cell) / t_total / 1e12,
                 flops_projections=fl_proj, flops_cell=fl_cell,
-                stages_ms={k: v * 1e3 for k, v in stages.items()},
+                stages_ms={k: v * 1e3 for k, v in stages.items()}, cell_on_contiguous_copies_ms=t_cell_contig * 1e3,
                 stages_share={k: v / t_total for k, v in stages.items()})
 
 

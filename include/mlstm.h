@@ -111,6 +111,29 @@ mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, ml
                                  void* workspace, size_t workspace_bytes, void* hip_stream);
 
 /*
+ * mlstm_chunkwise_fwd on strided q, k, v (for instance per-head views of one
+ * projection output [B, T, NH, D], which a layer then need not copy into
+ * head-major order).  qkv_strides holds 9 element strides: q's for the
+ * batch, head and token axes, then k's, then v's; the D elements of a row are
+ * contiguous.  Every stride must be a multiple of 8 (16-byte rows;
+ * MLSTM_ERR_MISALIGNED), non-negative, with token strides of at least D
+ * (MLSTM_ERR_BAD_SHAPE), and one sequence's rows plus 127 more token
+ * strides must span under 2^31 bytes (MLSTM_ERR_UNSUPPORTED).  The other
+ * arguments, results and workspace (mlstm_chunkwise_workspace_bytes) are
+ * those of mlstm_chunkwise_fwd; the alias checks cover the element ranges
+ * the views span.  Built for the bf16
+ * MFMA path (dt = MLSTM_BF16, DQK = 256, DV = 512, L in {64, 128}); other
+ * shapes return MLSTM_ERR_UNSUPPORTED.  qkv_strides NULL is MLSTM_ERR_NULL_PTR.
+ */
+mlstm_status mlstm_chunkwise_fwd_strided(const void* q, const void* k, const void* v,
+                                         const int64_t* qkv_strides, mlstm_dtype dt,
+                                         const float* ipre, const float* fpre,
+                                         const float* C0, const float* n0, const float* m0,
+                                         int B, int NH, int T, int DQK, int DV, int L,
+                                         void* h, float* CT, float* nT, float* mT,
+                                         void* workspace, size_t workspace_bytes, void* hip_stream);
+
+/*
  * For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc):
  * mlstm_chunkwise_fwd with no workspace argument and no allocation.  Same

@@ -38,6 +38,9 @@ _i = ctypes.c_int
 lib.mlstm_chunkwise_fwd.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                     _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
 lib.mlstm_chunkwise_fwd.restype = _i
+lib.mlstm_chunkwise_fwd_strided.argtypes = [_vp, _vp, _vp, ctypes.POINTER(ctypes.c_int64), _i, _vp, _vp, _vp, _vp, _vp,
+                                            _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+lib.mlstm_chunkwise_fwd_strided.restype = _i
 lib.mlstm_chunkwise_fwd_noalloc.argtypes = [_vp, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                             _vp, _vp, _vp, _vp, _vp]
 lib.mlstm_chunkwise_fwd_noalloc.restype = _i
@@ -103,6 +106,11 @@ def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return t.data_ptr()
 
 
+def _view_ptr(t: torch.Tensor) -> int:
+    """Data pointer of a strided view (its strides travel separately)."""
+    return t.data_ptr()
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -134,6 +142,23 @@ def mlstm_chunkwise_fwd(q, k, v, ipre, fpre, C0, n0, m0, L, h, CT, nT, mT,
                                    _ptr(C0), _ptr(n0), _ptr(m0), B, NH, T, DQK, DV, int(L),
                                    _ptr(h), _ptr(CT), _ptr(nT), _ptr(mT), _ptr(workspace), ws_bytes,
                                    _stream(stream)))
+
+
+def mlstm_chunkwise_fwd_strided(q, k, v, ipre, fpre, C0, n0, m0, L, h, CT, nT, mT,
+                                workspace=None, stream=None) -> None:
+    """mlstm_chunkwise_fwd on strided views q, k [B, NH, T, DQK], v [B, NH, T, DV] (bf16, rows of D
+    contiguous), for instance ``x.view(B, T, NH, D).transpose(1, 2)`` of a projection output."""
+    B, NH, T, DQK = q.shape
+    DV = v.shape[3]
+    for t in (q, k, v):
+        if t.stride(3) != 1:
+            raise ValueError("the rows (last axis) of q, k, v must be contiguous")
+    st = (ctypes.c_int64 * 9)(*(q.stride()[:3] + k.stride()[:3] + v.stride()[:3]))
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib.mlstm_chunkwise_fwd_strided(_view_ptr(q), _view_ptr(k), _view_ptr(v), st, _dtype_code(q), _ptr(ipre),
+                                           _ptr(fpre),
+                                           _ptr(C0), _ptr(n0), _ptr(m0), B, NH, T, DQK, DV, L, _ptr(h), _ptr(CT),
+                                           _ptr(nT), _ptr(mT), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def mlstm_chunkwise_scratch_bytes() -> int:

@@ -78,6 +78,9 @@ struct ChunkArgs {
     float* CT;
     float* nT;
     float* mT;
+    // q, k, v element strides (batch, head, token) x 3, rows of D contiguous; NULL: contiguous
+    // [B, NH, T, D] (the bf16 MFMA path reads them; the other kernels take contiguous rows only)
+    const int64_t* strides = nullptr;
 };
 
 // Returns the dv tile the fp32 kernel would use, or 0 if no tile fits its LDS budget.

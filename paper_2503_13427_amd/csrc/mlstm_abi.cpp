@@ -81,8 +81,9 @@ size_t mlstm_chunkwise_workspace_bytes(int B, int NH, int T, int DQK, int DV, in
 }
 
 // Validation and launch shared by mlstm_chunkwise_fwd (caller workspace) and
-// mlstm_chunkwise_fwd_noalloc (the library's fixed device scratch, use_scratch).
-static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void* v, int dtc,
+// mlstm_chunkwise_fwd_noalloc (the library's fixed device scratch, use_scratch) and
+// mlstm_chunkwise_fwd_strided (strides: q, k, v element strides, else NULL for contiguous rows).
+static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void* v, const int64_t* strides, int dtc,
                                        const float* ipre, const float* fpre, const float* C0, const float* n0,
                                        const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
                                        float* CT, float* nT, float* mT, void* workspace, size_t workspace_bytes,
@@ -107,7 +108,31 @@ static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void*
         if (misaligned(p)) return MLSTM_ERR_MISALIGNED;
 
     const size_t eb = elem_bytes(dt);
-    const Range in[] = {range_of(q, nq * eb), range_of(k, nq * eb), range_of(v, nv * eb),
+    // strided q, k, v: the element range each view spans (rows of D contiguous, every row 16-byte aligned)
+    int64_t eq = nq, ek = nq, ev = nv;
+    if (strides) {
+        for (int i = 0; i < 9; ++i) {
+            if (strides[i] < 0) return MLSTM_ERR_BAD_SHAPE;
+            if (strides[i] % 8) return MLSTM_ERR_MISALIGNED;
+        }
+        if (strides[2] < DQK || strides[5] < DQK || strides[8] < DV) return MLSTM_ERR_BAD_SHAPE;   // rows overlap
+        int64_t* ext[3] = {&eq, &ek, &ev};
+        const int D[3] = {DQK, DQK, DV};
+        for (int j = 0; j < 3; ++j) {
+            const int64_t* x = strides + 3 * j;
+            if (ST == 0) {
+                *ext[j] = 0;
+                continue;
+            }
+            if (x[0] > INT64_MAX / 4 / B || x[1] > INT64_MAX / 4 / NH || x[2] > INT64_MAX / 4 / T)
+                return MLSTM_ERR_BAD_SHAPE;
+            *ext[j] = (B - 1) * x[0] + (NH - 1) * x[1] + (static_cast<int64_t>(T) - 1) * x[2] + D[j];
+            // one sequence's rows are addressed through a 32-bit buffer offset, including the up to 127
+            // rows past its end that a partial last chunk reads (as zeros, outside the buffer range)
+            if (((static_cast<int64_t>(T) + 127) * x[2] + D[j]) * 2 >= (int64_t(1) << 31)) return MLSTM_ERR_UNSUPPORTED;
+        }
+    }
+    const Range in[] = {range_of(q, eq * eb), range_of(k, ek * eb), range_of(v, ev * eb),
                         range_of(ipre, ST * 4), range_of(fpre, ST * 4), range_of(C0, C0 ? nC * 4 : 0),
                         range_of(n0, n0 ? nn * 4 : 0), range_of(m0, m0 ? S * 4 : 0)};
     const Range out[] = {range_of(h, nv * eb), range_of(CT, nC * 4), range_of(nT, nn * 4), range_of(mT, S * 4),
@@ -121,7 +146,7 @@ static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void*
             if (overlap(out[a], out[b])) return MLSTM_ERR_ALIAS;
 
     const bool mfma = mlstm::chunk_mfma_supported(dt, DQK, DV, L);
-    if (!mfma && mlstm::chunk_f32_tile(DQK, DV, L) == 0) return MLSTM_ERR_UNSUPPORTED;
+    if (!mfma && (strides || mlstm::chunk_f32_tile(DQK, DV, L) == 0)) return MLSTM_ERR_UNSUPPORTED;
     // the MFMA kernel addresses one sequence's v through a 32-bit buffer range
     if (mfma && static_cast<int64_t>(T) * DV * 2 >= (int64_t(1) << 31)) return MLSTM_ERR_UNSUPPORTED;
 
@@ -130,7 +155,7 @@ static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void*
     if (workspace_bytes > 0 && workspace_bytes < ws_need) return MLSTM_ERR_WORKSPACE;
     if (use_scratch && ws_need > mlstm::kChunkScratchBytes) return MLSTM_ERR_WORKSPACE;
 
-    mlstm::ChunkArgs a{q, k, v, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT};
+    mlstm::ChunkArgs a{q, k, v, ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, strides};
     hipStream_t stream = static_cast<hipStream_t>(hip_stream);
     if (use_scratch && ws_need > 0) {
         hipError_t e = mlstm::chunk_scratch(&workspace);
@@ -148,8 +173,18 @@ mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, ml
                                  const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
                                  float* CT, float* nT, float* mT, void* workspace, size_t workspace_bytes,
                                  void* hip_stream) {
-    return chunkwise_fwd_impl(q, k, v, dtype_code(&dt), ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, workspace,
-                              workspace_bytes, false, hip_stream);
+    return chunkwise_fwd_impl(q, k, v, nullptr, dtype_code(&dt), ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT,
+                              nT, mT, workspace, workspace_bytes, false, hip_stream);
+}
+
+mlstm_status mlstm_chunkwise_fwd_strided(const void* q, const void* k, const void* v, const int64_t* qkv_strides,
+                                         mlstm_dtype dt, const float* ipre, const float* fpre, const float* C0,
+                                         const float* n0, const float* m0, int B, int NH, int T, int DQK, int DV,
+                                         int L, void* h, float* CT, float* nT, float* mT, void* workspace,
+                                         size_t workspace_bytes, void* hip_stream) {
+    if (!qkv_strides) return MLSTM_ERR_NULL_PTR;
+    return chunkwise_fwd_impl(q, k, v, qkv_strides, dtype_code(&dt), ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h,
+                              CT, nT, mT, workspace, workspace_bytes, false, hip_stream);
 }
 
 size_t mlstm_chunkwise_scratch_bytes(void) { return mlstm::kChunkScratchBytes; }
@@ -158,8 +193,8 @@ mlstm_status mlstm_chunkwise_fwd_noalloc(const void* q, const void* k, const voi
                                          const float* ipre, const float* fpre, const float* C0, const float* n0,
                                          const float* m0, int B, int NH, int T, int DQK, int DV, int L, void* h,
                                          float* CT, float* nT, float* mT, void* hip_stream) {
-    return chunkwise_fwd_impl(q, k, v, dtype_code(&dt), ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT, nT, mT, nullptr, 0,
-                              true, hip_stream);
+    return chunkwise_fwd_impl(q, k, v, nullptr, dtype_code(&dt), ipre, fpre, C0, n0, m0, B, NH, T, DQK, DV, L, h, CT,
+                              nT, mT, nullptr, 0, true, hip_stream);
 }
 
 // Validation shared by mlstm_step and mlstm_step_output (extra: the o~, weight and bias ranges

@@ -170,20 +170,21 @@ struct VRegs {
 // With K^T staging (L = 128) K is loaded in pieces in the MFMA A-operand layout: piece i of wave w
 // (pc = w + 8 i, a = pc % (L / 16), b = pc / (L / 16)) has lane (l16, g16) holding
 // K[tau 16 a + l16][d 32 b + 8 g16 + 0..7] of the d block.
-// The chunk's row offset t0 rides in the per-lane offset, which the buffer range check covers (the
-// scalar offset is outside it), so rows past the end of a sequence read as zero in a partial last
-// chunk; the scalar offset carries only the column base.
+// The chunk's row offset t0 rides in the per-lane offset with the row, so rows past the end of a
+// sequence fall outside the buffer range and read as zero in a partial last chunk; the scalar offset
+// carries only the column base.  Row strides (bytes) come from the call: q, k and v may be strided
+// views of one projection output.
 template <int L>
-__device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, int p, int tid) {
+__device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, int p, int tid, uint32_t rq,
+                                        uint32_t rk) {
     constexpr int DB = Cfg<L>::DB, PR = DB / 8;   // 16-byte pieces per row
     const uint32_t soff = p * (DB * 2);
-    const uint32_t roff = static_cast<uint32_t>(t0) * (kDQK * 2);
 #pragma unroll
     for (int i = 0; i < QKRegs<L>::N; ++i) {
         const int item = tid + i * kThreads;
-        const uint32_t voff = roff + (item / PR) * (kDQK * 2) + 16 * (item % PR);
-        r.q[i] = bload128(R.q, voff, soff);
-        if constexpr (!Cfg<L>::KT) r.k[i] = bload128(R.k, voff, soff);
+        const uint32_t row = static_cast<uint32_t>(t0 + item / PR), col = 16 * (item % PR);
+        r.q[i] = bload128(R.q, row * rq + col, soff);
+        if constexpr (!Cfg<L>::KT) r.k[i] = bload128(R.k, row * rk + col, soff);
     }
     if constexpr (Cfg<L>::KT) {
         static_assert(QKRegs<L>::N * kWaves == (L / 16) * (DB / 32), "pieces of one K block");
@@ -193,7 +194,8 @@ __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, 
 #pragma unroll
         for (int i = 0; i < QKRegs<L>::N; ++i) {
             const int pc = wave + kWaves * i, a = pc % (L / 16), b = pc / (L / 16);
-            r.k[i] = bload128(R.k, roff + (16 * a + (ln & 15)) * (kDQK * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
+            r.k[i] = bload128(R.k, static_cast<uint32_t>(t0 + 16 * a + (ln & 15)) * rk + (32 * b + 8 * (ln >> 4)) * 2,
+                              soff);
         }
     }
 }
@@ -245,17 +247,17 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
 // of wave w holds V[tau 16 a + l16][v 32 b + 8 g16 + 0..7] with pc = w + 8 (part N + i) and
 // (a, b) = (pc % (L / 16), pc / (L / 16)), so the workgroup's pieces cover the L x 128 chunk once.
 template <int L>
-__device__ __forceinline__ void load_v_tr(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane, int part) {
+__device__ __forceinline__ void load_v_tr(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane, int part,
+                                          uint32_t rv) {
     static_assert(VRegs<L>::PARTS * VRegs<L>::N * kWaves == (L / 16) * (kDVT / 32), "pieces of one L x 128 chunk");
     constexpr int NA = L / 16;
-    const uint32_t soff = v0 * 2;   // the row offset goes in the range-checked per-lane offset
-    const uint32_t roff = static_cast<uint32_t>(t0) * (kDV * 2);
+    const uint32_t soff = v0 * 2;   // the row offset goes in the per-lane offset
     int ln = lane;   // opaque: the offsets are recomputed per call rather than held across the loop
     asm volatile("" : "+v"(ln));
 #pragma unroll
     for (int i = 0; i < VRegs<L>::N; ++i) {
         const int pc = wave + kWaves * (part * VRegs<L>::N + i), a = pc % NA, b = pc / NA;
-        r.v[i] = bload128(R.v, roff + (16 * a + (ln & 15)) * (kDV * 2) + (32 * b + 8 * (ln >> 4)) * 2, soff);
+        r.v[i] = bload128(R.v, static_cast<uint32_t>(t0 + 16 * a + (ln & 15)) * rv + (32 * b + 8 * (ln >> 4)) * 2, soff);
     }
 }
 template <int L>
@@ -441,7 +443,18 @@ struct ChunkKernelArgs {
     float* CT;
     float* nT;
     float* mT;
+    int NH;
+    int64_t sq[2], sk[2], sv[2];   // (batch, head) element strides of q, k, v
+    uint32_t rq, rk, rv;           // their row (token) strides in bytes
 };
+
+// first row of sequence s = (batch s / NH, head s % NH) and the byte span of its T rows of D elements
+__device__ __forceinline__ const uint16_t* seq_rows(const uint16_t* p, int s, int NH, const int64_t (&st)[2]) {
+    return p + static_cast<int64_t>(s / NH) * st[0] + static_cast<int64_t>(s % NH) * st[1];
+}
+__device__ __forceinline__ uint32_t seq_span(int T, uint32_t row_bytes, int D) {
+    return T > 0 ? static_cast<uint32_t>(T - 1) * row_bytes + static_cast<uint32_t>(D) * 2u : 0u;
+}
 
 // row pitch (floats) of the entry-state staging of a 256 x 128 tile in LDS: 528 bytes puts the
 // rows 8 apart that one read of the accumulator pickup touches in different banks
@@ -502,9 +515,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     const int c_end = min(nc_total, c_begin + A.seg_chunks);
 
     SeqRsrc P;
-    P.q = make_rsrc(A.q + static_cast<int64_t>(s) * A.T * kDQK, static_cast<uint32_t>(A.T) * kDQK * 2);
-    P.k = make_rsrc(A.k + static_cast<int64_t>(s) * A.T * kDQK, static_cast<uint32_t>(A.T) * kDQK * 2);
-    P.v = make_rsrc(A.v + static_cast<int64_t>(s) * A.T * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
+    P.q = make_rsrc(seq_rows(A.q, s, A.NH, A.sq), seq_span(A.T, A.rq, kDQK));
+    P.k = make_rsrc(seq_rows(A.k, s, A.NH, A.sk), seq_span(A.T, A.rk, kDQK));
+    P.v = make_rsrc(seq_rows(A.v, s, A.NH, A.sv), seq_span(A.T, A.rv, kDV));
     P.ig = make_rsrc(A.ipre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
     P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
     P.h = make_rsrc(A.h + static_cast<int64_t>(s) * A.T * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
@@ -581,7 +594,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     VtPacked<L> pv;   // the next chunk's V^T, packed, until its stores
     if (c_begin < c_end) {
         const int t0 = c_begin * L;
-        load_qk<L>(rqk, P, t0, 0, tid);
+        load_qk<L>(rqk, P, t0, 0, tid, A.rq, A.rk);
         if (gate_wave) {
             load_gates<L>(gi, gf, P, t0, lane);
             gate_phase<L>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane, A.T - t0);
@@ -589,13 +602,13 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         store_qk<L>(S.QK[0], S.QK[0] + CF::QKE, rqk, tid);
 #pragma unroll
         for (int part = 0; part < VRegs<L>::PARTS; ++part) {
-            load_v_tr<L>(rv, P, t0, v0, wave, lane, part);
+            load_v_tr<L>(rv, P, t0, v0, wave, lane, part, A.rv);
             vt_transpose<L>(pv, rv, lane, part);
         }
         __syncthreads();   // the first chunk's gates are visible
         vt_store_scaled<L>(S.Vs[1], pv, S.G[c_begin & 1].wC, wave, lane);
         vt_store_plain<L>(S.Vs[0], pv, wave, lane);
-        load_qk<L>(rqk, P, t0, 1, tid);
+        load_qk<L>(rqk, P, t0, 1, tid, A.rq, A.rk);
     }
     if (slot_entry && L == 64) {
         // a segment entry slot (four rows interleaved): each accumulator tile is one 16-byte load
@@ -632,13 +645,13 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         __syncthreads();   // the previous chunk is done; block 0, V and the gates of this chunk are visible
         // block 1 -> set 1 (its readers in the previous chunk, the last d block and S~, are done)
         store_qk<L>(S.QK[1], S.QK[1] + CF::QKE, rqk, tid);
-        if constexpr (NDB > 2) load_qk<L>(rqk, P, t0, 2, tid);
-        else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid);
+        if constexpr (NDB > 2) load_qk<L>(rqk, P, t0, 2, tid, A.rq, A.rk);
+        else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid, A.rq, A.rk);
         if (gate_wave && c + 1 < c_end) load_gates<L>(gi, gf, P, t0 + L, lane);
         // this chunk's plain V^T (its readers in the previous chunk are done); the next chunk's V,
         // part 0 now, part k at the barrier that opens d block k + 1
         if (c > c_begin) vt_store_plain<L>(S.Vs[0], pv, wave, lane);
-        if (c + 1 < c_end) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane, 0);
+        if (c + 1 < c_end) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane, 0, A.rv);
         const float decay_n = Gc.scal[0];
         const float m_next = Gc.scal[1];
         const float s_new = Gc.scal[2];
@@ -664,17 +677,17 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 __syncthreads();   // block p visible, block p - 1 fully read
                 if (p + 1 < NDB) {
                     store_qk<L>(S.QK[(p + 1) & 1], S.QK[(p + 1) & 1] + CF::QKE, rqk, tid);
-                    if (p + 2 < NDB) load_qk<L>(rqk, P, t0, p + 2, tid);
-                    else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid);
+                    if (p + 2 < NDB) load_qk<L>(rqk, P, t0, p + 2, tid, A.rq, A.rk);
+                    else if (c + 1 < c_end) load_qk<L>(rqk, P, t0 + L, 0, tid, A.rq, A.rk);
                 } else if (c + 1 < c_end) {
                     // block 0 of the next chunk
                     store_qk<L>(S.QK[0], S.QK[0] + CF::QKE, rqk, tid);
-                    load_qk<L>(rqk, P, t0 + L, 1, tid);
+                    load_qk<L>(rqk, P, t0 + L, 1, tid, A.rq, A.rk);
                 }
                 // the next chunk's V, part p - 1, transposed in registers; part p requested
                 if (p <= VRegs<L>::PARTS && c + 1 < c_end) {
                     vt_transpose<L>(pv, rv, lane, p - 1);
-                    if (p < VRegs<L>::PARTS) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane, p);
+                    if (p < VRegs<L>::PARTS) load_v_tr<L>(rv, P, t0 + L, v0, wave, lane, p, A.rv);
                 }
             }
             // (i) S^T += K_p Q_p^T on this wave's causal tiles.  K^T staging (L = 128): the A operand
@@ -999,17 +1012,18 @@ struct LocRegs {
     uint32_t k[2][8];
     uint32_t v[8];
 };
-__device__ __forceinline__ void loc_load(LocRegs& r, const SeqRsrc& R, int t, int v0, int tid) {
+__device__ __forceinline__ void loc_load(LocRegs& r, const SeqRsrc& R, int t, int v0, int tid, uint32_t rk,
+                                         uint32_t rv) {
 #pragma unroll
     for (int it = 0; it < 2; ++it) {
         const int item = tid + it * kThreads;
-        const uint32_t vo = (8 * (item / (kDQK / 2))) * (kDQK * 2) + 4 * (item % (kDQK / 2));
+        const uint32_t vo = (8 * (item / (kDQK / 2))) * rk + 4 * (item % (kDQK / 2));
 #pragma unroll
-        for (int j = 0; j < 8; ++j) r.k[it][j] = bload32(R.k, vo, static_cast<uint32_t>(t + j) * (kDQK * 2));
+        for (int j = 0; j < 8; ++j) r.k[it][j] = bload32(R.k, vo, static_cast<uint32_t>(t + j) * rk);
     }
-    const uint32_t vo = (8 * (tid / (kDVT / 2))) * (kDV * 2) + 4 * (tid % (kDVT / 2));
+    const uint32_t vo = (8 * (tid / (kDVT / 2))) * rv + 4 * (tid % (kDVT / 2));
 #pragma unroll
-    for (int j = 0; j < 8; ++j) r.v[j] = bload32(R.v, vo, static_cast<uint32_t>(t + j) * (kDV * 2) + v0 * 2);
+    for (int j = 0; j < 8; ++j) r.v[j] = bload32(R.v, vo, static_cast<uint32_t>(t + j) * rv + v0 * 2);
 }
 __device__ __forceinline__ void loc_store(uint16_t* Kt, uint16_t* Vt, const LocRegs& r, int tid) {
     u32x4_t c0, c1;
@@ -1030,6 +1044,9 @@ __device__ __forceinline__ void loc_store(uint16_t* Kt, uint16_t* Vt, const LocR
 struct LocalArgs {
     const uint16_t* k;
     const uint16_t* v;
+    int NH;
+    int64_t sk[2], sv[2];   // (batch, head) element strides of k and v
+    uint32_t rk, rv;        // their row strides in bytes
     const float* ipre;
     const float* fpre;
     float* ws;
@@ -1068,13 +1085,13 @@ local_state_kernel(LocalArgs A) {
     const int ntok = (tile_e - tile_b) * kLocTile;
 
     SeqRsrc P;
-    P.k = make_rsrc(A.k + static_cast<int64_t>(s) * A.T * kDQK, static_cast<uint32_t>(A.T) * kDQK * 2);
-    P.v = make_rsrc(A.v + static_cast<int64_t>(s) * A.T * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
+    P.k = make_rsrc(seq_rows(A.k, s, A.NH, A.sk), seq_span(A.T, A.rk, kDQK));
+    P.v = make_rsrc(seq_rows(A.v, s, A.NH, A.sv), seq_span(A.T, A.rv, kDV));
     P.ig = make_rsrc(A.ipre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
     P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
 
     LocRegs rg;
-    if (ntok > 0) loc_load(rg, P, tb, v0, tid);   // first tile, in flight during the gate pass
+    if (ntok > 0) loc_load(rg, P, tb, v0, tid, A.rk, A.rv);   // first tile, in flight during the gate pass
 
     // gates: block-wide prefix sums of logsig(f~) in rounds of 512 tokens (restart tokens add
     // nothing), x_t into LDS, the last restart R, then X over the tokens from R on
@@ -1140,13 +1157,13 @@ local_state_kernel(LocalArgs A) {
     const int nt = ntok / kLocTile;
     if (nt > 0) {
         loc_store(S.Kt[0], S.Vt[0], rg, tid);
-        if (nt > 1) loc_load(rg, P, tb + kLocTile, v0, tid);
+        if (nt > 1) loc_load(rg, P, tb + kLocTile, v0, tid, A.rk, A.rv);
     }
     for (int i = 0; i < nt; ++i) {
         __syncthreads();   // tile i and the weights are visible; the other buffer's readers are done
         if (i + 1 < nt) {
             loc_store(S.Kt[(i + 1) & 1], S.Vt[(i + 1) & 1], rg, tid);
-            if (i + 2 < nt) loc_load(rg, P, tb + (i + 2) * kLocTile, v0, tid);
+            if (i + 2 < nt) loc_load(rg, P, tb + (i + 2) * kLocTile, v0, tid, A.rk, A.rv);
         }
         const uint16_t* Kt = S.Kt[i & 1];
         const uint16_t* Vt = S.Vt[i & 1];
@@ -1283,6 +1300,28 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
     }
 }
 
+// q, k, v strides of a call: the caller's (elements; batch, head, token for each), or contiguous
+// [B, NH, T, D] rows
+void set_strides(const ChunkArgs& a, int& NH, int64_t* sq, int64_t* sk, int64_t* sv, uint32_t* rq, uint32_t* rk,
+                 uint32_t* rv) {
+    NH = a.NH;
+    const int64_t T = a.T;
+    const int64_t st[9] = {a.NH * T * kDQK, T * kDQK, kDQK, a.NH * T * kDQK, T * kDQK, kDQK,
+                           a.NH * T * kDV, T * kDV, kDV};
+    const int64_t* x = a.strides ? a.strides : st;
+    if (sq) {
+        sq[0] = x[0];
+        sq[1] = x[1];
+    }
+    sk[0] = x[3];
+    sk[1] = x[4];
+    sv[0] = x[6];
+    sv[1] = x[7];
+    if (rq) *rq = static_cast<uint32_t>(x[2] * 2);
+    *rk = static_cast<uint32_t>(x[5] * 2);
+    *rv = static_cast<uint32_t>(x[8] * 2);
+}
+
 template <int L>
 hipError_t launch_variant(const ChunkKernelArgs& a, int S, hipStream_t stream) {
     const size_t lds = sizeof(Smem<L>);
@@ -1350,6 +1389,7 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
     k.q = static_cast<const uint16_t*>(a.q);
     k.k = static_cast<const uint16_t*>(a.k);
     k.v = static_cast<const uint16_t*>(a.v);
+    set_strides(a, k.NH, k.sq, k.sk, k.sv, &k.rq, &k.rk, &k.rv);
     k.ipre = a.ipre;
     k.fpre = a.fpre;
     k.C0 = a.C0;
@@ -1371,6 +1411,7 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
         LocalArgs la{};
         la.k = k.k;
         la.v = k.v;
+        set_strides(a, la.NH, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
         la.ipre = a.ipre;
         la.fpre = a.fpre;
         la.ws = k.ws;
@@ -1401,6 +1442,7 @@ hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, uint16_t* rowhl
     LocalArgs la{};
     la.k = static_cast<const uint16_t*>(a.k);
     la.v = static_cast<const uint16_t*>(a.v);
+    set_strides(a, la.NH, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
     la.ipre = a.ipre;
     la.fpre = a.fpre;
     la.ws = slots;

@@ -7,14 +7,13 @@ x [B, T, d] -> y [B, T, d], d = NH * DV:
 2. ``mlstm_gate_preact``: the two gate pre-activations per head (bf16 products, fp32), their
    biases, the soft-cap a * tanh(x / a) of Eq. 13 (a = 15) and the document borders of a packed
    sequence (f~ = -inf, App. B), written head-major;
-3. head-major copies of q, k and v, since the cell takes [B, NH, T, D] rows (a decode step,
-   with T = 1, takes o~ contiguous as well);
-4. the cell: ``mlstm_chunkwise_fwd`` for a prefill, ``mlstm_step_output`` for one decode step
-   (the step with the output norm of step 5 in its epilogue);
-5. the output norm h = sigmoid(o~) * LayerNorm(h~) * weight, per head: for a prefill
+3. the cell: ``mlstm_chunkwise_fwd_strided`` for a prefill, which reads q, k and v as per-head
+   views of the projection output (no head-major copies), ``mlstm_step_output`` for one decode
+   step (the step with the output norm of step 4 in its epilogue; q, k, v, o~ contiguous);
+4. the output norm h = sigmoid(o~) * LayerNorm(h~) * weight, per head: for a prefill
    ``mlstm_output_norm_tokens`` reads o~ in place in the projection output and writes h
    token-major [B, T, NH, DV], which is already the concatenation of the heads;
-6. the output projection (bf16 GEMM).
+5. the output projection (bf16 GEMM).
 
 The q, k, v, o~ and output projections are plain library GEMMs around the cell; the gates, the
 cell and the output norm run in libmlstm.  The layer's pre-norm (Norm(x) in the block, Eq. 12) belongs to
@@ -107,8 +106,9 @@ class MLSTMLayer:
         B, T, d = x.shape
         NH, DQK, DV = w.NH, w.DQK, w.DV
         q, k, v, o = self._project(x.reshape(B * T, d))
-        hm = lambda a, D: a.view(B, T, NH, D).transpose(1, 2).contiguous()   # head-major [B, NH, T, D]
-        q, k, v = hm(q, DQK), hm(k, DQK), hm(v, DV)
+        # head-major views of the projection output, no copy: the cell takes strided q, k, v rows
+        hv = lambda a, D: a.view(B, T, NH, D).transpose(1, 2)
+        q, k, v = hv(q, DQK), hv(k, DQK), hv(v, DV)
         ig, fg = self.gates(x, border)
         h = torch.empty(B, NH, T, DV, dtype=torch.bfloat16, device=x.device)
         C = torch.empty(B, NH, DQK, DV, device=x.device)
@@ -118,7 +118,7 @@ class MLSTMLayer:
         if workspace is None:   # the segment schedule needs one; without it the call runs one block per sequence
             nb = mb.mlstm_chunkwise_workspace_bytes(B, NH, T, DQK, DV, self.L)
             workspace = torch.empty(nb, dtype=torch.uint8, device=x.device) if nb else None
-        mb.mlstm_chunkwise_fwd(q, k, v, ig, fg, C0, n0, m0, self.L, h, C, n, m, workspace=workspace)
+        mb.mlstm_chunkwise_fwd_strided(q, k, v, ig, fg, C0, n0, m0, self.L, h, C, n, m, workspace=workspace)
         # o~ stays in the projection output and the result comes out token-major for W_proj
         yh = torch.empty(B, T, NH, DV, dtype=torch.bfloat16, device=x.device)
         mb.mlstm_output_norm_tokens(h, o.view(B, T, NH, DV), w.norm_weight, None, self.eps, "layer", yh)

@@ -27,6 +27,7 @@ def declared_functions():
 def test_header_declares_expected_entry_points():
     assert declared_functions() == sorted(["mlstm_chunkwise_fwd", "mlstm_chunkwise_workspace_bytes", "mlstm_step",
                                            "mlstm_chunkwise_fwd_noalloc", "mlstm_chunkwise_scratch_bytes",
+                                           "mlstm_chunkwise_fwd_strided",
                                            "mlstm_step_output", "mlstm_chunkwise_bwd",
                                            "mlstm_chunkwise_bwd_workspace_bytes",
                                            "mlstm_output_norm", "mlstm_output_norm_tokens", "mlstm_gate_preact", "mlstm_parallel_bwd",
@@ -416,6 +417,62 @@ def test_noalloc_validates_like_the_workspace_entry_point(field):
     assert call_chunk_noalloc(a) == 4
     assert call_chunk_noalloc(chunk_args(B=0)) == 2
     assert call_chunk_noalloc(chunk_args(h=fake(1, 64))) == 5
+
+
+# ---- strided q, k, v ------------------------------------------------------------------------------
+
+def proj_strides(B=1, NH=8, T=256, DQK=256, DV=512):
+    """q, k, v as per-head views of one projection output [B, T, NH * (2 DQK + DV)] (element strides)."""
+    row = NH * (2 * DQK + DV)
+    return [T * row, DQK, row, T * row, DQK, row, T * row, DV, row]
+
+
+def call_strided(a, st):
+    arr = None if st is None else (ctypes.c_int64 * 9)(*st)
+    return lib.mlstm_chunkwise_fwd_strided(a["q"], a["k"], a["v"], arr, a["dt"], a["ipre"], a["fpre"], a["C0"],
+                                           a["n0"], a["m0"], a["B"], a["NH"], a["T"], a["DQK"], a["DV"], a["L"],
+                                           a["h"], a["CT"], a["nT"], a["mT"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+def test_strided_null_strides_and_pointers():
+    assert call_strided(chunk_args(), None) == 1
+    assert call_strided(chunk_args(k=None), proj_strides()) == 1
+
+
+@pytest.mark.parametrize("i,val,status", [(2, 4100, 4), (0, 8 * 3 + 4, 4), (4, -256, 2), (5, 248, 2), (8, 504, 2),
+                                          (2, 1 << 24, 3)])
+def test_strided_stride_checks(i, val, status):
+    """A stride that is not a multiple of 8 elements is misaligned; a negative one, or a token stride
+    under D (rows that overlap), is a bad shape; a sequence whose rows (plus the rows a partial last
+    chunk reads past its end) span 2^31 bytes or more is unsupported."""
+    st = proj_strides()
+    st[i] = val
+    assert call_strided(chunk_args(), st) == status
+
+
+def test_strided_span_bound_counts_the_padding_rows():
+    # T = 1 with a token stride of 2^23 elements: the row itself fits, the 127 padding rows do not
+    st = proj_strides(T=1)
+    st[2] = 1 << 23
+    assert call_strided(chunk_args(T=1), st) == 3
+    st[2] = (1 << 23) - 8
+    a = chunk_args(T=1)
+    a["h"] = a["CT"]                   # within the bound: validation goes on to the alias checks
+    assert call_strided(a, st) == 5
+
+
+@pytest.mark.parametrize("over", [dict(dt=Bd.MLSTM_F32), dict(DQK=128, DV=128, L=64), dict(L=32)])
+def test_strided_unsupported_shapes(over):
+    st = proj_strides(DQK=over.get("DQK", 256), DV=over.get("DV", 512))
+    assert call_strided(chunk_args(**over), st) == 3
+
+
+def test_strided_alias_covers_the_view_extent():
+    """h placed past q's contiguous size but inside the range its strided view spans is an alias."""
+    a = chunk_args()
+    nq = 1 * 8 * 256 * 256
+    a["h"] = a["q"] + 2 * nq * 2      # 2 nq elements in: beyond [B, NH, T, DQK], inside the strided view
+    assert call_strided(a, proj_strides()) == 5
 
 
 # ---- the decode step with the output epilogue ----------------------------------------------------

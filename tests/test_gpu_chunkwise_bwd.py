@@ -145,3 +145,29 @@ def test_chunk_bwd_prefill_shapes_sampled_heads(T):
         sl = slice(hd, hd + 1)
         ref = G.parallel_grad(q[sl], k[sl], v[sl], ip[sl], fp[sl], dh[sl])
         compare([g[sl] for g in got], ref, f"T{T} head {hd}", q=q[sl], k=k[sl], fp=fp[sl])
+
+
+@pytest.mark.parametrize("fwd_L", [64, 128])
+def test_autograd_cell_with_state_and_borders(fwd_L):
+    """Gradients through ``mlstm_cell`` (chunkwise forward from a given state, chunkwise backward) for
+    the loss sum(h * w), with document borders, against the fp64 oracle with dh = w (bf16)."""
+    from paper_2503_13427_amd.cell import mlstm_cell
+    S, T = 2, 170
+    q, k, v, ip, fp, w, st = draw(640 + fwd_L, S, T, state=True, borders=(30, 64, 129))
+    dev = lambda x, *shape: torch.from_numpy(np.ascontiguousarray(x)).reshape(*shape).cuda()
+    leaf = lambda x, dt, *shape: dev(x, *shape).to(dt).requires_grad_(True)
+    tq, tk = leaf(q, torch.bfloat16, 1, S, T, DQK), leaf(k, torch.bfloat16, 1, S, T, DQK)
+    tv = leaf(v, torch.bfloat16, 1, S, T, DV)
+    tip, tfp = leaf(ip, torch.float32, 1, S, T), leaf(fp, torch.float32, 1, S, T)
+    tC, tn, tm = (leaf(st[0], torch.float32, 1, S, DQK, DV), leaf(st[1], torch.float32, 1, S, DQK),
+                  leaf(st[2], torch.float32, 1, S))
+    h, (CT, nT, mT) = mlstm_cell(tq, tk, tv, tip, tfp, L=fwd_L, state=(tC, tn, tm), return_state=True)
+    assert h.dtype == torch.bfloat16 and not CT.requires_grad
+    (h * dev(w, 1, S, T, DV).bfloat16()).sum().backward()
+    torch.cuda.synchronize()
+    got = [t.grad.float().cpu().numpy().astype(np.float64).reshape(S, T, -1) for t in (tq, tk, tv, tip, tfp)]
+    got += [tC.grad.cpu().numpy().astype(np.float64).reshape(S, DQK, DV),
+            tn.grad.cpu().numpy().astype(np.float64).reshape(S, DQK), tm.grad.cpu().numpy().astype(np.float64)]
+    ref = G.recurrent_grad_state(q, k, v, ip, fp, *st, w)
+    # dq, dk, dv come back in bf16 (the dtype of q, k, v): one more rounding of 2^-9 within the bar
+    compare(got, ref, f"autograd cell L{fwd_L}", state=st, q=q, k=k, fp=fp)

@@ -128,9 +128,10 @@ def test_parallel_bwd_bf16_xlstm_head(T):
 
 @pytest.mark.parametrize("dtype,DQK,DV", [("f32", 64, 128), ("bf16", 256, 512)])
 def test_autograd_cell_gradients(dtype, DQK, DV):
-    """Gradients through ``mlstm_cell`` (forward on the chunkwise kernels, backward on the parallel-form
-    kernels) for a loss sum(h * w), against the fp64 gradient oracle with dh = w (for bf16 the forward
-    output h, and so dh = w, enter in bf16, and the gradients return in bf16: the bf16 bar)."""
+    """Gradients through ``mlstm_cell`` (forward on the chunkwise kernels; backward on the parallel-form
+    kernels for fp32 64 x 128 heads, on the chunkwise backward for the bf16 xLSTM-7B head) for a loss
+    sum(h * w), against the fp64 gradient oracle with dh = w (for bf16 the forward output h, and so
+    dh = w, enter in bf16, and the gradients return in bf16: the bf16 bar)."""
     from paper_2503_13427_amd.cell import mlstm_cell
     B, NH, T = 1, 2, 90
     q, k, v, ip, fp, w = draw(330, B, NH, T, DQK, DV, dtype)

@@ -118,7 +118,8 @@ mlstm_status mlstm_chunkwise_fwd(const void* q, const void* k, const void* v, ml
  * contiguous.  Every stride must be a multiple of 8 (16-byte rows;
  * MLSTM_ERR_MISALIGNED), non-negative, with token strides of at least D
  * (MLSTM_ERR_BAD_SHAPE), and one sequence's rows plus 127 more token
- * strides must span under 2^31 bytes (MLSTM_ERR_UNSUPPORTED).  The other
+ * strides must span under 2^31 bytes and B NH^2 stay under 2^32
+ * (MLSTM_ERR_UNSUPPORTED).  The other
  * arguments, results and workspace (mlstm_chunkwise_workspace_bytes) are
  * those of mlstm_chunkwise_fwd; the alias checks cover the element ranges
  * the views span.  Built for the bf16

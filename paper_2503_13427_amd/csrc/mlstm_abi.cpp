@@ -116,6 +116,8 @@ static mlstm_status chunkwise_fwd_impl(const void* q, const void* k, const void*
             if (strides[i] % 8) return MLSTM_ERR_MISALIGNED;
         }
         if (strides[2] < DQK || strides[5] < DQK || strides[8] < DV) return MLSTM_ERR_BAD_SHAPE;   // rows overlap
+        // the kernels split a sequence index into (batch, head) by a 32-bit reciprocal multiply
+        if (static_cast<int64_t>(B) * NH * NH >= (int64_t(1) << 32)) return MLSTM_ERR_UNSUPPORTED;
         int64_t* ext[3] = {&eq, &ek, &ev};
         const int D[3] = {DQK, DQK, DV};
         for (int j = 0; j < 3; ++j) {

@@ -150,18 +150,19 @@ static_assert(Cfg<128>::ST_ALIAS && 128 * Cfg<128>::SP <= Cfg<128>::SETE, "S~ mu
 static_assert(sizeof(Smem<64>) <= 160 * 1024 && sizeof(Smem<128>) <= 160 * 1024, "LDS budget");
 
 // Per-thread staging registers: one Q/K d block and one chunk of V in flight.
-template <int L>
+// NT: the threads that stage (all of the workgroup, or its intra waves in the warp-specialised kernel)
+template <int L, int NT = kThreads>
 struct QKRegs {
-    static constexpr int N = (L * Cfg<L>::DB / 8) / kThreads;   // 16-byte pieces per thread per matrix
+    static constexpr int N = (L * Cfg<L>::DB / 8) / NT;   // 16-byte pieces per thread per matrix
     u32x4_t q[N];
     u32x4_t k[N];
 };
 // V is staged in VPARTS parts (two at L = 128, whose four d blocks leave time for it) so
 // that fewer registers hold it at once.
-template <int L>
+template <int L, int NT = kThreads>
 struct VRegs {
     static constexpr int PARTS = (Cfg<L>::NDB >= 3) ? 2 : 1;
-    static constexpr int N = (L * kDVT / 8) / kThreads / PARTS;   // pieces per thread per part
+    static constexpr int N = (L * kDVT / 8) / NT / PARTS;   // pieces per thread per part
     u32x4_t v[N];
 };
 
@@ -174,26 +175,27 @@ struct VRegs {
 // sequence fall outside the buffer range and read as zero in a partial last chunk; the scalar offset
 // carries only the column base.  Row strides (bytes) come from the call: q, k and v may be strided
 // views of one projection output.
-template <int L>
-__device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, int p, int tid, uint32_t rq,
+template <int L, int NT = kThreads>
+__device__ __forceinline__ void load_qk(QKRegs<L, NT>& r, const SeqRsrc& R, int t0, int p, int tid, uint32_t rq,
                                         uint32_t rk) {
+    constexpr int NW = NT / 64;
     constexpr int DB = Cfg<L>::DB, PR = DB / 8;   // 16-byte pieces per row
     const uint32_t soff = p * (DB * 2);
 #pragma unroll
-    for (int i = 0; i < QKRegs<L>::N; ++i) {
-        const int item = tid + i * kThreads;
+    for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
+        const int item = tid + i * NT;
         const uint32_t row = static_cast<uint32_t>(t0 + item / PR), col = 16 * (item % PR);
         r.q[i] = bload128(R.q, row * rq + col, soff);
         if constexpr (!Cfg<L>::KT) r.k[i] = bload128(R.k, row * rk + col, soff);
     }
     if constexpr (Cfg<L>::KT) {
-        static_assert(QKRegs<L>::N * kWaves == (L / 16) * (DB / 32), "pieces of one K block");
+        static_assert(QKRegs<L, NT>::N * NW == (L / 16) * (DB / 32), "pieces of one K block");
         int ln = tid & 63;   // opaque: recomputed per call rather than held across the loop
         asm volatile("" : "+v"(ln));
         const int wave = tid >> 6;
 #pragma unroll
-        for (int i = 0; i < QKRegs<L>::N; ++i) {
-            const int pc = wave + kWaves * i, a = pc % (L / 16), b = pc / (L / 16);
+        for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
+            const int pc = wave + NW * i, a = pc % (L / 16), b = pc / (L / 16);
             r.k[i] = bload128(R.k, static_cast<uint32_t>(t0 + 16 * a + (ln & 15)) * rk + (32 * b + 8 * (ln >> 4)) * 2,
                               soff);
         }
@@ -213,12 +215,12 @@ __device__ __forceinline__ void onehot_pair(u32x4_t (&E)[2], int lane) {
         for (int d = 0; d < 4; ++d) E[h][d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
     }
 }
-template <int L>
-__device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKRegs<L>& r, int tid) {
-    constexpr int PR = Cfg<L>::DB / 8, QP = Cfg<L>::QP;
+template <int L, int NT = kThreads>
+__device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKRegs<L, NT>& r, int tid) {
+    constexpr int PR = Cfg<L>::DB / 8, QP = Cfg<L>::QP, NW = NT / 64;
 #pragma unroll
-    for (int i = 0; i < QKRegs<L>::N; ++i) {
-        const int item = tid + i * kThreads;
+    for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
+        const int item = tid + i * NT;
         const int off = (item / PR) * QP + 8 * (item % PR);
         *reinterpret_cast<u32x4_t*>(&Qd[off]) = r.q[i];
         if constexpr (!Cfg<L>::KT) *reinterpret_cast<u32x4_t*>(&Kd[off]) = r.k[i];
@@ -232,8 +234,8 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
         onehot_pair(E, lane);
         const int l16 = lane & 15, g16 = lane >> 4;
 #pragma unroll
-        for (int i = 0; i < QKRegs<L>::N; ++i) {
-            const int pc = wave + kWaves * i, a = pc % (L / 16), b = pc / (L / 16);
+        for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
+            const int pc = wave + NW * i, a = pc % (L / 16), b = pc / (L / 16);
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const f32x4_t d = mfma16(r.k[i], E[h], f32x4_t{});
@@ -246,28 +248,29 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
 // V pieces in the MFMA A-operand layout for vt_transpose: for piece i of part `part`, lane (l16, g16)
 // of wave w holds V[tau 16 a + l16][v 32 b + 8 g16 + 0..7] with pc = w + 8 (part N + i) and
 // (a, b) = (pc % (L / 16), pc / (L / 16)), so the workgroup's pieces cover the L x 128 chunk once.
-template <int L>
-__device__ __forceinline__ void load_v_tr(VRegs<L>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane, int part,
+template <int L, int NT = kThreads>
+__device__ __forceinline__ void load_v_tr(VRegs<L, NT>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane, int part,
                                           uint32_t rv) {
-    static_assert(VRegs<L>::PARTS * VRegs<L>::N * kWaves == (L / 16) * (kDVT / 32), "pieces of one L x 128 chunk");
+    constexpr int NW = NT / 64;
+    static_assert(VRegs<L, NT>::PARTS * VRegs<L, NT>::N * NW == (L / 16) * (kDVT / 32), "pieces of one L x 128 chunk");
     constexpr int NA = L / 16;
     const uint32_t soff = v0 * 2;   // the row offset goes in the per-lane offset
     int ln = lane;   // opaque: the offsets are recomputed per call rather than held across the loop
     asm volatile("" : "+v"(ln));
 #pragma unroll
-    for (int i = 0; i < VRegs<L>::N; ++i) {
-        const int pc = wave + kWaves * (part * VRegs<L>::N + i), a = pc % NA, b = pc / NA;
+    for (int i = 0; i < VRegs<L, NT>::N; ++i) {
+        const int pc = wave + NW * (part * VRegs<L, NT>::N + i), a = pc % NA, b = pc / NA;
         r.v[i] = bload128(R.v, static_cast<uint32_t>(t0 + 16 * a + (ln & 15)) * rv + (32 * b + 8 * (ln >> 4)) * 2, soff);
     }
 }
-template <int L>
-using VtPacked = u32x2_t[2 * VRegs<L>::N * VRegs<L>::PARTS];
+template <int L, int NT = kThreads>
+using VtPacked = u32x2_t[2 * VRegs<L, NT>::N * VRegs<L, NT>::PARTS];
 // The transposition on the matrix cores: D = A E_h with A a piece (16 tau x 32 v) and E_h the 32 x 16
 // one-hot selection of its columns 16 h + 0..15 (exact in fp32).  Lane (n = l16, g16) of D holds
 // V[tau 16 a + 4 g16 + j][v 32 b + 16 h + n], j = 0..3: four consecutive tau of one row of V^T, kept
 // packed in pv until the stores below.
-template <int L>
-__device__ __forceinline__ void vt_transpose(VtPacked<L>& pv, const VRegs<L>& r, int lane, int part) {
+template <int L, int NT = kThreads>
+__device__ __forceinline__ void vt_transpose(VtPacked<L, NT>& pv, const VRegs<L, NT>& r, int lane, int part) {
     // E_h in the B-operand layout: lane (l16, g16) holds k slots 8 g16 + 0..7 of column l16, whose
     // one (if any) is slot 16 h + l16.  Built from an opaque copy of the lane index so that it is not
     // hoisted out of the chunk loop (eight more registers held across the loop would spill).
@@ -282,21 +285,22 @@ __device__ __forceinline__ void vt_transpose(VtPacked<L>& pv, const VRegs<L>& r,
         for (int d = 0; d < 4; ++d) E[h][d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
     }
 #pragma unroll
-    for (int i = 0; i < VRegs<L>::N; ++i)
+    for (int i = 0; i < VRegs<L, NT>::N; ++i)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const f32x4_t d = mfma16(r.v[i], E[h], f32x4_t{});
-            pv[2 * (part * VRegs<L>::N + i) + h] = u32x2_t{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
+            pv[2 * (part * VRegs<L, NT>::N + i) + h] = u32x2_t{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
         }
 }
 // (w V)^T from the packed V^T: row weights wC of the chunk, rounded to bf16 once
-template <int L>
-__device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const VtPacked<L>& pv, const float* wC, int wave, int lane) {
-    constexpr int TP = Cfg<L>::TP, NA = L / 16;
+template <int L, int NT = kThreads>
+__device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const VtPacked<L, NT>& pv, const float* wC, int wave,
+                                                int lane) {
+    constexpr int TP = Cfg<L>::TP, NA = L / 16, NW = NT / 64;
     const int l16 = lane & 15, g16 = lane >> 4;
 #pragma unroll
-    for (int i = 0; i < VRegs<L>::N * VRegs<L>::PARTS; ++i) {
-        const int pc = wave + kWaves * i, a = pc % NA, b = pc / NA;
+    for (int i = 0; i < VRegs<L, NT>::N * VRegs<L, NT>::PARTS; ++i) {
+        const int pc = wave + NW * i, a = pc % NA, b = pc / NA;
         const int tau = 16 * a + 4 * g16;
         const f32x4_t w = *reinterpret_cast<const f32x4_t*>(&wC[tau]);
 #pragma unroll
@@ -309,13 +313,13 @@ __device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const VtPacked<L>
         }
     }
 }
-template <int L>
-__device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const VtPacked<L>& pv, int wave, int lane) {
-    constexpr int TP = Cfg<L>::TP, NA = L / 16;
+template <int L, int NT = kThreads>
+__device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const VtPacked<L, NT>& pv, int wave, int lane) {
+    constexpr int TP = Cfg<L>::TP, NA = L / 16, NW = NT / 64;
     const int l16 = lane & 15, g16 = lane >> 4;
 #pragma unroll
-    for (int i = 0; i < VRegs<L>::N * VRegs<L>::PARTS; ++i) {
-        const int pc = wave + kWaves * i, a = pc % NA, b = pc / NA;
+    for (int i = 0; i < VRegs<L, NT>::N * VRegs<L, NT>::PARTS; ++i) {
+        const int pc = wave + NW * i, a = pc % NA, b = pc / NA;
 #pragma unroll
         for (int h = 0; h < 2; ++h)
             *reinterpret_cast<u32x2_t*>(&VtT[(32 * b + 16 * h + l16) * TP + 16 * a + 4 * g16]) = pv[2 * i + h];
@@ -443,14 +447,22 @@ struct ChunkKernelArgs {
     float* CT;
     float* nT;
     float* mT;
-    int NH;
-    int64_t sq[2], sk[2], sv[2];   // (batch, head) element strides of q, k, v
+    uint32_t nh_magic;             // floor(2^32 / NH) + 1, or 0 for NH = 1 (see seq_rows)
+    // element strides of q, k, v: [0] batch stride - NH head stride, [1] head stride (see seq_rows)
+    int64_t sq[2], sk[2], sv[2];
     uint32_t rq, rk, rv;           // their row (token) strides in bytes
 };
 
-// first row of sequence s = (batch s / NH, head s % NH) and the byte span of its T rows of D elements
-__device__ __forceinline__ const uint16_t* seq_rows(const uint16_t* p, int s, int NH, const int64_t (&st)[2]) {
-    return p + static_cast<int64_t>(s / NH) * st[0] + static_cast<int64_t>(s % NH) * st[1];
+// First row of sequence s = (batch b, head s - b NH), written as s st_h + b (st_b - NH st_h) with
+// st = {st_b - NH st_h, st_h}, and the byte span of its T rows of D elements.  b = floor(s / NH)
+// comes from a multiply by the host's nh_magic (nh_magic = 0 stands for NH = 1, b = s): it is exact
+// while s NH < 2^32 (the host checks this for strided calls), and contiguous rows have st[0] = 0.
+// (An integer division, the form b st_b + (s - b NH) st_h, and this helper itself in the chunk
+// kernel all made the compiler's code for its chunk loop markedly slower; the chunk kernel writes the
+// same sum out in place.)
+__device__ __forceinline__ const uint16_t* seq_rows(const uint16_t* p, int s, uint32_t nh_magic, const int64_t (&st)[2]) {
+    const int b = nh_magic ? static_cast<int>(__umulhi(static_cast<uint32_t>(s), nh_magic)) : s;
+    return p + static_cast<int64_t>(s) * st[1] + static_cast<int64_t>(b) * st[0];
 }
 __device__ __forceinline__ uint32_t seq_span(int T, uint32_t row_bytes, int D) {
     return T > 0 ? static_cast<uint32_t>(T - 1) * row_bytes + static_cast<uint32_t>(D) * 2u : 0u;
@@ -515,9 +527,12 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
     const int c_end = min(nc_total, c_begin + A.seg_chunks);
 
     SeqRsrc P;
-    P.q = make_rsrc(seq_rows(A.q, s, A.NH, A.sq), seq_span(A.T, A.rq, kDQK));
-    P.k = make_rsrc(seq_rows(A.k, s, A.NH, A.sk), seq_span(A.T, A.rk, kDQK));
-    P.v = make_rsrc(seq_rows(A.v, s, A.NH, A.sv), seq_span(A.T, A.rv, kDV));
+    // the sequence's rows, written out here rather than through seq_rows: this form keeps the
+    // compiler's code for the chunk loop as fast as with contiguous-only addressing
+    const int bq = A.nh_magic ? static_cast<int>(__umulhi(static_cast<uint32_t>(s), A.nh_magic)) : s;
+    P.q = make_rsrc(A.q + static_cast<int64_t>(s) * A.sq[1] + static_cast<int64_t>(bq) * A.sq[0], seq_span(A.T, A.rq, kDQK));
+    P.k = make_rsrc(A.k + static_cast<int64_t>(s) * A.sk[1] + static_cast<int64_t>(bq) * A.sk[0], seq_span(A.T, A.rk, kDQK));
+    P.v = make_rsrc(A.v + static_cast<int64_t>(s) * A.sv[1] + static_cast<int64_t>(bq) * A.sv[0], seq_span(A.T, A.rv, kDV));
     P.ig = make_rsrc(A.ipre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
     P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
     P.h = make_rsrc(A.h + static_cast<int64_t>(s) * A.T * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
@@ -1044,8 +1059,8 @@ __device__ __forceinline__ void loc_store(uint16_t* Kt, uint16_t* Vt, const LocR
 struct LocalArgs {
     const uint16_t* k;
     const uint16_t* v;
-    int NH;
-    int64_t sk[2], sv[2];   // (batch, head) element strides of k and v
+    uint32_t nh_magic;      // as in ChunkKernelArgs
+    int64_t sk[2], sv[2];   // as in ChunkKernelArgs
     uint32_t rk, rv;        // their row strides in bytes
     const float* ipre;
     const float* fpre;
@@ -1085,8 +1100,8 @@ local_state_kernel(LocalArgs A) {
     const int ntok = (tile_e - tile_b) * kLocTile;
 
     SeqRsrc P;
-    P.k = make_rsrc(seq_rows(A.k, s, A.NH, A.sk), seq_span(A.T, A.rk, kDQK));
-    P.v = make_rsrc(seq_rows(A.v, s, A.NH, A.sv), seq_span(A.T, A.rv, kDV));
+    P.k = make_rsrc(seq_rows(A.k, s, A.nh_magic, A.sk), seq_span(A.T, A.rk, kDQK));
+    P.v = make_rsrc(seq_rows(A.v, s, A.nh_magic, A.sv), seq_span(A.T, A.rv, kDV));
     P.ig = make_rsrc(A.ipre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
     P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
 
@@ -1301,21 +1316,20 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
 }
 
 // q, k, v strides of a call: the caller's (elements; batch, head, token for each), or contiguous
-// [B, NH, T, D] rows
-void set_strides(const ChunkArgs& a, int& NH, int64_t* sq, int64_t* sk, int64_t* sv, uint32_t* rq, uint32_t* rk,
-                 uint32_t* rv) {
-    NH = a.NH;
-    const int64_t T = a.T;
-    const int64_t st[9] = {a.NH * T * kDQK, T * kDQK, kDQK, a.NH * T * kDQK, T * kDQK, kDQK,
-                           a.NH * T * kDV, T * kDV, kDV};
+// [B, NH, T, D] rows; the kernels take {batch - NH head, head} per matrix (see seq_rows)
+void set_strides(const ChunkArgs& a, uint32_t& nh_magic, int64_t* sq, int64_t* sk, int64_t* sv, uint32_t* rq,
+                 uint32_t* rk, uint32_t* rv) {
+    nh_magic = a.NH > 1 ? static_cast<uint32_t>((uint64_t(1) << 32) / static_cast<uint64_t>(a.NH) + 1) : 0u;
+    const int64_t T = a.T, NH = a.NH;
+    const int64_t st[9] = {NH * T * kDQK, T * kDQK, kDQK, NH * T * kDQK, T * kDQK, kDQK, NH * T * kDV, T * kDV, kDV};
     const int64_t* x = a.strides ? a.strides : st;
     if (sq) {
-        sq[0] = x[0];
+        sq[0] = x[0] - NH * x[1];
         sq[1] = x[1];
     }
-    sk[0] = x[3];
+    sk[0] = x[3] - NH * x[4];
     sk[1] = x[4];
-    sv[0] = x[6];
+    sv[0] = x[6] - NH * x[7];
     sv[1] = x[7];
     if (rq) *rq = static_cast<uint32_t>(x[2] * 2);
     *rk = static_cast<uint32_t>(x[5] * 2);
@@ -1389,7 +1403,7 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
     k.q = static_cast<const uint16_t*>(a.q);
     k.k = static_cast<const uint16_t*>(a.k);
     k.v = static_cast<const uint16_t*>(a.v);
-    set_strides(a, k.NH, k.sq, k.sk, k.sv, &k.rq, &k.rk, &k.rv);
+    set_strides(a, k.nh_magic, k.sq, k.sk, k.sv, &k.rq, &k.rk, &k.rv);
     k.ipre = a.ipre;
     k.fpre = a.fpre;
     k.C0 = a.C0;
@@ -1411,7 +1425,7 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
         LocalArgs la{};
         la.k = k.k;
         la.v = k.v;
-        set_strides(a, la.NH, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
+        set_strides(a, la.nh_magic, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
         la.ipre = a.ipre;
         la.fpre = a.fpre;
         la.ws = k.ws;
@@ -1442,7 +1456,7 @@ hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, uint16_t* rowhl
     LocalArgs la{};
     la.k = static_cast<const uint16_t*>(a.k);
     la.v = static_cast<const uint16_t*>(a.v);
-    set_strides(a, la.NH, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
+    set_strides(a, la.nh_magic, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
     la.ipre = a.ipre;
     la.fpre = a.fpre;
     la.ws = slots;

@@ -461,7 +461,8 @@ def test_strided_span_bound_counts_the_padding_rows():
     assert call_strided(a, st) == 5
 
 
-@pytest.mark.parametrize("over", [dict(dt=Bd.MLSTM_F32), dict(DQK=128, DV=128, L=64), dict(L=32)])
+@pytest.mark.parametrize("over", [dict(dt=Bd.MLSTM_F32), dict(DQK=128, DV=128, L=64), dict(L=32),
+                                  dict(B=1 << 20, NH=64, T=64)])
 def test_strided_unsupported_shapes(over):
     st = proj_strides(DQK=over.get("DQK", 256), DV=over.get("DV", 512))
     assert call_strided(chunk_args(**over), st) == 3

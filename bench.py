@@ -584,6 +584,13 @@ def env_info():
         info["git_commit"] = r.stdout.strip() if r.returncode == 0 else None
     except (OSError, subprocess.SubprocessError):
         info["git_commit"] = None
+    # a copy of the tree without .git: the commit the library was built from (build.py records it)
+    try:
+        b = json.load(open(os.path.join(ROOT, "paper_2503_13427_amd", "build_info.json")))
+        info["built_from_commit"] = b.get("git_commit")
+        info["built_from_dirty_tree"] = b.get("git_dirty")
+    except (OSError, ValueError):
+        pass
     h = hashlib.sha256()
     for name in sorted(os.listdir(CSRC)):
         h.update(name.encode())

@@ -44,6 +44,28 @@ def _compile(src: str) -> str:
     return obj
 
 
+BUILD_INFO = os.path.join(PKG, "build_info.json")
+
+
+def _write_build_info() -> None:
+    """Records the git commit the library was built from (and whether the tree had uncommitted
+    changes) next to it, so that a copy of the tree without its .git still says what it runs."""
+    import json
+
+    info = {"git_commit": None, "git_dirty": None}
+    try:
+        r = subprocess.run(["git", "-C", ROOT, "rev-parse", "HEAD"], capture_output=True, text=True, timeout=10)
+        if r.returncode == 0:
+            info["git_commit"] = r.stdout.strip()
+            d = subprocess.run(["git", "-C", ROOT, "status", "--porcelain", "--untracked-files=no"],
+                               capture_output=True, text=True, timeout=10)
+            info["git_dirty"] = bool(d.stdout.strip()) if d.returncode == 0 else None
+    except (OSError, subprocess.SubprocessError):
+        pass
+    with open(BUILD_INFO, "w") as f:
+        json.dump(info, f)
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
     with cf.ThreadPoolExecutor(min(8, len(SOURCES))) as ex:
@@ -54,6 +76,7 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
+    _write_build_info()
     if verbose:
         print(LIB)
     return LIB

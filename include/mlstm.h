@@ -368,6 +368,21 @@ const char* mlstm_status_string(mlstm_status s);
 /* Library version: major * 10000 + minor * 100 + patch. */
 int mlstm_version(void);
 
+/*
+ * Debug builds only (compiled with -DMLSTM_DEBUG, libmlstm_debug.so): the
+ * kernels check their computed indices (state slots, LDS tiles, sequence and
+ * row offsets) against the extents of what they address, and a failed check
+ * sets a bit instead of faulting.  This call returns the bits set since the
+ * previous call and clears them: 1 chunkwise prefill (bf16 MFMA, including the
+ * segment passes), 2 chunkwise prefill (fp32), 4 decode step, 8 output norm,
+ * 16 gate pre-activations, 32 chunkwise backward, 64 parallel-form backward.
+ * 0 means no check failed.  The caller synchronises the device first (the
+ * words are read with a synchronous copy on the default stream).  A library
+ * built without the checks returns MLSTM_DEBUG_NOT_BUILT.
+ */
+#define MLSTM_DEBUG_NOT_BUILT 0x80000000u
+unsigned int mlstm_debug_flags(void);
+
 #ifdef __cplusplus
 }
 #endif

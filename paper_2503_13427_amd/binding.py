@@ -74,6 +74,8 @@ lib.mlstm_status_string.argtypes = [_i]
 lib.mlstm_status_string.restype = ctypes.c_char_p
 lib.mlstm_version.argtypes = []
 lib.mlstm_version.restype = _i
+lib.mlstm_debug_flags.argtypes = []
+lib.mlstm_debug_flags.restype = ctypes.c_uint
 
 
 class MlstmError(RuntimeError):
@@ -88,6 +90,15 @@ def mlstm_status_string(status: int) -> str:
 
 def mlstm_version() -> int:
     return lib.mlstm_version()
+
+
+MLSTM_DEBUG_NOT_BUILT = 0x80000000
+
+
+def mlstm_debug_flags() -> int:
+    """Debug builds: the bounds-check bits set since the last call (0: none failed); other builds
+    return MLSTM_DEBUG_NOT_BUILT.  Synchronise the device first."""
+    return int(lib.mlstm_debug_flags())
 
 
 def _dtype_code(t: torch.Tensor) -> int:

@@ -17,6 +17,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmlstm.so")
+# the same sources with the device bounds checks compiled in (-DMLSTM_DEBUG; mlstm_debug_flags)
+DEBUG_OBJDIR = os.path.join(PKG, "_build_debug")
+DEBUG_LIB = os.path.join(PKG, "libmlstm_debug.so")
 ARCH = "gfx950"
 
 SOURCES = ["mlstm_abi.cpp", "mlstm_step.hip", "mlstm_chunkwise_f32.hip", "mlstm_chunkwise_mfma.hip",
@@ -34,9 +37,10 @@ def _hipcc() -> str:
     return "hipcc"
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc()] + COMMON + NO_PACKED_FP32 + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(src: str, debug: bool = False) -> str:
+    obj = os.path.join(DEBUG_OBJDIR if debug else OBJDIR, os.path.splitext(src)[0] + ".o")
+    extra = ["-DMLSTM_DEBUG"] if debug else []
+    cmd = [_hipcc()] + COMMON + NO_PACKED_FP32 + extra + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
@@ -66,20 +70,23 @@ def _write_build_info() -> None:
         json.dump(info, f)
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(OBJDIR, exist_ok=True)
+def build(verbose: bool = False, debug: bool = False) -> str:
+    """Builds libmlstm.so, or with ``debug`` libmlstm_debug.so (device bounds checks compiled in)."""
+    os.makedirs(DEBUG_OBJDIR if debug else OBJDIR, exist_ok=True)
     with cf.ThreadPoolExecutor(min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp%d" % os.getpid()
+        objs = list(ex.map(lambda src: _compile(src, debug), SOURCES))
+    target = DEBUG_LIB if debug else LIB
+    tmp = target + ".tmp%d" % os.getpid()
     cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
-    _write_build_info()
+    os.replace(tmp, target)
+    if not debug:
+        _write_build_info()
     if verbose:
-        print(LIB)
-    return LIB
+        print(target)
+    return target
 
 
 if __name__ == "__main__":

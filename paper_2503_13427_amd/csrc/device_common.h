@@ -6,6 +6,35 @@
 
 namespace mlstm {
 
+// Debug builds (-DMLSTM_DEBUG): bounds checks on computed indices that record a violation in a
+// flag word of the translation unit (one bit per source file) instead of trapping, so a violated
+// check never faults the device.  The host collects and clears the words with mlstm_debug_flags().
+// In the default build the checks compile to nothing.
+#ifdef MLSTM_DEBUG
+namespace {
+__device__ unsigned int g_debug_flags;
+}  // namespace
+#define MLSTM_CHECK(cond, bit)                                           \
+    do {                                                                 \
+        if (!(cond)) atomicOr(&::mlstm::g_debug_flags, (bit));           \
+    } while (0)
+// Defines `fn(unsigned int* out)`: ORs this translation unit's flag word into *out and clears it.
+#define MLSTM_DEBUG_READER(fn)                                                                              \
+    hipError_t fn(unsigned int* out) {                                                                      \
+        unsigned int v = 0;                                                                                 \
+        hipError_t e = hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_debug_flags), sizeof(v), 0, hipMemcpyDeviceToHost); \
+        if (e != hipSuccess) return e;                                                                      \
+        *out |= v;                                                                                          \
+        v = 0;                                                                                              \
+        return hipMemcpyToSymbol(HIP_SYMBOL(g_debug_flags), &v, sizeof(v), 0, hipMemcpyHostToDevice);       \
+    }
+#else
+#define MLSTM_CHECK(cond, bit) ((void)0)
+#endif
+// bits of the flag word, one per source file
+constexpr unsigned int kDbgChunkMfma = 1u, kDbgChunkF32 = 2u, kDbgStep = 4u, kDbgOutputNorm = 8u,
+                       kDbgGatePreact = 16u, kDbgChunkBwd = 32u, kDbgParallelBwd = 64u;
+
 // bf16 is carried as its uint16 bit pattern.
 struct bf16_t {
     uint16_t bits;

@@ -119,4 +119,15 @@ hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t 
 constexpr size_t kChunkScratchBytes = size_t(64) << 20;
 hipError_t chunk_scratch(void** ptr);
 
+#ifdef MLSTM_DEBUG
+// Debug builds: each source file's bounds-check flag word, ORed into *out and cleared.
+hipError_t debug_flags_chunk_mfma(unsigned int* out);
+hipError_t debug_flags_chunk_f32(unsigned int* out);
+hipError_t debug_flags_step(unsigned int* out);
+hipError_t debug_flags_output_norm(unsigned int* out);
+hipError_t debug_flags_gate_preact(unsigned int* out);
+hipError_t debug_flags_chunk_bwd(unsigned int* out);
+hipError_t debug_flags_parallel_bwd(unsigned int* out);
+#endif
+
 }  // namespace mlstm

@@ -74,6 +74,21 @@ const char* mlstm_status_string(mlstm_status s) {
 
 int mlstm_version(void) { return 100; }
 
+unsigned int mlstm_debug_flags(void) {
+#ifdef MLSTM_DEBUG
+    unsigned int f = 0;
+    hipError_t (*const readers[])(unsigned int*) = {
+        mlstm::debug_flags_chunk_mfma, mlstm::debug_flags_chunk_f32,  mlstm::debug_flags_step,
+        mlstm::debug_flags_output_norm, mlstm::debug_flags_gate_preact, mlstm::debug_flags_chunk_bwd,
+        mlstm::debug_flags_parallel_bwd};
+    for (auto r : readers)
+        if (r(&f) != hipSuccess) return MLSTM_DEBUG_NOT_BUILT | 0x40000000u;   // the words could not be read
+    return f;
+#else
+    return MLSTM_DEBUG_NOT_BUILT;
+#endif
+}
+
 size_t mlstm_chunkwise_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L, mlstm_dtype dt) {
     if (B <= 0 || NH <= 0 || T < 0 || L <= 0 || !dtype_valid(&dt)) return 0;
     if (!mlstm::chunk_mfma_supported(dt, DQK, DV, L)) return 0;

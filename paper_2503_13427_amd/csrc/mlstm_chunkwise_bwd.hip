@@ -101,10 +101,12 @@ struct BwdParams {
 };
 
 __device__ __forceinline__ float* lz_of(const BwdParams& A, int s, int c) {
+    MLSTM_CHECK(c >= 0 && c < A.NC && s >= 0, kDbgChunkBwd);
     return c ? A.slots + (static_cast<int64_t>(s) * (A.NC - 1) + c - 1) * kSlotFloats
              : A.lz0 + static_cast<int64_t>(s) * kLzFloats;
 }
 __device__ __forceinline__ uint16_t* hl_of(const BwdParams& A, int s, int slot) {
+    MLSTM_CHECK(slot >= 0 && slot < A.NC - 1 && s >= 0, kDbgChunkBwd);
     return A.hl + (static_cast<int64_t>(s) * (A.NC - 1) + slot) * 2 * kCV;
 }
 
@@ -925,5 +927,9 @@ hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t 
     hipLaunchKernelGGL(bwd_gate_kernel, dim3(S), dim3(256), 0, stream, p);
     return hipGetLastError();
 }
+
+#ifdef MLSTM_DEBUG
+MLSTM_DEBUG_READER(debug_flags_chunk_bwd)
+#endif
 
 }  // namespace mlstm

@@ -78,6 +78,7 @@ chunk_f32_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn
     const int ntiles = DV / DVT;
     const int64_t seq = blockIdx.x / ntiles;
     const int tile = blockIdx.x % ntiles;
+    MLSTM_CHECK(ntiles * DVT == DV && L <= T + L, kDbgChunkF32);
     const int v0 = tile * DVT;
     const int tid = threadIdx.x;
     const float qscale = rsqrtf(static_cast<float>(DQK));
@@ -221,5 +222,9 @@ hipError_t launch_chunk_f32(mlstm_dtype dt, const ChunkArgs& a, hipStream_t stre
     }
     return hipGetLastError();
 }
+
+#ifdef MLSTM_DEBUG
+MLSTM_DEBUG_READER(debug_flags_chunk_f32)
+#endif
 
 }  // namespace mlstm

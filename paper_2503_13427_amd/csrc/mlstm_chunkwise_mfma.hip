@@ -223,6 +223,7 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
     for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
         const int item = tid + i * NT;
         const int off = (item / PR) * QP + 8 * (item % PR);
+        MLSTM_CHECK(off >= 0 && off + 8 <= Cfg<L>::QKE, kDbgChunkMfma);
         *reinterpret_cast<u32x4_t*>(&Qd[off]) = r.q[i];
         if constexpr (!Cfg<L>::KT) *reinterpret_cast<u32x4_t*>(&Kd[off]) = r.k[i];
     }
@@ -241,6 +242,7 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
             for (int h = 0; h < 2; ++h) {
                 const f32x4_t d = mfma16(r.k[i], E[h], f32x4_t{});
                 const u32x2_t o{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
+                MLSTM_CHECK(kt_row(32 * b + 16 * h + l16) < Cfg<L>::DB && 16 * a + 4 * g16 + 4 <= KTP, kDbgChunkMfma);
                 *reinterpret_cast<u32x2_t*>(&Kd[kt_row(32 * b + 16 * h + l16) * KTP + 16 * a + 4 * g16]) = o;
             }
         }
@@ -310,6 +312,7 @@ __device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const VtPacked<L,
             u32x2_t o;
             o[0] = pack_bf16x2(lo_f32(x[0]) * w[0], hi_f32(x[0]) * w[1]);
             o[1] = pack_bf16x2(lo_f32(x[1]) * w[2], hi_f32(x[1]) * w[3]);
+            MLSTM_CHECK(32 * b + 16 * h + l16 < kDVT && tau + 4 <= TP, kDbgChunkMfma);
             *reinterpret_cast<u32x2_t*>(&VwT[(32 * b + 16 * h + l16) * TP + tau]) = o;
         }
     }
@@ -322,8 +325,10 @@ __device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const VtPacked<L, 
     for (int i = 0; i < VRegs<L, NT>::N * VRegs<L, NT>::PARTS; ++i) {
         const int pc = wave + NW * i, a = pc % NA, b = pc / NA;
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < 2; ++h) {
+            MLSTM_CHECK(32 * b + 16 * h + l16 < kDVT && 16 * a + 4 * g16 + 4 <= TP, kDbgChunkMfma);
             *reinterpret_cast<u32x2_t*>(&VtT[(32 * b + 16 * h + l16) * TP + 16 * a + 4 * g16]) = pv[2 * i + h];
+        }
     }
 }
 // Gate pre-activations of one chunk, one (L = 64) or two (L = 128) per lane of the gate wave.
@@ -439,6 +444,7 @@ struct ChunkKernelArgs {
     const float* n0;
     const float* m0;
     float* ws;         // segment slots (NULL when G == 1)
+    int S;             // sequences (B NH)
     int T;
     int G;             // segments per sequence
     int R;             // local sub-segments per segment; segment g >= 1 enters from slot g R - 1
@@ -552,11 +558,13 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         nin = A.n0 ? A.n0 + static_cast<int64_t>(s) * kDQK : nullptr;
         m_prev = A.m0 ? A.m0[s] : 0.0f;
     } else {
+        MLSTM_CHECK(s < A.S && g * A.R - 1 >= 0 && g * A.R - 1 < A.NS, kDbgChunkMfma);
         const float* slot = A.ws + (static_cast<int64_t>(s) * A.NS + g * A.R - 1) * kSlotFloats;
         Cin = slot;
         nin = slot + kDQK * kDV;
         m_prev = slot[kDQK * kDV + kDQK + 2];
     }
+    MLSTM_CHECK(s < A.S, kDbgChunkMfma);
     // L = 64: a segment entry slot is loaded after the first chunk's staging loads, so that their
     // waits do not include it (at L = 128 the early load measured faster)
     const bool slot_entry = (Cin && g > 0);
@@ -869,8 +877,11 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             for (int vt = 0; vt < VT; ++vt)
 #pragma unroll
                 for (int T = 0; T < NTT; ++T)
-                    if ((T & 1) != dh)
+                    if ((T & 1) != dh) {
+                        MLSTM_CHECK(((((vg * VT + vt) * NTT + T) * 64 + lane) * 4 + 4) <= static_cast<int>(sizeof(S.X) / 4),
+                                    kDbgChunkMfma);
                         *reinterpret_cast<f32x4_t*>(&S.X[(((vg * VT + vt) * NTT + T) * 64 + lane) * 4]) = Nacc[vt][T];
+                    }
         }
         if constexpr (CF::ST_ALIAS) __syncthreads();   // the last d block is fully read before S~ overwrites it
         // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums (fp32, before the
@@ -899,6 +910,9 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 u32x2_t o;
                 o[0] = pack_bf16x2(vals[0], vals[1]);
                 o[1] = pack_bf16x2(vals[2], vals[3]);
+                MLSTM_CHECK(tau < L && 16 * sb + 4 * g16 + 4 <= SP &&
+                                tau * SP + 16 * sb + 4 * g16 + 4 <= (CF::ST_ALIAS ? CF::SETE : L * SP),
+                            kDbgChunkMfma);
                 *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
                 rsum = sum_rows4(rsum);
                 if (g16 == 0) S.rs[sb][tau] = rsum;
@@ -933,6 +947,8 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                 acc *= ic;
 #pragma unroll
                 for (int ks = 0; ks <= T / 2; ++ks) {
+                    MLSTM_CHECK(32 * ks + 8 * g16 + 8 <= SP && vcol(vt) + l16 < kDVT && 32 * ks + 8 * g16 + 8 <= CF::TP,
+                                kDbgChunkMfma);
                     const u32x4_t b = *reinterpret_cast<const u32x4_t*>(&St[tau * SP + 32 * ks + 8 * g16]);
                     const u32x4_t va = *reinterpret_cast<const u32x4_t*>(&VtT[(vcol(vt) + l16) * CF::TP + 32 * ks + 8 * g16]);
                     acc = mfma16(va, b, acc);
@@ -1066,6 +1082,7 @@ struct LocalArgs {
     const float* ipre;
     const float* fpre;
     float* ws;
+    int S;             // sequences (B NH)
     int T;
     int NS;            // local slots per sequence: (G - 1) segments x R sub-segments
     int R;             // sub-segments per segment
@@ -1222,6 +1239,7 @@ local_state_kernel(LocalArgs A) {
     }
 
     // slot (s, local slot sl): C [DQK x DV] row-major, then n, m_loc, logsig sum
+    MLSTM_CHECK(s < A.S && sl < A.NS && ntok <= kLocMax, kDbgChunkMfma);
     float* slot = A.ws + (static_cast<int64_t>(s) * A.NS + sl) * kSlotFloats;
 #pragma unroll
     for (int q = 0; q < 8; ++q)
@@ -1411,6 +1429,7 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
     k.n0 = a.n0;
     k.m0 = a.m0;
     k.ws = static_cast<float*>(workspace);
+    k.S = S;
     k.T = a.T;
     k.G = G;
     k.R = R;
@@ -1430,6 +1449,7 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
         la.ipre = a.ipre;
         la.fpre = a.fpre;
         la.ws = k.ws;
+        la.S = S;
         la.T = a.T;
         la.NS = k.NS;
         la.R = R;
@@ -1461,6 +1481,7 @@ hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, uint16_t* rowhl
     la.ipre = a.ipre;
     la.fpre = a.fpre;
     la.ws = slots;
+    la.S = S;
     la.T = a.T;
     la.NS = nc - 1;
     la.R = 1;
@@ -1500,5 +1521,9 @@ hipError_t chunk_scratch(void** ptr) {
     *ptr = g_scratch_ptr[dev];
     return hipSuccess;
 }
+
+#ifdef MLSTM_DEBUG
+MLSTM_DEBUG_READER(debug_flags_chunk_mfma)
+#endif
 
 }  // namespace mlstm

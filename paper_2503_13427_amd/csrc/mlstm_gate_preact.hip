@@ -73,6 +73,7 @@ __global__ void __launch_bounds__(64 * NW) gate_preact_kernel(GateArgs A) {
 
     const int kq = A.d / NW;         // this wave's share of K (a multiple of 32)
     const int k0 = wave * kq;
+    MLSTM_CHECK(k0 + kq <= A.d && kq % 32 == 0, kDbgGatePreact);
     const int steps = kq / 32;
     f32x4_t acc[MT][NCT];
 #pragma unroll
@@ -174,5 +175,9 @@ hipError_t launch_gate_preact(const void* x, const void* w_t, const float* bias,
     else launch_mt<1, 4>(a, nct, stream);
     return hipGetLastError();
 }
+
+#ifdef MLSTM_DEBUG
+MLSTM_DEBUG_READER(debug_flags_gate_preact)
+#endif
 
 }  // namespace mlstm

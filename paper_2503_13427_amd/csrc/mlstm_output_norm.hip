@@ -95,6 +95,7 @@ output_norm_kernel(const TIn* ht, const TIn* __restrict__ op, const float* __res
     const int64_t bb = bh / NH;
     const int head = static_cast<int>(bh - bb * NH);
     const int ng = DV / 4;
+    MLSTM_CHECK(t < T && head < NH && DV % 4 == 0, kDbgOutputNorm);
     const TIn* x = ht + row * DV;
     const TIn* o = op + bb * so.b + head * so.h + t * so.t;
     TIn* y = h + bb * sy.b + head * sy.h + t * sy.t;
@@ -189,5 +190,9 @@ hipError_t launch_output_norm(mlstm_dtype dt, const void* h_tilde, const void* o
     else by_width(float{});
     return hipGetLastError();
 }
+
+#ifdef MLSTM_DEBUG
+MLSTM_DEBUG_READER(debug_flags_output_norm)
+#endif
 
 }  // namespace mlstm

@@ -138,6 +138,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_kernel(BwdArgs A) {
     const int ntile = (T + kBT - 1) / kBT;
     const int64_t seq = blockIdx.x / ntile;
     const int t0 = (blockIdx.x % ntile) * kBT;
+    MLSTM_CHECK(t0 < T && DQK % 16 == 0 && DV % 16 == 0, kDbgParallelBwd);
     const int tid = threadIdx.x;
     // pair (row pr, column pc); for outputs, row pr and the columns j kBT + pc
     const int pr = tid / kBT, pc = tid % kBT;
@@ -502,6 +503,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_row_mfma_kernel(BwdArgs A) {
     const int ntile = (T + kBT - 1) / kBT;
     const int64_t seq = blockIdx.x / ntile;
     const int t0 = (blockIdx.x % ntile) * kBT;
+    MLSTM_CHECK(t0 < T && DQK % 16 == 0 && DV % 16 == 0, kDbgParallelBwd);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, g = lane >> 4;
     const int pr = tid / kBT, pc = tid % kBT;
@@ -933,5 +935,9 @@ hipError_t launch_parallel_bwd(mlstm_dtype dt, const void* q, const void* k, con
     const int S = B * NH;
     return dt == MLSTM_BF16 ? launch_typed<bf16_t>(a, S, stream) : launch_typed<float>(a, S, stream);
 }
+
+#ifdef MLSTM_DEBUG
+MLSTM_DEBUG_READER(debug_flags_parallel_bwd)
+#endif
 
 }  // namespace mlstm

@@ -87,6 +87,7 @@ step_kernel(const TIn* __restrict__ q, const TIn* __restrict__ k, const TIn* __r
     const int c4_stride = RG == 1 ? kStepThreads : NC4;
     const bool active = rg < RG;
     const int nrows = active ? (DQK - rg + RG - 1) / RG : 0;
+    MLSTM_CHECK(cv0 + DVs <= DV && (DVs & 3) == 0 && (nrows == 0 || rg + (nrows - 1) * RG < DQK), kDbgStep);
 
     // C' = f C + (i k) v^T is streamed once (Eq. 3) with kBatch rows in flight per thread.
     // C_out may be C itself, so the compiler cannot hoist loads over stores; the next batch
@@ -331,5 +332,9 @@ size_t step_lds_bytes(int DQK, int DVs) {
     const int RG = NC4 >= kStepThreads ? 1 : kStepThreads / NC4;
     return sizeof(float) * (2 * static_cast<size_t>(DQK) + (RG > 1 ? static_cast<size_t>(RG) * DVs : 0));
 }
+
+#ifdef MLSTM_DEBUG
+MLSTM_DEBUG_READER(debug_flags_step)
+#endif
 
 }  // namespace mlstm

@@ -32,12 +32,27 @@ def test_header_declares_expected_entry_points():
                                            "mlstm_chunkwise_bwd_workspace_bytes",
                                            "mlstm_output_norm", "mlstm_output_norm_tokens", "mlstm_gate_preact", "mlstm_parallel_bwd",
                                            "mlstm_parallel_bwd_workspace_bytes", "mlstm_status_string",
-                                           "mlstm_version"])
+                                           "mlstm_version", "mlstm_debug_flags"])
 
 
 @pytest.mark.parametrize("name", declared_functions())
 def test_library_exports_every_declared_symbol(name):
     assert hasattr(lib, name)
+
+
+def test_default_build_reports_no_debug_checks():
+    """The default library carries no device bounds checks and says so without touching a device."""
+    if os.path.basename(Bd.LIB_PATH) != "libmlstm.so":
+        pytest.skip("another build of the library is loaded")
+    assert Bd.mlstm_debug_flags() == Bd.MLSTM_DEBUG_NOT_BUILT
+
+
+@pytest.mark.skipif(not os.path.exists(os.path.join(ROOT, "paper_2503_13427_amd", "libmlstm_debug.so")),
+                    reason="libmlstm_debug.so is not built")
+def test_debug_build_exports_every_declared_symbol():
+    dbg = ctypes.CDLL(os.path.join(ROOT, "paper_2503_13427_amd", "libmlstm_debug.so"))
+    for name in declared_functions():
+        assert hasattr(dbg, name), name
     out = os.popen(f"nm -D --defined-only {Bd.LIB_PATH}").read()
     assert re.search(rf"\bT {name}$", out, flags=re.M), name
 

@@ -93,9 +93,10 @@ bool chunk_mfma_supported(mlstm_dtype dt, int DQK, int DV, int L);
 int chunk_mfma_segments(int B, int NH, int T, int L);
 size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L);
 hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream);
-// State entering every 64-token chunk c >= 1 (slots: S (NC - 1) segment slots; rowhl: the same C as
-// bf16 hi + lo rows, S (NC - 1) x 2 x DQK x DV)
-hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, uint16_t* rowhl, hipStream_t stream);
+// State entering every 64-token chunk c >= 1 (slots: S (NC - 1) slots, fp32 C in the four-row
+// interleaved layout, n and m); seg: chunk_states_workspace_bytes of segment slots (NULL: one segment)
+size_t chunk_states_workspace_bytes(int B, int NH, int T);
+hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, float* seg, hipStream_t stream);
 // --- chunkwise backward (bf16, DQK = 256, DV = 512, L = 64) --------------------
 bool chunk_bwd_supported(mlstm_dtype dt, int DQK, int DV, int L);
 size_t chunk_bwd_workspace_bytes(int B, int NH, int T);

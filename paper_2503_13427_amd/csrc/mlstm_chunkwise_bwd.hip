@@ -30,10 +30,12 @@
 // rounding of h~ would dominate the result.  The forward's output is not an input.
 //
 // Passes (one stream, in order):
-//   states  the forward's local-state and combine passes over one-chunk segments leave the entry
-//           state of every chunk c >= 1 (fp32 C, n, m, and C as bf16 hi + lo rows)
-//   dhc     one workgroup per (chunk, 64-row d tile): X = dH C^T on the entry state's hi + lo rows
-//           (kept in dq) and the tile's share of q^_t . X_t
+//   states  the entry state of every chunk c >= 1 (fp32 C, n, m in slot c - 1): the prefill's
+//           segment schedule (local pass in the bf16 hi + lo form, combine) for the entry states of
+//           segments of several chunks, then a walk over each segment's chunks with the state
+//           update alone, which writes each chunk's entry state
+//   dhc     one workgroup per (chunk, 128-row d tile): X = dH C^T on the entry state, split into
+//           bf16 hi + lo in registers (kept in dq), and the tile's share of q^_t . X_t
 //   intra   one workgroup per chunk: gates, S, D, den; per 128-column piece of dv, (dH V^T), the
 //           intra term of dv and the piece's columns of L_c; then w, P, dq (complete), the intra
 //           term of dk and z_c; writes the key weights, the chunk's decay and q_t . dq_t
@@ -68,7 +70,7 @@ constexpr int64_t kLzFloats = kCV + kDQK;                 // L_c then z_c
 constexpr int kScanE4 = static_cast<int>(kLzFloats / 4);  // float4 items of the reverse scan
 constexpr int kScanBlocks = (kScanE4 + 255) / 256;
 constexpr int kTokF = 1;                                  // per-token floats: the key weight
-constexpr int kPartF = 8;                                 // per-token partial sums: q^.X x 4 (then q.dq), k.dk x 4
+constexpr int kPartF = 8;                                 // per-token partial sums: q^.X x 2 (then q.dq), k.dk x 4
 
 struct BwdParams {
     const uint16_t* q;
@@ -89,7 +91,7 @@ struct BwdParams {
     float* dn0;
     float* dm0;
     float* slots;        // S (NC - 1) state slots: entry state of chunk c in slot c - 1, then L_c, z_c
-    uint16_t* hl;        // S (NC - 1) x 2 x DQK x DV: C of slot c as bf16 hi + lo rows, then Gam_c
+    uint16_t* hl;        // S (NC - 1) x 2 x DQK x DV: Gam_c as bf16 hi + lo rows
     float* lz0;          // S x (DQK DV + DQK): L_0, z_0
     float* gamn;         // S x NC x DQK: gam_c
     float* tok;          // S x T x kTokF
@@ -199,8 +201,29 @@ struct DhcSmem {
 };
 static_assert(sizeof(DhcSmem) <= 160 * 1024, "LDS budget");
 
-// One workgroup per (chunk, 64-row d tile): X = dH C^T on the entry state's hi + lo rows, stored in dq
-// (the intra pass scales it by g / den and adds the rest), and the tile's share of q^_t . X_t.
+// One-hot selection E_h (32 x 16: column n has its one in row 16 h + n) in the B-operand layout: lane
+// (l16, g16) holds k slots 8 g16 + 0..7 of column l16.
+__device__ __forceinline__ u32x4_t onehot(int h, int lane) {
+    const int pos = 16 * h + (lane & 15) - 8 * (lane >> 4);
+    const uint32_t one = (pos & 1) ? 0x3F800000u : 0x3F80u;   // bf16 1.0 in the high or low half
+    u32x4_t e;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) e[d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
+    return e;
+}
+__device__ __forceinline__ u32x4_t pack4x2(const f32x4_t& a, const f32x4_t& b) {
+    return u32x4_t{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
+}
+
+// One workgroup per (chunk, 128-row d tile); wave w owns rows dw = d0 + 32 w + 0..31.  X^T [d][tau] =
+// sum_v C[d][v] dH[tau][v] on the entry state, stored in dq (the intra pass scales it by g / den and
+// adds the rest), and the tile's share of q^_t . X_t.
+// The entry state is the fp32 slot (four rows interleaved: one 16-byte piece holds four consecutive
+// d of one v), split into bf16 hi + lo in registers.  The A operand of the product wants eight v of one
+// d per lane, so each 32 d x 16 v piece is transposed on the matrix cores: as the A operand of a
+// product with the one-hot E_h it gives, in lane (l16, g16), C[dw + 16 h + l16][v 4 g16 + 0..3] (exact).
+// A k step of 32 v takes two such pieces; its k slots are v = 4 g16 + 0..3 and 16 + 4 g16 + 0..3, and
+// the dH operand (two 8-byte reads of a dH row) uses the same order.
 __global__ void __launch_bounds__(kBT) bwd_dhc_kernel(BwdParams A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     DhcSmem& S = *reinterpret_cast<DhcSmem*>(smem_raw);
@@ -208,57 +231,80 @@ __global__ void __launch_bounds__(kBT) bwd_dhc_kernel(BwdParams A) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g16 = lane >> 4, l16 = lane & 15;
     const int wi = work_index();
-    const int j = wi % 4, c = (wi / 4) % A.NC, s = wi / 4 / A.NC;
-    const int T = A.T, t0 = c * kBL, d0 = 64 * j;
+    const int j = wi % 2, c = (wi / 2) % A.NC, s = wi / 2 / A.NC;
+    const int T = A.T, t0 = c * kBL, dw = 128 * j + 32 * wave;
     const int64_t st = static_cast<int64_t>(s) * T;
     const auto rdh = make_rsrc(A.dh + st * kDV, static_cast<uint32_t>(T) * kDV * 2);
     const bool has_c = (c > 0) || (A.C0 != nullptr);
 
     if (has_c) stage_rows<kDV>(S.dH, kHP, rdh, kDV, t0, 0, tid);
     __syncthreads();
-    // X^T [d][tau] = sum_v C[d][v] dH[tau][v]; rows d = d0 + 16 wave + l16 of the entry state
-    f32x4_t acc[4];
+    f32x4_t acc[2][4];   // [16-row d tile h][tau block]
 #pragma unroll
-    for (int tb = 0; tb < 4; ++tb) acc[tb] = f32x4_t{};
-    const int drow = d0 + 16 * wave + l16;
-    if (c > 0) {
-        const uint16_t* hi = hl_of(A, s, c - 1) + static_cast<int64_t>(drow) * kDV + 8 * g16;
-        const uint16_t* lo = hi + kCV;
-#pragma unroll 4
-        for (int ks = 0; ks < kDV / 32; ++ks) {
-            const u32x4_t ah = *reinterpret_cast<const u32x4_t*>(hi + 32 * ks);
-            const u32x4_t al = *reinterpret_cast<const u32x4_t*>(lo + 32 * ks);
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int tb = 0; tb < 4; ++tb) {
-                const u32x4_t b = row_op(S.dH, kHP, 16 * tb, 32 * ks, lane);
-                acc[tb] = mfma16(ah, b, acc[tb]);
-                acc[tb] = mfma16(al, b, acc[tb]);
-            }
-        }
-    } else if (A.C0) {
-        const float* c0 = A.C0 + static_cast<int64_t>(s) * kCV + static_cast<int64_t>(drow) * kDV + 8 * g16;
+        for (int tb = 0; tb < 4; ++tb) acc[h][tb] = f32x4_t{};
+    if (has_c) {
+        const float* slot = c > 0 ? lz_of(A, s, c) : nullptr;   // the entry state of chunk c
+        const float* c0 = A.C0 ? A.C0 + static_cast<int64_t>(s) * kCV : nullptr;
+        const u32x4_t E0 = onehot(0, lane), E1 = onehot(1, lane);
 #pragma unroll 2
         for (int ks = 0; ks < kDV / 32; ++ks) {
-            u32x4_t ah, al;
-            split8(*reinterpret_cast<const float4*>(c0 + 32 * ks), *reinterpret_cast<const float4*>(c0 + 32 * ks + 4), ah, al);
+            u32x4_t ah[2], al[2];   // [h]
+            if (c > 0) {
+                // pieces u = 0, 1: lane (l16, g16) loads C[dw + 8 g16 + 0..7][32 ks + 16 u + l16]
+                f32x4_t th[2][2], tl[2][2];   // [u][h]
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int v = 32 * ks + 16 * u + l16;
+                    const f32x4_t p0 = *reinterpret_cast<const f32x4_t*>(slot + slot_c4(dw / 4 + 2 * g16, v));
+                    const f32x4_t p1 = *reinterpret_cast<const f32x4_t*>(slot + slot_c4(dw / 4 + 2 * g16 + 1, v));
+                    u32x4_t xh, xl;
+                    split8(make_float4(p0[0], p0[1], p0[2], p0[3]), make_float4(p1[0], p1[1], p1[2], p1[3]), xh, xl);
+                    th[u][0] = mfma16(xh, E0, f32x4_t{});
+                    th[u][1] = mfma16(xh, E1, f32x4_t{});
+                    tl[u][0] = mfma16(xl, E0, f32x4_t{});
+                    tl[u][1] = mfma16(xl, E1, f32x4_t{});
+                }
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    ah[h] = pack4x2(th[0][h], th[1][h]);
+                    al[h] = pack4x2(tl[0][h], tl[1][h]);
+                }
+            } else {
+                // C0, row-major: lane (l16, g16) reads row dw + 16 h + l16 at v = 32 ks + 4 g16 and + 16
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const float* r = c0 + static_cast<int64_t>(dw + 16 * h + l16) * kDV + 32 * ks + 4 * g16;
+                    split8(*reinterpret_cast<const float4*>(r), *reinterpret_cast<const float4*>(r + 16), ah[h], al[h]);
+                }
+            }
 #pragma unroll
             for (int tb = 0; tb < 4; ++tb) {
-                const u32x4_t b = row_op(S.dH, kHP, 16 * tb, 32 * ks, lane);
-                acc[tb] = mfma16(ah, b, acc[tb]);
-                acc[tb] = mfma16(al, b, acc[tb]);
+                const uint16_t* row = S.dH + (16 * tb + l16) * kHP + 32 * ks + 4 * g16;
+                const u32x2_t b0 = lds_u32x2(row), b1 = lds_u32x2(row + 16);
+                const u32x4_t b = u32x4_t{b0[0], b0[1], b1[0], b1[1]};
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    acc[h][tb] = mfma16(ah[h], b, acc[h][tb]);
+                    acc[h][tb] = mfma16(al[h], b, acc[h][tb]);
+                }
             }
         }
     }
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) {
         const int tt = 16 * tb + l16;
-        const int d = d0 + 16 * wave + 4 * g16;
         float qx = 0.0f;
         if (t0 + tt < T) {
-            *reinterpret_cast<f32x4_t*>(&A.dq[(st + t0 + tt) * kDQK + d]) = acc[tb];
-            const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(&A.q[(st + t0 + tt) * kDQK + d]);
-            qx = lo_f32(qv[0]) * acc[tb][0] + hi_f32(qv[0]) * acc[tb][1] + lo_f32(qv[1]) * acc[tb][2] +
-                 hi_f32(qv[1]) * acc[tb][3];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int d = dw + 16 * h + 4 * g16;
+                *reinterpret_cast<f32x4_t*>(&A.dq[(st + t0 + tt) * kDQK + d]) = acc[h][tb];
+                const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(&A.q[(st + t0 + tt) * kDQK + d]);
+                qx += lo_f32(qv[0]) * acc[h][tb][0] + hi_f32(qv[0]) * acc[h][tb][1] + lo_f32(qv[1]) * acc[h][tb][2] +
+                      hi_f32(qv[1]) * acc[h][tb][3];
+            }
         }
         qx = sum_rows4(qx);
         if (g16 == 0) S.red[wave][tt] = qx * kQScale;
@@ -469,7 +515,7 @@ __global__ void __launch_bounds__(kBT) bwd_intra_kernel(BwdParams A) {
     float qx = 0.0f;
     if (valid) {
         const float* pp = &A.part[(st + t0 + tau) * kPartF];
-        qx = (pp[0] + pp[1]) + (pp[2] + pp[3]);
+        qx = pp[0] + pp[1];
     }
     dhn += gt * qx;
     const float wt = (act && valid) ? -(dhn * rden) * (Dt > 0.0f ? 1.0f : -1.0f) * rden : 0.0f;
@@ -835,7 +881,7 @@ hipError_t launch_big(const void* kern, const BwdParams& p, unsigned grid, hipSt
 size_t align256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
 
 struct BwdLayout {
-    size_t slots, hl, lz0, gamn, tok, part, chunk, dmp, total;
+    size_t slots, seg, hl, lz0, gamn, tok, part, chunk, dmp, total;
 };
 BwdLayout bwd_layout(int64_t S, int T) {
     const int64_t NC = (T + kBL - 1) / kBL, NC1 = NC > 0 ? NC - 1 : 0;
@@ -847,6 +893,7 @@ BwdLayout bwd_layout(int64_t S, int T) {
         return o;
     };
     L.slots = take(static_cast<size_t>(S * NC1 * kSlotFloats) * 4);
+    L.seg = take(chunk_states_workspace_bytes(static_cast<int>(S), 1, T));
     L.hl = take(static_cast<size_t>(S * NC1 * 2 * kCV) * 2);
     L.lz0 = take(static_cast<size_t>(S * kLzFloats) * 4);
     L.gamn = take(static_cast<size_t>(S * NC * kDQK) * 4);
@@ -911,11 +958,11 @@ hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t 
     p.T = T;
     p.NC = (T + kBL - 1) / kBL;
 
-    hipError_t e = launch_chunk_states(a.f, p.slots, p.hl, stream);
+    hipError_t e = launch_chunk_states(a.f, p.slots, reinterpret_cast<float*>(ws + L.seg), stream);
     if (e != hipSuccess) return e;
     const unsigned nchunks = static_cast<unsigned>(S) * p.NC;
     static std::atomic<uint64_t> r_intra{0}, r_q{0}, r_kv{0};
-    e = launch_big<DhcSmem>(reinterpret_cast<const void*>(bwd_dhc_kernel), p, nchunks * 4, stream, r_q);
+    e = launch_big<DhcSmem>(reinterpret_cast<const void*>(bwd_dhc_kernel), p, nchunks * 2, stream, r_q);
     if (e != hipSuccess) return e;
     e = launch_big<IntraSmem>(reinterpret_cast<const void*>(bwd_intra_kernel), p, nchunks, stream, r_intra);
     if (e != hipSuccess) return e;

@@ -1262,7 +1262,7 @@ local_state_kernel(LocalArgs A) {
 // (slot g R + R - 1) receives the state after local slots 0..g R + R - 1, the entry state of
 // segment g + 1; the other sub-segment slots are only read.
 __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0, const float* n0, const float* m0,
-                                                      int NS, int R, uint16_t* rowhl) {
+                                                      int NS, int R) {
     const int s = blockIdx.y;
     float* base = ws + static_cast<int64_t>(s) * NS * kSlotFloats;
     // scalar chain of entry max states (every block computes it; block 0 stores it)
@@ -1312,20 +1312,7 @@ __global__ void __launch_bounds__(256) combine_kernel(float* ws, const float* C0
                     cur.y = a * cur.y + b * loc[u].y;
                     cur.z = a * cur.z + b * loc[u].z;
                     cur.w = a * cur.w + b * loc[u].w;
-                    // (with rowhl, C goes out only as bf16 hi + lo rows; n and m stay in the slot)
-                    if (entry && (!rowhl || e4 >= kDQK * kDV / 4)) reinterpret_cast<float4*>(slot)[e4] = cur;
-                    if (entry && rowhl && e4 < kDQK * kDV / 4) {
-                        // the entry state also as bf16 hi + lo rows [d][v] (the backward pass's operand)
-                        uint16_t* hl = rowhl + (static_cast<int64_t>(s) * NS + g0 + u) * 2 * kDQK * kDV;
-                        const int d0 = 4 * (e4 / kDV), v = e4 % kDV;
-                        const float cv[4] = {cur.x, cur.y, cur.z, cur.w};
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            const uint16_t hi = f32_to_bf16(cv[j]);
-                            hl[(d0 + j) * kDV + v] = hi;
-                            hl[kDQK * kDV + (d0 + j) * kDV + v] = f32_to_bf16(cv[j] - bf16_to_f32(hi));
-                        }
-                    }
+                    if (entry) reinterpret_cast<float4*>(slot)[e4] = cur;
                 }
                 if (entry && blockIdx.x == 0 && threadIdx.x == 0) slot[kDQK * kDV + kDQK + 2] = m_new;
                 m_in = m_new;
@@ -1379,6 +1366,283 @@ hipError_t launch_local(const LocalArgs& a, int S, hipStream_t stream, bool hilo
 
 // sub-segments of a local segment: at most kLocMax tokens each
 int local_subsegments(int seg_tokens) { return (seg_tokens + kLocMax - 1) / kLocMax; }
+
+// ---- chunk-boundary states for the backward pass ------------------------------------------------
+// The backward needs the state entering every 64-token chunk.  A walk over the chunks provides it:
+// one workgroup of 8 waves per (sequence, 128-column dv tile, segment), with the accumulator layout,
+// gate phase and lazy scale of chunk_mfma_kernel<64> but the state update alone (no logits, no
+// read-out, no h): C += K^T (w e^{-s} V) and n += K^T w.  The weighted values enter the update as a
+// bf16 pair hi + lo (the products to about 2^-17, against 2^-9 for one rounding), because the
+// backward's gradients can cancel against the state.  At the top of chunk c >= 1 the workgroup writes
+// the state entering it into slot c - 1: C in the four-row interleaved layout, n at DQK DV and the
+// max state at DQK DV + DQK + 2.  Segment g >= 1 enters from the segment slots of the local pass (in
+// its hi + lo form) and the combine.
+struct WalkSmem {
+    uint16_t K[Cfg<64>::NDB][64 * Cfg<64>::QP];   // the chunk's K rows, two d blocks of 128
+    uint16_t Vw[2][kDVT * Cfg<64>::TP];           // (w e^{-s} V)^T of the chunk as bf16 hi [0] and lo [1]
+    float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
+    GateBuf<64> G[2];                              // by chunk parity
+};
+static_assert(sizeof(WalkSmem) <= 160 * 1024, "LDS budget");
+
+struct WalkArgs {
+    const uint16_t* k;
+    const uint16_t* v;
+    const float* ipre;
+    const float* fpre;
+    const float* C0;      // entry state of segment 0 (NULL: zero state, m = m0 or 0)
+    const float* n0;
+    const float* m0;
+    const float* seg;     // segment slots of the local pass and the combine (G > 1)
+    float* out;           // S (NC - 1) chunk slots
+    int S;
+    int T;
+    int G;                // segments per sequence
+    int R;                // local sub-segments per segment; segment g >= 1 enters from slot g R - 1
+    int NS;               // segment slots per sequence, (G - 1) R
+    int seg_chunks;       // chunks per segment (the last may be shorter)
+    uint32_t nh_magic;    // as in ChunkKernelArgs
+    int64_t sk[2], sv[2];
+    uint32_t rk, rv;
+};
+
+// the chunk's K rows, both d blocks: two 16-byte pieces per thread and block
+constexpr int kWalkKP = 64 * (Cfg<64>::DB / 8) / kThreads;
+__device__ __forceinline__ void walk_load_k(u32x4_t (&r)[Cfg<64>::NDB][kWalkKP], const SeqRsrc& R, int t0, int tid,
+                                            uint32_t rk) {
+    constexpr int PR = Cfg<64>::DB / 8;
+#pragma unroll
+    for (int p = 0; p < Cfg<64>::NDB; ++p)
+#pragma unroll
+        for (int i = 0; i < kWalkKP; ++i) {
+            const int item = tid + i * kThreads;
+            r[p][i] = bload128(R.k, static_cast<uint32_t>(t0 + item / PR) * rk + 16 * (item % PR), p * Cfg<64>::DB * 2);
+        }
+}
+__device__ __forceinline__ void walk_store_k(WalkSmem& S, const u32x4_t (&r)[Cfg<64>::NDB][kWalkKP], int tid) {
+    constexpr int PR = Cfg<64>::DB / 8;
+#pragma unroll
+    for (int p = 0; p < Cfg<64>::NDB; ++p)
+#pragma unroll
+        for (int i = 0; i < kWalkKP; ++i) {
+            const int item = tid + i * kThreads;
+            const int off = (item / PR) * Cfg<64>::QP + 8 * (item % PR);
+            MLSTM_CHECK(off + 8 <= 64 * Cfg<64>::QP, kDbgChunkMfma);
+            *reinterpret_cast<u32x4_t*>(&S.K[p][off]) = r[p][i];
+        }
+}
+// (w V)^T from the packed V^T as a bf16 pair: hi = bf16(w v), lo = bf16(w v - hi)
+__device__ __forceinline__ void vt_store_hilo(WalkSmem& S, const VtPacked<64>& pv, const float* wC, int wave, int lane) {
+    constexpr int TP = Cfg<64>::TP, NA = 64 / 16;
+    const int l16 = lane & 15, g16 = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < VRegs<64>::N * VRegs<64>::PARTS; ++i) {
+        const int pc = wave + kWaves * i, a = pc % NA, b = pc / NA;
+        const int tau = 16 * a + 4 * g16;
+        const f32x4_t w = *reinterpret_cast<const f32x4_t*>(&wC[tau]);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const u32x2_t x = pv[2 * i + h];
+            const float f0 = lo_f32(x[0]) * w[0], f1 = hi_f32(x[0]) * w[1];
+            const float f2 = lo_f32(x[1]) * w[2], f3 = hi_f32(x[1]) * w[3];
+            u32x2_t oh, ol;
+            oh[0] = pack_bf16x2(f0, f1);
+            oh[1] = pack_bf16x2(f2, f3);
+            ol[0] = pack_bf16x2(f0 - lo_f32(oh[0]), f1 - hi_f32(oh[0]));
+            ol[1] = pack_bf16x2(f2 - lo_f32(oh[1]), f3 - hi_f32(oh[1]));
+            const int row = 32 * b + 16 * h + l16;
+            MLSTM_CHECK(row < kDVT && tau + 4 <= TP, kDbgChunkMfma);
+            *reinterpret_cast<u32x2_t*>(&S.Vw[0][row * TP + tau]) = oh;
+            *reinterpret_cast<u32x2_t*>(&S.Vw[1][row * TP + tau]) = ol;
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kThreads, 1) chunk_states_kernel(WalkArgs A) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+    WalkSmem& S = *reinterpret_cast<WalkSmem*>(smem_raw);
+    constexpr int L = 64;
+    using CF = Cfg<64>;
+    constexpr int QP = CF::QP, TP = CF::TP, DB = CF::DB, NDB = CF::NDB, DH = CF::DH, VT = CF::VT, NVG = CF::NVG;
+    constexpr int NQ = CF::DT / DH;   // this wave's 16-row C tiles per d block
+    constexpr int NKS = L / 32;
+    static_assert(DB / 16 == kWaves, "one n-update tile per wave and d block");
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g16 = lane >> 4, l16 = lane & 15;
+    const int vg = wave % NVG, dh = wave / NVG;
+    auto vcol = [&](int vt) { return 16 * (vg * VT + vt); };
+    // d row of element j of accumulator tile t: the layout of chunk_mfma_kernel<64>
+    auto cdrow = [&](int t, int j) {
+        const int q = t % NQ;
+        return (t / NQ) * DB + 32 * ((q / 2) * DH + dh) + 8 * g16 + 4 * (q % 2) + j;
+    };
+    const bool gate_wave = (wave == kGateWave);
+
+    const int wi = work_index();
+    const int tile = wi % kNTile;
+    const int sg = wi / kNTile;
+    const int g = sg % A.G;
+    const int s = sg / A.G;
+    const int v0 = tile * kDVT;
+    const int nc_total = (A.T + L - 1) / L;
+    const int c_begin = g * A.seg_chunks;
+    const int c_end = min(nc_total, c_begin + A.seg_chunks);
+    MLSTM_CHECK(s < A.S, kDbgChunkMfma);
+
+    SeqRsrc P;
+    P.k = make_rsrc(seq_rows(A.k, s, A.nh_magic, A.sk), seq_span(A.T, A.rk, kDQK));
+    P.v = make_rsrc(seq_rows(A.v, s, A.nh_magic, A.sv), seq_span(A.T, A.rv, kDV));
+    P.ig = make_rsrc(A.ipre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
+    P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
+
+    // entry state into the accumulators
+    f32x4_t Cacc[NDB * NQ][VT];
+    const float* nin;
+    float m_prev;
+    if (g == 0) {
+        const float* C0 = A.C0 ? A.C0 + static_cast<int64_t>(s) * kDQK * kDV : nullptr;
+#pragma unroll
+        for (int t = 0; t < NDB * NQ; ++t)
+#pragma unroll
+            for (int vt = 0; vt < VT; ++vt)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    Cacc[t][vt][j] = C0 ? C0[static_cast<int64_t>(cdrow(t, j)) * kDV + v0 + vcol(vt) + l16] : 0.0f;
+        nin = A.n0 ? A.n0 + static_cast<int64_t>(s) * kDQK : nullptr;
+        m_prev = A.m0 ? A.m0[s] : 0.0f;
+    } else {
+        MLSTM_CHECK(g * A.R - 1 >= 0 && g * A.R - 1 < A.NS, kDbgChunkMfma);
+        const float* slot = A.seg + (static_cast<int64_t>(s) * A.NS + g * A.R - 1) * kSlotFloats;
+#pragma unroll
+        for (int t = 0; t < NDB * NQ; ++t)
+#pragma unroll
+            for (int vt = 0; vt < VT; ++vt)
+                Cacc[t][vt] = *reinterpret_cast<const f32x4_t*>(slot + slot_c4(cdrow(t, 0) / 4, v0 + vcol(vt) + l16));
+        nin = slot + kDQK * kDV;
+        m_prev = slot[kDQK * kDV + kDQK + 2];
+    }
+    if (tid < kDQK) S.n[0][tid] = nin ? nin[tid] : 0.0f;
+    float s_off = 0.0f;   // C = C_acc e^{s_off}
+    float g_m = m_prev, g_s = 0.0f;
+    float gi[2] = {0.f, 0.f}, gf[2] = {0.f, 0.f};
+
+    u32x4_t rk[NDB][kWalkKP];
+    VRegs<64> rv;
+    VtPacked<64> pv;
+    if (c_begin < c_end) {
+        const int t0 = c_begin * L;
+        walk_load_k(rk, P, t0, tid, A.rk);
+        load_v_tr<64>(rv, P, t0, v0, wave, lane, 0, A.rv);
+        if (gate_wave) {
+            load_gates<64>(gi, gf, P, t0, lane);
+            gate_phase<64>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane, A.T - t0);
+        }
+    }
+
+    for (int c = c_begin; c < c_end; ++c) {
+        const int t0 = c * L;
+        const int cur = (c - c_begin) & 1;
+        const int par = c & 1;
+        const GateBuf<64>& Gc = S.G[par];
+        __syncthreads();   // the previous chunk's update is done; this chunk's gates and n are visible
+        walk_store_k(S, rk, tid);
+        vt_transpose<64>(pv, rv, lane, 0);
+        vt_store_hilo(S, pv, Gc.wC, wave, lane);
+        if (c + 1 < c_end) {
+            walk_load_k(rk, P, t0 + L, tid, A.rk);
+            load_v_tr<64>(rv, P, t0 + L, v0, wave, lane, 0, A.rv);
+            if (gate_wave) load_gates<64>(gi, gf, P, t0 + L, lane);
+        }
+        if (c > 0) {
+            // the state entering chunk c
+            MLSTM_CHECK(c - 1 < nc_total - 1, kDbgChunkMfma);
+            float* slot = A.out + (static_cast<int64_t>(s) * (nc_total - 1) + c - 1) * kSlotFloats;
+            const float esc = expf(s_off);
+#pragma unroll
+            for (int t = 0; t < NDB * NQ; ++t)
+#pragma unroll
+                for (int vt = 0; vt < VT; ++vt)
+                    *reinterpret_cast<f32x4_t*>(slot + slot_c4(cdrow(t, 0) / 4, v0 + vcol(vt) + l16)) = Cacc[t][vt] * esc;
+            if (tile == 0 && tid < kDQK) slot[kDQK * kDV + tid] = S.n[cur][tid];
+            if (tile == 0 && tid == 0) slot[kDQK * kDV + kDQK + 2] = m_prev;
+        }
+        __syncthreads();   // the chunk's K rows and weighted V^T are visible
+        // gates of the next chunk, one chunk ahead
+        if (gate_wave && c + 1 < c_end) gate_phase<64>(S.G[par ^ 1], gi, gf, g_m, g_s, lane, A.T - (t0 + L));
+
+        const float decay_n = Gc.scal[0];
+        const float m_next = Gc.scal[1];
+        const float s_new = Gc.scal[2];
+        const float c_scale = Gc.scal[3];   // != 1: apply this chunk's decay to C_acc eagerly
+        if (c_scale != 1.0f) {
+#pragma unroll
+            for (int t = 0; t < NDB * NQ; ++t)
+#pragma unroll
+                for (int vt = 0; vt < VT; ++vt) Cacc[t][vt] *= c_scale;
+        }
+        const int tr_row = (l16 >> 2) + 8 * g16;
+        const int tr_col = 4 * (l16 & 3);
+        const float* n_old = S.n[cur];
+        float* n_new = S.n[cur ^ 1];
+#pragma unroll
+        for (int p = 0; p < NDB; ++p) {
+            const uint16_t* Ks = S.K[p];
+            // C_p += K_p^T (w e^{-s} V) (hi, then lo): A = K read transposed, B = the weighted V^T rows
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+                u32x4_t a[NQ];
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * ((q / 2) * DH + dh) + 2 * tr_col + 4 * (q % 2)];
+                    a[q] = cat(tr_read(kb), tr_read(kb + 4 * QP));
+                }
+                u32x4_t vh[VT], vl[VT];
+#pragma unroll
+                for (int vt = 0; vt < VT; ++vt) {
+                    const int off = (vcol(vt) + l16) * TP + 32 * ks + 8 * g16;
+                    vh[vt] = *reinterpret_cast<const u32x4_t*>(&S.Vw[0][off]);
+                    vl[vt] = *reinterpret_cast<const u32x4_t*>(&S.Vw[1][off]);
+                }
+#pragma unroll
+                for (int q = 0; q < NQ; ++q)
+#pragma unroll
+                    for (int vt = 0; vt < VT; ++vt) {
+                        Cacc[p * NQ + q][vt] = mfma16(a[q], vh[vt], Cacc[p * NQ + q][vt]);
+                        Cacc[p * NQ + q][vt] = mfma16(a[q], vl[vt], Cacc[p * NQ + q][vt]);
+                    }
+            }
+            // n_p = decay n_p + K_p^T w over this wave's 16 columns of the block: A = w as bf16 hi / lo
+            // rows, B = K read transposed
+            f32x4_t nacc = f32x4_t{};
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+                const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&Gc.wb[l16 & 1][32 * ks + 8 * g16])
+                                             : u32x4_t{0u, 0u, 0u, 0u};
+                const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * wave + tr_col];
+                nacc = mfma16(wa, cat(tr_read(kb), tr_read(kb + 4 * QP)), nacc);
+            }
+            if (g16 == 0) {
+                const int d = p * DB + 16 * wave + l16;
+                n_new[d] = decay_n * n_old[d] + nacc[0] + nacc[1];
+            }
+        }
+        s_off = s_new;
+        m_prev = m_next;
+    }
+}
+
+hipError_t launch_walk(const WalkArgs& a, hipStream_t stream) {
+    const size_t lds = sizeof(WalkSmem);
+    static std::atomic<uint64_t> raised{0};
+    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(chunk_states_kernel), lds, raised);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(chunk_states_kernel, dim3(static_cast<unsigned>(a.S * a.G * kNTile)), dim3(kThreads), lds, stream,
+                       a);
+    return hipGetLastError();
+}
 
 }  // namespace
 
@@ -1458,7 +1722,7 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
         if (e != hipSuccess) return e;
         constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
         hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, k.ws, a.C0, a.n0, a.m0,
-                           k.NS, R, static_cast<uint16_t*>(nullptr));
+                           k.NS, R);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -1466,32 +1730,59 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
 }
 
 // ---- chunk-boundary states for the backward pass -----------------------------------------------
-// The state entering every chunk c >= 1 of 64 tokens: the local pass over one-chunk sub-segments
-// (its closed form from an empty state, in the bf16 hi + lo form) and the combine scan, which leaves in slot c - 1 the fp32
-// state (C in the four-row interleaved layout, n, and the entry max state m_in) and writes C as bf16
-// hi + lo rows into rowhl.  ``slots`` holds S (NC - 1) slots, ``rowhl`` S (NC - 1) x 2 x DQK x DV.
-hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, uint16_t* rowhl, hipStream_t stream) {
+// The state entering every chunk c >= 1 of 64 tokens, into slot c - 1 of ``slots`` (S (NC - 1) slots:
+// fp32 C in the four-row interleaved layout, n, and the entry max state): the segment schedule of the
+// prefill (local pass in the bf16 hi + lo form, combine) for the segments' entry states, then the walk.
+size_t chunk_states_workspace_bytes(int B, int NH, int T) {
+    return chunk_mfma_workspace_bytes(B, NH, T, kDQK, kDV, 64);
+}
+
+hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, float* seg, hipStream_t stream) {
     const int S = a.B * a.NH;
     const int nc = (a.T + 63) / 64;
     if (nc <= 1) return hipSuccess;
-    LocalArgs la{};
-    la.k = static_cast<const uint16_t*>(a.k);
-    la.v = static_cast<const uint16_t*>(a.v);
-    set_strides(a, la.nh_magic, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
-    la.ipre = a.ipre;
-    la.fpre = a.fpre;
-    la.ws = slots;
-    la.S = S;
-    la.T = a.T;
-    la.NS = nc - 1;
-    la.R = 1;
-    la.seg_tokens = 64;
-    hipError_t e = launch_local(la, S, stream, true);
-    if (e != hipSuccess) return e;
-    constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
-    hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, slots, a.C0, a.n0, a.m0, nc - 1,
-                       1, rowhl);
-    return hipGetLastError();
+    const int G = seg ? chunk_mfma_segments(a.B, a.NH, a.T, 64) : 1;
+    const int seg_chunks = G > 1 ? (nc + G - 1) / G : nc;
+    const int R = G > 1 ? local_subsegments(seg_chunks * 64) : 1;
+    WalkArgs w{};
+    w.k = static_cast<const uint16_t*>(a.k);
+    w.v = static_cast<const uint16_t*>(a.v);
+    set_strides(a, w.nh_magic, nullptr, w.sk, w.sv, nullptr, &w.rk, &w.rv);
+    w.ipre = a.ipre;
+    w.fpre = a.fpre;
+    w.C0 = a.C0;
+    w.n0 = a.n0;
+    w.m0 = a.m0;
+    w.seg = seg;
+    w.out = slots;
+    w.S = S;
+    w.T = a.T;
+    w.G = G;
+    w.R = R;
+    w.NS = (G - 1) * R;
+    w.seg_chunks = seg_chunks;
+    if (G > 1) {
+        LocalArgs la{};
+        la.k = w.k;
+        la.v = w.v;
+        set_strides(a, la.nh_magic, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
+        la.ipre = a.ipre;
+        la.fpre = a.fpre;
+        la.ws = seg;
+        la.S = S;
+        la.T = a.T;
+        la.NS = w.NS;
+        la.R = R;
+        la.seg_tokens = seg_chunks * 64;
+        hipError_t e = launch_local(la, S, stream, true);
+        if (e != hipSuccess) return e;
+        constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
+        hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, seg, a.C0, a.n0, a.m0, w.NS,
+                           R);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return launch_walk(w, stream);
 }
 
 // ---- fixed scratch for callers that cannot allocate ---------------------------------------------

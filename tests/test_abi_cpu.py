@@ -50,11 +50,12 @@ def test_default_build_reports_no_debug_checks():
 @pytest.mark.skipif(not os.path.exists(os.path.join(ROOT, "paper_2503_13427_amd", "libmlstm_debug.so")),
                     reason="libmlstm_debug.so is not built")
 def test_debug_build_exports_every_declared_symbol():
-    dbg = ctypes.CDLL(os.path.join(ROOT, "paper_2503_13427_amd", "libmlstm_debug.so"))
+    path = os.path.join(ROOT, "paper_2503_13427_amd", "libmlstm_debug.so")
+    dbg = ctypes.CDLL(path)
+    out = os.popen(f"nm -D --defined-only {path}").read()
     for name in declared_functions():
         assert hasattr(dbg, name), name
-    out = os.popen(f"nm -D --defined-only {Bd.LIB_PATH}").read()
-    assert re.search(rf"\bT {name}$", out, flags=re.M), name
+        assert re.search(rf"\bT {name}$", out, flags=re.M), name
 
 
 def test_status_strings_and_version():
@@ -533,13 +534,15 @@ def call_cbwd(a):
 
 
 def test_chunk_bwd_workspace_size():
-    """Entry states (fp32 slot and bf16 hi + lo rows) of every chunk but the first, L_0, gam per chunk,
-    per-token key weights and partial sums, per-chunk decays, dm0 partial sums; each region 256-byte
-    aligned."""
+    """Entry states (fp32 slots) of every chunk but the first; the segment slots of the state walk
+    (32 sequence-tile workgroups per segment, so eight segments of four chunks: seven segment slots
+    per sequence); Gam_c as bf16 hi + lo rows; L_0, gam per chunk, per-token key weights and partial
+    sums, per-chunk decays, dm0 partial sums; each region 256-byte aligned."""
     al = lambda b: (b + 255) // 256 * 256
     S, T, NC = 8, 2048, 32
     slot = 256 * 512 + 256 + 4
-    want = (al(S * (NC - 1) * slot * 4) + al(S * (NC - 1) * 2 * 256 * 512 * 2) + al(S * (256 * 512 + 256) * 4)
+    want = (al(S * (NC - 1) * slot * 4) + al(S * 7 * slot * 4) + al(S * (NC - 1) * 2 * 256 * 512 * 2)
+            + al(S * (256 * 512 + 256) * 4)
             + al(S * NC * 256 * 4) + al(S * T * 4) + al(S * T * 32) + al(S * NC * 4) + al(S * 129 * 4))
     assert Bd.mlstm_chunkwise_bwd_workspace_bytes(1, 8, T, 256, 512, 64) == want
     assert Bd.mlstm_chunkwise_bwd_workspace_bytes(1, 8, T, 256, 512, 128) == 0

@@ -41,8 +41,7 @@
 //           term of dk and z_c; writes the key weights, the chunk's decay and q_t . dq_t
 //   scan    the reverse recurrence of (Gam, gam), elementwise over the state, writing Gam_c as
 //           bf16 hi + lo rows; dC0, dn0 and partial sums of dm0
-//   interkv one workgroup per (chunk, tile): dk of a 64-row d tile and dv of a 128-column v
-//           tile from Gam_c; the partial k . dk of the tile
+//   interkv one workgroup per chunk: the inter terms of dk and dv from Gam_c, read once; k . dk
 //   gates   one workgroup per sequence: the reverse prefix sums of r - c, di~ and df~, dm0
 //
 // MFMA mapping (16x16x32 bf16, fp32 accumulate): lane (l16, g16) holds A[m = l16][k = 8 g16 + 0..7]
@@ -679,142 +678,193 @@ __global__ void __launch_bounds__(256) bwd_scan_kernel(BwdParams A) {
 }
 
 // ---- dk and dv inter terms ---------------------------------------------------------------------
+// One workgroup of 8 waves per chunk: dk^T += Gam_c V^T (over v) and dv^T += Gam_c^T K^T (over d),
+// each complete inside the workgroup, so Gam_c is read from memory once.  It streams through LDS in
+// 16 blocks of 64 rows d x 128 columns v (hi and lo; the next block in registers), while K and V of
+// the chunk stay in LDS.  Waves 0-3 form dk: wave m owns the rows d = 64 jd + 16 m + 0..15 of every
+// block row jd; waves 4-7 form dv: wave m owns the columns v = 128 jv + 32 m + 0..31 of block column
+// jv; both cover the four tau tiles, and each runs 32 MFMAs per block.  The blocks go column by
+// column, so a dv wave finishes its columns of jv after four blocks.
+constexpr int kIKT = 512;    // threads of the inter pass
 struct InterKVSmem {
-    uint16_t G[2][kBL * kWP];   // 64 rows d x 128 columns v of Gam_c, hi and lo
+    uint16_t K[kBL * kQP];     // the chunk's K rows
+    uint16_t V[kBL * kHP];     // the chunk's V rows
+    uint16_t G[2][64 * kWP];   // one block of Gam_c: hi, lo
     float wk[kBL];
-    float red[4][kBL];
+    float gam[kDQK];
+    float red[4][kBL];         // k . dk partials of the dk waves
 };
 static_assert(sizeof(InterKVSmem) <= 160 * 1024, "LDS budget");
 
-__global__ void __launch_bounds__(kBT) bwd_interkv_kernel(BwdParams A) {
+__global__ void __launch_bounds__(kIKT) bwd_interkv_kernel(BwdParams A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     InterKVSmem& S = *reinterpret_cast<InterKVSmem*>(smem_raw);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g16 = lane >> 4, l16 = lane & 15;
-    const int wi = work_index();
-    const int j = wi % 4, c = (wi / 4) % A.NC, s = wi / 4 / A.NC;
-    const int T = A.T, t0 = c * kBL, d0 = 64 * j, v0 = 128 * j;
+    const int c = blockIdx.x % A.NC, s = blockIdx.x / A.NC;
+    const int T = A.T, t0 = c * kBL;
     const int64_t st = static_cast<int64_t>(s) * T;
-    const auto rk = make_rsrc(A.k + st * kDQK, static_cast<uint32_t>(T) * kDQK * 2);
-    const auto rv = make_rsrc(A.v + st * kDV, static_cast<uint32_t>(T) * kDV * 2);
     const bool has_g = c < A.NC - 1;   // the last chunk's exit state receives no gradient
+    const bool dk_role = wave < 4;
+    const int m = wave & 3;
 
     if (tid < kBL) S.wk[tid] = (t0 + tid < T) ? A.tok[(st + t0 + tid) * kTokF] : 0.0f;
-    __syncthreads();
-
-    // dk^T [d][tau] += wk_tau (sum_v Gam[d][v] V[tau][v] + gam[d]); rows d = d0 + 16 wave + l16
-    {
-        f32x4_t acc[4];
+    const uint16_t* gbase = has_g ? hl_of(A, s, c) : nullptr;
+    // this thread's two 16-byte pieces of a Gam block (rows e / 16, columns 8 (e % 16) + 0..7)
+    u32x4_t gh[2], gl[2];
+    auto gload = [&](int jd, int jv) {
 #pragma unroll
-        for (int tb = 0; tb < 4; ++tb) acc[tb] = f32x4_t{};
-        if (has_g) {
-            const uint16_t* hi = hl_of(A, s, c) + static_cast<int64_t>(d0 + 16 * wave + l16) * kDV + 8 * g16;
-            const uint16_t* lo = hi + kCV;
-            // V rows (B operands) straight from memory, shared by the chunk's four tiles in L2; the LDS
-            // then holds only the Gam block, so several workgroups share a CU
-#pragma unroll 2
-            for (int ks = 0; ks < kDV / 32; ++ks) {
-                const u32x4_t ah = *reinterpret_cast<const u32x4_t*>(hi + 32 * ks);
-                const u32x4_t al = *reinterpret_cast<const u32x4_t*>(lo + 32 * ks);
-                u32x4_t b[4];
-#pragma unroll
-                for (int tb = 0; tb < 4; ++tb)
-                    b[tb] = bload128(rv, static_cast<uint32_t>((t0 + 16 * tb + l16) * kDV + 32 * ks + 8 * g16) * 2u, 0);
-#pragma unroll
-                for (int tb = 0; tb < 4; ++tb) {
-                    acc[tb] = mfma16(ah, b[tb], acc[tb]);
-                    acc[tb] = mfma16(al, b[tb], acc[tb]);
-                }
-            }
+        for (int i = 0; i < 2; ++i) {
+            const int e = tid + kIKT * i;
+            const uint16_t* p = gbase + static_cast<int64_t>(64 * jd + (e >> 4)) * kDV + 128 * jv + 8 * (e & 15);
+            gh[i] = *reinterpret_cast<const u32x4_t*>(p);
+            gl[i] = *reinterpret_cast<const u32x4_t*>(p + kCV);
         }
-        const int d = d0 + 16 * wave + 4 * g16;
-        f32x4_t gam = f32x4_t{};
-        if (has_g) gam = *reinterpret_cast<const f32x4_t*>(&A.gamn[(static_cast<int64_t>(s) * A.NC + c) * kDQK + d]);
-#pragma unroll
-        for (int tb = 0; tb < 4; ++tb) {
-            const int tt = 16 * tb + l16;
-            float cp = 0.0f;
-            if (t0 + tt < T) {
-                float* dkp = &A.dk[(st + t0 + tt) * kDQK + d];
-                f32x4_t o = *reinterpret_cast<const f32x4_t*>(dkp);
-                if (has_g) {
-                    const float w = S.wk[tt];
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) o[r] += w * (acc[tb][r] + gam[r]);
-                    *reinterpret_cast<f32x4_t*>(dkp) = o;
-                }
-                const u32x2_t kv = *reinterpret_cast<const u32x2_t*>(&A.k[(st + t0 + tt) * kDQK + d]);
-                cp = lo_f32(kv[0]) * o[0] + hi_f32(kv[0]) * o[1] + lo_f32(kv[1]) * o[2] + hi_f32(kv[1]) * o[3];
-            }
-            cp = sum_rows4(cp);
-            if (g16 == 0) S.red[wave][tt] = cp;
-        }
-    }
-    // dv^T [v][tau] += wk_tau sum_d Gam^T[v][d] K[tau][d]; this wave: v = v0 + 16 (2 wave + vb) + ...
+    };
     if (has_g) {
-        f32x4_t acc[2][4];
+        gload(0, 0);
+        const auto rk = make_rsrc(A.k + st * kDQK, static_cast<uint32_t>(T) * kDQK * 2);
+        const auto rv = make_rsrc(A.v + st * kDV, static_cast<uint32_t>(T) * kDV * 2);
 #pragma unroll
-        for (int vb = 0; vb < 2; ++vb)
+        for (int h = 0; h < 2; ++h) {   // two rounds, so that fewer staging registers are live
+            u32x4_t tk[2], tv[4];
 #pragma unroll
-            for (int tb = 0; tb < 4; ++tb) acc[vb][tb] = f32x4_t{};
-        const uint16_t* ghi = hl_of(A, s, c);
-        for (int db = 0; db < kDQK / 64; ++db) {
-            __syncthreads();   // the previous block is consumed
-            // rows 64 db .. 64 db + 63, columns v0 .. v0 + 127 of Gam (hi, lo): 2 x 1024 pieces
-#pragma unroll
-            for (int part = 0; part < 2; ++part) {
-                u32x4_t tmp[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int e = tid + kBT * i, row = e / 16, pc = e % 16;
-                    tmp[i] = *reinterpret_cast<const u32x4_t*>(ghi + part * kCV + static_cast<int64_t>(64 * db + row) * kDV +
-                                                             v0 + 8 * pc);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int e = tid + kBT * i, row = e / 16, pc = e % 16;
-                    *reinterpret_cast<u32x4_t*>(&S.G[part][row * kWP + 8 * pc]) = tmp[i];
-                }
+            for (int i = 0; i < 2; ++i) {
+                const int e = tid + kIKT * (2 * h + i), row = e >> 5, pc = e & 31;
+                tk[i] = bload128(rk, static_cast<uint32_t>((t0 + row) * kDQK + 8 * pc) * 2u, 0);
             }
-            __syncthreads();
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                u32x4_t bk[4];
+            for (int i = 0; i < 4; ++i) {
+                const int e = tid + kIKT * (4 * h + i), row = e >> 6, pc = e & 63;
+                tv[i] = bload128(rv, static_cast<uint32_t>((t0 + row) * kDV + 8 * pc) * 2u, 0);
+            }
 #pragma unroll
-                for (int tb = 0; tb < 4; ++tb)
-                    bk[tb] = bload128(rk, static_cast<uint32_t>((t0 + 16 * tb + l16) * kDQK + 64 * db + 32 * ks + 8 * g16) * 2u, 0);
+            for (int i = 0; i < 2; ++i) {
+                const int e = tid + kIKT * (2 * h + i), row = e >> 5, pc = e & 31;
+                *reinterpret_cast<u32x4_t*>(&S.K[row * kQP + 8 * pc]) = tk[i];
+            }
 #pragma unroll
-                for (int vb = 0; vb < 2; ++vb) {
-                    const int vl = 16 * (2 * wave + vb);
-                    const u32x4_t ah = tr_op(S.G[0], kWP, 32 * ks, vl, lane);
-                    const u32x4_t al = tr_op(S.G[1], kWP, 32 * ks, vl, lane);
+            for (int i = 0; i < 4; ++i) {
+                const int e = tid + kIKT * (4 * h + i), row = e >> 6, pc = e & 63;
+                *reinterpret_cast<u32x4_t*>(&S.V[row * kHP + 8 * pc]) = tv[i];
+            }
+        }
+        if (tid < kDQK) S.gam[tid] = A.gamn[(static_cast<int64_t>(s) * A.NC + c) * kDQK + tid];
+    }
+
+    // dk waves: acc[4 jd + t] (tau tile t); dv waves: acc[4 e + t] (columns 32 m + 16 e of the current
+    // block column, tau tile t)
+    f32x4_t acc[16];
 #pragma unroll
-                    for (int tb = 0; tb < 4; ++tb) {
-                        acc[vb][tb] = mfma16(ah, bk[tb], acc[vb][tb]);
-                        acc[vb][tb] = mfma16(al, bk[tb], acc[vb][tb]);
+    for (int i = 0; i < 16; ++i) acc[i] = f32x4_t{};
+    if (has_g) {
+#pragma unroll 1
+        for (int jv = 0; jv < 4; ++jv) {
+#pragma unroll
+            for (int jd = 0; jd < 4; ++jd) {
+                __syncthreads();   // the previous block is consumed (first: K, V, wk, gam staged)
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const int e = tid + kIKT * i;
+                    *reinterpret_cast<u32x4_t*>(&S.G[0][(e >> 4) * kWP + 8 * (e & 15)]) = gh[i];
+                    *reinterpret_cast<u32x4_t*>(&S.G[1][(e >> 4) * kWP + 8 * (e & 15)]) = gl[i];
+                }
+                if (jd < 3) gload(jd + 1, jv);
+                else if (jv < 3) gload(0, jv + 1);
+                __syncthreads();
+                if (dk_role) {
+                    // dk^T [d][tau] += sum_v Gam[d][v] V[tau][v]: A = Gam rows, B = V rows
+#pragma unroll
+                    for (int ks = 0; ks < 4; ++ks) {
+                        const u32x4_t ah = row_op(S.G[0], kWP, 16 * m, 32 * ks, lane);
+                        const u32x4_t al = row_op(S.G[1], kWP, 16 * m, 32 * ks, lane);
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            const u32x4_t b = row_op(S.V, kHP, 16 * t, 128 * jv + 32 * ks, lane);
+                            acc[4 * jd + t] = mfma16(ah, b, acc[4 * jd + t]);
+                            acc[4 * jd + t] = mfma16(al, b, acc[4 * jd + t]);
+                        }
+                    }
+                } else {
+                    // dv^T [v][tau] += sum_d Gam[d][v] K[tau][d]: A = Gam read transposed, B = K rows
+#pragma unroll
+                    for (int ks = 0; ks < 2; ++ks) {
+                        u32x4_t ah[2], al[2];
+#pragma unroll
+                        for (int e = 0; e < 2; ++e) {
+                            ah[e] = tr_op(S.G[0], kWP, 32 * ks, 32 * m + 16 * e, lane);
+                            al[e] = tr_op(S.G[1], kWP, 32 * ks, 32 * m + 16 * e, lane);
+                        }
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            const u32x4_t b = row_op(S.K, kQP, 16 * t, 64 * jd + 32 * ks, lane);
+#pragma unroll
+                            for (int e = 0; e < 2; ++e) {
+                                acc[4 * e + t] = mfma16(ah[e], b, acc[4 * e + t]);
+                                acc[4 * e + t] = mfma16(al[e], b, acc[4 * e + t]);
+                            }
+                        }
                     }
                 }
             }
+            if (!dk_role) {
+                // dv of this wave's columns of block column jv: dv += wk (Gam^T K^T)^T
+#pragma unroll
+                for (int e = 0; e < 2; ++e)
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const int tt = 16 * t + l16;
+                        if (t0 + tt < T) {
+                            float* dvp = &A.dv[(st + t0 + tt) * kDV + 128 * jv + 32 * m + 16 * e + 4 * g16];
+                            f32x4_t o = *reinterpret_cast<const f32x4_t*>(dvp);
+                            o += S.wk[tt] * acc[4 * e + t];
+                            *reinterpret_cast<f32x4_t*>(dvp) = o;
+                        }
+                        acc[4 * e + t] = f32x4_t{};
+                    }
+            }
         }
+    } else {
+        __syncthreads();   // wk staged
+    }
+    if (dk_role) {
+        // dk += wk (Gam V^T + gam), then this wave's share of k . dk
+        float cp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int vb = 0; vb < 2; ++vb)
+        for (int jd = 0; jd < 4; ++jd) {
+            const int d = 64 * jd + 16 * m + 4 * g16;
 #pragma unroll
-            for (int tb = 0; tb < 4; ++tb) {
-                const int tt = 16 * tb + l16;
+            for (int t = 0; t < 4; ++t) {
+                const int tt = 16 * t + l16;
                 if (t0 + tt < T) {
-                    float* dvp = &A.dv[(st + t0 + tt) * kDV + v0 + 16 * (2 * wave + vb) + 4 * g16];
-                    f32x4_t o = *reinterpret_cast<const f32x4_t*>(dvp);
-                    const float w = S.wk[tt];
+                    float* dkp = &A.dk[(st + t0 + tt) * kDQK + d];
+                    f32x4_t o = *reinterpret_cast<const f32x4_t*>(dkp);
+                    if (has_g) {
+                        const float w = S.wk[tt];
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) o[r] += w * acc[vb][tb][r];
-                    *reinterpret_cast<f32x4_t*>(dvp) = o;
+                        for (int r = 0; r < 4; ++r) o[r] += w * (acc[4 * jd + t][r] + S.gam[d + r]);
+                        *reinterpret_cast<f32x4_t*>(dkp) = o;
+                    }
+                    const u32x2_t kv = *reinterpret_cast<const u32x2_t*>(&A.k[(st + t0 + tt) * kDQK + d]);
+                    cp[t] += lo_f32(kv[0]) * o[0] + hi_f32(kv[0]) * o[1] + lo_f32(kv[1]) * o[2] + hi_f32(kv[1]) * o[3];
                 }
             }
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const float v = sum_rows4(cp[t]);
+            if (g16 == 0) S.red[m][16 * t + l16] = v;
+        }
     }
     __syncthreads();
-    if (tid < kBL && t0 + tid < T)
-        A.part[(st + t0 + tid) * kPartF + 4 + j] = S.red[0][tid] + S.red[1][tid] + S.red[2][tid] + S.red[3][tid];
+    if (tid < kBL && t0 + tid < T) {
+        float* pp = &A.part[(st + t0 + tid) * kPartF + 4];
+        pp[0] = (S.red[0][tid] + S.red[1][tid]) + (S.red[2][tid] + S.red[3][tid]);
+        pp[1] = 0.0f;
+        pp[2] = 0.0f;
+        pp[3] = 0.0f;
+    }
 }
 
 // ---- gate gradients ----------------------------------------------------------------------------
@@ -870,12 +920,12 @@ __global__ void __launch_bounds__(256) bwd_zero_state_kernel(float* dC0, float* 
 
 template <class Smem>
 hipError_t launch_big(const void* kern, const BwdParams& p, unsigned grid, hipStream_t stream,
-                      std::atomic<uint64_t>& raised) {
+                      std::atomic<uint64_t>& raised, int threads = kBT) {
     const size_t lds = sizeof(Smem);
     hipError_t e = raise_dynamic_lds(kern, lds, raised);
     if (e != hipSuccess) return e;
     void* args[] = {const_cast<BwdParams*>(&p)};
-    return hipLaunchKernel(kern, dim3(grid), dim3(kBT), args, lds, stream);
+    return hipLaunchKernel(kern, dim3(grid), dim3(threads), args, lds, stream);
 }
 
 size_t align256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
@@ -969,7 +1019,7 @@ hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t 
     hipLaunchKernelGGL(bwd_scan_kernel, dim3(kScanBlocks, S), dim3(256), 0, stream, p);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = launch_big<InterKVSmem>(reinterpret_cast<const void*>(bwd_interkv_kernel), p, nchunks * 4, stream, r_kv);
+    e = launch_big<InterKVSmem>(reinterpret_cast<const void*>(bwd_interkv_kernel), p, nchunks, stream, r_kv, kIKT);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bwd_gate_kernel, dim3(S), dim3(256), 0, stream, p);
     return hipGetLastError();

@@ -93,10 +93,13 @@ bool chunk_mfma_supported(mlstm_dtype dt, int DQK, int DV, int L);
 int chunk_mfma_segments(int B, int NH, int T, int L);
 size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L);
 hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream);
-// State entering every 64-token chunk c >= 1 (slots: S (NC - 1) slots, fp32 C in the four-row
-// interleaved layout, n and m); seg: chunk_states_workspace_bytes of segment slots (NULL: one segment)
-size_t chunk_states_workspace_bytes(int B, int NH, int T);
-hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, float* seg, hipStream_t stream);
+// The backward's walk over 64-token chunks: X (kNTile x [S, T, DQK]) receives each dv tile's partial
+// sum of X^T = C dH^T on the state entering the token's chunk, part[t * part_stride + tile] its
+// q^ . X share, and slot c - 1 of ``slots`` (S (NC - 1) slots) n and m entering chunk c >= 1; seg:
+// bwd_walk_workspace_bytes of segment slots (NULL: one segment per sequence).
+size_t bwd_walk_workspace_bytes(int B, int NH, int T);
+hipError_t launch_bwd_walk(const ChunkArgs& a, const void* dh, float* slots, float* seg, float* X, float* part,
+                           int part_stride, hipStream_t stream);
 // --- chunkwise backward (bf16, DQK = 256, DV = 512, L = 64) --------------------
 bool chunk_bwd_supported(mlstm_dtype dt, int DQK, int DV, int L);
 size_t chunk_bwd_workspace_bytes(int B, int NH, int T);

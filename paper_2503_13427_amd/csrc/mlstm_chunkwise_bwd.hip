@@ -30,12 +30,12 @@
 // rounding of h~ would dominate the result.  The forward's output is not an input.
 //
 // Passes (one stream, in order):
-//   states  the entry state of every chunk c >= 1 (fp32 C, n, m in slot c - 1): the prefill's
-//           segment schedule (local pass in the bf16 hi + lo form, combine) for the entry states of
-//           segments of several chunks, then a walk over each segment's chunks with the state
-//           update alone, which writes each chunk's entry state
-//   dhc     one workgroup per (chunk, 128-row d tile): X = dH C^T on the entry state, split into
-//           bf16 hi + lo in registers (kept in dq), and the tile's share of q^_t . X_t
+//   walk    the prefill's segment schedule (local pass in the bf16 hi + lo form, combine) for the
+//           entry states of segments of several chunks, then a walk over each segment's chunks per
+//           dv tile, holding its slice of the state in registers: per chunk the tile's partial sum of
+//           X = dH C^T on the entry state, its share of q^_t . X_t, then the state update; n and m
+//           entering each chunk go to its slot
+//   xsum    X, the sum of the four tiles' partials, into dq
 //   intra   one workgroup per chunk: gates, S, D, den; per 128-column piece of dv, (dH V^T), the
 //           intra term of dv and the piece's columns of L_c; then w, P, dq (complete), the intra
 //           term of dk and z_c; writes the key weights, the chunk's decay and q_t . dq_t
@@ -69,7 +69,7 @@ constexpr int64_t kLzFloats = kCV + kDQK;                 // L_c then z_c
 constexpr int kScanE4 = static_cast<int>(kLzFloats / 4);  // float4 items of the reverse scan
 constexpr int kScanBlocks = (kScanE4 + 255) / 256;
 constexpr int kTokF = 1;                                  // per-token floats: the key weight
-constexpr int kPartF = 8;                                 // per-token partial sums: q^.X x 2 (then q.dq), k.dk x 4
+constexpr int kPartF = 8;                                 // per-token partial sums: q^.X x 4 (then q.dq), k.dk x 4
 
 struct BwdParams {
     const uint16_t* q;
@@ -89,7 +89,7 @@ struct BwdParams {
     float* dC0;          // NULL: not requested (with dn0, dm0)
     float* dn0;
     float* dm0;
-    float* slots;        // S (NC - 1) state slots: entry state of chunk c in slot c - 1, then L_c, z_c
+    float* slots;        // S (NC - 1) slots: n, m entering chunk c in slot c - 1, then L_c, z_c
     uint16_t* hl;        // S (NC - 1) x 2 x DQK x DV: Gam_c as bf16 hi + lo rows
     float* lz0;          // S x (DQK DV + DQK): L_0, z_0
     float* gamn;         // S x NC x DQK: gam_c
@@ -193,124 +193,12 @@ __device__ __forceinline__ void bwd_gates(__amdgpu_buffer_rsrc_t ig, __amdgpu_bu
     decay = (restart || ML == -INFINITY || m_prev == -INFINITY) ? 0.0f : fexp(m_prev - ML);
 }
 
-// ---- dH C^T: the entry state's share of dq ----------------------------------------------------
-struct DhcSmem {
-    uint16_t dH[kBL * kHP];
-    float red[4][kBL];
-};
-static_assert(sizeof(DhcSmem) <= 160 * 1024, "LDS budget");
-
-// One-hot selection E_h (32 x 16: column n has its one in row 16 h + n) in the B-operand layout: lane
-// (l16, g16) holds k slots 8 g16 + 0..7 of column l16.
-__device__ __forceinline__ u32x4_t onehot(int h, int lane) {
-    const int pos = 16 * h + (lane & 15) - 8 * (lane >> 4);
-    const uint32_t one = (pos & 1) ? 0x3F800000u : 0x3F80u;   // bf16 1.0 in the high or low half
-    u32x4_t e;
-#pragma unroll
-    for (int d = 0; d < 4; ++d) e[d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
-    return e;
-}
-__device__ __forceinline__ u32x4_t pack4x2(const f32x4_t& a, const f32x4_t& b) {
-    return u32x4_t{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
-}
-
-// One workgroup per (chunk, 128-row d tile); wave w owns rows dw = d0 + 32 w + 0..31.  X^T [d][tau] =
-// sum_v C[d][v] dH[tau][v] on the entry state, stored in dq (the intra pass scales it by g / den and
-// adds the rest), and the tile's share of q^_t . X_t.
-// The entry state is the fp32 slot (four rows interleaved: one 16-byte piece holds four consecutive
-// d of one v), split into bf16 hi + lo in registers.  The A operand of the product wants eight v of one
-// d per lane, so each 32 d x 16 v piece is transposed on the matrix cores: as the A operand of a
-// product with the one-hot E_h it gives, in lane (l16, g16), C[dw + 16 h + l16][v 4 g16 + 0..3] (exact).
-// A k step of 32 v takes two such pieces; its k slots are v = 4 g16 + 0..3 and 16 + 4 g16 + 0..3, and
-// the dH operand (two 8-byte reads of a dH row) uses the same order.
-__global__ void __launch_bounds__(kBT) bwd_dhc_kernel(BwdParams A) {
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-    DhcSmem& S = *reinterpret_cast<DhcSmem*>(smem_raw);
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int g16 = lane >> 4, l16 = lane & 15;
-    const int wi = work_index();
-    const int j = wi % 2, c = (wi / 2) % A.NC, s = wi / 2 / A.NC;
-    const int T = A.T, t0 = c * kBL, dw = 128 * j + 32 * wave;
-    const int64_t st = static_cast<int64_t>(s) * T;
-    const auto rdh = make_rsrc(A.dh + st * kDV, static_cast<uint32_t>(T) * kDV * 2);
-    const bool has_c = (c > 0) || (A.C0 != nullptr);
-
-    if (has_c) stage_rows<kDV>(S.dH, kHP, rdh, kDV, t0, 0, tid);
-    __syncthreads();
-    f32x4_t acc[2][4];   // [16-row d tile h][tau block]
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int tb = 0; tb < 4; ++tb) acc[h][tb] = f32x4_t{};
-    if (has_c) {
-        const float* slot = c > 0 ? lz_of(A, s, c) : nullptr;   // the entry state of chunk c
-        const float* c0 = A.C0 ? A.C0 + static_cast<int64_t>(s) * kCV : nullptr;
-        const u32x4_t E0 = onehot(0, lane), E1 = onehot(1, lane);
-#pragma unroll 2
-        for (int ks = 0; ks < kDV / 32; ++ks) {
-            u32x4_t ah[2], al[2];   // [h]
-            if (c > 0) {
-                // pieces u = 0, 1: lane (l16, g16) loads C[dw + 8 g16 + 0..7][32 ks + 16 u + l16]
-                f32x4_t th[2][2], tl[2][2];   // [u][h]
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const int v = 32 * ks + 16 * u + l16;
-                    const f32x4_t p0 = *reinterpret_cast<const f32x4_t*>(slot + slot_c4(dw / 4 + 2 * g16, v));
-                    const f32x4_t p1 = *reinterpret_cast<const f32x4_t*>(slot + slot_c4(dw / 4 + 2 * g16 + 1, v));
-                    u32x4_t xh, xl;
-                    split8(make_float4(p0[0], p0[1], p0[2], p0[3]), make_float4(p1[0], p1[1], p1[2], p1[3]), xh, xl);
-                    th[u][0] = mfma16(xh, E0, f32x4_t{});
-                    th[u][1] = mfma16(xh, E1, f32x4_t{});
-                    tl[u][0] = mfma16(xl, E0, f32x4_t{});
-                    tl[u][1] = mfma16(xl, E1, f32x4_t{});
-                }
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    ah[h] = pack4x2(th[0][h], th[1][h]);
-                    al[h] = pack4x2(tl[0][h], tl[1][h]);
-                }
-            } else {
-                // C0, row-major: lane (l16, g16) reads row dw + 16 h + l16 at v = 32 ks + 4 g16 and + 16
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const float* r = c0 + static_cast<int64_t>(dw + 16 * h + l16) * kDV + 32 * ks + 4 * g16;
-                    split8(*reinterpret_cast<const float4*>(r), *reinterpret_cast<const float4*>(r + 16), ah[h], al[h]);
-                }
-            }
-#pragma unroll
-            for (int tb = 0; tb < 4; ++tb) {
-                const uint16_t* row = S.dH + (16 * tb + l16) * kHP + 32 * ks + 4 * g16;
-                const u32x2_t b0 = lds_u32x2(row), b1 = lds_u32x2(row + 16);
-                const u32x4_t b = u32x4_t{b0[0], b0[1], b1[0], b1[1]};
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    acc[h][tb] = mfma16(ah[h], b, acc[h][tb]);
-                    acc[h][tb] = mfma16(al[h], b, acc[h][tb]);
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int tb = 0; tb < 4; ++tb) {
-        const int tt = 16 * tb + l16;
-        float qx = 0.0f;
-        if (t0 + tt < T) {
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int d = dw + 16 * h + 4 * g16;
-                *reinterpret_cast<f32x4_t*>(&A.dq[(st + t0 + tt) * kDQK + d]) = acc[h][tb];
-                const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(&A.q[(st + t0 + tt) * kDQK + d]);
-                qx += lo_f32(qv[0]) * acc[h][tb][0] + hi_f32(qv[0]) * acc[h][tb][1] + lo_f32(qv[1]) * acc[h][tb][2] +
-                      hi_f32(qv[1]) * acc[h][tb][3];
-            }
-        }
-        qx = sum_rows4(qx);
-        if (g16 == 0) S.red[wave][tt] = qx * kQScale;
-    }
-    __syncthreads();
-    if (tid < kBL && t0 + tid < T)
-        A.part[(st + t0 + tid) * kPartF + j] = S.red[0][tid] + S.red[1][tid] + S.red[2][tid] + S.red[3][tid];
+// ---- X: the sum of the walk's tile partials, into dq ---------------------------------------------
+__global__ void __launch_bounds__(256) bwd_xsum_kernel(const float* __restrict__ X, float* __restrict__ dq, int64_t n4) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= n4) return;
+    const f32x4_t* x = reinterpret_cast<const f32x4_t*>(X);
+    reinterpret_cast<f32x4_t*>(dq)[i] = (x[i] + x[n4 + i]) + (x[2 * n4 + i] + x[3 * n4 + i]);
 }
 
 // ---- intra pass --------------------------------------------------------------------------------
@@ -514,7 +402,7 @@ __global__ void __launch_bounds__(kBT) bwd_intra_kernel(BwdParams A) {
     float qx = 0.0f;
     if (valid) {
         const float* pp = &A.part[(st + t0 + tau) * kPartF];
-        qx = pp[0] + pp[1];
+        qx = (pp[0] + pp[1]) + (pp[2] + pp[3]);
     }
     dhn += gt * qx;
     const float wt = (act && valid) ? -(dhn * rden) * (Dt > 0.0f ? 1.0f : -1.0f) * rden : 0.0f;
@@ -534,8 +422,8 @@ __global__ void __launch_bounds__(kBT) bwd_intra_kernel(BwdParams A) {
                     pack_bf16x2(pv[2] - lo_f32(h23), pv[3] - hi_f32(h23))};
     }
     __syncthreads();
-    // dq^T [d][tau] = (g / den X + sum_sigma K^T[d][sigma] P^T[sigma][tau] + g w n) / sqrt(DQK), X from
-    // the dhc pass; r_t = q_t . dq_t
+    // dq^T [d][tau] = (g / den X + sum_sigma K^T[d][sigma] P^T[sigma][tau] + g w n) / sqrt(DQK), X (in
+    // dq) the sum of the walk's four tile partials; r_t = q_t . dq_t
     float rpart[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
@@ -931,7 +819,7 @@ hipError_t launch_big(const void* kern, const BwdParams& p, unsigned grid, hipSt
 size_t align256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
 
 struct BwdLayout {
-    size_t slots, seg, hl, lz0, gamn, tok, part, chunk, dmp, total;
+    size_t slots, seg, xp, hl, lz0, gamn, tok, part, chunk, dmp, total;
 };
 BwdLayout bwd_layout(int64_t S, int T) {
     const int64_t NC = (T + kBL - 1) / kBL, NC1 = NC > 0 ? NC - 1 : 0;
@@ -943,7 +831,8 @@ BwdLayout bwd_layout(int64_t S, int T) {
         return o;
     };
     L.slots = take(static_cast<size_t>(S * NC1 * kSlotFloats) * 4);
-    L.seg = take(chunk_states_workspace_bytes(static_cast<int>(S), 1, T));
+    L.seg = take(bwd_walk_workspace_bytes(static_cast<int>(S), 1, T));
+    L.xp = take(static_cast<size_t>(4 * S * T * kDQK) * 4);
     L.hl = take(static_cast<size_t>(S * NC1 * 2 * kCV) * 2);
     L.lz0 = take(static_cast<size_t>(S * kLzFloats) * 4);
     L.gamn = take(static_cast<size_t>(S * NC * kDQK) * 4);
@@ -1008,12 +897,15 @@ hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t 
     p.T = T;
     p.NC = (T + kBL - 1) / kBL;
 
-    hipError_t e = launch_chunk_states(a.f, p.slots, reinterpret_cast<float*>(ws + L.seg), stream);
+    float* X = reinterpret_cast<float*>(ws + L.xp);
+    hipError_t e = launch_bwd_walk(a.f, a.dh, p.slots, reinterpret_cast<float*>(ws + L.seg), X, p.part, kPartF, stream);
+    if (e != hipSuccess) return e;
+    const int64_t n4 = static_cast<int64_t>(S) * T * kDQK / 4;
+    hipLaunchKernelGGL(bwd_xsum_kernel, dim3(static_cast<unsigned>((n4 + 255) / 256)), dim3(256), 0, stream, X, a.dq, n4);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned nchunks = static_cast<unsigned>(S) * p.NC;
-    static std::atomic<uint64_t> r_intra{0}, r_q{0}, r_kv{0};
-    e = launch_big<DhcSmem>(reinterpret_cast<const void*>(bwd_dhc_kernel), p, nchunks * 2, stream, r_q);
-    if (e != hipSuccess) return e;
+    static std::atomic<uint64_t> r_intra{0}, r_kv{0};
     e = launch_big<IntraSmem>(reinterpret_cast<const void*>(bwd_intra_kernel), p, nchunks, stream, r_intra);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bwd_scan_kernel, dim3(kScanBlocks, S), dim3(256), 0, stream, p);

@@ -1367,34 +1367,50 @@ hipError_t launch_local(const LocalArgs& a, int S, hipStream_t stream, bool hilo
 // sub-segments of a local segment: at most kLocMax tokens each
 int local_subsegments(int seg_tokens) { return (seg_tokens + kLocMax - 1) / kLocMax; }
 
-// ---- chunk-boundary states for the backward pass ------------------------------------------------
-// The backward needs the state entering every 64-token chunk.  A walk over the chunks provides it:
-// one workgroup of 8 waves per (sequence, 128-column dv tile, segment), with the accumulator layout,
-// gate phase and lazy scale of chunk_mfma_kernel<64> but the state update alone (no logits, no
-// read-out, no h): C += K^T (w e^{-s} V) and n += K^T w.  The weighted values enter the update as a
-// bf16 pair hi + lo (the products to about 2^-17, against 2^-9 for one rounding), because the
-// backward's gradients can cancel against the state.  At the top of chunk c >= 1 the workgroup writes
-// the state entering it into slot c - 1: C in the four-row interleaved layout, n at DQK DV and the
-// max state at DQK DV + DQK + 2.  Segment g >= 1 enters from the segment slots of the local pass (in
-// its hi + lo form) and the combine.
+// ---- the backward's forward walk ----------------------------------------------------------------
+// The backward needs, for every 64-token chunk c, X_c = dH_c C_c^T on the state C_c entering the chunk
+// (the inter-chunk term of dq), with q^_t . X_t, and the chunk's entry normaliser and max state.  A
+// walk over the chunks gives them without writing the states out: one workgroup of 8 waves per
+// (sequence, 128-column dv tile, segment), with the gate phase and lazy scale of chunk_mfma_kernel<64>,
+// holds its 256 x 128 slice of C in registers and per chunk
+//   - forms X^T = C dH^T over its 128 columns (the four tiles' partial sums are added by the
+//     backward) and its share of q^ . X,
+//   - applies the update C += K^T (w e^{-s} V), the weighted values as a bf16 pair hi + lo (products
+//     to about 2^-17 rather than the 2^-9 of one rounding, because the backward's gradients can
+//     cancel against the state), and n += K^T w,
+//   - writes n and m entering the chunk into slot c - 1 (tile 0).
+// Layout: wave w owns d = 32 w + 0..31 (two 16-column tiles dt) and all 128 v, as accumulator tiles
+// of C^T: tile (dt, pp, e) lane (l16, g16) holds C[32 w + 16 dt + l16][32 pp + 8 g16 + 4 e + j],
+// j = 0..3.  The two tiles e of a pair give a lane eight consecutive v, the A operand of C dH^T (with
+// 16-byte reads of dH rows); the update reads the weighted V^T rows in the same permuted order.
+// Segment g >= 1 enters from the segment slots of the local pass (in its hi + lo form) and the
+// combine.
+constexpr int kWalkHP = kDVT + 8;   // dH row pitch (elements): 272 bytes
 struct WalkSmem {
     uint16_t K[Cfg<64>::NDB][64 * Cfg<64>::QP];   // the chunk's K rows, two d blocks of 128
     uint16_t Vw[2][kDVT * Cfg<64>::TP];           // (w e^{-s} V)^T of the chunk as bf16 hi [0] and lo [1]
+    uint16_t dH[64 * kWalkHP];                     // the chunk's dH rows, this tile's 128 columns
     float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
     GateBuf<64> G[2];                              // by chunk parity
+    float red[kWaves][64];                         // q^ . X partial sums per wave
 };
 static_assert(sizeof(WalkSmem) <= 160 * 1024, "LDS budget");
 
 struct WalkArgs {
+    const uint16_t* q;    // [S, T, DQK] rows
     const uint16_t* k;
     const uint16_t* v;
+    const uint16_t* dh;   // [S, T, DV] rows
     const float* ipre;
     const float* fpre;
     const float* C0;      // entry state of segment 0 (NULL: zero state, m = m0 or 0)
     const float* n0;
     const float* m0;
     const float* seg;     // segment slots of the local pass and the combine (G > 1)
-    float* out;           // S (NC - 1) chunk slots
+    float* out;           // S (NC - 1) chunk slots: n and m entering chunk c >= 1 in slot c - 1
+    float* X;             // kNTile x [S, T, DQK]: X^T partial sums over each tile's columns
+    float* part;          // [S, T, part_stride]: q^ . X partial sum of tile j at offset j
+    int part_stride;
     int S;
     int T;
     int G;                // segments per sequence
@@ -1431,6 +1447,21 @@ __device__ __forceinline__ void walk_store_k(WalkSmem& S, const u32x4_t (&r)[Cfg
             *reinterpret_cast<u32x4_t*>(&S.K[p][off]) = r[p][i];
         }
 }
+// the chunk's dH rows, this tile's 128 columns: two 16-byte pieces per thread
+__device__ __forceinline__ void walk_load_dh(u32x4_t (&r)[2], __amdgpu_buffer_rsrc_t rdh, int t0, int v0, int tid) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int item = tid + i * kThreads;
+        r[i] = bload128(rdh, static_cast<uint32_t>((t0 + item / 16) * kDV + v0 + 8 * (item % 16)) * 2u, 0);
+    }
+}
+__device__ __forceinline__ void walk_store_dh(WalkSmem& S, const u32x4_t (&r)[2], int tid) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int item = tid + i * kThreads;
+        *reinterpret_cast<u32x4_t*>(&S.dH[(item / 16) * kWalkHP + 8 * (item % 16)]) = r[i];
+    }
+}
 // (w V)^T from the packed V^T as a bf16 pair: hi = bf16(w v), lo = bf16(w v - hi)
 __device__ __forceinline__ void vt_store_hilo(WalkSmem& S, const VtPacked<64>& pv, const float* wC, int wave, int lane) {
     constexpr int TP = Cfg<64>::TP, NA = 64 / 16;
@@ -1458,13 +1489,12 @@ __device__ __forceinline__ void vt_store_hilo(WalkSmem& S, const VtPacked<64>& p
     }
 }
 
-__global__ void __launch_bounds__(kThreads, 1) chunk_states_kernel(WalkArgs A) {
+__global__ void __launch_bounds__(kThreads, 1) bwd_walk_kernel(WalkArgs A) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     WalkSmem& S = *reinterpret_cast<WalkSmem*>(smem_raw);
     constexpr int L = 64;
     using CF = Cfg<64>;
-    constexpr int QP = CF::QP, TP = CF::TP, DB = CF::DB, NDB = CF::NDB, DH = CF::DH, VT = CF::VT, NVG = CF::NVG;
-    constexpr int NQ = CF::DT / DH;   // this wave's 16-row C tiles per d block
+    constexpr int QP = CF::QP, TP = CF::TP, DB = CF::DB, NDB = CF::NDB;
     constexpr int NKS = L / 32;
     static_assert(DB / 16 == kWaves, "one n-update tile per wave and d block");
 
@@ -1472,13 +1502,6 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_states_kernel(WalkArgs A) {
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g16 = lane >> 4, l16 = lane & 15;
-    const int vg = wave % NVG, dh = wave / NVG;
-    auto vcol = [&](int vt) { return 16 * (vg * VT + vt); };
-    // d row of element j of accumulator tile t: the layout of chunk_mfma_kernel<64>
-    auto cdrow = [&](int t, int j) {
-        const int q = t % NQ;
-        return (t / NQ) * DB + 32 * ((q / 2) * DH + dh) + 8 * g16 + 4 * (q % 2) + j;
-    };
     const bool gate_wave = (wave == kGateWave);
 
     const int wi = work_index();
@@ -1491,36 +1514,49 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_states_kernel(WalkArgs A) {
     const int c_begin = g * A.seg_chunks;
     const int c_end = min(nc_total, c_begin + A.seg_chunks);
     MLSTM_CHECK(s < A.S, kDbgChunkMfma);
+    const int64_t st = static_cast<int64_t>(s) * A.T;
 
     SeqRsrc P;
     P.k = make_rsrc(seq_rows(A.k, s, A.nh_magic, A.sk), seq_span(A.T, A.rk, kDQK));
     P.v = make_rsrc(seq_rows(A.v, s, A.nh_magic, A.sv), seq_span(A.T, A.rv, kDV));
-    P.ig = make_rsrc(A.ipre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
-    P.fg = make_rsrc(A.fpre + static_cast<int64_t>(s) * A.T, static_cast<uint32_t>(A.T) * 4);
+    P.ig = make_rsrc(A.ipre + st, static_cast<uint32_t>(A.T) * 4);
+    P.fg = make_rsrc(A.fpre + st, static_cast<uint32_t>(A.T) * 4);
+    const __amdgpu_buffer_rsrc_t rdh = make_rsrc(A.dh + st * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
+    float* Xt = A.X + static_cast<int64_t>(tile) * A.S * A.T * kDQK;
 
-    // entry state into the accumulators
-    f32x4_t Cacc[NDB * NQ][VT];
+    // entry state into the C^T tiles: Ct[dt][pp][e][j] = C[dw(dt) + l16][v0 + 32 pp + 8 g16 + 4 e + j]
+    auto dw = [&](int dt) { return 32 * wave + 16 * dt; };
+    f32x4_t Ct[2][4][2];
     const float* nin;
     float m_prev;
     if (g == 0) {
         const float* C0 = A.C0 ? A.C0 + static_cast<int64_t>(s) * kDQK * kDV : nullptr;
 #pragma unroll
-        for (int t = 0; t < NDB * NQ; ++t)
+        for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
-            for (int vt = 0; vt < VT; ++vt)
+            for (int pp = 0; pp < 4; ++pp)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    Cacc[t][vt][j] = C0 ? C0[static_cast<int64_t>(cdrow(t, j)) * kDV + v0 + vcol(vt) + l16] : 0.0f;
+                for (int e = 0; e < 2; ++e)
+                    Ct[dt][pp][e] = C0 ? *reinterpret_cast<const f32x4_t*>(
+                                             C0 + static_cast<int64_t>(dw(dt) + l16) * kDV + v0 + 32 * pp + 8 * g16 + 4 * e)
+                                       : f32x4_t{};
         nin = A.n0 ? A.n0 + static_cast<int64_t>(s) * kDQK : nullptr;
         m_prev = A.m0 ? A.m0[s] : 0.0f;
     } else {
         MLSTM_CHECK(g * A.R - 1 >= 0 && g * A.R - 1 < A.NS, kDbgChunkMfma);
         const float* slot = A.seg + (static_cast<int64_t>(s) * A.NS + g * A.R - 1) * kSlotFloats;
+        // the slot holds four rows interleaved: element (d, v) at slot_c4(d / 4, v) + d % 4
 #pragma unroll
-        for (int t = 0; t < NDB * NQ; ++t)
+        for (int dt = 0; dt < 2; ++dt) {
+            const int d = dw(dt) + l16;
 #pragma unroll
-            for (int vt = 0; vt < VT; ++vt)
-                Cacc[t][vt] = *reinterpret_cast<const f32x4_t*>(slot + slot_c4(cdrow(t, 0) / 4, v0 + vcol(vt) + l16));
+            for (int pp = 0; pp < 4; ++pp)
+#pragma unroll
+                for (int e = 0; e < 2; ++e)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        Ct[dt][pp][e][j] = slot[slot_c4(d / 4, v0 + 32 * pp + 8 * g16 + 4 * e + j) + d % 4];
+        }
         nin = slot + kDQK * kDV;
         m_prev = slot[kDQK * kDV + kDQK + 2];
     }
@@ -1530,12 +1566,14 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_states_kernel(WalkArgs A) {
     float gi[2] = {0.f, 0.f}, gf[2] = {0.f, 0.f};
 
     u32x4_t rk[NDB][kWalkKP];
+    u32x4_t rdhv[2];
     VRegs<64> rv;
     VtPacked<64> pv;
     if (c_begin < c_end) {
         const int t0 = c_begin * L;
         walk_load_k(rk, P, t0, tid, A.rk);
         load_v_tr<64>(rv, P, t0, v0, wave, lane, 0, A.rv);
+        walk_load_dh(rdhv, rdh, t0, v0, tid);
         if (gate_wave) {
             load_gates<64>(gi, gf, P, t0, lane);
             gate_phase<64>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane, A.T - t0);
@@ -1547,31 +1585,102 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_states_kernel(WalkArgs A) {
         const int cur = (c - c_begin) & 1;
         const int par = c & 1;
         const GateBuf<64>& Gc = S.G[par];
-        __syncthreads();   // the previous chunk's update is done; this chunk's gates and n are visible
+        __syncthreads();   // the previous chunk is done; this chunk's gates and n are visible
+        if (c > c_begin && tid < L && t0 - L + tid < A.T) {
+            // the previous chunk's q^ . X share of this tile
+            float qx = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) qx += S.red[w][tid];
+            A.part[(st + t0 - L + tid) * A.part_stride + tile] = qx;
+        }
         walk_store_k(S, rk, tid);
+        walk_store_dh(S, rdhv, tid);
         vt_transpose<64>(pv, rv, lane, 0);
         vt_store_hilo(S, pv, Gc.wC, wave, lane);
         if (c + 1 < c_end) {
             walk_load_k(rk, P, t0 + L, tid, A.rk);
             load_v_tr<64>(rv, P, t0 + L, v0, wave, lane, 0, A.rv);
+            walk_load_dh(rdhv, rdh, t0 + L, v0, tid);
             if (gate_wave) load_gates<64>(gi, gf, P, t0 + L, lane);
         }
-        if (c > 0) {
-            // the state entering chunk c
+        if (c > 0 && tile == 0) {
+            // n and m entering chunk c
             MLSTM_CHECK(c - 1 < nc_total - 1, kDbgChunkMfma);
             float* slot = A.out + (static_cast<int64_t>(s) * (nc_total - 1) + c - 1) * kSlotFloats;
-            const float esc = expf(s_off);
-#pragma unroll
-            for (int t = 0; t < NDB * NQ; ++t)
-#pragma unroll
-                for (int vt = 0; vt < VT; ++vt)
-                    *reinterpret_cast<f32x4_t*>(slot + slot_c4(cdrow(t, 0) / 4, v0 + vcol(vt) + l16)) = Cacc[t][vt] * esc;
-            if (tile == 0 && tid < kDQK) slot[kDQK * kDV + tid] = S.n[cur][tid];
-            if (tile == 0 && tid == 0) slot[kDQK * kDV + kDQK + 2] = m_prev;
+            if (tid < kDQK) slot[kDQK * kDV + tid] = S.n[cur][tid];
+            if (tid == 0) slot[kDQK * kDV + kDQK + 2] = m_prev;
         }
-        __syncthreads();   // the chunk's K rows and weighted V^T are visible
+        __syncthreads();   // the chunk's K rows, dH rows and weighted V^T are visible
         // gates of the next chunk, one chunk ahead
         if (gate_wave && c + 1 < c_end) gate_phase<64>(S.G[par ^ 1], gi, gf, g_m, g_s, lane, A.T - (t0 + L));
+
+        // X^T [d][tau] = sum_v C[d][v] dH[tau][v] over this tile's columns, C as a bf16 pair hi + lo
+        {
+            // the q rows of q^ . X, requested before the products so that their latency is covered
+            u32x2_t qv[2][4];
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb) {
+                    const int tau = 16 * tb + l16;
+                    qv[dt][tb] = (t0 + tau < A.T)
+                                     ? *reinterpret_cast<const u32x2_t*>(A.q + (st + t0 + tau) * kDQK + dw(dt) + 4 * g16)
+                                     : u32x2_t{0u, 0u};
+                }
+            f32x4_t X[2][4];
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb) X[dt][tb] = f32x4_t{};
+#pragma unroll
+            for (int pp = 0; pp < 4; ++pp) {
+                u32x4_t b[4];
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb)
+                    b[tb] = *reinterpret_cast<const u32x4_t*>(&S.dH[(16 * tb + l16) * kWalkHP + 32 * pp + 8 * g16]);
+#pragma unroll
+                for (int dt = 0; dt < 2; ++dt) {
+                    const f32x4_t& c0 = Ct[dt][pp][0];
+                    const f32x4_t& c1 = Ct[dt][pp][1];
+                    u32x4_t ah, al;
+                    ah[0] = pack_bf16x2(c0[0], c0[1]);
+                    ah[1] = pack_bf16x2(c0[2], c0[3]);
+                    ah[2] = pack_bf16x2(c1[0], c1[1]);
+                    ah[3] = pack_bf16x2(c1[2], c1[3]);
+                    al[0] = pack_bf16x2(c0[0] - lo_f32(ah[0]), c0[1] - hi_f32(ah[0]));
+                    al[1] = pack_bf16x2(c0[2] - lo_f32(ah[1]), c0[3] - hi_f32(ah[1]));
+                    al[2] = pack_bf16x2(c1[0] - lo_f32(ah[2]), c1[1] - hi_f32(ah[2]));
+                    al[3] = pack_bf16x2(c1[2] - lo_f32(ah[3]), c1[3] - hi_f32(ah[3]));
+#pragma unroll
+                    for (int tb = 0; tb < 4; ++tb) {
+                        X[dt][tb] = mfma16(ah, b[tb], X[dt][tb]);
+                        X[dt][tb] = mfma16(al, b[tb], X[dt][tb]);
+                    }
+                }
+            }
+            // C = C_acc e^{s}; lane (tau = 16 tb + l16, g16) holds X^T[dw(dt) + 4 g16 + 0..3][tau]
+            const float esc = expf(s_off);
+            float qx[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt) {
+                const int d = dw(dt) + 4 * g16;
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb) {
+                    const int tau = 16 * tb + l16;
+                    if (t0 + tau < A.T) {
+                        const f32x4_t x = X[dt][tb] * esc;
+                        *reinterpret_cast<f32x4_t*>(Xt + (st + t0 + tau) * kDQK + d) = x;
+                        const u32x2_t q = qv[dt][tb];
+                        qx[tb] += lo_f32(q[0]) * x[0] + hi_f32(q[0]) * x[1] + lo_f32(q[1]) * x[2] + hi_f32(q[1]) * x[3];
+                    }
+                }
+            }
+#pragma unroll
+            for (int tb = 0; tb < 4; ++tb) {
+                const float v = sum_rows4(qx[tb]);
+                if (g16 == 0) S.red[wave][16 * tb + l16] = v * kQScale;
+            }
+        }
 
         const float decay_n = Gc.scal[0];
         const float m_next = Gc.scal[1];
@@ -1579,43 +1688,48 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_states_kernel(WalkArgs A) {
         const float c_scale = Gc.scal[3];   // != 1: apply this chunk's decay to C_acc eagerly
         if (c_scale != 1.0f) {
 #pragma unroll
-            for (int t = 0; t < NDB * NQ; ++t)
+            for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
-                for (int vt = 0; vt < VT; ++vt) Cacc[t][vt] *= c_scale;
+                for (int pp = 0; pp < 4; ++pp)
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) Ct[dt][pp][e] *= c_scale;
         }
         const int tr_row = (l16 >> 2) + 8 * g16;
         const int tr_col = 4 * (l16 & 3);
+        // C^T += (w e^{-s} V)^T K (hi, then lo): A = the weighted V^T rows in the pair order (row l16 of
+        // tile (pp, e) is v = 32 pp + 8 (l16 / 4) + 4 e + l16 % 4), B = K read transposed (this wave's d)
+        {
+            const uint16_t* Ks = S.K[wave / 4];
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+                u32x4_t kt[2];
+#pragma unroll
+                for (int dt = 0; dt < 2; ++dt) {
+                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * (wave % 4) + 16 * dt + tr_col];
+                    kt[dt] = cat(tr_read(kb), tr_read(kb + 4 * QP));
+                }
+#pragma unroll
+                for (int pp = 0; pp < 4; ++pp)
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int off = (32 * pp + 8 * (l16 >> 2) + 4 * e + (l16 & 3)) * TP + 32 * ks + 8 * g16;
+                        const u32x4_t vh = *reinterpret_cast<const u32x4_t*>(&S.Vw[0][off]);
+                        const u32x4_t vl = *reinterpret_cast<const u32x4_t*>(&S.Vw[1][off]);
+#pragma unroll
+                        for (int dt = 0; dt < 2; ++dt) {
+                            Ct[dt][pp][e] = mfma16(vh, kt[dt], Ct[dt][pp][e]);
+                            Ct[dt][pp][e] = mfma16(vl, kt[dt], Ct[dt][pp][e]);
+                        }
+                    }
+            }
+        }
+        // n_p = decay n_p + K_p^T w over this wave's 16 columns of each block: A = w as bf16 hi / lo
+        // rows, B = K read transposed
         const float* n_old = S.n[cur];
         float* n_new = S.n[cur ^ 1];
 #pragma unroll
         for (int p = 0; p < NDB; ++p) {
             const uint16_t* Ks = S.K[p];
-            // C_p += K_p^T (w e^{-s} V) (hi, then lo): A = K read transposed, B = the weighted V^T rows
-#pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) {
-                u32x4_t a[NQ];
-#pragma unroll
-                for (int q = 0; q < NQ; ++q) {
-                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * ((q / 2) * DH + dh) + 2 * tr_col + 4 * (q % 2)];
-                    a[q] = cat(tr_read(kb), tr_read(kb + 4 * QP));
-                }
-                u32x4_t vh[VT], vl[VT];
-#pragma unroll
-                for (int vt = 0; vt < VT; ++vt) {
-                    const int off = (vcol(vt) + l16) * TP + 32 * ks + 8 * g16;
-                    vh[vt] = *reinterpret_cast<const u32x4_t*>(&S.Vw[0][off]);
-                    vl[vt] = *reinterpret_cast<const u32x4_t*>(&S.Vw[1][off]);
-                }
-#pragma unroll
-                for (int q = 0; q < NQ; ++q)
-#pragma unroll
-                    for (int vt = 0; vt < VT; ++vt) {
-                        Cacc[p * NQ + q][vt] = mfma16(a[q], vh[vt], Cacc[p * NQ + q][vt]);
-                        Cacc[p * NQ + q][vt] = mfma16(a[q], vl[vt], Cacc[p * NQ + q][vt]);
-                    }
-            }
-            // n_p = decay n_p + K_p^T w over this wave's 16 columns of the block: A = w as bf16 hi / lo
-            // rows, B = K read transposed
             f32x4_t nacc = f32x4_t{};
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks) {
@@ -1632,14 +1746,24 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_states_kernel(WalkArgs A) {
         s_off = s_new;
         m_prev = m_next;
     }
+    __syncthreads();
+    if (c_begin < c_end && tid < L) {
+        const int t0 = (c_end - 1) * L;   // the last chunk's q^ . X share
+        if (t0 + tid < A.T) {
+            float qx = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) qx += S.red[w][tid];
+            A.part[(st + t0 + tid) * A.part_stride + tile] = qx;
+        }
+    }
 }
 
 hipError_t launch_walk(const WalkArgs& a, hipStream_t stream) {
     const size_t lds = sizeof(WalkSmem);
     static std::atomic<uint64_t> raised{0};
-    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(chunk_states_kernel), lds, raised);
+    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_walk_kernel), lds, raised);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(chunk_states_kernel, dim3(static_cast<unsigned>(a.S * a.G * kNTile)), dim3(kThreads), lds, stream,
+    hipLaunchKernelGGL(bwd_walk_kernel, dim3(static_cast<unsigned>(a.S * a.G * kNTile)), dim3(kThreads), lds, stream,
                        a);
     return hipGetLastError();
 }
@@ -1729,24 +1853,27 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
     return (a.L == 64) ? launch_variant<64>(k, S, stream) : launch_variant<128>(k, S, stream);
 }
 
-// ---- chunk-boundary states for the backward pass -----------------------------------------------
-// The state entering every chunk c >= 1 of 64 tokens, into slot c - 1 of ``slots`` (S (NC - 1) slots:
-// fp32 C in the four-row interleaved layout, n, and the entry max state): the segment schedule of the
-// prefill (local pass in the bf16 hi + lo form, combine) for the segments' entry states, then the walk.
-size_t chunk_states_workspace_bytes(int B, int NH, int T) {
+// ---- the backward's forward walk ----------------------------------------------------------------
+// For every 64-token chunk: the tiles' partial sums of X^T = C dH^T into X, their q^ . X shares into
+// part, and n, m entering chunk c >= 1 into slot c - 1 of ``slots``.  The segment schedule of the
+// prefill (local pass in the bf16 hi + lo form, combine) gives the entry states of the segments.
+size_t bwd_walk_workspace_bytes(int B, int NH, int T) {
     return chunk_mfma_workspace_bytes(B, NH, T, kDQK, kDV, 64);
 }
 
-hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, float* seg, hipStream_t stream) {
+hipError_t launch_bwd_walk(const ChunkArgs& a, const void* dh, float* slots, float* seg, float* X, float* part,
+                           int part_stride, hipStream_t stream) {
     const int S = a.B * a.NH;
     const int nc = (a.T + 63) / 64;
-    if (nc <= 1) return hipSuccess;
+    if (nc == 0) return hipSuccess;
     const int G = seg ? chunk_mfma_segments(a.B, a.NH, a.T, 64) : 1;
     const int seg_chunks = G > 1 ? (nc + G - 1) / G : nc;
     const int R = G > 1 ? local_subsegments(seg_chunks * 64) : 1;
     WalkArgs w{};
+    w.q = static_cast<const uint16_t*>(a.q);
     w.k = static_cast<const uint16_t*>(a.k);
     w.v = static_cast<const uint16_t*>(a.v);
+    w.dh = static_cast<const uint16_t*>(dh);
     set_strides(a, w.nh_magic, nullptr, w.sk, w.sv, nullptr, &w.rk, &w.rv);
     w.ipre = a.ipre;
     w.fpre = a.fpre;
@@ -1755,6 +1882,9 @@ hipError_t launch_chunk_states(const ChunkArgs& a, float* slots, float* seg, hip
     w.m0 = a.m0;
     w.seg = seg;
     w.out = slots;
+    w.X = X;
+    w.part = part;
+    w.part_stride = part_stride;
     w.S = S;
     w.T = a.T;
     w.G = G;

@@ -93,13 +93,16 @@ bool chunk_mfma_supported(mlstm_dtype dt, int DQK, int DV, int L);
 int chunk_mfma_segments(int B, int NH, int T, int L);
 size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L);
 hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream);
-// The backward's walk over 64-token chunks: X (kNTile x [S, T, DQK]) receives each dv tile's partial
-// sum of X^T = C dH^T on the state entering the token's chunk, part[t * part_stride + tile] its
-// q^ . X share, and slot c - 1 of ``slots`` (S (NC - 1) slots) n and m entering chunk c >= 1; seg:
-// bwd_walk_workspace_bytes of segment slots (NULL: one segment per sequence).
-size_t bwd_walk_workspace_bytes(int B, int NH, int T);
-hipError_t launch_bwd_walk(const ChunkArgs& a, const void* dh, float* slots, float* seg, float* X, float* part,
-                           int part_stride, hipStream_t stream);
+// The prefill's segment schedule for chunks of L tokens: the segment count G (1: one segment per
+// sequence), local sub-segments R per segment and chunks per segment.  launch_segment_states runs,
+// when G > 1, the local pass (bf16 hi + lo products when hilo) and the combine into the segment slots
+// ``seg`` (chunk_mfma_workspace_bytes of them).
+struct SegmentShape {
+    int G, R, seg_chunks;
+};
+SegmentShape segment_shape(int B, int NH, int T, int L, bool use_segments);
+hipError_t launch_segment_states(const ChunkArgs& a, int L, const SegmentShape& sh, float* seg, bool hilo,
+                                 hipStream_t stream);
 // --- chunkwise backward (bf16, DQK = 256, DV = 512, L = 64) --------------------
 bool chunk_bwd_supported(mlstm_dtype dt, int DQK, int DV, int L);
 size_t chunk_bwd_workspace_bytes(int B, int NH, int T);

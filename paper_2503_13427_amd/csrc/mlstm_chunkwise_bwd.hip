@@ -52,8 +52,8 @@
 //
 // Rows past the end of the sequence (a partial last chunk) are read through buffer resources with
 // the row offset in the range-checked offset, so they read as zero.
+#include "chunk_common.h"
 #include "launch.h"
-#include "mfma_common.h"
 
 namespace mlstm {
 namespace {
@@ -191,6 +191,450 @@ __device__ __forceinline__ void bwd_gates(__amdgpu_buffer_rsrc_t ig, __amdgpu_bu
     const bool none = (x == -INFINITY) || (static_cast<float>(lane) < rL);
     G.wk = none ? 0.0f : fexp(x - ML);
     decay = (restart || ML == -INFINITY || m_prev == -INFINITY) ? 0.0f : fexp(m_prev - ML);
+}
+
+// ---- the backward's forward walk ----------------------------------------------------------------
+// The backward needs, for every 64-token chunk c, X_c = dH_c C_c^T on the state C_c entering the chunk
+// (the inter-chunk term of dq), with q^_t . X_t, and the chunk's entry normaliser and max state.  A
+// walk over the chunks gives them without writing the states out: one workgroup of 8 waves per
+// (sequence, 128-column dv tile, segment), with the gate phase and lazy scale of chunk_mfma_kernel<64>,
+// holds its 256 x 128 slice of C in registers and per chunk
+//   - forms X^T = C dH^T over its 128 columns (the four tiles' partial sums are added by the
+//     backward) and its share of q^ . X,
+//   - applies the update C += K^T (w e^{-s} V), the weighted values as a bf16 pair hi + lo (products
+//     to about 2^-17 rather than the 2^-9 of one rounding, because the backward's gradients can
+//     cancel against the state), and n += K^T w,
+//   - writes n and m entering the chunk into slot c - 1 (tile 0).
+// Layout: wave w owns d = 32 w + 0..31 (two 16-column tiles dt) and all 128 v, as accumulator tiles
+// of C^T: tile (dt, pp, e) lane (l16, g16) holds C[32 w + 16 dt + l16][32 pp + 8 g16 + 4 e + j],
+// j = 0..3.  The two tiles e of a pair give a lane eight consecutive v, the A operand of C dH^T (with
+// 16-byte reads of dH rows); the update reads the weighted V^T rows in the same permuted order.
+// Segment g >= 1 enters from the segment slots of the local pass (in its hi + lo form) and the
+// combine.
+constexpr int kWalkHP = kDVT + 8;   // dH row pitch (elements): 272 bytes
+struct WalkSmem {
+    uint16_t K[Cfg<64>::NDB][64 * Cfg<64>::QP];   // the chunk's K rows, two d blocks of 128
+    uint16_t Vw[2][kDVT * Cfg<64>::TP];           // (w e^{-s} V)^T of the chunk as bf16 hi [0] and lo [1]
+    uint16_t dH[64 * kWalkHP];                     // the chunk's dH rows, this tile's 128 columns
+    float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
+    GateBuf<64> G[2];                              // by chunk parity
+    float red[kWaves][64];                         // q^ . X partial sums per wave
+};
+static_assert(sizeof(WalkSmem) <= 160 * 1024, "LDS budget");
+
+struct WalkArgs {
+    const uint16_t* q;    // [S, T, DQK] rows
+    const uint16_t* k;
+    const uint16_t* v;
+    const uint16_t* dh;   // [S, T, DV] rows
+    const float* ipre;
+    const float* fpre;
+    const float* C0;      // entry state of segment 0 (NULL: zero state, m = m0 or 0)
+    const float* n0;
+    const float* m0;
+    const float* seg;     // segment slots of the local pass and the combine (G > 1)
+    float* out;           // S (NC - 1) chunk slots: n and m entering chunk c >= 1 in slot c - 1
+    float* X;             // kNTile x [S, T, DQK]: X^T partial sums over each tile's columns
+    float* part;          // [S, T, part_stride]: q^ . X partial sum of tile j at offset j
+    int part_stride;
+    int S;
+    int T;
+    int G;                // segments per sequence
+    int R;                // local sub-segments per segment; segment g >= 1 enters from slot g R - 1
+    int NS;               // segment slots per sequence, (G - 1) R
+    int seg_chunks;       // chunks per segment (the last may be shorter)
+    uint32_t nh_magic;    // as in ChunkKernelArgs
+    int64_t sk[2], sv[2];
+    uint32_t rk, rv;
+};
+
+// the chunk's K rows, both d blocks: two 16-byte pieces per thread and block
+constexpr int kWalkKP = 64 * (Cfg<64>::DB / 8) / kThreads;
+__device__ __forceinline__ void walk_load_k(u32x4_t (&r)[Cfg<64>::NDB][kWalkKP], const SeqRsrc& R, int t0, int tid,
+                                            uint32_t rk) {
+    constexpr int PR = Cfg<64>::DB / 8;
+#pragma unroll
+    for (int p = 0; p < Cfg<64>::NDB; ++p)
+#pragma unroll
+        for (int i = 0; i < kWalkKP; ++i) {
+            const int item = tid + i * kThreads;
+            r[p][i] = bload128(R.k, static_cast<uint32_t>(t0 + item / PR) * rk + 16 * (item % PR), p * Cfg<64>::DB * 2);
+        }
+}
+__device__ __forceinline__ void walk_store_k(WalkSmem& S, const u32x4_t (&r)[Cfg<64>::NDB][kWalkKP], int tid) {
+    constexpr int PR = Cfg<64>::DB / 8;
+#pragma unroll
+    for (int p = 0; p < Cfg<64>::NDB; ++p)
+#pragma unroll
+        for (int i = 0; i < kWalkKP; ++i) {
+            const int item = tid + i * kThreads;
+            const int off = (item / PR) * Cfg<64>::QP + 8 * (item % PR);
+            MLSTM_CHECK(off + 8 <= 64 * Cfg<64>::QP, kDbgChunkBwd);
+            *reinterpret_cast<u32x4_t*>(&S.K[p][off]) = r[p][i];
+        }
+}
+// the chunk's dH rows, this tile's 128 columns: two 16-byte pieces per thread
+__device__ __forceinline__ void walk_load_dh(u32x4_t (&r)[2], __amdgpu_buffer_rsrc_t rdh, int t0, int v0, int tid) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int item = tid + i * kThreads;
+        r[i] = bload128(rdh, static_cast<uint32_t>((t0 + item / 16) * kDV + v0 + 8 * (item % 16)) * 2u, 0);
+    }
+}
+__device__ __forceinline__ void walk_store_dh(WalkSmem& S, const u32x4_t (&r)[2], int tid) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int item = tid + i * kThreads;
+        *reinterpret_cast<u32x4_t*>(&S.dH[(item / 16) * kWalkHP + 8 * (item % 16)]) = r[i];
+    }
+}
+// (w V)^T from the packed V^T as a bf16 pair: hi = bf16(w v), lo = bf16(w v - hi)
+__device__ __forceinline__ void vt_store_hilo(WalkSmem& S, const VtPacked<64>& pv, const float* wC, int wave, int lane) {
+    constexpr int TP = Cfg<64>::TP, NA = 64 / 16;
+    const int l16 = lane & 15, g16 = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < VRegs<64>::N * VRegs<64>::PARTS; ++i) {
+        const int pc = wave + kWaves * i, a = pc % NA, b = pc / NA;
+        const int tau = 16 * a + 4 * g16;
+        const f32x4_t w = *reinterpret_cast<const f32x4_t*>(&wC[tau]);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const u32x2_t x = pv[2 * i + h];
+            const float f0 = lo_f32(x[0]) * w[0], f1 = hi_f32(x[0]) * w[1];
+            const float f2 = lo_f32(x[1]) * w[2], f3 = hi_f32(x[1]) * w[3];
+            u32x2_t oh, ol;
+            oh[0] = pack_bf16x2(f0, f1);
+            oh[1] = pack_bf16x2(f2, f3);
+            ol[0] = pack_bf16x2(f0 - lo_f32(oh[0]), f1 - hi_f32(oh[0]));
+            ol[1] = pack_bf16x2(f2 - lo_f32(oh[1]), f3 - hi_f32(oh[1]));
+            const int row = 32 * b + 16 * h + l16;
+            MLSTM_CHECK(row < kDVT && tau + 4 <= TP, kDbgChunkBwd);
+            *reinterpret_cast<u32x2_t*>(&S.Vw[0][row * TP + tau]) = oh;
+            *reinterpret_cast<u32x2_t*>(&S.Vw[1][row * TP + tau]) = ol;
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kThreads, 1) bwd_walk_kernel(WalkArgs A) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+    WalkSmem& S = *reinterpret_cast<WalkSmem*>(smem_raw);
+    constexpr int L = 64;
+    using CF = Cfg<64>;
+    constexpr int QP = CF::QP, TP = CF::TP, DB = CF::DB, NDB = CF::NDB;
+    constexpr int NKS = L / 32;
+    static_assert(DB / 16 == kWaves, "one n-update tile per wave and d block");
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g16 = lane >> 4, l16 = lane & 15;
+    const bool gate_wave = (wave == kGateWave);
+
+    const int wi = work_index();
+    const int tile = wi % kNTile;
+    const int sg = wi / kNTile;
+    const int g = sg % A.G;
+    const int s = sg / A.G;
+    const int v0 = tile * kDVT;
+    const int nc_total = (A.T + L - 1) / L;
+    const int c_begin = g * A.seg_chunks;
+    const int c_end = min(nc_total, c_begin + A.seg_chunks);
+    MLSTM_CHECK(s < A.S, kDbgChunkBwd);
+    const int64_t st = static_cast<int64_t>(s) * A.T;
+
+    SeqRsrc P;
+    P.k = make_rsrc(seq_rows(A.k, s, A.nh_magic, A.sk), seq_span(A.T, A.rk, kDQK));
+    P.v = make_rsrc(seq_rows(A.v, s, A.nh_magic, A.sv), seq_span(A.T, A.rv, kDV));
+    P.ig = make_rsrc(A.ipre + st, static_cast<uint32_t>(A.T) * 4);
+    P.fg = make_rsrc(A.fpre + st, static_cast<uint32_t>(A.T) * 4);
+    const __amdgpu_buffer_rsrc_t rdh = make_rsrc(A.dh + st * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
+    float* Xt = A.X + static_cast<int64_t>(tile) * A.S * A.T * kDQK;
+
+    // entry state into the C^T tiles: Ct[dt][pp][e][j] = C[dw(dt) + l16][v0 + 32 pp + 8 g16 + 4 e + j]
+    auto dw = [&](int dt) { return 32 * wave + 16 * dt; };
+    f32x4_t Ct[2][4][2];
+    const float* nin;
+    float m_prev;
+    if (g == 0) {
+        const float* C0 = A.C0 ? A.C0 + static_cast<int64_t>(s) * kDQK * kDV : nullptr;
+#pragma unroll
+        for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+            for (int pp = 0; pp < 4; ++pp)
+#pragma unroll
+                for (int e = 0; e < 2; ++e)
+                    Ct[dt][pp][e] = C0 ? *reinterpret_cast<const f32x4_t*>(
+                                             C0 + static_cast<int64_t>(dw(dt) + l16) * kDV + v0 + 32 * pp + 8 * g16 + 4 * e)
+                                       : f32x4_t{};
+        nin = A.n0 ? A.n0 + static_cast<int64_t>(s) * kDQK : nullptr;
+        m_prev = A.m0 ? A.m0[s] : 0.0f;
+    } else {
+        MLSTM_CHECK(g * A.R - 1 >= 0 && g * A.R - 1 < A.NS, kDbgChunkBwd);
+        const float* slot = A.seg + (static_cast<int64_t>(s) * A.NS + g * A.R - 1) * kSlotFloats;
+        // the slot holds four rows interleaved: element (d, v) at slot_c4(d / 4, v) + d % 4
+#pragma unroll
+        for (int dt = 0; dt < 2; ++dt) {
+            const int d = dw(dt) + l16;
+#pragma unroll
+            for (int pp = 0; pp < 4; ++pp)
+#pragma unroll
+                for (int e = 0; e < 2; ++e)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        Ct[dt][pp][e][j] = slot[slot_c4(d / 4, v0 + 32 * pp + 8 * g16 + 4 * e + j) + d % 4];
+        }
+        nin = slot + kDQK * kDV;
+        m_prev = slot[kDQK * kDV + kDQK + 2];
+    }
+    if (tid < kDQK) S.n[0][tid] = nin ? nin[tid] : 0.0f;
+    float s_off = 0.0f;   // C = C_acc e^{s_off}
+    float g_m = m_prev, g_s = 0.0f;
+    float gi[2] = {0.f, 0.f}, gf[2] = {0.f, 0.f};
+
+    u32x4_t rk[NDB][kWalkKP];
+    u32x4_t rdhv[2];
+    VRegs<64> rv;
+    VtPacked<64> pv;
+    if (c_begin < c_end) {
+        const int t0 = c_begin * L;
+        walk_load_k(rk, P, t0, tid, A.rk);
+        load_v_tr<64>(rv, P, t0, v0, wave, lane, 0, A.rv);
+        walk_load_dh(rdhv, rdh, t0, v0, tid);
+        if (gate_wave) {
+            load_gates<64>(gi, gf, P, t0, lane);
+            gate_phase<64>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane, A.T - t0);
+        }
+    }
+
+    for (int c = c_begin; c < c_end; ++c) {
+        const int t0 = c * L;
+        const int cur = (c - c_begin) & 1;
+        const int par = c & 1;
+        const GateBuf<64>& Gc = S.G[par];
+        __syncthreads();   // the previous chunk is done; this chunk's gates and n are visible
+        if (c > c_begin && tid < L && t0 - L + tid < A.T) {
+            // the previous chunk's q^ . X share of this tile
+            float qx = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) qx += S.red[w][tid];
+            A.part[(st + t0 - L + tid) * A.part_stride + tile] = qx;
+        }
+        walk_store_k(S, rk, tid);
+        walk_store_dh(S, rdhv, tid);
+        vt_transpose<64>(pv, rv, lane, 0);
+        vt_store_hilo(S, pv, Gc.wC, wave, lane);
+        if (c + 1 < c_end) {
+            walk_load_k(rk, P, t0 + L, tid, A.rk);
+            load_v_tr<64>(rv, P, t0 + L, v0, wave, lane, 0, A.rv);
+            walk_load_dh(rdhv, rdh, t0 + L, v0, tid);
+            if (gate_wave) load_gates<64>(gi, gf, P, t0 + L, lane);
+        }
+        if (c > 0 && tile == 0) {
+            // n and m entering chunk c
+            MLSTM_CHECK(c - 1 < nc_total - 1, kDbgChunkBwd);
+            float* slot = A.out + (static_cast<int64_t>(s) * (nc_total - 1) + c - 1) * kSlotFloats;
+            if (tid < kDQK) slot[kDQK * kDV + tid] = S.n[cur][tid];
+            if (tid == 0) slot[kDQK * kDV + kDQK + 2] = m_prev;
+        }
+        __syncthreads();   // the chunk's K rows, dH rows and weighted V^T are visible
+        // gates of the next chunk, one chunk ahead
+        if (gate_wave && c + 1 < c_end) gate_phase<64>(S.G[par ^ 1], gi, gf, g_m, g_s, lane, A.T - (t0 + L));
+
+        // X^T [d][tau] = sum_v C[d][v] dH[tau][v] over this tile's columns, C as a bf16 pair hi + lo
+        {
+            // the q rows of q^ . X, requested before the products so that their latency is covered
+            u32x2_t qv[2][4];
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb) {
+                    const int tau = 16 * tb + l16;
+                    qv[dt][tb] = (t0 + tau < A.T)
+                                     ? *reinterpret_cast<const u32x2_t*>(A.q + (st + t0 + tau) * kDQK + dw(dt) + 4 * g16)
+                                     : u32x2_t{0u, 0u};
+                }
+            f32x4_t X[2][4];
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb) X[dt][tb] = f32x4_t{};
+#pragma unroll
+            for (int pp = 0; pp < 4; ++pp) {
+                u32x4_t b[4];
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb)
+                    b[tb] = *reinterpret_cast<const u32x4_t*>(&S.dH[(16 * tb + l16) * kWalkHP + 32 * pp + 8 * g16]);
+#pragma unroll
+                for (int dt = 0; dt < 2; ++dt) {
+                    const f32x4_t& c0 = Ct[dt][pp][0];
+                    const f32x4_t& c1 = Ct[dt][pp][1];
+                    u32x4_t ah, al;
+                    ah[0] = pack_bf16x2(c0[0], c0[1]);
+                    ah[1] = pack_bf16x2(c0[2], c0[3]);
+                    ah[2] = pack_bf16x2(c1[0], c1[1]);
+                    ah[3] = pack_bf16x2(c1[2], c1[3]);
+                    al[0] = pack_bf16x2(c0[0] - lo_f32(ah[0]), c0[1] - hi_f32(ah[0]));
+                    al[1] = pack_bf16x2(c0[2] - lo_f32(ah[1]), c0[3] - hi_f32(ah[1]));
+                    al[2] = pack_bf16x2(c1[0] - lo_f32(ah[2]), c1[1] - hi_f32(ah[2]));
+                    al[3] = pack_bf16x2(c1[2] - lo_f32(ah[3]), c1[3] - hi_f32(ah[3]));
+#pragma unroll
+                    for (int tb = 0; tb < 4; ++tb) {
+                        X[dt][tb] = mfma16(ah, b[tb], X[dt][tb]);
+                        X[dt][tb] = mfma16(al, b[tb], X[dt][tb]);
+                    }
+                }
+            }
+            // C = C_acc e^{s}; lane (tau = 16 tb + l16, g16) holds X^T[dw(dt) + 4 g16 + 0..3][tau]
+            const float esc = expf(s_off);
+            float qx[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt) {
+                const int d = dw(dt) + 4 * g16;
+#pragma unroll
+                for (int tb = 0; tb < 4; ++tb) {
+                    const int tau = 16 * tb + l16;
+                    if (t0 + tau < A.T) {
+                        const f32x4_t x = X[dt][tb] * esc;
+                        *reinterpret_cast<f32x4_t*>(Xt + (st + t0 + tau) * kDQK + d) = x;
+                        const u32x2_t q = qv[dt][tb];
+                        qx[tb] += lo_f32(q[0]) * x[0] + hi_f32(q[0]) * x[1] + lo_f32(q[1]) * x[2] + hi_f32(q[1]) * x[3];
+                    }
+                }
+            }
+#pragma unroll
+            for (int tb = 0; tb < 4; ++tb) {
+                const float v = sum_rows4(qx[tb]);
+                if (g16 == 0) S.red[wave][16 * tb + l16] = v * kQScale;
+            }
+        }
+
+        const float decay_n = Gc.scal[0];
+        const float m_next = Gc.scal[1];
+        const float s_new = Gc.scal[2];
+        const float c_scale = Gc.scal[3];   // != 1: apply this chunk's decay to C_acc eagerly
+        if (c_scale != 1.0f) {
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+                for (int pp = 0; pp < 4; ++pp)
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) Ct[dt][pp][e] *= c_scale;
+        }
+        const int tr_row = (l16 >> 2) + 8 * g16;
+        const int tr_col = 4 * (l16 & 3);
+        // C^T += (w e^{-s} V)^T K (hi, then lo): A = the weighted V^T rows in the pair order (row l16 of
+        // tile (pp, e) is v = 32 pp + 8 (l16 / 4) + 4 e + l16 % 4), B = K read transposed (this wave's d)
+        {
+            const uint16_t* Ks = S.K[wave / 4];
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+                u32x4_t kt[2];
+#pragma unroll
+                for (int dt = 0; dt < 2; ++dt) {
+                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * (wave % 4) + 16 * dt + tr_col];
+                    kt[dt] = cat(tr_read(kb), tr_read(kb + 4 * QP));
+                }
+#pragma unroll
+                for (int pp = 0; pp < 4; ++pp)
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int off = (32 * pp + 8 * (l16 >> 2) + 4 * e + (l16 & 3)) * TP + 32 * ks + 8 * g16;
+                        const u32x4_t vh = *reinterpret_cast<const u32x4_t*>(&S.Vw[0][off]);
+                        const u32x4_t vl = *reinterpret_cast<const u32x4_t*>(&S.Vw[1][off]);
+#pragma unroll
+                        for (int dt = 0; dt < 2; ++dt) {
+                            Ct[dt][pp][e] = mfma16(vh, kt[dt], Ct[dt][pp][e]);
+                            Ct[dt][pp][e] = mfma16(vl, kt[dt], Ct[dt][pp][e]);
+                        }
+                    }
+            }
+        }
+        // n_p = decay n_p + K_p^T w over this wave's 16 columns of each block: A = w as bf16 hi / lo
+        // rows, B = K read transposed
+        const float* n_old = S.n[cur];
+        float* n_new = S.n[cur ^ 1];
+#pragma unroll
+        for (int p = 0; p < NDB; ++p) {
+            const uint16_t* Ks = S.K[p];
+            f32x4_t nacc = f32x4_t{};
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+                const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&Gc.wb[l16 & 1][32 * ks + 8 * g16])
+                                             : u32x4_t{0u, 0u, 0u, 0u};
+                const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * wave + tr_col];
+                nacc = mfma16(wa, cat(tr_read(kb), tr_read(kb + 4 * QP)), nacc);
+            }
+            if (g16 == 0) {
+                const int d = p * DB + 16 * wave + l16;
+                n_new[d] = decay_n * n_old[d] + nacc[0] + nacc[1];
+            }
+        }
+        s_off = s_new;
+        m_prev = m_next;
+    }
+    __syncthreads();
+    if (c_begin < c_end && tid < L) {
+        const int t0 = (c_end - 1) * L;   // the last chunk's q^ . X share
+        if (t0 + tid < A.T) {
+            float qx = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) qx += S.red[w][tid];
+            A.part[(st + t0 + tid) * A.part_stride + tile] = qx;
+        }
+    }
+}
+
+hipError_t launch_walk(const WalkArgs& a, hipStream_t stream) {
+    const size_t lds = sizeof(WalkSmem);
+    static std::atomic<uint64_t> raised{0};
+    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_walk_kernel), lds, raised);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bwd_walk_kernel, dim3(static_cast<unsigned>(a.S * a.G * kNTile)), dim3(kThreads), lds, stream,
+                       a);
+    return hipGetLastError();
+}
+
+// The walk after the prefill's segment schedule (local pass in the bf16 hi + lo form, combine), which
+// gives the entry states of the segments; q, k, v and dh are contiguous [S, T, D] rows.
+size_t bwd_walk_workspace_bytes(int64_t S, int T) {
+    return chunk_mfma_workspace_bytes(static_cast<int>(S), 1, T, kDQK, kDV, kBL);
+}
+
+hipError_t launch_bwd_walk(const ChunkArgs& a, const void* dh, float* slots, float* seg, float* X, float* part,
+                           hipStream_t stream) {
+    if (a.T == 0) return hipSuccess;
+    const SegmentShape sh = segment_shape(a.B, a.NH, a.T, kBL, seg != nullptr);
+    hipError_t e = launch_segment_states(a, kBL, sh, seg, true, stream);
+    if (e != hipSuccess) return e;
+    WalkArgs w{};
+    w.q = static_cast<const uint16_t*>(a.q);
+    w.k = static_cast<const uint16_t*>(a.k);
+    w.v = static_cast<const uint16_t*>(a.v);
+    w.dh = static_cast<const uint16_t*>(dh);
+    w.nh_magic = 0;
+    w.sk[0] = 0;
+    w.sk[1] = static_cast<int64_t>(a.T) * kDQK;
+    w.sv[0] = 0;
+    w.sv[1] = static_cast<int64_t>(a.T) * kDV;
+    w.rk = kDQK * 2;
+    w.rv = kDV * 2;
+    w.ipre = a.ipre;
+    w.fpre = a.fpre;
+    w.C0 = a.C0;
+    w.n0 = a.n0;
+    w.m0 = a.m0;
+    w.seg = seg;
+    w.out = slots;
+    w.X = X;
+    w.part = part;
+    w.part_stride = kPartF;
+    w.S = a.B * a.NH;
+    w.T = a.T;
+    w.G = sh.G;
+    w.R = sh.R;
+    w.NS = (sh.G - 1) * sh.R;
+    w.seg_chunks = sh.seg_chunks;
+    return launch_walk(w, stream);
 }
 
 // ---- X: the sum of the walk's tile partials, into dq ---------------------------------------------
@@ -831,7 +1275,7 @@ BwdLayout bwd_layout(int64_t S, int T) {
         return o;
     };
     L.slots = take(static_cast<size_t>(S * NC1 * kSlotFloats) * 4);
-    L.seg = take(bwd_walk_workspace_bytes(static_cast<int>(S), 1, T));
+    L.seg = take(bwd_walk_workspace_bytes(S, T));
     L.xp = take(static_cast<size_t>(4 * S * T * kDQK) * 4);
     L.hl = take(static_cast<size_t>(S * NC1 * 2 * kCV) * 2);
     L.lz0 = take(static_cast<size_t>(S * kLzFloats) * 4);
@@ -898,7 +1342,7 @@ hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t 
     p.NC = (T + kBL - 1) / kBL;
 
     float* X = reinterpret_cast<float*>(ws + L.xp);
-    hipError_t e = launch_bwd_walk(a.f, a.dh, p.slots, reinterpret_cast<float*>(ws + L.seg), X, p.part, kPartF, stream);
+    hipError_t e = launch_bwd_walk(a.f, a.dh, p.slots, reinterpret_cast<float*>(ws + L.seg), X, p.part, stream);
     if (e != hipSuccess) return e;
     const int64_t n4 = static_cast<int64_t>(S) * T * kDQK / 4;
     hipLaunchKernelGGL(bwd_xsum_kernel, dim3(static_cast<unsigned>((n4 + 255) / 256)), dim3(256), 0, stream, X, a.dq, n4);

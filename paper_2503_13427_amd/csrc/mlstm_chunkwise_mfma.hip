@@ -63,71 +63,11 @@
 // kernel runs every segment from its entry state.
 #include <mutex>
 
+#include "chunk_common.h"
 #include "launch.h"
-#include "mfma_common.h"
 
 namespace mlstm {
 namespace {
-
-constexpr int kThreads = 512;
-constexpr int kWaves = 8;
-constexpr int kGateWave = kWaves - 1; // the wave with the least MFMA work runs the gate scans
-constexpr float kRenorm = -20.0f;     // rescale C eagerly when its lazy log-scale would drop below this
-
-template <int L>
-struct Cfg {
-    static constexpr int NDB = (L == 128) ? 4 : 2;  // d blocks staged per chunk
-    static constexpr int DB = kDQK / NDB;           // 128 or 64
-    static constexpr int DT = DB / 16;              // 16-row C tiles per d block
-    // row pitch (elements) of Q and K blocks: 288 bytes (L = 64) or 160 bytes (L = 128) keep the
-    // 16-byte row reads of 16 consecutive rows free of bank conflicts (a 144-byte pitch measured 1.6%
-    // slower on the B = 4 x T = 32768 prefill)
-    static constexpr int QP = DB + 16;
-    static constexpr int SP = (L == 64) ? L + 16 : L + 8;   // row pitch of S~ (160 bytes at L = 64)
-    static constexpr int NB = L / 16;               // 16-wide blocks along the chunk
-    static constexpr int QKE = L * QP;              // elements of one Q or K block buffer
-    // L = 128: S~ lives in the second Q/K buffer set, which is free from the end of the
-    // chunk's last d block to the next chunk's first store into it; this keeps the
-    // workgroup within the 160 KB of LDS
-    static constexpr bool ST_ALIAS = (L == 128);
-    // Wave split of the workgroup's 256 x 128 slice of C: DH d partitions x (8 / DH) column
-    // groups of VT = DH 16-column tiles.  DH = 2 (L = 64) halves the Q and K^T operand reads of
-    // (iii) and (iv) at the price of summing the two partial read-outs of (iii) through LDS;
-    // L = 128 keeps DH = 1 (its read-out accumulators would not fit twice).
-    static constexpr int DH = (L == 64) ? 2 : 1;
-    static constexpr int VT = DH;
-    static constexpr int NVG = kWaves / DH;
-    // V is kept in LDS transposed (rows v, tau contiguous, pitch TP), once plain for (ii) and once
-    // scaled by the C-update key weights for (iv), so both read it with plain 16-byte row reads
-    static constexpr int TP = L + 8;
-    // L = 128 stages K only transposed (K^T rows [d][tau], pitch KTP, transposed on the matrix cores
-    // like V): (iv) and the n update read it with 16-byte row reads, (i) with transpose reads.  L = 64
-    // stages K rows (its LDS holds no room for a second layout next to the read-out exchange).
-    static constexpr bool KT = (L == 128);
-    static constexpr int KTP = L + 8;
-    static constexpr int KTE = DB * KTP;
-    static constexpr int SETE = QKE + (KT ? KTE : QKE);   // elements of one d-block set: Q, then K
-};
-
-// Physical K^T row of d (within a d block): bit 2 flipped when bit 4 is set, so that the 16 rows an
-// (iv) operand reads (d = 32 pp + 8 i + 4 e + 0..3, i = 0..3) and the 16 consecutive rows an n-update
-// operand reads fall in 16 different 4-bank groups at a 272-byte pitch; four consecutive d stay
-// consecutive (the transpose reads of (i) take them four at a time).
-__device__ __forceinline__ int kt_row(int d) { return d ^ (((d >> 4) & 1) << 2); }
-
-// Per-chunk gate quantities, written one chunk ahead by the gate wave.
-template <int L>
-struct alignas(16) GateBuf {
-    float x2[L];        // (i~ - b) * log2 e
-    float M2[L];        // M * log2 e (0 for a row with no input at all)
-    int R[L];           // last restart (forget gate exactly zero) at or before the row, -1: none
-    float interC[L];    // exp(m_prev - M + s) / sqrt(DQK): scale of C_acc^T Q^T
-    float interN[L];    // exp(m_prev - M) / sqrt(DQK):     scale of Q n
-    float floorv[L];    // exp(-(b + M))
-    float wC[L];        // C-update weights exp(x - M_L - s_new)
-    uint16_t wb[2][L];  // n-update weights exp(x - M_L) as bf16 hi / lo rows
-    float scal[4];      // [0] n decay, [1] m_next, [2] s_new, [3] eager C scale (1: none)
-};
 
 template <int L>
 struct Smem {
@@ -150,21 +90,12 @@ struct Smem {
 static_assert(Cfg<128>::ST_ALIAS && 128 * Cfg<128>::SP <= Cfg<128>::SETE, "S~ must fit in one Q/K set");
 static_assert(sizeof(Smem<64>) <= 160 * 1024 && sizeof(Smem<128>) <= 160 * 1024, "LDS budget");
 
-// Per-thread staging registers: one Q/K d block and one chunk of V in flight.
-// NT: the threads that stage (all of the workgroup, or its intra waves in the warp-specialised kernel)
-template <int L, int NT = kThreads>
+// Per-thread staging registers: one Q/K d block in flight (V: VRegs).
+template <int L>
 struct QKRegs {
-    static constexpr int N = (L * Cfg<L>::DB / 8) / NT;   // 16-byte pieces per thread per matrix
+    static constexpr int N = (L * Cfg<L>::DB / 8) / kThreads;   // 16-byte pieces per thread per matrix
     u32x4_t q[N];
     u32x4_t k[N];
-};
-// V is staged in VPARTS parts (two at L = 128, whose four d blocks leave time for it) so
-// that fewer registers hold it at once.
-template <int L, int NT = kThreads>
-struct VRegs {
-    static constexpr int PARTS = (Cfg<L>::NDB >= 3) ? 2 : 1;
-    static constexpr int N = (L * kDVT / 8) / NT / PARTS;   // pieces per thread per part
-    u32x4_t v[N];
 };
 
 
@@ -176,26 +107,26 @@ struct VRegs {
 // sequence fall outside the buffer range and read as zero in a partial last chunk; the scalar offset
 // carries only the column base.  Row strides (bytes) come from the call: q, k and v may be strided
 // views of one projection output.
-template <int L, int NT = kThreads>
-__device__ __forceinline__ void load_qk(QKRegs<L, NT>& r, const SeqRsrc& R, int t0, int p, int tid, uint32_t rq,
+template <int L>
+__device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, int p, int tid, uint32_t rq,
                                         uint32_t rk) {
-    constexpr int NW = NT / 64;
+    constexpr int NW = kWaves;
     constexpr int DB = Cfg<L>::DB, PR = DB / 8;   // 16-byte pieces per row
     const uint32_t soff = p * (DB * 2);
 #pragma unroll
-    for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
-        const int item = tid + i * NT;
+    for (int i = 0; i < QKRegs<L>::N; ++i) {
+        const int item = tid + i * kThreads;
         const uint32_t row = static_cast<uint32_t>(t0 + item / PR), col = 16 * (item % PR);
         r.q[i] = bload128(R.q, row * rq + col, soff);
         if constexpr (!Cfg<L>::KT) r.k[i] = bload128(R.k, row * rk + col, soff);
     }
     if constexpr (Cfg<L>::KT) {
-        static_assert(QKRegs<L, NT>::N * NW == (L / 16) * (DB / 32), "pieces of one K block");
+        static_assert(QKRegs<L>::N * NW == (L / 16) * (DB / 32), "pieces of one K block");
         int ln = tid & 63;   // opaque: recomputed per call rather than held across the loop
         asm volatile("" : "+v"(ln));
         const int wave = tid >> 6;
 #pragma unroll
-        for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
+        for (int i = 0; i < QKRegs<L>::N; ++i) {
             const int pc = wave + NW * i, a = pc % (L / 16), b = pc / (L / 16);
             r.k[i] = bload128(R.k, static_cast<uint32_t>(t0 + 16 * a + (ln & 15)) * rk + (32 * b + 8 * (ln >> 4)) * 2,
                               soff);
@@ -216,12 +147,12 @@ __device__ __forceinline__ void onehot_pair(u32x4_t (&E)[2], int lane) {
         for (int d = 0; d < 4; ++d) E[h][d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
     }
 }
-template <int L, int NT = kThreads>
-__device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKRegs<L, NT>& r, int tid) {
-    constexpr int PR = Cfg<L>::DB / 8, QP = Cfg<L>::QP, NW = NT / 64;
+template <int L>
+__device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKRegs<L>& r, int tid) {
+    constexpr int PR = Cfg<L>::DB / 8, QP = Cfg<L>::QP, NW = kWaves;
 #pragma unroll
-    for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
-        const int item = tid + i * NT;
+    for (int i = 0; i < QKRegs<L>::N; ++i) {
+        const int item = tid + i * kThreads;
         const int off = (item / PR) * QP + 8 * (item % PR);
         MLSTM_CHECK(off >= 0 && off + 8 <= Cfg<L>::QKE, kDbgChunkMfma);
         *reinterpret_cast<u32x4_t*>(&Qd[off]) = r.q[i];
@@ -236,7 +167,7 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
         onehot_pair(E, lane);
         const int l16 = lane & 15, g16 = lane >> 4;
 #pragma unroll
-        for (int i = 0; i < QKRegs<L, NT>::N; ++i) {
+        for (int i = 0; i < QKRegs<L>::N; ++i) {
             const int pc = wave + NW * i, a = pc % (L / 16), b = pc / (L / 16);
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
@@ -248,61 +179,14 @@ __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKReg
         }
     }
 }
-// V pieces in the MFMA A-operand layout for vt_transpose: for piece i of part `part`, lane (l16, g16)
-// of wave w holds V[tau 16 a + l16][v 32 b + 8 g16 + 0..7] with pc = w + 8 (part N + i) and
-// (a, b) = (pc % (L / 16), pc / (L / 16)), so the workgroup's pieces cover the L x 128 chunk once.
-template <int L, int NT = kThreads>
-__device__ __forceinline__ void load_v_tr(VRegs<L, NT>& r, const SeqRsrc& R, int t0, int v0, int wave, int lane, int part,
-                                          uint32_t rv) {
-    constexpr int NW = NT / 64;
-    static_assert(VRegs<L, NT>::PARTS * VRegs<L, NT>::N * NW == (L / 16) * (kDVT / 32), "pieces of one L x 128 chunk");
-    constexpr int NA = L / 16;
-    const uint32_t soff = v0 * 2;   // the row offset goes in the per-lane offset
-    int ln = lane;   // opaque: the offsets are recomputed per call rather than held across the loop
-    asm volatile("" : "+v"(ln));
-#pragma unroll
-    for (int i = 0; i < VRegs<L, NT>::N; ++i) {
-        const int pc = wave + NW * (part * VRegs<L, NT>::N + i), a = pc % NA, b = pc / NA;
-        r.v[i] = bload128(R.v, static_cast<uint32_t>(t0 + 16 * a + (ln & 15)) * rv + (32 * b + 8 * (ln >> 4)) * 2, soff);
-    }
-}
-template <int L, int NT = kThreads>
-using VtPacked = u32x2_t[2 * VRegs<L, NT>::N * VRegs<L, NT>::PARTS];
-// The transposition on the matrix cores: D = A E_h with A a piece (16 tau x 32 v) and E_h the 32 x 16
-// one-hot selection of its columns 16 h + 0..15 (exact in fp32).  Lane (n = l16, g16) of D holds
-// V[tau 16 a + 4 g16 + j][v 32 b + 16 h + n], j = 0..3: four consecutive tau of one row of V^T, kept
-// packed in pv until the stores below.
-template <int L, int NT = kThreads>
-__device__ __forceinline__ void vt_transpose(VtPacked<L, NT>& pv, const VRegs<L, NT>& r, int lane, int part) {
-    // E_h in the B-operand layout: lane (l16, g16) holds k slots 8 g16 + 0..7 of column l16, whose
-    // one (if any) is slot 16 h + l16.  Built from an opaque copy of the lane index so that it is not
-    // hoisted out of the chunk loop (eight more registers held across the loop would spill).
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    u32x4_t E[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const int pos = 16 * h + (ln & 15) - 8 * (ln >> 4);
-        const uint32_t one = (pos & 1) ? 0x3F800000u : 0x3F80u;
-#pragma unroll
-        for (int d = 0; d < 4; ++d) E[h][d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
-    }
-#pragma unroll
-    for (int i = 0; i < VRegs<L, NT>::N; ++i)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const f32x4_t d = mfma16(r.v[i], E[h], f32x4_t{});
-            pv[2 * (part * VRegs<L, NT>::N + i) + h] = u32x2_t{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
-        }
-}
 // (w V)^T from the packed V^T: row weights wC of the chunk, rounded to bf16 once
-template <int L, int NT = kThreads>
-__device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const VtPacked<L, NT>& pv, const float* wC, int wave,
+template <int L>
+__device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const VtPacked<L>& pv, const float* wC, int wave,
                                                 int lane) {
-    constexpr int TP = Cfg<L>::TP, NA = L / 16, NW = NT / 64;
+    constexpr int TP = Cfg<L>::TP, NA = L / 16, NW = kWaves;
     const int l16 = lane & 15, g16 = lane >> 4;
 #pragma unroll
-    for (int i = 0; i < VRegs<L, NT>::N * VRegs<L, NT>::PARTS; ++i) {
+    for (int i = 0; i < VRegs<L>::N * VRegs<L>::PARTS; ++i) {
         const int pc = wave + NW * i, a = pc % NA, b = pc / NA;
         const int tau = 16 * a + 4 * g16;
         const f32x4_t w = *reinterpret_cast<const f32x4_t*>(&wC[tau]);
@@ -317,12 +201,12 @@ __device__ __forceinline__ void vt_store_scaled(uint16_t* VwT, const VtPacked<L,
         }
     }
 }
-template <int L, int NT = kThreads>
-__device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const VtPacked<L, NT>& pv, int wave, int lane) {
-    constexpr int TP = Cfg<L>::TP, NA = L / 16, NW = NT / 64;
+template <int L>
+__device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const VtPacked<L>& pv, int wave, int lane) {
+    constexpr int TP = Cfg<L>::TP, NA = L / 16, NW = kWaves;
     const int l16 = lane & 15, g16 = lane >> 4;
 #pragma unroll
-    for (int i = 0; i < VRegs<L, NT>::N * VRegs<L, NT>::PARTS; ++i) {
+    for (int i = 0; i < VRegs<L>::N * VRegs<L>::PARTS; ++i) {
         const int pc = wave + NW * i, a = pc % NA, b = pc / NA;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -332,106 +216,6 @@ __device__ __forceinline__ void vt_store_plain(uint16_t* VtT, const VtPacked<L, 
     }
 }
 // Gate pre-activations of one chunk, one (L = 64) or two (L = 128) per lane of the gate wave.
-template <int L>
-__device__ __forceinline__ void load_gates(float (&gi)[2], float (&gf)[2], const SeqRsrc& R, int t0, int lane) {
-    const uint32_t goff = static_cast<uint32_t>(t0 + lane) * 4;   // range-checked: zero past the end
-    gi[0] = bloadf(R.ig, goff, 0);
-    gf[0] = bloadf(R.fg, goff, 0);
-    if constexpr (L == 128) {
-        gi[1] = bloadf(R.ig, goff + 256, 0);
-        gf[1] = bloadf(R.fg, goff + 256, 0);
-    }
-}
-
-
-// Gate phase of one chunk (run by one wave): in-chunk prefix sums and maxima, the max
-// state, the lazy C scale, and every per-row scale of the chunk.  m_prev and s_cur
-// carry the max state and the lazy log-scale from chunk to chunk.  Rows at or beyond
-// nvalid (the partial last chunk of a sequence) are neutral tokens: no input (x = -inf)
-// and no decay (logsig f~ = 0), so they leave the state unchanged.
-//
-// A forget gate of exactly zero (f~ = -inf, a document border) restarts the state: nothing
-// before that token reaches it or any later token.  The prefix sum b skips the restart token
-// (the decay from s to t over tokens s+1..t never includes a restart for the pairs that
-// survive), every row keeps R, its last restart at or before it, and the row's maxima, weights
-// and entry-state terms cover only the tokens from R on.  A chunk that holds a restart drops
-// its entry state: C and n are scaled by zero before this chunk's keys are added.
-template <int L>
-__device__ __forceinline__ void gate_phase(GateBuf<L>& Gb, const float (&gi)[2], const float (&gf)[2], float& m_prev,
-                                           float& s_cur, int lane, int nvalid) {
-    const bool ok0 = lane < nvalid;
-    const float lg0 = ok0 ? flogsig(gf[0]) : 0.0f;
-    const bool rs0 = (lg0 == -INFINITY);
-    bool rs1 = false;
-    float lg1 = 0.f;
-    if constexpr (L == 128) {
-        lg1 = (64 + lane < nvalid) ? flogsig(gf[1]) : 0.0f;
-        rs1 = (lg1 == -INFINITY);
-    }
-    // restarts are rare: a chunk without one (a wave-uniform test) takes the plain scans
-    const bool any_restart = __builtin_amdgcn_ballot_w64(rs0 || rs1) != 0;
-    const float b = wave_incl_sum(rs0 ? 0.0f : lg0);
-    const float x = ok0 ? gi[0] - b : -INFINITY;
-    float r = -1.f, p;
-    if (any_restart) {
-        r = wave_incl_max(rs0 ? static_cast<float>(lane) : -1.0f);
-        p = wave_seg_incl_max(x, rs0);
-    } else {
-        p = wave_incl_max(x);
-    }
-    float b2 = 0.f, x2 = 0.f, p2 = 0.f, r2 = -1.f;
-    if constexpr (L == 128) {
-        const bool ok1 = 64 + lane < nvalid;
-        b2 = lane63(b) + wave_incl_sum(rs1 ? 0.0f : lg1);
-        x2 = ok1 ? gi[1] - b2 : -INFINITY;
-        if (any_restart) {
-            const float r_own = wave_incl_max(rs1 ? static_cast<float>(64 + lane) : -1.0f);
-            r2 = fmaxf(lane63(r), r_own);
-            const float q2 = wave_seg_incl_max(x2, rs1);
-            p2 = (r_own >= 0.0f) ? q2 : fmaxf(lane63(p), q2);
-        } else {
-            p2 = fmaxf(lane63(p), wave_incl_max(x2));
-        }
-    }
-    const float pL = lane63(L == 128 ? p2 : p);
-    const float bL = lane63(L == 128 ? b2 : b);
-    const float rL = lane63(L == 128 ? r2 : r);
-    const bool restart = (rL >= 0.0f);
-    const float ML = restart ? pL : fmaxf(m_prev, pL);
-    // an empty state (m = -inf) has nothing to decay, and a restart drops the state
-    const bool empty = restart || (m_prev == -INFINITY);
-    const float dlog = empty ? 0.0f : m_prev - ML;
-    const float s_try = s_cur + dlog;
-    const bool eager = restart || s_try < kRenorm;
-    const float s_new = eager ? 0.0f : s_try;
-    auto emit = [&](int tau, float bb, float xx, float pp, float rr) {
-        const bool fresh = (rr >= 0.0f);   // a restart at or before this row: no entry-state term
-        const float M = fresh ? pp : fmaxf(m_prev, pp);
-        Gb.x2[tau] = xx * kLog2e;
-        Gb.M2[tau] = (M == -INFINITY) ? 0.0f : M * kLog2e;
-        Gb.R[tau] = static_cast<int>(rr);
-        Gb.interC[tau] = (fresh || M == -INFINITY) ? 0.0f : fexp(m_prev - M + s_cur) * kQScale;
-        Gb.interN[tau] = (fresh || M == -INFINITY) ? 0.0f : fexp(m_prev - M) * kQScale;
-        Gb.floorv[tau] = fexp(-(bb + M));
-        const bool none = (xx == -INFINITY) || (static_cast<float>(tau) < rL);
-        Gb.wC[tau] = none ? 0.0f : fexp(xx - ML - s_new);
-        const float wn = none ? 0.0f : fexp(xx - ML);
-        const uint16_t whi = f32_to_bf16(wn);
-        Gb.wb[0][tau] = whi;
-        Gb.wb[1][tau] = f32_to_bf16(wn - bf16_to_f32(whi));
-    };
-    emit(lane, b, x, p, r);
-    if constexpr (L == 128) emit(64 + lane, b2, x2, p2, r2);
-    const float m_next = bL + ML;
-    if (lane == 0) {
-        Gb.scal[0] = (empty || ML == -INFINITY) ? 0.0f : fexp(m_prev - ML);
-        Gb.scal[1] = m_next;
-        Gb.scal[2] = s_new;
-        Gb.scal[3] = restart ? 0.0f : (eager ? fexp(s_try) : 1.0f);
-    }
-    m_prev = m_next;
-    s_cur = s_new;
-}
 
 
 struct ChunkKernelArgs {
@@ -460,20 +244,6 @@ struct ChunkKernelArgs {
     uint32_t rq, rk, rv;           // their row (token) strides in bytes
 };
 
-// First row of sequence s = (batch b, head s - b NH), written as s st_h + b (st_b - NH st_h) with
-// st = {st_b - NH st_h, st_h}, and the byte span of its T rows of D elements.  b = floor(s / NH)
-// comes from a multiply by the host's nh_magic (nh_magic = 0 stands for NH = 1, b = s): it is exact
-// while s NH < 2^32 (the host checks this for strided calls), and contiguous rows have st[0] = 0.
-// (An integer division, the form b st_b + (s - b NH) st_h, and this helper itself in the chunk
-// kernel all made the compiler's code for its chunk loop markedly slower; the chunk kernel writes the
-// same sum out in place.)
-__device__ __forceinline__ const uint16_t* seq_rows(const uint16_t* p, int s, uint32_t nh_magic, const int64_t (&st)[2]) {
-    const int b = nh_magic ? static_cast<int>(__umulhi(static_cast<uint32_t>(s), nh_magic)) : s;
-    return p + static_cast<int64_t>(s) * st[1] + static_cast<int64_t>(b) * st[0];
-}
-__device__ __forceinline__ uint32_t seq_span(int T, uint32_t row_bytes, int D) {
-    return T > 0 ? static_cast<uint32_t>(T - 1) * row_bytes + static_cast<uint32_t>(D) * 2u : 0u;
-}
 
 // row pitch (floats) of the entry-state staging of a 256 x 128 tile in LDS: 528 bytes puts the
 // rows 8 apart that one read of the accumulator pickup touches in different banks
@@ -1367,407 +1137,6 @@ hipError_t launch_local(const LocalArgs& a, int S, hipStream_t stream, bool hilo
 // sub-segments of a local segment: at most kLocMax tokens each
 int local_subsegments(int seg_tokens) { return (seg_tokens + kLocMax - 1) / kLocMax; }
 
-// ---- the backward's forward walk ----------------------------------------------------------------
-// The backward needs, for every 64-token chunk c, X_c = dH_c C_c^T on the state C_c entering the chunk
-// (the inter-chunk term of dq), with q^_t . X_t, and the chunk's entry normaliser and max state.  A
-// walk over the chunks gives them without writing the states out: one workgroup of 8 waves per
-// (sequence, 128-column dv tile, segment), with the gate phase and lazy scale of chunk_mfma_kernel<64>,
-// holds its 256 x 128 slice of C in registers and per chunk
-//   - forms X^T = C dH^T over its 128 columns (the four tiles' partial sums are added by the
-//     backward) and its share of q^ . X,
-//   - applies the update C += K^T (w e^{-s} V), the weighted values as a bf16 pair hi + lo (products
-//     to about 2^-17 rather than the 2^-9 of one rounding, because the backward's gradients can
-//     cancel against the state), and n += K^T w,
-//   - writes n and m entering the chunk into slot c - 1 (tile 0).
-// Layout: wave w owns d = 32 w + 0..31 (two 16-column tiles dt) and all 128 v, as accumulator tiles
-// of C^T: tile (dt, pp, e) lane (l16, g16) holds C[32 w + 16 dt + l16][32 pp + 8 g16 + 4 e + j],
-// j = 0..3.  The two tiles e of a pair give a lane eight consecutive v, the A operand of C dH^T (with
-// 16-byte reads of dH rows); the update reads the weighted V^T rows in the same permuted order.
-// Segment g >= 1 enters from the segment slots of the local pass (in its hi + lo form) and the
-// combine.
-constexpr int kWalkHP = kDVT + 8;   // dH row pitch (elements): 272 bytes
-struct WalkSmem {
-    uint16_t K[Cfg<64>::NDB][64 * Cfg<64>::QP];   // the chunk's K rows, two d blocks of 128
-    uint16_t Vw[2][kDVT * Cfg<64>::TP];           // (w e^{-s} V)^T of the chunk as bf16 hi [0] and lo [1]
-    uint16_t dH[64 * kWalkHP];                     // the chunk's dH rows, this tile's 128 columns
-    float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
-    GateBuf<64> G[2];                              // by chunk parity
-    float red[kWaves][64];                         // q^ . X partial sums per wave
-};
-static_assert(sizeof(WalkSmem) <= 160 * 1024, "LDS budget");
-
-struct WalkArgs {
-    const uint16_t* q;    // [S, T, DQK] rows
-    const uint16_t* k;
-    const uint16_t* v;
-    const uint16_t* dh;   // [S, T, DV] rows
-    const float* ipre;
-    const float* fpre;
-    const float* C0;      // entry state of segment 0 (NULL: zero state, m = m0 or 0)
-    const float* n0;
-    const float* m0;
-    const float* seg;     // segment slots of the local pass and the combine (G > 1)
-    float* out;           // S (NC - 1) chunk slots: n and m entering chunk c >= 1 in slot c - 1
-    float* X;             // kNTile x [S, T, DQK]: X^T partial sums over each tile's columns
-    float* part;          // [S, T, part_stride]: q^ . X partial sum of tile j at offset j
-    int part_stride;
-    int S;
-    int T;
-    int G;                // segments per sequence
-    int R;                // local sub-segments per segment; segment g >= 1 enters from slot g R - 1
-    int NS;               // segment slots per sequence, (G - 1) R
-    int seg_chunks;       // chunks per segment (the last may be shorter)
-    uint32_t nh_magic;    // as in ChunkKernelArgs
-    int64_t sk[2], sv[2];
-    uint32_t rk, rv;
-};
-
-// the chunk's K rows, both d blocks: two 16-byte pieces per thread and block
-constexpr int kWalkKP = 64 * (Cfg<64>::DB / 8) / kThreads;
-__device__ __forceinline__ void walk_load_k(u32x4_t (&r)[Cfg<64>::NDB][kWalkKP], const SeqRsrc& R, int t0, int tid,
-                                            uint32_t rk) {
-    constexpr int PR = Cfg<64>::DB / 8;
-#pragma unroll
-    for (int p = 0; p < Cfg<64>::NDB; ++p)
-#pragma unroll
-        for (int i = 0; i < kWalkKP; ++i) {
-            const int item = tid + i * kThreads;
-            r[p][i] = bload128(R.k, static_cast<uint32_t>(t0 + item / PR) * rk + 16 * (item % PR), p * Cfg<64>::DB * 2);
-        }
-}
-__device__ __forceinline__ void walk_store_k(WalkSmem& S, const u32x4_t (&r)[Cfg<64>::NDB][kWalkKP], int tid) {
-    constexpr int PR = Cfg<64>::DB / 8;
-#pragma unroll
-    for (int p = 0; p < Cfg<64>::NDB; ++p)
-#pragma unroll
-        for (int i = 0; i < kWalkKP; ++i) {
-            const int item = tid + i * kThreads;
-            const int off = (item / PR) * Cfg<64>::QP + 8 * (item % PR);
-            MLSTM_CHECK(off + 8 <= 64 * Cfg<64>::QP, kDbgChunkMfma);
-            *reinterpret_cast<u32x4_t*>(&S.K[p][off]) = r[p][i];
-        }
-}
-// the chunk's dH rows, this tile's 128 columns: two 16-byte pieces per thread
-__device__ __forceinline__ void walk_load_dh(u32x4_t (&r)[2], __amdgpu_buffer_rsrc_t rdh, int t0, int v0, int tid) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int item = tid + i * kThreads;
-        r[i] = bload128(rdh, static_cast<uint32_t>((t0 + item / 16) * kDV + v0 + 8 * (item % 16)) * 2u, 0);
-    }
-}
-__device__ __forceinline__ void walk_store_dh(WalkSmem& S, const u32x4_t (&r)[2], int tid) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int item = tid + i * kThreads;
-        *reinterpret_cast<u32x4_t*>(&S.dH[(item / 16) * kWalkHP + 8 * (item % 16)]) = r[i];
-    }
-}
-// (w V)^T from the packed V^T as a bf16 pair: hi = bf16(w v), lo = bf16(w v - hi)
-__device__ __forceinline__ void vt_store_hilo(WalkSmem& S, const VtPacked<64>& pv, const float* wC, int wave, int lane) {
-    constexpr int TP = Cfg<64>::TP, NA = 64 / 16;
-    const int l16 = lane & 15, g16 = lane >> 4;
-#pragma unroll
-    for (int i = 0; i < VRegs<64>::N * VRegs<64>::PARTS; ++i) {
-        const int pc = wave + kWaves * i, a = pc % NA, b = pc / NA;
-        const int tau = 16 * a + 4 * g16;
-        const f32x4_t w = *reinterpret_cast<const f32x4_t*>(&wC[tau]);
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const u32x2_t x = pv[2 * i + h];
-            const float f0 = lo_f32(x[0]) * w[0], f1 = hi_f32(x[0]) * w[1];
-            const float f2 = lo_f32(x[1]) * w[2], f3 = hi_f32(x[1]) * w[3];
-            u32x2_t oh, ol;
-            oh[0] = pack_bf16x2(f0, f1);
-            oh[1] = pack_bf16x2(f2, f3);
-            ol[0] = pack_bf16x2(f0 - lo_f32(oh[0]), f1 - hi_f32(oh[0]));
-            ol[1] = pack_bf16x2(f2 - lo_f32(oh[1]), f3 - hi_f32(oh[1]));
-            const int row = 32 * b + 16 * h + l16;
-            MLSTM_CHECK(row < kDVT && tau + 4 <= TP, kDbgChunkMfma);
-            *reinterpret_cast<u32x2_t*>(&S.Vw[0][row * TP + tau]) = oh;
-            *reinterpret_cast<u32x2_t*>(&S.Vw[1][row * TP + tau]) = ol;
-        }
-    }
-}
-
-__global__ void __launch_bounds__(kThreads, 1) bwd_walk_kernel(WalkArgs A) {
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-    WalkSmem& S = *reinterpret_cast<WalkSmem*>(smem_raw);
-    constexpr int L = 64;
-    using CF = Cfg<64>;
-    constexpr int QP = CF::QP, TP = CF::TP, DB = CF::DB, NDB = CF::NDB;
-    constexpr int NKS = L / 32;
-    static_assert(DB / 16 == kWaves, "one n-update tile per wave and d block");
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int g16 = lane >> 4, l16 = lane & 15;
-    const bool gate_wave = (wave == kGateWave);
-
-    const int wi = work_index();
-    const int tile = wi % kNTile;
-    const int sg = wi / kNTile;
-    const int g = sg % A.G;
-    const int s = sg / A.G;
-    const int v0 = tile * kDVT;
-    const int nc_total = (A.T + L - 1) / L;
-    const int c_begin = g * A.seg_chunks;
-    const int c_end = min(nc_total, c_begin + A.seg_chunks);
-    MLSTM_CHECK(s < A.S, kDbgChunkMfma);
-    const int64_t st = static_cast<int64_t>(s) * A.T;
-
-    SeqRsrc P;
-    P.k = make_rsrc(seq_rows(A.k, s, A.nh_magic, A.sk), seq_span(A.T, A.rk, kDQK));
-    P.v = make_rsrc(seq_rows(A.v, s, A.nh_magic, A.sv), seq_span(A.T, A.rv, kDV));
-    P.ig = make_rsrc(A.ipre + st, static_cast<uint32_t>(A.T) * 4);
-    P.fg = make_rsrc(A.fpre + st, static_cast<uint32_t>(A.T) * 4);
-    const __amdgpu_buffer_rsrc_t rdh = make_rsrc(A.dh + st * kDV, static_cast<uint32_t>(A.T) * kDV * 2);
-    float* Xt = A.X + static_cast<int64_t>(tile) * A.S * A.T * kDQK;
-
-    // entry state into the C^T tiles: Ct[dt][pp][e][j] = C[dw(dt) + l16][v0 + 32 pp + 8 g16 + 4 e + j]
-    auto dw = [&](int dt) { return 32 * wave + 16 * dt; };
-    f32x4_t Ct[2][4][2];
-    const float* nin;
-    float m_prev;
-    if (g == 0) {
-        const float* C0 = A.C0 ? A.C0 + static_cast<int64_t>(s) * kDQK * kDV : nullptr;
-#pragma unroll
-        for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-            for (int pp = 0; pp < 4; ++pp)
-#pragma unroll
-                for (int e = 0; e < 2; ++e)
-                    Ct[dt][pp][e] = C0 ? *reinterpret_cast<const f32x4_t*>(
-                                             C0 + static_cast<int64_t>(dw(dt) + l16) * kDV + v0 + 32 * pp + 8 * g16 + 4 * e)
-                                       : f32x4_t{};
-        nin = A.n0 ? A.n0 + static_cast<int64_t>(s) * kDQK : nullptr;
-        m_prev = A.m0 ? A.m0[s] : 0.0f;
-    } else {
-        MLSTM_CHECK(g * A.R - 1 >= 0 && g * A.R - 1 < A.NS, kDbgChunkMfma);
-        const float* slot = A.seg + (static_cast<int64_t>(s) * A.NS + g * A.R - 1) * kSlotFloats;
-        // the slot holds four rows interleaved: element (d, v) at slot_c4(d / 4, v) + d % 4
-#pragma unroll
-        for (int dt = 0; dt < 2; ++dt) {
-            const int d = dw(dt) + l16;
-#pragma unroll
-            for (int pp = 0; pp < 4; ++pp)
-#pragma unroll
-                for (int e = 0; e < 2; ++e)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        Ct[dt][pp][e][j] = slot[slot_c4(d / 4, v0 + 32 * pp + 8 * g16 + 4 * e + j) + d % 4];
-        }
-        nin = slot + kDQK * kDV;
-        m_prev = slot[kDQK * kDV + kDQK + 2];
-    }
-    if (tid < kDQK) S.n[0][tid] = nin ? nin[tid] : 0.0f;
-    float s_off = 0.0f;   // C = C_acc e^{s_off}
-    float g_m = m_prev, g_s = 0.0f;
-    float gi[2] = {0.f, 0.f}, gf[2] = {0.f, 0.f};
-
-    u32x4_t rk[NDB][kWalkKP];
-    u32x4_t rdhv[2];
-    VRegs<64> rv;
-    VtPacked<64> pv;
-    if (c_begin < c_end) {
-        const int t0 = c_begin * L;
-        walk_load_k(rk, P, t0, tid, A.rk);
-        load_v_tr<64>(rv, P, t0, v0, wave, lane, 0, A.rv);
-        walk_load_dh(rdhv, rdh, t0, v0, tid);
-        if (gate_wave) {
-            load_gates<64>(gi, gf, P, t0, lane);
-            gate_phase<64>(S.G[c_begin & 1], gi, gf, g_m, g_s, lane, A.T - t0);
-        }
-    }
-
-    for (int c = c_begin; c < c_end; ++c) {
-        const int t0 = c * L;
-        const int cur = (c - c_begin) & 1;
-        const int par = c & 1;
-        const GateBuf<64>& Gc = S.G[par];
-        __syncthreads();   // the previous chunk is done; this chunk's gates and n are visible
-        if (c > c_begin && tid < L && t0 - L + tid < A.T) {
-            // the previous chunk's q^ . X share of this tile
-            float qx = 0.0f;
-#pragma unroll
-            for (int w = 0; w < kWaves; ++w) qx += S.red[w][tid];
-            A.part[(st + t0 - L + tid) * A.part_stride + tile] = qx;
-        }
-        walk_store_k(S, rk, tid);
-        walk_store_dh(S, rdhv, tid);
-        vt_transpose<64>(pv, rv, lane, 0);
-        vt_store_hilo(S, pv, Gc.wC, wave, lane);
-        if (c + 1 < c_end) {
-            walk_load_k(rk, P, t0 + L, tid, A.rk);
-            load_v_tr<64>(rv, P, t0 + L, v0, wave, lane, 0, A.rv);
-            walk_load_dh(rdhv, rdh, t0 + L, v0, tid);
-            if (gate_wave) load_gates<64>(gi, gf, P, t0 + L, lane);
-        }
-        if (c > 0 && tile == 0) {
-            // n and m entering chunk c
-            MLSTM_CHECK(c - 1 < nc_total - 1, kDbgChunkMfma);
-            float* slot = A.out + (static_cast<int64_t>(s) * (nc_total - 1) + c - 1) * kSlotFloats;
-            if (tid < kDQK) slot[kDQK * kDV + tid] = S.n[cur][tid];
-            if (tid == 0) slot[kDQK * kDV + kDQK + 2] = m_prev;
-        }
-        __syncthreads();   // the chunk's K rows, dH rows and weighted V^T are visible
-        // gates of the next chunk, one chunk ahead
-        if (gate_wave && c + 1 < c_end) gate_phase<64>(S.G[par ^ 1], gi, gf, g_m, g_s, lane, A.T - (t0 + L));
-
-        // X^T [d][tau] = sum_v C[d][v] dH[tau][v] over this tile's columns, C as a bf16 pair hi + lo
-        {
-            // the q rows of q^ . X, requested before the products so that their latency is covered
-            u32x2_t qv[2][4];
-#pragma unroll
-            for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-                for (int tb = 0; tb < 4; ++tb) {
-                    const int tau = 16 * tb + l16;
-                    qv[dt][tb] = (t0 + tau < A.T)
-                                     ? *reinterpret_cast<const u32x2_t*>(A.q + (st + t0 + tau) * kDQK + dw(dt) + 4 * g16)
-                                     : u32x2_t{0u, 0u};
-                }
-            f32x4_t X[2][4];
-#pragma unroll
-            for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-                for (int tb = 0; tb < 4; ++tb) X[dt][tb] = f32x4_t{};
-#pragma unroll
-            for (int pp = 0; pp < 4; ++pp) {
-                u32x4_t b[4];
-#pragma unroll
-                for (int tb = 0; tb < 4; ++tb)
-                    b[tb] = *reinterpret_cast<const u32x4_t*>(&S.dH[(16 * tb + l16) * kWalkHP + 32 * pp + 8 * g16]);
-#pragma unroll
-                for (int dt = 0; dt < 2; ++dt) {
-                    const f32x4_t& c0 = Ct[dt][pp][0];
-                    const f32x4_t& c1 = Ct[dt][pp][1];
-                    u32x4_t ah, al;
-                    ah[0] = pack_bf16x2(c0[0], c0[1]);
-                    ah[1] = pack_bf16x2(c0[2], c0[3]);
-                    ah[2] = pack_bf16x2(c1[0], c1[1]);
-                    ah[3] = pack_bf16x2(c1[2], c1[3]);
-                    al[0] = pack_bf16x2(c0[0] - lo_f32(ah[0]), c0[1] - hi_f32(ah[0]));
-                    al[1] = pack_bf16x2(c0[2] - lo_f32(ah[1]), c0[3] - hi_f32(ah[1]));
-                    al[2] = pack_bf16x2(c1[0] - lo_f32(ah[2]), c1[1] - hi_f32(ah[2]));
-                    al[3] = pack_bf16x2(c1[2] - lo_f32(ah[3]), c1[3] - hi_f32(ah[3]));
-#pragma unroll
-                    for (int tb = 0; tb < 4; ++tb) {
-                        X[dt][tb] = mfma16(ah, b[tb], X[dt][tb]);
-                        X[dt][tb] = mfma16(al, b[tb], X[dt][tb]);
-                    }
-                }
-            }
-            // C = C_acc e^{s}; lane (tau = 16 tb + l16, g16) holds X^T[dw(dt) + 4 g16 + 0..3][tau]
-            const float esc = expf(s_off);
-            float qx[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int dt = 0; dt < 2; ++dt) {
-                const int d = dw(dt) + 4 * g16;
-#pragma unroll
-                for (int tb = 0; tb < 4; ++tb) {
-                    const int tau = 16 * tb + l16;
-                    if (t0 + tau < A.T) {
-                        const f32x4_t x = X[dt][tb] * esc;
-                        *reinterpret_cast<f32x4_t*>(Xt + (st + t0 + tau) * kDQK + d) = x;
-                        const u32x2_t q = qv[dt][tb];
-                        qx[tb] += lo_f32(q[0]) * x[0] + hi_f32(q[0]) * x[1] + lo_f32(q[1]) * x[2] + hi_f32(q[1]) * x[3];
-                    }
-                }
-            }
-#pragma unroll
-            for (int tb = 0; tb < 4; ++tb) {
-                const float v = sum_rows4(qx[tb]);
-                if (g16 == 0) S.red[wave][16 * tb + l16] = v * kQScale;
-            }
-        }
-
-        const float decay_n = Gc.scal[0];
-        const float m_next = Gc.scal[1];
-        const float s_new = Gc.scal[2];
-        const float c_scale = Gc.scal[3];   // != 1: apply this chunk's decay to C_acc eagerly
-        if (c_scale != 1.0f) {
-#pragma unroll
-            for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-                for (int pp = 0; pp < 4; ++pp)
-#pragma unroll
-                    for (int e = 0; e < 2; ++e) Ct[dt][pp][e] *= c_scale;
-        }
-        const int tr_row = (l16 >> 2) + 8 * g16;
-        const int tr_col = 4 * (l16 & 3);
-        // C^T += (w e^{-s} V)^T K (hi, then lo): A = the weighted V^T rows in the pair order (row l16 of
-        // tile (pp, e) is v = 32 pp + 8 (l16 / 4) + 4 e + l16 % 4), B = K read transposed (this wave's d)
-        {
-            const uint16_t* Ks = S.K[wave / 4];
-#pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) {
-                u32x4_t kt[2];
-#pragma unroll
-                for (int dt = 0; dt < 2; ++dt) {
-                    const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 32 * (wave % 4) + 16 * dt + tr_col];
-                    kt[dt] = cat(tr_read(kb), tr_read(kb + 4 * QP));
-                }
-#pragma unroll
-                for (int pp = 0; pp < 4; ++pp)
-#pragma unroll
-                    for (int e = 0; e < 2; ++e) {
-                        const int off = (32 * pp + 8 * (l16 >> 2) + 4 * e + (l16 & 3)) * TP + 32 * ks + 8 * g16;
-                        const u32x4_t vh = *reinterpret_cast<const u32x4_t*>(&S.Vw[0][off]);
-                        const u32x4_t vl = *reinterpret_cast<const u32x4_t*>(&S.Vw[1][off]);
-#pragma unroll
-                        for (int dt = 0; dt < 2; ++dt) {
-                            Ct[dt][pp][e] = mfma16(vh, kt[dt], Ct[dt][pp][e]);
-                            Ct[dt][pp][e] = mfma16(vl, kt[dt], Ct[dt][pp][e]);
-                        }
-                    }
-            }
-        }
-        // n_p = decay n_p + K_p^T w over this wave's 16 columns of each block: A = w as bf16 hi / lo
-        // rows, B = K read transposed
-        const float* n_old = S.n[cur];
-        float* n_new = S.n[cur ^ 1];
-#pragma unroll
-        for (int p = 0; p < NDB; ++p) {
-            const uint16_t* Ks = S.K[p];
-            f32x4_t nacc = f32x4_t{};
-#pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) {
-                const u32x4_t wa = (l16 < 2) ? *reinterpret_cast<const u32x4_t*>(&Gc.wb[l16 & 1][32 * ks + 8 * g16])
-                                             : u32x4_t{0u, 0u, 0u, 0u};
-                const uint16_t* kb = &Ks[(32 * ks + tr_row) * QP + 16 * wave + tr_col];
-                nacc = mfma16(wa, cat(tr_read(kb), tr_read(kb + 4 * QP)), nacc);
-            }
-            if (g16 == 0) {
-                const int d = p * DB + 16 * wave + l16;
-                n_new[d] = decay_n * n_old[d] + nacc[0] + nacc[1];
-            }
-        }
-        s_off = s_new;
-        m_prev = m_next;
-    }
-    __syncthreads();
-    if (c_begin < c_end && tid < L) {
-        const int t0 = (c_end - 1) * L;   // the last chunk's q^ . X share
-        if (t0 + tid < A.T) {
-            float qx = 0.0f;
-#pragma unroll
-            for (int w = 0; w < kWaves; ++w) qx += S.red[w][tid];
-            A.part[(st + t0 + tid) * A.part_stride + tile] = qx;
-        }
-    }
-}
-
-hipError_t launch_walk(const WalkArgs& a, hipStream_t stream) {
-    const size_t lds = sizeof(WalkSmem);
-    static std::atomic<uint64_t> raised{0};
-    hipError_t e = raise_dynamic_lds(reinterpret_cast<const void*>(bwd_walk_kernel), lds, raised);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_walk_kernel, dim3(static_cast<unsigned>(a.S * a.G * kNTile)), dim3(kThreads), lds, stream,
-                       a);
-    return hipGetLastError();
-}
-
 }  // namespace
 
 bool chunk_mfma_supported(mlstm_dtype dt, int DQK, int DV, int L) {
@@ -1797,14 +1166,45 @@ size_t chunk_mfma_workspace_bytes(int B, int NH, int T, int DQK, int DV, int L) 
     return static_cast<size_t>(B) * NH * (G - 1) * local_subsegments(seg_tokens) * kSlotFloats * sizeof(float);
 }
 
+// ---- the segment schedule ---------------------------------------------------------------------
+SegmentShape segment_shape(int B, int NH, int T, int L, bool use_segments) {
+    SegmentShape sh{};
+    const int nc = (T + L - 1) / L;
+    sh.G = (use_segments && nc > 0) ? chunk_mfma_segments(B, NH, T, L) : 1;
+    sh.seg_chunks = sh.G > 1 ? (nc + sh.G - 1) / sh.G : nc;
+    sh.R = sh.G > 1 ? local_subsegments(sh.seg_chunks * L) : 1;
+    return sh;
+}
+
+hipError_t launch_segment_states(const ChunkArgs& a, int L, const SegmentShape& sh, float* seg, bool hilo,
+                                 hipStream_t stream) {
+    if (sh.G <= 1) return hipSuccess;
+    const int S = a.B * a.NH;
+    LocalArgs la{};
+    la.k = static_cast<const uint16_t*>(a.k);
+    la.v = static_cast<const uint16_t*>(a.v);
+    set_strides(a, la.nh_magic, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
+    la.ipre = a.ipre;
+    la.fpre = a.fpre;
+    la.ws = seg;
+    la.S = S;
+    la.T = a.T;
+    la.NS = (sh.G - 1) * sh.R;
+    la.R = sh.R;
+    la.seg_tokens = sh.seg_chunks * L;
+    hipError_t e = launch_local(la, S, stream, hilo);
+    if (e != hipSuccess) return e;
+    constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
+    hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, seg, a.C0, a.n0, a.m0, la.NS,
+                       sh.R);
+    return hipGetLastError();
+}
+
 hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspace_bytes, hipStream_t stream) {
     const int S = a.B * a.NH;
-    const int nc = (a.T + a.L - 1) / a.L;
-    int G = workspace ? chunk_mfma_segments(a.B, a.NH, a.T, a.L) : 1;
-    if (G > 1 && workspace_bytes < chunk_mfma_workspace_bytes(a.B, a.NH, a.T, a.DQK, a.DV, a.L)) G = 1;
-    if (nc == 0) G = 1;
-    const int seg_chunks = G > 1 ? (nc + G - 1) / G : nc;
-    const int R = G > 1 ? local_subsegments(seg_chunks * a.L) : 1;
+    const bool use_segments =
+        workspace != nullptr && workspace_bytes >= chunk_mfma_workspace_bytes(a.B, a.NH, a.T, a.DQK, a.DV, a.L);
+    const SegmentShape sh = segment_shape(a.B, a.NH, a.T, a.L, use_segments);
 
     ChunkKernelArgs k{};
     k.q = static_cast<const uint16_t*>(a.q);
@@ -1819,100 +1219,18 @@ hipError_t launch_chunk_mfma(const ChunkArgs& a, void* workspace, size_t workspa
     k.ws = static_cast<float*>(workspace);
     k.S = S;
     k.T = a.T;
-    k.G = G;
-    k.R = R;
-    k.NS = (G - 1) * R;
-    k.seg_chunks = seg_chunks;
+    k.G = sh.G;
+    k.R = sh.R;
+    k.NS = (sh.G - 1) * sh.R;
+    k.seg_chunks = sh.seg_chunks;
     k.h = static_cast<uint16_t*>(a.h);
     k.CT = a.CT;
     k.nT = a.nT;
     k.mT = a.mT;
 
-    hipError_t e;
-    if (G > 1) {
-        LocalArgs la{};
-        la.k = k.k;
-        la.v = k.v;
-        set_strides(a, la.nh_magic, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
-        la.ipre = a.ipre;
-        la.fpre = a.fpre;
-        la.ws = k.ws;
-        la.S = S;
-        la.T = a.T;
-        la.NS = k.NS;
-        la.R = R;
-        la.seg_tokens = seg_chunks * a.L;
-        e = launch_local(la, S, stream);
-        if (e != hipSuccess) return e;
-        constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
-        hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, k.ws, a.C0, a.n0, a.m0,
-                           k.NS, R);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
+    hipError_t e = launch_segment_states(a, a.L, sh, k.ws, false, stream);
+    if (e != hipSuccess) return e;
     return (a.L == 64) ? launch_variant<64>(k, S, stream) : launch_variant<128>(k, S, stream);
-}
-
-// ---- the backward's forward walk ----------------------------------------------------------------
-// For every 64-token chunk: the tiles' partial sums of X^T = C dH^T into X, their q^ . X shares into
-// part, and n, m entering chunk c >= 1 into slot c - 1 of ``slots``.  The segment schedule of the
-// prefill (local pass in the bf16 hi + lo form, combine) gives the entry states of the segments.
-size_t bwd_walk_workspace_bytes(int B, int NH, int T) {
-    return chunk_mfma_workspace_bytes(B, NH, T, kDQK, kDV, 64);
-}
-
-hipError_t launch_bwd_walk(const ChunkArgs& a, const void* dh, float* slots, float* seg, float* X, float* part,
-                           int part_stride, hipStream_t stream) {
-    const int S = a.B * a.NH;
-    const int nc = (a.T + 63) / 64;
-    if (nc == 0) return hipSuccess;
-    const int G = seg ? chunk_mfma_segments(a.B, a.NH, a.T, 64) : 1;
-    const int seg_chunks = G > 1 ? (nc + G - 1) / G : nc;
-    const int R = G > 1 ? local_subsegments(seg_chunks * 64) : 1;
-    WalkArgs w{};
-    w.q = static_cast<const uint16_t*>(a.q);
-    w.k = static_cast<const uint16_t*>(a.k);
-    w.v = static_cast<const uint16_t*>(a.v);
-    w.dh = static_cast<const uint16_t*>(dh);
-    set_strides(a, w.nh_magic, nullptr, w.sk, w.sv, nullptr, &w.rk, &w.rv);
-    w.ipre = a.ipre;
-    w.fpre = a.fpre;
-    w.C0 = a.C0;
-    w.n0 = a.n0;
-    w.m0 = a.m0;
-    w.seg = seg;
-    w.out = slots;
-    w.X = X;
-    w.part = part;
-    w.part_stride = part_stride;
-    w.S = S;
-    w.T = a.T;
-    w.G = G;
-    w.R = R;
-    w.NS = (G - 1) * R;
-    w.seg_chunks = seg_chunks;
-    if (G > 1) {
-        LocalArgs la{};
-        la.k = w.k;
-        la.v = w.v;
-        set_strides(a, la.nh_magic, nullptr, la.sk, la.sv, nullptr, &la.rk, &la.rv);
-        la.ipre = a.ipre;
-        la.fpre = a.fpre;
-        la.ws = seg;
-        la.S = S;
-        la.T = a.T;
-        la.NS = w.NS;
-        la.R = R;
-        la.seg_tokens = seg_chunks * 64;
-        hipError_t e = launch_local(la, S, stream, true);
-        if (e != hipSuccess) return e;
-        constexpr int kE4 = (kDQK * kDV + kDQK) / 4;
-        hipLaunchKernelGGL(combine_kernel, dim3((kE4 + 255) / 256, S), dim3(256), 0, stream, seg, a.C0, a.n0, a.m0, w.NS,
-                           R);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    return launch_walk(w, stream);
 }
 
 // ---- fixed scratch for callers that cannot allocate ---------------------------------------------

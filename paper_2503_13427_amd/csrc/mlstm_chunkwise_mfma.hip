@@ -287,6 +287,27 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         return (t / NQ) * DB + 32 * ((q / 2) * DH + dh) + 8 * g16 + 4 * (q % 2) + j;
     };
     const bool gate_wave = (wave == kGateWave);
+    // L = 128: the causal 16x16 tiles (tau block tb, sigma block sb) of S^T go to the waves by sigma
+    // block, so that a wave reads the transposed K operand of (i) for one or two sigma blocks only.
+    // Waves w and w + 4 share a SIMD and split the nine tiles of the sigma blocks p = w % 4 and 7 - p:
+    // wave p takes tau blocks p..p+4 of block p (slots 0..4); wave p + 4 takes tau blocks p+5..7 of
+    // block p (group A, slots 0..2-p) and tau blocks 7-p..7 of block 7 - p (group B, slot 3 - j for
+    // tau block 7 - p + j): five and four tiles per wave, as in the round robin of L = 64.
+    const int pr = wave & 3;
+    const int nA = wave < 4 ? 5 : 3 - pr;      // tiles of group A (sigma block pr)
+    const int tbA = wave < 4 ? pr : pr + 5;   // its first tau block
+    const int nB = wave < 4 ? 0 : pr + 1;     // tiles of group B (sigma block 7 - pr)
+    auto tile128 = [&](int i, int& tb, int& sb) -> bool {
+        if (i < nA) {
+            sb = pr;
+            tb = tbA + i;
+            return true;
+        }
+        const int j = 3 - i;
+        sb = 7 - pr;
+        tb = 7 - pr + j;
+        return j >= 0 && j < nB;
+    };
     uint16_t* const St = CF::ST_ALIAS ? &S.QK[1][0] : S.St_own;
     // Q n tile of this wave (>= NTT: none): with fewer tau tiles than waves, the waves after
     // the two that hold two S tiles take it
@@ -486,23 +507,41 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             }
             // (i) S^T += K_p Q_p^T on this wave's causal tiles.  K^T staging (L = 128): the A operand
             // (K rows sigma, 8 consecutive d) is two transpose reads of 4 K^T rows x 16 tau
+            if constexpr (CF::KT) {
+                // per group, the A operands (two transpose reads per k step) are read once
 #pragma unroll
-            for (int i = 0; i < MAXT; ++i) {
-                const int t = wave + kWaves * i;
-                if (t < NT_S) {
-                    int tb = 0, rem = t;
-                    while (rem > tb) { rem -= tb + 1; ++tb; }
-                    const int sb = rem;
-                    const uint16_t* qb = &Qs[(16 * tb + l16) * QP + 8 * g16];
-                    if constexpr (CF::KT) {
+                for (int grp = 0; grp < 2; ++grp) {
+                    const int sb = grp ? 7 - pr : pr;
+                    const int n = grp ? nB : nA;
+                    const int tb0 = grp ? 7 - pr : tbA;
+                    if (n == 0) continue;
+                    u32x4_t a[DB / 32];
 #pragma unroll
-                        for (int ks = 0; ks < DB / 32; ++ks) {
-                            const int d0 = 32 * ks + 8 * g16 + (l16 >> 2);
-                            const u32x4_t a = cat(tr_read(&Ks[kt_row(d0) * CF::KTP + 16 * sb + tr_col]),
-                                                  tr_read(&Ks[kt_row(d0 + 4) * CF::KTP + 16 * sb + tr_col]));
-                            Sacc[i] = mfma16(a, *reinterpret_cast<const u32x4_t*>(qb + 32 * ks), Sacc[i]);
+                    for (int ks = 0; ks < DB / 32; ++ks) {
+                        const int d0 = 32 * ks + 8 * g16 + (l16 >> 2);
+                        a[ks] = cat(tr_read(&Ks[kt_row(d0) * CF::KTP + 16 * sb + tr_col]),
+                                    tr_read(&Ks[kt_row(d0 + 4) * CF::KTP + 16 * sb + tr_col]));
+                    }
+#pragma unroll
+                    for (int j = 0; j < (grp ? 4 : MAXT); ++j) {
+                        if (j < n) {
+                            const uint16_t* qb = &Qs[(16 * (tb0 + j) + l16) * QP + 8 * g16];
+                            f32x4_t& acc = Sacc[grp ? 3 - j : j];
+#pragma unroll
+                            for (int ks = 0; ks < DB / 32; ++ks)
+                                acc = mfma16(a[ks], *reinterpret_cast<const u32x4_t*>(qb + 32 * ks), acc);
                         }
-                    } else {
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < MAXT; ++i) {
+                    const int t = wave + kWaves * i;
+                    if (t < NT_S) {
+                        int tb = 0, rem = t;
+                        while (rem > tb) { rem -= tb + 1; ++tb; }
+                        const int sb = rem;
+                        const uint16_t* qb = &Qs[(16 * tb + l16) * QP + 8 * g16];
                         const uint16_t* ka = &Ks[(16 * sb + l16) * QP + 8 * g16];
 #pragma unroll
                         for (int ks = 0; ks < DB / 32; ++ks)
@@ -656,36 +695,68 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
         if constexpr (CF::ST_ALIAS) __syncthreads();   // the last d block is fully read before S~ overwrites it
         // gate matrix on the S^T tiles -> S~ (bf16, tau-major) and row sums (fp32, before the
         // bf16 rounding); branch-free, one 16-byte read of the four sigma exponents per lane
+        if constexpr (L == 128) {
 #pragma unroll
-        for (int i = 0; i < MAXT; ++i) {
-            const int t = wave + kWaves * i;
-            if (t < NT_S) {
-                int tb = 0, rem = t;
-                while (rem > tb) { rem -= tb + 1; ++tb; }
-                const int sb = rem;
-                const int tau = 16 * tb + l16;
-                const float Mt = Gc.M2[tau];
-                const int Rt = Gc.R[tau];
-                const f32x4_t xs = *reinterpret_cast<const f32x4_t*>(&Gc.x2[16 * sb + 4 * g16]);
-                float vals[4];
-                float rsum = 0.f;
+            for (int i = 0; i < MAXT; ++i) {
+                int tb, sb;
+                if (tile128(i, tb, sb)) {
+                    const int tau = 16 * tb + l16;
+                    const float Mt = Gc.M2[tau];
+                    const int Rt = Gc.R[tau];
+                    const f32x4_t xs = *reinterpret_cast<const f32x4_t*>(&Gc.x2[16 * sb + 4 * g16]);
+                    float vals[4];
+                    float rsum = 0.f;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int sig = 16 * sb + 4 * g16 + j;
-                    const float val = Sacc[i][j] * kQScale * fast_exp2(xs[j] - Mt);
-                    // Rt <= sig <= tau as one unsigned comparison (Rt <= tau always)
-                    vals[j] = (static_cast<unsigned>(sig - Rt) <= static_cast<unsigned>(tau - Rt)) ? val : 0.f;
-                    rsum += vals[j];
+                    for (int j = 0; j < 4; ++j) {
+                        const int sig = 16 * sb + 4 * g16 + j;
+                        const float val = Sacc[i][j] * kQScale * fast_exp2(xs[j] - Mt);
+                        // Rt <= sig <= tau as one unsigned comparison (Rt <= tau always)
+                        vals[j] = (static_cast<unsigned>(sig - Rt) <= static_cast<unsigned>(tau - Rt)) ? val : 0.f;
+                        rsum += vals[j];
+                    }
+                    u32x2_t o;
+                    o[0] = pack_bf16x2(vals[0], vals[1]);
+                    o[1] = pack_bf16x2(vals[2], vals[3]);
+                    MLSTM_CHECK(tau < L && 16 * sb + 4 * g16 + 4 <= SP &&
+                                    tau * SP + 16 * sb + 4 * g16 + 4 <= (CF::ST_ALIAS ? CF::SETE : L * SP),
+                                kDbgChunkMfma);
+                    *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
+                    rsum = sum_rows4(rsum);
+                    if (g16 == 0) S.rs[sb][tau] = rsum;
                 }
-                u32x2_t o;
-                o[0] = pack_bf16x2(vals[0], vals[1]);
-                o[1] = pack_bf16x2(vals[2], vals[3]);
-                MLSTM_CHECK(tau < L && 16 * sb + 4 * g16 + 4 <= SP &&
-                                tau * SP + 16 * sb + 4 * g16 + 4 <= (CF::ST_ALIAS ? CF::SETE : L * SP),
-                            kDbgChunkMfma);
-                *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
-                rsum = sum_rows4(rsum);
-                if (g16 == 0) S.rs[sb][tau] = rsum;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < MAXT; ++i) {
+                const int t = wave + kWaves * i;
+                if (t < NT_S) {
+                    int tb = 0, rem = t;
+                    while (rem > tb) { rem -= tb + 1; ++tb; }
+                    const int sb = rem;
+                    const int tau = 16 * tb + l16;
+                    const float Mt = Gc.M2[tau];
+                    const int Rt = Gc.R[tau];
+                    const f32x4_t xs = *reinterpret_cast<const f32x4_t*>(&Gc.x2[16 * sb + 4 * g16]);
+                    float vals[4];
+                    float rsum = 0.f;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int sig = 16 * sb + 4 * g16 + j;
+                        const float val = Sacc[i][j] * kQScale * fast_exp2(xs[j] - Mt);
+                        // Rt <= sig <= tau as one unsigned comparison (Rt <= tau always)
+                        vals[j] = (static_cast<unsigned>(sig - Rt) <= static_cast<unsigned>(tau - Rt)) ? val : 0.f;
+                        rsum += vals[j];
+                    }
+                    u32x2_t o;
+                    o[0] = pack_bf16x2(vals[0], vals[1]);
+                    o[1] = pack_bf16x2(vals[2], vals[3]);
+                    MLSTM_CHECK(tau < L && 16 * sb + 4 * g16 + 4 <= SP &&
+                                    tau * SP + 16 * sb + 4 * g16 + 4 <= (CF::ST_ALIAS ? CF::SETE : L * SP),
+                                kDbgChunkMfma);
+                    *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
+                    rsum = sum_rows4(rsum);
+                    if (g16 == 0) S.rs[sb][tau] = rsum;
+                }
             }
         }
         // zero the masked 16x16 tiles (sigma block T+1, tau block T) for even T: the k steps

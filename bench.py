@@ -110,17 +110,28 @@ class Prefill:
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "chunkwise_traffic_B4_NH8_T32768_L128.md")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2503_13427_amd", "csrc", "mlstm_chunkwise_mfma.hip")
 CSRC = os.path.join(ROOT, "paper_2503_13427_amd", "csrc")
+# the chunkwise prefill's source and the device headers it includes, hashed in this order
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in
+                  ("mlstm_chunkwise_mfma.hip", "chunk_common.h", "mfma_common.h", "device_common.h")]
+
+
+def kernel_source_sha16():
+    """First 16 hex digits of the SHA-256 over the prefill kernel's source files, concatenated."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic():
     """HBM bytes per headline call from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary, or None
     when that summary is missing or was taken on a different chunkwise kernel source."""
-    import hashlib
     try:
         text = open(TRAFFIC_PROFILE).read()
-        src = open(KERNEL_SOURCE, "rb").read()
+        src_sha = kernel_source_sha16()
     except OSError:
         return None
     nbytes = sha = None
@@ -129,7 +140,7 @@ def measured_traffic():
             nbytes = float(line.split(":")[1])
         elif line.startswith("kernel_source_sha256_16:"):
             sha = line.split(":")[1].split()[0]
-    if nbytes is None or sha != hashlib.sha256(src).hexdigest()[:16]:
+    if nbytes is None or sha != src_sha:
         return None
     return nbytes
 

@@ -102,21 +102,30 @@ using VtPacked = u32x2_t[2 * VRegs<L>::N * VRegs<L>::PARTS];
 // one-hot selection of its columns 16 h + 0..15 (exact in fp32).  Lane (n = l16, g16) of D holds
 // V[tau 16 a + 4 g16 + j][v 32 b + 16 h + n], j = 0..3: four consecutive tau of one row of V^T, kept
 // packed in pv until the stores below.
-template <int L>
-__device__ __forceinline__ void vt_transpose(VtPacked<L>& pv, const VRegs<L>& r, int lane, int part) {
-    // E_h in the B-operand layout: lane (l16, g16) holds k slots 8 g16 + 0..7 of column l16, whose
-    // one (if any) is slot 16 h + l16.  Built from an opaque copy of the lane index so that it is not
-    // hoisted out of the chunk loop (eight more registers held across the loop would spill).
+// One-hot selection E_h (32 x 16, columns 16 h + 0..15 of a 32-column piece) in the B-operand layout:
+// lane (l16, g16) holds k slots 8 g16 + 0..7 of column l16, whose one (if any) is slot 16 h + l16.
+// That slot lies in the lane's eight when 16 h + l16 - 8 g16 is in 0..7, i.e. when g16 = 2 h + l16 / 8,
+// and is then slot l16 % 8 of them: register (l16 / 2) % 4, half l16 % 2.  Built from an opaque copy
+// of the lane index so that it is not hoisted out of the chunk loop (eight more registers held
+// across the loop would spill).
+__device__ __forceinline__ void onehot_pair(u32x4_t (&E)[2], int lane) {
     int ln = lane;
     asm volatile("" : "+v"(ln));
-    u32x4_t E[2];
+    const int sel = (ln >> 1) & 3;
+    const int gh = (ln >> 4) - ((ln >> 3) & 1);   // 2 h for the h whose column this lane can hold
+    const uint32_t one = (ln & 1) ? 0x3F800000u : 0x3F80u;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        const int pos = 16 * h + (ln & 15) - 8 * (ln >> 4);
-        const uint32_t one = (pos & 1) ? 0x3F800000u : 0x3F80u;
+        const uint32_t oh = (gh == 2 * h) ? one : 0u;
 #pragma unroll
-        for (int d = 0; d < 4; ++d) E[h][d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
+        for (int d = 0; d < 4; ++d) E[h][d] = (sel == d) ? oh : 0u;
     }
+}
+
+template <int L>
+__device__ __forceinline__ void vt_transpose(VtPacked<L>& pv, const VRegs<L>& r, int lane, int part) {
+    u32x4_t E[2];
+    onehot_pair(E, lane);
 #pragma unroll
     for (int i = 0; i < VRegs<L>::N; ++i)
 #pragma unroll

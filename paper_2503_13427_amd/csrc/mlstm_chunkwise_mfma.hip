@@ -133,20 +133,6 @@ __device__ __forceinline__ void load_qk(QKRegs<L>& r, const SeqRsrc& R, int t0, 
         }
     }
 }
-// One-hot selection E_h (32 x 16, columns 16 h + 0..15 of a 32-column piece) in the B-operand layout:
-// lane (l16, g16) holds k slots 8 g16 + 0..7 of column l16, whose one (if any) is slot 16 h + l16.
-// Built from an opaque copy of the lane index so that it is not held across the chunk loop.
-__device__ __forceinline__ void onehot_pair(u32x4_t (&E)[2], int lane) {
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const int pos = 16 * h + (ln & 15) - 8 * (ln >> 4);
-        const uint32_t one = (pos & 1) ? 0x3F800000u : 0x3F80u;
-#pragma unroll
-        for (int d = 0; d < 4; ++d) E[h][d] = (pos >= 0 && pos < 8 && (pos >> 1) == d) ? one : 0u;
-    }
-}
 template <int L>
 __device__ __forceinline__ void store_qk(uint16_t* Qd, uint16_t* Kd, const QKRegs<L>& r, int tid) {
     constexpr int PR = Cfg<L>::DB / 8, QP = Cfg<L>::QP, NW = kWaves;

@@ -81,7 +81,10 @@ struct Smem {
     uint16_t nb[2][2][kDQK];                       // normaliser as bf16 hi / lo rows, double-buffered
     float n[2][kDQK];                              // fp32 normaliser, double-buffered across chunks
     float dq[L];                                   // Q n_{k-1} (unscaled q)
-    float rs[L / 16][L];                           // row sums of S~ per (sigma block, tau)
+    // row sums of S~ per (sigma block, tau): at L = 128 tau-major, so (ii) reads a row's eight in two
+    // 16-byte reads; at L = 64 sigma-block-major (measured faster there)
+    alignas(16) float rs[L * (L / 16)];
+    __device__ float& rsum_at(int tau, int sb) { return rs[L == 128 ? tau * (L / 16) + sb : sb * L + tau]; }
     GateBuf<L> G[2];                               // by chunk parity
     // partial read-outs exchanged between the two d partitions of a column group (DH = 2):
     // [column group][v tile][tau tile][lane] as float4
@@ -708,7 +711,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                                 kDbgChunkMfma);
                     *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
                     rsum = sum_rows4(rsum);
-                    if (g16 == 0) S.rs[sb][tau] = rsum;
+                    if (g16 == 0) S.rsum_at(tau, sb) = rsum;
                 }
             }
         } else {
@@ -741,7 +744,7 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
                                 kDbgChunkMfma);
                     *reinterpret_cast<u32x2_t*>(&St[tau * SP + 16 * sb + 4 * g16]) = o;
                     rsum = sum_rows4(rsum);
-                    if (g16 == 0) S.rs[sb][tau] = rsum;
+                    if (g16 == 0) S.rsum_at(tau, sb) = rsum;
                 }
             }
         }
@@ -762,8 +765,19 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             if (DH == 2 && (T & 1) != dh) continue;
             const int tau = 16 * T + l16;
             float den = Gc.interN[tau] * S.dq[tau];
+            // the row sums of sigma blocks 0..T (L = 128: in groups of four per 16-byte read)
+            if constexpr (L == 128) {
 #pragma unroll
-            for (int sb = 0; sb <= T; ++sb) den += S.rs[sb][tau];
+                for (int sg = 0; 4 * sg <= T; ++sg) {
+                    const f32x4_t r4 = *reinterpret_cast<const f32x4_t*>(&S.rsum_at(tau, 4 * sg));
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (4 * sg + j <= T) den += r4[j];
+                }
+            } else {
+#pragma unroll
+                for (int sb = 0; sb <= T; ++sb) den += S.rsum_at(tau, sb);
+            }
             const float hv = __builtin_amdgcn_rcpf(fmaxf(fabsf(den), Gc.floorv[tau]));
             const float ic = Gc.interC[tau];
 #pragma unroll

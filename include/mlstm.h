@@ -327,8 +327,9 @@ mlstm_status mlstm_parallel_bwd(const void* q, const void* k, const void* v, mls
  * the chunk recurrence of App. D.1; document borders (fpre = -inf, App. B)
  * restart that recurrence as in the forward.  The forward's output is not
  * needed: dh . h~ is formed from the recomputed numerator in fp32.  Products
- * run on bf16 MFMA with fp32 accumulation; the recomputed states and the
- * state gradients enter them as bf16 hi + lo pairs.  No float atomics: the
+ * run on bf16 MFMA with fp32 accumulation; the recomputed states enter them
+ * as bf16 hi + lo pairs, the carried state gradients (accumulated in fp32)
+ * rounded once to bf16.  No float atomics: the
  * result is deterministic.
  *
  *   q, k [B, NH, T, DQK], v [B, NH, T, DV] (dt)   ipre, fpre [B, NH, T] fp32

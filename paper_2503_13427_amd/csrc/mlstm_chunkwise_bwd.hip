@@ -39,8 +39,8 @@
 //   intra   one workgroup per chunk: gates, S, D, den; per 128-column piece of dv, (dH V^T), the
 //           intra term of dv and the piece's columns of L_c; then w, P, dq (complete), the intra
 //           term of dk and z_c; writes the key weights, the chunk's decay and q_t . dq_t
-//   scan    the reverse recurrence of (Gam, gam), elementwise over the state, writing Gam_c as
-//           bf16 hi + lo rows; dC0, dn0 and partial sums of dm0
+//   scan    the reverse recurrence of (Gam, gam), elementwise over the state (fp32), writing Gam_c
+//           rounded once to bf16; dC0, dn0 and partial sums of dm0
 //   interkv one workgroup per chunk: the inter terms of dk and dv from Gam_c, read once; k . dk
 //   gates   one workgroup per sequence: the reverse prefix sums of r - c, di~ and df~, dm0
 //
@@ -90,7 +90,7 @@ struct BwdParams {
     float* dn0;
     float* dm0;
     float* slots;        // S (NC - 1) slots: n, m entering chunk c in slot c - 1, then L_c, z_c
-    uint16_t* hl;        // S (NC - 1) x 2 x DQK x DV: Gam_c as bf16 hi + lo rows
+    uint16_t* hl;        // S (NC - 1) x DQK x DV: Gam_c in bf16
     float* lz0;          // S x (DQK DV + DQK): L_0, z_0
     float* gamn;         // S x NC x DQK: gam_c
     float* tok;          // S x T x kTokF
@@ -108,7 +108,7 @@ __device__ __forceinline__ float* lz_of(const BwdParams& A, int s, int c) {
 }
 __device__ __forceinline__ uint16_t* hl_of(const BwdParams& A, int s, int slot) {
     MLSTM_CHECK(slot >= 0 && slot < A.NC - 1 && s >= 0, kDbgChunkBwd);
-    return A.hl + (static_cast<int64_t>(s) * (A.NC - 1) + slot) * 2 * kCV;
+    return A.hl + (static_cast<int64_t>(s) * (A.NC - 1) + slot) * kCV;
 }
 
 __device__ __forceinline__ u32x4_t lds16(const uint16_t* p) { return *reinterpret_cast<const u32x4_t*>(p); }
@@ -967,12 +967,11 @@ __global__ void __launch_bounds__(256) bwd_scan_kernel(BwdParams A) {
                 const int c = c1 - u;
                 if (ok && c < NC - 1) {
                     if (isC) {
-                        uint16_t* hi = hl_of(A, s, c) + 4 * static_cast<int64_t>(e4);
-                        const uint32_t h01 = pack_bf16x2(G[0], G[1]), h23 = pack_bf16x2(G[2], G[3]);
-                        const uint32_t l01 = pack_bf16x2(G[0] - lo_f32(h01), G[1] - hi_f32(h01));
-                        const uint32_t l23 = pack_bf16x2(G[2] - lo_f32(h23), G[3] - hi_f32(h23));
-                        *reinterpret_cast<u32x2_t*>(hi) = u32x2_t{h01, h23};
-                        *reinterpret_cast<u32x2_t*>(hi + kCV) = u32x2_t{l01, l23};
+                        // one bf16 rounding, like the other operands of the bf16 products: the
+                        // inter terms of dk and dv sum it against v and k (a hi + lo pair measured
+                        // 1.5 x smaller row errors, at twice the traffic of this pass and the next)
+                        uint16_t* hb = hl_of(A, s, c) + 4 * static_cast<int64_t>(e4);
+                        *reinterpret_cast<u32x2_t*>(hb) = u32x2_t{pack_bf16x2(G[0], G[1]), pack_bf16x2(G[2], G[3])};
                     } else {
                         reinterpret_cast<f32x4_t*>(A.gamn + (static_cast<int64_t>(s) * NC + c) * kDQK)[e4 - kCV / 4] = G;
                     }
@@ -1012,7 +1011,7 @@ __global__ void __launch_bounds__(256) bwd_scan_kernel(BwdParams A) {
 // ---- dk and dv inter terms ---------------------------------------------------------------------
 // One workgroup of 8 waves per chunk: dk^T += Gam_c V^T (over v) and dv^T += Gam_c^T K^T (over d),
 // each complete inside the workgroup, so Gam_c is read from memory once.  It streams through LDS in
-// 16 blocks of 64 rows d x 128 columns v (hi and lo; the next block in registers), while K and V of
+// 16 blocks of 64 rows d x 128 columns v (the next block in registers), while K and V of
 // the chunk stay in LDS.  Waves 0-3 form dk: wave m owns the rows d = 64 jd + 16 m + 0..15 of every
 // block row jd; waves 4-7 form dv: wave m owns the columns v = 128 jv + 32 m + 0..31 of block column
 // jv; both cover the four tau tiles, and each runs 32 MFMAs per block.  The blocks go column by
@@ -1021,7 +1020,7 @@ constexpr int kIKT = 512;    // threads of the inter pass
 struct InterKVSmem {
     uint16_t K[kBL * kQP];     // the chunk's K rows
     uint16_t V[kBL * kHP];     // the chunk's V rows
-    uint16_t G[2][64 * kWP];   // one block of Gam_c: hi, lo
+    uint16_t G[64 * kWP];      // one block of Gam_c
     float wk[kBL];
     float gam[kDQK];
     float red[4][kBL];         // k . dk partials of the dk waves
@@ -1044,14 +1043,13 @@ __global__ void __launch_bounds__(kIKT) bwd_interkv_kernel(BwdParams A) {
     if (tid < kBL) S.wk[tid] = (t0 + tid < T) ? A.tok[(st + t0 + tid) * kTokF] : 0.0f;
     const uint16_t* gbase = has_g ? hl_of(A, s, c) : nullptr;
     // this thread's two 16-byte pieces of a Gam block (rows e / 16, columns 8 (e % 16) + 0..7)
-    u32x4_t gh[2], gl[2];
+    u32x4_t gh[2];
     auto gload = [&](int jd, int jv) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int e = tid + kIKT * i;
             const uint16_t* p = gbase + static_cast<int64_t>(64 * jd + (e >> 4)) * kDV + 128 * jv + 8 * (e & 15);
             gh[i] = *reinterpret_cast<const u32x4_t*>(p);
-            gl[i] = *reinterpret_cast<const u32x4_t*>(p + kCV);
         }
     };
     if (has_g) {
@@ -1099,8 +1097,7 @@ __global__ void __launch_bounds__(kIKT) bwd_interkv_kernel(BwdParams A) {
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     const int e = tid + kIKT * i;
-                    *reinterpret_cast<u32x4_t*>(&S.G[0][(e >> 4) * kWP + 8 * (e & 15)]) = gh[i];
-                    *reinterpret_cast<u32x4_t*>(&S.G[1][(e >> 4) * kWP + 8 * (e & 15)]) = gl[i];
+                    *reinterpret_cast<u32x4_t*>(&S.G[(e >> 4) * kWP + 8 * (e & 15)]) = gh[i];
                 }
                 if (jd < 3) gload(jd + 1, jv);
                 else if (jv < 3) gload(0, jv + 1);
@@ -1109,33 +1106,25 @@ __global__ void __launch_bounds__(kIKT) bwd_interkv_kernel(BwdParams A) {
                     // dk^T [d][tau] += sum_v Gam[d][v] V[tau][v]: A = Gam rows, B = V rows
 #pragma unroll
                     for (int ks = 0; ks < 4; ++ks) {
-                        const u32x4_t ah = row_op(S.G[0], kWP, 16 * m, 32 * ks, lane);
-                        const u32x4_t al = row_op(S.G[1], kWP, 16 * m, 32 * ks, lane);
+                        const u32x4_t ah = row_op(S.G, kWP, 16 * m, 32 * ks, lane);
 #pragma unroll
                         for (int t = 0; t < 4; ++t) {
                             const u32x4_t b = row_op(S.V, kHP, 16 * t, 128 * jv + 32 * ks, lane);
                             acc[4 * jd + t] = mfma16(ah, b, acc[4 * jd + t]);
-                            acc[4 * jd + t] = mfma16(al, b, acc[4 * jd + t]);
                         }
                     }
                 } else {
                     // dv^T [v][tau] += sum_d Gam[d][v] K[tau][d]: A = Gam read transposed, B = K rows
 #pragma unroll
                     for (int ks = 0; ks < 2; ++ks) {
-                        u32x4_t ah[2], al[2];
+                        u32x4_t ah[2];
 #pragma unroll
-                        for (int e = 0; e < 2; ++e) {
-                            ah[e] = tr_op(S.G[0], kWP, 32 * ks, 32 * m + 16 * e, lane);
-                            al[e] = tr_op(S.G[1], kWP, 32 * ks, 32 * m + 16 * e, lane);
-                        }
+                        for (int e = 0; e < 2; ++e) ah[e] = tr_op(S.G, kWP, 32 * ks, 32 * m + 16 * e, lane);
 #pragma unroll
                         for (int t = 0; t < 4; ++t) {
                             const u32x4_t b = row_op(S.K, kQP, 16 * t, 64 * jd + 32 * ks, lane);
 #pragma unroll
-                            for (int e = 0; e < 2; ++e) {
-                                acc[4 * e + t] = mfma16(ah[e], b, acc[4 * e + t]);
-                                acc[4 * e + t] = mfma16(al[e], b, acc[4 * e + t]);
-                            }
+                            for (int e = 0; e < 2; ++e) acc[4 * e + t] = mfma16(ah[e], b, acc[4 * e + t]);
                         }
                     }
                 }
@@ -1277,7 +1266,7 @@ BwdLayout bwd_layout(int64_t S, int T) {
     L.slots = take(static_cast<size_t>(S * NC1 * kSlotFloats) * 4);
     L.seg = take(bwd_walk_workspace_bytes(S, T));
     L.xp = take(static_cast<size_t>(4 * S * T * kDQK) * 4);
-    L.hl = take(static_cast<size_t>(S * NC1 * 2 * kCV) * 2);
+    L.hl = take(static_cast<size_t>(S * NC1 * kCV) * 2);
     L.lz0 = take(static_cast<size_t>(S * kLzFloats) * 4);
     L.gamn = take(static_cast<size_t>(S * NC * kDQK) * 4);
     L.tok = take(static_cast<size_t>(S * T * kTokF) * 4);

@@ -536,14 +536,14 @@ def call_cbwd(a):
 def test_chunk_bwd_workspace_size():
     """Slots of every chunk but the first (n, m, then L_c, z_c); the segment slots of the walk (32
     sequence-tile workgroups per segment, so eight segments of four chunks: seven segment slots per
-    sequence); the four dv tiles' partial sums of X; Gam_c as bf16 hi + lo rows; L_0, gam per chunk,
+    sequence); the four dv tiles' partial sums of X; Gam_c in bf16; L_0, gam per chunk,
     per-token key weights and partial sums, per-chunk decays, dm0 partial sums; each region 256-byte
     aligned."""
     al = lambda b: (b + 255) // 256 * 256
     S, T, NC = 8, 2048, 32
     slot = 256 * 512 + 256 + 4
     want = (al(S * (NC - 1) * slot * 4) + al(S * 7 * slot * 4) + al(4 * S * T * 256 * 4)
-            + al(S * (NC - 1) * 2 * 256 * 512 * 2)
+            + al(S * (NC - 1) * 256 * 512 * 2)
             + al(S * (256 * 512 + 256) * 4)
             + al(S * NC * 256 * 4) + al(S * T * 4) + al(S * T * 32) + al(S * NC * 4) + al(S * 129 * 4))
     assert Bd.mlstm_chunkwise_bwd_workspace_bytes(1, 8, T, 256, 512, 64) == want

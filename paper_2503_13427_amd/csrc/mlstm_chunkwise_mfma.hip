@@ -660,8 +660,13 @@ __global__ void __launch_bounds__(kThreads, 1) chunk_mfma_kernel(ChunkKernelArgs
             }
         }
 
-        // gates of the next chunk, one chunk ahead
-        if (gate_wave && c + 1 < c_end) gate_phase<L>(S.G[par ^ 1], gi, gf, g_m, g_s, lane, A.T - (t0 + L));
+        // gates of the next chunk, one chunk ahead; the other waves wait for them at the next
+        // barrier, so the gate wave issues ahead of its SIMD partner meanwhile
+        if (gate_wave && c + 1 < c_end) {
+            __builtin_amdgcn_s_setprio(1);
+            gate_phase<L>(S.G[par ^ 1], gi, gf, g_m, g_s, lane, A.T - (t0 + L));
+            __builtin_amdgcn_s_setprio(0);
+        }
 
         // finish Q n: columns 0 and 1 of the 16x16 tile are lanes l16 = 0 and 1
 #pragma unroll

@@ -641,7 +641,7 @@ def main():
                     help="size of the calibration copy after the calls (0: none)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported (every (batch, head) "
+        print(f"bench.py: the benchmark runs on one GPU; --gpus {args.gpus} is not supported (every (batch, head) "
               "sequence is independent, so more GPUs would shard B*NH with no exchange)", file=sys.stderr)
         sys.exit(2)
     if args.only == "cpu":

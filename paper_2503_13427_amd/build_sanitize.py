@@ -5,7 +5,7 @@ The device code is compiled exactly as in ``build.py``: every sanitizer flag is 
 ``-Xarch_host``, so only the host pass is instrumented.  The objects are linked with the host clang
 against the shared ASan runtime; a process that loads ``libmlstm_san.so`` must preload that runtime
 (``runtime_path()``) and select the library with ``MLSTM_LIBRARY`` (see ``binding.py``).  Nothing on
-the GPU path uses this build.
+the GPU path uses this sanitized library.
 """
 from __future__ import annotations
 

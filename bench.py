@@ -427,11 +427,9 @@ def bench_layer(steps, decode_steps, stream):
     return out
 
 
-def bench_backward(w, steps, stream, parallel=True):
-    """The training-mode backward on a prefill shape (bf16 q/k/v and dh, fp32 gates, zero initial
-    state): mlstm_chunkwise_bwd (per-call median of ``steps`` calls), the forward on the same inputs
-    for the ratio, and (``parallel``) mlstm_parallel_bwd for comparison.  FLOP figures use App. D.2's
-    count, twice the App. D.1 forward, against the bf16 MFMA peak."""
+def backward_inputs(w):
+    """Seeded inputs of the training-mode backward on a prefill shape (bf16 q/k/v and dh, fp32 gates,
+    zero initial state), its fp32 outputs and its workspace."""
     from paper_2503_13427_amd import binding as mb
     g = torch.Generator(device="cuda").manual_seed(17)
     B, NH, T, DQK, DV = w.B, w.NH, w.T, w.DQK, w.DV
@@ -445,6 +443,17 @@ def bench_backward(w, steps, stream, parallel=True):
             torch.empty(B, NH, T, DV, device="cuda"), torch.empty(B, NH, T, device="cuda"),
             torch.empty(B, NH, T, device="cuda")]
     wsb = torch.empty(mb.mlstm_chunkwise_bwd_workspace_bytes(B, NH, T, DQK, DV, 64), dtype=torch.uint8, device="cuda")
+    return q, k, v, ip, fp, dh, outs, wsb
+
+
+def bench_backward(w, steps, stream, parallel=True):
+    """The training-mode backward on a prefill shape (inputs of ``backward_inputs``):
+    mlstm_chunkwise_bwd (per-call median of ``steps`` calls), the forward on the same inputs
+    for the ratio, and (``parallel``) mlstm_parallel_bwd for comparison.  FLOP figures use App. D.2's
+    count, twice the App. D.1 forward, against the bf16 MFMA peak."""
+    from paper_2503_13427_amd import binding as mb
+    B, NH, T, DQK, DV = w.B, w.NH, w.T, w.DQK, w.DV
+    q, k, v, ip, fp, dh, outs, wsb = backward_inputs(w)
 
     def per_call(fn, n):
         settle(fn)
@@ -637,6 +646,8 @@ def main():
     ap.add_argument("--workload", default=configs.CONT_PREFILL_T32768.name,
                     help="workload name for --only calls")
     ap.add_argument("--calls", type=int, default=3)
+    ap.add_argument("--backward", action="store_true",
+                    help="with --only calls on a prefill workload: chunkwise backward calls instead of the forward")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="size of the calibration copy after the calls (0: none)")
     args = ap.parse_args()
@@ -668,6 +679,14 @@ def main():
             torch.cuda.synchronize()
             for _ in range(args.calls):
                 mb.mlstm_step(q, k, v, ip, fp, C, n, m, h, C, n, m, stream=stream)
+        elif args.backward:
+            # the chunkwise backward on the prefill shape (counter runs of the training-mode passes)
+            from paper_2503_13427_amd import binding as mb
+            q, k, v, ip, fp, dh, outs, wsb = backward_inputs(wl)
+            torch.cuda.synchronize()
+            for _ in range(args.calls):
+                mb.mlstm_chunkwise_bwd(q, k, v, ip, fp, None, None, None, 64, dh, *outs, None, None, None, wsb,
+                                       stream=stream)
         else:
             p = Prefill(wl, 1)
             for _ in range(args.calls):

@@ -1189,13 +1189,14 @@ __global__ void __launch_bounds__(kIKT) bwd_interkv_kernel(BwdParams A) {
 }
 
 // ---- gate gradients ----------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) bwd_gate_kernel(BwdParams A) {
+constexpr int kGT = 1024;   // threads of the gate pass: one block of kGT tokens per step of its scan
+__global__ void __launch_bounds__(kGT) bwd_gate_kernel(BwdParams A) {
     const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int T = A.T;
     const int64_t st = static_cast<int64_t>(s) * T;
-    __shared__ float wsum[4];
+    __shared__ float wsum[kGT / 64];
     double carry = 0.0;
-    for (int base = ((T + 255) / 256 - 1) * 256; base >= 0; base -= 256) {
+    for (int base = ((T + kGT - 1) / kGT - 1) * kGT; base >= 0; base -= kGT) {
         const int t = base + tid;
         float val = 0.0f, ci = 0.0f;
         if (t < T) {
@@ -1211,7 +1212,7 @@ __global__ void __launch_bounds__(256) bwd_gate_kernel(BwdParams A) {
         __syncthreads();
         float before = 0.0f, total = 0.0f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
+        for (int w = 0; w < kGT / 64; ++w) {
             if (w < wave) before += wsum[w];
             total += wsum[w];
         }
@@ -1346,7 +1347,7 @@ hipError_t launch_chunk_bwd(const ChunkBwdArgs& a, void* workspace, hipStream_t 
     if (e != hipSuccess) return e;
     e = launch_big<InterKVSmem>(reinterpret_cast<const void*>(bwd_interkv_kernel), p, nchunks, stream, r_kv, kIKT);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_gate_kernel, dim3(S), dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(bwd_gate_kernel, dim3(S), dim3(kGT), 0, stream, p);
     return hipGetLastError();
 }
 
